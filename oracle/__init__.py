@@ -1,0 +1,1 @@
+"""PalQuant CPU oracle (test infrastructure only; see oracle.py)."""
