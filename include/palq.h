@@ -1,0 +1,272 @@
+/*
+ * palq.h -- C ABI of the PalQuant inference library for AMD MI355X (gfx950).
+ *
+ * PalQuant (parallel low-precision quantisation) runs a high-precision
+ * network as G parallel groups of B-bit convolutions (Section 4.1), with a
+ * cyclic permutation of the groups between layers (Section 4.2, Eq. 6-8).
+ * This library computes the integer inference path of such a network on one
+ * GPU: quantise (Eq. 2), grouped B-bit convolution with int32 accumulation
+ * (Eq. 1 per group), a fixed-point requantisation with ReLU, and the cyclic
+ * permutation applied as the write address of the result.
+ *
+ * Conventions for every call
+ *  - Tensor and parameter pointers are DEVICE pointers owned by the caller
+ *    unless a comment says "host".  The library never frees them.
+ *  - Calls are asynchronous on the context's stream.  All argument checks
+ *    happen on the host before anything is enqueued: a call that returns an
+ *    error other than PALQ_ERR_DEVICE has written nothing.  Device faults
+ *    surface on a later call or on palq_sync.
+ *  - No call throws or aborts across the ABI.  palq_last_error() gives a
+ *    human-readable reason for the last failing call on that context.
+ *  - A context is used by one host thread at a time.
+ *  - A context created with device = -1 is "validate only": every call checks
+ *    its arguments exactly as on a GPU and then returns without device work.
+ *
+ * Packed code layout (activations and filters)
+ *  A tensor [N][H][W][G][C^] of b-bit codes is stored NHWC, group-major
+ *  (channel g*C^ + j, the [N, G, C^, H, W] view of Section 4.2).  Each
+ *  (pixel, group) row of C^ codes occupies palq_row_bytes(C^, b) bytes and
+ *  rows follow each other with no gap; a pixel is G rows.
+ *   - b in {2, 4, 8}: code j sits at bits [b*j, b*j + b) of the row read as
+ *     one little-endian bit string; the row is padded with zero bits to a
+ *     multiple of 32 bits.
+ *   - b = 3: the row is cut into chunks of 32 codes (the last one padded with
+ *     zero codes), 12 bytes each.  In a chunk, bytes 0-7 are a little-endian
+ *     64-bit field holding bits 0-1 of code j at bits [2j, 2j+2); bytes 8-11
+ *     are a little-endian 32-bit field holding bit 2 of code j at bit
+ *     8*((j>>2)&3) + 4*(j>>4) + (j&3).
+ *  Signed codes are b-bit two's complement, unsigned codes are plain binary.
+ *  Padding bits are written as zero and ignored when read.
+ *  A filter [G][C^out][kh][kw][C^in] has the layout of an activation tensor
+ *  with N = G*C^out, H = kh, W = kw and one group of C^in codes.
+ */
+#ifndef PALQ_H
+#define PALQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t palq_status;
+#define PALQ_OK 0
+#define PALQ_ERR_ARG (-1)         /* malformed or inconsistent arguments        */
+#define PALQ_ERR_UNSUPPORTED (-2) /* well formed but outside what is built      */
+#define PALQ_ERR_OVERFLOW (-3)    /* the int32 accumulator bound could be broken */
+#define PALQ_ERR_DEVICE (-4)      /* HIP runtime error                          */
+#define PALQ_ERR_NOMEM (-5)       /* device or host allocation failed           */
+
+typedef struct palq_ctx palq_ctx;
+typedef struct palq_net palq_net;
+
+/* An activation tensor: n x h x w pixels of `groups` rows of ch_per_group
+ * codes, `bits` in {2, 3, 4, 8}.  data: device, palq_act_bytes() bytes. */
+typedef struct {
+  int32_t n, h, w;
+  int32_t groups, ch_per_group;
+  int32_t bits;
+  int32_t is_signed;
+  void *data;
+} palq_act;
+
+/* A grouped filter: groups x cout_pg output channels, each a kh x kw x
+ * cin_pg block of signed `bits`-bit codes (bits in {2, 3, 4, 8}).
+ * data: device, packed as described above. */
+typedef struct {
+  int32_t groups, cout_pg, cin_pg, kh, kw, bits;
+  const void *data;
+} palq_filter;
+
+/* Per-output-channel fixed-point requantisation, arrays of groups*cout_pg
+ * int32 on the device, indexed by the convolution's own output channel
+ * g*cout_pg + k (before the cyclic permutation moves it):
+ *   q = clamp(floor((t * mult + 2^(shift-1)) / 2^shift), 0, 2^out_bits - 1)
+ * with t = acc + bias + residual (below).  The clamp at 0 is the fused ReLU.
+ * The result is exact for mult in [0, 2^31), shift in [1, 62], |bias| < 2^30
+ * and |res_mult| < 2^15 (outside that range the output is unspecified but
+ * no memory outside the output tensor is touched).  bias may be NULL (0).
+ * out_bits in {2, 3, 4, 8}; output codes are unsigned.  The arrays (and
+ * res_mult below) must be 16-byte aligned. */
+typedef struct {
+  const int32_t *mult;
+  const int32_t *shift;
+  const int32_t *bias;
+  int32_t out_bits;
+} palq_requant;
+
+/* Shortcut added to t in int64 before requantisation, at the DESTINATION
+ * channel of the cyclic permutation.  At most one of the two kinds:
+ *  - identity: t += res_mult[c] * identity[pixel, dest channel], where
+ *    `identity` has the output's shape (any unsigned bits) and res_mult is
+ *    indexed like the requant arrays (device, groups*cout_pg int32);
+ *  - projection: t += the int32 accumulator, at the destination channel, of
+ *    the 1x1 grouped convolution of proj_in with proj_w at stride
+ *    proj_stride, pad 0 (proj_w: same groups and cout_pg as the main filter,
+ *    kh = kw = 1; proj_in: unsigned codes, groups = proj_w->groups). */
+typedef struct {
+  const palq_act *identity;
+  const int32_t *res_mult;
+  const palq_act *proj_in;
+  const palq_filter *proj_w;
+  int32_t proj_stride;
+} palq_residual;
+
+/* ---------------------------------------------------------------- context */
+
+/* Creates a context on HIP device `device` (or -1: validate only) that
+ * enqueues on `hip_stream` (a hipStream_t; NULL = the null stream).
+ * Returns PALQ_ERR_DEVICE when the device cannot be used. */
+palq_status palq_create(int32_t device, void *hip_stream, palq_ctx **out);
+void palq_destroy(palq_ctx *ctx);
+palq_status palq_set_stream(palq_ctx *ctx, void *hip_stream);
+/* Waits for all work on the context's stream; reports deferred device errors. */
+palq_status palq_sync(palq_ctx *ctx);
+/* Reason for the last failed call on ctx; owned by ctx, valid until its next call. */
+const char *palq_last_error(const palq_ctx *ctx);
+/* Library build string (host; static storage). */
+const char *palq_version(void);
+
+/* Bytes of one packed row of `codes` codes at `bits` bits (-1 if invalid). */
+int64_t palq_row_bytes(int32_t codes, int32_t bits);
+/* Bytes of a packed activation tensor (-1 if the descriptor is invalid). */
+int64_t palq_act_bytes(const palq_act *a);
+
+/* ------------------------------------------------------------ data layout */
+
+/* Packs one code per byte, [n][h][w][groups*ch_per_group] (int8 for signed,
+ * uint8 for unsigned codes), into `out`'s layout.  Codes outside the b-bit
+ * range are truncated to their low b bits. */
+palq_status palq_pack(palq_ctx *ctx, const void *codes, const palq_act *out);
+/* The inverse: one code per byte, signed codes sign-extended. */
+palq_status palq_unpack(palq_ctx *ctx, const palq_act *in, void *codes);
+
+/* ------------------------------------------------------------ hot path */
+
+/* Uniform quantiser, Section 3.2 Eq. 2, elementwise over an fp32 NHWC tensor
+ * x of out's shape: d = x - l, r = u - l, t = d / r (IEEE fp32, correctly
+ * rounded), t = min(t, 1), t = (t >= 0 ? t : 0) (NaN -> 0),
+ * q = rint(t * (2^b - 1)) with ties to even, and q - 2^(b-1) for signed
+ * codes.  If l or u is NaN both are taken as the min and max of the non-NaN
+ * elements of x (computed on the device); range_out (device, 2 floats,
+ * nullable) receives the l and u used.  Host check: u > l and u - l finite
+ * when both are given.  If the calibrated range is empty or degenerate the
+ * output is all zero codes (the minimum code when signed). */
+palq_status palq_quantize(palq_ctx *ctx, const float *x, float l, float u, const palq_act *out,
+                          float *range_out);
+
+/* One PalQuant layer: G parallel B-bit convolutions (Section 4.1; Eq. 1 per
+ * group), int32 accumulation, then requantisation (palq_requant) with the
+ * optional shortcut (palq_residual), and the cyclic permutation of Eq. 8
+ * applied `shuffle_steps` times as the write address: the result of source
+ * group g is stored in group (g + shuffle_steps) mod G.
+ *   in  : unsigned codes of 2, 3 or 4 bits, or signed 8-bit codes;
+ *         groups == w->groups, ch_per_group == w->cin_pg
+ *   out : n x ho x wo, groups == w->groups, ch_per_group == w->cout_pg,
+ *         bits == rq->out_bits, unsigned; ho = (h + 2 pad - kh)/stride + 1
+ *   acc_dump (nullable, 16-byte aligned): int32 [n][ho][wo][groups*cout_pg], the sum of all
+ *         products that land in each output channel (destination order:
+ *         the permuted main accumulator plus any projection accumulator).
+ * PALQ_ERR_OVERFLOW when K*max|code|*max|weight| >= 2^27 for the main or the
+ * projection product (K = kh*kw*cin_pg).  out must not overlap any input. */
+palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
+                            int32_t pad, const palq_requant *rq, const palq_residual *res,
+                            int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump);
+
+/* The cyclic permutation of Section 4.2 (Eq. 6-8) on its own:
+ * out[pixel, (g + steps) mod G, :] = in[pixel, g, :], any integer steps.
+ * in and out have the same shape and bits and must not overlap. */
+palq_status palq_cyclic_shuffle(palq_ctx *ctx, const palq_act *in, int32_t steps,
+                                const palq_act *out);
+
+/* k x k max pool with stride and zero-area padding (max over the in-image
+ * part of each window) on unsigned codes; out has in's groups and bits. */
+palq_status palq_maxpool(palq_ctx *ctx, const palq_act *in, int32_t k, int32_t stride, int32_t pad,
+                         const palq_act *out);
+
+/* Global average pool kept as the exact integer sum over h x w of unsigned
+ * codes: out int32 [n][groups*ch_per_group]. */
+palq_status palq_avgsum(palq_ctx *ctx, const palq_act *in, int32_t *out);
+
+/* Fully connected layer on integer features (Eq. 1):
+ * logits[i][o] = sum_c x[i][c] * w[o][c], x int32 [n][cin], w int8
+ * [cout][cin], logits int32 [n][cout].  The sum is formed modulo 2^32, so a
+ * logit is exact whenever its true value fits int32. */
+palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, const int8_t *w,
+                    int32_t cout, int32_t *logits);
+
+/* ------------------------------------------------------------ networks */
+
+#define PALQ_OP_CONV 1
+#define PALQ_OP_MAXPOOL 2
+#define PALQ_OP_AVGSUM 3
+#define PALQ_OP_FC 4
+
+#define PALQ_NET_KEEP_ALL 1 /* every tensor keeps its own buffer (for inspection) */
+#define PALQ_NET_TIMING 2   /* record a HIP event pair around every layer      */
+
+/* One layer of a network.  Tensor ids: 0 is the network input; each layer
+ * writes a new id `dst` larger than every id before it.  Every pointer in
+ * a layer is a HOST pointer to data that palq_net_create copies (the caller
+ * may free it afterwards):
+ *   w.data / proj_w.data: packed filter bytes; mult/shift/bias/res_mult:
+ *   int32 [groups*cout_pg]; fc_w: int8 [fc_out][cin].
+ *  PALQ_OP_CONV    src (codes, viewed as w.groups rows of w.cin_pg codes; a
+ *                  tensor may be re-grouped when its rows have no padding),
+ *                  w, stride, pad, mult/shift/bias (bias nullable), out_bits,
+ *                  shuffle_steps; optional identity shortcut res_src (>= 0)
+ *                  with res_mult, or projection proj_src (>= 0) with proj_w
+ *                  and proj_stride.  Same arithmetic as palq_group_conv.
+ *  PALQ_OP_MAXPOOL src, pool_k, pool_stride, pool_pad.
+ *  PALQ_OP_AVGSUM  src -> int32 sums [n][channels].
+ *  PALQ_OP_FC      src (an AVGSUM output), fc_w, fc_out -> int32 logits.
+ * The last layer must be PALQ_OP_FC; its output is forward's logits. */
+typedef struct {
+  int32_t op;
+  int32_t src, dst;
+  palq_filter w;
+  int32_t stride, pad;
+  const int32_t *mult, *shift, *bias;
+  int32_t out_bits;
+  int32_t shuffle_steps;
+  int32_t res_src;
+  const int32_t *res_mult;
+  int32_t proj_src;
+  palq_filter proj_w;
+  int32_t proj_stride;
+  int32_t pool_k, pool_stride, pool_pad;
+  const int8_t *fc_w;
+  int32_t fc_out;
+} palq_layer;
+
+/* Validates the layer list against the input descriptor (shape, bits, sign;
+ * its data pointer is ignored), plans buffers, copies all parameters to the
+ * device and returns a network bound to ctx.  flags: PALQ_NET_*. */
+palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_layer *layers,
+                            int32_t n_layers, int32_t flags, palq_net **out);
+void palq_net_destroy(palq_net *net);
+
+/* Runs the network on `input` (device, packed as the input descriptor says)
+ * and writes logits (device, int32 [n][fc_out]).  Asynchronous. */
+palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_t *logits);
+
+/* Descriptor (with device data pointer) of tensor `id` after a forward pass.
+ * Conv/maxpool outputs are packed codes; an AVGSUM output is reported with
+ * bits = 32 (int32 values, one per channel, h = w = 1).  Valid for every id
+ * only with PALQ_NET_KEEP_ALL; otherwise buffers are reused between layers. */
+palq_status palq_net_tensor(const palq_net *net, int32_t id, palq_act *desc);
+
+/* Algorithmic work of one forward pass: 2 * multiply-accumulates of every
+ * conv (main and projection) and FC layer (host). */
+int64_t palq_net_ops(const palq_net *net);
+
+/* With PALQ_NET_TIMING: per-layer device time of every forward since the
+ * last reset, summed, in milliseconds (host array of n_layers floats), and
+ * the number of forwards it covers.  Synchronises the stream. */
+palq_status palq_net_layer_times(palq_net *net, float *ms, int32_t *forwards);
+palq_status palq_net_reset_times(palq_net *net);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PALQ_H */

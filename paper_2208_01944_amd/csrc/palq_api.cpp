@@ -1,0 +1,378 @@
+// C ABI of the PalQuant library: context handling, host-side validation of
+// every call, and dispatch to the kernels.  Nothing is enqueued before all
+// checks pass.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+#include <string>
+
+#include "palq_internal.h"
+
+using namespace palq;
+
+namespace {
+
+palq_status fail(palq_ctx *ctx, palq_status code, const std::string &msg) {
+  if (ctx) ctx->err = msg;
+  return code;
+}
+
+palq_status device_fail(palq_ctx *ctx, hipError_t e, const char *what) {
+  return fail(ctx, PALQ_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+bool valid_bits(int b) { return b == 2 || b == 3 || b == 4 || b == 8; }
+
+int64_t act_elems(const palq_act *a) {
+  return (int64_t)a->n * a->h * a->w * a->groups * a->ch_per_group;
+}
+
+// Checks a descriptor; `what` names it in the message.
+palq_status check_act(palq_ctx *ctx, const palq_act *a, const char *what) {
+  if (!a) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": null descriptor");
+  if (a->n < 0 || a->h < 1 || a->w < 1 || a->groups < 1 || a->ch_per_group < 1)
+    return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": non-positive size");
+  if (!valid_bits(a->bits)) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": bits not in {2,3,4,8}");
+  if (a->is_signed != 0 && a->is_signed != 1)
+    return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": is_signed must be 0 or 1");
+  const int64_t row = row_bytes(a->ch_per_group, a->bits);
+  const double bytes = (double)a->n * a->h * a->w * a->groups * (double)row;
+  if (bytes > 9.0e18) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": tensor too large");
+  if (a->n > 0 && !a->data) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": null data");
+  if (((uintptr_t)a->data & 15u) != 0)
+    return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": data not 16-byte aligned");
+  return PALQ_OK;
+}
+
+palq_status check_filter(palq_ctx *ctx, const palq_filter *f, const char *what) {
+  if (!f) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": null filter");
+  if (f->groups < 1 || f->cout_pg < 1 || f->cin_pg < 1 || f->kh < 1 || f->kw < 1)
+    return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": non-positive size");
+  if (!valid_bits(f->bits)) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": bits not in {2,3,4,8}");
+  if (!f->data) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": null data");
+  if (((uintptr_t)f->data & 15u) != 0)
+    return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": data not 16-byte aligned");
+  return PALQ_OK;
+}
+
+int64_t filter_bytes(const palq_filter *f) {
+  return (int64_t)f->groups * f->cout_pg * f->kh * f->kw * row_bytes(f->cin_pg, f->bits);
+}
+
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb) {
+  if (!a || !b || na <= 0 || nb <= 0) return false;
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + (uintptr_t)nb && b0 < a0 + (uintptr_t)na;
+}
+
+int64_t max_code(int bits, int is_signed) {
+  return is_signed ? ((int64_t)1 << (bits - 1)) : (((int64_t)1 << bits) - 1);
+}
+
+bool same_shape(const palq_act *a, const palq_act *b) {
+  return a->n == b->n && a->h == b->h && a->w == b->w && a->groups == b->groups &&
+         a->ch_per_group == b->ch_per_group;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *palq_version(void) { return "palq 0.1 (gfx950)"; }
+
+int64_t palq_row_bytes(int32_t codes, int32_t bits) {
+  if (!valid_bits(bits)) return -1;
+  return row_bytes(codes, bits);
+}
+
+int64_t palq_act_bytes(const palq_act *a) {
+  if (!a || a->n < 0 || a->h < 1 || a->w < 1 || a->groups < 1 || a->ch_per_group < 1 ||
+      !valid_bits(a->bits))
+    return -1;
+  return (int64_t)a->n * a->h * a->w * a->groups * row_bytes(a->ch_per_group, a->bits);
+}
+
+palq_status palq_create(int32_t device, void *hip_stream, palq_ctx **out) {
+  if (!out) return PALQ_ERR_ARG;
+  *out = nullptr;
+  if (device < -1) return PALQ_ERR_ARG;
+  palq_ctx *ctx = new (std::nothrow) palq_ctx();
+  if (!ctx) return PALQ_ERR_NOMEM;
+  ctx->device = device;
+  ctx->stream = (hipStream_t)hip_stream;
+  if (device >= 0) {
+    int count = 0;
+    hipError_t e = hipGetDeviceCount(&count);
+    if (e != hipSuccess || device >= count) {
+      delete ctx;
+      return PALQ_ERR_DEVICE;
+    }
+    e = hipSetDevice(device);
+    if (e == hipSuccess) e = hipMalloc(&ctx->range_scratch, 2 * sizeof(float));
+    if (e != hipSuccess) {
+      delete ctx;
+      return PALQ_ERR_DEVICE;
+    }
+  }
+  *out = ctx;
+  return PALQ_OK;
+}
+
+void palq_destroy(palq_ctx *ctx) {
+  if (!ctx) return;
+  if (ctx->device >= 0) {
+    hipSetDevice(ctx->device);
+    if (ctx->range_scratch) hipFree(ctx->range_scratch);
+  }
+  delete ctx;
+}
+
+palq_status palq_set_stream(palq_ctx *ctx, void *hip_stream) {
+  if (!ctx) return PALQ_ERR_ARG;
+  ctx->stream = (hipStream_t)hip_stream;
+  return PALQ_OK;
+}
+
+palq_status palq_sync(palq_ctx *ctx) {
+  if (!ctx) return PALQ_ERR_ARG;
+  if (ctx->device < 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) return device_fail(ctx, e, "stream synchronize");
+  return PALQ_OK;
+}
+
+const char *palq_last_error(const palq_ctx *ctx) { return ctx ? ctx->err.c_str() : "null context"; }
+
+// ------------------------------------------------------------ layout
+palq_status palq_pack(palq_ctx *ctx, const void *codes, const palq_act *out) {
+  if (!ctx) return PALQ_ERR_ARG;
+  palq_status st = check_act(ctx, out, "out");
+  if (st) return st;
+  if (act_elems(out) > 0 && !codes) return fail(ctx, PALQ_ERR_ARG, "codes: null");
+  if (overlaps(codes, act_elems(out), out->data, palq_act_bytes(out)))
+    return fail(ctx, PALQ_ERR_ARG, "codes and out overlap");
+  if (ctx->device < 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  hipError_t e = launch_pack(codes, view_of(out), ctx->stream);
+  return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "pack");
+}
+
+palq_status palq_unpack(palq_ctx *ctx, const palq_act *in, void *codes) {
+  if (!ctx) return PALQ_ERR_ARG;
+  palq_status st = check_act(ctx, in, "in");
+  if (st) return st;
+  if (act_elems(in) > 0 && !codes) return fail(ctx, PALQ_ERR_ARG, "codes: null");
+  if (overlaps(codes, act_elems(in), in->data, palq_act_bytes(in)))
+    return fail(ctx, PALQ_ERR_ARG, "codes and in overlap");
+  if (ctx->device < 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  hipError_t e = launch_unpack(view_of(in), codes, ctx->stream);
+  return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "unpack");
+}
+
+// ------------------------------------------------------------ quantiser
+palq_status palq_quantize(palq_ctx *ctx, const float *x, float l, float u, const palq_act *out,
+                          float *range_out) {
+  if (!ctx) return PALQ_ERR_ARG;
+  palq_status st = check_act(ctx, out, "out");
+  if (st) return st;
+  const int64_t count = act_elems(out);
+  if (count > 0 && !x) return fail(ctx, PALQ_ERR_ARG, "x: null");
+  if (((uintptr_t)x & 3u) != 0) return fail(ctx, PALQ_ERR_ARG, "x: not 4-byte aligned");
+  const bool calibrate = isnan(l) || isnan(u);
+  if (!calibrate) {
+    if (!isfinite(l) || !isfinite(u)) return fail(ctx, PALQ_ERR_ARG, "l/u must be finite or NaN");
+    if (!(u > l) || !isfinite(u - l)) return fail(ctx, PALQ_ERR_ARG, "need u > l with finite u - l");
+  }
+  if (overlaps(x, count * 4, out->data, palq_act_bytes(out)))
+    return fail(ctx, PALQ_ERR_ARG, "x and out overlap");
+  if (range_out && ((uintptr_t)range_out & 3u) != 0)
+    return fail(ctx, PALQ_ERR_ARG, "range_out: not 4-byte aligned");
+  if (ctx->device < 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  hipError_t e = hipSuccess;
+  const ActView ov = view_of(out);
+  if (calibrate) {
+    e = launch_minmax(x, count, ctx->range_scratch, ctx->stream);
+    if (e == hipSuccess && range_out) e = launch_range_out(ctx->range_scratch, range_out, ctx->stream);
+    if (e == hipSuccess) e = launch_quantize(x, 0.f, 0.f, ctx->range_scratch, ov, ctx->stream);
+  } else {
+    if (range_out) {
+      const float lu[2] = {l, u};
+      e = hipMemcpyAsync(range_out, lu, sizeof(lu), hipMemcpyHostToDevice, ctx->stream);
+      if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);  // lu is on this stack frame
+    }
+    if (e == hipSuccess) e = launch_quantize(x, l, u, nullptr, ov, ctx->stream);
+  }
+  return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "quantize");
+}
+
+// ------------------------------------------------------------ group conv
+palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
+                            int32_t pad, const palq_requant *rq, const palq_residual *res,
+                            int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump) {
+  if (!ctx) return PALQ_ERR_ARG;
+  palq_status st;
+  if ((st = check_act(ctx, in, "in")) || (st = check_filter(ctx, w, "w")) ||
+      (st = check_act(ctx, out, "out")))
+    return st;
+  if (!rq || !rq->mult || !rq->shift) return fail(ctx, PALQ_ERR_ARG, "requant: mult/shift required");
+  if (((uintptr_t)rq->mult | (uintptr_t)rq->shift | (uintptr_t)rq->bias) & 15u)
+    return fail(ctx, PALQ_ERR_ARG, "requant arrays must be 16-byte aligned");
+  if (res && ((uintptr_t)res->res_mult & 15u))
+    return fail(ctx, PALQ_ERR_ARG, "res_mult must be 16-byte aligned");
+  if (!valid_bits(rq->out_bits)) return fail(ctx, PALQ_ERR_ARG, "requant: out_bits not in {2,3,4,8}");
+  if (stride < 1 || pad < 0) return fail(ctx, PALQ_ERR_ARG, "stride must be >= 1 and pad >= 0");
+  if (in->groups != w->groups || in->ch_per_group != w->cin_pg)
+    return fail(ctx, PALQ_ERR_ARG, "input groups/channels do not match the filter");
+  if (in->is_signed ? in->bits != 8 : in->bits == 8)
+    return fail(ctx, PALQ_ERR_UNSUPPORTED,
+                "input codes must be unsigned 2/3/4-bit or signed 8-bit");
+  const int64_t ho = ((int64_t)in->h + 2 * pad - w->kh) / stride + 1;
+  const int64_t wo = ((int64_t)in->w + 2 * pad - w->kw) / stride + 1;
+  if ((int64_t)in->h + 2 * pad < w->kh || (int64_t)in->w + 2 * pad < w->kw || ho < 1 || wo < 1)
+    return fail(ctx, PALQ_ERR_ARG, "kernel larger than the padded input");
+  if (out->n != in->n || out->h != ho || out->w != wo || out->groups != w->groups ||
+      out->ch_per_group != w->cout_pg)
+    return fail(ctx, PALQ_ERR_ARG, "output shape does not match the convolution");
+  if (out->bits != rq->out_bits || out->is_signed)
+    return fail(ctx, PALQ_ERR_ARG, "output must be unsigned codes of requant.out_bits bits");
+  const int64_t K = (int64_t)w->kh * w->kw * w->cin_pg;
+  const int64_t lim = (int64_t)1 << 27;
+  if (K * max_code(in->bits, in->is_signed) * max_code(w->bits, 1) >= lim)
+    return fail(ctx, PALQ_ERR_OVERFLOW, "accumulator bound K*max|a|*max|w| >= 2^27");
+
+  const palq_act *rid = res ? res->identity : nullptr;
+  const palq_act *pin = res ? res->proj_in : nullptr;
+  const palq_filter *pw = res ? res->proj_w : nullptr;
+  if (rid && pin) return fail(ctx, PALQ_ERR_ARG, "residual: identity and projection both given");
+  if (rid) {
+    if ((st = check_act(ctx, rid, "residual.identity"))) return st;
+    if (!same_shape(rid, out) || rid->is_signed)
+      return fail(ctx, PALQ_ERR_ARG, "identity residual must be unsigned codes of the output's shape");
+    if (!res->res_mult) return fail(ctx, PALQ_ERR_ARG, "identity residual needs res_mult");
+  }
+  if (pin || pw) {
+    if (!pin || !pw) return fail(ctx, PALQ_ERR_ARG, "projection needs proj_in and proj_w");
+    if ((st = check_act(ctx, pin, "residual.proj_in")) || (st = check_filter(ctx, pw, "residual.proj_w")))
+      return st;
+    if (pw->kh != 1 || pw->kw != 1 || pw->groups != w->groups || pw->cout_pg != w->cout_pg ||
+        pin->groups != pw->groups || pin->ch_per_group != pw->cin_pg)
+      return fail(ctx, PALQ_ERR_ARG, "projection filter/input do not match");
+    if (pin->is_signed || pin->bits == 8)
+      return fail(ctx, PALQ_ERR_UNSUPPORTED, "projection input must be unsigned 2/3/4-bit codes");
+    if (res->proj_stride < 1) return fail(ctx, PALQ_ERR_ARG, "proj_stride must be >= 1");
+    if (pin->n != in->n || ((int64_t)pin->h - 1) / res->proj_stride + 1 != ho ||
+        ((int64_t)pin->w - 1) / res->proj_stride + 1 != wo)
+      return fail(ctx, PALQ_ERR_ARG, "projection output size differs from the convolution's");
+    if ((int64_t)pw->cin_pg * max_code(pin->bits, 0) * max_code(pw->bits, 1) >= lim)
+      return fail(ctx, PALQ_ERR_OVERFLOW, "projection accumulator bound >= 2^27");
+  }
+  const int64_t ob = palq_act_bytes(out);
+  if (overlaps(out->data, ob, in->data, palq_act_bytes(in)) ||
+      overlaps(out->data, ob, w->data, filter_bytes(w)) ||
+      (rid && overlaps(out->data, ob, rid->data, palq_act_bytes(rid))) ||
+      (pin && overlaps(out->data, ob, pin->data, palq_act_bytes(pin))))
+    return fail(ctx, PALQ_ERR_ARG, "output overlaps an input");
+  const int64_t dump_bytes = (int64_t)out->n * ho * wo * w->groups * w->cout_pg * 4;
+  if (acc_dump && (((uintptr_t)acc_dump & 15u) != 0 || overlaps(acc_dump, dump_bytes, out->data, ob)))
+    return fail(ctx, PALQ_ERR_ARG, "acc_dump misaligned or overlapping the output");
+  if (ctx->device < 0) return PALQ_OK;
+
+  ConvArgs a{};
+  a.in = view_of(in);
+  a.out = view_of(out);
+  a.w = (const uint8_t *)w->data;
+  a.cout = w->cout_pg; a.kh = w->kh; a.kw = w->kw; a.stride = stride; a.pad = pad;
+  a.w_bits = w->bits;
+  a.ho = (int32_t)ho; a.wo = (int32_t)wo;
+  a.mult = rq->mult; a.shift = rq->shift; a.bias = rq->bias;
+  a.shuffle = (int32_t)(((int64_t)shuffle_steps % w->groups + w->groups) % w->groups);
+  if (rid) { a.res = view_of(rid); a.res_mult = res->res_mult; }
+  if (pin) { a.proj = view_of(pin); a.proj_w = (const uint8_t *)pw->data; a.proj_stride = res->proj_stride; }
+  a.acc_dump = acc_dump;
+  if (out->n == 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  hipError_t e = (conv_mfma_supported(a) && (!pin || pw->bits == w->bits))
+                     ? launch_conv_mfma(a, ctx->stream)
+                     : launch_conv_direct(a, ctx->stream);
+  return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "group conv");
+}
+
+// ------------------------------------------------------------ shuffle
+palq_status palq_cyclic_shuffle(palq_ctx *ctx, const palq_act *in, int32_t steps, const palq_act *out) {
+  if (!ctx) return PALQ_ERR_ARG;
+  palq_status st;
+  if ((st = check_act(ctx, in, "in")) || (st = check_act(ctx, out, "out"))) return st;
+  if (!same_shape(in, out) || in->bits != out->bits || in->is_signed != out->is_signed)
+    return fail(ctx, PALQ_ERR_ARG, "in and out must have the same shape and bits");
+  if (overlaps(in->data, palq_act_bytes(in), out->data, palq_act_bytes(out)))
+    return fail(ctx, PALQ_ERR_ARG, "in and out overlap");
+  if (ctx->device < 0 || in->n == 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  const int32_t s = (int32_t)(((int64_t)steps % in->groups + in->groups) % in->groups);
+  hipError_t e = launch_shuffle(view_of(in), s, view_of(out), ctx->stream);
+  return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "cyclic shuffle");
+}
+
+// ------------------------------------------------------------ glue
+palq_status palq_maxpool(palq_ctx *ctx, const palq_act *in, int32_t k, int32_t stride, int32_t pad,
+                         const palq_act *out) {
+  if (!ctx) return PALQ_ERR_ARG;
+  palq_status st;
+  if ((st = check_act(ctx, in, "in")) || (st = check_act(ctx, out, "out"))) return st;
+  if (k < 1 || stride < 1 || pad < 0 || pad >= k)
+    return fail(ctx, PALQ_ERR_ARG, "need k >= 1, stride >= 1, 0 <= pad < k");
+  if (in->is_signed) return fail(ctx, PALQ_ERR_UNSUPPORTED, "max pool takes unsigned codes");
+  if ((int64_t)in->h + 2 * pad < k || (int64_t)in->w + 2 * pad < k)
+    return fail(ctx, PALQ_ERR_ARG, "window larger than the padded input");
+  const int64_t ho = ((int64_t)in->h + 2 * pad - k) / stride + 1;
+  const int64_t wo = ((int64_t)in->w + 2 * pad - k) / stride + 1;
+  if (out->n != in->n || out->h != ho || out->w != wo || out->groups != in->groups ||
+      out->ch_per_group != in->ch_per_group || out->bits != in->bits || out->is_signed)
+    return fail(ctx, PALQ_ERR_ARG, "output shape does not match the pool");
+  if (overlaps(in->data, palq_act_bytes(in), out->data, palq_act_bytes(out)))
+    return fail(ctx, PALQ_ERR_ARG, "in and out overlap");
+  if (ctx->device < 0 || in->n == 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  hipError_t e = launch_maxpool(view_of(in), k, stride, pad, view_of(out), ctx->stream);
+  return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "max pool");
+}
+
+palq_status palq_avgsum(palq_ctx *ctx, const palq_act *in, int32_t *out) {
+  if (!ctx) return PALQ_ERR_ARG;
+  palq_status st = check_act(ctx, in, "in");
+  if (st) return st;
+  if (in->is_signed) return fail(ctx, PALQ_ERR_UNSUPPORTED, "sum takes unsigned codes");
+  if (in->n > 0 && (!out || ((uintptr_t)out & 3u)))
+    return fail(ctx, PALQ_ERR_ARG, "out: null or misaligned");
+  if ((double)in->h * in->w * (double)max_code(in->bits, 0) >= 2147483648.0)
+    return fail(ctx, PALQ_ERR_OVERFLOW, "sum may exceed int32");
+  if (overlaps(in->data, palq_act_bytes(in), out, (int64_t)in->n * in->groups * in->ch_per_group * 4))
+    return fail(ctx, PALQ_ERR_ARG, "in and out overlap");
+  if (ctx->device < 0 || in->n == 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  hipError_t e = launch_avgsum(view_of(in), out, ctx->stream);
+  return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "avgsum");
+}
+
+palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, const int8_t *w,
+                    int32_t cout, int32_t *logits) {
+  if (!ctx) return PALQ_ERR_ARG;
+  if (n < 0 || cin < 1 || cout < 1) return fail(ctx, PALQ_ERR_ARG, "non-positive size");
+  if (n > 0 && (!x || !w || !logits)) return fail(ctx, PALQ_ERR_ARG, "null pointer");
+  if (((uintptr_t)x & 3u) || ((uintptr_t)logits & 3u))
+    return fail(ctx, PALQ_ERR_ARG, "x/logits not 4-byte aligned");
+  if (overlaps(logits, (int64_t)n * cout * 4, x, (int64_t)n * cin * 4) ||
+      overlaps(logits, (int64_t)n * cout * 4, w, (int64_t)cout * cin))
+    return fail(ctx, PALQ_ERR_ARG, "logits overlap an input");
+  if (ctx->device < 0 || n == 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  hipError_t e = launch_fc(x, n, cin, w, cout, logits, ctx->stream);
+  return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "fc");
+}
+
+}  // extern "C"

@@ -1,0 +1,99 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "palq.h"
+
+namespace palq {
+
+// ----------------------------------------------------------------- layout
+// Bytes of a packed row of `codes` codes at `bits` bits (the layout of
+// include/palq.h): 4-byte words for b in {2,4,8}, 12-byte chunks of 32
+// codes for b = 3.
+__host__ __device__ inline int64_t row_bytes(int64_t codes, int bits) {
+  if (codes <= 0) return -1;
+  switch (bits) {
+    case 2: case 4: case 8: return 4 * ((codes * bits + 31) / 32);
+    case 3: return 12 * ((codes + 31) / 32);
+    default: return -1;
+  }
+}
+
+// True when a row holds exactly its codes (no padding bits), so a pixel's
+// rows can be re-grouped without moving data.
+__host__ __device__ inline bool row_exact(int64_t codes, int bits) {
+  if (bits == 3) return codes % 32 == 0;
+  return (codes * bits) % 32 == 0;
+}
+
+// Device view of an activation tensor.
+struct ActView {
+  uint8_t *data;
+  int32_t n, h, w, groups, cpg, bits, is_signed;
+  int64_t row;    // bytes per (pixel, group) row
+  int64_t pixel;  // bytes per pixel = groups * row
+};
+
+inline ActView view_of(const palq_act *a) {
+  ActView v;
+  v.data = (uint8_t *)a->data;
+  v.n = a->n; v.h = a->h; v.w = a->w;
+  v.groups = a->groups; v.cpg = a->ch_per_group;
+  v.bits = a->bits; v.is_signed = a->is_signed;
+  v.row = row_bytes(a->ch_per_group, a->bits);
+  v.pixel = v.row * a->groups;
+  return v;
+}
+
+// ----------------------------------------------------------------- conv
+// Everything a conv launch needs, all device pointers.
+struct ConvArgs {
+  ActView in;            // input codes
+  ActView out;           // output codes
+  const uint8_t *w;      // packed filter
+  int32_t cout, kh, kw, stride, pad, w_bits;
+  int32_t ho, wo;
+  const int32_t *mult, *shift, *bias;  // bias may be null
+  int32_t shuffle;                     // already reduced to [0, G)
+  // identity shortcut
+  ActView res;           // res.data null when absent
+  const int32_t *res_mult;
+  // projection shortcut (fused as extra contraction)
+  ActView proj;          // proj.data null when absent
+  const uint8_t *proj_w;
+  int32_t proj_stride;
+  int32_t *acc_dump;     // may be null
+};
+
+// Kernel launchers (return hipError_t of the launch).
+hipError_t launch_conv_direct(const ConvArgs &a, hipStream_t s);
+// Returns hipErrorNotSupported when the shape is outside the MFMA path.
+bool conv_mfma_supported(const ConvArgs &a);
+hipError_t launch_conv_mfma(const ConvArgs &a, hipStream_t s);
+
+hipError_t launch_pack(const void *codes, const ActView &out, hipStream_t s);
+hipError_t launch_unpack(const ActView &in, void *codes, hipStream_t s);
+hipError_t launch_minmax(const float *x, int64_t count, float *range, hipStream_t s);
+hipError_t launch_range_out(const float *enc, float *range_out, hipStream_t s);
+hipError_t launch_quantize(const float *x, float l, float u, const float *range, const ActView &out,
+                           hipStream_t s);
+hipError_t launch_shuffle(const ActView &in, int32_t steps, const ActView &out, hipStream_t s);
+hipError_t launch_maxpool(const ActView &in, int k, int stride, int pad, const ActView &out,
+                          hipStream_t s);
+hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s);
+hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout, int32_t *logits,
+                     hipStream_t s);
+
+}  // namespace palq
+
+// The context (opaque to callers).
+struct palq_ctx {
+  int device = -1;           // -1: validate only
+  hipStream_t stream = nullptr;
+  std::string err;
+  float *range_scratch = nullptr;  // 2 floats for calibration without range_out
+};

@@ -1,0 +1,99 @@
+"""GPU parity of palq_forward (whole networks) against the CPU oracle."""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2208_01944_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    from paper_2208_01944_amd import palq
+    return palq.Context(0)
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    return torch
+
+
+def gpu_forward(ctx, torch, spec, keep=False):
+    from paper_2208_01944_amd import palq
+    net = palq.Net(ctx, spec, flags=palq.NET_KEEP_ALL if keep else 0)
+    x = spec["x"]
+    xt = ctx.pack(x, 1, 8, signed=True)
+    logits = torch.empty(x.shape[0] * net.classes, dtype=torch.int32, device=ctx.dev)
+    net.forward(xt.buf, logits)
+    ctx.sync()
+    return net, logits.cpu().numpy().astype(np.int64).reshape(x.shape[0], net.classes)
+
+
+def compare_tensors(ctx, net, spec, tensors, images):
+    for L in spec["layers"]:
+        d = L["dst"]
+        if L["op"] in ("conv", "maxpool"):
+            got = ctx.unpack(net.tensor(d))[images]
+            np.testing.assert_array_equal(got, tensors[d], err_msg=f"tensor {d} ({L['op']})")
+
+
+@pytest.mark.parametrize("variant", ["stated", "centred"])
+def test_resnet18_small_all_tensors(ctx, torch, variant):
+    say(f"resnet18 hw=64 n=2 G=4 b=2 {variant}")
+    spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=11)
+    if variant == "centred":
+        spec = O.calibrate_centring(spec, spec["x"])
+    net, logits = gpu_forward(ctx, torch, spec, keep=True)
+    ref, tensors, _ = O.run_net(spec, spec["x"], keep=True)
+    compare_tensors(ctx, net, spec, tensors, slice(None))
+    np.testing.assert_array_equal(logits, ref)
+
+
+def test_resnet50_small_all_tensors(ctx, torch):
+    say("resnet50 hw=64 n=2 G=2 b=2 centred")
+    spec = I.resnet50(n=2, groups=2, bits=2, hw=64, classes=50, seed=12)
+    spec = O.calibrate_centring(spec, spec["x"])
+    net, logits = gpu_forward(ctx, torch, spec, keep=True)
+    ref, tensors, _ = O.run_net(spec, spec["x"], keep=True)
+    compare_tensors(ctx, net, spec, tensors, slice(None))
+    np.testing.assert_array_equal(logits, ref)
+
+
+def test_resnet18_bits3_g3(ctx, torch):
+    say("resnet18 hw=32 n=3 G=3 b=3 centred")
+    spec = I.resnet18(n=3, groups=3, bits=3, hw=32, classes=10, seed=13)
+    spec = O.calibrate_centring(spec, spec["x"])
+    _, logits = gpu_forward(ctx, torch, spec)
+    np.testing.assert_array_equal(logits, O.run_net(spec, spec["x"]))
+
+
+def test_c3_full_size_sampled(ctx, torch):
+    """The benchmark workload (ResNet-18 topology, G=4, 2-bit, 224x224,
+    batch 64) at full size; the oracle runs the first and last image."""
+    say("C3 resnet18 n=64 224x224 G=4 b=2 (centred on images 0 and 63)")
+    spec = I.resnet18()
+    pick = [0, 63]
+    spec = O.calibrate_centring(spec, spec["x"][pick])
+    net, logits = gpu_forward(ctx, torch, spec)
+    ref = O.run_net(spec, spec["x"][pick])
+    np.testing.assert_array_equal(logits[pick], ref)
+    assert len(np.unique(ref)) > 100  # logits are not degenerate
+
+
+def test_c5_full_size_sampled(ctx, torch):
+    say("C5 resnet50 n=128 224x224 G=2 b=2 (centred on image 127)")
+    spec = I.resnet50()
+    pick = [127]
+    spec = O.calibrate_centring(spec, spec["x"][pick])
+    net, logits = gpu_forward(ctx, torch, spec)
+    ref = O.run_net(spec, spec["x"][pick])
+    np.testing.assert_array_equal(logits[pick], ref)

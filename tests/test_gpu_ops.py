@@ -1,0 +1,271 @@
+"""GPU parity of the single-op entry points against the CPU oracle.
+
+Every case draws seeded inputs (paper_2208_01944_amd.inputs), runs the HIP
+library through its C ABI and compares with oracle/ element by element:
+codes and int32 accumulators bit-exact.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2208_01944_amd import inputs as I
+from tests import packref
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    from paper_2208_01944_amd import palq
+    return palq.Context(0)
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    return torch
+
+
+# ---------------------------------------------------------------- layout
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
+@pytest.mark.parametrize("cpg", [1, 5, 16, 37, 64, 96])
+def test_pack_bytes_match_reference(ctx, bits, cpg):
+    say(f"pack bits={bits} cpg={cpg}")
+    g = np.random.default_rng(bits * 100 + cpg)
+    for signed in (False, True):
+        x = I.codes(g, (2, 3, 5, 3 * cpg), bits, signed).astype(np.int64)
+        t = ctx.pack(x, 3, bits, signed)
+        got = t.buf[:packref.row_bytes(cpg, bits) * 2 * 3 * 5 * 3].cpu().numpy()
+        np.testing.assert_array_equal(got, packref.pack(x, 3, bits))
+        np.testing.assert_array_equal(ctx.unpack(t), x)
+
+
+# ---------------------------------------------------------------- quantiser
+@pytest.mark.parametrize("bits,signed", [(2, False), (3, False), (4, False), (8, True), (2, True)])
+def test_quantize_matches_oracle(ctx, torch, bits, signed):
+    say(f"quantize bits={bits} signed={signed}")
+    g = np.random.default_rng(bits)
+    x = g.normal(0, 1.5, (3, 17, 11, 2 * 21)).astype(np.float32)
+    x.flat[::97] = np.nan
+    x.flat[5::211] = np.inf
+    x.flat[7::233] = -np.inf
+    # exact ties of Eq. 2 for l=0, u=3 at 2 bits
+    x.flat[:3] = [0.5, 1.5, 2.5]
+    xd = ctx.upload(x)
+    out = ctx.empty_act(3, 17, 11, 2, 21, bits, signed)
+    rng = torch.empty(2, dtype=torch.float32, device=ctx.dev)
+    ctx.quantize(xd, -2.0, 3.0, out, rng)
+    np.testing.assert_array_equal(ctx.unpack(out), O.quantize(x, -2.0, 3.0, bits, signed))
+    np.testing.assert_array_equal(rng.cpu().numpy(), np.array([-2.0, 3.0], np.float32))
+    # calibrated range (NaN bounds): min/max of the finite... non-NaN values
+    x2 = np.where(np.isinf(x), 0.0, x).astype(np.float32)
+    ctx.quantize(ctx.upload(x2), float("nan"), float("nan"), out, rng)
+    l, u = O.calibrate_range(x2)
+    np.testing.assert_array_equal(rng.cpu().numpy(), np.array([l, u], np.float32))
+    np.testing.assert_array_equal(ctx.unpack(out), O.quantize(x2, l, u, bits, signed))
+
+
+# ---------------------------------------------------------------- conv
+def run_conv(ctx, torch, case, centred=False):
+    """Runs a single_layer() case on the GPU; returns (codes, acc, ref_codes, ref_acc)."""
+    L = case["layer"]
+    x = case["x"]
+    G, co, kh, kw, ci = L["w"].shape
+    res = case["extra"].get(1) if L["res"] >= 0 else None
+    px = case["extra"].get(1) if L["proj_src"] >= 0 else None
+    bias = L["bias"]
+    if centred:
+        _, acc0 = O.conv_layer(x, L["w"], L["stride"], L["pad"], L["mult"], L["shift"], None,
+                               L["out_bits"], L["shuffle"], res=res, res_mult=L["res_mult"],
+                               proj_x=px, proj_w=L["proj_w"], proj_stride=L["proj_stride"])
+        t = acc0
+        if res is not None:
+            t = t + O.cyclic_permute(np.asarray(L["res_mult"], np.int64), G, L["shuffle"]) * res
+        mean = np.floor(t.reshape(-1, t.shape[-1]).mean(axis=0) + 0.5).astype(np.int64)
+        bias = O.cyclic_permute(-mean, G, -L["shuffle"]).astype(np.int32)
+    ref_q, ref_acc = O.conv_layer(x, L["w"], L["stride"], L["pad"], L["mult"], L["shift"], bias,
+                                  L["out_bits"], L["shuffle"], res=res, res_mult=L["res_mult"],
+                                  proj_x=px, proj_w=L["proj_w"], proj_stride=L["proj_stride"])
+    in_signed = bool(L["in_signed"])
+    xt = ctx.pack(x, G, L["in_bits"], in_signed)
+    wt, wf = ctx.pack_filter(L["w"], L["w_bits"])
+    n, h, w, _ = x.shape
+    ho = (h + 2 * L["pad"] - kh) // L["stride"] + 1
+    wo = (w + 2 * L["pad"] - kw) // L["stride"] + 1
+    out = ctx.empty_act(n, ho, wo, G, co, L["out_bits"])
+    dump = torch.zeros(max(n * ho * wo * G * co, 4), dtype=torch.int32, device=ctx.dev)
+    i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
+    kw_ = {}
+    if res is not None:
+        kw_["identity"] = ctx.pack(res, G, L["out_bits"])
+        kw_["res_mult"] = i32(L["res_mult"])
+    if px is not None:
+        kw_["proj_in"] = ctx.pack(px, G, L["in_bits"])
+        pt, kw_["proj_w"] = ctx.pack_filter(L["proj_w"], L["w_bits"])
+        kw_["proj_stride"] = L["proj_stride"]
+    ctx.group_conv(xt, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(bias), out,
+                   shuffle=L["shuffle"], acc_dump=dump, **kw_)
+    ctx.sync()
+    acc = dump[:n * ho * wo * G * co].cpu().numpy().astype(np.int64).reshape(ref_acc.shape)
+    return ctx.unpack(out), acc, ref_q, ref_acc
+
+
+def check_conv(ctx, torch, case, centred=False, spread=False):
+    q, acc, rq, racc = run_conv(ctx, torch, case, centred)
+    np.testing.assert_array_equal(acc, racc)
+    np.testing.assert_array_equal(q, rq)
+    if spread:  # the centred variant must exercise every output code
+        hist = np.bincount(rq.reshape(-1), minlength=1 << case["layer"]["out_bits"])
+        assert np.all(hist > 0), hist
+
+
+def test_conv_c1_stated_and_centred(ctx, torch):
+    say("conv C1 (N=1, 56x56, G=2, 64->64, 2-bit, shift 20)")
+    case = I.config_c1()
+    check_conv(ctx, torch, case)
+    check_conv(ctx, torch, case, centred=True, spread=True)
+
+
+CONV_CASES = [
+    # several tiles + ragged tail, MFMA path
+    dict(n=2, h=13, w=13, groups=3, cin=64, cout=64, k=3, stride=1, pad=1, bits=2),
+    dict(n=2, h=15, w=15, groups=2, cin=64, cout=96, k=3, stride=2, pad=1, bits=2),
+    dict(n=3, h=9, w=11, groups=2, cin=128, cout=64, k=1, stride=1, pad=0, bits=2),
+    dict(n=2, h=10, w=10, groups=2, cin=64, cout=64, k=3, stride=1, pad=1, bits=3),
+    dict(n=2, h=10, w=10, groups=2, cin=64, cout=128, k=3, stride=1, pad=1, bits=4),
+    dict(n=1, h=7, w=7, groups=4, cin=192, cout=32, k=3, stride=1, pad=1, bits=2),
+    dict(n=2, h=6, w=5, groups=2, cin=64, cout=64, k=3, stride=1, pad=1, bits=2, out_bits=8),
+    dict(n=2, h=6, w=5, groups=2, cin=64, cout=64, k=3, stride=1, pad=1, bits=2, out_bits=3),
+    dict(n=2, h=6, w=5, groups=2, cin=64, cout=64, k=3, stride=1, pad=1, bits=2, out_bits=4),
+    dict(n=2, h=8, w=8, groups=4, cin=64, cout=64, k=3, stride=1, pad=1, bits=2, residual="identity"),
+    dict(n=2, h=9, w=9, groups=4, cin=64, cout=64, k=3, stride=2, pad=1, bits=2, residual="projection"),
+    dict(n=2, h=8, w=8, groups=3, cin=64, cout=64, k=3, stride=1, pad=1, bits=3, residual="identity"),
+    # direct path: odd channel counts, mixed widths, 5x5
+    dict(n=2, h=7, w=6, groups=3, cin=5, cout=7, k=3, stride=1, pad=1, bits=2),
+    dict(n=1, h=9, w=9, groups=2, cin=16, cout=40, k=5, stride=2, pad=2, bits=4),
+    dict(n=2, h=6, w=6, groups=2, cin=20, cout=20, k=3, stride=1, pad=0, bits=3, residual="identity"),
+    dict(n=2, h=7, w=7, groups=2, cin=24, cout=32, k=3, stride=2, pad=1, bits=2, residual="projection"),
+    dict(n=2, h=6, w=6, groups=2, cin=64, cout=64, k=3, stride=1, pad=1, bits=2, w_bits=4),
+]
+
+
+@pytest.mark.parametrize("i", range(len(CONV_CASES)))
+@pytest.mark.parametrize("shuffle", [0, 1, -1, 7])
+def test_conv_cases(ctx, torch, i, shuffle):
+    p = dict(CONV_CASES[i])
+    say(f"conv case {i} {p} shuffle={shuffle}")
+    case = I.single_layer(1000 + i, shuffle=shuffle, **p)
+    check_conv(ctx, torch, case, centred=(shuffle == 1))
+
+
+def test_conv_stem_shape(ctx, torch):
+    """8-bit signed input, 3 channels, 7x7/s2/p3 (the network's first layer)."""
+    say("conv stem 8-bit 7x7/s2")
+    g = I.rng(77)
+    x = I.codes(g, (2, 23, 21, 3), 8, True)
+    L = I.conv_layer_spec(g, src=0, dst=1, groups=1, cin=3, cout=64, k=7, stride=2, pad=3,
+                          in_bits=8, in_signed=True, w_bits=8, out_bits=2)
+    check_conv(ctx, torch, dict(x=x, extra={}, layer=L), centred=True)
+
+
+def test_conv_empty_batch(ctx, torch):
+    say("conv n=0")
+    case = I.single_layer(5, n=0, h=8, w=8, groups=2, cin=64, cout=64)
+    q, acc, rq, racc = run_conv(ctx, torch, case)
+    assert q.size == 0 and racc.size == 0
+
+
+@pytest.mark.parametrize("layer", range(4))
+def test_conv_c2_full_batch_sampled(ctx, torch, layer):
+    """Each ResNet-18 stage shape at G=4, batch 32, in the launch the benchmark
+    uses; the oracle checks the first and last image."""
+    say(f"conv C2 layer {layer} batch 32")
+    case = I.config_c2(layer)
+    full = run_conv_full(ctx, torch, case)
+    for img in (0, 31):
+        sub = dict(case, x=case["x"][img:img + 1])
+        _, _, rq, racc = run_conv(ctx, torch, sub)
+        np.testing.assert_array_equal(full[0][img:img + 1], rq)
+        np.testing.assert_array_equal(full[1][img:img + 1], racc)
+
+
+def run_conv_full(ctx, torch, case):
+    """GPU only (no oracle): codes and accumulators of the whole batch."""
+    L = case["layer"]
+    x = case["x"]
+    G, co, kh, kw, ci = L["w"].shape
+    xt = ctx.pack(x, G, L["in_bits"])
+    wt, wf = ctx.pack_filter(L["w"], L["w_bits"])
+    n, h, w, _ = x.shape
+    ho = (h + 2 * L["pad"] - kh) // L["stride"] + 1
+    wo = (w + 2 * L["pad"] - kw) // L["stride"] + 1
+    out = ctx.empty_act(n, ho, wo, G, co, L["out_bits"])
+    dump = torch.zeros(n * ho * wo * G * co, dtype=torch.int32, device=ctx.dev)
+    i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
+    ctx.group_conv(xt, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(L["bias"]),
+                   out, shuffle=L["shuffle"], acc_dump=dump)
+    ctx.sync()
+    acc = dump.cpu().numpy().astype(np.int64).reshape(n, ho, wo, G * co)
+    return ctx.unpack(out), acc
+
+
+@pytest.mark.parametrize("groups", [1, 2, 4])
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_conv_c4_sweep_sampled(ctx, torch, groups, bits):
+    say(f"conv C4 G={groups} b={bits} batch 128")
+    case = I.config_c4(groups, bits)
+    full = run_conv_full(ctx, torch, case)
+    for img in (0, 127):
+        sub = dict(case, x=case["x"][img:img + 1])
+        _, _, rq, racc = run_conv(ctx, torch, sub)
+        np.testing.assert_array_equal(full[1][img:img + 1], racc)
+        np.testing.assert_array_equal(full[0][img:img + 1], rq)
+
+
+def test_conv_deterministic(ctx, torch):
+    say("conv determinism")
+    case = I.config_c2(1, n=4)
+    a = run_conv_full(ctx, torch, case)
+    b = run_conv_full(ctx, torch, case)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+
+
+# ---------------------------------------------------------------- shuffle & glue
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
+def test_cyclic_shuffle(ctx, bits):
+    say(f"shuffle bits={bits}")
+    g = np.random.default_rng(bits)
+    x = I.codes(g, (2, 5, 4, 4 * 40), bits, False).astype(np.int64)
+    t = ctx.pack(x, 4, bits)
+    out = ctx.empty_act(2, 5, 4, 4, 40, bits)
+    for s in (0, 1, 3, 4, -1, 9):
+        ctx.cyclic_shuffle(t, s, out)
+        np.testing.assert_array_equal(ctx.unpack(out), O.cyclic_permute(x, 4, s))
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_maxpool_avgsum_fc(ctx, torch, bits):
+    say(f"maxpool/avgsum/fc bits={bits}")
+    g = np.random.default_rng(bits)
+    x = I.codes(g, (3, 13, 12, 2 * 48), bits, False).astype(np.int64)
+    t = ctx.pack(x, 2, bits)
+    out = ctx.empty_act(3, 7, 6, 2, 48, bits)
+    ctx.maxpool(t, 3, 2, 1, out)
+    np.testing.assert_array_equal(ctx.unpack(out), O.maxpool(x, 3, 2, 1))
+    sums = torch.empty(3 * 96, dtype=torch.int32, device=ctx.dev)
+    ctx.avgsum(t, sums)
+    ref_s = O.avgsum(x)
+    np.testing.assert_array_equal(sums.cpu().numpy().reshape(3, 96), ref_s)
+    w = I.codes(g, (10, 96), 8, True)
+    logits = torch.empty(30, dtype=torch.int32, device=ctx.dev)
+    ctx.fc(sums, 3, 96, ctx.upload(w), 10, logits)
+    ctx.sync()
+    np.testing.assert_array_equal(logits.cpu().numpy().reshape(3, 10), O.fc(ref_s, w))
