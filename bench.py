@@ -121,7 +121,9 @@ def main():
             kk = k * k * ci + (L["proj_w"].shape[-1] if L.get("proj_w") is not None else 0)
             ops = 2 * n * ho * ho * g * co * kk
             shapes[L["dst"]] = (ho, ho, g * co)
-            mfma = ci % 64 == 0 and co % 32 == 0 and L["in_bits"] == L["w_bits"] and not L["in_signed"]
+            stem = L["in_bits"] == 8 and L["in_signed"] and L["w_bits"] == 8 and ci <= 4 and k <= 8
+            mfma = co % 32 == 0 and (stem or (ci % 64 == 0 and L["in_bits"] == L["w_bits"]
+                                               and not L["in_signed"]))
             per_layer.append(dict(layer=i, op="conv", kernel="mfma" if mfma else "direct",
                                   ops=ops, ms=float(layer_ms[i])))
             if mfma:

@@ -167,8 +167,9 @@ palq_status palq_quantize(palq_ctx *ctx, const float *x, float l, float u, const
  *   acc_dump (nullable, 16-byte aligned): int32 [n][ho][wo][groups*cout_pg], the sum of all
  *         products that land in each output channel (destination order:
  *         the permuted main accumulator plus any projection accumulator).
- * PALQ_ERR_OVERFLOW when K*max|code|*max|weight| >= 2^27 for the main or the
- * projection product (K = kh*kw*cin_pg).  out must not overlap any input. */
+ * PALQ_ERR_OVERFLOW when K*max|code|*max|weight| (K = kh*kw*cin_pg), plus
+ * the same bound of the projection product, reaches 2^26.  out must not
+ * overlap any input. */
 palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
                             int32_t pad, const palq_requant *rq, const palq_residual *res,
                             int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump);

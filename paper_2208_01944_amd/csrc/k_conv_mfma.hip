@@ -2,30 +2,36 @@
 //
 // Per group g (Section 4.1: G independent B-bit convolutions) the layer is
 // D[k][m] = sum_K W[k][K] X[K][m] (Eq. 1) with k an output channel of the
-// group, m an output pixel (n, oy, ox) and K = (ky, kx, c).  One workgroup
-// owns a tile of CB*32 output channels x 4*PB*32 pixels of one group; its
-// four waves share the channels and split the pixels.
+// group, m an output pixel (n, oy, ox) and K = (ky, kx, c), contracted with
+// v_mfma_i32_32x32x32_i8: A = weights (rows = channels), B = activations
+// (columns = pixels), int32 accumulation.
 //
-//  * Weights (MFMA A operand, rows = channels): packed b-bit units are read
-//    from global memory, sign-extended to int8 in registers and written to
-//    LDS in MFMA operand order, KS 64-code K-blocks per stage, two stages in
-//    flight (one barrier per stage).
-//  * Activations (MFMA B operand, columns = pixels): each lane reads its own
-//    pixel's packed codes for the current tap straight from global memory
-//    (the 3x3 taps re-hit L1/L2) and unpacks them in registers with a few
-//    shift/mask operations.  K order inside a 16-code unit is permuted by
-//    the unpack; the weights are placed with the same permutation, which
-//    leaves the contraction unchanged.
+//  * Weights are prepacked once per layer (prepack_kernel): sign-extended to
+//    int8, in MFMA operand order, 2 KB per (64-code K-block, 32 channels).
+//    A persistent workgroup copies the whole K extent of its 32 or 64
+//    channels into LDS once and keeps it there.
+//  * Activations stay packed in HBM; each lane reads its own pixel's codes
+//    for the current tap with a buffer load (out-of-image taps and pixels
+//    past the end use an out-of-range offset, which the hardware returns as
+//    zero) and unpacks them in registers with a few shift/mask operations.
+//    The K order inside a 16-code unit is permuted by the unpack; the
+//    weights are prepacked with the same permutation, which leaves the
+//    contraction unchanged.
 //  * 2-bit codes: the unpack leaves code 4e+d of a unit at bits 2d..2d+1 of
 //    byte e without shifting it down (d = 0, 1, 2) or after one shift
 //    (d = 3), i.e. scaled by 1, 4, 16, 16; the weights of those positions
 //    are pre-scaled by 16, 4, 1, 1 so every product carries the factor 16,
-//    which the epilogue removes exactly with an arithmetic shift.
-//  * Epilogue: int32 accumulator -> + bias + shortcut (int64) -> fixed-point
-//    requant with ReLU -> b-bit codes, written to group (g + s) mod G: the
-//    cyclic permutation of Eq. 8 is only the store address.  A projection
-//    shortcut is fused as extra K-blocks (1x1 conv of the block input of the
+//    which the epilogue removes exactly.
+//  * Epilogue: accumulator + shortcut -> exact fixed-point requant with
+//    ReLU -> b-bit codes, written to group (g + s) mod G: the cyclic
+//    permutation of Eq. 8 is only the store address.  A projection shortcut
+//    is fused as extra K-blocks (1x1 conv of the block input of the
 //    destination group), so its accumulator lands in the same registers.
+#include <stdio.h>
+#include <stdlib.h>
+
+#include <algorithm>
+
 #include "codes.h"
 #include "palq_internal.h"
 
@@ -36,8 +42,6 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
-constexpr int kWaves = 4;
-constexpr int kThreads = kWaves * 64;
 
 // ---------------------------------------------------------------- unpack
 // Activation unit (16 unsigned codes) -> MFMA operand (16 int8), and the
@@ -110,28 +114,13 @@ template <int B> struct Blk {
   static constexpr int lane_words = B;      // 32 codes = B words (3 for B = 3)
 };
 
-// Raw packed words a lane holds for one K-block (its half: two units).
-template <int B> struct Raw { uint32_t w[B]; };
-
-template <int B>
-__device__ inline Raw<B> load_half(const uint8_t *p, bool valid) {
-  Raw<B> r;
-  if constexpr (B == 2) {
-    uint2 v = valid ? *(const uint2 *)p : make_uint2(0, 0);
-    r.w[0] = v.x; r.w[1] = v.y;
-  } else if constexpr (B == 4) {
-    uint4 v = valid ? *(const uint4 *)p : make_uint4(0, 0, 0, 0);
-    r.w[0] = v.x; r.w[1] = v.y; r.w[2] = v.z; r.w[3] = v.w;
-  } else {
-    const uint32_t *q = (const uint32_t *)p;
-    r.w[0] = valid ? q[0] : 0u; r.w[1] = valid ? q[1] : 0u; r.w[2] = valid ? q[2] : 0u;
-  }
-  return r;
-}
+// Raw packed words a lane holds for one K-block (its half: two units); the
+// stem layout holds eight 4-byte pixels.
+template <int B, bool STEM> struct RawT { uint32_t w[STEM ? 8 : B]; };
 
 // MFMA B operand for K-step j (0/1) from a lane's raw half block.
 template <int B>
-__device__ inline v4i act_operand(const Raw<B> &r, int j) {
+__device__ inline v4i act_operand(const RawT<B, false> &r, int j) {
   if constexpr (B == 2) return act_unpack2(r.w[j]);
   else if constexpr (B == 4) return unpack4_nibbles(r.w[2 * j], r.w[2 * j + 1]);
   else return unpack3(r.w[j], r.w[2], j);
@@ -146,334 +135,863 @@ __device__ inline v4i load_weight_unit(const uint8_t *p, int u) {
   else return wt_unpack3(q[3 * (u >> 1) + (u & 1)], q[3 * (u >> 1) + 2], u & 1);
 }
 
-// ---------------------------------------------------------------- epilogue
-__device__ inline int64_t requant_one(int64_t t, int32_t m, int32_t sh, int qmax) {
+// ---------------------------------------------------------------- requant
+// Exact fixed-point requant with an int64 product (fallback path).
+__device__ inline int requant_mul(int64_t t, int32_t m, int32_t sh, int qmax) {
   const int64_t num = t * (int64_t)m + ((int64_t)1 << (sh - 1));
   int64_t q = num >> sh;
   q = q < 0 ? 0 : q;
-  return q > qmax ? qmax : q;
+  return (int)(q > qmax ? qmax : q);
 }
 
 // Code j (0..31) of a 32-code chunk held in registers.
 __device__ inline int chunk_code(const uint32_t *cw, int j, int bits) {
   if (bits == 3) {
-    uint32_t v = (cw[j >> 4] >> (2 * (j & 15))) & 3u;
+    const uint32_t v = (cw[j >> 4] >> (2 * (j & 15))) & 3u;
     return (int)(v | (((cw[2] >> b3_hi_pos(j)) & 1u) << 2));
   }
   const int bit = j * bits;
   return (int)((cw[bit >> 5] >> (bit & 31)) & ((1u << bits) - 1u));
 }
 
-// ---------------------------------------------------------------- kernel
-struct Geo {
-  int32_t M;          // output pixels per group
-  int32_t taps;       // kh * kw
-  int32_t cpb;        // 64-code blocks per tap row
-  int32_t kb_main;    // taps * cpb
-  int32_t kb_total;   // + projection blocks
-  int32_t pcpb;       // projection 64-code blocks
-  int64_t w_ch;       // bytes of one output channel's filter (all taps)
-  int64_t pw_ch;      // bytes of one projection channel
+// Codes of 4 consecutive channels c0..c0+3 (c0 % 4 == 0) of a packed row.
+__device__ inline void row_quad(const uint8_t *row, int c0, int bits, int out[4]) {
+  const uint32_t *w = (const uint32_t *)row;
+  if (bits == 3) {
+    const uint32_t *ch = w + 3 * (c0 >> 5);
+    const int j0 = c0 & 31;
+    const uint32_t lo = ch[j0 >> 4] >> (2 * (j0 & 15));
+    const uint32_t hi = ch[2];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      out[e] = (int)(((lo >> (2 * e)) & 3u) | (((hi >> b3_hi_pos(j0 + e)) & 1u) << 2));
+    return;
+  }
+  const int bit = c0 * bits;
+  const uint32_t v = w[bit >> 5] >> (bit & 31);
+  const uint32_t mask = (1u << bits) - 1u;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) out[e] = (int)((v >> (bits * e)) & mask);
+}
+
+// Per-channel requant constants in fp64.  With v = scale * (acc + residual)
+// (an integer, |v| < 2^31) and t = acc + residual + bias:
+//   s = M 2^-sh / scale,  o = (bias M + 2^(sh-1)) 2^-sh,
+//   fma(v, s, o) = (t M + 2^(sh-1)) 2^-sh exactly whenever |t| M < 2^52,
+// so q = clamp(trunc(fma(v, s, o)), 0, qmax) equals the definition (trunc
+// and floor differ only below zero, where both clamp to 0).  The prep kernel
+// checks that bound for every channel from the accumulator bound; if any
+// channel could break it, the layer's flag selects the int64 path instead.
+struct RqConst {
+  double s, o;
 };
 
-template <int B, int CB, int PB, int KS>
-__global__ __launch_bounds__(kThreads) void conv_mfma_kernel(ConvArgs a, Geo geo) {
-  constexpr int TPIX = kWaves * PB * 32;
-  constexpr int KSTEP_BYTES = 32 * 16;                 // one (cb, half) slab: 32 ch x 16 B
-  constexpr int KBLK_BYTES = 2 * CB * 2 * KSTEP_BYTES; // 2 K-steps x CB x 2 halves
-  constexpr int STAGE_BYTES = KS * KBLK_BYTES;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * STAGE_BYTES];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int l32 = lane & 31;
-  const int half = lane >> 5;
-
-  const int G = a.in.groups;
-  const int g = blockIdx.z;
-  const int gd = (g + a.shuffle) % G;
-  const int ch0 = blockIdx.y * CB * 32;          // first output channel of the tile (in group)
-  const int64_t m0 = (int64_t)blockIdx.x * TPIX;
-
-  // ---- per pixel-block geometry of this lane
-  int iy0[PB], ix0[PB], nimg[PB];
-  bool pvalid[PB];
-  int64_t mpix[PB];
-  _Pragma("unroll") for (int pb = 0; pb < PB; ++pb) {
-    const int64_t m = m0 + (wave * PB + pb) * 32 + l32;
-    mpix[pb] = m;
-    pvalid[pb] = m < geo.M;
-    const int64_t mm = pvalid[pb] ? m : 0;
-    const int ox = (int)(mm % a.wo);
-    const int oy = (int)((mm / a.wo) % a.ho);
-    nimg[pb] = (int)(mm / ((int64_t)a.wo * a.ho));
-    iy0[pb] = oy * a.stride - a.pad;
-    ix0[pb] = ox * a.stride - a.pad;
-  }
-
-  // ---- weight staging: items (cb, ch, kbl, u), 4 units per (channel, block)
-  constexpr int ITEMS = CB * 32 * KS * 4;
-  static_assert(ITEMS % kThreads == 0, "stage items must divide the block");
-  constexpr int IPT = ITEMS / kThreads;
-
-  auto stage_weights = [&](int kb0, v4i (&regs)[IPT]) {
-    _Pragma("unroll") for (int i = 0; i < IPT; ++i) {
-      const int item = i * kThreads + tid;
-      const int u = item & 3;
-      const int kbl = (item >> 2) % KS;
-      const int chn = (item >> 2) / KS;  // cb*32 + ch
-      const int kb = kb0 + kbl;
-      v4i v = {0, 0, 0, 0};
-      if (kb < geo.kb_total) {
-        const int k = ch0 + chn;
-        const uint8_t *p;
-        if (kb < geo.kb_main) {
-          p = a.w + ((int64_t)g * a.cout + k) * geo.w_ch + (int64_t)kb * Blk<B>::bytes;
-        } else {
-          p = a.proj_w + ((int64_t)gd * a.cout + k) * geo.pw_ch +
-              (int64_t)(kb - geo.kb_main) * Blk<B>::bytes;
-        }
-        v = load_weight_unit<B>(p, u);
-      }
-      regs[i] = v;
-    }
-  };
-  auto store_weights = [&](int buf, const v4i (&regs)[IPT]) {
-    _Pragma("unroll") for (int i = 0; i < IPT; ++i) {
-      const int item = i * kThreads + tid;
-      const int u = item & 3;
-      const int kbl = (item >> 2) % KS;
-      const int chn = (item >> 2) / KS;
-      const int cb = chn >> 5, ch = chn & 31;
-      const int h = u >> 1, j = u & 1;
-      const int off = buf * STAGE_BYTES + kbl * KBLK_BYTES + ((j * CB + cb) * 2 + h) * KSTEP_BYTES +
-                      ch * 16;
-      *(v4i *)(lds + off) = regs[i];
-    }
-  };
-
-  // ---- activation addressing for K-block kb
-  const int64_t in_img = (int64_t)a.in.h * a.in.w;
-  auto act_ptr = [&](int kb, int pb, bool &valid) -> const uint8_t * {
-    if (kb < geo.kb_main) {
-      const int tap = kb / geo.cpb;
-      const int cblk = kb - tap * geo.cpb;
-      const int ky = tap / a.kw, kx = tap - (tap / a.kw) * a.kw;
-      const int iy = iy0[pb] + ky, ix = ix0[pb] + kx;
-      valid = pvalid[pb] && iy >= 0 && iy < a.in.h && ix >= 0 && ix < a.in.w;
-      const int64_t pix = (int64_t)nimg[pb] * in_img + (int64_t)(valid ? iy : 0) * a.in.w + (valid ? ix : 0);
-      return a.in.data + pix * a.in.pixel + (int64_t)g * a.in.row + cblk * Blk<B>::bytes +
-             half * (Blk<B>::bytes / 2);
-    }
-    const int cblk = kb - geo.kb_main;
-    const int iy = (iy0[pb] + a.pad) * a.proj_stride / a.stride;
-    const int ix = (ix0[pb] + a.pad) * a.proj_stride / a.stride;
-    valid = pvalid[pb];
-    const int64_t pix = ((int64_t)nimg[pb] * a.proj.h + iy) * a.proj.w + ix;
-    return a.proj.data + pix * a.proj.pixel + (int64_t)gd * a.proj.row + cblk * Blk<B>::bytes +
-           half * (Blk<B>::bytes / 2);
-  };
-
-  v16i acc[CB][PB];
-  _Pragma("unroll") for (int cb = 0; cb < CB; ++cb)
-    _Pragma("unroll") for (int pb = 0; pb < PB; ++pb)
-      _Pragma("unroll") for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0;
-
-  const int nstages = (geo.kb_total + KS - 1) / KS;
-  v4i wreg[IPT];
-  stage_weights(0, wreg);
-  store_weights(0, wreg);
+__global__ void requant_prep_kernel(const int32_t *mult, const int32_t *shift, const int32_t *bias,
+                                    const int32_t *res_mult, int res_max, int nch, int scale,
+                                    int64_t acc_bound, RqConst *rq, int32_t *flag) {
+  __shared__ int any;
+  if (threadIdx.x == 0) any = 0;
   __syncthreads();
-
-  Raw<B> xcur[PB];
-  _Pragma("unroll") for (int pb = 0; pb < PB; ++pb) {
-    bool v;
-    const uint8_t *p = act_ptr(0, pb, v);
-    xcur[pb] = load_half<B>(p, v);
-  }
-
-  for (int s = 0; s < nstages; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < nstages) stage_weights((s + 1) * KS, wreg);
-    const int kb0 = s * KS;
-    const int kmax = min(KS, geo.kb_total - kb0);
-    for (int kbl = 0; kbl < kmax; ++kbl) {
-      const int kb = kb0 + kbl;
-      // prefetch the next K-block's activations
-      Raw<B> xnext[PB];
-      if (kb + 1 < geo.kb_total) {
-        _Pragma("unroll") for (int pb = 0; pb < PB; ++pb) {
-          bool v;
-          const uint8_t *p = act_ptr(kb + 1, pb, v);
-          xnext[pb] = load_half<B>(p, v);
-        }
-      }
-      _Pragma("unroll") for (int j = 0; j < 2; ++j) {
-        v4i bop[PB];
-        _Pragma("unroll") for (int pb = 0; pb < PB; ++pb) bop[pb] = act_operand<B>(xcur[pb], j);
-        _Pragma("unroll") for (int cb = 0; cb < CB; ++cb) {
-          const v4i aop = *(const v4i *)(lds + buf * STAGE_BYTES + kbl * KBLK_BYTES +
-                                         ((j * CB + cb) * 2 + half) * KSTEP_BYTES + l32 * 16);
-          _Pragma("unroll") for (int pb = 0; pb < PB; ++pb)
-            acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(aop, bop[pb], acc[cb][pb], 0, 0, 0);
-        }
-      }
-      if (kb + 1 < geo.kb_total)
-        _Pragma("unroll") for (int pb = 0; pb < PB; ++pb) xcur[pb] = xnext[pb];
+  int bad = 0;
+  for (int c = threadIdx.x; c < nch; c += blockDim.x) {
+    const int64_t m = mult[c];
+    const int sh = shift[c];
+    const int64_t b = bias ? bias[c] : 0;
+    const int64_t rm = res_mult ? res_mult[c] : 0;
+    RqConst k{0.0, 0.0};
+    if (m < 0 || sh < 1 || sh > 62) {
+      bad = 1;
+    } else {
+      const int64_t tmax = acc_bound + (b < 0 ? -b : b) + (rm < 0 ? -rm : rm) * res_max;
+      const int64_t lim = (int64_t)1 << 52;
+      if (m > 0 && tmax >= lim / m) bad = 1;
+      const int64_t num = b * m + ((int64_t)1 << (sh - 1));  // |b m| < 2^61
+      if (num >= lim || num <= -lim) bad = 1;
+      k.s = ldexp((double)m, -sh) / (double)scale;  // scale is a power of two: exact
+      k.o = ldexp((double)num, -sh);
     }
-    if (s + 1 < nstages) store_weights(buf ^ 1, wreg);
-    __syncthreads();
+    rq[c] = k;
   }
+  if (bad) atomicOr(&any, 1);
+  __syncthreads();
+  if (threadIdx.x == 0) *flag = any;
+}
 
-  // ---------------------------------------------------------------- epilogue
-  // Lane holds, for block (cb, pb), rows (channels) 8*(r/4) + 4*half + r%4 of
-  // pixel l32: four quads Q = 2*qi + half of four consecutive channels.
-  const int qmax = (1 << a.out.bits) - 1;
+// ---------------------------------------------------------------- geometry
+struct Geo {
+  int32_t M;          // output pixels per group
+  int32_t cpb;        // 64-code K-blocks per tap (grouped mode)
+  int32_t kb_main;    // K-blocks of the main convolution
+  int32_t kb_total;   // + projection K-blocks
+  int64_t w_ch;       // bytes of one output channel's filter
+  int64_t pw_ch;      // bytes of one projection filter channel
+  int32_t scale;      // operand scale of the accumulator (16 for 2-bit codes)
+  const uint8_t *wp;  // weights in MFMA operand order (see prepack_kernel)
+  const RqConst *rq;  // per-channel requant constants, then the int64-path flag
+};
+
+// A (kb, 32-channel block) slab of prepacked weights: [j][half][ch][16 B].
+constexpr int kSlab = 2048;
+constexpr int kLdsBudget = 160 * 1024;  // gfx950 LDS per CU
+constexpr int kNW = 8;                  // waves per workgroup
+
+// Sign-extended (and, for 2-bit activations, scaled) weight unit u (0..3) of
+// K-block kb for output channel k of group g: the 16 int8 values lane
+// (ch, half = u >> 1) feeds to K-step j = u & 1.
+template <int B, bool STEM>
+__device__ inline v4i weight_unit(const ConvArgs &a, const Geo &geo, int g, int gd, int k, int kb, int u) {
+  v4i v = {0, 0, 0, 0};
+  if constexpr (STEM) {
+    // unit u of K-block kb: filter row ky = 2 kb + (u >> 1), taps kx = 4 (u & 1) + d
+    const int ky = 2 * kb + (u >> 1);
+    if (ky < a.kh) {
+      const uint32_t *wr = (const uint32_t *)(a.w + (((int64_t)g * a.cout + k) * a.kh + ky) * a.kw * 4);
+      const uint32_t cmask = a.in.cpg >= 4 ? 0xffffffffu : ((1u << (8 * a.in.cpg)) - 1u);
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        const int kx = 4 * (u & 1) + d;
+        v[d] = kx < a.kw ? (int)(wr[kx] & cmask) : 0;
+      }
+    }
+  } else {
+    constexpr int BLK = Blk<B>::bytes;
+    if (kb < geo.kb_total) {
+      const uint8_t *p = kb < geo.kb_main
+                             ? a.w + ((int64_t)g * a.cout + k) * geo.w_ch + (int64_t)kb * BLK
+                             : a.proj_w + ((int64_t)gd * a.cout + k) * geo.pw_ch +
+                                   (int64_t)(kb - geo.kb_main) * BLK;
+      v = load_weight_unit<B>(p, u);
+    }
+  }
+  return v;
+}
+
+// Weights -> [G][cout/32][kb_total][j][half][ch][16 B] int8, one thread per
+// 16-byte operand chunk.  The projection K-blocks of source group g hold the
+// projection filter of its destination group (g + s) mod G.
+template <int B, bool STEM>
+__global__ void prepack_kernel(ConvArgs a, Geo geo, uint8_t *wp) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int nc32 = a.cout / 32;
+  const int64_t total = (int64_t)a.in.groups * nc32 * geo.kb_total * 128;
+  if (t >= total) return;
+  const int within = (int)(t & 127);
+  const int64_t rest = t >> 7;
+  const int kb = (int)(rest % geo.kb_total);
+  const int64_t r2 = rest / geo.kb_total;
+  const int cblk = (int)(r2 % nc32);
+  const int g = (int)(r2 / nc32);
+  const int j = within >> 6, half = (within >> 5) & 1, ch = within & 31;
+  const int gd = (g + a.shuffle) % a.in.groups;
+  *(v4i *)(wp + t * 16) = weight_unit<B, STEM>(a, geo, g, gd, cblk * 32 + ch, kb, 2 * half + j);
+}
+
+// Buffer resource over `bytes` bytes at `base`: loads at an offset >= bytes
+// return zero (hardware range check), which implements the zero padding of
+// out-of-image taps and of pixels past the end without branches.
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void *base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, (int)bytes, 0x00020000);
+}
+constexpr uint32_t kOob = 0x40000000u;  // offset past any tensor these kernels accept (< 2^30 B)
+
+template <int B>
+__device__ inline RawT<B, false> buf_half(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff) {
+  RawT<B, false> x;
+  if constexpr (B == 2) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, soff, 0);
+    const uint2 u = __builtin_bit_cast(uint2, v);
+    x.w[0] = u.x; x.w[1] = u.y;
+  } else if constexpr (B == 4) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, soff, 0);
+    const uint4 u = __builtin_bit_cast(uint4, v);
+    x.w[0] = u.x; x.w[1] = u.y; x.w[2] = u.z; x.w[3] = u.w;
+  } else {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b96(r, (int)voff, soff, 0);
+    x.w[0] = v[0]; x.w[1] = v[1]; x.w[2] = v[2];
+  }
+  return x;
+}
+
+// floor(m / d) for 0 <= m < 2^24, d >= 1, from a float estimate corrected
+// by one step each way (the estimate is off by at most one).
+__device__ inline int fdiv(int m, int d, float inv_d) {
+  int q = (int)((float)m * inv_d);
+  const int r = m - q * d;
+  q -= r < 0 ? 1 : 0;
+  q += r >= d ? 1 : 0;
+  return q;
+}
+
+// Workgroup prologue shared by both kernels: copy the channel block's
+// prepacked weights (all K-blocks) and its requant constants into LDS.
+template <int CB>
+__device__ inline void stage_block(const ConvArgs &a, const Geo &geo, int g, uint8_t *lds) {
+  const int KB = geo.kb_total;
+  const uint8_t *wsrc = geo.wp + (int64_t)(g * (a.cout / 32) + blockIdx.y * CB) * KB * kSlab;
+  const int chunks = KB * CB * 128;
+  for (int c = threadIdx.x; c < chunks; c += kNW * 64) {
+    const int kb = c / (CB * 128);
+    const int cb = (c >> 7) % CB;
+    *(uint4 *)(lds + c * 16) = *(const uint4 *)(wsrc + ((int64_t)cb * KB + kb) * kSlab + (c & 127) * 16);
+  }
+  RqConst *rq = (RqConst *)(lds + KB * CB * kSlab);
+  const int c0 = g * a.cout + blockIdx.y * CB * 32;
+  for (int c = threadIdx.x; c < CB * 32; c += kNW * 64) rq[c] = geo.rq[c0 + c];
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------- epilogue
+// Requant (+ shortcut) of one wave's CB x PB accumulator blocks and the
+// store through the cyclic permutation.  Block (cb, pb) covers channels
+// ch0 + 32 cb .. + 31 (rows of the MFMA output: lane holds rows
+// 8 (r / 4) + 4 half + r % 4) of pixels mbase + 32 pb + lane % 32.
+// RB: 2 = 2-bit identity shortcut prefetched into rw; -1 = identity shortcut
+// of other widths read here; 0 = none.
+template <int CB, int PB, int RB>
+__device__ inline void epilogue(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB], const uint32_t (&rw)[CB][PB][2],
+                                int64_t mbase, int g, int gd, int ch0, int l32, int half, const uint8_t *lds) {
   const int bo = a.out.bits;
-  const int64_t outC = (int64_t)G * a.cout;
-  _Pragma("unroll") for (int cb = 0; cb < CB; ++cb) {
-    const int kc = ch0 + cb * 32;   // first channel of this 32-channel chunk (in group)
+  const int qmax = (1 << bo) - 1;
+  const int64_t outC = (int64_t)a.in.groups * a.cout;
+  const int lsc = geo.scale == 16 ? 4 : 0;
+  const RqConst *rq = (const RqConst *)(lds + geo.kb_total * CB * kSlab);
+  const bool exact64 = ((const int32_t *)(geo.rq + (int64_t)a.in.groups * a.cout))[0] != 0;
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int kc = ch0 + cb * 32;
     const int csb = g * a.cout + kc;
     const int cdb = gd * a.cout + kc;
-    // quad values per pixel block
-    uint32_t qv[PB][4];
-    uint32_t hq[PB][4];  // bit-2 nibbles for 3-bit output
-    _Pragma("unroll") for (int qi = 0; qi < 4; ++qi) {
-      const int cq = 8 * qi + 4 * half;  // first channel of this quad within the chunk
-      const v4i mul = *(const v4i *)(a.mult + csb + cq);
-      const v4i shf = *(const v4i *)(a.shift + csb + cq);
-      v4i bia = {0, 0, 0, 0};
-      if (a.bias) bia = *(const v4i *)(a.bias + csb + cq);
+    uint32_t qv[PB][4], hq[PB][4];
+#pragma unroll
+    for (int qi = 0; qi < 4; ++qi) {
+      // keep the scheduler from hoisting every quad's constants to the top
+      // (that would hold 8 quads x 16 VGPRs of fp64 constants at once)
+      __builtin_amdgcn_sched_barrier(0);
+      const int cq = 8 * qi + 4 * half;
       v4i rmu = {0, 0, 0, 0};
-      if (a.res.data) rmu = *(const v4i *)(a.res_mult + csb + cq);
-      _Pragma("unroll") for (int pb = 0; pb < PB; ++pb) {
-        uint32_t rw[8];
-        if (a.res.data) {
-          const int rb = a.res.bits;
-          const int nw = rb == 3 ? 3 : rb;
-          const uint32_t *rp = (const uint32_t *)(a.res.data + (pvalid[pb] ? mpix[pb] : 0) * a.res.pixel +
-                                                  (int64_t)gd * a.res.row) +
-                               (int64_t)(kc >> 5) * nw;
-          _Pragma("unroll") for (int k = 0; k < 8; ++k) rw[k] = k < nw ? rp[k] : 0u;
+      if constexpr (RB != 0) rmu = *(const v4i *)(a.res_mult + csb + cq);
+      RqConst k[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) k[e] = rq[cb * 32 + cq + e];
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        const int64_t mp = mbase + pb * 32 + l32;
+        int32_t v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[cb][pb][4 * qi + e];
+        if constexpr (RB == 2) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += (rmu[e] * chunk_code(rw[cb][pb], cq + e, 2)) << lsc;
+        } else if constexpr (RB < 0) {
+          int rc[4];
+          row_quad(a.res.data + (mp < geo.M ? mp : 0) * a.res.pixel + (int64_t)gd * a.res.row, kc + cq,
+                   a.res.bits, rc);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += (rmu[e] * rc[e]) << lsc;
         }
         uint32_t qword = 0, hword = 0;
-        int32_t accq[4];
-        _Pragma("unroll") for (int e = 0; e < 4; ++e) {
-          int32_t av = acc[cb][pb][4 * qi + e];
-          if (B == 2) av >>= 4;  // remove the x16 operand scale (exact)
-          accq[e] = av;
-          int64_t t = (int64_t)av + bia[e];
-          if (a.res.data) t += (int64_t)rmu[e] * chunk_code(rw, cq + e, a.res.bits);
-          const uint32_t q = (uint32_t)requant_one(t, mul[e], shf[e], qmax);
-          if (bo == 3) {
-            qword |= (q & 3u) << (2 * e);
-            hword |= ((q >> 2) & 1u) << e;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          int q;
+          if (!exact64) {
+            q = (int)__builtin_fma((double)v[e], k[e].s, k[e].o);
+            q = min(max(q, 0), qmax);
           } else {
-            qword |= q << (bo * e);
+            const int cs = csb + cq + e;
+            q = requant_mul((int64_t)(v[e] >> lsc) + (a.bias ? a.bias[cs] : 0), a.mult[cs], a.shift[cs], qmax);
+          }
+          if (bo == 3) {
+            qword |= (uint32_t)(q & 3) << (2 * e);
+            hword |= (uint32_t)((q >> 2) & 1) << e;
+          } else {
+            qword |= (uint32_t)q << (bo * e);
           }
         }
         qv[pb][qi] = qword;
         hq[pb][qi] = hword;
-        if (a.acc_dump && pvalid[pb]) {
-          v4i dv = {accq[0], accq[1], accq[2], accq[3]};
-          *(v4i *)(a.acc_dump + mpix[pb] * outC + cdb + cq) = dv;
+        if (a.acc_dump && mp < geo.M) {
+          const v4i dv = {acc[cb][pb][4 * qi] >> lsc, acc[cb][pb][4 * qi + 1] >> lsc,
+                          acc[cb][pb][4 * qi + 2] >> lsc, acc[cb][pb][4 * qi + 3] >> lsc};
+          *(v4i *)(a.acc_dump + mp * outC + cdb + cq) = dv;
         }
       }
     }
     // exchange quads with the partner lane (half ^ 1) and store
-    _Pragma("unroll") for (int pb = 0; pb < PB; ++pb) {
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const int64_t mp = mbase + pb * 32 + l32;
       const uint32_t s0 = half ? qv[pb][0] : qv[pb][2];
       const uint32_t s1 = half ? qv[pb][1] : qv[pb][3];
       const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
       const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
-      // the four quads this lane writes, in channel order
       uint32_t Q[4];
       if (half == 0) { Q[0] = qv[pb][0]; Q[1] = r0; Q[2] = qv[pb][1]; Q[3] = r1; }
       else           { Q[0] = r0; Q[1] = qv[pb][2]; Q[2] = r1; Q[3] = qv[pb][3]; }
       uint32_t hpart = 0;
       if (bo == 3) {
-        _Pragma("unroll") for (int qi = 0; qi < 4; ++qi) {
+#pragma unroll
+        for (int qi = 0; qi < 4; ++qi) {
           const int Qn = 2 * qi + half;
           hpart |= hq[pb][qi] << (8 * (Qn & 3) + 4 * (Qn >> 2));
         }
         hpart |= (uint32_t)__shfl_xor((int)hpart, 32);
       }
-      if (!pvalid[pb]) continue;
-      uint8_t *orow = a.out.data + mpix[pb] * a.out.pixel + (int64_t)gd * a.out.row;
+      if (mp >= geo.M) continue;
+      uint8_t *orow = a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row;
       if (bo == 3) {
         uint32_t *cw = (uint32_t *)orow + (int64_t)(kc >> 5) * 3;
-        const uint32_t lo = Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24);
-        cw[half] = lo;
+        cw[half] = Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24);
         if (half == 0) cw[2] = hpart;
       } else {
-        // 16*bo bits per lane: bo/2 words
         uint32_t *cw = (uint32_t *)orow + (int64_t)(kc >> 5) * bo + half * (bo / 2);
         if (bo == 2) {
           cw[0] = Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24);
         } else if (bo == 4) {
-          cw[0] = Q[0] | (Q[1] << 16);
-          cw[1] = Q[2] | (Q[3] << 16);
+          *(uint2 *)cw = make_uint2(Q[0] | (Q[1] << 16), Q[2] | (Q[3] << 16));
         } else {
-          cw[0] = Q[0]; cw[1] = Q[1]; cw[2] = Q[2]; cw[3] = Q[3];
+          *(uint4 *)cw = make_uint4(Q[0], Q[1], Q[2], Q[3]);
         }
       }
     }
   }
 }
 
-template <int B, int CB, int PB, int KS>
-hipError_t launch_cfg(const ConvArgs &a, const Geo &geo, hipStream_t s) {
-  constexpr int TPIX = kWaves * PB * 32;
-  dim3 grid((unsigned)((geo.M + TPIX - 1) / TPIX), (unsigned)(a.cout / (CB * 32)),
-            (unsigned)a.in.groups);
-  hipLaunchKernelGGL((conv_mfma_kernel<B, CB, PB, KS>), grid, dim3(kThreads), 0, s, a, geo);
+// Common-case epilogue: fp64 requant valid for the layer, no accumulator
+// dump, 2-, 4- or 8-bit output.  Same arithmetic as `epilogue`, without
+// per-element branches; each quad's constants are fetched from LDS one quad
+// ahead.
+template <int CB, int PB, int RB>
+__device__ inline void epilogue_fast(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB],
+                                     const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
+                                     int l32, int half, const uint8_t *lds) {
+  const int bo = a.out.bits;
+  const int qmax = (1 << bo) - 1;
+  const int lsc = geo.scale == 16 ? 4 : 0;
+  const RqConst *rq = (const RqConst *)(lds + geo.kb_total * CB * kSlab);
+  RqConst kn[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) kn[e] = rq[4 * half + e];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int kc = ch0 + cb * 32;
+    const int csb = g * a.cout + kc;
+    uint32_t qv[PB][4];
+#pragma unroll
+    for (int qi = 0; qi < 4; ++qi) {
+      const int cq = 8 * qi + 4 * half;
+      RqConst k[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) k[e] = kn[e];
+      // next quad's constants (the last one of a block wraps harmlessly)
+      const int nxt = (qi < 3 ? cb * 32 + cq + 8 : (cb + 1 < CB ? (cb + 1) * 32 + 4 * half : 0));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) kn[e] = rq[nxt + e];
+      v4i rmu = {0, 0, 0, 0};
+      if constexpr (RB != 0) rmu = *(const v4i *)(a.res_mult + csb + cq);
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        int32_t v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = acc[cb][pb][4 * qi + e];
+        if constexpr (RB == 2) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += (rmu[e] * chunk_code(rw[cb][pb], cq + e, 2)) << lsc;
+        } else if constexpr (RB < 0) {
+          const int64_t mp = mbase + pb * 32 + l32;
+          int rc[4];
+          row_quad(a.res.data + (mp < geo.M ? mp : 0) * a.res.pixel + (int64_t)gd * a.res.row, kc + cq,
+                   a.res.bits, rc);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += (rmu[e] * rc[e]) << lsc;
+        }
+        uint32_t qword = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          int q = (int)__builtin_fma((double)v[e], k[e].s, k[e].o);
+          q = min(max(q, 0), qmax);
+          qword |= (uint32_t)q << (bo * e);
+        }
+        qv[pb][qi] = qword;
+      }
+    }
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const int64_t mp = mbase + pb * 32 + l32;
+      const uint32_t s0 = half ? qv[pb][0] : qv[pb][2];
+      const uint32_t s1 = half ? qv[pb][1] : qv[pb][3];
+      const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
+      const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
+      uint32_t Q[4];
+      if (half == 0) { Q[0] = qv[pb][0]; Q[1] = r0; Q[2] = qv[pb][1]; Q[3] = r1; }
+      else           { Q[0] = r0; Q[1] = qv[pb][2]; Q[2] = r1; Q[3] = qv[pb][3]; }
+      if (mp >= geo.M) continue;
+      uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row) +
+                     (int64_t)(kc >> 5) * bo + half * (bo / 2);
+      if (bo == 2) {
+        cw[0] = Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24);
+      } else if (bo == 4) {
+        *(uint2 *)cw = make_uint2(Q[0] | (Q[1] << 16), Q[2] | (Q[3] << 16));
+      } else {
+        *(uint4 *)cw = make_uint4(Q[0], Q[1], Q[2], Q[3]);
+      }
+    }
+  }
+}
+
+// Picks the epilogue once per tile (all conditions are uniform).
+template <int CB, int PB, int RB>
+__device__ inline void finish_tile(const ConvArgs &a, const Geo &geo, bool fast, v16i (&acc)[CB][PB],
+                                   const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
+                                   int l32, int half, const uint8_t *lds) {
+  if (fast) epilogue_fast<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, lds);
+  else epilogue<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, lds);
+}
+
+// Loads of the K loop, the LDS operand reads and the MFMAs of one K-block
+// are the same for both kernels; the loader differs.  Three activation
+// slots rotate: K-block kb uses one slot and refills another with K-block
+// kb + 2, which may already belong to the wave's next tile.  PALQ_KLOOP walks
+// one tile starting with the slots in (A, B, C) order (A holds K-block 0, B
+// K-block 1); the three call orders keep every slot in fixed registers.  The
+// weight operands of a K-block are read from LDS at its start; the
+// activation unpack covers most of that latency.
+#define PALQ_KLOOP_BODY(KBI, XU, XF)                                                             \
+  {                                                                                               \
+    v4i wu[2][CB];                                                                                \
+    read_w(KBI, wu);                                                                              \
+    load_next(XF);                                                                                \
+    _Pragma("unroll") for (int j = 0; j < 2; ++j) {                                               \
+      v4i bop[PB];                                                                                \
+      _Pragma("unroll") for (int pb = 0; pb < PB; ++pb) bop[pb] = operand(XU[pb], j);             \
+      _Pragma("unroll") for (int cb = 0; cb < CB; ++cb)                                           \
+          _Pragma("unroll") for (int pb = 0; pb < PB; ++pb) acc[cb][pb] =                         \
+              __builtin_amdgcn_mfma_i32_32x32x32_i8(wu[j][cb], bop[pb], acc[cb][pb], 0, 0, 0);    \
+    }                                                                                             \
+  }
+
+#define PALQ_KLOOP(XA, XB, XC)                                  \
+  {                                                             \
+    int kb = 0;                                                 \
+    for (; kb + 3 <= KB; kb += 3) {                             \
+      PALQ_KLOOP_BODY(kb, XA, XC)                               \
+      PALQ_KLOOP_BODY(kb + 1, XB, XA)                           \
+      PALQ_KLOOP_BODY(kb + 2, XC, XB)                           \
+    }                                                           \
+    if (kb < KB) PALQ_KLOOP_BODY(kb, XA, XC)                    \
+    if (kb + 1 < KB) PALQ_KLOOP_BODY(kb + 1, XB, XA)            \
+  }
+
+// ---------------------------------------------------------------- grouped kernel
+// Grouped B-bit conv.  Persistent workgroups of kNW waves keep the whole K
+// extent of CB x 32 output channels of one group resident in LDS (one
+// barrier, at the start); each wave then walks its own tiles of PB x 32 output
+// pixels.  Per K-block a lane issues one buffer load per pixel block (its
+// pixel's 32 codes of the current tap and 64-code block), two K-blocks ahead
+// of use and across tile boundaries; the weight operands are read from LDS
+// two K-blocks ahead too.
+template <int B, int CB, int PB, int RB>
+__global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo geo, int tiles) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  constexpr int BLK = Blk<B>::bytes;
+  using Raw = RawT<B, false>;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int l32 = lane & 31;
+  const int half = lane >> 5;
+  const int G = a.in.groups;
+  const int g = blockIdx.z;
+  const int gd = (g + a.shuffle) % G;
+  const int ch0 = blockIdx.y * CB * 32;
+  const int KB = geo.kb_total;
+
+  stage_block<CB>(a, geo, g, lds);
+  const bool fast = !((const int32_t *)(geo.rq + (int64_t)a.in.groups * a.cout))[0] && !a.acc_dump &&
+                    a.out.bits != 3;
+  const int first = blockIdx.x * kNW + wave;
+  const int tstride = gridDim.x * kNW;
+  if (first >= tiles) return;  // no barrier follows
+
+  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
+  // without a projection this resource has no bytes: every load returns 0
+  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, (int64_t)a.proj.n * a.proj.h * a.proj.w * a.proj.pixel)
+                               : make_rsrc(a.in.data, 0);
+  const int pixb = (int)a.in.pixel;
+  const int rowb = a.in.w * pixb;
+  const int HW = a.ho * a.wo;
+  const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
+
+  // ---- loader: tile lt, K-block cursor; geometry of tile lt per pixel block
+  int lt = first, l_kb = 0, l_tap = 0, l_cblk = 0, l_ky = 0, l_kx = 0, l_tapoff = 0;
+  int off0[PB];
+  uint32_t tmask[PB], poff[PB];
+  auto geometry = [&](int t) {
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const int m = t * PB * 32 + pb * 32 + l32;
+      const bool valid = t < tiles && m < geo.M;
+      const int mm = valid ? m : 0;
+      const int n = fdiv(mm, HW, inv_hw);
+      const int rem = mm - n * HW;
+      const int oy = fdiv(rem, a.wo, inv_wo);
+      const int ox = rem - oy * a.wo;
+      const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
+      off0[pb] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.row + half * (BLK / 2);
+      const int xlo = max(0, -ix0), xhi = min(a.kw, a.in.w - ix0);
+      const uint32_t below = xhi >= 32 ? 0xffffffffu : ((1u << max(xhi, 0)) - 1u);
+      const uint32_t cols = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
+      const int ylo = max(0, -iy0), yhi = min(a.kh, a.in.h - iy0);
+      uint32_t mk = 0;
+      for (int ky = ylo; ky < yhi; ++ky) mk |= cols << (ky * a.kw);
+      tmask[pb] = valid ? mk : 0u;
+      poff[pb] = (a.proj.data && valid)
+                     ? (uint32_t)(((n * a.proj.h + oy * a.proj_stride) * a.proj.w + ox * a.proj_stride) *
+                                      (int)a.proj.pixel +
+                                  gd * (int)a.proj.row + half * (BLK / 2))
+                     : kOob;
+    }
+  };
+  geometry(lt);
+  // Every call issues exactly PB loads (K-blocks with no data read the
+  // zero-returning offset), so the wait counts are static.
+  auto load_next = [&](Raw (&x)[PB]) {
+    if (l_kb < geo.kb_main) {
+      // the per-lane offset carries the tap so that it is >= 0 whenever the
+      // tap is in the image (off0 alone is negative on the top/left border);
+      // only the non-negative block offset goes to soffset
+      const int soff = l_cblk * BLK;
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        const uint32_t vo = ((tmask[pb] >> l_tap) & 1u) ? (uint32_t)(off0[pb] + l_tapoff) : kOob;
+        x[pb] = buf_half<B>(rin, vo, soff);
+      }
+      if (++l_cblk == geo.cpb) {
+        l_cblk = 0;
+        ++l_tap;
+        if (++l_kx == a.kw) { l_kx = 0; ++l_ky; }
+        l_tapoff = l_ky * rowb + l_kx * pixb;
+      }
+    } else {
+      const int soff = (l_kb - geo.kb_main) * BLK;
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) x[pb] = buf_half<B>(rpj, poff[pb], soff);
+    }
+    if (++l_kb == KB) {  // move on to the wave's next tile
+      l_kb = l_tap = l_cblk = l_ky = l_kx = l_tapoff = 0;
+      lt += tstride;
+      geometry(lt);
+    }
+  };
+  auto read_w = [&](int kb, v4i (&aop)[2][CB]) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+        aop[j][cb] = *(const v4i *)(lds + (kb * CB + cb) * kSlab + ((j * 2 + half) * 32 + l32) * 16);
+  };
+  auto operand = [&](const Raw &r, int j) -> v4i { return act_operand<B>(r, j); };
+
+  Raw xs0[PB], xs1[PB], xs2[PB];
+  load_next(xs0);
+  load_next(xs1);
+  int phase = 0;
+  const auto rres = make_rsrc(a.res.data, a.res.data ? (int64_t)a.res.n * a.res.h * a.res.w * a.res.pixel : 0);
+  for (int ct = first; ct < tiles; ct += tstride) {
+    // shortcut codes of this tile (2-bit): fetched now, used by the epilogue
+    uint32_t rw[CB][PB][2];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        rw[cb][pb][0] = rw[cb][pb][1] = 0;
+        if constexpr (RB == 2) {
+          const int m = ct * PB * 32 + pb * 32 + l32;
+          const uint32_t ro = m < geo.M ? (uint32_t)(m * (int)a.res.pixel + gd * (int)a.res.row + ((ch0 + cb * 32) >> 5) * 8)
+                                        : kOob;
+          const auto v = __builtin_amdgcn_raw_buffer_load_b64(rres, (int)ro, 0, 0);
+          const uint2 u = __builtin_bit_cast(uint2, v);
+          rw[cb][pb][0] = u.x;
+          rw[cb][pb][1] = u.y;
+        }
+      }
+    v16i acc[CB][PB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0;
+    if (phase == 0) PALQ_KLOOP(xs0, xs1, xs2)
+    else if (phase == 1) PALQ_KLOOP(xs1, xs2, xs0)
+    else PALQ_KLOOP(xs2, xs0, xs1)
+    phase = (phase + KB) % 3;
+    finish_tile<CB, PB, RB>(a, geo, fast, acc, rw, (int64_t)ct * PB * 32, g, gd, ch0, l32, half, lds);
+  }
+}
+
+// ---------------------------------------------------------------- stem kernel
+// First layer: 8-bit signed input with at most 4 channels per pixel (one
+// 4-byte row), 8-bit weights, any kh and kw <= 8.  One 16-code operand unit
+// is four consecutive kx taps of one filter row (pixel-major, 4 bytes each;
+// the filter's padding byte is masked to 0 in the prepacked weights), a
+// K-block is two filter rows.  Same persistent structure as the grouped
+// kernel.
+template <int CB, int PB, int RB>
+__global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo, int tiles) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  using Raw = RawT<8, true>;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int l32 = lane & 31;
+  const int half = lane >> 5;
+  const int G = a.in.groups;
+  const int g = blockIdx.z;
+  const int gd = (g + a.shuffle) % G;
+  const int ch0 = blockIdx.y * CB * 32;
+  const int KB = geo.kb_total;
+
+  stage_block<CB>(a, geo, g, lds);
+  const bool fast = !((const int32_t *)(geo.rq + (int64_t)a.in.groups * a.cout))[0] && !a.acc_dump &&
+                    a.out.bits != 3;
+  const int first = blockIdx.x * kNW + wave;
+  const int tstride = gridDim.x * kNW;
+  if (first >= tiles) return;
+
+  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
+  const int pixb = (int)a.in.pixel;
+  const int rowb = a.in.w * pixb;
+  const int HW = a.ho * a.wo;
+  const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
+
+  int lt = first, l_kb = 0;
+  int off0[PB], iy0[PB];
+  uint32_t xmask[PB];
+  auto geometry = [&](int t) {
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const int m = t * PB * 32 + pb * 32 + l32;
+      const bool valid = t < tiles && m < geo.M;
+      const int mm = valid ? m : 0;
+      const int n = fdiv(mm, HW, inv_hw);
+      const int rem = mm - n * HW;
+      const int oy = fdiv(rem, a.wo, inv_wo);
+      const int ox = rem - oy * a.wo;
+      iy0[pb] = valid ? oy * a.stride - a.pad : -(1 << 20);  // invalid pixel: every row out of range
+      const int ix0 = ox * a.stride - a.pad;
+      off0[pb] = ((n * a.in.h + oy * a.stride - a.pad) * a.in.w + ix0) * pixb + g * (int)a.in.row;
+      const int xlo = max(0, -ix0), xhi = min(min(8, a.kw), a.in.w - ix0);
+      const uint32_t below = (1u << max(xhi, 0)) - 1u;
+      xmask[pb] = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
+    }
+  };
+  geometry(lt);
+  auto load_next = [&](Raw (&x)[PB]) {
+    const int ky = 2 * l_kb + half;  // this lane's filter row
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const bool rowok = ky < a.kh && iy0[pb] + ky >= 0 && iy0[pb] + ky < a.in.h;
+      const int rbase = off0[pb] + ky * rowb;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const uint32_t vo = (rowok && ((xmask[pb] >> i) & 1u)) ? (uint32_t)(rbase + i * pixb) : kOob;
+        x[pb].w[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rin, (int)vo, 0, 0);
+      }
+    }
+    if (++l_kb == KB) {
+      l_kb = 0;
+      lt += tstride;
+      geometry(lt);
+    }
+  };
+  auto read_w = [&](int kb, v4i (&aop)[2][CB]) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+        aop[j][cb] = *(const v4i *)(lds + (kb * CB + cb) * kSlab + ((j * 2 + half) * 32 + l32) * 16);
+  };
+  auto operand = [&](const Raw &r, int j) -> v4i {
+    v4i o = {(int)r.w[4 * j], (int)r.w[4 * j + 1], (int)r.w[4 * j + 2], (int)r.w[4 * j + 3]};
+    return o;
+  };
+
+  Raw xs0[PB], xs1[PB], xs2[PB];
+  load_next(xs0);
+  load_next(xs1);
+  int phase = 0;
+  uint32_t rw[CB][PB][2] = {};
+  for (int ct = first; ct < tiles; ct += tstride) {
+    v16i acc[CB][PB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0;
+    if (phase == 0) PALQ_KLOOP(xs0, xs1, xs2)
+    else if (phase == 1) PALQ_KLOOP(xs1, xs2, xs0)
+    else PALQ_KLOOP(xs2, xs0, xs1)
+    phase = (phase + KB) % 3;
+    finish_tile<CB, PB, RB>(a, geo, fast, acc, rw, (int64_t)ct * PB * 32, g, gd, ch0, l32, half, lds);
+  }
+}
+
+// ---------------------------------------------------------------- launch
+bool is_stem(const ConvArgs &a) {
+  return a.in.bits == 8 && a.in.is_signed && a.w_bits == 8 && a.in.row == 4 && a.kw <= 8 &&
+         !a.proj.data;
+}
+
+Geo make_geo(const ConvArgs &a) {
+  Geo geo{};
+  geo.M = a.out.n * a.ho * a.wo;
+  if (is_stem(a)) {
+    geo.kb_main = (a.kh + 1) / 2;  // two filter rows per K-block
+    geo.kb_total = geo.kb_main;
+    geo.scale = 1;
+  } else {
+    geo.cpb = a.in.cpg / 64;
+    geo.kb_main = a.kh * a.kw * geo.cpb;
+    geo.kb_total = geo.kb_main + (a.proj.data ? a.proj.cpg / 64 : 0);
+    geo.w_ch = (int64_t)a.kh * a.kw * row_bytes(a.in.cpg, a.w_bits);
+    geo.pw_ch = a.proj.data ? row_bytes(a.proj.cpg, a.w_bits) : 0;
+    geo.scale = a.in.bits == 2 ? 16 : 1;
+  }
+  return geo;
+}
+
+size_t lds_bytes(const Geo &geo, int cb) { return (size_t)geo.kb_total * cb * kSlab + (size_t)cb * 32 * sizeof(RqConst); }
+
+// Largest channel block (32 or 64 channels) whose filter fits LDS, 0 if none.
+int pick_cb(const ConvArgs &a, const Geo &geo) {
+  if (a.cout % 64 == 0 && lds_bytes(geo, 2) <= kLdsBudget / 2) return 2;
+  if (lds_bytes(geo, 1) <= kLdsBudget) return 1;
+  return 0;
+}
+
+// Optional tile override for tuning sweeps: PALQ_CONV_TILE="cb,pb".
+void tile_override(const ConvArgs &a, const Geo &geo, int &cb, int &pb) {
+  static int ocb = -1, opb = -1;
+  if (ocb < 0) {
+    ocb = opb = 0;
+    if (const char *e = getenv("PALQ_CONV_TILE")) {
+      int x = 0, y = 0;
+      if (sscanf(e, "%d,%d", &x, &y) == 2) { ocb = x; opb = y; }
+    }
+  }
+  if (ocb == 1 || (ocb == 2 && a.cout % 64 == 0 && lds_bytes(geo, 2) <= kLdsBudget)) cb = ocb;
+  if (opb == 1 || opb == 2) pb = opb;
+}
+
+template <typename K>
+hipError_t launch_persistent(K kern, const ConvArgs &a, const Geo &geo, int cb, int pb, hipStream_t s) {
+  const size_t lds = lds_bytes(geo, cb);
+  hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBudget);
+  if (e != hipSuccess) return e;
+  const int tiles = (int)((geo.M + pb * 32 - 1) / (pb * 32));
+  const int combos = (a.cout / (cb * 32)) * a.in.groups;
+  const int per_cu = (int)std::min<size_t>(2, kLdsBudget / std::max<size_t>(lds, 1));
+  int gx = std::max(1, (256 * per_cu + combos - 1) / combos);
+  gx = std::min(gx, (tiles + kNW - 1) / kNW);
+  dim3 grid((unsigned)gx, (unsigned)(a.cout / (cb * 32)), (unsigned)a.in.groups);
+  hipLaunchKernelGGL(kern, grid, dim3(kNW * 64), lds, s, a, geo, tiles);
   return hipGetLastError();
 }
 
+template <int B, int CB, int PB>
+hipError_t launch_grouped(const ConvArgs &a, const Geo &geo, hipStream_t s) {
+  if (!a.res.data) return launch_persistent(conv_grouped_kernel<B, CB, PB, 0>, a, geo, CB, PB, s);
+  if (a.res.bits == 2) return launch_persistent(conv_grouped_kernel<B, CB, PB, 2>, a, geo, CB, PB, s);
+  return launch_persistent(conv_grouped_kernel<B, CB, PB, -1>, a, geo, CB, PB, s);
+}
+
+template <int CB, int PB>
+hipError_t launch_stem(const ConvArgs &a, const Geo &geo, hipStream_t s) {
+  if (!a.res.data) return launch_persistent(conv_stem_kernel<CB, PB, 0>, a, geo, CB, PB, s);
+  return launch_persistent(conv_stem_kernel<CB, PB, -1>, a, geo, CB, PB, s);
+}
+
 template <int B>
-hipError_t launch_bits(const ConvArgs &a, const Geo &geo, hipStream_t s) {
-  const int cb = (a.cout % 64 == 0) ? 2 : 1;
-  // smallest pixel tile that still gives about two workgroups per CU
-  const int64_t ch_tiles = (int64_t)(a.cout / (cb * 32)) * a.in.groups;
-  const int64_t want = 512;
-  int pb = 4;
-  while (pb > 1 && ((geo.M + kWaves * pb * 32 - 1) / (kWaves * pb * 32)) * ch_tiles < want) pb >>= 1;
-  if (cb == 2) {
-    if (pb == 4) return launch_cfg<B, 2, 4, 4>(a, geo, s);
-    if (pb == 2) return launch_cfg<B, 2, 2, 4>(a, geo, s);
-    return launch_cfg<B, 2, 1, 4>(a, geo, s);
-  }
-  if (pb == 4) return launch_cfg<B, 1, 4, 8>(a, geo, s);
-  if (pb == 2) return launch_cfg<B, 1, 2, 8>(a, geo, s);
-  return launch_cfg<B, 1, 1, 8>(a, geo, s);
+hipError_t dispatch_bits(const ConvArgs &a, const Geo &geo, int cb, int pb, hipStream_t s) {
+  if (cb == 2) return pb == 2 ? launch_grouped<B, 2, 2>(a, geo, s) : launch_grouped<B, 2, 1>(a, geo, s);
+  return pb == 2 ? launch_grouped<B, 1, 2>(a, geo, s) : launch_grouped<B, 1, 1>(a, geo, s);
+}
+
+// Largest magnitude of a code of the given width and sign.
+int64_t code_max(int bits, int is_signed) {
+  return is_signed ? ((int64_t)1 << (bits - 1)) : (((int64_t)1 << bits) - 1);
 }
 
 }  // namespace
 
 bool conv_mfma_supported(const ConvArgs &a) {
-  const int b = a.in.bits;
-  if (a.in.is_signed || (b != 2 && b != 3 && b != 4) || a.w_bits != b) return false;
-  if (a.in.cpg % 64 != 0 || a.cout % 32 != 0) return false;
-  if (a.proj.data && (a.proj.bits != b || a.proj.cpg % 64 != 0 || a.proj.is_signed)) return false;
-  return true;
+  if (a.cout % 32 != 0) return false;
+  const int64_t lim = (int64_t)1 << 30;
+  auto bytes = [](const ActView &v) { return v.data ? (int64_t)v.n * v.h * v.w * v.pixel : 0; };
+  if (bytes(a.in) >= lim || bytes(a.out) >= lim || bytes(a.res) >= lim || bytes(a.proj) >= lim) return false;
+  if ((int64_t)a.out.n * a.ho * a.wo >= (1 << 24)) return false;
+  if (!is_stem(a)) {
+    const int b = a.in.bits;
+    if (a.in.is_signed || (b != 2 && b != 3 && b != 4) || a.w_bits != b) return false;
+    if (a.in.cpg % 64 != 0 || a.kh * a.kw > 32) return false;
+    if (a.proj.data && (a.proj.bits != b || a.proj.cpg % 64 != 0 || a.proj.is_signed)) return false;
+  }
+  return pick_cb(a, make_geo(a)) > 0;
 }
 
-hipError_t launch_conv_mfma(const ConvArgs &a, hipStream_t s) {
-  Geo geo;
-  geo.M = a.out.n * a.ho * a.wo;
-  geo.taps = a.kh * a.kw;
-  geo.cpb = a.in.cpg / 64;
-  geo.kb_main = geo.taps * geo.cpb;
-  geo.pcpb = a.proj.data ? a.proj.cpg / 64 : 0;
-  geo.kb_total = geo.kb_main + geo.pcpb;
-  geo.w_ch = (int64_t)geo.taps * row_bytes(a.in.cpg, a.w_bits);
-  geo.pw_ch = a.proj.data ? row_bytes(a.proj.cpg, a.w_bits) : 0;
+ConvPlan conv_mfma_plan(const ConvArgs &a) {
+  ConvPlan p{};
+  const Geo geo = make_geo(a);
+  p.w_bytes = (size_t)a.in.groups * a.cout * geo.kb_total * 64;
+  p.thr_bytes = (size_t)a.in.groups * a.cout * sizeof(RqConst) + 16;  // + int64-path flag
+  return p;
+}
+
+hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hipStream_t s) {
+  const Geo geo = make_geo(a);
+  const int64_t chunks = (int64_t)a.in.groups * (a.cout / 32) * geo.kb_total * 128;
+  const unsigned grid = (unsigned)((chunks + 255) / 256);
+  if (is_stem(a)) {
+    hipLaunchKernelGGL((prepack_kernel<8, true>), dim3(grid), dim3(256), 0, s, a, geo, wp);
+  } else {
+    switch (a.in.bits) {
+      case 2: hipLaunchKernelGGL((prepack_kernel<2, false>), dim3(grid), dim3(256), 0, s, a, geo, wp); break;
+      case 3: hipLaunchKernelGGL((prepack_kernel<3, false>), dim3(grid), dim3(256), 0, s, a, geo, wp); break;
+      case 4: hipLaunchKernelGGL((prepack_kernel<4, false>), dim3(grid), dim3(256), 0, s, a, geo, wp); break;
+      default: return hipErrorNotSupported;
+    }
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // accumulator bound: every product of the main and projection contractions
+  int64_t acc_bound = (int64_t)a.kh * a.kw * a.in.cpg * code_max(a.in.bits, a.in.is_signed) * code_max(a.w_bits, 1);
+  if (a.proj.data) acc_bound += (int64_t)a.proj.cpg * code_max(a.proj.bits, 0) * code_max(a.w_bits, 1);
+  const int res_max = a.res.data ? (int)code_max(a.res.bits, 0) : 0;
+  const int nch = a.in.groups * a.cout;
+  RqConst *rq = (RqConst *)thr;
+  hipLaunchKernelGGL(requant_prep_kernel, dim3(1), dim3(256), 0, s, a.mult, a.shift, a.bias, a.res.data ? a.res_mult : nullptr,
+                     res_max, nch, geo.scale, acc_bound, rq, (int32_t *)(rq + nch));
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, hipStream_t s) {
+  Geo geo = make_geo(a);
   if (geo.M == 0) return hipSuccess;
+  geo.wp = wp;
+  geo.rq = (const RqConst *)thr;
+  int cb = pick_cb(a, geo);
+  if (cb == 0) return hipErrorNotSupported;
+  int pb = 1;
+  tile_override(a, geo, cb, pb);
+  if (is_stem(a)) {
+    if (cb == 2) return pb == 2 ? launch_stem<2, 2>(a, geo, s) : launch_stem<2, 1>(a, geo, s);
+    return pb == 2 ? launch_stem<1, 2>(a, geo, s) : launch_stem<1, 1>(a, geo, s);
+  }
   switch (a.in.bits) {
-    case 2: return launch_bits<2>(a, geo, s);
-    case 3: return launch_bits<3>(a, geo, s);
-    case 4: return launch_bits<4>(a, geo, s);
+    case 2: return dispatch_bits<2>(a, geo, cb, pb, s);
+    case 3: return dispatch_bits<3>(a, geo, cb, pb, s);
+    case 4: return dispatch_bits<4>(a, geo, cb, pb, s);
   }
   return hipErrorNotSupported;
 }

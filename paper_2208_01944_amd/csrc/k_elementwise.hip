@@ -94,11 +94,20 @@ __global__ void range_out_kernel(const uint32_t *enc, float *range_out) {
   range_out[1] = empty ? __uint_as_float(0x7fc00000u) : ord2f(enc[1]);
 }
 
-// Eq. 2 in the documented fp32 op order.
+// Eq. 2 in the documented fp32 op order, for one code.
+__device__ inline int quant_one(float x, float l, float rng, float qmax) {
+  const float d = x - l;
+  float t = d / rng;  // correctly rounded (built with correctly rounded division)
+  t = t > 1.0f ? 1.0f : t;
+  t = t >= 0.0f ? t : 0.0f;
+  return (int)rintf(t * qmax);
+}
+
+// One thread per packed word (b in {2, 4, 8}) or 32-code chunk (b = 3).
 __global__ void quantize_kernel(const float *x, float l, float u, const uint32_t *enc, ActView out,
-                                int64_t rows, int chunks) {
+                                int64_t rows, int units) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= rows * chunks) return;
+  if (t >= rows * units) return;
   bool degenerate = false;
   if (enc) {
     const bool empty = enc[0] == 0xffffffffu && enc[1] == 0u;
@@ -106,32 +115,36 @@ __global__ void quantize_kernel(const float *x, float l, float u, const uint32_t
     u = ord2f(enc[1]);
     degenerate = empty || !(u > l);
   }
-  const int64_t r = t / chunks;
-  const int ci = (int)(t % chunks);
-  const int j0 = ci * 32;
-  const int nc = min(32, out.cpg - j0);
-  const float *src = x + r * out.cpg + j0;
+  const int64_t r = t / units;
+  const int wi = (int)(t % units);
   const float qmax = (float)((1 << out.bits) - 1);
   const float rng = u - l;
   const int off = out.is_signed ? (1 << (out.bits - 1)) : 0;
-  int c[32];
-  for (int j = 0; j < 32; ++j) {
-    int q = 0;
-    if (j < nc && !degenerate) {
-      const float d = src[j] - l;
-      float tt = d / rng;  // correctly rounded (built with correctly rounded division)
-      tt = tt > 1.0f ? 1.0f : tt;
-      tt = tt >= 0.0f ? tt : 0.0f;
-      q = (int)rintf(tt * qmax);
-    }
-    c[j] = q - off;
+  const float *src = x + r * out.cpg;
+  uint32_t *dst = (uint32_t *)(out.data + r * out.row);
+  if (out.bits == 3) {
+    int c[32];
+    const int j0 = wi * 32;
+    const int nc = min(32, out.cpg - j0);
+    for (int j = 0; j < 32; ++j)
+      c[j] = (j < nc && !degenerate ? quant_one(src[j0 + j], l, rng, qmax) : 0) - off;
+    uint32_t words[3];
+    pack_chunk(c, nc, 3, words);
+    dst[3 * wi] = words[0];
+    dst[3 * wi + 1] = words[1];
+    dst[3 * wi + 2] = words[2];
+    return;
   }
-  uint32_t words[8];
-  pack_chunk(c, nc, out.bits, words);
-  const int per_chunk = out.bits == 3 ? 3 : out.bits;
-  const int nw = chunk_words_in_row(ci, out.bits, out.row / 4);
-  uint32_t *dst = (uint32_t *)(out.data + r * out.row) + (int64_t)ci * per_chunk;
-  for (int k = 0; k < nw; ++k) dst[k] = words[k];
+  const int per = 32 / out.bits;
+  const int j0 = wi * per;
+  const int nc = min(per, out.cpg - j0);
+  const uint32_t mask = (1u << out.bits) - 1u;
+  uint32_t w = 0;
+  for (int k = 0; k < nc; ++k) {
+    const int q = (degenerate ? 0 : quant_one(src[j0 + k], l, rng, qmax)) - off;
+    w |= ((uint32_t)q & mask) << (k * out.bits);
+  }
+  dst[wi] = w;
 }
 
 // ------------------------------------------------------------ shuffle (Eq. 8)
@@ -151,19 +164,48 @@ __global__ void shuffle_kernel(ActView in, int steps, ActView out, int64_t pixel
 }
 
 // ------------------------------------------------------------ max pool
-__global__ void maxpool_kernel(ActView in, int k, int stride, int pad, ActView out, int chunks) {
+// Field-wise max of sixteen 2-bit unsigned fields packed in a word.
+__device__ inline uint32_t max2x16(uint32_t a, uint32_t b) {
+  const uint32_t L = 0x55555555u;
+  const uint32_t a1 = (a >> 1) & L, a0 = a & L, b1 = (b >> 1) & L, b0 = b & L;
+  const uint32_t eq = ~(a1 ^ b1) & L;
+  const uint32_t lo = (eq & (a0 | b0)) | (a1 & ~b1 & a0) | (b1 & ~a1 & b0);
+  return ((a1 | b1) << 1) | lo;
+}
+
+// One thread per output word (b in {2, 4, 8}) or 32-code chunk (b = 3).
+__global__ void maxpool_kernel(ActView in, int k, int stride, int pad, ActView out, int units) {
   const int64_t rows = (int64_t)out.n * out.h * out.w * out.groups;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= rows * chunks) return;
-  const int64_t r = t / chunks;
-  const int ci = (int)(t % chunks);
+  if (t >= rows * units) return;
+  const int64_t r = t / units;
+  const int wi = (int)(t % units);
   const int g = (int)(r % out.groups);
   const int64_t p = r / out.groups;
   const int ox = (int)(p % out.w);
   const int oy = (int)((p / out.w) % out.h);
   const int n = (int)(p / ((int64_t)out.w * out.h));
-  const int j0 = ci * 32;
-  const int nc = min(32, out.cpg - j0);
+  uint32_t *dst = (uint32_t *)(out.data + r * out.row);
+  if (in.bits == 2) {
+    uint32_t m = 0;
+    for (int ky = 0; ky < k; ++ky) {
+      const int iy = oy * stride - pad + ky;
+      if (iy < 0 || iy >= in.h) continue;
+      for (int kx = 0; kx < k; ++kx) {
+        const int ix = ox * stride - pad + kx;
+        if (ix < 0 || ix >= in.w) continue;
+        const uint32_t *row = (const uint32_t *)(in.data + (((int64_t)n * in.h + iy) * in.w + ix) * in.pixel +
+                                                 (int64_t)g * in.row);
+        m = max2x16(m, row[wi]);
+      }
+    }
+    const int used = out.cpg * 2 - wi * 32;  // code bits of this word inside the row
+    dst[wi] = used >= 32 ? m : (m & ((1u << used) - 1u));
+    return;
+  }
+  const int per = in.bits == 3 ? 32 : 32 / in.bits;
+  const int j0 = wi * per;
+  const int nc = min(per, out.cpg - j0);
   int c[32];
   for (int j = 0; j < 32; ++j) c[j] = 0;  // codes are >= 0
   for (int ky = 0; ky < k; ++ky) {
@@ -176,12 +218,17 @@ __global__ void maxpool_kernel(ActView in, int k, int stride, int pad, ActView o
       for (int j = 0; j < nc; ++j) c[j] = max(c[j], read_code(row, j0 + j, in.bits, 0));
     }
   }
-  uint32_t words[8];
-  pack_chunk(c, nc, out.bits, words);
-  const int per_chunk = out.bits == 3 ? 3 : out.bits;
-  const int nw = chunk_words_in_row(ci, out.bits, out.row / 4);
-  uint32_t *dst = (uint32_t *)(out.data + r * out.row) + (int64_t)ci * per_chunk;
-  for (int kk = 0; kk < nw; ++kk) dst[kk] = words[kk];
+  if (in.bits == 3) {
+    uint32_t words[3];
+    pack_chunk(c, nc, 3, words);
+    dst[3 * wi] = words[0];
+    dst[3 * wi + 1] = words[1];
+    dst[3 * wi + 2] = words[2];
+  } else {
+    uint32_t w = 0;
+    for (int j = 0; j < nc; ++j) w |= (uint32_t)c[j] << (j * in.bits);
+    dst[wi] = w;
+  }
 }
 
 // ------------------------------------------------------------ global sum
@@ -200,16 +247,53 @@ __global__ void avgsum_kernel(ActView in, int32_t *out) {
 }
 
 // ------------------------------------------------------------ FC
-__global__ void fc_kernel(const int32_t *x, int n, int cin, const int8_t *w, int cout,
-                          int32_t *logits) {
+// Workgroup tile: 64 images x 64 outputs over a K slice of FC_KS features,
+// staged through LDS; each thread owns a 4 x 4 block of outputs.  K slices
+// are summed with integer atomics (order-free, hence exact).
+constexpr int FC_T = 64, FC_KC = 64, FC_KS = 256;
+
+__global__ void fill_i32_kernel(int32_t *p, int64_t n) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)n * cout) return;
-  const int i = (int)(t / cout), o = (int)(t % cout);
-  const int32_t *xr = x + (int64_t)i * cin;
-  const int8_t *wr = w + (int64_t)o * cin;
-  uint32_t s = 0;  // modular: exact whenever the true sum fits int32
-  for (int c = 0; c < cin; ++c) s += (uint32_t)xr[c] * (uint32_t)(int32_t)wr[c];
-  logits[t] = (int32_t)s;
+  if (t < n) p[t] = 0;
+}
+
+__global__ __launch_bounds__(256) void fc_kernel(const int32_t *x, int n, int cin, const int8_t *w,
+                                                 int cout, int32_t *logits) {
+  __shared__ int32_t xs[FC_KC][FC_T + 1];
+  __shared__ int32_t ws[FC_KC][FC_T + 1];
+  const int i0 = blockIdx.y * FC_T, o0 = blockIdx.x * FC_T;
+  const int c_begin = blockIdx.z * FC_KS;
+  const int c_end = min(cin, c_begin + FC_KS);
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;  // outputs o0+4tx.., images i0+4ty..
+  uint32_t acc[4][4];
+  for (int a = 0; a < 4; ++a)
+    for (int b = 0; b < 4; ++b) acc[a][b] = 0;
+  for (int c0 = c_begin; c0 < c_end; c0 += FC_KC) {
+    for (int e = threadIdx.x; e < FC_KC * FC_T; e += 256) {
+      const int cc = e % FC_KC, rr = e / FC_KC;
+      const int c = c0 + cc;
+      const bool cok = c < c_end;
+      xs[cc][rr] = (cok && i0 + rr < n) ? x[(int64_t)(i0 + rr) * cin + c] : 0;
+      ws[cc][rr] = (cok && o0 + rr < cout) ? (int32_t)w[(int64_t)(o0 + rr) * cin + c] : 0;
+    }
+    __syncthreads();
+    for (int cc = 0; cc < FC_KC; ++cc) {
+      uint32_t xv[4], wv[4];
+      for (int a = 0; a < 4; ++a) xv[a] = (uint32_t)xs[cc][4 * ty + a];
+      for (int b = 0; b < 4; ++b) wv[b] = (uint32_t)ws[cc][4 * tx + b];
+      for (int a = 0; a < 4; ++a)
+        for (int b = 0; b < 4; ++b) acc[a][b] += xv[a] * wv[b];  // modular int32
+    }
+    __syncthreads();
+  }
+  for (int a = 0; a < 4; ++a) {
+    const int i = i0 + 4 * ty + a;
+    if (i >= n) continue;
+    for (int b = 0; b < 4; ++b) {
+      const int o = o0 + 4 * tx + b;
+      if (o < cout) atomicAdd((uint32_t *)&logits[(int64_t)i * cout + o], acc[a][b]);
+    }
+  }
 }
 
 }  // namespace
@@ -246,10 +330,10 @@ hipError_t launch_minmax(const float *x, int64_t count, float *range, hipStream_
 hipError_t launch_quantize(const float *x, float l, float u, const float *range, const ActView &out,
                            hipStream_t s) {
   const int64_t rows = (int64_t)out.n * out.h * out.w * out.groups;
-  const int chunks = (out.cpg + 31) / 32;
+  const int units = out.bits == 3 ? (out.cpg + 31) / 32 : (int)(out.row / 4);
   if (rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(quantize_kernel, dim3(grid_for(rows * chunks)), dim3(kBlock), 0, s, x, l, u,
-                     (const uint32_t *)range, out, rows, chunks);
+  hipLaunchKernelGGL(quantize_kernel, dim3(grid_for(rows * units)), dim3(kBlock), 0, s, x, l, u,
+                     (const uint32_t *)range, out, rows, units);
   return hipGetLastError();
 }
 
@@ -270,10 +354,10 @@ hipError_t launch_shuffle(const ActView &in, int32_t steps, const ActView &out, 
 hipError_t launch_maxpool(const ActView &in, int k, int stride, int pad, const ActView &out,
                           hipStream_t s) {
   const int64_t rows = (int64_t)out.n * out.h * out.w * out.groups;
-  const int chunks = (out.cpg + 31) / 32;
+  const int units = out.bits == 3 ? (out.cpg + 31) / 32 : (int)(out.row / 4);
   if (rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(maxpool_kernel, dim3(grid_for(rows * chunks)), dim3(kBlock), 0, s, in, k,
-                     stride, pad, out, chunks);
+  hipLaunchKernelGGL(maxpool_kernel, dim3(grid_for(rows * units)), dim3(kBlock), 0, s, in, k,
+                     stride, pad, out, units);
   return hipGetLastError();
 }
 
@@ -288,8 +372,10 @@ hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout
                      hipStream_t s) {
   const int64_t items = (int64_t)n * cout;
   if (items == 0) return hipSuccess;
-  hipLaunchKernelGGL(fc_kernel, dim3(grid_for(items)), dim3(kBlock), 0, s, x, n, cin, w, cout,
-                     logits);
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(items)), dim3(kBlock), 0, s, logits, items);
+  dim3 grid((unsigned)((cout + FC_T - 1) / FC_T), (unsigned)((n + FC_T - 1) / FC_T),
+            (unsigned)((cin + FC_KS - 1) / FC_KS));
+  hipLaunchKernelGGL(fc_kernel, grid, dim3(256), 0, s, x, n, cin, w, cout, logits);
   return hipGetLastError();
 }
 

@@ -125,6 +125,7 @@ void palq_destroy(palq_ctx *ctx) {
   if (ctx->device >= 0) {
     hipSetDevice(ctx->device);
     if (ctx->range_scratch) hipFree(ctx->range_scratch);
+    if (ctx->conv_scratch) hipFree(ctx->conv_scratch);
   }
   delete ctx;
 }
@@ -224,6 +225,8 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
     return fail(ctx, PALQ_ERR_ARG, "requant arrays must be 16-byte aligned");
   if (res && ((uintptr_t)res->res_mult & 15u))
     return fail(ctx, PALQ_ERR_ARG, "res_mult must be 16-byte aligned");
+  if (w->groups * (int64_t)w->cout_pg > (1 << 24))
+    return fail(ctx, PALQ_ERR_UNSUPPORTED, "more than 2^24 output channels");
   if (!valid_bits(rq->out_bits)) return fail(ctx, PALQ_ERR_ARG, "requant: out_bits not in {2,3,4,8}");
   if (stride < 1 || pad < 0) return fail(ctx, PALQ_ERR_ARG, "stride must be >= 1 and pad >= 0");
   if (in->groups != w->groups || in->ch_per_group != w->cin_pg)
@@ -241,9 +244,9 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
   if (out->bits != rq->out_bits || out->is_signed)
     return fail(ctx, PALQ_ERR_ARG, "output must be unsigned codes of requant.out_bits bits");
   const int64_t K = (int64_t)w->kh * w->kw * w->cin_pg;
-  const int64_t lim = (int64_t)1 << 27;
+  const int64_t lim = (int64_t)1 << 26;
   if (K * max_code(in->bits, in->is_signed) * max_code(w->bits, 1) >= lim)
-    return fail(ctx, PALQ_ERR_OVERFLOW, "accumulator bound K*max|a|*max|w| >= 2^27");
+    return fail(ctx, PALQ_ERR_OVERFLOW, "accumulator bound K*max|a|*max|w| >= 2^26");
 
   const palq_act *rid = res ? res->identity : nullptr;
   const palq_act *pin = res ? res->proj_in : nullptr;
@@ -268,8 +271,9 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
     if (pin->n != in->n || ((int64_t)pin->h - 1) / res->proj_stride + 1 != ho ||
         ((int64_t)pin->w - 1) / res->proj_stride + 1 != wo)
       return fail(ctx, PALQ_ERR_ARG, "projection output size differs from the convolution's");
-    if ((int64_t)pw->cin_pg * max_code(pin->bits, 0) * max_code(pw->bits, 1) >= lim)
-      return fail(ctx, PALQ_ERR_OVERFLOW, "projection accumulator bound >= 2^27");
+    if (K * max_code(in->bits, in->is_signed) * max_code(w->bits, 1) +
+            (int64_t)pw->cin_pg * max_code(pin->bits, 0) * max_code(pw->bits, 1) >= lim)
+      return fail(ctx, PALQ_ERR_OVERFLOW, "projection accumulator bound >= 2^26");
   }
   const int64_t ob = palq_act_bytes(out);
   if (overlaps(out->data, ob, in->data, palq_act_bytes(in)) ||
@@ -296,9 +300,26 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
   a.acc_dump = acc_dump;
   if (out->n == 0) return PALQ_OK;
   hipSetDevice(ctx->device);
-  hipError_t e = (conv_mfma_supported(a) && (!pin || pw->bits == w->bits))
-                     ? launch_conv_mfma(a, ctx->stream)
-                     : launch_conv_direct(a, ctx->stream);
+  hipError_t e;
+  if (conv_mfma_supported(a)) {
+    const ConvPlan plan = conv_mfma_plan(a);
+    const size_t wbytes = (plan.w_bytes + 255) & ~(size_t)255;
+    const size_t need = wbytes + plan.thr_bytes;
+    if (need > ctx->conv_scratch_bytes) {
+      if (ctx->conv_scratch) hipFree(ctx->conv_scratch);  // waits for work still reading it
+      ctx->conv_scratch = nullptr;
+      ctx->conv_scratch_bytes = 0;
+      if (hipMalloc(&ctx->conv_scratch, need) != hipSuccess)
+        return fail(ctx, PALQ_ERR_NOMEM, "conv scratch");
+      ctx->conv_scratch_bytes = need;
+    }
+    uint8_t *wp = ctx->conv_scratch;
+    int32_t *thr = (int32_t *)(ctx->conv_scratch + wbytes);
+    e = launch_conv_prepare(a, wp, thr, ctx->stream);
+    if (e == hipSuccess) e = launch_conv_mfma(a, wp, thr, ctx->stream);
+  } else {
+    e = launch_conv_direct(a, ctx->stream);
+  }
   return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "group conv");
 }
 

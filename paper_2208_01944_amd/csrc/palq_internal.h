@@ -71,9 +71,18 @@ struct ConvArgs {
 
 // Kernel launchers (return hipError_t of the launch).
 hipError_t launch_conv_direct(const ConvArgs &a, hipStream_t s);
-// Returns hipErrorNotSupported when the shape is outside the MFMA path.
+// Whether the MFMA kernel takes this layer.
 bool conv_mfma_supported(const ConvArgs &a);
-hipError_t launch_conv_mfma(const ConvArgs &a, hipStream_t s);
+// Device scratch the MFMA kernel reads besides the ConvArgs tensors:
+// weights in MFMA operand order and, for 2-bit outputs, requant thresholds.
+struct ConvPlan {
+  size_t w_bytes;
+  size_t thr_bytes;
+};
+ConvPlan conv_mfma_plan(const ConvArgs &a);
+// Fills wp (w_bytes) and thr (thr_bytes) for this layer.
+hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hipStream_t s);
+hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, hipStream_t s);
 
 hipError_t launch_pack(const void *codes, const ActView &out, hipStream_t s);
 hipError_t launch_unpack(const ActView &in, void *codes, hipStream_t s);
@@ -96,4 +105,6 @@ struct palq_ctx {
   hipStream_t stream = nullptr;
   std::string err;
   float *range_scratch = nullptr;  // 2 floats for calibration without range_out
+  uint8_t *conv_scratch = nullptr; // prepacked weights + thresholds of the last conv call
+  size_t conv_scratch_bytes = 0;
 };

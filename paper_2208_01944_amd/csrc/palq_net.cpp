@@ -35,6 +35,8 @@ struct Layer {
   // prepared launch arguments (input pointers patched for tensor 0)
   ConvArgs conv{};
   bool use_mfma = false;
+  int32_t *thr = nullptr;        // requant thresholds (2-bit outputs)
+  uint8_t *wp = nullptr;         // weights in MFMA operand order
   palq_act in_view{}, out_view{};
   int32_t *sums_out = nullptr;   // AVGSUM
   const int32_t *fc_in = nullptr;
@@ -145,7 +147,8 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
   int64_t pool_bytes = 0;
   auto reserve = [&](int64_t b) { int64_t off = pool_bytes; pool_bytes += (b + 255) & ~(int64_t)255; return off; };
   std::vector<int64_t> off_w(n_layers, -1), off_pw(n_layers, -1), off_mult(n_layers, -1),
-      off_shift(n_layers, -1), off_bias(n_layers, -1), off_rm(n_layers, -1), off_fc(n_layers, -1);
+      off_shift(n_layers, -1), off_bias(n_layers, -1), off_rm(n_layers, -1), off_fc(n_layers, -1),
+      off_thr(n_layers, -1);
   std::string err;
   palq_status st = PALQ_OK;
   for (int i = 0; i < n_layers && st == PALQ_OK; ++i) {
@@ -212,6 +215,7 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       off_shift[i] = reserve(nch * 4);
       if (L.bias) off_bias[i] = reserve(nch * 4);
       if (L.res_src >= 0) off_rm[i] = reserve(nch * 4);
+
       if (L.proj_src >= 0)
         off_pw[i] = reserve((int64_t)L.proj_w.groups * L.proj_w.cout_pg * row_bytes(L.proj_w.cin_pg, L.proj_w.bits));
       const int64_t mac = (int64_t)o.n * o.h * o.w * nch *
@@ -355,7 +359,22 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
         regroup(net->tensors[L.proj_src].d, L.proj_w.groups, L.proj_w.cin_pg, &pv);
         a.proj = view_of(&pv);
       }
-      NL.use_mfma = conv_mfma_supported(a) && (L.proj_src < 0 || L.proj_w.bits == L.w.bits);
+      NL.use_mfma = conv_mfma_supported(a);
+      if (NL.use_mfma) {
+        const ConvPlan plan = conv_mfma_plan(a);
+        void *mem = nullptr;
+        if (hipMalloc(&mem, ((plan.w_bytes + 255) & ~(size_t)255) + plan.thr_bytes + 256) != hipSuccess) {
+          free_net(net);
+          return net_fail(ctx, PALQ_ERR_NOMEM, "prepacked weights");
+        }
+        net->bufs.push_back(mem);  // freed with the activation buffers
+        NL.wp = (uint8_t *)mem;
+        NL.thr = (int32_t *)((uint8_t *)mem + ((plan.w_bytes + 255) & ~(size_t)255));
+        if (launch_conv_prepare(a, NL.wp, NL.thr, ctx->stream) != hipSuccess) {
+          free_net(net);
+          return net_fail(ctx, PALQ_ERR_DEVICE, "weight prepack");
+        }
+      }
     } else if (L.op == PALQ_OP_AVGSUM) {
       NL.sums_out = (int32_t *)net->tensors[L.dst].d.data;
     } else if (L.op == PALQ_OP_FC) {
@@ -363,6 +382,10 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
     }
   }
 
+  if (hipStreamSynchronize(ctx->stream) != hipSuccess) {
+    free_net(net);
+    return net_fail(ctx, PALQ_ERR_DEVICE, "requant thresholds");
+  }
   if (flags & PALQ_NET_TIMING) {
     net->events.assign((size_t)kRing * (n_layers + 1), nullptr);
     for (auto &ev : net->events)
@@ -407,7 +430,7 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
         if (sp.src == 0) a.in.data = (uint8_t *)input;
         if (sp.res_src == 0) a.res.data = (uint8_t *)input;
         if (sp.proj_src == 0) a.proj.data = (uint8_t *)input;
-        e = NL.use_mfma ? launch_conv_mfma(a, s) : launch_conv_direct(a, s);
+        e = NL.use_mfma ? launch_conv_mfma(a, NL.wp, NL.thr, s) : launch_conv_direct(a, s);
         break;
       }
       case PALQ_OP_MAXPOOL: {

@@ -102,7 +102,7 @@ def test_validate_only_group_conv_errors(P, vctx):
     big = P.Filter(1, 32, 8192, 3, 3, 8, _fake(10))
     assert _conv(P, vctx, x=_act(P, g=1, c=8192, bits=8, signed=True), f=big,
                  out=_act(P, g=1, c=32, slot=20)) == P.ERR_OVERFLOW
-    assert "2^27" in vctx.last_error()
+    assert "2^26" in vctx.last_error()
 
 
 def test_validate_only_residual_errors(P, vctx):

@@ -110,11 +110,19 @@ def run_conv(ctx, torch, case, centred=False):
         kw_["proj_in"] = ctx.pack(px, G, L["in_bits"])
         pt, kw_["proj_w"] = ctx.pack_filter(L["proj_w"], L["w_bits"])
         kw_["proj_stride"] = L["proj_stride"]
+    # without the accumulator dump (the kernels' common-case epilogue) ...
+    ctx.group_conv(xt, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(bias), out,
+                   shuffle=L["shuffle"], **kw_)
+    ctx.sync()
+    q_plain = ctx.unpack(out)
+    # ... and with it (the general epilogue)
     ctx.group_conv(xt, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(bias), out,
                    shuffle=L["shuffle"], acc_dump=dump, **kw_)
     ctx.sync()
     acc = dump[:n * ho * wo * G * co].cpu().numpy().astype(np.int64).reshape(ref_acc.shape)
-    return ctx.unpack(out), acc, ref_q, ref_acc
+    q = ctx.unpack(out)
+    np.testing.assert_array_equal(q_plain, q)
+    return q, acc, ref_q, ref_acc
 
 
 def check_conv(ctx, torch, case, centred=False, spread=False):
@@ -210,10 +218,16 @@ def run_conv_full(ctx, torch, case):
     dump = torch.zeros(n * ho * wo * G * co, dtype=torch.int32, device=ctx.dev)
     i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
     ctx.group_conv(xt, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(L["bias"]),
+                   out, shuffle=L["shuffle"])
+    ctx.sync()
+    q_plain = ctx.unpack(out)
+    ctx.group_conv(xt, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(L["bias"]),
                    out, shuffle=L["shuffle"], acc_dump=dump)
     ctx.sync()
     acc = dump.cpu().numpy().astype(np.int64).reshape(n, ho, wo, G * co)
-    return ctx.unpack(out), acc
+    q = ctx.unpack(out)
+    np.testing.assert_array_equal(q_plain, q)
+    return q, acc
 
 
 @pytest.mark.parametrize("groups", [1, 2, 4])
@@ -251,21 +265,36 @@ def test_cyclic_shuffle(ctx, bits):
         np.testing.assert_array_equal(ctx.unpack(out), O.cyclic_permute(x, 4, s))
 
 
-@pytest.mark.parametrize("bits", [2, 3, 4])
-def test_maxpool_avgsum_fc(ctx, torch, bits):
-    say(f"maxpool/avgsum/fc bits={bits}")
+@pytest.mark.parametrize("bits,cpg", [(2, 48), (2, 21), (3, 48), (4, 48), (4, 7)])
+def test_maxpool_avgsum_fc(ctx, torch, bits, cpg):
+    say(f"maxpool/avgsum/fc bits={bits} cpg={cpg}")
     g = np.random.default_rng(bits)
-    x = I.codes(g, (3, 13, 12, 2 * 48), bits, False).astype(np.int64)
+    x = I.codes(g, (3, 13, 12, 2 * cpg), bits, False).astype(np.int64)
     t = ctx.pack(x, 2, bits)
-    out = ctx.empty_act(3, 7, 6, 2, 48, bits)
+    out = ctx.empty_act(3, 7, 6, 2, cpg, bits)
     ctx.maxpool(t, 3, 2, 1, out)
     np.testing.assert_array_equal(ctx.unpack(out), O.maxpool(x, 3, 2, 1))
-    sums = torch.empty(3 * 96, dtype=torch.int32, device=ctx.dev)
+    got = out.buf.cpu().numpy()[:3 * 7 * 6 * 2 * packref.row_bytes(cpg, bits)]
+    np.testing.assert_array_equal(got, packref.pack(O.maxpool(x, 3, 2, 1), 2, bits))  # zero padding
+    C = 2 * cpg
+    sums = torch.empty(3 * C, dtype=torch.int32, device=ctx.dev)
     ctx.avgsum(t, sums)
     ref_s = O.avgsum(x)
-    np.testing.assert_array_equal(sums.cpu().numpy().reshape(3, 96), ref_s)
-    w = I.codes(g, (10, 96), 8, True)
+    np.testing.assert_array_equal(sums.cpu().numpy().reshape(3, C), ref_s)
+    w = I.codes(g, (10, C), 8, True)
     logits = torch.empty(30, dtype=torch.int32, device=ctx.dev)
-    ctx.fc(sums, 3, 96, ctx.upload(w), 10, logits)
+    ctx.fc(sums, 3, C, ctx.upload(w), 10, logits)
     ctx.sync()
     np.testing.assert_array_equal(logits.cpu().numpy().reshape(3, 10), O.fc(ref_s, w))
+
+
+def test_fc_large(ctx, torch):
+    """The network's FC shape (64 x 2048 -> 1000) with several K slices."""
+    say("fc 64x2048->1000")
+    g = np.random.default_rng(5)
+    x = g.integers(0, 148, (64, 2048)).astype(np.int32)
+    w = I.codes(g, (1000, 2048), 8, True)
+    logits = torch.empty(64 * 1000, dtype=torch.int32, device=ctx.dev)
+    ctx.fc(ctx.upload(x), 64, 2048, ctx.upload(w), 1000, logits)
+    ctx.sync()
+    np.testing.assert_array_equal(logits.cpu().numpy().reshape(64, 1000), O.fc(x, w))
