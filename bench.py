@@ -37,7 +37,142 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="wall-clock budget of the oracle sample")
+    ap.add_argument("--summarize-profile", metavar="DIR", default=None,
+                    help="only turn the rocprofv3 outputs under DIR (kt/, fetch/, write/, cfetch/, "
+                         "cwrite/ and bench.json, made by the commands written into the summaries) "
+                         "into the text summaries under profiles/ and exit")
+    ap.add_argument("--hbm-copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB three times (the calibration "
+                         "kernel for the FETCH_SIZE / WRITE_SIZE counters) and exit")
     return ap.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_grouped_kernel_resnet18_g4_b2_bs64_traffic.txt")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2208_01944_amd", "csrc", "k_conv_mfma.hip")
+
+
+def measured_traffic():
+    """HBM bytes per conv_grouped_kernel launch from the committed counter
+    summary, or None when the kernel source has changed since the counters
+    were taken (the summary records the source's sha256)."""
+    import hashlib
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith((" ", "#", "|")):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    if kv.get("kernel_source_sha256") != src or "hbm_bytes_per_launch" not in kv:
+        return None
+    return float(kv["hbm_bytes_per_launch"])
+
+
+PROFILE_CMDS = {
+    "kt": "rocprofv3 --kernel-trace --stats --output-format csv -d DIR/kt -o run -- "
+          "python3 bench.py --steps 20 --warmup 2 --no-cpu-baseline",
+    "fetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR/fetch -o run -- "
+             "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
+    "write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d DIR/write -o run -- "
+             "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
+    "cfetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR/cfetch -o run -- "
+              "python3 bench.py --hbm-copy-probe 1024",
+    "cwrite": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d DIR/cwrite -o run -- "
+              "python3 bench.py --hbm-copy-probe 1024",
+    "bench": "python3 bench.py --steps 50 --warmup 5 --no-cpu-baseline > DIR/bench.json",
+}
+
+
+def _short(name):
+    return name.replace("void ", "").replace("palq::(anonymous namespace)::", "").split("(")[0]
+
+
+def summarize_profile(d):
+    """Writes the kernel-time and HBM-traffic summaries of one profiling
+    session (rocprofv3 csv output) under profiles/."""
+    import csv
+    import hashlib
+    bench = json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
+    head = ["# commands (run from the repository root, on one MI355X, `cd /tmp && export TMPDIR=/tmp` first;",
+            "# DIR is any output folder)"]
+    # ---- kernel time
+    rows = list(csv.DictReader(open(os.path.join(d, "kt", "run_kernel_stats.csv"))))
+    out = head + ["#   " + PROFILE_CMDS["kt"], "#   " + PROFILE_CMDS["bench"], "",
+                  "Kernel time, rocprofv3 --kernel-trace --stats (all launches of the profiled run:",
+                  "create-time weight prepack, 2+20 steps of the plain network and of the HIP-event-timed one)", "",
+                  "| kernel | calls | total ms | avg us | min us | max us | % |", "|---|---|---|---|---|---|---|"]
+    fam = {}
+    for r in rows:
+        k = _short(r["Name"])
+        out.append(f"| {k} | {r['Calls']} | {int(r['TotalDurationNs']) / 1e6:.3f} | "
+                   f"{float(r['AverageNs']) / 1e3:.1f} | {int(r['MinNs']) / 1e3:.1f} | {int(r['MaxNs']) / 1e3:.1f} | "
+                   f"{float(r['Percentage']):.2f} |")
+        f = fam.setdefault(k.split("<")[0], [0, 0])
+        f[0] += int(r["Calls"])
+        f[1] += int(r["TotalDurationNs"])
+    g = fam["conv_grouped_kernel"]
+    rf = bench["roofline"]
+    out += ["", "conv_grouped_kernel, all instantiations: %d calls, average %.1f us per launch" % (g[0], g[1] / g[0] / 1e3),
+            "bench.py HIP events on the library stream, same kernel: average %.1f us per launch over %d launches/step"
+            % (rf["avg_launch_us"], rf["launches_per_step"]),
+            "bench.py (plain timed region): %.1f images/s, %.4f ms/step; roofline frac %.4f (%.0f of %.0f int8 TOPS)"
+            % (bench["value"], bench["ms_per_step"], rf["frac"], rf["achieved"], rf["peak"]), "",
+            "Per layer (bench.py HIP events, us per launch):", ""]
+    out += ["| layer | op | kernel | us | int ops | alg. bytes |", "|---|---|---|---|---|---|"]
+    for L in bench["layers"]:
+        out.append(f"| {L['layer']} | {L['op']} | {L.get('kernel', '')} | {L['ms'] * 1e3:.1f} | "
+                   f"{L.get('ops', 0):.3e} | {L.get('bytes', 0):.3e} |")
+    open(os.path.join(ROOT, "profiles", "resnet18_g4_b2_bs64_kernel_stats.md"), "w").write("\n".join(out) + "\n")
+
+    # ---- traffic
+    def load(sub):
+        return [(_short(r["Kernel_Name"]), float(r["Counter_Value"]))
+                for r in csv.DictReader(open(os.path.join(d, sub, "run_counter_collection.csv")))]
+    cf = [v for k, v in load("cfetch") if "copyBuffer" in k]
+    cw = [v for k, v in load("cwrite") if "copyBuffer" in k]
+    probe_kib = 1024 * 1024
+    ff, fw = probe_kib / (sum(cf) / len(cf)), probe_kib / (sum(cw) / len(cw))
+    F, W = load("fetch"), load("write")
+    assert [k for k, _ in F] == [k for k, _ in W]
+    gl = [(f * ff * 1024, w * fw * 1024) for (k, f), (_, w) in zip(F, W) if k.startswith("conv_grouped_kernel")]
+    layers = [L for L in bench["layers"] if L.get("kernel") == "conv_grouped_kernel"]
+    nl = len(layers)
+    assert len(gl) % nl == 0
+    nf = len(gl) // nl
+    per_launch = sum(a + b for a, b in gl) / len(gl)
+    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    out = head + ["#   " + PROFILE_CMDS[k] for k in ("fetch", "write", "cfetch", "cwrite")] + [
+        "",
+        "HBM traffic of conv_grouped_kernel, ResNet-18 PalQuant G=4 2-bit, batch 64 (%d forwards x %d launches)"
+        % (nf, nl), "",
+        "copy calibration (1 GiB device copy): FETCH_SIZE reads %.1f KiB per launch for 1048576 KiB copied"
+        % (sum(cf) / len(cf)),
+        "  -> fetch factor %.4f; WRITE_SIZE reads %.1f KiB -> write factor %.4f" % (ff, sum(cw) / len(cw), fw), "",
+        "| layer | alg. MB | HBM read MB | HBM write MB | (read+write)/alg |", "|---|---|---|---|---|"]
+    for i, L in enumerate(layers):
+        r = sum(gl[j * nl + i][0] for j in range(nf)) / nf
+        w = sum(gl[j * nl + i][1] for j in range(nf)) / nf
+        out.append(f"| {L['layer']} | {L['bytes'] / 1e6:.2f} | {r / 1e6:.2f} | {w / 1e6:.2f} | "
+                   f"{(r + w) / L['bytes']:.2f} |")
+    out += ["", "kernel: conv_grouped_kernel",
+            "kernel_source_sha256: " + src,
+            "hbm_bytes_per_launch: %.0f" % per_launch,
+            "algorithmic_bytes_per_launch: %.0f" % rf["algorithmic_bytes_per_launch"]]
+    open(TRAFFIC_FILE, "w").write("\n".join(out) + "\n")
+    print("wrote", TRAFFIC_FILE)
+
+
+def copy_probe(mib):
+    import torch
+    n = mib << 18                      # int32 elements
+    src = torch.full((n,), 7, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 3}))
 
 
 def cpu_baseline(spec, x_f32, l, u, budget_s):
@@ -64,6 +199,12 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
+    if args.summarize_profile:
+        summarize_profile(args.summarize_profile)
+        return
+    if args.hbm_copy_probe:
+        copy_probe(args.hbm_copy_probe)
+        return
     import torch
     from paper_2208_01944_amd import inputs as I
     from paper_2208_01944_amd import palq
@@ -109,9 +250,15 @@ def main():
     layer_ms, fw = net_t.layer_times()
     layer_ms = layer_ms / max(fw, 1)
 
-    # algorithmic work per layer (2 x MACs) and which kernel runs it
-    conv_ops, conv_ms, other_ms = 0, 0.0, 0.0
-    shapes = {0: (224, 224, 3)}
+    # algorithmic work per layer (2 x MACs, and the bytes a launch must move
+    # at least once: packed input codes, packed weights, packed output codes,
+    # the residual / projection input and the per-channel requant arrays) and
+    # which kernel runs it
+    def act_bytes(h, w, c, bits):
+        return n * h * w * c * bits / 8
+
+    kern = {}
+    shapes = {0: (224, 224, 3, 8)}
     per_layer = []
     for i, L in enumerate(spec["layers"]):
         s = shapes[L["src"]]
@@ -120,30 +267,46 @@ def main():
             ho = (s[0] + 2 * L["pad"] - k) // L["stride"] + 1
             kk = k * k * ci + (L["proj_w"].shape[-1] if L.get("proj_w") is not None else 0)
             ops = 2 * n * ho * ho * g * co * kk
-            shapes[L["dst"]] = (ho, ho, g * co)
+            shapes[L["dst"]] = (ho, ho, g * co, L["out_bits"])
+            nbytes = act_bytes(s[0], s[1], s[2], s[3]) + g * co * k * k * ci * L["w_bits"] / 8 \
+                + act_bytes(ho, ho, g * co, L["out_bits"]) + 3 * 4 * g * co
+            if L.get("res", -1) >= 0:
+                r = shapes[L["res"]]
+                nbytes += act_bytes(r[0], r[1], r[2], r[3]) + 4 * g * co
+            if L.get("proj_src", -1) >= 0:
+                r = shapes[L["proj_src"]]
+                nbytes += act_bytes(r[0], r[1], r[2], r[3]) + L["proj_w"].size * L["w_bits"] / 8
             stem = L["in_bits"] == 8 and L["in_signed"] and L["w_bits"] == 8 and ci <= 4 and k <= 8
-            mfma = co % 32 == 0 and (stem or (ci % 64 == 0 and L["in_bits"] == L["w_bits"]
-                                               and not L["in_signed"]))
-            per_layer.append(dict(layer=i, op="conv", kernel="mfma" if mfma else "direct",
-                                  ops=ops, ms=float(layer_ms[i])))
-            if mfma:
-                conv_ops += ops
-                conv_ms += layer_ms[i]
-            else:
-                other_ms += layer_ms[i]
+            grouped = co % 32 == 0 and ci % 64 == 0 and L["in_bits"] == L["w_bits"] and not L["in_signed"]
+            kname = "conv_stem_kernel" if stem and co % 32 == 0 else \
+                "conv_grouped_kernel" if grouped else "conv_direct_kernel"
+            per_layer.append(dict(layer=i, op="conv", kernel=kname, ops=ops, bytes=nbytes,
+                                  ms=float(layer_ms[i])))
         else:
             if L["op"] == "maxpool":
                 ho = (s[0] + 2 * L["pad"] - L["k"]) // L["stride"] + 1
-                shapes[L["dst"]] = (ho, ho, s[2])
+                shapes[L["dst"]] = (ho, ho, s[2], s[3])
+                kname = "maxpool_kernel"
             else:
-                shapes[L["dst"]] = (1, 1, s[2])
-            per_layer.append(dict(layer=i, op=L["op"], ms=float(layer_ms[i])))
-            other_ms += layer_ms[i]
+                shapes[L["dst"]] = (1, 1, s[2], 32)
+                kname = "avgsum_kernel" if L["op"] == "avgsum" else "fc_kernel"
+            per_layer.append(dict(layer=i, op=L["op"], kernel=kname, ms=float(layer_ms[i])))
+        K = kern.setdefault(kname, dict(launches=0, ops=0, bytes=0.0, ms=0.0))
+        K["launches"] += 1
+        K["ms"] += float(layer_ms[i])
+        K["ops"] += per_layer[-1].get("ops", 0)
+        K["bytes"] += per_layer[-1].get("bytes", 0.0)
 
     total_ops = net.ops
     img_s = n / (ms_per_step / 1e3)
     tops = total_ops / (ms_per_step / 1e3) / 1e12
-    achieved = conv_ops / (conv_ms / 1e3) / 1e12 if conv_ms > 0 else 0.0
+    # the dominant kernel: the grouped B-bit conv (3x3 convs of the residual
+    # blocks, projections fused), 16 launches per step
+    D = kern["conv_grouped_kernel"]
+    launch_ms = D["ms"] / D["launches"]
+    ops_per_launch = D["ops"] / D["launches"]
+    achieved = ops_per_launch / (launch_ms / 1e3) / 1e12
+    traffic = measured_traffic()
     res = {
         "metric": METRIC,
         "value": img_s,
@@ -162,9 +325,12 @@ def main():
         "effective_tops": tops,
         "int_ops_per_step": total_ops,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": INT8_MFMA_PEAK_TOPS,
-                     "unit": "TFLOP/s", "frac": achieved / INT8_MFMA_PEAK_TOPS, "traffic": None,
-                     "kernel": "conv_mfma_kernel (all MFMA conv launches of one step)",
-                     "kernel_ms_per_step": conv_ms, "kernel_int_ops_per_step": conv_ops},
+                     "unit": "TFLOP/s", "frac": achieved / INT8_MFMA_PEAK_TOPS, "traffic": traffic,
+                     "kernel": "conv_grouped_kernel", "launches_per_step": D["launches"],
+                     "avg_launch_us": launch_ms * 1e3, "int_ops_per_launch": ops_per_launch,
+                     "algorithmic_bytes_per_launch": D["bytes"] / D["launches"],
+                     "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"},
+        "kernels": {k: dict(v, avg_launch_us=v["ms"] * 1e3 / v["launches"]) for k, v in kern.items()},
         "timing_pass_ms_per_step": wall_t * 1e3 / args.steps,
         "layers": per_layer,
     }
