@@ -208,8 +208,9 @@ palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, con
 
 /* One layer of a network.  Tensor ids: 0 is the network input; each layer
  * writes a new id `dst` larger than every id before it.  Every pointer in
- * a layer is a HOST pointer to data that palq_net_create copies (the caller
- * may free it afterwards):
+ * a layer is a host or device pointer (any address HIP's default copy kind
+ * accepts) to data that palq_net_create copies into the network's own pool
+ * before it returns (the caller may free it afterwards):
  *   w.data / proj_w.data: packed filter bytes; mult/shift/bias/res_mult:
  *   int32 [groups*cout_pg]; fc_w: int8 [fc_out][cin].
  *  PALQ_OP_CONV    src (codes, viewed as w.groups rows of w.cin_pg codes; a
