@@ -478,6 +478,9 @@ __device__ inline void epilogue_fast(const ConvArgs &a, const Geo &geo, v16i (&a
     uint32_t qv[PB][4];
 #pragma unroll
     for (int qi = 0; qi < 4; ++qi) {
+      // one quad at a time: without this the scheduler hoists the constant
+      // loads of every quad above the last MFMAs and runs out of registers
+      __builtin_amdgcn_sched_barrier(0);
       const int cq = 8 * qi + 4 * half;
       RqConst k[4];
 #pragma unroll
@@ -538,13 +541,22 @@ __device__ inline void epilogue_fast(const ConvArgs &a, const Geo &geo, v16i (&a
   }
 }
 
-// Picks the epilogue once per tile (all conditions are uniform).
-template <int CB, int PB, int RB>
-__device__ inline void finish_tile(const ConvArgs &a, const Geo &geo, bool fast, v16i (&acc)[CB][PB],
+// Each kernel is built twice: GEN = false carries only the fast epilogue
+// (and so needs far fewer registers), GEN = true the general one.
+template <int CB, int PB, int RB, bool GEN>
+__device__ inline void finish_tile(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB],
                                    const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
                                    int l32, int half, const uint8_t *lds) {
-  if (fast) epilogue_fast<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, lds);
-  else epilogue<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, lds);
+  if constexpr (GEN) epilogue<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, lds);
+  else epilogue_fast<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, lds);
+}
+
+// Whether a layer needs the general epilogue: the int64 requant fallback
+// (flag written by requant_prep_kernel), the accumulator dump, 3-bit
+// outputs or an identity shortcut of other than 2 bits.  Uniform.
+__device__ inline bool needs_general(const ConvArgs &a, const Geo &geo, int rb) {
+  return ((const int32_t *)(geo.rq + (int64_t)a.in.groups * a.cout))[0] != 0 || a.acc_dump != nullptr ||
+         a.out.bits == 3 || rb < 0;
 }
 
 // Loads of the K loop, the LDS operand reads and the MFMAs of one K-block
@@ -589,7 +601,7 @@ __device__ inline void finish_tile(const ConvArgs &a, const Geo &geo, bool fast,
 // pixel's 32 codes of the current tap and 64-code block), two K-blocks ahead
 // of use and across tile boundaries; the weight operands are read from LDS
 // two K-blocks ahead too.
-template <int B, int CB, int PB, int RB>
+template <int B, int CB, int PB, int RB, bool GEN>
 __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo geo, int tiles) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   constexpr int BLK = Blk<B>::bytes;
@@ -605,9 +617,10 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
   const int ch0 = blockIdx.y * CB * 32;
   const int KB = geo.kb_total;
 
+  // the launcher may start both builds when it cannot tell which applies:
+  // the other one leaves at once (before any barrier)
+  if (needs_general(a, geo, RB) != GEN) return;
   stage_block<CB>(a, geo, g, lds);
-  const bool fast = !((const int32_t *)(geo.rq + (int64_t)a.in.groups * a.cout))[0] && !a.acc_dump &&
-                    a.out.bits != 3;
   const int first = blockIdx.x * kNW + wave;
   const int tstride = gridDim.x * kNW;
   if (first >= tiles) return;  // no barrier follows
@@ -725,7 +738,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
     else if (phase == 1) PALQ_KLOOP(xs1, xs2, xs0)
     else PALQ_KLOOP(xs2, xs0, xs1)
     phase = (phase + KB) % 3;
-    finish_tile<CB, PB, RB>(a, geo, fast, acc, rw, (int64_t)ct * PB * 32, g, gd, ch0, l32, half, lds);
+    finish_tile<CB, PB, RB, GEN>(a, geo, acc, rw, (int64_t)ct * PB * 32, g, gd, ch0, l32, half, lds);
   }
 }
 
@@ -736,7 +749,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
 // the filter's padding byte is masked to 0 in the prepacked weights), a
 // K-block is two filter rows.  Same persistent structure as the grouped
 // kernel.
-template <int CB, int PB, int RB>
+template <int CB, int PB, int RB, bool GEN>
 __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo, int tiles) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   using Raw = RawT<8, true>;
@@ -751,9 +764,10 @@ __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo
   const int ch0 = blockIdx.y * CB * 32;
   const int KB = geo.kb_total;
 
+  // the launcher may start both builds when it cannot tell which applies:
+  // the other one leaves at once (before any barrier)
+  if (needs_general(a, geo, RB) != GEN) return;
   stage_block<CB>(a, geo, g, lds);
-  const bool fast = !((const int32_t *)(geo.rq + (int64_t)a.in.groups * a.cout))[0] && !a.acc_dump &&
-                    a.out.bits != 3;
   const int first = blockIdx.x * kNW + wave;
   const int tstride = gridDim.x * kNW;
   if (first >= tiles) return;
@@ -833,7 +847,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo
     else if (phase == 1) PALQ_KLOOP(xs1, xs2, xs0)
     else PALQ_KLOOP(xs2, xs0, xs1)
     phase = (phase + KB) % 3;
-    finish_tile<CB, PB, RB>(a, geo, fast, acc, rw, (int64_t)ct * PB * 32, g, gd, ch0, l32, half, lds);
+    finish_tile<CB, PB, RB, GEN>(a, geo, acc, rw, (int64_t)ct * PB * 32, g, gd, ch0, l32, half, lds);
   }
 }
 
@@ -863,9 +877,10 @@ Geo make_geo(const ConvArgs &a) {
 
 size_t lds_bytes(const Geo &geo, int cb) { return (size_t)geo.kb_total * cb * kSlab + (size_t)cb * 32 * sizeof(RqConst); }
 
-// Largest channel block (32 or 64 channels) whose filter fits LDS, 0 if none.
+// Largest channel block (32 or 64 channels) whose filter fits LDS, 0 if
+// none.  Two blocks per wave share every activation load and unpack.
 int pick_cb(const ConvArgs &a, const Geo &geo) {
-  if (a.cout % 64 == 0 && lds_bytes(geo, 2) <= kLdsBudget / 2) return 2;
+  if (a.cout % 64 == 0 && lds_bytes(geo, 2) <= kLdsBudget) return 2;
   if (lds_bytes(geo, 1) <= kLdsBudget) return 1;
   return 0;
 }
@@ -899,23 +914,40 @@ hipError_t launch_persistent(K kern, const ConvArgs &a, const Geo &geo, int cb, 
   return hipGetLastError();
 }
 
+// Starts the fast build, the general build or both (epi -1: which one
+// applies is only known on the device; the other returns at once).
+template <typename KF, typename KG>
+hipError_t launch_pair(KF kfast, KG kgen, int epi, const ConvArgs &a, const Geo &geo, int cb, int pb,
+                       hipStream_t s) {
+  hipError_t e = hipSuccess;
+  if (epi != 1) e = launch_persistent(kfast, a, geo, cb, pb, s);
+  if (e == hipSuccess && epi != 0) e = launch_persistent(kgen, a, geo, cb, pb, s);
+  return e;
+}
+
 template <int B, int CB, int PB>
-hipError_t launch_grouped(const ConvArgs &a, const Geo &geo, hipStream_t s) {
-  if (!a.res.data) return launch_persistent(conv_grouped_kernel<B, CB, PB, 0>, a, geo, CB, PB, s);
-  if (a.res.bits == 2) return launch_persistent(conv_grouped_kernel<B, CB, PB, 2>, a, geo, CB, PB, s);
-  return launch_persistent(conv_grouped_kernel<B, CB, PB, -1>, a, geo, CB, PB, s);
+hipError_t launch_grouped(const ConvArgs &a, const Geo &geo, int epi, hipStream_t s) {
+  if (!a.res.data)
+    return launch_pair(conv_grouped_kernel<B, CB, PB, 0, false>, conv_grouped_kernel<B, CB, PB, 0, true>, epi, a,
+                       geo, CB, PB, s);
+  if (a.res.bits == 2)
+    return launch_pair(conv_grouped_kernel<B, CB, PB, 2, false>, conv_grouped_kernel<B, CB, PB, 2, true>, epi, a,
+                       geo, CB, PB, s);
+  return launch_persistent(conv_grouped_kernel<B, CB, PB, -1, true>, a, geo, CB, PB, s);
 }
 
 template <int CB, int PB>
-hipError_t launch_stem(const ConvArgs &a, const Geo &geo, hipStream_t s) {
-  if (!a.res.data) return launch_persistent(conv_stem_kernel<CB, PB, 0>, a, geo, CB, PB, s);
-  return launch_persistent(conv_stem_kernel<CB, PB, -1>, a, geo, CB, PB, s);
+hipError_t launch_stem(const ConvArgs &a, const Geo &geo, int epi, hipStream_t s) {
+  if (!a.res.data)
+    return launch_pair(conv_stem_kernel<CB, PB, 0, false>, conv_stem_kernel<CB, PB, 0, true>, epi, a, geo, CB, PB,
+                       s);
+  return launch_persistent(conv_stem_kernel<CB, PB, -1, true>, a, geo, CB, PB, s);
 }
 
 template <int B>
-hipError_t dispatch_bits(const ConvArgs &a, const Geo &geo, int cb, int pb, hipStream_t s) {
-  if (cb == 2) return pb == 2 ? launch_grouped<B, 2, 2>(a, geo, s) : launch_grouped<B, 2, 1>(a, geo, s);
-  return pb == 2 ? launch_grouped<B, 1, 2>(a, geo, s) : launch_grouped<B, 1, 1>(a, geo, s);
+hipError_t dispatch_bits(const ConvArgs &a, const Geo &geo, int cb, int pb, int epi, hipStream_t s) {
+  if (cb == 2) return pb == 2 ? launch_grouped<B, 2, 2>(a, geo, epi, s) : launch_grouped<B, 2, 1>(a, geo, epi, s);
+  return pb == 2 ? launch_grouped<B, 1, 2>(a, geo, epi, s) : launch_grouped<B, 1, 1>(a, geo, epi, s);
 }
 
 // Largest magnitude of a code of the given width and sign.
@@ -975,7 +1007,16 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
   return hipGetLastError();
 }
 
-hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, hipStream_t s) {
+int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr) {
+  if (a.acc_dump || a.out.bits == 3 || (a.res.data && a.res.bits != 2)) return 1;
+  int32_t flag = 0;
+  const RqConst *rq = (const RqConst *)thr;
+  if (hipMemcpy(&flag, rq + (int64_t)a.in.groups * a.cout, sizeof(flag), hipMemcpyDeviceToHost) != hipSuccess)
+    return -1;
+  return flag != 0 ? 1 : 0;
+}
+
+hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, int epi, hipStream_t s) {
   Geo geo = make_geo(a);
   if (geo.M == 0) return hipSuccess;
   geo.wp = wp;
@@ -984,14 +1025,15 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
   if (cb == 0) return hipErrorNotSupported;
   int pb = 1;
   tile_override(a, geo, cb, pb);
+  if (a.acc_dump || a.out.bits == 3) epi = 1;
   if (is_stem(a)) {
-    if (cb == 2) return pb == 2 ? launch_stem<2, 2>(a, geo, s) : launch_stem<2, 1>(a, geo, s);
-    return pb == 2 ? launch_stem<1, 2>(a, geo, s) : launch_stem<1, 1>(a, geo, s);
+    if (cb == 2) return pb == 2 ? launch_stem<2, 2>(a, geo, epi, s) : launch_stem<2, 1>(a, geo, epi, s);
+    return pb == 2 ? launch_stem<1, 2>(a, geo, epi, s) : launch_stem<1, 1>(a, geo, epi, s);
   }
   switch (a.in.bits) {
-    case 2: return dispatch_bits<2>(a, geo, cb, pb, s);
-    case 3: return dispatch_bits<3>(a, geo, cb, pb, s);
-    case 4: return dispatch_bits<4>(a, geo, cb, pb, s);
+    case 2: return dispatch_bits<2>(a, geo, cb, pb, epi, s);
+    case 3: return dispatch_bits<3>(a, geo, cb, pb, epi, s);
+    case 4: return dispatch_bits<4>(a, geo, cb, pb, epi, s);
   }
   return hipErrorNotSupported;
 }

@@ -316,7 +316,7 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
     uint8_t *wp = ctx->conv_scratch;
     int32_t *thr = (int32_t *)(ctx->conv_scratch + wbytes);
     e = launch_conv_prepare(a, wp, thr, ctx->stream);
-    if (e == hipSuccess) e = launch_conv_mfma(a, wp, thr, ctx->stream);
+    if (e == hipSuccess) e = launch_conv_mfma(a, wp, thr, -1, ctx->stream);
   } else {
     e = launch_conv_direct(a, ctx->stream);
   }

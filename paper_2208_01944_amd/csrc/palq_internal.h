@@ -82,7 +82,13 @@ struct ConvPlan {
 ConvPlan conv_mfma_plan(const ConvArgs &a);
 // Fills wp (w_bytes) and thr (thr_bytes) for this layer.
 hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hipStream_t s);
-hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, hipStream_t s);
+// Which epilogue build the layer needs once launch_conv_prepare has run and
+// the stream has drained: 0 fast, 1 general, -1 unknown (copy failed).
+// Synchronous; for planning only.
+int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr);
+// epi: the value above, or -1 to start both builds (each checks on the
+// device whether it applies and the other returns at once).
+hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, int epi, hipStream_t s);
 
 hipError_t launch_pack(const void *codes, const ActView &out, hipStream_t s);
 hipError_t launch_unpack(const ActView &in, void *codes, hipStream_t s);

@@ -35,6 +35,7 @@ struct Layer {
   // prepared launch arguments (input pointers patched for tensor 0)
   ConvArgs conv{};
   bool use_mfma = false;
+  int epi = -1;                  // MFMA epilogue build (conv_mfma_epilogue)
   int32_t *thr = nullptr;        // requant thresholds (2-bit outputs)
   uint8_t *wp = nullptr;         // weights in MFMA operand order
   palq_act in_view{}, out_view{};
@@ -386,6 +387,9 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
     free_net(net);
     return net_fail(ctx, PALQ_ERR_DEVICE, "requant thresholds");
   }
+  // the requant constants are final: fix each MFMA layer's epilogue build
+  for (Layer &NL : net->layers)
+    if (NL.spec.op == PALQ_OP_CONV && NL.use_mfma) NL.epi = conv_mfma_epilogue(NL.conv, NL.thr);
   if (flags & PALQ_NET_TIMING) {
     net->events.assign((size_t)kRing * (n_layers + 1), nullptr);
     for (auto &ev : net->events)
@@ -430,7 +434,7 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
         if (sp.src == 0) a.in.data = (uint8_t *)input;
         if (sp.res_src == 0) a.res.data = (uint8_t *)input;
         if (sp.proj_src == 0) a.proj.data = (uint8_t *)input;
-        e = NL.use_mfma ? launch_conv_mfma(a, NL.wp, NL.thr, s) : launch_conv_direct(a, s);
+        e = NL.use_mfma ? launch_conv_mfma(a, NL.wp, NL.thr, NL.epi, s) : launch_conv_direct(a, s);
         break;
       }
       case PALQ_OP_MAXPOOL: {
