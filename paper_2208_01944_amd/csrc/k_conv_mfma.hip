@@ -29,6 +29,7 @@
 //    destination group), so its accumulator lands in the same registers.
 #include <stdio.h>
 #include <stdlib.h>
+#include <string.h>
 
 #include <algorithm>
 
@@ -348,13 +349,12 @@ __device__ inline void stage_block(const ConvArgs &a, const Geo &geo, int g, uin
 // RB: 2 = 2-bit identity shortcut prefetched into rw; -1 = identity shortcut
 // of other widths read here; 0 = none.
 template <int CB, int PB, int RB>
-__device__ inline void epilogue(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB], const uint32_t (&rw)[CB][PB][2],
-                                int64_t mbase, int g, int gd, int ch0, int l32, int half, const uint8_t *lds) {
+__device__ __forceinline__ void epilogue(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB], const uint32_t (&rw)[CB][PB][2],
+                                int64_t mbase, int g, int gd, int ch0, int l32, int half, const RqConst *rq) {
   const int bo = a.out.bits;
   const int qmax = (1 << bo) - 1;
   const int64_t outC = (int64_t)a.in.groups * a.cout;
   const int lsc = geo.scale == 16 ? 4 : 0;
-  const RqConst *rq = (const RqConst *)(lds + geo.kb_total * CB * kSlab);
   const bool exact64 = ((const int32_t *)(geo.rq + (int64_t)a.in.groups * a.cout))[0] != 0;
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
@@ -456,21 +456,54 @@ __device__ inline void epilogue(const ConvArgs &a, const Geo &geo, v16i (&acc)[C
   }
 }
 
+typedef double dbl2 __attribute__((ext_vector_type(2)));
+
+// Four consecutive RqConst records at LDS byte address addr, read with
+// inline asm (invisible to the compiler's memory model, see the tile
+// kernel); rq_wait4 waits for them and hands the registers back.
+__device__ __forceinline__ void rq_read4(uint32_t addr, dbl2 (&k)[4]) {
+  asm volatile("ds_read_b128 %0, %1" : "=v"(k[0]) : "v"(addr));
+  asm volatile("ds_read_b128 %0, %1 offset:16" : "=v"(k[1]) : "v"(addr));
+  asm volatile("ds_read_b128 %0, %1 offset:32" : "=v"(k[2]) : "v"(addr));
+  asm volatile("ds_read_b128 %0, %1 offset:48" : "=v"(k[3]) : "v"(addr));
+}
+__device__ __forceinline__ void rq_wait4(dbl2 (&k)[4]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(k[0]), "+v"(k[1]), "+v"(k[2]), "+v"(k[3]));
+}
+// Four consecutive int32 at LDS byte address addr (same protocol).
+__device__ __forceinline__ void rm_read4(uint32_t addr, v4i &r) {
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
+}
+__device__ __forceinline__ void rm_wait(v4i &r) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r)); }
+
 // Common-case epilogue: fp64 requant valid for the layer, no accumulator
 // dump, 2-, 4- or 8-bit output.  Same arithmetic as `epilogue`, without
 // per-element branches; each quad's constants are fetched from LDS one quad
-// ahead.
-template <int CB, int PB, int RB>
-__device__ inline void epilogue_fast(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB],
-                                     const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
-                                     int l32, int half, const uint8_t *lds) {
-  const int bo = a.out.bits;
-  const int qmax = (1 << bo) - 1;
+// ahead, through rq (LDSASM false) or with rq_read4 at LDS address rq_lds
+// (and the shortcut multipliers with rm_read4 at rm_lds, indexed alike).
+// Output width BO is a compile-time constant here; fma -> saturating
+// unsigned conversion (negative values and NaN give 0, which is the ReLU
+// clamp) -> min with 2^BO - 1 -> shift into the quad's word.
+template <int BO, int CB, int PB, int RB, bool LDSASM>
+__device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB],
+                                        const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
+                                        int l32, int half, const RqConst *rq, uint32_t rq_lds, uint32_t rm_lds) {
+  constexpr int bo = BO;
+  constexpr uint32_t qmax = (1u << BO) - 1u;
   const int lsc = geo.scale == 16 ? 4 : 0;
-  const RqConst *rq = (const RqConst *)(lds + geo.kb_total * CB * kSlab);
-  RqConst kn[4];
+  dbl2 kn[4];
+  v4i rmn = {0, 0, 0, 0};
+  if constexpr (LDSASM) {
+    rq_read4(rq_lds + 4 * half * 16, kn);
+    if constexpr (RB != 0) {
+      rm_read4(rm_lds + 4 * half * 4, rmn);
+      rm_wait(rmn);
+    }
+    rq_wait4(kn);
+  } else {
 #pragma unroll
-  for (int e = 0; e < 4; ++e) kn[e] = rq[4 * half + e];
+    for (int e = 0; e < 4; ++e) kn[e] = dbl2{rq[4 * half + e].s, rq[4 * half + e].o};
+  }
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     const int kc = ch0 + cb * 32;
@@ -482,23 +515,30 @@ __device__ inline void epilogue_fast(const ConvArgs &a, const Geo &geo, v16i (&a
       // loads of every quad above the last MFMAs and runs out of registers
       __builtin_amdgcn_sched_barrier(0);
       const int cq = 8 * qi + 4 * half;
-      RqConst k[4];
+      dbl2 k[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) k[e] = kn[e];
       // next quad's constants (the last one of a block wraps harmlessly)
       const int nxt = (qi < 3 ? cb * 32 + cq + 8 : (cb + 1 < CB ? (cb + 1) * 32 + 4 * half : 0));
-#pragma unroll
-      for (int e = 0; e < 4; ++e) kn[e] = rq[nxt + e];
       v4i rmu = {0, 0, 0, 0};
-      if constexpr (RB != 0) rmu = *(const v4i *)(a.res_mult + csb + cq);
+      if constexpr (LDSASM) {
+        rmu = rmn;
+        rq_read4(rq_lds + nxt * 16, kn);
+        if constexpr (RB != 0) rm_read4(rm_lds + nxt * 4, rmn);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) kn[e] = dbl2{rq[nxt + e].s, rq[nxt + e].o};
+        if constexpr (RB != 0) rmu = *(const v4i *)(a.res_mult + csb + cq);
+      }
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb) {
         int32_t v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[cb][pb][4 * qi + e];
         if constexpr (RB == 2) {
+          // |res_mult| < 2^15 and codes < 4: 24-bit signed products
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] += (rmu[e] * chunk_code(rw[cb][pb], cq + e, 2)) << lsc;
+          for (int e = 0; e < 4; ++e) v[e] += __mul24(rmu[e] << lsc, chunk_code(rw[cb][pb], cq + e, 2));
         } else if constexpr (RB < 0) {
           const int64_t mp = mbase + pb * 32 + l32;
           int rc[4];
@@ -510,11 +550,16 @@ __device__ inline void epilogue_fast(const ConvArgs &a, const Geo &geo, v16i (&a
         uint32_t qword = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          int q = (int)__builtin_fma((double)v[e], k[e].s, k[e].o);
-          q = min(max(q, 0), qmax);
-          qword |= (uint32_t)q << (bo * e);
+          const double d = __builtin_fma((double)v[e], k[e].x, k[e].y);
+          uint32_t q;
+          asm("v_cvt_u32_f64 %0, %1" : "=v"(q) : "v"(d));
+          qword |= min(q, qmax) << (bo * e);
         }
         qv[pb][qi] = qword;
+      }
+      if constexpr (LDSASM) {
+        if constexpr (RB != 0) rm_wait(rmn);
+        rq_wait4(kn);
       }
     }
 #pragma unroll
@@ -541,14 +586,28 @@ __device__ inline void epilogue_fast(const ConvArgs &a, const Geo &geo, v16i (&a
   }
 }
 
+template <int CB, int PB, int RB, bool LDSASM = false>
+__device__ __forceinline__ void epilogue_fast(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB],
+                                     const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
+                                     int l32, int half, const RqConst *rq, uint32_t rq_lds = 0,
+                                     uint32_t rm_lds = 0) {
+  if (a.out.bits == 2)
+    epilogue_fast_bo<2, CB, PB, RB, LDSASM>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rq_lds, rm_lds);
+  else if (a.out.bits == 4)
+    epilogue_fast_bo<4, CB, PB, RB, LDSASM>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rq_lds, rm_lds);
+  else
+    epilogue_fast_bo<8, CB, PB, RB, LDSASM>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rq_lds, rm_lds);
+}
+
 // Each kernel is built twice: GEN = false carries only the fast epilogue
 // (and so needs far fewer registers), GEN = true the general one.
 template <int CB, int PB, int RB, bool GEN>
 __device__ inline void finish_tile(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB],
                                    const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
                                    int l32, int half, const uint8_t *lds) {
-  if constexpr (GEN) epilogue<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, lds);
-  else epilogue_fast<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, lds);
+  const RqConst *rq = (const RqConst *)(lds + geo.kb_total * CB * kSlab);
+  if constexpr (GEN) epilogue<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq);
+  else epilogue_fast<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq);
 }
 
 // Whether a layer needs the general epilogue: the int64 requant fallback
@@ -851,6 +910,311 @@ __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo
   }
 }
 
+// ---------------------------------------------------------------- tile kernel
+// Grouped 2-bit conv as a tiled implicit GEMM.  A tile is TN output channels
+// x TM output pixels of one group; a workgroup's WN x WM waves each own
+// CB x 32 channels x PB x 32 pixels of it.  The prepacked int8 weight slabs
+// and the packed activation codes of every 64-code K-block go straight from
+// memory into a ring of kStages LDS stages (buffer loads with the LDS
+// destination, 16 bytes per lane, coalesced), kStages - 1 K-blocks ahead of
+// the MFMAs; one barrier per K-block.  No registers hold data in flight
+// except the operands of the next K-block, which are read from LDS while
+// the MFMAs of the current one run.
+// The compiler makes every ordinary LDS access wait for all outstanding
+// LDS-destination loads, which would drain the ring at each K-block, so the
+// kernel's LDS reads are inline asm with explicit waits, the requant
+// constants (of the at most two channel blocks a run of tiles touches) are
+// staged before the first load, and a 2-bit identity shortcut's codes for a
+// tile come through the same load stream (into one of two LDS buffers).
+//
+// Workgroups are persistent: workgroup w walks a contiguous run of tiles
+// (pixel tile fastest), and the fetches run across tile boundaries, so the
+// next tile's first K-blocks are in flight during this tile's epilogue.
+// Workgroup ids are dealt round-robin over the 8 XCDs; the runs are laid out
+// so that each XCD gets one contiguous range of tiles, which keeps a group's
+// weights in that XCD's L2.  Fast epilogue only: layers that need the
+// general one leave at once.
+constexpr int kStages = 5;
+
+// s_waitcnt immediates (gfx9 encoding): vmcnt(n) alone, and lgkmcnt(0) alone.
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xF00; }
+constexpr int kWaitLgkm0 = 0xC07F;
+
+// Barrier for the LDS ring: the caller has already waited for what must be
+// complete; the empty asm statements keep the compiler from moving memory
+// operations across it.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int CB, int PB, int WN, int WM, int RB>
+__global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_kernel(ConvArgs a, Geo geo, int npt,
+                                                                                      int ncb, int per) {
+  constexpr int B = 2;
+  constexpr int NT = WN * WM * 64;
+  constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
+  constexpr int BLK = Blk<B>::bytes;  // packed bytes of one pixel's 64-code block
+  constexpr int WST = TN * 64;        // int8 weight bytes of one K-block
+  constexpr int XST = TM * BLK;       // packed activation bytes of one K-block
+  constexpr int SST = WST + XST;      // one ring stage
+  constexpr int WLD = WST / (NT * 16);  // 16-byte weight loads per thread and K-block
+  constexpr int XTH = XST / 16;         // threads that load one 16-byte activation piece
+  static_assert(WLD == 1 || WLD == 2, "weight loads per thread");
+  static_assert(XTH == NT || XTH == NT / 2, "activation pieces");
+  // loads per K-block of the waves with the fewest (the ring waits on that)
+  constexpr int LPK = WLD + (XTH == NT ? 1 : 0);
+  constexpr int RQB = 2 * TN * (int)sizeof(RqConst);  // requant constants of two channel blocks
+  constexpr int RMB = RB ? 2 * TN * 4 : 0;            // their shortcut multipliers
+  constexpr int RPX = TN / 4;                          // shortcut code bytes per pixel of a tile
+  constexpr int RSB = RB ? TM * RPX : 0;               // shortcut codes of one tile
+  static_assert(RB == 0 || TM * RPX == NT * 16, "one 16-byte shortcut piece per thread");
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kStages * SST + RQB + RMB + 2 * RSB];
+  static_assert(CB == 2 && PB == 2, "compute() below is written out for 2 x 2 blocks");
+  using Raw = RawT<B, false>;
+
+  if (needs_general(a, geo, RB)) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int wn = wave / WM, wm = wave % WM;
+
+  // this workgroup's run of tiles; tile = (g * ncb + cbk) * npt + pt
+  const int G = a.in.groups;
+  const int T = npt * ncb * G;
+  const int nwg = (int)gridDim.x;  // a multiple of 8
+  const int lw = (int)(blockIdx.x & 7) * (nwg >> 3) + (int)(blockIdx.x >> 3);
+  const int t_begin = lw * per;
+  const int t_end = min(T, t_begin + per);
+  if (t_begin >= t_end) return;  // no barrier yet
+  const int KB = geo.kb_total;
+  const int total = (t_end - t_begin) * KB;  // K-blocks this workgroup runs
+
+  // requant constants of the channel blocks (g, cbk) = combo c0 and c0 + 1
+  // (a run spans at most two: the launcher keeps per <= npt)
+  const int c0 = t_begin / npt;
+  RqConst *rq_area = (RqConst *)(lds + kStages * SST);
+  int32_t *rm_area = (int32_t *)(lds + kStages * SST + RQB);
+  for (int c = tid; c < 2 * TN; c += NT) {
+    const int combo = min(c0 + c / TN, ncb * G - 1);
+    const int cbk = combo % ncb, g = combo / ncb;
+    rq_area[c] = geo.rq[(int64_t)g * a.cout + cbk * TN + c % TN];
+    if constexpr (RB != 0) rm_area[c] = a.res_mult[(int64_t)g * a.cout + cbk * TN + c % TN];
+  }
+  __syncthreads();
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
+
+  const auto rw_src = make_rsrc(geo.wp, (int64_t)G * a.cout * KB * 64);
+  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
+  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, (int64_t)a.proj.n * a.proj.h * a.proj.w * a.proj.pixel)
+                               : make_rsrc(a.in.data, 0);
+  const int pixb = (int)a.in.pixel;
+  const int rowb = a.in.w * pixb;
+  const int HW = a.ho * a.wo;
+  const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
+
+  // ---- fetcher: this thread's share of K-block f_kb of tile f_tile
+  // weights: 16-byte pieces tid + i * NT of the K-block's TN/32 slabs;
+  // activations: piece tid (threads < XTH), i.e. pixel xp of the tile
+  const int xp = tid, xb = 0;
+  typedef __attribute__((address_space(3))) void *lds_ptr;
+  int f_tile = t_begin, f_kb = 0, f_tap = 0, f_cblk = 0, f_kx = 0, f_ky = 0, f_tapoff = 0;
+  uint32_t wbase, tmask;
+  int off0, poff;
+  auto tile_geometry = [&]() __attribute__((always_inline)) {
+    const int pt = f_tile % npt;
+    const int cbk = (f_tile / npt) % ncb;
+    const int g = f_tile / (npt * ncb);
+    const int gd = (g + a.shuffle) % G;
+    wbase = (uint32_t)((((int64_t)g * (a.cout / 32) + cbk * (TN / 32)) * KB) * kSlab);
+    const int m = pt * TM + xp;
+    const bool valid = f_tile < t_end && m < geo.M && xp < TM;
+    const int mm = valid ? m : 0;
+    const int n = fdiv(mm, HW, inv_hw);
+    const int rem = mm - n * HW;
+    const int oy = fdiv(rem, a.wo, inv_wo);
+    const int ox = rem - oy * a.wo;
+    const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
+    off0 = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.row + xb;
+    const int xlo = max(0, -ix0), xhi = min(a.kw, a.in.w - ix0);
+    const uint32_t below = xhi >= 32 ? 0xffffffffu : ((1u << max(xhi, 0)) - 1u);
+    const uint32_t cols = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
+    const int ylo = max(0, -iy0), yhi = min(a.kh, a.in.h - iy0);
+    uint32_t mk = 0;
+    for (int ky = ylo; ky < yhi; ++ky) mk |= cols << (ky * a.kw);
+    tmask = valid ? mk : 0u;
+    poff = (a.proj.data && valid)
+               ? (((n * a.proj.h + oy * a.proj_stride) * a.proj.w + ox * a.proj_stride) * (int)a.proj.pixel +
+                  gd * (int)a.proj.row + xb)
+               : (int)kOob;
+  };
+  tile_geometry();
+  // Fetches K-block f_kb of tile f_tile into ring stage st.  Fetches past
+  // the last tile read out-of-range offsets (zeros), so every call issues
+  // the same loads.
+  const auto rres = make_rsrc(a.res.data, a.res.data ? (int64_t)a.res.n * a.res.h * a.res.w * a.res.pixel : 0);
+  auto fetch = [&](int st) __attribute__((always_inline)) {
+    const bool live = f_tile < t_end;
+    uint8_t *ws = lds + st * SST;
+    if constexpr (RB == 2) {
+      if (f_kb == 0) {  // the tile's shortcut codes, 16 bytes per thread
+        const int pt = f_tile % npt;
+        const int cbk = (f_tile / npt) % ncb;
+        const int gd = (f_tile / (npt * ncb) + a.shuffle) % G;
+        const int m = pt * TM + tid / (RPX / 16);
+        const uint32_t ro = live && m < geo.M
+                                ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.row + cbk * RPX + (tid % (RPX / 16)) * 16)
+                                : kOob;
+        uint8_t *rb = lds + kStages * SST + RQB + RMB + ((f_tile - t_begin) & 1) * RSB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(rb + wave * 1024), 16, (int)ro, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < WLD; ++i) {
+      const int c = tid + i * NT;  // piece of the K-block's weights
+      const uint32_t woff = live ? wbase + (uint32_t)((c >> 7) * KB + f_kb) * kSlab + (c & 127) * 16 : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + i * NT * 16 + wave * 1024), 16, (int)woff, 0, 0, 0);
+    }
+    if (XTH == NT || tid < XTH) {
+      uint32_t xo;
+      __amdgpu_buffer_rsrc_t xr;
+      if (f_kb < geo.kb_main) {
+        xo = ((tmask >> f_tap) & 1u) ? (uint32_t)(off0 + f_tapoff + f_cblk * BLK) : kOob;
+        xr = rin;
+      } else {
+        xo = (uint32_t)(poff + (f_kb - geo.kb_main) * BLK);
+        xr = rpj;
+      }
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr)(ws + WST + wave * 1024), 16, (int)xo, 0, 0, 0);
+    }
+    if (++f_cblk == geo.cpb) {
+      f_cblk = 0;
+      ++f_tap;
+      if (++f_kx == a.kw) { f_kx = 0; ++f_ky; }
+      f_tapoff = f_ky * rowb + f_kx * pixb;
+    }
+    if (++f_kb == KB) {
+      f_kb = f_tap = f_cblk = f_kx = f_ky = f_tapoff = 0;
+      ++f_tile;
+      tile_geometry();
+    }
+  };
+
+  // ---- compute side: tile c_tile, K-block c_kb
+  int c_tile = t_begin, c_kb = 0;
+  v16i acc[CB][PB];
+  // Per tile, at its first K-block: zeroed accumulators.
+  auto tile_start = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0;
+  };
+  auto tile_end = [&]() __attribute__((always_inline)) {
+    const int pt = c_tile % npt;
+    const int cbk = (c_tile / npt) % ncb;
+    const int g = c_tile / (npt * ncb);
+    const int gd = (g + a.shuffle) % G;
+    uint32_t rw[CB][PB][2] = {};
+    if constexpr (RB == 2) {  // this lane's shortcut codes: pixel block pb, channel block cb
+      const uint32_t ra = lds_base + kStages * SST + RQB + RMB + ((c_tile - t_begin) & 1) * RSB +
+                          (uint32_t)((wm * PB * 32 + l32) * RPX + wn * CB * 8);
+      uint2 r00, r01, r10, r11;  // r[pb][cb]
+      asm volatile(
+          "ds_read_b64 %0, %4\n\t"
+          "ds_read_b64 %1, %4 offset:8\n\t"
+          "ds_read_b64 %2, %4 offset:%5\n\t"
+          "ds_read_b64 %3, %4 offset:%6\n\t"
+          "s_waitcnt lgkmcnt(0)"
+          : "=v"(r00), "=v"(r01), "=v"(r10), "=v"(r11)
+          : "v"(ra), "i"(32 * RPX), "i"(32 * RPX + 8));
+      rw[0][0][0] = r00.x; rw[0][0][1] = r00.y;
+      rw[1][0][0] = r01.x; rw[1][0][1] = r01.y;
+      rw[0][1][0] = r10.x; rw[0][1][1] = r10.y;
+      rw[1][1][0] = r11.x; rw[1][1][1] = r11.y;
+    }
+    const int rec = (c_tile / npt - c0) * TN + wn * CB * 32;  // first record of this wave's channels
+    const uint32_t rq_lds = lds_base + kStages * SST + (uint32_t)(rec * (int)sizeof(RqConst));
+    const uint32_t rm_lds = lds_base + kStages * SST + RQB + (uint32_t)(rec * 4);
+    epilogue_fast<CB, PB, RB, true>(a, geo, acc, rw, (int64_t)pt * TM + wm * PB * 32, g, gd,
+                                    cbk * TN + wn * CB * 32, l32, half, nullptr, rq_lds, rm_lds);
+  };
+  // LDS addresses of this lane's operands in stage 0: activation half row
+  // of pixel block 0, weight unit (j = 0) of channel block 0
+  const uint32_t xaddr0 = lds_base + WST + (uint32_t)((wm * PB * 32 + l32) * BLK + half * (BLK / 2));
+  const uint32_t aaddr0 = lds_base + (uint32_t)((wn * CB) * kSlab + (half * 32 + l32) * 16);
+  // MFMA operands of one K-block: this lane's activation half rows of the two
+  // pixel blocks and weight units a[j][cb].  Read with asm (no wait), waited
+  // for with wait_ops, which hands the registers back to the compiler.
+  struct Ops { uint2 x0, x1; v4i a00, a01, a10, a11; };
+  auto read_ops = [&](int stage, Ops &o) __attribute__((always_inline)) {
+    const uint32_t xa = xaddr0 + stage * SST, aa = aaddr0 + stage * SST;
+    asm volatile(
+        "ds_read_b64 %0, %6\n\t"
+        "ds_read_b64 %1, %6 offset:512\n\t"
+        "ds_read_b128 %2, %7\n\t"
+        "ds_read_b128 %3, %7 offset:2048\n\t"
+        "ds_read_b128 %4, %7 offset:1024\n\t"
+        "ds_read_b128 %5, %7 offset:3072"
+        : "=v"(o.x0), "=v"(o.x1), "=v"(o.a00), "=v"(o.a01), "=v"(o.a10), "=v"(o.a11)
+        : "v"(xa), "v"(aa));
+  };
+  auto wait_ops = [&](Ops &o) __attribute__((always_inline)) {
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(o.x0), "+v"(o.x1), "+v"(o.a00), "+v"(o.a01), "+v"(o.a10), "+v"(o.a11));
+  };
+  auto mfmas = [&](const Ops &o) __attribute__((always_inline)) {
+    Raw xr[PB];
+    xr[0].w[0] = o.x0.x; xr[0].w[1] = o.x0.y;
+    xr[1].w[0] = o.x1.x; xr[1].w[1] = o.x1.y;
+    const v4i A[2][CB] = {{o.a00, o.a01}, {o.a10, o.a11}};
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        const v4i bop = act_operand<B>(xr[pb], j);
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+          acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[j][cb], bop, acc[cb][pb], 0, 0, 0);
+      }
+    }
+  };
+  // K-block gk (operands already in cur): wait until this wave's loads of
+  // K-block gk + 1 have landed, barrier (everyone's have, and everyone is
+  // done with step gk - 1), fetch K-block gk + kStages - 1 into the stage
+  // K-block gk - 1 used, start reading K-block gk + 1's operands, run the
+  // MFMAs of K-block gk, and finish the tile after its last K-block.
+  auto step = [&](int gk, Ops &cur, Ops &nxt) __attribute__((always_inline)) {
+    if (c_kb == 0) tile_start();
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kStages - 3) * LPK));
+    ring_barrier();
+    fetch((gk + kStages - 1) % kStages);
+    read_ops((gk + 1) % kStages, nxt);
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas(cur);
+    wait_ops(nxt);
+    if (++c_kb == KB) {
+      tile_end();
+      c_kb = 0;
+      ++c_tile;
+    }
+  };
+  for (int s = 0; s < kStages - 1; ++s) fetch(s);
+  Ops o0, o1;
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm((kStages - 2) * LPK));
+  ring_barrier();
+  read_ops(0, o0);
+  wait_ops(o0);
+  for (int gk = 0; gk < total; gk += 2) {
+    step(gk, o0, o1);
+    if (gk + 1 >= total) break;
+    step(gk + 1, o1, o0);
+  }
+}
+
 // ---------------------------------------------------------------- launch
 bool is_stem(const ConvArgs &a) {
   return a.in.bits == 8 && a.in.is_signed && a.w_bits == 8 && a.in.row == 4 && a.kw <= 8 &&
@@ -1016,6 +1380,65 @@ int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr) {
   return flag != 0 ? 1 : 0;
 }
 
+// Pixel tile of the tiled kernel for 128-channel blocks (PALQ_TILE_TM=128
+// or 256).
+int tile_tm() {
+  static int v = -1;
+  if (v < 0) {
+    v = 256;
+    if (const char *e = getenv("PALQ_TILE_TM")) v = atoi(e) == 128 ? 128 : 256;
+  }
+  return v;
+}
+
+// Persistent workgroups of the tiled kernel (PALQ_TILE_WGS overrides).
+int tile_wgs() {
+  static int n = -1;
+  if (n < 0) {
+    n = 512;  // 256 CUs x 2
+    if (const char *e = getenv("PALQ_TILE_WGS")) {
+      const int v = atoi(e);
+      if (v >= 8 && v <= 65536) n = v / 8 * 8;
+    }
+  }
+  return n;
+}
+
+// The tiled kernel takes 2-bit grouped layers with 64-channel blocks whose
+// epilogue is the fast one (PALQ_CONV_KERNEL=persistent turns it off).
+bool tile_kernel_applies(const ConvArgs &a) {
+  static int off = -1;
+  if (off < 0) {
+    const char *e = getenv("PALQ_CONV_KERNEL");
+    off = (e && strcmp(e, "persistent") == 0) ? 1 : 0;
+  }
+  const int64_t wbytes = (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64;
+  return !off && !is_stem(a) && a.in.bits == 2 && a.w_bits == 2 && a.cout % 64 == 0 && !a.acc_dump &&
+         wbytes < ((int64_t)1 << 30) && make_geo(a).kb_total >= kStages &&
+         (a.out.bits == 2 || a.out.bits == 4 || a.out.bits == 8) && (!a.res.data || a.res.bits == 2);
+}
+
+// Persistent grid: two workgroups per CU (the kernel's register budget),
+// a multiple of 8 so that every XCD gets the same number of workgroups.
+template <int CB, int PB, int WN, int WM>
+hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
+  constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
+  const int npt = (int)((geo.M + TM - 1) / TM);
+  const int ncb = a.cout / TN;
+  const int64_t T = (int64_t)npt * ncb * a.in.groups;
+  if (T <= 0 || T > 0x7fffffff) return hipErrorInvalidValue;
+  const int slots = tile_wgs() * 256 / (WN * WM * 64);  // 512 threads per CU
+  const int per = (int)std::min<int64_t>((T + slots - 1) / slots, npt);  // runs span <= 2 channel blocks
+  const int nwg = (int)(((T + per - 1) / per + 7) / 8 * 8);
+  if (!a.res.data)
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0, s, a,
+                       geo, npt, ncb, per);
+  else
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0, s, a,
+                       geo, npt, ncb, per);
+  return hipGetLastError();
+}
+
 hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, int epi, hipStream_t s) {
   Geo geo = make_geo(a);
   if (geo.M == 0) return hipSuccess;
@@ -1026,6 +1449,13 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
   int pb = 1;
   tile_override(a, geo, cb, pb);
   if (a.acc_dump || a.out.bits == 3) epi = 1;
+  if (epi != 1 && tile_kernel_applies(a)) {
+    hipError_t e = a.cout % 128 != 0 ? launch_tile<2, 2, 1, 4>(a, geo, s)
+                   : tile_tm() == 128 ? launch_tile<2, 2, 2, 2>(a, geo, s)
+                                      : launch_tile<2, 2, 2, 4>(a, geo, s);
+    if (e != hipSuccess || epi == 0) return e;
+    return dispatch_bits<2>(a, geo, cb, pb, 1, s);  // unknown: the general build decides on the device
+  }
   if (is_stem(a)) {
     if (cb == 2) return pb == 2 ? launch_stem<2, 2>(a, geo, epi, s) : launch_stem<2, 1>(a, geo, epi, s);
     return pb == 2 ? launch_stem<1, 2>(a, geo, epi, s) : launch_stem<1, 1>(a, geo, epi, s);
