@@ -859,8 +859,30 @@ __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo
     }
   };
   geometry(lt);
+  // Without padding (the network pads the input beforehand) every tap
+  // with a non-zero weight lies inside the image: a lane's 8 taps of one
+  // filter row are two 16-byte loads, with no masks (bytes past the real
+  // taps, even in the next row, meet zero weights; past the tensor's end
+  // they read as zero).
+  const bool unpadded = a.pad == 0;
   auto load_next = [&](Raw (&x)[PB]) {
     const int ky = 2 * l_kb + half;  // this lane's filter row
+    if (unpadded) {
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        const uint32_t vo = iy0[pb] >= 0 ? (uint32_t)(off0[pb] + ky * rowb) : kOob;
+        const uint4 v0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rin, (int)vo, 0, 0));
+        const uint4 v1 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rin, (int)vo, 16, 0));
+        x[pb].w[0] = v0.x; x[pb].w[1] = v0.y; x[pb].w[2] = v0.z; x[pb].w[3] = v0.w;
+        x[pb].w[4] = v1.x; x[pb].w[5] = v1.y; x[pb].w[6] = v1.z; x[pb].w[7] = v1.w;
+      }
+      if (++l_kb == KB) {
+        l_kb = 0;
+        lt += tstride;
+        geometry(lt);
+      }
+      return;
+    }
 #pragma unroll
     for (int pb = 0; pb < PB; ++pb) {
       const bool rowok = ky < a.kh && iy0[pb] + ky >= 0 && iy0[pb] + ky < a.in.h;
@@ -1370,6 +1392,8 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
                      res_max, nch, geo.scale, acc_bound, rq, (int32_t *)(rq + nch));
   return hipGetLastError();
 }
+
+bool conv_mfma_pads_input(const ConvArgs &a) { return is_stem(a) && a.pad > 0; }
 
 int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr) {
   if (a.acc_dump || a.out.bits == 3 || (a.res.data && a.res.bits != 2)) return 1;

@@ -7,6 +7,8 @@
 #include <math.h>
 
 #include "codes.h"
+#include <algorithm>
+
 #include "palq_internal.h"
 
 namespace palq {
@@ -231,7 +233,111 @@ __global__ void maxpool_kernel(ActView in, int k, int stride, int pad, ActView o
   }
 }
 
+// 2-bit codes, group rows of a multiple of 16 bytes: one thread per 16-byte
+// piece of one output pixel's group row; grid (pieces of a pixel row, oy, n).
+__global__ void maxpool2_kernel(ActView in, int k, int stride, int pad, ActView out) {
+  const int qpr = (int)(out.row / 16);  // pieces per group row
+  const int per_px = out.groups * qpr;
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= out.w * per_px) return;
+  const int ox = t / per_px;
+  const int rem = t - ox * per_px;
+  const int g = rem / qpr, q = rem - g * qpr;
+  const int oy = blockIdx.y, n = blockIdx.z;
+  uint4 m = make_uint4(0, 0, 0, 0);
+  const int y0 = oy * stride - pad, x0 = ox * stride - pad;
+  const int ylo = max(0, y0), yhi = min(in.h, y0 + k), xlo = max(0, x0), xhi = min(in.w, x0 + k);
+  for (int iy = ylo; iy < yhi; ++iy)
+    for (int ix = xlo; ix < xhi; ++ix) {
+      const uint4 v = *(const uint4 *)(in.data + (((int64_t)n * in.h + iy) * in.w + ix) * in.pixel +
+                                       (int64_t)g * in.row + 16 * q);
+      m.x = max2x16(m.x, v.x);
+      m.y = max2x16(m.y, v.y);
+      m.z = max2x16(m.z, v.z);
+      m.w = max2x16(m.w, v.w);
+    }
+  *(uint4 *)(out.data + (((int64_t)n * out.h + oy) * out.w + ox) * out.pixel + (int64_t)g * out.row + 16 * q) = m;
+}
+
+// ------------------------------------------------------------ zero border
+// out = in with a border of `pad` zero pixels on every side (whole pixels
+// copied as 4-byte words).  One thread per output word.
+__global__ void pad_pixels_kernel(ActView in, int pad, ActView out, int64_t words) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= words) return;
+  const int wpp = (int)(out.pixel / 4);
+  const int64_t px = t / wpp;
+  const int wi = (int)(t - px * wpp);
+  const int x = (int)(px % out.w);
+  const int64_t r = px / out.w;
+  const int y = (int)(r % out.h);
+  const int n = (int)(r / out.h);
+  const int iy = y - pad, ix = x - pad;
+  uint32_t v = 0;
+  if (iy >= 0 && iy < in.h && ix >= 0 && ix < in.w)
+    v = ((const uint32_t *)(in.data + (((int64_t)n * in.h + iy) * in.w + ix) * in.pixel))[wi];
+  ((uint32_t *)out.data)[t] = v;
+}
+
 // ------------------------------------------------------------ global sum
+// 2-bit codes, at most 85 pixels (85 x 3 < 256), 16 | cpg: one thread per
+// (image, group, word of 16 codes).  The word's codes k, k+4, k+8, k+12 sit
+// in the four bytes of (w >> 2k) & 0x03030303, so four byte-lane
+// accumulators sum all 16 codes without carries.
+__global__ void avgsum2_kernel(ActView in, int32_t *out) {
+  const int wpr = in.cpg / 16;  // words per group row
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)in.n * in.groups * wpr) return;
+  const int wi = (int)(t % wpr);
+  const int64_t r = t / wpr;
+  const int g = (int)(r % in.groups);
+  const int n = (int)(r / in.groups);
+  const int hw = in.h * in.w;
+  const uint8_t *base = in.data + (int64_t)n * hw * in.pixel + (int64_t)g * in.row + 4 * wi;
+  uint32_t acc[4] = {0, 0, 0, 0};
+  for (int p = 0; p < hw; ++p) {
+    const uint32_t w = *(const uint32_t *)(base + (int64_t)p * in.pixel);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) acc[kk] += (w >> (2 * kk)) & 0x03030303u;
+  }
+  int32_t *o = out + (int64_t)n * in.groups * in.cpg + (int64_t)g * in.cpg + 16 * wi;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int4 v = make_int4((int)((acc[0] >> (8 * b)) & 255u), (int)((acc[1] >> (8 * b)) & 255u),
+                             (int)((acc[2] >> (8 * b)) & 255u), (int)((acc[3] >> (8 * b)) & 255u));
+    *(int4 *)(o + 4 * b) = v;
+  }
+}
+
+// Same sums with one workgroup per (image, group) when 256 is a multiple of
+// the words per row: thread (word, r) takes pixels r, r + R, ... (R = 256 /
+// words), and the R partial byte-lane sums of a word are added in LDS.
+__global__ __launch_bounds__(256) void avgsum2_wg_kernel(ActView in, int32_t *out) {
+  __shared__ uint32_t part[4][256];
+  const int wpr = in.cpg / 16;
+  const int R = 256 / wpr;
+  const int n = (int)(blockIdx.x / in.groups), g = (int)(blockIdx.x % in.groups);
+  const int wi = threadIdx.x % wpr, r = threadIdx.x / wpr;
+  const int hw = in.h * in.w;
+  const uint8_t *base = in.data + (int64_t)n * hw * in.pixel + (int64_t)g * in.row + 4 * wi;
+  uint32_t acc[4] = {0, 0, 0, 0};
+  for (int p = r; p < hw; p += R) {
+    const uint32_t w = *(const uint32_t *)(base + (int64_t)p * in.pixel);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) acc[kk] += (w >> (2 * kk)) & 0x03030303u;
+  }
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) part[kk][threadIdx.x] = acc[kk];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 4 * wpr; idx += 256) {
+    const int w2 = idx >> 2, kk = idx & 3;
+    uint32_t sum = 0;
+    for (int rr = 0; rr < R; ++rr) sum += part[kk][rr * wpr + w2];
+    int32_t *o = out + (int64_t)n * in.groups * in.cpg + (int64_t)g * in.cpg + 16 * w2 + kk;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) o[4 * b] = (int32_t)((sum >> (8 * b)) & 255u);
+  }
+}
 __global__ void avgsum_kernel(ActView in, int32_t *out) {
   const int64_t C = (int64_t)in.groups * in.cpg;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -296,7 +402,98 @@ __global__ __launch_bounds__(256) void fc_kernel(const int32_t *x, int n, int ci
   }
 }
 
+// FC on the matrix cores.  x = d0 + d1 256 + d2 256^2 + d3 256^3 (mod 2^32)
+// with signed digits d_p in [-128, 127] (each taken from what remains after
+// the lower ones, so the sum is exact modulo 2^32), so
+// logits = sum_p 256^p (D_p W^T) with four int8 x int8 -> int32 products,
+// each exact modulo 2^32 like the definition.  Digit planes: int8
+// [4][n][cin].
+
+// Four consecutive features per thread (cin % 16 == 0); also clears the
+// logits, which fc_mfma_kernel's K slices add into.
+__global__ void fc_digits_kernel(const int32_t *x, int64_t count, int8_t *planes, int32_t *logits,
+                                 int64_t nlogits) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (int64_t i = t; i < nlogits; i += (int64_t)gridDim.x * blockDim.x) logits[i] = 0;
+  if (4 * t >= count) return;
+  const int4 v4 = *(const int4 *)(x + 4 * t);
+  const int32_t v[4] = {v4.x, v4.y, v4.z, v4.w};
+  uint32_t word[4] = {0, 0, 0, 0};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    int64_t r = v[e];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int d = (int)(int8_t)(uint8_t)(r & 255);  // signed digit
+      word[p] |= (uint32_t)(uint8_t)d << (8 * e);
+      r = (r - d) >> 8;                                 // exact: r - d is a multiple of 256
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < 4; ++p) *(uint32_t *)(planes + p * count + 4 * t) = word[p];
+}
+
+typedef int v4i_t __attribute__((ext_vector_type(4)));
+typedef int v16i_t __attribute__((ext_vector_type(16)));
+
+// Workgroup: 32 outputs x 32 images x one K slice (blockIdx.z of
+// gridDim.z); its 4 waves take every 4th 32-wide K step of the slice, sum
+// their partial blocks in LDS and add the result to the logits (integer
+// atomics: order-free, exact modulo 2^32).  A = weights (rows = outputs),
+// B = one digit plane (columns = images); rows and images past the end
+// read out-of-range offsets (zeros).
+__global__ __launch_bounds__(256) void fc_mfma_kernel(const int8_t *w, const int8_t *planes, int n, int cin,
+                                                      int cout, int32_t *logits) {
+  __shared__ int32_t part[3][16][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int o0 = blockIdx.x * 32, i0 = blockIdx.y * 32;
+  const int64_t plane = (int64_t)n * cin;
+  const auto rw = __builtin_amdgcn_make_buffer_rsrc((void *)w, (short)0, (int)((int64_t)cout * cin), 0x00020000);
+  const auto rd = __builtin_amdgcn_make_buffer_rsrc((void *)planes, (short)0, (int)(4 * plane), 0x00020000);
+  const uint32_t kOut = 0x80000000u;  // past every buffer this kernel reads
+  const uint32_t wrow = o0 + l32 < cout ? (uint32_t)((o0 + l32) * cin + 16 * half) : kOut;
+  const uint32_t drow = i0 + l32 < n ? (uint32_t)((i0 + l32) * cin + 16 * half) : kOut;
+  v16i_t acc[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[p][r] = 0;
+  const int steps = cin / 32;
+  const int per = (steps + gridDim.z - 1) / gridDim.z;
+  const int k_end = 32 * min(steps, per * (int)(blockIdx.z + 1));
+  for (int k = 32 * (per * (int)blockIdx.z + wave); k < k_end; k += 128) {
+    const v4i_t a = __builtin_bit_cast(v4i_t, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(wrow + k), 0, 0));
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const uint32_t off = drow == kOut ? kOut : drow + (uint32_t)(p * plane) + k;
+      const v4i_t b = __builtin_bit_cast(v4i_t, __builtin_amdgcn_raw_buffer_load_b128(rd, (int)off, 0, 0));
+      acc[p] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, acc[p], 0, 0, 0);
+    }
+  }
+  uint32_t tot[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r)
+    tot[r] = (uint32_t)acc[0][r] + ((uint32_t)acc[1][r] << 8) + ((uint32_t)acc[2][r] << 16) +
+             ((uint32_t)acc[3][r] << 24);
+  if (wave > 0)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) part[wave - 1][r][lane] = (int32_t)tot[r];
+  __syncthreads();
+  if (wave != 0) return;
+  const int i = i0 + l32;
+  if (i >= n) return;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int o = o0 + 8 * (r >> 2) + 4 * half + (r & 3);
+    const uint32_t sum = tot[r] + (uint32_t)part[0][r][lane] + (uint32_t)part[1][r][lane] + (uint32_t)part[2][r][lane];
+    if (o < cout) atomicAdd((uint32_t *)&logits[(int64_t)i * cout + o], sum);
+  }
+}
+
 }  // namespace
+
+size_t fc_scratch_bytes(int n, int cin) { return cin % 32 == 0 ? (size_t)4 * n * cin : 0; }
 
 hipError_t launch_pack(const void *codes, const ActView &out, hipStream_t s) {
   const int64_t rows = (int64_t)out.n * out.h * out.w * out.groups;
@@ -356,22 +553,60 @@ hipError_t launch_maxpool(const ActView &in, int k, int stride, int pad, const A
   const int64_t rows = (int64_t)out.n * out.h * out.w * out.groups;
   const int units = out.bits == 3 ? (out.cpg + 31) / 32 : (int)(out.row / 4);
   if (rows == 0) return hipSuccess;
+  if (in.bits == 2 && out.row % 16 == 0 && out.h <= 65535 && out.n <= 65535 &&
+      (((uintptr_t)in.data | (uintptr_t)out.data) & 15u) == 0 &&
+      (int64_t)out.w * out.groups * (out.row / 16) < ((int64_t)1 << 30)) {
+    const int64_t per_row = (int64_t)out.w * out.groups * (out.row / 16);
+    dim3 grid((unsigned)((per_row + kBlock - 1) / kBlock), (unsigned)out.h, (unsigned)out.n);
+    hipLaunchKernelGGL(maxpool2_kernel, grid, dim3(kBlock), 0, s, in, k, stride, pad, out);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(maxpool_kernel, dim3(grid_for(rows * units)), dim3(kBlock), 0, s, in, k,
                      stride, pad, out, units);
+  return hipGetLastError();
+}
+
+hipError_t launch_pad_pixels(const ActView &in, int pad, const ActView &out, hipStream_t s) {
+  const int64_t words = (int64_t)out.n * out.h * out.w * (out.pixel / 4);
+  if (words == 0) return hipSuccess;
+  hipLaunchKernelGGL(pad_pixels_kernel, dim3(grid_for(words)), dim3(kBlock), 0, s, in, pad, out, words);
   return hipGetLastError();
 }
 
 hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s) {
   const int64_t items = (int64_t)in.n * in.groups * in.cpg;
   if (items == 0) return hipSuccess;
+  if (in.bits == 2 && in.cpg % 16 == 0 && (int64_t)in.h * in.w <= 85) {
+    const int wpr = in.cpg / 16;
+    if (wpr <= 256 && 256 % wpr == 0 && (int64_t)in.n * in.groups < ((int64_t)1 << 31)) {
+      hipLaunchKernelGGL(avgsum2_wg_kernel, dim3((unsigned)(in.n * in.groups)), dim3(256), 0, s, in, out);
+      return hipGetLastError();
+    }
+    if (((uintptr_t)out & 15u) == 0) {
+      hipLaunchKernelGGL(avgsum2_kernel, dim3(grid_for(items / 16)), dim3(kBlock), 0, s, in, out);
+      return hipGetLastError();
+    }
+  }
   hipLaunchKernelGGL(avgsum_kernel, dim3(grid_for(items)), dim3(kBlock), 0, s, in, out);
   return hipGetLastError();
 }
 
 hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout, int32_t *logits,
-                     hipStream_t s) {
+                     int8_t *scratch, hipStream_t s) {
   const int64_t items = (int64_t)n * cout;
   if (items == 0) return hipSuccess;
+  if (scratch && cin % 32 == 0 && ((uintptr_t)x & 15u) == 0 && (int64_t)4 * n * cin < ((int64_t)1 << 31) &&
+      (int64_t)cout * cin < ((int64_t)1 << 31)) {
+    const int64_t count = (int64_t)n * cin;
+    hipLaunchKernelGGL(fc_digits_kernel, dim3(grid_for(count / 4)), dim3(kBlock), 0, s, x, count, scratch, logits,
+                       items);
+    // enough K slices (of at least 4 steps) for about 512 workgroups
+    const int64_t blocks = (int64_t)((cout + 31) / 32) * ((n + 31) / 32);
+    const int slices = (int)std::max<int64_t>(1, std::min<int64_t>((512 + blocks - 1) / blocks, cin / 128));
+    dim3 grid((unsigned)((cout + 31) / 32), (unsigned)((n + 31) / 32), (unsigned)slices);
+    hipLaunchKernelGGL(fc_mfma_kernel, grid, dim3(256), 0, s, w, (const int8_t *)scratch, n, cin, cout, logits);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(items)), dim3(kBlock), 0, s, logits, items);
   dim3 grid((unsigned)((cout + FC_T - 1) / FC_T), (unsigned)((n + FC_T - 1) / FC_T),
             (unsigned)((cin + FC_KS - 1) / FC_KS));

@@ -126,6 +126,7 @@ void palq_destroy(palq_ctx *ctx) {
     hipSetDevice(ctx->device);
     if (ctx->range_scratch) hipFree(ctx->range_scratch);
     if (ctx->conv_scratch) hipFree(ctx->conv_scratch);
+    if (ctx->fc_scratch) hipFree(ctx->fc_scratch);
   }
   delete ctx;
 }
@@ -392,7 +393,15 @@ palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, con
     return fail(ctx, PALQ_ERR_ARG, "logits overlap an input");
   if (ctx->device < 0 || n == 0) return PALQ_OK;
   hipSetDevice(ctx->device);
-  hipError_t e = launch_fc(x, n, cin, w, cout, logits, ctx->stream);
+  const size_t need = fc_scratch_bytes(n, cin);
+  if (need > ctx->fc_scratch_bytes) {
+    if (ctx->fc_scratch) hipFree(ctx->fc_scratch);  // waits for work still reading it
+    ctx->fc_scratch = nullptr;
+    ctx->fc_scratch_bytes = 0;
+    if (hipMalloc(&ctx->fc_scratch, need) != hipSuccess) return fail(ctx, PALQ_ERR_NOMEM, "fc scratch");
+    ctx->fc_scratch_bytes = need;
+  }
+  hipError_t e = launch_fc(x, n, cin, w, cout, logits, need ? ctx->fc_scratch : nullptr, ctx->stream);
   return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "fc");
 }
 

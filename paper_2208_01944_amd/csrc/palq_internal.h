@@ -82,6 +82,10 @@ struct ConvPlan {
 ConvPlan conv_mfma_plan(const ConvArgs &a);
 // Fills wp (w_bytes) and thr (thr_bytes) for this layer.
 hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hipStream_t s);
+// Whether the MFMA path runs faster on a copy of the input with the zero
+// border made explicit (launch_pad_pixels, then the same layer with pad 0):
+// the 8-bit first layer, whose taps are then fetched without masks.
+bool conv_mfma_pads_input(const ConvArgs &a);
 // Which epilogue build the layer needs once launch_conv_prepare has run and
 // the stream has drained: 0 fast, 1 general, -1 unknown (copy failed).
 // Synchronous; for planning only.
@@ -100,8 +104,13 @@ hipError_t launch_shuffle(const ActView &in, int32_t steps, const ActView &out, 
 hipError_t launch_maxpool(const ActView &in, int k, int stride, int pad, const ActView &out,
                           hipStream_t s);
 hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s);
+// out: in's shape grown by 2 pad pixels in h and w, same pixel bytes.
+hipError_t launch_pad_pixels(const ActView &in, int pad, const ActView &out, hipStream_t s);
+// FC: with scratch (fc_scratch_bytes, device) the matrix-core path runs,
+// else (or when that returns 0) the vector path.
+size_t fc_scratch_bytes(int n, int cin);
 hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout, int32_t *logits,
-                     hipStream_t s);
+                     int8_t *scratch, hipStream_t s);
 
 }  // namespace palq
 
@@ -113,4 +122,6 @@ struct palq_ctx {
   float *range_scratch = nullptr;  // 2 floats for calibration without range_out
   uint8_t *conv_scratch = nullptr; // prepacked weights + thresholds of the last conv call
   size_t conv_scratch_bytes = 0;
+  int8_t *fc_scratch = nullptr;    // digit planes of the last FC call
+  size_t fc_scratch_bytes = 0;
 };

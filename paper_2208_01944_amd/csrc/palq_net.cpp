@@ -35,6 +35,8 @@ struct Layer {
   // prepared launch arguments (input pointers patched for tensor 0)
   ConvArgs conv{};
   bool use_mfma = false;
+  int pad = 0;                   // > 0: the input is first copied with this zero border
+  ActView pad_in{};              // the conv's own input (data patched for tensor 0)
   int epi = -1;                  // MFMA epilogue build (conv_mfma_epilogue)
   int32_t *thr = nullptr;        // requant thresholds (2-bit outputs)
   uint8_t *wp = nullptr;         // weights in MFMA operand order
@@ -43,6 +45,7 @@ struct Layer {
   const int32_t *fc_in = nullptr;
   int8_t *fc_w = nullptr;
   int fc_cin = 0;
+  int8_t *fc_scratch = nullptr;  // digit planes of the FC input
 };
 
 constexpr int kRing = 64;  // forwards whose layer events can be outstanding
@@ -361,6 +364,22 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
         a.proj = view_of(&pv);
       }
       NL.use_mfma = conv_mfma_supported(a);
+      if (NL.use_mfma && conv_mfma_pads_input(a)) {
+        palq_act pv = iv;
+        pv.h += 2 * a.pad;
+        pv.w += 2 * a.pad;
+        void *mem = nullptr;
+        if (hipMalloc(&mem, (size_t)act_bytes(pv) + 256) != hipSuccess) {
+          free_net(net);
+          return net_fail(ctx, PALQ_ERR_NOMEM, "padded input");
+        }
+        net->bufs.push_back(mem);
+        pv.data = mem;
+        NL.pad = a.pad;
+        NL.pad_in = a.in;
+        a.in = view_of(&pv);
+        a.pad = 0;
+      }
       if (NL.use_mfma) {
         const ConvPlan plan = conv_mfma_plan(a);
         void *mem = nullptr;
@@ -380,6 +399,16 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       NL.sums_out = (int32_t *)net->tensors[L.dst].d.data;
     } else if (L.op == PALQ_OP_FC) {
       NL.fc_in = (const int32_t *)net->tensors[L.src].d.data;
+      const size_t need = fc_scratch_bytes(net->n, NL.fc_cin);
+      if (need) {
+        void *mem = nullptr;
+        if (hipMalloc(&mem, need) != hipSuccess) {
+          free_net(net);
+          return net_fail(ctx, PALQ_ERR_NOMEM, "fc scratch");
+        }
+        net->bufs.push_back(mem);
+        NL.fc_scratch = (int8_t *)mem;
+      }
     }
   }
 
@@ -431,7 +460,14 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
     switch (sp.op) {
       case PALQ_OP_CONV: {
         ConvArgs a = NL.conv;
-        if (sp.src == 0) a.in.data = (uint8_t *)input;
+        if (NL.pad > 0) {
+          ActView src = NL.pad_in;
+          if (sp.src == 0) src.data = (uint8_t *)input;
+          e = launch_pad_pixels(src, NL.pad, a.in, s);
+          if (e != hipSuccess) break;
+        } else if (sp.src == 0) {
+          a.in.data = (uint8_t *)input;
+        }
         if (sp.res_src == 0) a.res.data = (uint8_t *)input;
         if (sp.proj_src == 0) a.proj.data = (uint8_t *)input;
         e = NL.use_mfma ? launch_conv_mfma(a, NL.wp, NL.thr, NL.epi, s) : launch_conv_direct(a, s);
@@ -451,7 +487,7 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
         break;
       }
       case PALQ_OP_FC:
-        e = launch_fc(NL.fc_in, net->n, NL.fc_cin, NL.fc_w, sp.fc_out, logits, s);
+        e = launch_fc(NL.fc_in, net->n, NL.fc_cin, NL.fc_w, sp.fc_out, logits, NL.fc_scratch, s);
         break;
     }
     if (ev && e == hipSuccess) hipEventRecord(ev[i + 1], s);

@@ -288,6 +288,45 @@ def test_maxpool_avgsum_fc(ctx, torch, bits, cpg):
     np.testing.assert_array_equal(logits.cpu().numpy().reshape(3, 10), O.fc(ref_s, w))
 
 
+@pytest.mark.parametrize("cpg,h,w", [(64, 9, 9), (16, 5, 17), (128, 7, 7), (64, 12, 11), (48, 7, 7), (512, 3, 5), (2048, 2, 2), (4096, 1, 3)])
+def test_maxpool_avgsum_2bit_vector_paths(ctx, torch, cpg, h, w):
+    """2-bit rows of a multiple of 16 bytes take the vector max pool; at
+    most 85 pixels take the byte-lane global sum (85 x 3 = 255 is the
+    largest sum a byte holds; 12 x 11 = 132 pixels takes the other path)."""
+    say(f"2-bit maxpool/avgsum cpg={cpg} {h}x{w}")
+    g = np.random.default_rng(cpg + h)
+    x = I.codes(g, (3, h, w, 2 * cpg), 2, False).astype(np.int64)
+    x[1] = 3  # every code at its maximum: sums reach 3 * h * w
+    t = ctx.pack(x, 2, 2)
+    ho, wo = O.out_size(h, 3, 2, 1), O.out_size(w, 3, 2, 1)
+    out = ctx.empty_act(3, ho, wo, 2, cpg, 2)
+    ctx.maxpool(t, 3, 2, 1, out)
+    np.testing.assert_array_equal(ctx.unpack(out), O.maxpool(x, 3, 2, 1))
+    sums = torch.empty(3 * 2 * cpg, dtype=torch.int32, device=ctx.dev)
+    ctx.avgsum(t, sums)
+    ctx.sync()
+    np.testing.assert_array_equal(sums.cpu().numpy().reshape(3, 2 * cpg), O.avgsum(x))
+
+
+@pytest.mark.parametrize("n,cin,cout", [(37, 96, 70), (3, 40, 5), (64, 2048, 1000)])
+def test_fc_full_range_modular(ctx, torch, n, cin, cout):
+    """Features over the whole int32 range (the matrix-core path splits them
+    into signed byte digits when cin % 32 == 0): logits equal the exact sum
+    reduced modulo 2^32."""
+    say(f"fc full range {n}x{cin}->{cout}")
+    g = np.random.default_rng(cin)
+    x = g.integers(-2**31, 2**31, (n, cin), dtype=np.int64)
+    x[0, :] = -2**31
+    x[-1, :] = 2**31 - 1
+    w = I.codes(g, (cout, cin), 8, True)
+    logits = torch.empty(n * cout, dtype=torch.int32, device=ctx.dev)
+    ctx.fc(ctx.upload(x.astype(np.int32)), n, cin, ctx.upload(w), cout, logits)
+    ctx.sync()
+    ref = O.fc(x, w)
+    ref32 = ((np.asarray(ref, dtype=object) % 2**32).astype(np.int64)).astype(np.uint32).view(np.int32)
+    np.testing.assert_array_equal(logits.cpu().numpy().reshape(n, cout), ref32)
+
+
 def test_fc_large(ctx, torch):
     """The network's FC shape (64 x 2048 -> 1000) with several K slices."""
     say("fc 64x2048->1000")
