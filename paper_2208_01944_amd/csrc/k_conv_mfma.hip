@@ -32,6 +32,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "codes.h"
 #include "palq_internal.h"
@@ -458,52 +459,19 @@ __device__ __forceinline__ void epilogue(const ConvArgs &a, const Geo &geo, v16i
 
 typedef double dbl2 __attribute__((ext_vector_type(2)));
 
-// Four consecutive RqConst records at LDS byte address addr, read with
-// inline asm (invisible to the compiler's memory model, see the tile
-// kernel); rq_wait4 waits for them and hands the registers back.
-__device__ __forceinline__ void rq_read4(uint32_t addr, dbl2 (&k)[4]) {
-  asm volatile("ds_read_b128 %0, %1" : "=v"(k[0]) : "v"(addr));
-  asm volatile("ds_read_b128 %0, %1 offset:16" : "=v"(k[1]) : "v"(addr));
-  asm volatile("ds_read_b128 %0, %1 offset:32" : "=v"(k[2]) : "v"(addr));
-  asm volatile("ds_read_b128 %0, %1 offset:48" : "=v"(k[3]) : "v"(addr));
-}
-__device__ __forceinline__ void rq_wait4(dbl2 (&k)[4]) {
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(k[0]), "+v"(k[1]), "+v"(k[2]), "+v"(k[3]));
-}
-// Four consecutive int32 at LDS byte address addr (same protocol).
-__device__ __forceinline__ void rm_read4(uint32_t addr, v4i &r) {
-  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
-}
-__device__ __forceinline__ void rm_wait(v4i &r) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r)); }
-
-// Common-case epilogue: fp64 requant valid for the layer, no accumulator
-// dump, 2-, 4- or 8-bit output.  Same arithmetic as `epilogue`, without
-// per-element branches; each quad's constants are fetched from LDS one quad
-// ahead, through rq (LDSASM false) or with rq_read4 at LDS address rq_lds
-// (and the shortcut multipliers with rm_read4 at rm_lds, indexed alike).
 // Output width BO is a compile-time constant here; fma -> saturating
 // unsigned conversion (negative values and NaN give 0, which is the ReLU
 // clamp) -> min with 2^BO - 1 -> shift into the quad's word.
-template <int BO, int CB, int PB, int RB, bool LDSASM>
+template <int BO, int CB, int PB, int RB>
 __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB],
                                         const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
-                                        int l32, int half, const RqConst *rq, uint32_t rq_lds, uint32_t rm_lds) {
+                                        int l32, int half, const RqConst *rq, const int32_t *rm) {
   constexpr int bo = BO;
   constexpr uint32_t qmax = (1u << BO) - 1u;
   const int lsc = geo.scale == 16 ? 4 : 0;
   dbl2 kn[4];
-  v4i rmn = {0, 0, 0, 0};
-  if constexpr (LDSASM) {
-    rq_read4(rq_lds + 4 * half * 16, kn);
-    if constexpr (RB != 0) {
-      rm_read4(rm_lds + 4 * half * 4, rmn);
-      rm_wait(rmn);
-    }
-    rq_wait4(kn);
-  } else {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) kn[e] = dbl2{rq[4 * half + e].s, rq[4 * half + e].o};
-  }
+  for (int e = 0; e < 4; ++e) kn[e] = dbl2{rq[4 * half + e].s, rq[4 * half + e].o};
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     const int kc = ch0 + cb * 32;
@@ -520,16 +488,10 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
       for (int e = 0; e < 4; ++e) k[e] = kn[e];
       // next quad's constants (the last one of a block wraps harmlessly)
       const int nxt = (qi < 3 ? cb * 32 + cq + 8 : (cb + 1 < CB ? (cb + 1) * 32 + 4 * half : 0));
-      v4i rmu = {0, 0, 0, 0};
-      if constexpr (LDSASM) {
-        rmu = rmn;
-        rq_read4(rq_lds + nxt * 16, kn);
-        if constexpr (RB != 0) rm_read4(rm_lds + nxt * 4, rmn);
-      } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) kn[e] = dbl2{rq[nxt + e].s, rq[nxt + e].o};
-        if constexpr (RB != 0) rmu = *(const v4i *)(a.res_mult + csb + cq);
-      }
+      for (int e = 0; e < 4; ++e) kn[e] = dbl2{rq[nxt + e].s, rq[nxt + e].o};
+      v4i rmu = {0, 0, 0, 0};
+      if constexpr (RB != 0) rmu = *(const v4i *)(rm + cb * 32 + cq);
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb) {
         int32_t v[4];
@@ -557,10 +519,6 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
         }
         qv[pb][qi] = qword;
       }
-      if constexpr (LDSASM) {
-        if constexpr (RB != 0) rm_wait(rmn);
-        rq_wait4(kn);
-      }
     }
 #pragma unroll
     for (int pb = 0; pb < PB; ++pb) {
@@ -586,17 +544,18 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
   }
 }
 
-template <int CB, int PB, int RB, bool LDSASM = false>
+// rq: requant constants from the wave's first channel on; rm: the shortcut
+// multipliers of the same channels (used with a shortcut only).
+template <int CB, int PB, int RB>
 __device__ __forceinline__ void epilogue_fast(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB],
                                      const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
-                                     int l32, int half, const RqConst *rq, uint32_t rq_lds = 0,
-                                     uint32_t rm_lds = 0) {
+                                     int l32, int half, const RqConst *rq, const int32_t *rm) {
   if (a.out.bits == 2)
-    epilogue_fast_bo<2, CB, PB, RB, LDSASM>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rq_lds, rm_lds);
+    epilogue_fast_bo<2, CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rm);
   else if (a.out.bits == 4)
-    epilogue_fast_bo<4, CB, PB, RB, LDSASM>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rq_lds, rm_lds);
+    epilogue_fast_bo<4, CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rm);
   else
-    epilogue_fast_bo<8, CB, PB, RB, LDSASM>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rq_lds, rm_lds);
+    epilogue_fast_bo<8, CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rm);
 }
 
 // Each kernel is built twice: GEN = false carries only the fast epilogue
@@ -607,7 +566,8 @@ __device__ inline void finish_tile(const ConvArgs &a, const Geo &geo, v16i (&acc
                                    int l32, int half, const uint8_t *lds) {
   const RqConst *rq = (const RqConst *)(lds + geo.kb_total * CB * kSlab);
   if constexpr (GEN) epilogue<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq);
-  else epilogue_fast<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq);
+  else epilogue_fast<CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq,
+                                 a.res_mult + (int64_t)g * a.cout + ch0);
 }
 
 // Whether a layer needs the general epilogue: the int64 requant fallback
@@ -939,15 +899,15 @@ __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo
 // and the packed activation codes of every 64-code K-block go straight from
 // memory into a ring of kStages LDS stages (buffer loads with the LDS
 // destination, 16 bytes per lane, coalesced), kStages - 1 K-blocks ahead of
-// the MFMAs; one barrier per K-block.  No registers hold data in flight
-// except the operands of the next K-block, which are read from LDS while
-// the MFMAs of the current one run.
-// The compiler makes every ordinary LDS access wait for all outstanding
-// LDS-destination loads, which would drain the ring at each K-block, so the
-// kernel's LDS reads are inline asm with explicit waits, the requant
-// constants (of the at most two channel blocks a run of tiles touches) are
+// the MFMAs; one barrier per K-block.  No registers hold data in flight.
+// The compiler makes every ordinary read of an LDS array that such loads
+// write wait for all of them, which would drain the ring at each K-block,
+// so the ring's operands are read by inline asm that waits for just those
+// reads; the requant constants and shortcut multipliers (of the at most two
+// channel blocks a run of tiles touches) live in arrays of their own,
 // staged before the first load, and a 2-bit identity shortcut's codes for a
-// tile come through the same load stream (into one of two LDS buffers).
+// tile come through the load stream into one of two buffers of the ring's
+// array.
 //
 // Workgroups are persistent: workgroup w walks a contiguous run of tiles
 // (pixel tile fastest), and the fetches run across tile boundaries, so the
@@ -972,28 +932,37 @@ __device__ __forceinline__ void ring_barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <int CB, int PB, int WN, int WM, int RB>
+// STEM: the 8-bit first layer on an input whose zero border is explicit
+// (pad 0): a K-block is two filter rows of 8 four-byte taps, 64 bytes per
+// pixel, fetched as four 16-byte pieces (lane half h of the MFMA takes row
+// 2 kb + h, its 8 taps being the two 16-code operand units); no unpack.
+template <int CB, int PB, int WN, int WM, int RB, bool STEM = false, int kStages = 5>
 __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_kernel(ConvArgs a, Geo geo, int npt,
                                                                                       int ncb, int per) {
   constexpr int B = 2;
   constexpr int NT = WN * WM * 64;
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
-  constexpr int BLK = Blk<B>::bytes;  // packed bytes of one pixel's 64-code block
+  constexpr int BLK = STEM ? 64 : Blk<B>::bytes;  // activation bytes of one pixel's K-block
   constexpr int WST = TN * 64;        // int8 weight bytes of one K-block
-  constexpr int XST = TM * BLK;       // packed activation bytes of one K-block
+  constexpr int XST = TM * BLK;       // activation bytes of one K-block
   constexpr int SST = WST + XST;      // one ring stage
   constexpr int WLD = WST / (NT * 16);  // 16-byte weight loads per thread and K-block
-  constexpr int XTH = XST / 16;         // threads that load one 16-byte activation piece
+  constexpr int XP = XST / 16;          // 16-byte activation pieces of a K-block
+  constexpr bool XALL = XP >= NT;       // every thread loads (XLD pieces), else the first XP threads one
+  constexpr int XLD = XALL ? XP / NT : 1;
   static_assert(WLD == 1 || WLD == 2, "weight loads per thread");
-  static_assert(XTH == NT || XTH == NT / 2, "activation pieces");
+  static_assert(XP == NT / 2 || XP % NT == 0, "activation pieces");
+  static_assert(!STEM || (XALL && RB == 0), "stem layout");
   // loads per K-block of the waves with the fewest (the ring waits on that)
-  constexpr int LPK = WLD + (XTH == NT ? 1 : 0);
+  constexpr int LPK = WLD + (XALL ? XLD : 0);
   constexpr int RQB = 2 * TN * (int)sizeof(RqConst);  // requant constants of two channel blocks
   constexpr int RMB = RB ? 2 * TN * 4 : 0;            // their shortcut multipliers
   constexpr int RPX = TN / 4;                          // shortcut code bytes per pixel of a tile
   constexpr int RSB = RB ? TM * RPX : 0;               // shortcut codes of one tile
   static_assert(RB == 0 || TM * RPX == NT * 16, "one 16-byte shortcut piece per thread");
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kStages * SST + RQB + RMB + 2 * RSB];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kStages * SST + 2 * RSB];
+  __shared__ RqConst rq_area[2 * TN];
+  __shared__ int32_t rm_area[RB ? 2 * TN : 1];
   static_assert(CB == 2 && PB == 2, "compute() below is written out for 2 x 2 blocks");
   using Raw = RawT<B, false>;
 
@@ -1016,8 +985,6 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   // requant constants of the channel blocks (g, cbk) = combo c0 and c0 + 1
   // (a run spans at most two: the launcher keeps per <= npt)
   const int c0 = t_begin / npt;
-  RqConst *rq_area = (RqConst *)(lds + kStages * SST);
-  int32_t *rm_area = (int32_t *)(lds + kStages * SST + RQB);
   for (int c = tid; c < 2 * TN; c += NT) {
     const int combo = min(c0 + c / TN, ncb * G - 1);
     const int cbk = combo % ncb, g = combo / ncb;
@@ -1044,12 +1011,31 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   int f_tile = t_begin, f_kb = 0, f_tap = 0, f_cblk = 0, f_kx = 0, f_ky = 0, f_tapoff = 0;
   uint32_t wbase, tmask;
   int off0, poff;
+  // stem: piece tid + i NT is quarter (tid & 3) of pixel tid / 4 + i NT / 4:
+  // filter row 2 kb + ((tid >> 1) & 1), bytes 16 (tid & 1) ..
+  int soff[XLD];
   auto tile_geometry = [&]() __attribute__((always_inline)) {
     const int pt = f_tile % npt;
     const int cbk = (f_tile / npt) % ncb;
     const int g = f_tile / (npt * ncb);
     const int gd = (g + a.shuffle) % G;
     wbase = (uint32_t)((((int64_t)g * (a.cout / 32) + cbk * (TN / 32)) * KB) * kSlab);
+    if constexpr (STEM) {
+#pragma unroll
+      for (int i = 0; i < XLD; ++i) {
+        const int m = pt * TM + (tid >> 2) + i * (NT / 4);
+        const bool valid = f_tile < t_end && m < geo.M;
+        const int mm = valid ? m : 0;
+        const int n = fdiv(mm, HW, inv_hw);
+        const int rem = mm - n * HW;
+        const int oy = fdiv(rem, a.wo, inv_wo);
+        const int ox = rem - oy * a.wo;
+        soff[i] = valid ? ((n * a.in.h + oy * a.stride) * a.in.w + ox * a.stride) * pixb + g * (int)a.in.row +
+                              ((tid >> 1) & 1) * rowb + (tid & 1) * 16
+                        : -1;
+      }
+      return;
+    }
     const int m = pt * TM + xp;
     const bool valid = f_tile < t_end && m < geo.M && xp < TM;
     const int mm = valid ? m : 0;
@@ -1088,7 +1074,7 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
         const uint32_t ro = live && m < geo.M
                                 ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.row + cbk * RPX + (tid % (RPX / 16)) * 16)
                                 : kOob;
-        uint8_t *rb = lds + kStages * SST + RQB + RMB + ((f_tile - t_begin) & 1) * RSB;
+        uint8_t *rb = lds + kStages * SST + ((f_tile - t_begin) & 1) * RSB;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(rb + wave * 1024), 16, (int)ro, 0, 0, 0);
       }
     }
@@ -1098,7 +1084,14 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
       const uint32_t woff = live ? wbase + (uint32_t)((c >> 7) * KB + f_kb) * kSlab + (c & 127) * 16 : kOob;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + i * NT * 16 + wave * 1024), 16, (int)woff, 0, 0, 0);
     }
-    if (XTH == NT || tid < XTH) {
+    if constexpr (STEM) {
+#pragma unroll
+      for (int i = 0; i < XLD; ++i) {
+        const uint32_t xo = soff[i] >= 0 ? (uint32_t)(soff[i] + 2 * f_kb * rowb) : kOob;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rin, (lds_ptr)(ws + WST + i * NT * 16 + wave * 1024), 16, (int)xo, 0, 0,
+                                                 0);
+      }
+    } else if (XALL || tid < XP) {
       uint32_t xo;
       __amdgpu_buffer_rsrc_t xr;
       if (f_kb < geo.kb_main) {
@@ -1142,7 +1135,7 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
     const int gd = (g + a.shuffle) % G;
     uint32_t rw[CB][PB][2] = {};
     if constexpr (RB == 2) {  // this lane's shortcut codes: pixel block pb, channel block cb
-      const uint32_t ra = lds_base + kStages * SST + RQB + RMB + ((c_tile - t_begin) & 1) * RSB +
+      const uint32_t ra = lds_base + kStages * SST + ((c_tile - t_begin) & 1) * RSB +
                           (uint32_t)((wm * PB * 32 + l32) * RPX + wn * CB * 8);
       uint2 r00, r01, r10, r11;  // r[pb][cb]
       asm volatile(
@@ -1151,7 +1144,7 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
           "ds_read_b64 %2, %4 offset:%5\n\t"
           "ds_read_b64 %3, %4 offset:%6\n\t"
           "s_waitcnt lgkmcnt(0)"
-          : "=v"(r00), "=v"(r01), "=v"(r10), "=v"(r11)
+          : "=&v"(r00), "=&v"(r01), "=&v"(r10), "=&v"(r11)
           : "v"(ra), "i"(32 * RPX), "i"(32 * RPX + 8));
       rw[0][0][0] = r00.x; rw[0][0][1] = r00.y;
       rw[1][0][0] = r01.x; rw[1][0][1] = r01.y;
@@ -1159,36 +1152,62 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
       rw[1][1][0] = r11.x; rw[1][1][1] = r11.y;
     }
     const int rec = (c_tile / npt - c0) * TN + wn * CB * 32;  // first record of this wave's channels
-    const uint32_t rq_lds = lds_base + kStages * SST + (uint32_t)(rec * (int)sizeof(RqConst));
-    const uint32_t rm_lds = lds_base + kStages * SST + RQB + (uint32_t)(rec * 4);
-    epilogue_fast<CB, PB, RB, true>(a, geo, acc, rw, (int64_t)pt * TM + wm * PB * 32, g, gd,
-                                    cbk * TN + wn * CB * 32, l32, half, nullptr, rq_lds, rm_lds);
+    epilogue_fast<CB, PB, RB>(a, geo, acc, rw, (int64_t)pt * TM + wm * PB * 32, g, gd, cbk * TN + wn * CB * 32,
+                              l32, half, rq_area + rec, rm_area + (RB ? rec : 0));
   };
   // LDS addresses of this lane's operands in stage 0: activation half row
   // of pixel block 0, weight unit (j = 0) of channel block 0
   const uint32_t xaddr0 = lds_base + WST + (uint32_t)((wm * PB * 32 + l32) * BLK + half * (BLK / 2));
   const uint32_t aaddr0 = lds_base + (uint32_t)((wn * CB) * kSlab + (half * 32 + l32) * 16);
   // MFMA operands of one K-block: this lane's activation half rows of the two
-  // pixel blocks and weight units a[j][cb].  Read with asm (no wait), waited
-  // for with wait_ops, which hands the registers back to the compiler.
-  struct Ops { uint2 x0, x1; v4i a00, a01, a10, a11; };
+  // pixel blocks and weight units a[j][cb], read by one asm statement that
+  // also waits for them (early-clobber outputs: a result must not land in an
+  // address register a later read of the statement still uses).
+  struct OpsG { uint2 x0, x1; v4i a00, a01, a10, a11; };
+  struct OpsS { v4i x0a, x0b, x1a, x1b, a00, a01, a10, a11; };  // stem: x[pb] words 0-3 / 4-7
+  using Ops = typename std::conditional<STEM, OpsS, OpsG>::type;
   auto read_ops = [&](int stage, Ops &o) __attribute__((always_inline)) {
     const uint32_t xa = xaddr0 + stage * SST, aa = aaddr0 + stage * SST;
+    if constexpr (STEM) {
+      asm volatile(
+          "ds_read_b128 %0, %8\n\t"
+          "ds_read_b128 %1, %8 offset:16\n\t"
+          "ds_read_b128 %2, %8 offset:2048\n\t"
+          "ds_read_b128 %3, %8 offset:2064\n\t"
+          "ds_read_b128 %4, %9\n\t"
+          "ds_read_b128 %5, %9 offset:2048\n\t"
+          "ds_read_b128 %6, %9 offset:1024\n\t"
+          "ds_read_b128 %7, %9 offset:3072\n\t"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(o.x0a), "=&v"(o.x0b), "=&v"(o.x1a), "=&v"(o.x1b), "=&v"(o.a00), "=&v"(o.a01), "=&v"(o.a10),
+            "=&v"(o.a11)
+          : "v"(xa), "v"(aa));
+      return;
+    } else
     asm volatile(
         "ds_read_b64 %0, %6\n\t"
         "ds_read_b64 %1, %6 offset:512\n\t"
         "ds_read_b128 %2, %7\n\t"
         "ds_read_b128 %3, %7 offset:2048\n\t"
         "ds_read_b128 %4, %7 offset:1024\n\t"
-        "ds_read_b128 %5, %7 offset:3072"
-        : "=v"(o.x0), "=v"(o.x1), "=v"(o.a00), "=v"(o.a01), "=v"(o.a10), "=v"(o.a11)
+        "ds_read_b128 %5, %7 offset:3072\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(o.x0), "=&v"(o.x1), "=&v"(o.a00), "=&v"(o.a01), "=&v"(o.a10), "=&v"(o.a11)
         : "v"(xa), "v"(aa));
   };
-  auto wait_ops = [&](Ops &o) __attribute__((always_inline)) {
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(o.x0), "+v"(o.x1), "+v"(o.a00), "+v"(o.a01), "+v"(o.a10), "+v"(o.a11));
-  };
   auto mfmas = [&](const Ops &o) __attribute__((always_inline)) {
+    if constexpr (STEM) {
+      const v4i X[2][PB] = {{o.x0a, o.x1a}, {o.x0b, o.x1b}};
+      const v4i A[2][CB] = {{o.a00, o.a01}, {o.a10, o.a11}};
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb)
+            acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[j][cb], X[j][pb], acc[cb][pb], 0, 0, 0);
+      return;
+    } else {
     Raw xr[PB];
     xr[0].w[0] = o.x0.x; xr[0].w[1] = o.x0.y;
     xr[1].w[0] = o.x1.x; xr[1].w[1] = o.x1.y;
@@ -1203,37 +1222,27 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
           acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[j][cb], bop, acc[cb][pb], 0, 0, 0);
       }
     }
+    }
   };
-  // K-block gk (operands already in cur): wait until this wave's loads of
-  // K-block gk + 1 have landed, barrier (everyone's have, and everyone is
-  // done with step gk - 1), fetch K-block gk + kStages - 1 into the stage
-  // K-block gk - 1 used, start reading K-block gk + 1's operands, run the
-  // MFMAs of K-block gk, and finish the tile after its last K-block.
-  auto step = [&](int gk, Ops &cur, Ops &nxt) __attribute__((always_inline)) {
+  // K-block gk: wait until this wave's loads of it have landed, barrier
+  // (everyone's have, and everyone is done with K-block gk - 1, whose stage
+  // the next fetch reuses), fetch K-block gk + kStages - 1, read the
+  // operands, run the MFMAs, and finish the tile after its last K-block.
+  for (int st = 0; st < kStages - 1; ++st) fetch(st);
+  for (int gk = 0; gk < total; ++gk) {
     if (c_kb == 0) tile_start();
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kStages - 3) * LPK));
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kStages - 2) * LPK));
     ring_barrier();
     fetch((gk + kStages - 1) % kStages);
-    read_ops((gk + 1) % kStages, nxt);
+    Ops o;
+    read_ops(gk % kStages, o);
     __builtin_amdgcn_sched_barrier(0);
-    mfmas(cur);
-    wait_ops(nxt);
+    mfmas(o);
     if (++c_kb == KB) {
       tile_end();
       c_kb = 0;
       ++c_tile;
     }
-  };
-  for (int s = 0; s < kStages - 1; ++s) fetch(s);
-  Ops o0, o1;
-  __builtin_amdgcn_s_waitcnt(waitcnt_vm((kStages - 2) * LPK));
-  ring_barrier();
-  read_ops(0, o0);
-  wait_ops(o0);
-  for (int gk = 0; gk < total; gk += 2) {
-    step(gk, o0, o1);
-    if (gk + 1 >= total) break;
-    step(gk + 1, o1, o0);
   }
 }
 
@@ -1444,7 +1453,20 @@ bool tile_kernel_applies(const ConvArgs &a) {
 
 // Persistent grid: two workgroups per CU (the kernel's register budget),
 // a multiple of 8 so that every XCD gets the same number of workgroups.
-template <int CB, int PB, int WN, int WM>
+// The stem on the tiled kernel: explicit zero border (pad 0), 128-channel
+// blocks, no shortcut, fast epilogue.
+bool stem_tile_applies(const ConvArgs &a) {
+  static int off = -1;
+  if (off < 0) {
+    const char *e = getenv("PALQ_CONV_KERNEL");
+    off = (e && strcmp(e, "persistent") == 0) ? 1 : 0;
+  }
+  return !off && is_stem(a) && a.pad == 0 && a.cout % 128 == 0 && !a.res.data && !a.acc_dump &&
+         (a.out.bits == 2 || a.out.bits == 4 || a.out.bits == 8) &&
+         (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64 < ((int64_t)1 << 30);
+}
+
+template <int CB, int PB, int WN, int WM, bool STEM = false, int S = 5>
 hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
   const int npt = (int)((geo.M + TM - 1) / TM);
@@ -1454,12 +1476,15 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   const int slots = tile_wgs() * 256 / (WN * WM * 64);  // 512 threads per CU
   const int per = (int)std::min<int64_t>((T + slots - 1) / slots, npt);  // runs span <= 2 channel blocks
   const int nwg = (int)(((T + per - 1) / per + 7) / 8 * 8);
-  if (!a.res.data)
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0, s, a,
-                       geo, npt, ncb, per);
+  if constexpr (STEM)
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, true, S>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0, s,
+                       a, geo, npt, ncb, per);
+  else if (!a.res.data)
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0,
+                       s, a, geo, npt, ncb, per);
   else
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0, s, a,
-                       geo, npt, ncb, per);
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0,
+                       s, a, geo, npt, ncb, per);
   return hipGetLastError();
 }
 
@@ -1473,6 +1498,11 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
   int pb = 1;
   tile_override(a, geo, cb, pb);
   if (a.acc_dump || a.out.bits == 3) epi = 1;
+  if (epi != 1 && stem_tile_applies(a)) {
+    hipError_t e = launch_tile<2, 2, 2, 2, true, 4>(a, geo, s);
+    if (e != hipSuccess || epi == 0) return e;
+    return launch_stem<2, 1>(a, geo, 1, s);  // unknown: the general build decides on the device
+  }
   if (epi != 1 && tile_kernel_applies(a)) {
     hipError_t e = a.cout % 128 != 0 ? launch_tile<2, 2, 1, 4>(a, geo, s)
                    : tile_tm() == 128 ? launch_tile<2, 2, 2, 2>(a, geo, s)

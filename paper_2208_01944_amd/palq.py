@@ -18,6 +18,12 @@ LIB_PATH = os.path.join(_HERE, "libpalq.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2208_01944_amd.build`")
 
+# torch ships its own HIP runtime under the same soname (libamdhip64.so.7).
+# Loading torch first makes the library bind to that runtime, so the process
+# has one HIP runtime that both use (loaded the other way round, the
+# library's context creation fails on the GPU machine).
+import torch  # noqa: E402,F401
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 c_i32, c_i64, c_p, c_f = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_float
