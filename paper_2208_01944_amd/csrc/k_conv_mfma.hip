@@ -32,6 +32,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 #include "codes.h"
@@ -916,7 +917,13 @@ __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo
 // so that each XCD gets one contiguous range of tiles, which keeps a group's
 // weights in that XCD's L2.  Fast epilogue only: layers that need the
 // general one leave at once.
-constexpr int kStages = 5;
+#ifndef PALQ_TILE_STAGES
+#define PALQ_TILE_STAGES 4
+#endif
+#ifndef PALQ_STEM_STAGES
+#define PALQ_STEM_STAGES 3
+#endif
+constexpr int kStages = PALQ_TILE_STAGES;
 
 // s_waitcnt immediates (gfx9 encoding): vmcnt(n) alone, and lgkmcnt(0) alone.
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x70 | 0xF00; }
@@ -936,7 +943,7 @@ __device__ __forceinline__ void ring_barrier() {
 // (pad 0): a K-block is two filter rows of 8 four-byte taps, 64 bytes per
 // pixel, fetched as four 16-byte pieces (lane half h of the MFMA takes row
 // 2 kb + h, its 8 taps being the two 16-code operand units); no unpack.
-template <int CB, int PB, int WN, int WM, int RB, bool STEM = false, int kStages = 5>
+template <int CB, int PB, int WN, int WM, int RB, bool STEM = false, int kStages = PALQ_TILE_STAGES>
 __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_kernel(ConvArgs a, Geo geo, int npt,
                                                                                       int ncb, int per) {
   constexpr int B = 2;
@@ -1152,8 +1159,8 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
       rw[1][1][0] = r11.x; rw[1][1][1] = r11.y;
     }
     const int rec = (c_tile / npt - c0) * TN + wn * CB * 32;  // first record of this wave's channels
-    epilogue_fast<CB, PB, RB>(a, geo, acc, rw, (int64_t)pt * TM + wm * PB * 32, g, gd, cbk * TN + wn * CB * 32,
-                              l32, half, rq_area + rec, rm_area + (RB ? rec : 0));
+    epilogue_fast_bo<2, CB, PB, RB>(a, geo, acc, rw, (int64_t)pt * TM + wm * PB * 32, g, gd,
+                                    cbk * TN + wn * CB * 32, l32, half, rq_area + rec, rm_area + (RB ? rec : 0));
   };
   // LDS addresses of this lane's operands in stage 0: activation half row
   // of pixel block 0, weight unit (j = 0) of channel block 0
@@ -1424,21 +1431,39 @@ int tile_tm() {
   return v;
 }
 
-// Persistent workgroups of the tiled kernel (PALQ_TILE_WGS overrides).
-int tile_wgs() {
-  static int n = -1;
-  if (n < 0) {
-    n = 512;  // 256 CUs x 2
-    if (const char *e = getenv("PALQ_TILE_WGS")) {
-      const int v = atoi(e);
-      if (v >= 8 && v <= 65536) n = v / 8 * 8;
-    }
+// Persistent workgroups of a tiled-kernel build: as many as are resident at
+// once (registers and LDS decide; the variants with and without a shortcut
+// need about the same), a multiple of 8.  PALQ_TILE_WGS overrides.
+int tile_slots(const void *kern, int threads) {
+  if (const char *e = getenv("PALQ_TILE_WGS")) {
+    const int v = atoi(e);
+    if (v >= 8 && v <= 65536) return v / 8 * 8;
   }
-  return n;
+  // cached per kernel and device (a handful of builds)
+  static std::mutex mu;
+  static const void *keys[32];
+  static int devs[32], vals[32], used = 0;
+  int dev = 0;
+  hipGetDevice(&dev);
+  std::lock_guard<std::mutex> lock(mu);
+  for (int i = 0; i < used; ++i)
+    if (keys[i] == kern && devs[i] == dev) return vals[i];
+  int cus = 256, per = 2;
+  hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kern, threads, 0) != hipSuccess || per < 1) per = 1;
+  const int v = std::max(8, cus * per / 8 * 8);
+  if (used < 32) {
+    keys[used] = kern;
+    devs[used] = dev;
+    vals[used] = v;
+    ++used;
+  }
+  return v;
 }
 
 // The tiled kernel takes 2-bit grouped layers with 64-channel blocks whose
-// epilogue is the fast one (PALQ_CONV_KERNEL=persistent turns it off).
+// epilogue is the fast one, with 2-bit outputs (PALQ_CONV_KERNEL=persistent
+// turns it off).
 bool tile_kernel_applies(const ConvArgs &a) {
   static int off = -1;
   if (off < 0) {
@@ -1447,8 +1472,8 @@ bool tile_kernel_applies(const ConvArgs &a) {
   }
   const int64_t wbytes = (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64;
   return !off && !is_stem(a) && a.in.bits == 2 && a.w_bits == 2 && a.cout % 64 == 0 && !a.acc_dump &&
-         wbytes < ((int64_t)1 << 30) && make_geo(a).kb_total >= kStages &&
-         (a.out.bits == 2 || a.out.bits == 4 || a.out.bits == 8) && (!a.res.data || a.res.bits == 2);
+         wbytes < ((int64_t)1 << 30) && make_geo(a).kb_total >= kStages && a.out.bits == 2 &&
+         (!a.res.data || a.res.bits == 2);
 }
 
 // Persistent grid: two workgroups per CU (the kernel's register budget),
@@ -1461,19 +1486,18 @@ bool stem_tile_applies(const ConvArgs &a) {
     const char *e = getenv("PALQ_CONV_KERNEL");
     off = (e && strcmp(e, "persistent") == 0) ? 1 : 0;
   }
-  return !off && is_stem(a) && a.pad == 0 && a.cout % 128 == 0 && !a.res.data && !a.acc_dump &&
-         (a.out.bits == 2 || a.out.bits == 4 || a.out.bits == 8) &&
+  return !off && is_stem(a) && a.pad == 0 && a.cout % 128 == 0 && !a.res.data && !a.acc_dump && a.out.bits == 2 &&
          (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64 < ((int64_t)1 << 30);
 }
 
-template <int CB, int PB, int WN, int WM, bool STEM = false, int S = 5>
+template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES>
 hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
   const int npt = (int)((geo.M + TM - 1) / TM);
   const int ncb = a.cout / TN;
   const int64_t T = (int64_t)npt * ncb * a.in.groups;
   if (T <= 0 || T > 0x7fffffff) return hipErrorInvalidValue;
-  const int slots = tile_wgs() * 256 / (WN * WM * 64);  // 512 threads per CU
+  const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S>, WN * WM * 64);
   const int per = (int)std::min<int64_t>((T + slots - 1) / slots, npt);  // runs span <= 2 channel blocks
   const int nwg = (int)(((T + per - 1) / per + 7) / 8 * 8);
   if constexpr (STEM)
@@ -1499,7 +1523,7 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
   tile_override(a, geo, cb, pb);
   if (a.acc_dump || a.out.bits == 3) epi = 1;
   if (epi != 1 && stem_tile_applies(a)) {
-    hipError_t e = launch_tile<2, 2, 2, 2, true, 4>(a, geo, s);
+    hipError_t e = launch_tile<2, 2, 2, 2, true, PALQ_STEM_STAGES>(a, geo, s);
     if (e != hipSuccess || epi == 0) return e;
     return launch_stem<2, 1>(a, geo, 1, s);  // unknown: the general build decides on the device
   }
