@@ -44,6 +44,8 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
 
 // ---------------------------------------------------------------- unpack
@@ -177,9 +179,9 @@ __device__ inline void row_quad(const uint8_t *row, int c0, int bits, int out[4]
   for (int e = 0; e < 4; ++e) out[e] = (int)((v >> (bits * e)) & mask);
 }
 
-// Per-channel requant constants in fp64.  With v = scale * (acc + residual)
+// Per-channel requant constants in fp64.  With v = 2^lscale (acc + residual)
 // (an integer, |v| < 2^31) and t = acc + residual + bias:
-//   s = M 2^-sh / scale,  o = (bias M + 2^(sh-1)) 2^-sh,
+//   s = M 2^-(sh + lscale),  o = (bias M + 2^(sh-1)) 2^-sh,
 //   fma(v, s, o) = (t M + 2^(sh-1)) 2^-sh exactly whenever |t| M < 2^52,
 // so q = clamp(trunc(fma(v, s, o)), 0, qmax) equals the definition (trunc
 // and floor differ only below zero, where both clamp to 0).  The prep kernel
@@ -190,7 +192,7 @@ struct RqConst {
 };
 
 __global__ void requant_prep_kernel(const int32_t *mult, const int32_t *shift, const int32_t *bias,
-                                    const int32_t *res_mult, int res_max, int nch, int scale,
+                                    const int32_t *res_mult, int res_max, int nch, int lscale,
                                     int64_t acc_bound, RqConst *rq, int32_t *flag) {
   __shared__ int any;
   if (threadIdx.x == 0) any = 0;
@@ -210,7 +212,7 @@ __global__ void requant_prep_kernel(const int32_t *mult, const int32_t *shift, c
       if (m > 0 && tmax >= lim / m) bad = 1;
       const int64_t num = b * m + ((int64_t)1 << (sh - 1));  // |b m| < 2^61
       if (num >= lim || num <= -lim) bad = 1;
-      k.s = ldexp((double)m, -sh) / (double)scale;  // scale is a power of two: exact
+      k.s = ldexp((double)m, -sh - lscale);  // the accumulator is 2^lscale (acc + residual): exact
       k.o = ldexp((double)num, -sh);
     }
     rq[c] = k;
@@ -287,6 +289,45 @@ __global__ void prepack_kernel(ConvArgs a, Geo geo, uint8_t *wp) {
   const int j = within >> 6, half = (within >> 5) & 1, ch = within & 31;
   const int gd = (g + a.shuffle) % a.in.groups;
   *(v4i *)(wp + t * 16) = weight_unit<B, STEM>(a, geo, g, gd, cblk * 32 + ch, kb, 2 * half + j);
+}
+
+// FP4 (E2M1) weight slabs for the 2-bit grouped tile kernel, one MFMA
+// (32 x 32 x 64) per K-block: [G][cout/32][kb_total][half][ch][16 B].
+// Nibble n (word q = n / 8, position j = n % 8) of lane (ch, half) holds the
+// K-block's weight code 32 half + 16 (q >> 1) + 2 j + (q & 1) as E2M1 of w / 2
+// (-1, -0.5, 0, 0.5 for w = -2, -1, 0, 1); the activation unpack puts the
+// same code index there (as c / 2), so every product is exact and carries a
+// factor 1/4.  One thread per 16-byte lane operand.
+constexpr int kSlab4 = 1024;
+__global__ void prepack_fp4_kernel(ConvArgs a, Geo geo, uint8_t *wp) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int nc32 = a.cout / 32;
+  const int64_t total = (int64_t)a.in.groups * nc32 * geo.kb_total * 64;
+  if (t >= total) return;
+  const int within = (int)(t & 63);
+  const int64_t rest = t >> 6;
+  const int kb = (int)(rest % geo.kb_total);
+  const int64_t r2 = rest / geo.kb_total;
+  const int cblk = (int)(r2 % nc32);
+  const int g = (int)(r2 / nc32);
+  const int half = within >> 5, k = cblk * 32 + (within & 31);
+  const int gd = (g + a.shuffle) % a.in.groups;
+  const uint8_t *p = kb < geo.kb_main ? a.w + ((int64_t)g * a.cout + k) * geo.w_ch + (int64_t)kb * 16
+                                      : a.proj_w + ((int64_t)gd * a.cout + k) * geo.pw_ch + (int64_t)(kb - geo.kb_main) * 16;
+  const uint32_t u[2] = {((const uint32_t *)p)[2 * half], ((const uint32_t *)p)[2 * half + 1]};
+  uint32_t o[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t src = u[q >> 1] >> (2 * (q & 1));
+    uint32_t w = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t c = (src >> (4 * j)) & 3u;               // 2-bit two's complement code
+      w |= ((0x9A10u >> (4 * c)) & 15u) << (4 * j);           // 0 -> 0, 1 -> 0.5, -2 -> -1, -1 -> -0.5
+    }
+    o[q] = w;
+  }
+  *(uint4 *)(wp + t * 16) = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 // Buffer resource over `bytes` bytes at `base`: loads at an offset >= bytes
@@ -463,8 +504,12 @@ typedef double dbl2 __attribute__((ext_vector_type(2)));
 // Output width BO is a compile-time constant here; fma -> saturating
 // unsigned conversion (negative values and NaN give 0, which is the ReLU
 // clamp) -> min with 2^BO - 1 -> shift into the quad's word.
-template <int BO, int CB, int PB, int RB>
-__device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB],
+// AccV = v16f: the FP4 tile kernel's accumulator, t / 4 held exactly (the
+// constants carry the factor 4); its shortcut term rm c / 4 is added in
+// fp32, exact because the layer's |t| + 3 |rm| stays below 2^24 (a multiple
+// of 1/4 below 2^22 fits the 24-bit significand).
+template <int BO, int CB, int PB, int RB, typename AccV>
+__device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &geo, AccV (&acc)[CB][PB],
                                         const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
                                         int l32, int half, const RqConst *rq, const int32_t *rm) {
   constexpr int bo = BO;
@@ -495,10 +540,15 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
       if constexpr (RB != 0) rmu = *(const v4i *)(rm + cb * 32 + cq);
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb) {
-        int32_t v[4];
+        constexpr bool FACC = std::is_same<AccV, v16f>::value;
+        typename std::conditional<FACC, float, int32_t>::type v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[cb][pb][4 * qi + e];
-        if constexpr (RB == 2) {
+        if constexpr (RB == 2 && FACC) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            v[e] = __builtin_fmaf((float)rmu[e] * 0.25f, (float)chunk_code(rw[cb][pb], cq + e, 2), v[e]);
+        } else if constexpr (RB == 2) {
           // |res_mult| < 2^15 and codes < 4: 24-bit signed products
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] += __mul24(rmu[e] << lsc, chunk_code(rw[cb][pb], cq + e, 2));
@@ -943,25 +993,37 @@ __device__ __forceinline__ void ring_barrier() {
 // (pad 0): a K-block is two filter rows of 8 four-byte taps, 64 bytes per
 // pixel, fetched as four 16-byte pieces (lane half h of the MFMA takes row
 // 2 kb + h, its 8 taps being the two 16-code operand units); no unpack.
-template <int CB, int PB, int WN, int WM, int RB, bool STEM = false, int kStages = PALQ_TILE_STAGES>
+// FP4: 2-bit layers on the FP4 (E2M1) matrix cores, one 32 x 32 x 64 MFMA
+// per K-block and 32-channel block (prepack_fp4_kernel); the activation
+// operand is the packed word split into its even and odd codes (values c / 2),
+// the accumulator fp32 (t / 4, exact: the launcher takes only layers whose
+// accumulator bound is below 2^23, so every partial sum is a multiple of
+// 1/4 below 2^21).
+template <int CB, int PB, int WN, int WM, int RB, bool STEM = false, int kStages = PALQ_TILE_STAGES,
+          bool FP4 = false>
 __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_kernel(ConvArgs a, Geo geo, int npt,
                                                                                       int ncb, int per) {
   constexpr int B = 2;
   constexpr int NT = WN * WM * 64;
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
   constexpr int BLK = STEM ? 64 : Blk<B>::bytes;  // activation bytes of one pixel's K-block
-  constexpr int WST = TN * 64;        // int8 weight bytes of one K-block
+  constexpr int SLAB = FP4 ? kSlab4 : kSlab;  // weight bytes of a (K-block, 32 channels)
+  constexpr int WST = TN / 32 * SLAB;  // weight bytes of one K-block
   constexpr int XST = TM * BLK;       // activation bytes of one K-block
   constexpr int SST = WST + XST;      // one ring stage
-  constexpr int WLD = WST / (NT * 16);  // 16-byte weight loads per thread and K-block
+  constexpr int WP = WST / 16;        // 16-byte weight pieces of a K-block
+  constexpr int WLD = FP4 ? 1 : WP / NT;  // weight loads per loading thread and K-block
   constexpr int XP = XST / 16;          // 16-byte activation pieces of a K-block
   constexpr bool XALL = XP >= NT;       // every thread loads (XLD pieces), else the first XP threads one
   constexpr int XLD = XALL ? XP / NT : 1;
-  static_assert(WLD == 1 || WLD == 2, "weight loads per thread");
+  static_assert(FP4 ? WP == NT / 2 : (WLD == 1 || WLD == 2), "weight loads per thread");
   static_assert(XP == NT / 2 || XP % NT == 0, "activation pieces");
   static_assert(!STEM || (XALL && RB == 0), "stem layout");
-  // loads per K-block of the waves with the fewest (the ring waits on that)
-  constexpr int LPK = WLD + (XALL ? XLD : 0);
+  static_assert(!FP4 || !STEM, "FP4 takes 2-bit grouped layers");
+  // loads per K-block of the waves with the fewest (the ring waits on that).
+  // FP4: the last NT / 2 threads load the weights, the first XP threads (or
+  // all) the activations.
+  constexpr int LPK = FP4 ? (XALL ? XLD : 1) : WLD + (XALL ? XLD : 0);
   constexpr int RQB = 2 * TN * (int)sizeof(RqConst);  // requant constants of two channel blocks
   constexpr int RMB = RB ? 2 * TN * 4 : 0;            // their shortcut multipliers
   constexpr int RPX = TN / 4;                          // shortcut code bytes per pixel of a tile
@@ -1001,7 +1063,7 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   __syncthreads();
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
 
-  const auto rw_src = make_rsrc(geo.wp, (int64_t)G * a.cout * KB * 64);
+  const auto rw_src = make_rsrc(geo.wp, (int64_t)G * a.cout * KB * (SLAB / 32));
   const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
   const auto rpj = a.proj.data ? make_rsrc(a.proj.data, (int64_t)a.proj.n * a.proj.h * a.proj.w * a.proj.pixel)
                                : make_rsrc(a.in.data, 0);
@@ -1026,7 +1088,7 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
     const int cbk = (f_tile / npt) % ncb;
     const int g = f_tile / (npt * ncb);
     const int gd = (g + a.shuffle) % G;
-    wbase = (uint32_t)((((int64_t)g * (a.cout / 32) + cbk * (TN / 32)) * KB) * kSlab);
+    wbase = (uint32_t)((((int64_t)g * (a.cout / 32) + cbk * (TN / 32)) * KB) * SLAB);
     if constexpr (STEM) {
 #pragma unroll
       for (int i = 0; i < XLD; ++i) {
@@ -1085,11 +1147,20 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(rb + wave * 1024), 16, (int)ro, 0, 0, 0);
       }
     }
+    if constexpr (FP4) {
+      if (tid >= NT - WP) {  // wave-uniform: WP is a multiple of 64
+        const int c = tid - (NT - WP);  // piece c: slab c / 64, lane operand c % 64
+        const uint32_t woff = live ? wbase + (uint32_t)((c >> 6) * KB + f_kb) * SLAB + (c & 63) * 16 : kOob;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + (c & ~63) * 16), 16, (int)woff, 0, 0, 0);
+      }
+    } else {
 #pragma unroll
-    for (int i = 0; i < WLD; ++i) {
-      const int c = tid + i * NT;  // piece of the K-block's weights
-      const uint32_t woff = live ? wbase + (uint32_t)((c >> 7) * KB + f_kb) * kSlab + (c & 127) * 16 : kOob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + i * NT * 16 + wave * 1024), 16, (int)woff, 0, 0, 0);
+      for (int i = 0; i < WLD; ++i) {
+        const int c = tid + i * NT;  // piece of the K-block's weights
+        const uint32_t woff = live ? wbase + (uint32_t)((c >> 7) * KB + f_kb) * kSlab + (c & 127) * 16 : kOob;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + i * NT * 16 + wave * 1024), 16, (int)woff, 0, 0,
+                                                 0);
+      }
     }
     if constexpr (STEM) {
 #pragma unroll
@@ -1125,7 +1196,7 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
 
   // ---- compute side: tile c_tile, K-block c_kb
   int c_tile = t_begin, c_kb = 0;
-  v16i acc[CB][PB];
+  typename std::conditional<FP4, v16f, v16i>::type acc[CB][PB];
   // Per tile, at its first K-block: zeroed accumulators.
   auto tile_start = [&]() __attribute__((always_inline)) {
 #pragma unroll
@@ -1165,14 +1236,15 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   // LDS addresses of this lane's operands in stage 0: activation half row
   // of pixel block 0, weight unit (j = 0) of channel block 0
   const uint32_t xaddr0 = lds_base + WST + (uint32_t)((wm * PB * 32 + l32) * BLK + half * (BLK / 2));
-  const uint32_t aaddr0 = lds_base + (uint32_t)((wn * CB) * kSlab + (half * 32 + l32) * 16);
+  const uint32_t aaddr0 = lds_base + (uint32_t)((wn * CB) * SLAB + (half * 32 + l32) * 16);
   // MFMA operands of one K-block: this lane's activation half rows of the two
   // pixel blocks and weight units a[j][cb], read by one asm statement that
   // also waits for them (early-clobber outputs: a result must not land in an
   // address register a later read of the statement still uses).
   struct OpsG { uint2 x0, x1; v4i a00, a01, a10, a11; };
   struct OpsS { v4i x0a, x0b, x1a, x1b, a00, a01, a10, a11; };  // stem: x[pb] words 0-3 / 4-7
-  using Ops = typename std::conditional<STEM, OpsS, OpsG>::type;
+  struct OpsF { uint2 x0, x1; v4i a0, a1; };                     // FP4: a[cb]
+  using Ops = typename std::conditional<STEM, OpsS, typename std::conditional<FP4, OpsF, OpsG>::type>::type;
   auto read_ops = [&](int stage, Ops &o) __attribute__((always_inline)) {
     const uint32_t xa = xaddr0 + stage * SST, aa = aaddr0 + stage * SST;
     if constexpr (STEM) {
@@ -1188,6 +1260,16 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
           "s_waitcnt lgkmcnt(0)"
           : "=&v"(o.x0a), "=&v"(o.x0b), "=&v"(o.x1a), "=&v"(o.x1b), "=&v"(o.a00), "=&v"(o.a01), "=&v"(o.a10),
             "=&v"(o.a11)
+          : "v"(xa), "v"(aa));
+      return;
+    } else if constexpr (FP4) {
+      asm volatile(
+          "ds_read_b64 %0, %4\n\t"
+          "ds_read_b64 %1, %4 offset:512\n\t"
+          "ds_read_b128 %2, %5\n\t"
+          "ds_read_b128 %3, %5 offset:1024\n\t"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(o.x0), "=&v"(o.x1), "=&v"(o.a0), "=&v"(o.a1)
           : "v"(xa), "v"(aa));
       return;
     } else
@@ -1213,6 +1295,27 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
 #pragma unroll
           for (int cb = 0; cb < CB; ++cb)
             acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[j][cb], X[j][pb], acc[cb][pb], 0, 0, 0);
+      return;
+    } else if constexpr (FP4) {
+      // E2M1 operands use the low four registers of each v8i (the rest is
+      // ignored for this format, left undefined here)
+      const uint2 xw[PB] = {o.x0, o.x1};
+      const v4i A[CB] = {o.a0, o.a1};
+      v8i Bop[PB], Aop[CB];
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        const uint32_t m = 0x33333333u;
+        const v4i b = {(int)(xw[pb].x & m), (int)((xw[pb].x >> 2) & m), (int)(xw[pb].y & m),
+                       (int)((xw[pb].y >> 2) & m)};
+        Bop[pb] = __builtin_shufflevector(b, b, 0, 1, 2, 3, -1, -1, -1, -1);
+      }
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) Aop[cb] = __builtin_shufflevector(A[cb], A[cb], 0, 1, 2, 3, -1, -1, -1, -1);
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+          acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop[cb], Bop[pb], acc[cb][pb], 4, 4, 0, 0, 0, 0);
       return;
     } else {
     Raw xr[PB];
@@ -1357,7 +1460,17 @@ int64_t code_max(int bits, int is_signed) {
   return is_signed ? ((int64_t)1 << (bits - 1)) : (((int64_t)1 << bits) - 1);
 }
 
+// Bound on |accumulator|: every product of the main and projection
+// contractions at its largest.
+int64_t acc_bound_of(const ConvArgs &a) {
+  int64_t b = (int64_t)a.kh * a.kw * a.in.cpg * code_max(a.in.bits, a.in.is_signed) * code_max(a.w_bits, 1);
+  if (a.proj.data) b += (int64_t)a.proj.cpg * code_max(a.proj.bits, 0) * code_max(a.w_bits, 1);
+  return b;
+}
+
 }  // namespace
+
+bool fp4_applies(const ConvArgs &a);
 
 bool conv_mfma_supported(const ConvArgs &a) {
   if (a.cout % 32 != 0) return false;
@@ -1379,6 +1492,10 @@ ConvPlan conv_mfma_plan(const ConvArgs &a) {
   const Geo geo = make_geo(a);
   p.w_bytes = (size_t)a.in.groups * a.cout * geo.kb_total * 64;
   p.thr_bytes = (size_t)a.in.groups * a.cout * sizeof(RqConst) + 16;  // + int64-path flag
+  if (fp4_applies(a)) {  // FP4 slabs and constants after the int8 ones (the general build keeps those)
+    p.w_bytes += (size_t)a.in.groups * a.cout * geo.kb_total * 32;
+    p.thr_bytes *= 2;
+  }
   return p;
 }
 
@@ -1398,14 +1515,21 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // accumulator bound: every product of the main and projection contractions
-  int64_t acc_bound = (int64_t)a.kh * a.kw * a.in.cpg * code_max(a.in.bits, a.in.is_signed) * code_max(a.w_bits, 1);
-  if (a.proj.data) acc_bound += (int64_t)a.proj.cpg * code_max(a.proj.bits, 0) * code_max(a.w_bits, 1);
+  const int64_t acc_bound = acc_bound_of(a);
   const int res_max = a.res.data ? (int)code_max(a.res.bits, 0) : 0;
   const int nch = a.in.groups * a.cout;
   RqConst *rq = (RqConst *)thr;
+  const int lscale = geo.scale == 16 ? 4 : 0;  // the int8 accumulator is 16 t for 2-bit codes
   hipLaunchKernelGGL(requant_prep_kernel, dim3(1), dim3(256), 0, s, a.mult, a.shift, a.bias, a.res.data ? a.res_mult : nullptr,
-                     res_max, nch, geo.scale, acc_bound, rq, (int32_t *)(rq + nch));
+                     res_max, nch, lscale, acc_bound, rq, (int32_t *)(rq + nch));
+  e = hipGetLastError();
+  if (e != hipSuccess || !fp4_applies(a)) return e;
+  const int64_t pieces = (int64_t)a.in.groups * (a.cout / 32) * geo.kb_total * 64;
+  hipLaunchKernelGGL(prepack_fp4_kernel, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, s, a, geo,
+                     wp + (size_t)a.in.groups * a.cout * geo.kb_total * 64);
+  RqConst *rq4 = rq + nch + 1;  // the FP4 accumulator is t / 4
+  hipLaunchKernelGGL(requant_prep_kernel, dim3(1), dim3(256), 0, s, a.mult, a.shift, a.bias, a.res.data ? a.res_mult : nullptr,
+                     res_max, nch, -2, acc_bound, rq4, (int32_t *)(rq4 + nch));
   return hipGetLastError();
 }
 
@@ -1476,8 +1600,18 @@ bool tile_kernel_applies(const ConvArgs &a) {
          (!a.res.data || a.res.bits == 2);
 }
 
-// Persistent grid: two workgroups per CU (the kernel's register budget),
-// a multiple of 8 so that every XCD gets the same number of workgroups.
+// FP4 matrix cores for a tiled-kernel layer whose accumulator bound is below
+// 2^23 (the fp32 accumulator then holds every partial sum, and the shortcut
+// term, exactly); PALQ_CONV_FP4=0 keeps such layers on int8.
+bool fp4_applies(const ConvArgs &a) {
+  static int off = -1;
+  if (off < 0) {
+    const char *e = getenv("PALQ_CONV_FP4");
+    off = (e && strcmp(e, "0") == 0) ? 1 : 0;
+  }
+  return !off && tile_kernel_applies(a) && acc_bound_of(a) < ((int64_t)1 << 23);
+}
+
 // The stem on the tiled kernel: explicit zero border (pad 0), 128-channel
 // blocks, no shortcut, fast epilogue.
 bool stem_tile_applies(const ConvArgs &a) {
@@ -1490,25 +1624,25 @@ bool stem_tile_applies(const ConvArgs &a) {
          (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64 < ((int64_t)1 << 30);
 }
 
-template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES>
+template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES, bool FP4 = false>
 hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
   const int npt = (int)((geo.M + TM - 1) / TM);
   const int ncb = a.cout / TN;
   const int64_t T = (int64_t)npt * ncb * a.in.groups;
   if (T <= 0 || T > 0x7fffffff) return hipErrorInvalidValue;
-  const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S>, WN * WM * 64);
+  const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S, FP4>, WN * WM * 64);
   const int per = (int)std::min<int64_t>((T + slots - 1) / slots, npt);  // runs span <= 2 channel blocks
   const int nwg = (int)(((T + per - 1) / per + 7) / 8 * 8);
   if constexpr (STEM)
     hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, true, S>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0, s,
                        a, geo, npt, ncb, per);
   else if (!a.res.data)
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0,
-                       s, a, geo, npt, ncb, per);
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, FP4>), dim3((unsigned)nwg), dim3(WN * WM * 64),
+                       0, s, a, geo, npt, ncb, per);
   else
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0,
-                       s, a, geo, npt, ncb, per);
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4>), dim3((unsigned)nwg), dim3(WN * WM * 64),
+                       0, s, a, geo, npt, ncb, per);
   return hipGetLastError();
 }
 
@@ -1526,6 +1660,16 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
     hipError_t e = launch_tile<2, 2, 2, 2, true, PALQ_STEM_STAGES>(a, geo, s);
     if (e != hipSuccess || epi == 0) return e;
     return launch_stem<2, 1>(a, geo, 1, s);  // unknown: the general build decides on the device
+  }
+  if (epi != 1 && fp4_applies(a)) {
+    const int nch = a.in.groups * a.cout;
+    Geo g4 = geo;
+    g4.wp = wp + (size_t)nch * geo.kb_total * 64;
+    g4.rq = geo.rq + nch + 1;
+    hipError_t e = a.cout % 128 != 0 ? launch_tile<2, 2, 1, 4, false, PALQ_TILE_STAGES, true>(a, g4, s)
+                                     : launch_tile<2, 2, 2, 4, false, PALQ_TILE_STAGES, true>(a, g4, s);
+    if (e != hipSuccess || epi == 0) return e;
+    return dispatch_bits<2>(a, geo, cb, pb, 1, s);  // unknown: the general build decides on the device
   }
   if (epi != 1 && tile_kernel_applies(a)) {
     hipError_t e = a.cout % 128 != 0 ? launch_tile<2, 2, 1, 4>(a, geo, s)
