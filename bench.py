@@ -25,6 +25,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "effective int TOPS + images/s, ResNet-18-shaped G=4 2-bit fwd, batch 64"
 INT8_MFMA_PEAK_TOPS = 5000.0   # MI355X dense int8 MFMA, 5.0 POP/s
+FP4_MFMA_PEAK_TFLOPS = 10100.0  # MI355X dense FP4 MFMA, 10.1 PFLOP/s
 HBM_PEAK_GBS = 8000.0
 
 
@@ -47,12 +48,13 @@ def parse():
     return ap.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_grouped_kernel_resnet18_g4_b2_bs64_traffic.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_tile_kernel_fp4_resnet18_g4_b2_bs64_traffic.txt")
+DOMINANT = "conv_tile_kernel[fp4]"
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2208_01944_amd", "csrc", "k_conv_mfma.hip")
 
 
 def measured_traffic():
-    """HBM bytes per conv_grouped_kernel launch from the committed counter
+    """HBM bytes per launch of the dominant kernel from the committed counter
     summary, or None when the kernel source has changed since the counters
     were taken (the summary records the source's sha256)."""
     import hashlib
@@ -88,6 +90,19 @@ def _short(name):
     return name.replace("void ", "").replace("palq::(anonymous namespace)::", "").split("(")[0]
 
 
+def family(short):
+    """Kernel family of a demangled kernel name: the tiled convolution splits
+    by its template arguments (CB, PB, WN, WM, RB, STEM, stages, FP4) into the
+    stem, the grouped FP4 and the grouped int8 builds."""
+    base = short.split("<")[0]
+    if base != "conv_tile_kernel" or "<" not in short:
+        return base
+    args = [t.strip() for t in short[short.index("<") + 1:short.rindex(">")].split(",")]
+    if args[5] == "true":
+        return "conv_tile_kernel[stem]"
+    return "conv_tile_kernel[fp4]" if len(args) > 7 and args[7] == "true" else "conv_tile_kernel[int8]"
+
+
 def summarize_profile(d):
     """Writes the kernel-time and HBM-traffic summaries of one profiling
     session (rocprofv3 csv output) under profiles/."""
@@ -108,16 +123,16 @@ def summarize_profile(d):
         out.append(f"| {k} | {r['Calls']} | {int(r['TotalDurationNs']) / 1e6:.3f} | "
                    f"{float(r['AverageNs']) / 1e3:.1f} | {int(r['MinNs']) / 1e3:.1f} | {int(r['MaxNs']) / 1e3:.1f} | "
                    f"{float(r['Percentage']):.2f} |")
-        f = fam.setdefault(k.split("<")[0], [0, 0])
+        f = fam.setdefault(family(k), [0, 0])
         f[0] += int(r["Calls"])
         f[1] += int(r["TotalDurationNs"])
-    g = fam["conv_grouped_kernel"]
+    g = fam[DOMINANT]
     rf = bench["roofline"]
-    out += ["", "conv_grouped_kernel, all instantiations: %d calls, average %.1f us per launch" % (g[0], g[1] / g[0] / 1e3),
+    out += ["", "%s, all instantiations: %d calls, average %.1f us per launch" % (DOMINANT, g[0], g[1] / g[0] / 1e3),
             "bench.py HIP events on the library stream, same kernel: average %.1f us per launch over %d launches/step"
             % (rf["avg_launch_us"], rf["launches_per_step"]),
-            "bench.py (plain timed region): %.1f images/s, %.4f ms/step; roofline frac %.4f (%.0f of %.0f int8 TOPS)"
-            % (bench["value"], bench["ms_per_step"], rf["frac"], rf["achieved"], rf["peak"]), "",
+            "bench.py (plain timed region): %.1f images/s, %.4f ms/step; roofline frac %.4f (%.0f of %.0f %s)"
+            % (bench["value"], bench["ms_per_step"], rf["frac"], rf["achieved"], rf["peak"], rf["unit"]), "",
             "Per layer (bench.py HIP events, us per launch):", ""]
     out += ["| layer | op | kernel | us | int ops | alg. bytes |", "|---|---|---|---|---|---|"]
     for L in bench["layers"]:
@@ -135,8 +150,8 @@ def summarize_profile(d):
     ff, fw = probe_kib / (sum(cf) / len(cf)), probe_kib / (sum(cw) / len(cw))
     F, W = load("fetch"), load("write")
     assert [k for k, _ in F] == [k for k, _ in W]
-    gl = [(f * ff * 1024, w * fw * 1024) for (k, f), (_, w) in zip(F, W) if k.startswith("conv_grouped_kernel")]
-    layers = [L for L in bench["layers"] if L.get("kernel") == "conv_grouped_kernel"]
+    gl = [(f * ff * 1024, w * fw * 1024) for (k, f), (_, w) in zip(F, W) if family(k) == DOMINANT]
+    layers = [L for L in bench["layers"] if L.get("kernel") == DOMINANT]
     nl = len(layers)
     assert len(gl) % nl == 0
     nf = len(gl) // nl
@@ -144,8 +159,8 @@ def summarize_profile(d):
     src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
     out = head + ["#   " + PROFILE_CMDS[k] for k in ("fetch", "write", "cfetch", "cwrite")] + [
         "",
-        "HBM traffic of conv_grouped_kernel, ResNet-18 PalQuant G=4 2-bit, batch 64 (%d forwards x %d launches)"
-        % (nf, nl), "",
+        "HBM traffic of %s, ResNet-18 PalQuant G=4 2-bit, batch 64 (%d forwards x %d launches)"
+        % (DOMINANT, nf, nl), "",
         "copy calibration (1 GiB device copy): FETCH_SIZE reads %.1f KiB per launch for 1048576 KiB copied"
         % (sum(cf) / len(cf)),
         "  -> fetch factor %.4f; WRITE_SIZE reads %.1f KiB -> write factor %.4f" % (ff, sum(cw) / len(cw), fw), "",
@@ -155,7 +170,7 @@ def summarize_profile(d):
         w = sum(gl[j * nl + i][1] for j in range(nf)) / nf
         out.append(f"| {L['layer']} | {L['bytes'] / 1e6:.2f} | {r / 1e6:.2f} | {w / 1e6:.2f} | "
                    f"{(r + w) / L['bytes']:.2f} |")
-    out += ["", "kernel: conv_grouped_kernel",
+    out += ["", "kernel: " + DOMINANT,
             "kernel_source_sha256: " + src,
             "hbm_bytes_per_launch: %.0f" % per_launch,
             "algorithmic_bytes_per_launch: %.0f" % rf["algorithmic_bytes_per_launch"]]
@@ -173,6 +188,25 @@ def copy_probe(mib):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 3}))
+
+
+def conv_kernel(L, ci, co, k):
+    """Which kernel family the library's selection rules give a conv layer of
+    this workload (the stem and 2-bit grouped layers take the tiled kernel;
+    2-bit layers run on FP4 matrix cores unless PALQ_CONV_FP4=0)."""
+    stem = L["in_bits"] == 8 and L["in_signed"] and L["w_bits"] == 8 and ci <= 4 and k <= 8
+    if stem:
+        tiled = co % 128 == 0 and L.get("res", -1) < 0 and L["out_bits"] == 2
+        return "conv_tile_kernel[stem]" if tiled else "conv_stem_kernel"
+    grouped = co % 32 == 0 and ci % 64 == 0 and L["in_bits"] == L["w_bits"] and not L["in_signed"]
+    if not grouped:
+        return "conv_direct_kernel"
+    tiled = L["in_bits"] == 2 and co % 64 == 0 and L["out_bits"] == 2
+    if not tiled:
+        return "conv_grouped_kernel"
+    bound = k * k * ci * 3 * 2 + (L["proj_w"].shape[-1] * 3 * 2 if L.get("proj_w") is not None else 0)
+    fp4 = os.environ.get("PALQ_CONV_FP4", "1") != "0" and bound < (1 << 23)
+    return "conv_tile_kernel[fp4]" if fp4 else "conv_tile_kernel[int8]"
 
 
 def cpu_baseline(spec, x_f32, l, u, budget_s):
@@ -276,10 +310,7 @@ def main():
             if L.get("proj_src", -1) >= 0:
                 r = shapes[L["proj_src"]]
                 nbytes += act_bytes(r[0], r[1], r[2], r[3]) + L["proj_w"].size * L["w_bits"] / 8
-            stem = L["in_bits"] == 8 and L["in_signed"] and L["w_bits"] == 8 and ci <= 4 and k <= 8
-            grouped = co % 32 == 0 and ci % 64 == 0 and L["in_bits"] == L["w_bits"] and not L["in_signed"]
-            kname = "conv_stem_kernel" if stem and co % 32 == 0 else \
-                "conv_grouped_kernel" if grouped else "conv_direct_kernel"
+            kname = conv_kernel(L, ci, co, k)
             per_layer.append(dict(layer=i, op="conv", kernel=kname, ops=ops, bytes=nbytes,
                                   ms=float(layer_ms[i])))
         else:
@@ -300,13 +331,16 @@ def main():
     total_ops = net.ops
     img_s = n / (ms_per_step / 1e3)
     tops = total_ops / (ms_per_step / 1e3) / 1e12
-    # the dominant kernel: the grouped B-bit conv (3x3 convs of the residual
-    # blocks, projections fused), 16 launches per step
-    D = kern["conv_grouped_kernel"]
+    # the dominant kernel: the grouped 2-bit conv (3x3 convs of the residual
+    # blocks, projections fused), 16 launches per step, on FP4 matrix cores
+    # (int8 with PALQ_CONV_FP4=0); its peak is that of the format it runs on
+    dom = DOMINANT if DOMINANT in kern else "conv_tile_kernel[int8]"
+    D = kern[dom]
+    peak = FP4_MFMA_PEAK_TFLOPS if dom == DOMINANT else INT8_MFMA_PEAK_TOPS
     launch_ms = D["ms"] / D["launches"]
     ops_per_launch = D["ops"] / D["launches"]
     achieved = ops_per_launch / (launch_ms / 1e3) / 1e12
-    traffic = measured_traffic()
+    traffic = measured_traffic() if dom == DOMINANT else None
     res = {
         "metric": METRIC,
         "value": img_s,
@@ -318,15 +352,15 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "int8",
+        "dtype": "fp4+int8" if dom == DOMINANT else "int8",
         "data": "synthetic (seeded uniform codes and random fp32 images, random weights)",
         "config": {"workload": "resnet18_palq_G4_b2_224_fwd", "global_batch": n, "image": [224, 224, 3],
                    "groups": 4, "bits": 2, "step": "quantize fp32 input + palq_forward"},
         "effective_tops": tops,
         "int_ops_per_step": total_ops,
-        "roofline": {"bound": "mfma", "achieved": achieved, "peak": INT8_MFMA_PEAK_TOPS,
-                     "unit": "TFLOP/s", "frac": achieved / INT8_MFMA_PEAK_TOPS, "traffic": traffic,
-                     "kernel": "conv_grouped_kernel", "launches_per_step": D["launches"],
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak,
+                     "unit": "TFLOP/s", "frac": achieved / peak, "traffic": traffic,
+                     "kernel": dom, "launches_per_step": D["launches"],
                      "avg_launch_us": launch_ms * 1e3, "int_ops_per_launch": ops_per_launch,
                      "algorithmic_bytes_per_launch": D["bytes"] / D["launches"],
                      "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"},

@@ -120,6 +120,14 @@ typedef struct {
 palq_status palq_create(int32_t device, void *hip_stream, palq_ctx **out);
 void palq_destroy(palq_ctx *ctx);
 palq_status palq_set_stream(palq_ctx *ctx, void *hip_stream);
+/* Matrix-core format of 2-bit grouped convolutions (Section 4.1): with
+ * enable = 1 (the default; environment PALQ_CONV_FP4=0 starts a context at
+ * 0) a layer whose accumulator bound sum |w| |x| stays below 2^23 runs on the
+ * FP4 (E2M1) matrix cores, where its fp32 accumulator is exact; with 0 every
+ * layer runs on int8.  Results are identical either way.  Applies to
+ * palq_group_conv calls and networks created after the call.
+ * PALQ_ERR_ARG: enable not 0 or 1. */
+palq_status palq_set_conv_fp4(palq_ctx *ctx, int32_t enable);
 /* Waits for all work on the context's stream; reports deferred device errors. */
 palq_status palq_sync(palq_ctx *ctx);
 /* Reason for the last failed call on ctx; owned by ctx, valid until its next call. */

@@ -989,6 +989,38 @@ __device__ __forceinline__ void ring_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Tile order of the tiled kernel.  The npt pixel tiles are cut into nch
+// chunks (1 <= nch <= npt; chunk c: tiles b_c .. b_(c+1) - 1 with
+// b_c = c npt / nch); the tile index runs over chunks, then (group, channel
+// block) combos, then the chunk's pixel tiles.  The workgroups of one XCD
+// take a contiguous range of indices: with nch = 8 about one chunk with all
+// its groups (a pixel's groups share its cache lines, which that XCD's L2
+// then fetches once), with nch = 1 a few combos over all pixels (each XCD
+// reads only its combos' weights).  Runs of at most npt / nch tiles touch
+// at most two (chunk, combo) segments.
+struct TileIt {
+  int pt, combo;  // pixel tile, combo g * ncb + cbk
+  int c, b, e;    // chunk and its pixel tiles b .. e - 1
+};
+__device__ __forceinline__ TileIt tile_at(int t, int npt, int ncombo, int nch) {
+  const int u = t / ncombo;
+  const int c = min(((u + 1) * nch + npt - 1) / npt - 1, nch - 1);  // last chunk with b_c <= u
+  const int b = c * npt / nch, e = (c + 1) * npt / nch;
+  const int r = t - ncombo * b;
+  return {b + r % (e - b), r / (e - b), c, b, e};
+}
+// The tile after `it` in the same order (past the last: pt >= npt).
+__device__ __forceinline__ void tile_next(TileIt &it, int npt, int ncombo, int nch) {
+  if (++it.pt < it.e) return;
+  it.pt = it.b;
+  if (++it.combo < ncombo) return;
+  it.combo = 0;
+  ++it.c;
+  it.b = it.e;
+  it.pt = it.b;
+  it.e = it.c < nch ? (it.c + 1) * npt / nch : npt + 1;
+}
+
 // STEM: the 8-bit first layer on an input whose zero border is explicit
 // (pad 0): a K-block is two filter rows of 8 four-byte taps, 64 bytes per
 // pixel, fetched as four 16-byte pieces (lane half h of the MFMA takes row
@@ -1002,7 +1034,7 @@ __device__ __forceinline__ void ring_barrier() {
 template <int CB, int PB, int WN, int WM, int RB, bool STEM = false, int kStages = PALQ_TILE_STAGES,
           bool FP4 = false>
 __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_kernel(ConvArgs a, Geo geo, int npt,
-                                                                                      int ncb, int per) {
+                                                                                      int ncb, int per, int nch) {
   constexpr int B = 2;
   constexpr int NT = WN * WM * 64;
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
@@ -1040,7 +1072,8 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   const int l32 = lane & 31, half = lane >> 5;
   const int wn = wave / WM, wm = wave % WM;
 
-  // this workgroup's run of tiles; tile = (g * ncb + cbk) * npt + pt
+  // this workgroup's run of tiles (tile_id: pixel tile and combo
+  // g * ncb + cbk)
   const int G = a.in.groups;
   const int T = npt * ncb * G;
   const int nwg = (int)gridDim.x;  // a multiple of 8
@@ -1051,11 +1084,12 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   const int KB = geo.kb_total;
   const int total = (t_end - t_begin) * KB;  // K-blocks this workgroup runs
 
-  // requant constants of the channel blocks (g, cbk) = combo c0 and c0 + 1
-  // (a run spans at most two: the launcher keeps per <= npt)
-  const int c0 = t_begin / npt;
+  // requant constants of the run's first and last combo (slots 0 and 1; a
+  // run spans at most two: the launcher keeps per <= npt / nch)
+  const int combo0 = tile_at(t_begin, npt, ncb * G, nch).combo;
+  const int combo1 = tile_at(t_end - 1, npt, ncb * G, nch).combo;
   for (int c = tid; c < 2 * TN; c += NT) {
-    const int combo = min(c0 + c / TN, ncb * G - 1);
+    const int combo = c < TN ? combo0 : combo1;
     const int cbk = combo % ncb, g = combo / ncb;
     rq_area[c] = geo.rq[(int64_t)g * a.cout + cbk * TN + c % TN];
     if constexpr (RB != 0) rm_area[c] = a.res_mult[(int64_t)g * a.cout + cbk * TN + c % TN];
@@ -1078,15 +1112,16 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   const int xp = tid, xb = 0;
   typedef __attribute__((address_space(3))) void *lds_ptr;
   int f_tile = t_begin, f_kb = 0, f_tap = 0, f_cblk = 0, f_kx = 0, f_ky = 0, f_tapoff = 0;
+  TileIt f_it = tile_at(t_begin, npt, ncb * G, nch);
   uint32_t wbase, tmask;
   int off0, poff;
   // stem: piece tid + i NT is quarter (tid & 3) of pixel tid / 4 + i NT / 4:
   // filter row 2 kb + ((tid >> 1) & 1), bytes 16 (tid & 1) ..
   int soff[XLD];
   auto tile_geometry = [&]() __attribute__((always_inline)) {
-    const int pt = f_tile % npt;
-    const int cbk = (f_tile / npt) % ncb;
-    const int g = f_tile / (npt * ncb);
+    const int pt = f_it.pt;
+    const int cbk = f_it.combo % ncb;
+    const int g = f_it.combo / ncb;
     const int gd = (g + a.shuffle) % G;
     wbase = (uint32_t)((((int64_t)g * (a.cout / 32) + cbk * (TN / 32)) * KB) * SLAB);
     if constexpr (STEM) {
@@ -1136,9 +1171,9 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
     uint8_t *ws = lds + st * SST;
     if constexpr (RB == 2) {
       if (f_kb == 0) {  // the tile's shortcut codes, 16 bytes per thread
-        const int pt = f_tile % npt;
-        const int cbk = (f_tile / npt) % ncb;
-        const int gd = (f_tile / (npt * ncb) + a.shuffle) % G;
+        const int pt = f_it.pt;
+        const int cbk = f_it.combo % ncb;
+        const int gd = (f_it.combo / ncb + a.shuffle) % G;
         const int m = pt * TM + tid / (RPX / 16);
         const uint32_t ro = live && m < geo.M
                                 ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.row + cbk * RPX + (tid % (RPX / 16)) * 16)
@@ -1190,12 +1225,14 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
     if (++f_kb == KB) {
       f_kb = f_tap = f_cblk = f_kx = f_ky = f_tapoff = 0;
       ++f_tile;
+      tile_next(f_it, npt, ncb * G, nch);
       tile_geometry();
     }
   };
 
   // ---- compute side: tile c_tile, K-block c_kb
   int c_tile = t_begin, c_kb = 0;
+  TileIt c_it = tile_at(t_begin, npt, ncb * G, nch);
   typename std::conditional<FP4, v16f, v16i>::type acc[CB][PB];
   // Per tile, at its first K-block: zeroed accumulators.
   auto tile_start = [&]() __attribute__((always_inline)) {
@@ -1207,9 +1244,9 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
         for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0;
   };
   auto tile_end = [&]() __attribute__((always_inline)) {
-    const int pt = c_tile % npt;
-    const int cbk = (c_tile / npt) % ncb;
-    const int g = c_tile / (npt * ncb);
+    const int pt = c_it.pt;
+    const int cbk = c_it.combo % ncb;
+    const int g = c_it.combo / ncb;
     const int gd = (g + a.shuffle) % G;
     uint32_t rw[CB][PB][2] = {};
     if constexpr (RB == 2) {  // this lane's shortcut codes: pixel block pb, channel block cb
@@ -1229,7 +1266,7 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
       rw[0][1][0] = r10.x; rw[0][1][1] = r10.y;
       rw[1][1][0] = r11.x; rw[1][1][1] = r11.y;
     }
-    const int rec = (c_tile / npt - c0) * TN + wn * CB * 32;  // first record of this wave's channels
+    const int rec = (c_it.combo == combo0 ? 0 : TN) + wn * CB * 32;  // first record of this wave's channels
     epilogue_fast_bo<2, CB, PB, RB>(a, geo, acc, rw, (int64_t)pt * TM + wm * PB * 32, g, gd,
                                     cbk * TN + wn * CB * 32, l32, half, rq_area + rec, rm_area + (RB ? rec : 0));
   };
@@ -1352,6 +1389,7 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
       tile_end();
       c_kb = 0;
       ++c_tile;
+      tile_next(c_it, npt, ncb * G, nch);
     }
   }
 }
@@ -1602,14 +1640,9 @@ bool tile_kernel_applies(const ConvArgs &a) {
 
 // FP4 matrix cores for a tiled-kernel layer whose accumulator bound is below
 // 2^23 (the fp32 accumulator then holds every partial sum, and the shortcut
-// term, exactly); PALQ_CONV_FP4=0 keeps such layers on int8.
+// term, exactly), unless the context keeps layers on int8 (a.fp4 = 0).
 bool fp4_applies(const ConvArgs &a) {
-  static int off = -1;
-  if (off < 0) {
-    const char *e = getenv("PALQ_CONV_FP4");
-    off = (e && strcmp(e, "0") == 0) ? 1 : 0;
-  }
-  return !off && tile_kernel_applies(a) && acc_bound_of(a) < ((int64_t)1 << 23);
+  return a.fp4 && tile_kernel_applies(a) && acc_bound_of(a) < ((int64_t)1 << 23);
 }
 
 // The stem on the tiled kernel: explicit zero border (pad 0), 128-channel
@@ -1632,17 +1665,24 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   const int64_t T = (int64_t)npt * ncb * a.in.groups;
   if (T <= 0 || T > 0x7fffffff) return hipErrorInvalidValue;
   const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S, FP4>, WN * WM * 64);
-  const int per = (int)std::min<int64_t>((T + slots - 1) / slots, npt);  // runs span <= 2 channel blocks
+  // Pixel chunks (tile_at): 8, so that an XCD fetches each input line once
+  // for all groups, unless the filter is the larger read (every XCD then
+  // reads all of it): about 7 W extra against (G - 1) X saved.
+  const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * (FP4 ? 32 : 64);
+  const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
+  const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(8, npt) : 1;
+  // runs span <= 2 (chunk, combo) segments
+  const int per = (int)std::min<int64_t>((T + slots - 1) / slots, npt / nch);
   const int nwg = (int)(((T + per - 1) / per + 7) / 8 * 8);
   if constexpr (STEM)
     hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, true, S>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0, s,
-                       a, geo, npt, ncb, per);
+                       a, geo, npt, ncb, per, nch);
   else if (!a.res.data)
     hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, FP4>), dim3((unsigned)nwg), dim3(WN * WM * 64),
-                       0, s, a, geo, npt, ncb, per);
+                       0, s, a, geo, npt, ncb, per, nch);
   else
     hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4>), dim3((unsigned)nwg), dim3(WN * WM * 64),
-                       0, s, a, geo, npt, ncb, per);
+                       0, s, a, geo, npt, ncb, per, nch);
   return hipGetLastError();
 }
 

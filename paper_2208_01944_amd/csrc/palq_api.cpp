@@ -3,6 +3,7 @@
 // checks pass.
 #include <math.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <new>
@@ -102,6 +103,7 @@ palq_status palq_create(int32_t device, void *hip_stream, palq_ctx **out) {
   if (!ctx) return PALQ_ERR_NOMEM;
   ctx->device = device;
   ctx->stream = (hipStream_t)hip_stream;
+  if (const char *e = getenv("PALQ_CONV_FP4")) ctx->conv_fp4 = strcmp(e, "0") != 0;
   if (device >= 0) {
     int count = 0;
     hipError_t e = hipGetDeviceCount(&count);
@@ -134,6 +136,12 @@ void palq_destroy(palq_ctx *ctx) {
 palq_status palq_set_stream(palq_ctx *ctx, void *hip_stream) {
   if (!ctx) return PALQ_ERR_ARG;
   ctx->stream = (hipStream_t)hip_stream;
+  return PALQ_OK;
+}
+
+palq_status palq_set_conv_fp4(palq_ctx *ctx, int32_t enable) {
+  if (!ctx || (enable != 0 && enable != 1)) return PALQ_ERR_ARG;
+  ctx->conv_fp4 = enable;
   return PALQ_OK;
 }
 
@@ -296,6 +304,7 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
   a.ho = (int32_t)ho; a.wo = (int32_t)wo;
   a.mult = rq->mult; a.shift = rq->shift; a.bias = rq->bias;
   a.shuffle = (int32_t)(((int64_t)shuffle_steps % w->groups + w->groups) % w->groups);
+  a.fp4 = ctx->conv_fp4;
   if (rid) { a.res = view_of(rid); a.res_mult = res->res_mult; }
   if (pin) { a.proj = view_of(pin); a.proj_w = (const uint8_t *)pw->data; a.proj_stride = res->proj_stride; }
   a.acc_dump = acc_dump;

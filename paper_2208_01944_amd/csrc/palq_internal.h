@@ -67,6 +67,7 @@ struct ConvArgs {
   const uint8_t *proj_w;
   int32_t proj_stride;
   int32_t *acc_dump;     // may be null
+  int32_t fp4;           // 1: 2-bit layers may run on the FP4 matrix cores (where exact)
 };
 
 // Kernel launchers (return hipError_t of the launch).
@@ -124,4 +125,5 @@ struct palq_ctx {
   size_t conv_scratch_bytes = 0;
   int8_t *fc_scratch = nullptr;    // digit planes of the last FC call
   size_t fc_scratch_bytes = 0;
+  int conv_fp4 = 1;                // palq_set_conv_fp4 (initial value: PALQ_CONV_FP4, default 1)
 };

@@ -298,6 +298,7 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       a.proj_w = L.proj_src >= 0 ? cp(off_pw[i], L.proj_w.data, (int64_t)L.proj_w.groups * L.proj_w.cout_pg * row_bytes(L.proj_w.cin_pg, L.proj_w.bits)) : nullptr;
       a.cout = L.w.cout_pg; a.kh = L.w.kh; a.kw = L.w.kw; a.stride = L.stride; a.pad = L.pad;
       a.w_bits = L.w.bits;
+      a.fp4 = ctx->conv_fp4;
       a.ho = NL.out_view.h; a.wo = NL.out_view.w;
       a.shuffle = (int32_t)(((int64_t)L.shuffle_steps % L.w.groups + L.w.groups) % L.w.groups);
       a.proj_stride = L.proj_stride;

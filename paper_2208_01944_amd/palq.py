@@ -74,6 +74,7 @@ _create = _sig("palq_create", c_i32, c_i32, c_p, ctypes.POINTER(c_p))
 _destroy = _sig("palq_destroy", None, c_p)
 _set_stream = _sig("palq_set_stream", c_i32, c_p, c_p)
 _sync = _sig("palq_sync", c_i32, c_p)
+_set_conv_fp4 = _sig("palq_set_conv_fp4", c_i32, c_p, c_i32)
 _last_error = _sig("palq_last_error", ctypes.c_char_p, c_p)
 _version = _sig("palq_version", ctypes.c_char_p)
 _row_bytes = _sig("palq_row_bytes", c_i64, c_i32, c_i32)
@@ -96,7 +97,7 @@ _net_ops = _sig("palq_net_ops", c_i64, c_p)
 _net_layer_times = _sig("palq_net_layer_times", c_i32, c_p, ctypes.POINTER(c_f), ctypes.POINTER(c_i32))
 _net_reset_times = _sig("palq_net_reset_times", c_i32, c_p)
 
-EXPORTS = ["palq_create", "palq_destroy", "palq_set_stream", "palq_sync", "palq_last_error",
+EXPORTS = ["palq_create", "palq_destroy", "palq_set_stream", "palq_set_conv_fp4", "palq_sync", "palq_last_error",
            "palq_version", "palq_row_bytes", "palq_act_bytes", "palq_pack", "palq_unpack",
            "palq_quantize", "palq_group_conv", "palq_cyclic_shuffle", "palq_maxpool",
            "palq_avgsum", "palq_fc", "palq_net_create", "palq_net_destroy", "palq_forward",
@@ -178,6 +179,10 @@ class Context:
 
     def sync(self):
         self._check(_sync(self.h))
+
+    def set_conv_fp4(self, enable: bool):
+        """FP4 matrix cores for exact 2-bit layers (True) or int8 only."""
+        self._check(_set_conv_fp4(self.h, int(bool(enable))))
 
     # ----------------------------------------------------------- memory
     def empty_act(self, n, h, w, groups, cpg, bits, signed=False) -> Tensor:

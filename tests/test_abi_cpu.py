@@ -143,6 +143,10 @@ def test_validate_only_other_calls(P, vctx):
     assert P._fc(vctx.h, _fake(9), 4, 128, _fake(11), 10, _fake(12)) == P.OK
     assert P._fc(vctx.h, _fake(9), 4, 0, _fake(11), 10, _fake(12)) == P.ERR_ARG
     assert P._pack(vctx.h, None, ctypes.byref(a)) == P.ERR_ARG
+    assert P._set_conv_fp4(vctx.h, 0) == P.OK
+    assert P._set_conv_fp4(vctx.h, 1) == P.OK
+    assert P._set_conv_fp4(vctx.h, 2) == P.ERR_ARG
+    assert P._set_conv_fp4(None, 1) == P.ERR_ARG
 
 
 def _layer(P, **kw):

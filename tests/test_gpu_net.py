@@ -58,6 +58,20 @@ def test_resnet18_small_all_tensors(ctx, torch, variant):
     np.testing.assert_array_equal(logits, ref)
 
 
+def test_resnet18_small_int8_matrix_cores(ctx, torch):
+    say("resnet18 hw=64 n=2 G=4 b=2 centred, int8 only")
+    spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=14)
+    spec = O.calibrate_centring(spec, spec["x"])
+    ctx.set_conv_fp4(False)
+    try:
+        net, logits = gpu_forward(ctx, torch, spec, keep=True)
+    finally:
+        ctx.set_conv_fp4(True)
+    ref, tensors, _ = O.run_net(spec, spec["x"], keep=True)
+    compare_tensors(ctx, net, spec, tensors, slice(None))
+    np.testing.assert_array_equal(logits, ref)
+
+
 def test_resnet50_small_all_tensors(ctx, torch):
     say("resnet50 hw=64 n=2 G=2 b=2 centred")
     spec = I.resnet50(n=2, groups=2, bits=2, hw=64, classes=50, seed=12)

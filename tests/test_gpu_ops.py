@@ -173,6 +173,19 @@ def test_conv_cases(ctx, torch, i, shuffle):
     check_conv(ctx, torch, case, centred=(shuffle == 1))
 
 
+@pytest.mark.parametrize("i", [0, 1, 2, 5, 9, 10])
+def test_conv_cases_int8_matrix_cores(ctx, torch, i):
+    """The 2-bit cases with the FP4 matrix cores switched off (int8 only)."""
+    p = dict(CONV_CASES[i])
+    say(f"conv case {i} {p} int8 only")
+    case = I.single_layer(1000 + i, shuffle=1, **p)
+    ctx.set_conv_fp4(False)
+    try:
+        check_conv(ctx, torch, case, centred=True)
+    finally:
+        ctx.set_conv_fp4(True)
+
+
 def test_conv_stem_shape(ctx, torch):
     """8-bit signed input, 3 channels, 7x7/s2/p3 (the network's first layer)."""
     say("conv stem 8-bit 7x7/s2")
@@ -190,13 +203,19 @@ def test_conv_empty_batch(ctx, torch):
     assert q.size == 0 and racc.size == 0
 
 
+@pytest.mark.parametrize("fp4", [True, False])
 @pytest.mark.parametrize("layer", range(4))
-def test_conv_c2_full_batch_sampled(ctx, torch, layer):
+def test_conv_c2_full_batch_sampled(ctx, torch, layer, fp4):
     """Each ResNet-18 stage shape at G=4, batch 32, in the launch the benchmark
-    uses; the oracle checks the first and last image."""
-    say(f"conv C2 layer {layer} batch 32")
+    uses (FP4 matrix cores, and int8 only); the oracle checks the first and
+    last image."""
+    say(f"conv C2 layer {layer} batch 32 fp4={fp4}")
     case = I.config_c2(layer)
-    full = run_conv_full(ctx, torch, case)
+    ctx.set_conv_fp4(fp4)
+    try:
+        full = run_conv_full(ctx, torch, case)
+    finally:
+        ctx.set_conv_fp4(True)
     for img in (0, 31):
         sub = dict(case, x=case["x"][img:img + 1])
         _, _, rq, racc = run_conv(ctx, torch, sub)
