@@ -1044,18 +1044,18 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   constexpr int XST = TM * BLK;       // activation bytes of one K-block
   constexpr int SST = WST + XST;      // one ring stage
   constexpr int WP = WST / 16;        // 16-byte weight pieces of a K-block
-  constexpr int WLD = FP4 ? 1 : WP / NT;  // weight loads per loading thread and K-block
+  constexpr int WLD = FP4 && WP < NT ? 1 : WP / NT;  // weight loads per loading thread and K-block
   constexpr int XP = XST / 16;          // 16-byte activation pieces of a K-block
   constexpr bool XALL = XP >= NT;       // every thread loads (XLD pieces), else the first XP threads one
   constexpr int XLD = XALL ? XP / NT : 1;
-  static_assert(FP4 ? WP == NT / 2 : (WLD == 1 || WLD == 2), "weight loads per thread");
+  static_assert(FP4 ? (WP == NT / 2 || WP == NT || WP == 2 * NT) : (WLD == 1 || WLD == 2), "weight loads per thread");
   static_assert(XP == NT / 2 || XP % NT == 0, "activation pieces");
   static_assert(!STEM || (XALL && RB == 0), "stem layout");
   static_assert(!FP4 || !STEM, "FP4 takes 2-bit grouped layers");
   // loads per K-block of the waves with the fewest (the ring waits on that).
-  // FP4: the last NT / 2 threads load the weights, the first XP threads (or
-  // all) the activations.
-  constexpr int LPK = FP4 ? (XALL ? XLD : 1) : WLD + (XALL ? XLD : 0);
+  // FP4: the last WP threads load one weight piece each (WP < NT), or all
+  // WLD pieces; the first XP threads (or all) the activations.
+  constexpr int LPK = FP4 && WP < NT ? (XALL ? XLD : 1) : WLD + (XALL ? XLD : 0);
   constexpr int RQB = 2 * TN * (int)sizeof(RqConst);  // requant constants of two channel blocks
   constexpr int RMB = RB ? 2 * TN * 4 : 0;            // their shortcut multipliers
   constexpr int RPX = TN / 4;                          // shortcut code bytes per pixel of a tile
@@ -1182,7 +1182,14 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(rb + wave * 1024), 16, (int)ro, 0, 0, 0);
       }
     }
-    if constexpr (FP4) {
+    if constexpr (FP4 && WP >= NT) {
+#pragma unroll
+      for (int i = 0; i < WLD; ++i) {
+        const int c = tid + i * NT;  // piece c: slab c / 64, lane operand c % 64
+        const uint32_t woff = live ? wbase + (uint32_t)((c >> 6) * KB + f_kb) * SLAB + (c & 63) * 16 : kOob;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + (c & ~63) * 16), 16, (int)woff, 0, 0, 0);
+      }
+    } else if constexpr (FP4) {
       if (tid >= NT - WP) {  // wave-uniform: WP is a multiple of 64
         const int c = tid - (NT - WP);  // piece c: slab c / 64, lane operand c % 64
         const uint32_t woff = live ? wbase + (uint32_t)((c >> 6) * KB + f_kb) * SLAB + (c & 63) * 16 : kOob;
@@ -1582,13 +1589,14 @@ int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr) {
   return flag != 0 ? 1 : 0;
 }
 
-// Pixel tile of the tiled kernel for 128-channel blocks (PALQ_TILE_TM=128
-// or 256).
+// Pixel tile of the tiled kernel for 128-channel blocks, for tuning
+// (PALQ_TILE_TM = 64, 128 or 256; 0 = the build's default).
 int tile_tm() {
   static int v = -1;
   if (v < 0) {
-    v = 256;
-    if (const char *e = getenv("PALQ_TILE_TM")) v = atoi(e) == 128 ? 128 : 256;
+    v = 0;
+    if (const char *e = getenv("PALQ_TILE_TM")) v = atoi(e);
+    if (v != 64 && v != 128 && v != 256) v = 0;
   }
   return v;
 }
@@ -1706,14 +1714,25 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
     Geo g4 = geo;
     g4.wp = wp + (size_t)nch * geo.kb_total * 64;
     g4.rq = geo.rq + nch + 1;
-    hipError_t e = a.cout % 128 != 0 ? launch_tile<2, 2, 1, 4, false, PALQ_TILE_STAGES, true>(a, g4, s)
-                                     : launch_tile<2, 2, 2, 4, false, PALQ_TILE_STAGES, true>(a, g4, s);
+    // pixel tile: 128 (256 / 64 for tuning via PALQ_TILE_TM); 64-channel
+    // layers: TM = 256 or (PALQ_TILE_TM64=128) 128
+    static int tm64 = -1;
+    if (tm64 < 0) {
+      const char *e = getenv("PALQ_TILE_TM64");
+      tm64 = e && atoi(e) == 128 ? 128 : 256;
+    }
+    const int tm = tile_tm() ? tile_tm() : 128;
+    hipError_t e = a.cout % 128 != 0 ? (tm64 == 128 ? launch_tile<2, 2, 1, 2, false, PALQ_TILE_STAGES, true>(a, g4, s)
+                                                    : launch_tile<2, 2, 1, 4, false, PALQ_TILE_STAGES, true>(a, g4, s))
+                   : tm == 64  ? launch_tile<2, 2, 2, 1, false, PALQ_TILE_STAGES, true>(a, g4, s)
+                   : tm == 128 ? launch_tile<2, 2, 2, 2, false, PALQ_TILE_STAGES, true>(a, g4, s)
+                               : launch_tile<2, 2, 2, 4, false, PALQ_TILE_STAGES, true>(a, g4, s);
     if (e != hipSuccess || epi == 0) return e;
     return dispatch_bits<2>(a, geo, cb, pb, 1, s);  // unknown: the general build decides on the device
   }
   if (epi != 1 && tile_kernel_applies(a)) {
     hipError_t e = a.cout % 128 != 0 ? launch_tile<2, 2, 1, 4>(a, geo, s)
-                   : tile_tm() == 128 ? launch_tile<2, 2, 2, 2>(a, geo, s)
+                   : tile_tm() == 128 || tile_tm() == 64 ? launch_tile<2, 2, 2, 2>(a, geo, s)
                                       : launch_tile<2, 2, 2, 4>(a, geo, s);
     if (e != hipSuccess || epi == 0) return e;
     return dispatch_bits<2>(a, geo, cb, pb, 1, s);  // unknown: the general build decides on the device
