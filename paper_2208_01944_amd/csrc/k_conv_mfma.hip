@@ -1031,9 +1031,10 @@ __device__ __forceinline__ void tile_next(TileIt &it, int npt, int ncombo, int n
 // the accumulator fp32 (t / 4, exact: the launcher takes only layers whose
 // accumulator bound is below 2^23, so every partial sum is a multiple of
 // 1/4 below 2^21).
+// KPI: K-blocks per ring stage (one wait and barrier per stage).
 template <int CB, int PB, int WN, int WM, int RB, bool STEM = false, int kStages = PALQ_TILE_STAGES,
-          bool FP4 = false>
-__global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_kernel(ConvArgs a, Geo geo, int npt,
+          bool FP4 = false, int KPI = 1>
+__global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, Geo geo, int npt,
                                                                                       int ncb, int per, int nch) {
   constexpr int B = 2;
   constexpr int NT = WN * WM * 64;
@@ -1042,7 +1043,8 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   constexpr int SLAB = FP4 ? kSlab4 : kSlab;  // weight bytes of a (K-block, 32 channels)
   constexpr int WST = TN / 32 * SLAB;  // weight bytes of one K-block
   constexpr int XST = TM * BLK;       // activation bytes of one K-block
-  constexpr int SST = WST + XST;      // one ring stage
+  constexpr int SSB = WST + XST;      // one K-block of a ring stage
+  constexpr int SST = KPI * SSB;      // one ring stage
   constexpr int WP = WST / 16;        // 16-byte weight pieces of a K-block
   constexpr int WLD = FP4 && WP < NT ? 1 : WP / NT;  // weight loads per loading thread and K-block
   constexpr int XP = XST / 16;          // 16-byte activation pieces of a K-block
@@ -1166,9 +1168,9 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   // the last tile read out-of-range offsets (zeros), so every call issues
   // the same loads.
   const auto rres = make_rsrc(a.res.data, a.res.data ? (int64_t)a.res.n * a.res.h * a.res.w * a.res.pixel : 0);
-  auto fetch = [&](int st) __attribute__((always_inline)) {
+  auto fetch = [&](int st, int h) __attribute__((always_inline)) {
     const bool live = f_tile < t_end;
-    uint8_t *ws = lds + st * SST;
+    uint8_t *ws = lds + st * SST + h * SSB;
     if constexpr (RB == 2) {
       if (f_kb == 0) {  // the tile's shortcut codes, 16 bytes per thread
         const int pt = f_it.pt;
@@ -1289,8 +1291,8 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
   struct OpsS { v4i x0a, x0b, x1a, x1b, a00, a01, a10, a11; };  // stem: x[pb] words 0-3 / 4-7
   struct OpsF { uint2 x0, x1; v4i a0, a1; };                     // FP4: a[cb]
   using Ops = typename std::conditional<STEM, OpsS, typename std::conditional<FP4, OpsF, OpsG>::type>::type;
-  auto read_ops = [&](int stage, Ops &o) __attribute__((always_inline)) {
-    const uint32_t xa = xaddr0 + stage * SST, aa = aaddr0 + stage * SST;
+  auto read_ops = [&](int stage, int h, Ops &o) __attribute__((always_inline)) {
+    const uint32_t xa = xaddr0 + stage * SST + h * SSB, aa = aaddr0 + stage * SST + h * SSB;
     if constexpr (STEM) {
       asm volatile(
           "ds_read_b128 %0, %8\n\t"
@@ -1378,25 +1380,35 @@ __global__ __launch_bounds__(WN * WM * 64, 512 / (WN * WM * 64)) void conv_tile_
     }
     }
   };
-  // K-block gk: wait until this wave's loads of it have landed, barrier
-  // (everyone's have, and everyone is done with K-block gk - 1, whose stage
-  // the next fetch reuses), fetch K-block gk + kStages - 1, read the
-  // operands, run the MFMAs, and finish the tile after its last K-block.
-  for (int st = 0; st < kStages - 1; ++st) fetch(st);
-  for (int gk = 0; gk < total; ++gk) {
-    if (c_kb == 0) tile_start();
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kStages - 2) * LPK));
+  // Stage of K-blocks gk .. gk + KPI - 1: wait until this wave's loads of
+  // it have landed, barrier (everyone's have, and everyone is done with the
+  // previous stage, which the next fetch reuses), fetch the stage kStages - 1
+  // ahead, then per K-block read the operands, run the MFMAs, and finish the
+  // tile after its last K-block.  A tile's shortcut codes (two buffers) are
+  // safe while kb_total >= kStages * KPI.
+  for (int st = 0; st < kStages - 1; ++st)
+#pragma unroll
+    for (int h = 0; h < KPI; ++h) fetch(st, h);
+  for (int gk = 0; gk < total; gk += KPI) {
+    const int st = (gk / KPI) % kStages;
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kStages - 2) * KPI * LPK));
     ring_barrier();
-    fetch((gk + kStages - 1) % kStages);
-    Ops o;
-    read_ops(gk % kStages, o);
-    __builtin_amdgcn_sched_barrier(0);
-    mfmas(o);
-    if (++c_kb == KB) {
-      tile_end();
-      c_kb = 0;
-      ++c_tile;
-      tile_next(c_it, npt, ncb * G, nch);
+#pragma unroll
+    for (int h = 0; h < KPI; ++h) fetch((st + kStages - 1) % kStages, h);
+#pragma unroll
+    for (int h = 0; h < KPI; ++h) {
+      if (KPI > 1 && gk + h >= total) break;  // uniform: the run's last stage may be half used
+      if (c_kb == 0) tile_start();
+      Ops o;
+      read_ops(st, h, o);
+      __builtin_amdgcn_sched_barrier(0);
+      mfmas(o);
+      if (++c_kb == KB) {
+        tile_end();
+        c_kb = 0;
+        ++c_tile;
+        tile_next(c_it, npt, ncb * G, nch);
+      }
     }
   }
 }
@@ -1665,14 +1677,15 @@ bool stem_tile_applies(const ConvArgs &a) {
          (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64 < ((int64_t)1 << 30);
 }
 
-template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES, bool FP4 = false>
+template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES, bool FP4 = false, int KPI = 1>
 hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
+  if (geo.kb_total < S * KPI) return hipErrorInvalidValue;
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
   const int npt = (int)((geo.M + TM - 1) / TM);
   const int ncb = a.cout / TN;
   const int64_t T = (int64_t)npt * ncb * a.in.groups;
   if (T <= 0 || T > 0x7fffffff) return hipErrorInvalidValue;
-  const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S, FP4>, WN * WM * 64);
+  const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S, FP4, KPI>, WN * WM * 64);
   // Pixel chunks (tile_at): 8, so that an XCD fetches each input line once
   // for all groups, unless the filter is the larger read (every XCD then
   // reads all of it): about 7 W extra against (G - 1) X saved.
@@ -1686,10 +1699,10 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
     hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, true, S>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0, s,
                        a, geo, npt, ncb, per, nch);
   else if (!a.res.data)
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, FP4>), dim3((unsigned)nwg), dim3(WN * WM * 64),
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, FP4, KPI>), dim3((unsigned)nwg), dim3(WN * WM * 64),
                        0, s, a, geo, npt, ncb, per, nch);
   else
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4>), dim3((unsigned)nwg), dim3(WN * WM * 64),
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4, KPI>), dim3((unsigned)nwg), dim3(WN * WM * 64),
                        0, s, a, geo, npt, ncb, per, nch);
   return hipGetLastError();
 }
@@ -1722,11 +1735,22 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
       tm64 = e && atoi(e) == 128 ? 128 : 256;
     }
     const int tm = tile_tm() ? tile_tm() : 128;
-    hipError_t e = a.cout % 128 != 0 ? (tm64 == 128 ? launch_tile<2, 2, 1, 2, false, PALQ_TILE_STAGES, true>(a, g4, s)
-                                                    : launch_tile<2, 2, 1, 4, false, PALQ_TILE_STAGES, true>(a, g4, s))
-                   : tm == 64  ? launch_tile<2, 2, 2, 1, false, PALQ_TILE_STAGES, true>(a, g4, s)
-                   : tm == 128 ? launch_tile<2, 2, 2, 2, false, PALQ_TILE_STAGES, true>(a, g4, s)
-                               : launch_tile<2, 2, 2, 4, false, PALQ_TILE_STAGES, true>(a, g4, s);
+    static int kpi = -1;  // K-blocks per ring stage (PALQ_TILE_KPI=2 for tuning)
+    if (kpi < 0) {
+      const char *e = getenv("PALQ_TILE_KPI");
+      kpi = e && atoi(e) == 2 ? 2 : 1;
+    }
+    constexpr int S4 = PALQ_TILE_STAGES;
+    hipError_t e;
+    if (kpi == 2 && geo.kb_total >= S4 * 2)
+      e = a.cout % 128 != 0 ? launch_tile<2, 2, 1, 4, false, S4, true, 2>(a, g4, s)
+                            : launch_tile<2, 2, 2, 2, false, S4, true, 2>(a, g4, s);
+    else
+      e = a.cout % 128 != 0 ? (tm64 == 128 ? launch_tile<2, 2, 1, 2, false, S4, true>(a, g4, s)
+                                           : launch_tile<2, 2, 1, 4, false, S4, true>(a, g4, s))
+          : tm == 64  ? launch_tile<2, 2, 2, 1, false, S4, true>(a, g4, s)
+          : tm == 128 ? launch_tile<2, 2, 2, 2, false, S4, true>(a, g4, s)
+                      : launch_tile<2, 2, 2, 4, false, S4, true>(a, g4, s);
     if (e != hipSuccess || epi == 0) return e;
     return dispatch_bits<2>(a, geo, cb, pb, 1, s);  // unknown: the general build decides on the device
   }
