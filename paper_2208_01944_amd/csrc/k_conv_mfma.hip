@@ -1035,7 +1035,7 @@ __device__ __forceinline__ void tile_next(TileIt &it, int npt, int ncombo, int n
 template <int CB, int PB, int WN, int WM, int RB, bool STEM = false, int kStages = PALQ_TILE_STAGES,
           bool FP4 = false, int KPI = 1>
 __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, Geo geo, int npt,
-                                                                                      int ncb, int per, int nch) {
+                                                                                      int ncb, int nch) {
   constexpr int B = 2;
   constexpr int NT = WN * WM * 64;
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
@@ -1074,20 +1074,27 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   const int l32 = lane & 31, half = lane >> 5;
   const int wn = wave / WM, wm = wave % WM;
 
-  // this workgroup's run of tiles (tile_id: pixel tile and combo
-  // g * ncb + cbk)
+  // This workgroup's run of tiles (tile_at: pixel tile and combo
+  // g * ncb + cbk).  Workgroup id i runs on XCD x = i mod 8; XCD x takes the
+  // x-th eighth of the tiles, split over its P = n / 8 workgroups in runs of
+  // floor or ceil(T_x / P) (the longer runs on the lowest y = i / 8, i.e. the
+  // first workgroups dispatched, one per CU), so every CU gets the same work
+  // to within one tile.
   const int G = a.in.groups;
   const int T = npt * ncb * G;
-  const int nwg = (int)gridDim.x;  // a multiple of 8
-  const int lw = (int)(blockIdx.x & 7) * (nwg >> 3) + (int)(blockIdx.x >> 3);
-  const int t_begin = lw * per;
-  const int t_end = min(T, t_begin + per);
+  const int P = (int)gridDim.x >> 3;  // the grid is a multiple of 8
+  const int x = (int)(blockIdx.x & 7), y = (int)(blockIdx.x >> 3);
+  const int Tq = T >> 3, Tr = T & 7;
+  const int Tx = Tq + (x < Tr ? 1 : 0);
+  const int base = Tx / P, ex = Tx % P;
+  const int t_begin = x * Tq + min(x, Tr) + y * base + min(y, ex);
+  const int t_end = t_begin + base + (y < ex ? 1 : 0);
   if (t_begin >= t_end) return;  // no barrier yet
   const int KB = geo.kb_total;
   const int total = (t_end - t_begin) * KB;  // K-blocks this workgroup runs
 
   // requant constants of the run's first and last combo (slots 0 and 1; a
-  // run spans at most two: the launcher keeps per <= npt / nch)
+  // run spans at most two: the launcher keeps runs <= npt / nch tiles)
   const int combo0 = tile_at(t_begin, npt, ncb * G, nch).combo;
   const int combo1 = tile_at(t_end - 1, npt, ncb * G, nch).combo;
   for (int c = tid; c < 2 * TN; c += NT) {
@@ -1692,18 +1699,22 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * (FP4 ? 32 : 64);
   const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
   const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(8, npt) : 1;
-  // runs span <= 2 (chunk, combo) segments
-  const int per = (int)std::min<int64_t>((T + slots - 1) / slots, npt / nch);
-  const int nwg = (int)(((T + per - 1) / per + 7) / 8 * 8);
+  // P workgroups per XCD: all resident slots, no more than the XCD's
+  // tiles, and runs of at most npt / nch tiles (two (chunk, combo) segments)
+  const int64_t Tx = (T + 7) / 8;
+  const int maxlen = npt / nch;
+  int64_t P = std::max<int64_t>(1, std::min<int64_t>(slots / 8, Tx));
+  if ((Tx + P - 1) / P > maxlen) P = (Tx + maxlen - 1) / maxlen;
+  const int nwg = (int)(8 * P);
   if constexpr (STEM)
     hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, true, S>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0, s,
-                       a, geo, npt, ncb, per, nch);
+                       a, geo, npt, ncb, nch);
   else if (!a.res.data)
     hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, FP4, KPI>), dim3((unsigned)nwg), dim3(WN * WM * 64),
-                       0, s, a, geo, npt, ncb, per, nch);
+                       0, s, a, geo, npt, ncb, nch);
   else
     hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4, KPI>), dim3((unsigned)nwg), dim3(WN * WM * 64),
-                       0, s, a, geo, npt, ncb, per, nch);
+                       0, s, a, geo, npt, ncb, nch);
   return hipGetLastError();
 }
 
