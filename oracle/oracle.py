@@ -217,6 +217,28 @@ def conv_layer(x, w, stride, pad, mult, shift, bias, out_bits, shuffle=0,
 
 
 # ---------------------------------------------------------------------------
+# Section 4.2 Eq. 9-10: the cyclic shuffle module.
+# ---------------------------------------------------------------------------
+def shuffle_module(x, w, mult, shift, bias, res_mult, out_bits):
+    """Z = X + Conv1x1(Y) with Y = CyclicPermute(X) (Eq. 9-10), as an integer
+    layer: the 1x1 B-bit group conv runs on the permuted input Y (Eq. 8, one
+    step), the shortcut X enters unpermuted, scaled by res_mult (the same
+    shortcut scale as an identity residual), and the sum is requantised.
+    Every per-channel array is indexed by the module's output channel.
+    Returns (codes, acc) with acc the 1x1 accumulator of each output channel.
+    """
+    w = np.asarray(w)
+    G = w.shape[0]
+    if w.shape[2:4] != (1, 1) or w.shape[1] != w.shape[4]:
+        raise ValueError("the module's conv is 1x1 with as many outputs as inputs per group")
+    y = cyclic_permute(x, G, 1)
+    acc = group_conv(y, w, 1, 0)
+    bias = np.zeros(acc.shape[-1], np.int64) if bias is None else np.asarray(bias, np.int64)
+    t = acc + bias + np.asarray(res_mult, np.int64) * np.asarray(x, np.int64)
+    return requant(t, mult, shift, out_bits), acc
+
+
+# ---------------------------------------------------------------------------
 # Network glue (stem/FC stay high precision, Section 5 "first and last
 # layer are not quantized"; here they are 8-bit integer).
 # ---------------------------------------------------------------------------
@@ -265,6 +287,11 @@ def run_net(net, x, keep=False):
                                 res=res, res_mult=L.get("res_mult"),
                                 proj_x=px, proj_w=L.get("proj_w"),
                                 proj_stride=L.get("proj_stride", 1))
+            accs[L["dst"]] = acc
+            out = q
+        elif op == "shuffle_module":
+            q, acc = shuffle_module(src, L["w"], L["mult"], L["shift"], L.get("bias"),
+                                    L["res_mult"], L["out_bits"])
             accs[L["dst"]] = acc
             out = q
         elif op == "maxpool":
@@ -316,6 +343,16 @@ def calibrate_centring(net, x):
                               L["out_bits"], L.get("shuffle", 0), res=res, res_mult=L.get("res_mult"),
                               proj_x=px, proj_w=L.get("proj_w"), proj_stride=L.get("proj_stride", 1))
             tensors[L["dst"]] = q
+        elif L["op"] == "shuffle_module":
+            _, acc = shuffle_module(src, L["w"], L["mult"], L["shift"], None, L["res_mult"],
+                                    L["out_bits"])
+            t = acc + np.asarray(L["res_mult"], np.int64) * src
+            cnt = t.shape[0] * t.shape[1] * t.shape[2]
+            sums = t.reshape(-1, t.shape[-1]).sum(axis=0)
+            L["bias"] = np.array([-int((Fraction(int(s), cnt) + Fraction(1, 2)).__floor__()) for s in sums],
+                                 dtype=np.int32)
+            tensors[L["dst"]], _ = shuffle_module(src, L["w"], L["mult"], L["shift"], L["bias"],
+                                                  L["res_mult"], L["out_bits"])
         elif L["op"] == "maxpool":
             tensors[L["dst"]] = maxpool(src, L["k"], L["stride"], L["pad"])
         elif L["op"] == "avgsum":

@@ -94,6 +94,18 @@ def conv_layer_spec(g, *, src, dst, groups, cin, cout, k, stride, pad, in_bits, 
     return L
 
 
+def shuffle_module_spec(g, *, src, dst, groups, ch, bits, shift=None):
+    """A cyclic shuffle module (Eq. 9-10) on a G x ch tensor of b-bit codes:
+    1x1 b-bit group filter [G][ch][1][1][ch], per-output-channel M, shift,
+    zero bias and an identity-shortcut scale res_mult (reading A10)."""
+    w = codes(g, (groups, ch, 1, 1, ch), bits, True)
+    if shift is None:
+        shift = default_shift(ch, bits, False, bits, bits)
+    mult, shift_a, bias, res_mult = conv_params(g, groups, ch, bits, shift, True)
+    return dict(op="shuffle_module", src=src, dst=dst, w=w, in_bits=bits, w_bits=bits,
+                out_bits=bits, mult=mult, shift=shift_a, bias=bias, res_mult=res_mult)
+
+
 # ---------------------------------------------------------------------------
 # Single-layer cases
 # ---------------------------------------------------------------------------
@@ -160,11 +172,15 @@ def _stem(g, layers, groups, bits, width=64):
     return 2, 3
 
 
-def resnet18(n=64, groups=4, bits=2, hw=224, classes=1000, seed=SEED_BASE + 3, stages=(2, 2, 2, 2)):
+def resnet18(n=64, groups=4, bits=2, hw=224, classes=1000, seed=SEED_BASE + 3, stages=(2, 2, 2, 2),
+             modules=False):
     """ResNet-18 topology with every 3x3 conv a G-group b-bit conv at the
     original width per group; conv2 of each basic block adds the shortcut in
     int32 before requantisation and writes its branch one cyclic step on;
-    stage-first blocks take a 1x1/s2 grouped projection shortcut."""
+    stage-first blocks take a 1x1/s2 grouped projection shortcut.  modules:
+    a cyclic shuffle module (Eq. 9-10) at the start of stages 2-4, after the
+    stage's first (strided) conv, at the stage's width and resolution
+    (Section 4.3 places the module at the beginning of each stage)."""
     g = rng(seed)
     x = codes(g, (n, hw, hw, 3), 8, True)
     layers = []
@@ -178,6 +194,11 @@ def resnet18(n=64, groups=4, bits=2, hw=224, classes=1000, seed=SEED_BASE + 3, s
             layers.append(conv_layer_spec(g, src=cur, dst=t1, groups=groups, cin=ch, cout=width, k=3,
                                           stride=s, pad=1, in_bits=bits, in_signed=False,
                                           w_bits=bits, out_bits=bits))
+            if modules and si > 0 and b == 0:
+                layers.append(shuffle_module_spec(g, src=t1, dst=nid, groups=groups, ch=width,
+                                                  bits=bits))
+                t1 = nid
+                nid += 1
             t2 = nid
             nid += 1
             proj = (s != 1 or ch != width)
@@ -189,8 +210,8 @@ def resnet18(n=64, groups=4, bits=2, hw=224, classes=1000, seed=SEED_BASE + 3, s
             cur, ch = t2, width
     layers.append(dict(op="avgsum", src=cur, dst=nid))
     layers.append(dict(op="fc", src=nid, dst=nid + 1, w=codes(g, (classes, ch * groups), 8, True)))
-    return dict(name=f"resnet18_palq_g{groups}_b{bits}", n=n, hw=hw, groups=groups, bits=bits,
-                x=x, layers=layers, classes=classes)
+    return dict(name=f"resnet18_palq_g{groups}_b{bits}" + ("_mod" if modules else ""), n=n, hw=hw,
+                groups=groups, bits=bits, x=x, layers=layers, classes=classes)
 
 
 def resnet50(n=128, groups=2, bits=2, hw=224, classes=1000, seed=SEED_BASE + 5,

@@ -310,6 +310,79 @@ def test_proposition1_reachability(G):
         assert len(nz) == G
 
 
+@pytest.mark.parametrize("G", [2, 3, 4])
+def test_shuffle_module_proposition1(G):
+    """The integer module (Eq. 9-10) with positive 1x1 weights and an
+    identity-like requant (M = 2^14, shift 14, 8-bit output): an impulse in
+    group i reaches exactly groups i..i+k after k modules, all groups after
+    G-1 (Proposition 1)."""
+    c = 3
+    w = np.ones((G, c, 1, 1, c), np.int64)
+    mult = np.full(G * c, 1 << 14)
+    shift = np.full(G * c, 14)
+    rm = np.ones(G * c, np.int64)
+    for i in range(G):
+        x = np.zeros((1, 2, 2, G * c), np.int64)
+        x[0, 1, 0, i * c + 1] = 1
+        for k in range(1, G):
+            x, _ = O.shuffle_module(x, w, mult, shift, None, rm, 8)
+            nz = {gg for gg in range(G) if np.any(x[..., gg * c:(gg + 1) * c])}
+            assert nz == {(i + j) % G for j in range(k + 1)}
+        assert len(nz) == G
+
+
+def test_shuffle_module_special_cases():
+    g = np.random.default_rng(5)
+    G, c = 3, 4
+    x = g.integers(0, 4, (2, 3, 5, G * c))
+    w = g.integers(-2, 2, (G, c, 1, 1, c))
+    mult = g.integers(1 << 14, 1 << 15, G * c)
+    shift = np.full(G * c, 12)
+    bias = g.integers(-50, 50, G * c)
+    rm = g.integers(1, 8, G * c)
+    # zero weights: only the (scaled) shortcut and the bias remain
+    q0, acc0 = O.shuffle_module(x, np.zeros_like(w), mult, shift, bias, rm, 2)
+    assert not acc0.any()
+    np.testing.assert_array_equal(q0, O.requant(bias + rm * x, mult, shift, 2))
+    # zero shortcut scale: the 1x1 conv of the input one group back
+    q1, acc1 = O.shuffle_module(x, w, mult, shift, bias, np.zeros(G * c, np.int64), 2)
+    xv = x.reshape(2, 3, 5, G, c)
+    for j in range(G):
+        ref = np.einsum("nhwc,kc->nhwk", xv[..., (j - 1) % G, :], w[j, :, 0, 0, :])
+        np.testing.assert_array_equal(acc1[..., j * c:(j + 1) * c], ref)
+    # G = 1: the permutation is the identity, so the module is a 1x1 layer
+    # with an identity shortcut taken from its own input
+    w1 = w[:1]
+    q2, acc2 = O.shuffle_module(x[..., :c], w1, mult[:c], shift[:c], bias[:c], rm[:c], 2)
+    q3, acc3 = O.conv_layer(x[..., :c], w1, 1, 0, mult[:c], shift[:c], bias[:c], 2, shuffle=0,
+                            res=x[..., :c], res_mult=rm[:c])
+    np.testing.assert_array_equal(q2, q3)
+    np.testing.assert_array_equal(acc2, acc3)
+
+
+@pytest.mark.parametrize("G", [1, 2, 3, 4])
+def test_shuffle_module_is_a_rotated_layer(G):
+    """The reading the GPU path uses: the module equals a 1x1 layer that
+    writes its branch one group on (Eq. 8 as the store address) with the
+    identity shortcut from its own input, when its per-group parameters are
+    rotated by one group (layer group g takes module group g + 1)."""
+    g = np.random.default_rng(G)
+    c = 5
+    x = g.integers(0, 4, (2, 4, 3, G * c))
+    w = g.integers(-2, 2, (G, c, 1, 1, c))
+    mult = g.integers(1 << 14, 1 << 15, G * c)
+    shift = np.full(G * c, 12)
+    bias = g.integers(-40, 40, G * c)
+    rm = g.integers(1, 16, G * c)
+    q, acc = O.shuffle_module(x, w, mult, shift, bias, rm, 2)
+    rot = lambda a: np.roll(np.asarray(a).reshape(G, -1), -1, axis=0).reshape(np.asarray(a).shape)
+    wr = np.roll(w, -1, axis=0)
+    q2, acc2 = O.conv_layer(x, wr, 1, 0, rot(mult), rot(shift), rot(bias), 2, shuffle=1, res=x,
+                            res_mult=rot(rm))
+    np.testing.assert_array_equal(q, q2)
+    np.testing.assert_array_equal(acc, acc2)
+
+
 def test_conv_layer_shuffle_writes_branch_one_group_on():
     """With an identity residual and zero weights in all groups but one, only
     the destination group (g+s) mod G changes."""
@@ -374,11 +447,10 @@ def test_avgsum_and_fc_closed_forms():
 # ---------------------------------------------------------------------------
 def _net_macs(stages, groups, modules: bool):
     """MAC count of the ResNet layer list the input generator builds (stem,
-    grouped 3x3 convs, grouped 1x1 projections, FC), plus, when modules is
-    set, one cyclic-shuffle module (a 1x1 grouped conv at the stage's width)
-    at the start of stages 2-4 (Section 4.3)."""
+    grouped 3x3 convs, grouped 1x1 projections, FC and, with modules, the
+    cyclic-shuffle modules it places at the start of stages 2-4)."""
     G = max(groups, 1)
-    net = I.resnet18(n=1, groups=G, bits=2, stages=stages)
+    net = I.resnet18(n=1, groups=G, bits=2, stages=stages, modules=modules)
     h = 224
     shapes = {0: (224, 224, 3)}
     macs = 0
@@ -392,6 +464,10 @@ def _net_macs(stages, groups, modules: bool):
                 pg, pco, _, _, pci = L["proj_w"].shape
                 macs += O.layer_macs(pg * pci, pg * pco, pg, 1, ho, ho)
             shapes[L["dst"]] = (ho, ho, gg * co)
+        elif L["op"] == "shuffle_module":
+            gg, co, _, _, ci = L["w"].shape
+            macs += O.layer_macs(gg * ci, gg * co, gg, 1, sh[0], sh[1])
+            shapes[L["dst"]] = sh
         elif L["op"] == "maxpool":
             ho = O.out_size(sh[0], L["k"], L["stride"], L["pad"])
             shapes[L["dst"]] = (ho, ho, sh[2])
@@ -399,9 +475,6 @@ def _net_macs(stages, groups, modules: bool):
             shapes[L["dst"]] = (1, 1, sh[2])
         elif L["op"] == "fc":
             macs += O.layer_macs(L["w"].shape[1], L["w"].shape[0], 1, 1, 1, 1)
-    if modules:
-        for width, hw in ((128, 28), (256, 14), (512, 7)):
-            macs += O.layer_macs(G * width, G * width, G, 1, hw, hw)
     del h
     return macs
 
