@@ -188,6 +188,25 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
 palq_status palq_cyclic_shuffle(palq_ctx *ctx, const palq_act *in, int32_t steps,
                                 const palq_act *out);
 
+/* The cyclic shuffle module of Section 4.2 (Eq. 9-10), Z = X + Conv1x1(Y)
+ * with Y = CyclicPermute(X) (Eq. 8, one step), as an integer layer:
+ *   t[p, j, k] = sum_c w[j][k][c] * in[p, (j - 1) mod G, c] + bias[j*C + k]
+ *                + res_mult[j*C + k] * in[p, j, k]
+ *   out[p, j, k] = clamp(floor((t M + 2^(sh-1)) / 2^sh), 0, 2^out_bits - 1)
+ * with M, sh = rq->mult, rq->shift [j*C + k].  Every per-channel array is
+ * indexed by the module's output channel j*C + k.
+ *   in  : unsigned codes of 2, 3 or 4 bits, G groups of C codes
+ *   w   : 1x1 filter, groups G, cout_pg == cin_pg == C, bits == in bits
+ *   out : in's n, h, w, groups and C; bits == rq->out_bits (2, 3, 4 or 8)
+ *   res_mult: device int32 [G*C], |res_mult| < 2^15
+ * Device pointers, caller-owned; out must not overlap in.  Runs as one
+ * grouped 1x1 layer that stores its branch one group on with the identity
+ * shortcut from in, its per-group parameters rotated by one group into
+ * context-owned memory first (asynchronously, on the context stream).
+ * Errors as palq_group_conv. */
+palq_status palq_shuffle_module(palq_ctx *ctx, const palq_act *in, const palq_filter *w,
+                                const palq_requant *rq, const int32_t *res_mult, const palq_act *out);
+
 /* k x k max pool with stride and zero-area padding (max over the in-image
  * part of each window) on unsigned codes; out has in's groups and bits. */
 palq_status palq_maxpool(palq_ctx *ctx, const palq_act *in, int32_t k, int32_t stride, int32_t pad,
@@ -210,6 +229,7 @@ palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, con
 #define PALQ_OP_MAXPOOL 2
 #define PALQ_OP_AVGSUM 3
 #define PALQ_OP_FC 4
+#define PALQ_OP_SHUFFLE_MODULE 5
 
 #define PALQ_NET_KEEP_ALL 1 /* every tensor keeps its own buffer (for inspection) */
 #define PALQ_NET_TIMING 2   /* record a HIP event pair around every layer      */
@@ -227,6 +247,10 @@ palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, con
  *                  shuffle_steps; optional identity shortcut res_src (>= 0)
  *                  with res_mult, or projection proj_src (>= 0) with proj_w
  *                  and proj_stride.  Same arithmetic as palq_group_conv.
+ *  PALQ_OP_SHUFFLE_MODULE src, w (1x1, cout_pg == cin_pg), mult/shift/bias
+ *                  (bias nullable), out_bits, res_mult: the cyclic shuffle
+ *                  module of palq_shuffle_module (the other conv fields are
+ *                  ignored).
  *  PALQ_OP_MAXPOOL src, pool_k, pool_stride, pool_pad.
  *  PALQ_OP_AVGSUM  src -> int32 sums [n][channels].
  *  PALQ_OP_FC      src (an AVGSUM output), fc_w, fc_out -> int32 logits.

@@ -129,6 +129,7 @@ void palq_destroy(palq_ctx *ctx) {
     if (ctx->range_scratch) hipFree(ctx->range_scratch);
     if (ctx->conv_scratch) hipFree(ctx->conv_scratch);
     if (ctx->fc_scratch) hipFree(ctx->fc_scratch);
+    if (ctx->mod_scratch) hipFree(ctx->mod_scratch);
   }
   delete ctx;
 }
@@ -218,6 +219,62 @@ palq_status palq_quantize(palq_ctx *ctx, const float *x, float l, float u, const
     if (e == hipSuccess) e = launch_quantize(x, l, u, nullptr, ov, ctx->stream);
   }
   return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "quantize");
+}
+
+// ------------------------------------------------------------ shuffle module
+// Eq. 9-10 run as the 1x1 layer it equals: the branch is stored one group on
+// (Eq. 8 as the write address), the shortcut is the identity residual from
+// the module's own input, and the per-group parameters are rotated by one
+// group (layer group g takes module group (g + 1) mod G).
+palq_status palq_shuffle_module(palq_ctx *ctx, const palq_act *in, const palq_filter *w,
+                                const palq_requant *rq, const int32_t *res_mult, const palq_act *out) {
+  if (!ctx) return PALQ_ERR_ARG;
+  palq_status st;
+  if ((st = check_act(ctx, in, "in")) || (st = check_filter(ctx, w, "w"))) return st;
+  if (w->kh != 1 || w->kw != 1 || w->cin_pg != w->cout_pg)
+    return fail(ctx, PALQ_ERR_ARG, "shuffle module: the filter must be 1x1 with cout_pg == cin_pg");
+  if (!rq || !res_mult) return fail(ctx, PALQ_ERR_ARG, "shuffle module: requant and res_mult required");
+  palq_residual res{};
+  res.identity = in;
+  res.res_mult = res_mult;
+  {
+    palq_ctx vctx;  // every other check is the layer's
+    vctx.device = -1;
+    st = palq_group_conv(&vctx, in, w, 1, 0, rq, &res, 1, out, nullptr);
+    if (st != PALQ_OK) return fail(ctx, st, vctx.err);
+  }
+  if (ctx->device < 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  const int G = w->groups;
+  auto up = [](int64_t b) { return (b + 255) & ~(int64_t)255; };
+  const int64_t wb = filter_bytes(w), cb = (int64_t)G * w->cout_pg * 4;
+  const int64_t off_m = up(wb), off_s = off_m + up(cb), off_b = off_s + up(cb), off_r = off_b + up(cb);
+  const size_t need = (size_t)(off_r + up(cb));
+  if (need > ctx->mod_scratch_bytes) {
+    if (ctx->mod_scratch) hipFree(ctx->mod_scratch);  // waits for work still reading it
+    ctx->mod_scratch = nullptr;
+    ctx->mod_scratch_bytes = 0;
+    if (hipMalloc(&ctx->mod_scratch, need) != hipSuccess)
+      return fail(ctx, PALQ_ERR_NOMEM, "shuffle module: parameter scratch");
+    ctx->mod_scratch_bytes = need;
+  }
+  uint8_t *sc = ctx->mod_scratch;
+  hipError_t e = hipSuccess;
+  auto rot = [&](int64_t off, const void *src, int64_t bytes) {  // group g <- group g + 1
+    const int64_t gb = bytes / G;
+    if (e == hipSuccess) e = hipMemcpyAsync(sc + off, (const uint8_t *)src + gb, bytes - gb, hipMemcpyDefault, ctx->stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(sc + off + bytes - gb, src, gb, hipMemcpyDefault, ctx->stream);
+    return sc + off;
+  };
+  palq_filter w2 = *w;
+  w2.data = rot(0, w->data, wb);
+  palq_requant rq2 = *rq;
+  rq2.mult = (const int32_t *)rot(off_m, rq->mult, cb);
+  rq2.shift = (const int32_t *)rot(off_s, rq->shift, cb);
+  rq2.bias = rq->bias ? (const int32_t *)rot(off_b, rq->bias, cb) : nullptr;
+  res.res_mult = (const int32_t *)rot(off_r, res_mult, cb);
+  if (e != hipSuccess) return device_fail(ctx, e, "shuffle module: parameter copies");
+  return palq_group_conv(ctx, in, &w2, 1, 0, &rq2, &res, 1, out, nullptr);
 }
 
 // ------------------------------------------------------------ group conv

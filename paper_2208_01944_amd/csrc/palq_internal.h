@@ -126,4 +126,6 @@ struct palq_ctx {
   int8_t *fc_scratch = nullptr;    // digit planes of the last FC call
   size_t fc_scratch_bytes = 0;
   int conv_fp4 = 1;                // palq_set_conv_fp4 (initial value: PALQ_CONV_FP4, default 1)
+  uint8_t *mod_scratch = nullptr;  // rotated parameters of the last shuffle-module call
+  size_t mod_scratch_bytes = 0;
 };

@@ -117,11 +117,32 @@ void accumulate_slot(palq_net *net, int slot) {
 
 extern "C" {
 
-palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_layer *layers,
+palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_layer *user_layers,
                             int32_t n_layers, int32_t flags, palq_net **out) {
   if (!ctx || !out) return PALQ_ERR_ARG;
   *out = nullptr;
-  if (!input || !layers || n_layers < 1) return net_fail(ctx, PALQ_ERR_ARG, "empty network");
+  if (!input || !user_layers || n_layers < 1) return net_fail(ctx, PALQ_ERR_ARG, "empty network");
+  // A cyclic shuffle module (Eq. 9-10) is planned as the 1x1 conv layer it
+  // equals: branch stored one group on, identity shortcut from its own
+  // input, per-group parameters rotated by one group (rotate[i]) when they
+  // are copied into the pool.
+  std::vector<palq_layer> norm(user_layers, user_layers + n_layers);
+  std::vector<char> rotate(n_layers, 0);
+  for (int i = 0; i < n_layers; ++i) {
+    palq_layer &L = norm[i];
+    if (L.op != PALQ_OP_SHUFFLE_MODULE) continue;
+    if (L.w.kh != 1 || L.w.kw != 1 || L.w.cin_pg != L.w.cout_pg)
+      return net_fail(ctx, PALQ_ERR_ARG, "layer " + std::to_string(i) + ": a shuffle module's filter is 1x1 with cout_pg == cin_pg");
+    if (!L.res_mult) return net_fail(ctx, PALQ_ERR_ARG, "layer " + std::to_string(i) + ": res_mult missing");
+    L.op = PALQ_OP_CONV;
+    L.stride = 1;
+    L.pad = 0;
+    L.shuffle_steps = 1;
+    L.res_src = L.src;
+    L.proj_src = -1;
+    rotate[i] = 1;
+  }
+  const palq_layer *layers = norm.data();
   if (flags & ~(PALQ_NET_KEEP_ALL | PALQ_NET_TIMING)) return net_fail(ctx, PALQ_ERR_ARG, "unknown flags");
   if (input->n < 1 || input->h < 1 || input->w < 1 || input->groups < 1 || input->ch_per_group < 1 ||
       row_bytes(input->ch_per_group, input->bits) < 0)
@@ -282,9 +303,20 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
   for (int i = 0; i < n_layers && e == hipSuccess; ++i) {
     const palq_layer &L = layers[i];
     Layer &NL = net->layers[i];
+    // group-major arrays; rotated: group g of the copy is group (g + 1) mod G
+    // of the source (a shuffle module, see above)
+    const int rot_groups = rotate[i] ? L.w.groups : 1;
     auto cp = [&](int64_t off, const void *src, int64_t bytes) {
-      if (e == hipSuccess && bytes > 0)
-        e = hipMemcpyAsync(pool + off, src, bytes, hipMemcpyDefault, ctx->stream);
+      if (e == hipSuccess && bytes > 0) {
+        const int64_t gb = bytes / rot_groups;
+        const uint8_t *s8 = (const uint8_t *)src;
+        if (rot_groups > 1) {
+          e = hipMemcpyAsync(pool + off, s8 + gb, bytes - gb, hipMemcpyDefault, ctx->stream);
+          if (e == hipSuccess) e = hipMemcpyAsync(pool + off + bytes - gb, s8, gb, hipMemcpyDefault, ctx->stream);
+        } else {
+          e = hipMemcpyAsync(pool + off, src, bytes, hipMemcpyDefault, ctx->stream);
+        }
+      }
       return pool + off;
     };
     if (L.op == PALQ_OP_CONV) {

@@ -183,3 +183,47 @@ def test_validate_only_net_create(P, vctx):
     Ls[2].w = P.Filter(4, 64, 64, 3, 3, 2, _fake(4))  # 4 x 64 != 128 input channels
     assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 5, 0, ctypes.byref(h)) == P.ERR_ARG
     assert "layer 2" in vctx.last_error()
+
+
+def test_validate_only_shuffle_module(P, vctx):
+    x = _act(P, c=64)
+    out = _act(P, c=64, slot=20)
+    f = P.Filter(2, 64, 64, 1, 1, 2, _fake(10))
+    rq = P.Requant(_fake(30), _fake(31), None, 2)
+
+    def mod(x=x, f=f, rq=rq, rm=_fake(40), out=out):
+        return P._shuffle_module(vctx.h, ctypes.byref(x), ctypes.byref(f), ctypes.byref(rq), rm,
+                                 ctypes.byref(out))
+    assert mod() == P.OK
+    assert mod(f=P.Filter(2, 64, 64, 3, 3, 2, _fake(10))) == P.ERR_ARG   # not 1x1
+    assert mod(f=P.Filter(2, 32, 64, 1, 1, 2, _fake(10))) == P.ERR_ARG   # cout != cin
+    assert mod(rm=None) == P.ERR_ARG
+    assert mod(out=_act(P, c=64, slot=0)) == P.ERR_ARG                    # out aliases in
+    assert mod(out=_act(P, h=4, c=64, slot=20)) == P.ERR_ARG              # wrong shape
+    assert mod(x=_act(P, c=64, g=3), f=P.Filter(3, 64, 64, 1, 1, 2, _fake(10)),
+               out=_act(P, c=64, g=3, slot=20)) == P.OK
+
+
+def test_validate_only_net_with_shuffle_module(P, vctx):
+    inp = P.make_act(2, 16, 16, 1, 3, 8, True, 0)
+    Ls = (P.Layer * 5)()
+    Ls[0] = _layer(P, op=P.OP_CONV, src=0, dst=1, w=P.Filter(1, 128, 3, 3, 3, 8, _fake(1)), stride=2,
+                   pad=1, mult=_fake(2), shift=_fake(3), out_bits=2)
+    Ls[1] = _layer(P, op=P.OP_SHUFFLE_MODULE, src=1, dst=2, w=P.Filter(2, 64, 64, 1, 1, 2, _fake(4)),
+                   mult=_fake(5), shift=_fake(6), out_bits=2, res_mult=_fake(7))
+    Ls[2] = _layer(P, op=P.OP_CONV, src=2, dst=3, w=P.Filter(2, 64, 64, 3, 3, 2, _fake(8)), stride=1,
+                   pad=1, mult=_fake(9), shift=_fake(10), out_bits=2)
+    Ls[3] = _layer(P, op=P.OP_AVGSUM, src=3, dst=4)
+    Ls[4] = _layer(P, op=P.OP_FC, src=4, dst=5, fc_w=_fake(11), fc_out=10)
+    h = ctypes.c_void_p()
+    assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 5, 0, ctypes.byref(h)) == P.OK
+    # 2 * MACs: stem + module (1x1, 64 per group) + 3x3 + FC
+    assert P._net_ops(h) == 2 * (2 * 8 * 8 * 128 * 27) + 2 * (2 * 8 * 8 * 128 * 64) + \
+        2 * (2 * 8 * 8 * 128 * 576) + 2 * (2 * 128 * 10)
+    P._net_destroy(h)
+    Ls[1].w = P.Filter(2, 64, 64, 3, 3, 2, _fake(4))
+    assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 5, 0, ctypes.byref(h)) == P.ERR_ARG
+    assert "layer 1" in vctx.last_error()
+    Ls[1].w = P.Filter(2, 64, 64, 1, 1, 2, _fake(4))
+    Ls[1].res_mult = None
+    assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 5, 0, ctypes.byref(h)) == P.ERR_ARG

@@ -41,7 +41,7 @@ def gpu_forward(ctx, torch, spec, keep=False):
 def compare_tensors(ctx, net, spec, tensors, images):
     for L in spec["layers"]:
         d = L["dst"]
-        if L["op"] in ("conv", "maxpool"):
+        if L["op"] in ("conv", "maxpool", "shuffle_module"):
             got = ctx.unpack(net.tensor(d))[images]
             np.testing.assert_array_equal(got, tensors[d], err_msg=f"tensor {d} ({L['op']})")
 
@@ -63,6 +63,22 @@ def test_resnet18_small_int8_matrix_cores(ctx, torch):
     spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=14)
     spec = O.calibrate_centring(spec, spec["x"])
     ctx.set_conv_fp4(False)
+    try:
+        net, logits = gpu_forward(ctx, torch, spec, keep=True)
+    finally:
+        ctx.set_conv_fp4(True)
+    ref, tensors, _ = O.run_net(spec, spec["x"], keep=True)
+    compare_tensors(ctx, net, spec, tensors, slice(None))
+    np.testing.assert_array_equal(logits, ref)
+
+
+@pytest.mark.parametrize("fp4", [True, False])
+def test_resnet18_with_shuffle_modules_all_tensors(ctx, torch, fp4):
+    say(f"resnet18 + cyclic shuffle modules hw=64 n=2 G=4 b=2 centred fp4={fp4}")
+    spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=15, modules=True)
+    assert sum(L["op"] == "shuffle_module" for L in spec["layers"]) == 3
+    spec = O.calibrate_centring(spec, spec["x"])
+    ctx.set_conv_fp4(fp4)
     try:
         net, logits = gpu_forward(ctx, torch, spec, keep=True)
     finally:

@@ -356,3 +356,35 @@ def test_fc_large(ctx, torch):
     ctx.fc(ctx.upload(x), 64, 2048, ctx.upload(w), 1000, logits)
     ctx.sync()
     np.testing.assert_array_equal(logits.cpu().numpy().reshape(64, 1000), O.fc(x, w))
+
+
+# ---------------------------------------------------------------- shuffle module
+@pytest.mark.parametrize("G,C,bits,n,h,w", [
+    (2, 64, 2, 2, 9, 7),      # grouped MFMA kernel
+    (4, 128, 2, 2, 6, 5),
+    (3, 64, 3, 1, 5, 9),      # 3-bit codes
+    (2, 64, 4, 2, 5, 5),      # 4-bit codes
+    (4, 32, 2, 2, 4, 4),      # direct kernel (32 channels per group)
+    (2, 256, 2, 1, 7, 7),     # long enough K for the tiled kernel
+])
+def test_shuffle_module_matches_oracle(ctx, torch, G, C, bits, n, h, w):
+    say(f"shuffle module G={G} C={C} b={bits} {n}x{h}x{w}")
+    g = I.rng(500 + G * 7 + C + bits)
+    x = I.codes(g, (n, h, w, G * C), bits, False)
+    L = I.shuffle_module_spec(g, src=0, dst=1, groups=G, ch=C, bits=bits)
+    # centred bias so that every output code occurs (reading A14)
+    _, acc = O.shuffle_module(x, L["w"], L["mult"], L["shift"], None, L["res_mult"], bits)
+    t = acc + np.asarray(L["res_mult"], np.int64) * x
+    mean = t.reshape(-1, G * C).sum(axis=0) / t.reshape(-1, G * C).shape[0]
+    bias = (-np.floor(mean + 0.5)).astype(np.int32)
+    ref, _ = O.shuffle_module(x, L["w"], L["mult"], L["shift"], bias, L["res_mult"], bits)
+    xt = ctx.pack(x, G, bits)
+    wt, wf = ctx.pack_filter(L["w"], bits)
+    out = ctx.empty_act(n, h, w, G, C, bits)
+    i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
+    ctx.shuffle_module(xt, wf, i32(L["mult"]), i32(L["shift"]), i32(bias), i32(L["res_mult"]), out)
+    ctx.sync()
+    got = ctx.unpack(out)
+    np.testing.assert_array_equal(got, ref)
+    hist = np.bincount(ref.reshape(-1), minlength=1 << bits)
+    assert np.count_nonzero(hist) >= 2, hist
