@@ -207,6 +207,12 @@ palq_status palq_cyclic_shuffle(palq_ctx *ctx, const palq_act *in, int32_t steps
 palq_status palq_shuffle_module(palq_ctx *ctx, const palq_act *in, const palq_filter *w,
                                 const palq_requant *rq, const int32_t *res_mult, const palq_act *out);
 
+/* Channel shuffle across the groups of each pixel (the per-stage channel
+ * shuffle of Section 4.3 and Table 3; the [G][C] channel matrix transposed
+ * to [C][G]): out channel o = g*C + c takes in channel (o mod G)*C + o / G.
+ * in and out have the same shape and bits and must not overlap. */
+palq_status palq_channel_shuffle(palq_ctx *ctx, const palq_act *in, const palq_act *out);
+
 /* k x k max pool with stride and zero-area padding (max over the in-image
  * part of each window) on unsigned codes; out has in's groups and bits. */
 palq_status palq_maxpool(palq_ctx *ctx, const palq_act *in, int32_t k, int32_t stride, int32_t pad,
@@ -230,6 +236,7 @@ palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, con
 #define PALQ_OP_AVGSUM 3
 #define PALQ_OP_FC 4
 #define PALQ_OP_SHUFFLE_MODULE 5
+#define PALQ_OP_CHANNEL_SHUFFLE 6
 
 #define PALQ_NET_KEEP_ALL 1 /* every tensor keeps its own buffer (for inspection) */
 #define PALQ_NET_TIMING 2   /* record a HIP event pair around every layer      */
@@ -251,6 +258,7 @@ palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, con
  *                  (bias nullable), out_bits, res_mult: the cyclic shuffle
  *                  module of palq_shuffle_module (the other conv fields are
  *                  ignored).
+ *  PALQ_OP_CHANNEL_SHUFFLE src -> the same shape (palq_channel_shuffle).
  *  PALQ_OP_MAXPOOL src, pool_k, pool_stride, pool_pad.
  *  PALQ_OP_AVGSUM  src -> int32 sums [n][channels].
  *  PALQ_OP_FC      src (an AVGSUM output), fc_w, fc_out -> int32 logits.

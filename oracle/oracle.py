@@ -216,6 +216,18 @@ def conv_layer(x, w, stride, pad, mult, shift, bias, out_bits, shuffle=0,
     return requant(t, mult_d, shift_d, out_bits), acc_d
 
 
+def channel_shuffle(x, groups: int) -> np.ndarray:
+    """Channel shuffle (Section 4.3, Table 3): the channel axis viewed as a
+    [G, C^] matrix is transposed to [C^, G] and flattened again, so output
+    channel o = c * G + g holds input channel g * C^ + c."""
+    x = np.asarray(x)
+    c = x.shape[-1]
+    if c % groups:
+        raise ValueError("channels not divisible by groups")
+    v = x.reshape(x.shape[:-1] + (groups, c // groups))
+    return np.swapaxes(v, -1, -2).reshape(x.shape)
+
+
 # ---------------------------------------------------------------------------
 # Section 4.2 Eq. 9-10: the cyclic shuffle module.
 # ---------------------------------------------------------------------------
@@ -294,6 +306,8 @@ def run_net(net, x, keep=False):
                                     L["res_mult"], L["out_bits"])
             accs[L["dst"]] = acc
             out = q
+        elif op == "channel_shuffle":
+            out = channel_shuffle(src, L["groups"])
         elif op == "maxpool":
             out = maxpool(src, L["k"], L["stride"], L["pad"])
         elif op == "avgsum":
@@ -353,6 +367,8 @@ def calibrate_centring(net, x):
                                  dtype=np.int32)
             tensors[L["dst"]], _ = shuffle_module(src, L["w"], L["mult"], L["shift"], L["bias"],
                                                   L["res_mult"], L["out_bits"])
+        elif L["op"] == "channel_shuffle":
+            tensors[L["dst"]] = channel_shuffle(src, L["groups"])
         elif L["op"] == "maxpool":
             tensors[L["dst"]] = maxpool(src, L["k"], L["stride"], L["pad"])
         elif L["op"] == "avgsum":

@@ -165,6 +165,36 @@ __global__ void shuffle_kernel(ActView in, int steps, ActView out, int64_t pixel
   dst[wi] = src[wi];
 }
 
+// ------------------------------------------------------------ channel shuffle
+// Channel shuffle across the G groups of a pixel (the [G][C] channel matrix
+// transposed to [C][G]): output channel o = g' C + c' takes input channel
+// (o mod G) C + o / G.  One thread per output 32-code chunk.
+__global__ void channel_shuffle_kernel(ActView in, ActView out, int64_t pixels, int chunks) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t per_pixel = (int64_t)out.groups * chunks;
+  if (t >= pixels * per_pixel) return;
+  const int64_t p = t / per_pixel;
+  const int rem = (int)(t % per_pixel);
+  const int gq = rem / chunks, ci = rem % chunks;
+  const int C = out.cpg, G = out.groups;
+  const uint8_t *src = in.data + p * in.pixel;
+  const int n = min(32, C - ci * 32);
+  int c[32];
+  for (int j = 0; j < 32; ++j) {
+    if (j < n) {
+      const int o = gq * C + ci * 32 + j;
+      c[j] = read_code(src + (int64_t)(o % G) * in.row, o / G, in.bits, in.is_signed);
+    } else {
+      c[j] = 0;
+    }
+  }
+  uint32_t words[8];
+  pack_chunk(c, n, out.bits, words);
+  uint32_t *dst = (uint32_t *)(out.data + p * out.pixel + (int64_t)gq * out.row) + (int64_t)ci * (out.bits == 3 ? 3 : out.bits);
+  const int nw = chunk_words_in_row(ci, out.bits, out.row / 4);
+  for (int wi = 0; wi < nw; ++wi) dst[wi] = words[wi];
+}
+
 // ------------------------------------------------------------ max pool
 // Field-wise max of sixteen 2-bit unsigned fields packed in a word.
 __device__ inline uint32_t max2x16(uint32_t a, uint32_t b) {
@@ -545,6 +575,16 @@ hipError_t launch_shuffle(const ActView &in, int32_t steps, const ActView &out, 
   if (items == 0) return hipSuccess;
   hipLaunchKernelGGL(shuffle_kernel, dim3(grid_for(items)), dim3(kBlock), 0, s, in, steps, out,
                      pixels);
+  return hipGetLastError();
+}
+
+hipError_t launch_channel_shuffle(const ActView &in, const ActView &out, hipStream_t s) {
+  const int64_t pixels = (int64_t)in.n * in.h * in.w;
+  const int chunks = (in.cpg + 31) / 32;
+  const int64_t items = pixels * in.groups * chunks;
+  if (items == 0) return hipSuccess;
+  hipLaunchKernelGGL(channel_shuffle_kernel, dim3(grid_for(items)), dim3(kBlock), 0, s, in, out, pixels,
+                     chunks);
   return hipGetLastError();
 }
 

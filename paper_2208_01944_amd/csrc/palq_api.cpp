@@ -406,6 +406,20 @@ palq_status palq_cyclic_shuffle(palq_ctx *ctx, const palq_act *in, int32_t steps
   return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "cyclic shuffle");
 }
 
+palq_status palq_channel_shuffle(palq_ctx *ctx, const palq_act *in, const palq_act *out) {
+  if (!ctx) return PALQ_ERR_ARG;
+  palq_status st;
+  if ((st = check_act(ctx, in, "in")) || (st = check_act(ctx, out, "out"))) return st;
+  if (!same_shape(in, out) || in->bits != out->bits || in->is_signed != out->is_signed)
+    return fail(ctx, PALQ_ERR_ARG, "in and out must have the same shape and bits");
+  if (overlaps(in->data, palq_act_bytes(in), out->data, palq_act_bytes(out)))
+    return fail(ctx, PALQ_ERR_ARG, "in and out overlap");
+  if (ctx->device < 0 || in->n == 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  hipError_t e = launch_channel_shuffle(view_of(in), view_of(out), ctx->stream);
+  return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "channel shuffle");
+}
+
 // ------------------------------------------------------------ glue
 palq_status palq_maxpool(palq_ctx *ctx, const palq_act *in, int32_t k, int32_t stride, int32_t pad,
                          const palq_act *out) {

@@ -248,6 +248,10 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       net->ops += 2 * mac;
       NL.in_view = in_v;
       NL.out_view = o;
+    } else if (L.op == PALQ_OP_CHANNEL_SHUFFLE) {
+      if (src.kind != kCodes) { bad(PALQ_ERR_ARG, "channel shuffle input must be codes"); break; }
+      dst.exists = true; dst.kind = kCodes; dst.d = src.d;
+      NL.in_view = src.d; NL.out_view = src.d;
     } else if (L.op == PALQ_OP_MAXPOOL) {
       if (src.kind != kCodes || src.d.is_signed) { bad(PALQ_ERR_ARG, "max pool input must be unsigned codes"); break; }
       if (L.pool_k < 1 || L.pool_stride < 1 || L.pool_pad < 0 || L.pool_pad >= L.pool_k ||
@@ -504,6 +508,12 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
         if (sp.res_src == 0) a.res.data = (uint8_t *)input;
         if (sp.proj_src == 0) a.proj.data = (uint8_t *)input;
         e = NL.use_mfma ? launch_conv_mfma(a, NL.wp, NL.thr, NL.epi, s) : launch_conv_direct(a, s);
+        break;
+      }
+      case PALQ_OP_CHANNEL_SHUFFLE: {
+        palq_act iv = net->tensors[sp.src].d;
+        if (sp.src == 0) iv.data = (void *)input;
+        e = launch_channel_shuffle(view_of(&iv), view_of(&net->tensors[sp.dst].d), s);
         break;
       }
       case PALQ_OP_MAXPOOL: {

@@ -173,14 +173,16 @@ def _stem(g, layers, groups, bits, width=64):
 
 
 def resnet18(n=64, groups=4, bits=2, hw=224, classes=1000, seed=SEED_BASE + 3, stages=(2, 2, 2, 2),
-             modules=False):
+             modules=False, channel_shuffle=False):
     """ResNet-18 topology with every 3x3 conv a G-group b-bit conv at the
     original width per group; conv2 of each basic block adds the shortcut in
     int32 before requantisation and writes its branch one cyclic step on;
     stage-first blocks take a 1x1/s2 grouped projection shortcut.  modules:
     a cyclic shuffle module (Eq. 9-10) at the start of stages 2-4, after the
     stage's first (strided) conv, at the stage's width and resolution
-    (Section 4.3 places the module at the beginning of each stage)."""
+    (Section 4.3 places the module at the beginning of each stage).
+    channel_shuffle: the per-stage channel shuffle (Section 4.3, Table 3) at
+    the end of the first block of stages 2-4."""
     g = rng(seed)
     x = codes(g, (n, hw, hw, 3), 8, True)
     layers = []
@@ -208,9 +210,14 @@ def resnet18(n=64, groups=4, bits=2, hw=224, classes=1000, seed=SEED_BASE + 3, s
                                           res=-1 if proj else cur, proj_src=cur if proj else -1,
                                           proj_cin=ch, proj_stride=s))
             cur, ch = t2, width
+            if channel_shuffle and si > 0 and b == 0:
+                layers.append(dict(op="channel_shuffle", src=cur, dst=nid, groups=groups))
+                cur = nid
+                nid += 1
     layers.append(dict(op="avgsum", src=cur, dst=nid))
     layers.append(dict(op="fc", src=nid, dst=nid + 1, w=codes(g, (classes, ch * groups), 8, True)))
-    return dict(name=f"resnet18_palq_g{groups}_b{bits}" + ("_mod" if modules else ""), n=n, hw=hw,
+    return dict(name=f"resnet18_palq_g{groups}_b{bits}" + ("_mod" if modules else "") +
+                ("_cs" if channel_shuffle else ""), n=n, hw=hw,
                 groups=groups, bits=bits, x=x, layers=layers, classes=classes)
 
 

@@ -29,7 +29,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 c_i32, c_i64, c_p, c_f = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_float
 
 OK, ERR_ARG, ERR_UNSUPPORTED, ERR_OVERFLOW, ERR_DEVICE, ERR_NOMEM = 0, -1, -2, -3, -4, -5
-OP_CONV, OP_MAXPOOL, OP_AVGSUM, OP_FC, OP_SHUFFLE_MODULE = 1, 2, 3, 4, 5
+OP_CONV, OP_MAXPOOL, OP_AVGSUM, OP_FC, OP_SHUFFLE_MODULE, OP_CHANNEL_SHUFFLE = 1, 2, 3, 4, 5, 6
 NET_KEEP_ALL, NET_TIMING = 1, 2
 
 
@@ -85,6 +85,7 @@ _quantize = _sig("palq_quantize", c_i32, c_p, c_p, c_f, c_f, P_ACT, c_p)
 _group_conv = _sig("palq_group_conv", c_i32, c_p, P_ACT, P_FIL, c_i32, c_i32,
                    ctypes.POINTER(Requant), ctypes.POINTER(Residual), c_i32, P_ACT, c_p)
 _shuffle = _sig("palq_cyclic_shuffle", c_i32, c_p, P_ACT, c_i32, P_ACT)
+_channel_shuffle = _sig("palq_channel_shuffle", c_i32, c_p, P_ACT, P_ACT)
 _shuffle_module = _sig("palq_shuffle_module", c_i32, c_p, P_ACT, P_FIL, ctypes.POINTER(Requant), c_p, P_ACT)
 _maxpool = _sig("palq_maxpool", c_i32, c_p, P_ACT, c_i32, c_i32, c_i32, P_ACT)
 _avgsum = _sig("palq_avgsum", c_i32, c_p, P_ACT, c_p)
@@ -100,7 +101,8 @@ _net_reset_times = _sig("palq_net_reset_times", c_i32, c_p)
 
 EXPORTS = ["palq_create", "palq_destroy", "palq_set_stream", "palq_set_conv_fp4", "palq_sync", "palq_last_error",
            "palq_version", "palq_row_bytes", "palq_act_bytes", "palq_pack", "palq_unpack",
-           "palq_quantize", "palq_group_conv", "palq_shuffle_module", "palq_cyclic_shuffle", "palq_maxpool",
+           "palq_quantize", "palq_group_conv", "palq_shuffle_module", "palq_cyclic_shuffle",
+           "palq_channel_shuffle", "palq_maxpool",
            "palq_avgsum", "palq_fc", "palq_net_create", "palq_net_destroy", "palq_forward",
            "palq_net_tensor", "palq_net_ops", "palq_net_layer_times", "palq_net_reset_times"]
 
@@ -252,6 +254,9 @@ class Context:
         self._check(_shuffle_module(self.h, ctypes.byref(x.act), ctypes.byref(w), ctypes.byref(rq),
                                     _ptr(res_mult), ctypes.byref(out.act)))
 
+    def channel_shuffle(self, x: Tensor, out: Tensor):
+        self._check(_channel_shuffle(self.h, ctypes.byref(x.act), ctypes.byref(out.act)))
+
     def cyclic_shuffle(self, x: Tensor, steps, out: Tensor):
         self._check(_shuffle(self.h, ctypes.byref(x.act), steps, ctypes.byref(out.act)))
 
@@ -308,6 +313,8 @@ class Net:
                 d.bias = i32(L["bias"]) if L.get("bias") is not None else None
                 d.out_bits = L["out_bits"]
                 d.res_mult = i32(L["res_mult"])
+            elif L["op"] == "channel_shuffle":
+                d.op = OP_CHANNEL_SHUFFLE
             elif L["op"] == "maxpool":
                 d.op = OP_MAXPOOL
                 d.pool_k, d.pool_stride, d.pool_pad = L["k"], L["stride"], L["pad"]

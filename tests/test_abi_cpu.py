@@ -227,3 +227,14 @@ def test_validate_only_net_with_shuffle_module(P, vctx):
     Ls[1].w = P.Filter(2, 64, 64, 1, 1, 2, _fake(4))
     Ls[1].res_mult = None
     assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 5, 0, ctypes.byref(h)) == P.ERR_ARG
+
+
+def test_validate_only_channel_shuffle(P, vctx):
+    a = _act(P, g=4, c=37, bits=3)
+    b = _act(P, g=4, c=37, bits=3, slot=5)
+    assert P._channel_shuffle(vctx.h, ctypes.byref(a), ctypes.byref(b)) == P.OK
+    assert P._channel_shuffle(vctx.h, ctypes.byref(a), ctypes.byref(a)) == P.ERR_ARG      # overlap
+    c = _act(P, g=4, c=37, bits=2, slot=5)
+    assert P._channel_shuffle(vctx.h, ctypes.byref(a), ctypes.byref(c)) == P.ERR_ARG      # bits differ
+    d = _act(P, g=2, c=74, bits=3, slot=5)
+    assert P._channel_shuffle(vctx.h, ctypes.byref(a), ctypes.byref(d)) == P.ERR_ARG      # grouping differs

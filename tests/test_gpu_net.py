@@ -41,7 +41,7 @@ def gpu_forward(ctx, torch, spec, keep=False):
 def compare_tensors(ctx, net, spec, tensors, images):
     for L in spec["layers"]:
         d = L["dst"]
-        if L["op"] in ("conv", "maxpool", "shuffle_module"):
+        if L["op"] in ("conv", "maxpool", "shuffle_module", "channel_shuffle"):
             got = ctx.unpack(net.tensor(d))[images]
             np.testing.assert_array_equal(got, tensors[d], err_msg=f"tensor {d} ({L['op']})")
 
@@ -83,6 +83,18 @@ def test_resnet18_with_shuffle_modules_all_tensors(ctx, torch, fp4):
         net, logits = gpu_forward(ctx, torch, spec, keep=True)
     finally:
         ctx.set_conv_fp4(True)
+    ref, tensors, _ = O.run_net(spec, spec["x"], keep=True)
+    compare_tensors(ctx, net, spec, tensors, slice(None))
+    np.testing.assert_array_equal(logits, ref)
+
+
+def test_resnet18_with_modules_and_channel_shuffle(ctx, torch):
+    say("resnet18 + cyclic shuffle modules + per-stage channel shuffle hw=64 n=2 G=4 b=2 centred")
+    spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=16, modules=True,
+                      channel_shuffle=True)
+    assert sum(L["op"] == "channel_shuffle" for L in spec["layers"]) == 3
+    spec = O.calibrate_centring(spec, spec["x"])
+    net, logits = gpu_forward(ctx, torch, spec, keep=True)
     ref, tensors, _ = O.run_net(spec, spec["x"], keep=True)
     compare_tensors(ctx, net, spec, tensors, slice(None))
     np.testing.assert_array_equal(logits, ref)

@@ -388,3 +388,15 @@ def test_shuffle_module_matches_oracle(ctx, torch, G, C, bits, n, h, w):
     np.testing.assert_array_equal(got, ref)
     hist = np.bincount(ref.reshape(-1), minlength=1 << bits)
     assert np.count_nonzero(hist) >= 2, hist
+
+
+@pytest.mark.parametrize("bits,G,C", [(2, 4, 64), (2, 2, 37), (3, 3, 48), (4, 4, 128), (8, 2, 40), (2, 4, 512)])
+def test_channel_shuffle_matches_oracle(ctx, bits, G, C):
+    say(f"channel shuffle b={bits} G={G} C={C}")
+    g = np.random.default_rng(bits * 100 + G * 10 + C)
+    x = I.codes(g, (2, 5, 3, G * C), bits, False).astype(np.int64)
+    xt = ctx.pack(x, G, bits)
+    out = ctx.empty_act(2, 5, 3, G, C, bits)
+    ctx.channel_shuffle(xt, out)
+    ctx.sync()
+    np.testing.assert_array_equal(ctx.unpack(out), O.channel_shuffle(x, G))

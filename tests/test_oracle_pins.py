@@ -383,6 +383,26 @@ def test_shuffle_module_is_a_rotated_layer(G):
     np.testing.assert_array_equal(acc, acc2)
 
 
+def test_channel_shuffle_definition_and_inverse():
+    # two groups of three: a0 a1 a2 | b0 b1 b2 -> a0 b0 a1 b1 a2 b2
+    x = np.arange(6)[None, :]
+    np.testing.assert_array_equal(O.channel_shuffle(x, 2), [[0, 3, 1, 4, 2, 5]])
+    g = np.random.default_rng(9)
+    for G, C in ((1, 5), (2, 4), (3, 7), (4, 64), (6, 2)):
+        x = g.integers(0, 16, (2, 3, G * C))
+        y = O.channel_shuffle(x, G)
+        # a permutation of each pixel's channels ...
+        np.testing.assert_array_equal(np.sort(y, axis=-1), np.sort(x, axis=-1))
+        # ... undone by the shuffle with the roles of G and C^ exchanged
+        np.testing.assert_array_equal(O.channel_shuffle(y, C), x)
+        if G == 1:
+            np.testing.assert_array_equal(y, x)
+        # output group 0 holds the first C^/G channels of every group, in turn
+        if C % G == 0:
+            v = x.reshape(2, 3, G, C)
+            np.testing.assert_array_equal(y[..., :G], v[..., :, 0])
+
+
 def test_conv_layer_shuffle_writes_branch_one_group_on():
     """With an identity residual and zero weights in all groups but one, only
     the destination group (g+s) mod G changes."""
