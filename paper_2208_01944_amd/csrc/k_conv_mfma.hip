@@ -508,21 +508,37 @@ typedef double dbl2 __attribute__((ext_vector_type(2)));
 // constants carry the factor 4); its shortcut term rm c / 4 is added in
 // fp32, exact because the layer's |t| + 3 |rm| stays below 2^24 (a multiple
 // of 1/4 below 2^22 fits the 24-bit significand).
-template <int BO, int CB, int PB, int RB, typename AccV>
+// LAZY (2-bit shortcut, PB = 2): rw is unused; each channel block's shortcut
+// words are read from LDS at rwl + 8 cb (pixel block 0) and + rws (pixel
+// block 1) when that block is processed, which keeps fewer registers live.
+template <int BO, int CB, int PB, int RB, typename AccV, bool LAZY = false>
 __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &geo, AccV (&acc)[CB][PB],
                                         const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
-                                        int l32, int half, const RqConst *rq, const int32_t *rm) {
+                                        int l32, int half, const RqConst *rq, const int32_t *rm,
+                                        uint32_t rwl = 0, uint32_t rws = 0) {
+  static_assert(!LAZY || PB == 2, "lazy shortcut reads are written for two pixel blocks");
   constexpr int bo = BO;
   constexpr uint32_t qmax = (1u << BO) - 1u;
   const int lsc = geo.scale == 16 ? 4 : 0;
-  dbl2 kn[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) kn[e] = dbl2{rq[4 * half + e].s, rq[4 * half + e].o};
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     const int kc = ch0 + cb * 32;
-    const int csb = g * a.cout + kc;
     uint32_t qv[PB][4];
+    uint32_t rwc[PB][2];
+    if constexpr (RB == 2 && LAZY) {
+      uint2 r0, r1;
+      asm volatile(
+          "ds_read_b64 %0, %2\n\t"
+          "ds_read_b64 %1, %3\n\t"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(r0), "=&v"(r1)
+          : "v"(rwl + 8 * cb), "v"(rwl + 8 * cb + rws));
+      rwc[0][0] = r0.x; rwc[0][1] = r0.y;
+      rwc[1][0] = r1.x; rwc[1][1] = r1.y;
+    } else {
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) { rwc[pb][0] = rw[cb][pb][0]; rwc[pb][1] = rw[cb][pb][1]; }
+    }
 #pragma unroll
     for (int qi = 0; qi < 4; ++qi) {
       // one quad at a time: without this the scheduler hoists the constant
@@ -531,11 +547,7 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
       const int cq = 8 * qi + 4 * half;
       dbl2 k[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) k[e] = kn[e];
-      // next quad's constants (the last one of a block wraps harmlessly)
-      const int nxt = (qi < 3 ? cb * 32 + cq + 8 : (cb + 1 < CB ? (cb + 1) * 32 + 4 * half : 0));
-#pragma unroll
-      for (int e = 0; e < 4; ++e) kn[e] = dbl2{rq[nxt + e].s, rq[nxt + e].o};
+      for (int e = 0; e < 4; ++e) k[e] = dbl2{rq[cb * 32 + cq + e].s, rq[cb * 32 + cq + e].o};
       v4i rmu = {0, 0, 0, 0};
       if constexpr (RB != 0) rmu = *(const v4i *)(rm + cb * 32 + cq);
 #pragma unroll
@@ -547,11 +559,11 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
         if constexpr (RB == 2 && FACC) {
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            v[e] = __builtin_fmaf((float)rmu[e] * 0.25f, (float)chunk_code(rw[cb][pb], cq + e, 2), v[e]);
+            v[e] = __builtin_fmaf((float)rmu[e] * 0.25f, (float)chunk_code(rwc[pb], cq + e, 2), v[e]);
         } else if constexpr (RB == 2) {
           // |res_mult| < 2^15 and codes < 4: 24-bit signed products
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] += __mul24(rmu[e] << lsc, chunk_code(rw[cb][pb], cq + e, 2));
+          for (int e = 0; e < 4; ++e) v[e] += __mul24(rmu[e] << lsc, chunk_code(rwc[pb], cq + e, 2));
         } else if constexpr (RB < 0) {
           const int64_t mp = mbase + pb * 32 + l32;
           int rc[4];
@@ -1265,9 +1277,12 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
     const int g = c_it.combo / ncb;
     const int gd = (g + a.shuffle) % G;
     uint32_t rw[CB][PB][2] = {};
-    if constexpr (RB == 2) {  // this lane's shortcut codes: pixel block pb, channel block cb
-      const uint32_t ra = lds_base + kStages * SST + ((c_tile - t_begin) & 1) * RSB +
-                          (uint32_t)((wm * PB * 32 + l32) * RPX + wn * CB * 8);
+    // this lane's shortcut codes: pixel block pb, channel block cb at
+    // ra + pb 32 RPX + 8 cb (the FP4 build reads them per channel block)
+    const uint32_t ra = RB == 2 ? lds_base + kStages * SST + ((c_tile - t_begin) & 1) * RSB +
+                                      (uint32_t)((wm * PB * 32 + l32) * RPX + wn * CB * 8)
+                                : 0u;
+    if constexpr (RB == 2 && !FP4) {
       uint2 r00, r01, r10, r11;  // r[pb][cb]
       asm volatile(
           "ds_read_b64 %0, %4\n\t"
@@ -1283,8 +1298,9 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
       rw[1][1][0] = r11.x; rw[1][1][1] = r11.y;
     }
     const int rec = (c_it.combo == combo0 ? 0 : TN) + wn * CB * 32;  // first record of this wave's channels
-    epilogue_fast_bo<2, CB, PB, RB>(a, geo, acc, rw, (int64_t)pt * TM + wm * PB * 32, g, gd,
-                                    cbk * TN + wn * CB * 32, l32, half, rq_area + rec, rm_area + (RB ? rec : 0));
+    epilogue_fast_bo<2, CB, PB, RB, typename std::remove_reference<decltype(acc[0][0])>::type, FP4>(
+        a, geo, acc, rw, (int64_t)pt * TM + wm * PB * 32, g, gd, cbk * TN + wn * CB * 32, l32, half, rq_area + rec,
+        rm_area + (RB ? rec : 0), ra, 32 * RPX);
   };
   // LDS addresses of this lane's operands in stage 0: activation half row
   // of pixel block 0, weight unit (j = 0) of channel block 0
