@@ -42,6 +42,9 @@ def parse():
                     help="only turn the rocprofv3 outputs under DIR (kt/, fetch/, write/, cfetch/, "
                          "cwrite/ and bench.json, made by the commands written into the summaries) "
                          "into the text summaries under profiles/ and exit")
+    ap.add_argument("--table2", action="store_true",
+                    help="only run the Table 2 analogue (PalQuant against the dense M-bit network and "
+                         "the bit-decomposition workload, forward only, batch --batch) and exit")
     ap.add_argument("--hbm-copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (the calibration "
                          "kernel for the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -209,6 +212,46 @@ def conv_kernel(L, ci, co, k):
     return "conv_tile_kernel[fp4]" if fp4 else "conv_tile_kernel[int8]"
 
 
+def table2(args):
+    """On-GPU analogue of the paper's Table 2 for M = 2G bits at B = 2: the
+    PalQuant ResNet-18 (G groups of 2-bit convs), the dense M-bit network of
+    the original width (G = 1, only M = 4 is a supported code width), and the
+    workload of the Eq. 4 bit-decomposition (G^2 2-bit products of the full
+    width, run as a dense 2-bit network with G-fold widths: the same MACs
+    and operand bytes, without the final shift-add).  One JSON line per G."""
+    import torch
+    from paper_2208_01944_amd import inputs as I
+    from paper_2208_01944_amd import palq
+
+    ctx = palq.Context(0)
+    n = args.batch
+
+    def timed(spec):
+        net = palq.Net(ctx, spec)
+        x = ctx.pack(spec["x"], 1, 8, signed=True)
+        logits = torch.empty(n * net.classes, dtype=torch.int32, device=ctx.dev)
+        for _ in range(max(args.warmup, 1)):
+            net.forward(x.buf, logits)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            net.forward(x.buf, logits)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        return {"images_per_s": n / dt, "ms_per_forward": dt * 1e3, "int_ops": net.ops}
+
+    for G in (2, 3, 4):
+        row = {"table2": f"ResNet-18, M = {2 * G} bits as G = {G} x B = 2", "batch": n}
+        row["palquant"] = timed(I.resnet18(n=n, groups=G, bits=2))
+        row["dense_m_bit"] = (timed(I.resnet18(n=n, groups=1, bits=4)) if 2 * G == 4
+                              else f"not run: {2 * G}-bit codes are outside the supported widths (2, 3, 4)")
+        row["bit_decomposition_workload"] = timed(I.resnet18(n=n, groups=1, bits=2, width_mult=G))
+        for k in ("dense_m_bit", "bit_decomposition_workload"):
+            if isinstance(row[k], dict):
+                row[f"speedup_vs_{k}"] = row["palquant"]["images_per_s"] / row[k]["images_per_s"]
+        print(json.dumps(row), flush=True)
+
+
 def cpu_baseline(spec, x_f32, l, u, budget_s):
     """The oracle (as it stands) on a bounded sample of the same workload:
     whole images (quantise + forward), one at a time, until the budget is
@@ -238,6 +281,9 @@ def main():
         return
     if args.hbm_copy_probe:
         copy_probe(args.hbm_copy_probe)
+        return
+    if args.table2:
+        table2(args)
         return
     import torch
     from paper_2208_01944_amd import inputs as I

@@ -1551,6 +1551,10 @@ int64_t acc_bound_of(const ConvArgs &a) {
 }  // namespace
 
 bool fp4_applies(const ConvArgs &a);
+bool tile_kernel_applies(const ConvArgs &a);
+bool stem_tile_applies(const ConvArgs &a);
+
+bool conv_mfma_general_fits(const ConvArgs &a) { return pick_cb(a, make_geo(a)) > 0; }
 
 bool conv_mfma_supported(const ConvArgs &a) {
   if (a.cout % 32 != 0) return false;
@@ -1564,7 +1568,9 @@ bool conv_mfma_supported(const ConvArgs &a) {
     if (a.in.cpg % 64 != 0 || a.kh * a.kw > 32) return false;
     if (a.proj.data && (a.proj.bits != b || a.proj.cpg % 64 != 0 || a.proj.is_signed)) return false;
   }
-  return pick_cb(a, make_geo(a)) > 0;
+  // the general build needs the filter in LDS; layers longer than that
+  // still run on the tiled kernel (its fast epilogue)
+  return pick_cb(a, make_geo(a)) > 0 || tile_kernel_applies(a) || stem_tile_applies(a);
 }
 
 ConvPlan conv_mfma_plan(const ConvArgs &a) {
@@ -1740,9 +1746,9 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
   geo.wp = wp;
   geo.rq = (const RqConst *)thr;
   int cb = pick_cb(a, geo);
-  if (cb == 0) return hipErrorNotSupported;
+  if (cb == 0 && epi != 0) return hipErrorNotSupported;  // no general build for this layer
   int pb = 1;
-  tile_override(a, geo, cb, pb);
+  if (cb > 0) tile_override(a, geo, cb, pb);
   if (a.acc_dump || a.out.bits == 3) epi = 1;
   if (epi != 1 && stem_tile_applies(a)) {
     hipError_t e = launch_tile<2, 2, 2, 2, true, PALQ_STEM_STAGES>(a, geo, s);
@@ -1788,6 +1794,7 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
     if (e != hipSuccess || epi == 0) return e;
     return dispatch_bits<2>(a, geo, cb, pb, 1, s);  // unknown: the general build decides on the device
   }
+  if (cb == 0) return hipErrorNotSupported;  // neither tiled build took the layer
   if (is_stem(a)) {
     if (cb == 2) return pb == 2 ? launch_stem<2, 2>(a, geo, epi, s) : launch_stem<2, 1>(a, geo, epi, s);
     return pb == 2 ? launch_stem<1, 2>(a, geo, epi, s) : launch_stem<1, 1>(a, geo, epi, s);

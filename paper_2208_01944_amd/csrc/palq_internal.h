@@ -72,8 +72,12 @@ struct ConvArgs {
 
 // Kernel launchers (return hipError_t of the launch).
 hipError_t launch_conv_direct(const ConvArgs &a, hipStream_t s);
-// Whether the MFMA kernel takes this layer.
+// Whether the MFMA kernels take this layer.
 bool conv_mfma_supported(const ConvArgs &a);
+// Whether the general (persistent, filter-in-LDS) build fits this layer;
+// when it does not, a supported layer runs only on the tiled kernel's fast
+// epilogue and launch_conv_mfma needs epi == 0.
+bool conv_mfma_general_fits(const ConvArgs &a);
 // Device scratch the MFMA kernel reads besides the ConvArgs tensors:
 // weights in MFMA operand order and, for 2-bit outputs, requant thresholds.
 struct ConvPlan {

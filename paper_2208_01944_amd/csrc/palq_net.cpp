@@ -455,7 +455,12 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
   }
   // the requant constants are final: fix each MFMA layer's epilogue build
   for (Layer &NL : net->layers)
-    if (NL.spec.op == PALQ_OP_CONV && NL.use_mfma) NL.epi = conv_mfma_epilogue(NL.conv, NL.thr);
+    if (NL.spec.op == PALQ_OP_CONV && NL.use_mfma) {
+      NL.epi = conv_mfma_epilogue(NL.conv, NL.thr);
+      // a layer too long for the general build's LDS runs its general
+      // epilogue on the direct kernel
+      if (NL.epi != 0 && !conv_mfma_general_fits(NL.conv)) NL.use_mfma = false;
+    }
   if (flags & PALQ_NET_TIMING) {
     net->events.assign((size_t)kRing * (n_layers + 1), nullptr);
     for (auto &ev : net->events)

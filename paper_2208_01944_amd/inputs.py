@@ -173,7 +173,7 @@ def _stem(g, layers, groups, bits, width=64):
 
 
 def resnet18(n=64, groups=4, bits=2, hw=224, classes=1000, seed=SEED_BASE + 3, stages=(2, 2, 2, 2),
-             modules=False, channel_shuffle=False):
+             modules=False, channel_shuffle=False, width_mult=1):
     """ResNet-18 topology with every 3x3 conv a G-group b-bit conv at the
     original width per group; conv2 of each basic block adds the shortcut in
     int32 before requantisation and writes its branch one cyclic step on;
@@ -182,13 +182,16 @@ def resnet18(n=64, groups=4, bits=2, hw=224, classes=1000, seed=SEED_BASE + 3, s
     stage's first (strided) conv, at the stage's width and resolution
     (Section 4.3 places the module at the beginning of each stage).
     channel_shuffle: the per-stage channel shuffle (Section 4.3, Table 3) at
-    the end of the first block of stages 2-4."""
+    the end of the first block of stages 2-4.  width_mult scales every
+    stage width (and the stem's output), e.g. for the dense workload of the
+    bit-decomposition baseline (Eq. 4: G^2 B-bit products of full width)."""
     g = rng(seed)
     x = codes(g, (n, hw, hw, 3), 8, True)
     layers = []
-    cur, nid = _stem(g, layers, groups, bits)
-    ch = 64
-    for si, (width, nblk) in enumerate(zip((64, 128, 256, 512), stages)):
+    cur, nid = _stem(g, layers, groups, bits, width=64 * width_mult)
+    ch = 64 * width_mult
+    for si, (width, nblk) in enumerate(zip((64 * width_mult, 128 * width_mult, 256 * width_mult,
+                                           512 * width_mult), stages)):
         for b in range(nblk):
             s = 2 if (si > 0 and b == 0) else 1
             t1 = nid

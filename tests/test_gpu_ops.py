@@ -400,3 +400,20 @@ def test_channel_shuffle_matches_oracle(ctx, bits, G, C):
     ctx.channel_shuffle(xt, out)
     ctx.sync()
     np.testing.assert_array_equal(ctx.unpack(out), O.channel_shuffle(x, G))
+
+
+@pytest.mark.parametrize("big_bias", [False, True])
+def test_conv_filter_longer_than_lds(ctx, torch, big_bias):
+    """A 2-bit layer whose filter (K = 9 x 1024) is too long for the general
+    build's filter-in-LDS: the tiled kernel takes it; the accumulator dump and
+    (big_bias: the int64 requant fallback) go to the direct kernel."""
+    say(f"conv K=9x1024 G=1 big_bias={big_bias}")
+    case = I.single_layer(77, n=1, h=7, w=7, groups=1, cin=1024, cout=128, shuffle=0)
+    if big_bias:
+        L = case["layer"]
+        L["mult"] = np.full_like(L["mult"], 1 << 23)
+        L["shift"] = np.full_like(L["shift"], 40)
+        L["bias"] = np.full_like(L["mult"], 1 << 29)
+    q, acc, rq, racc = run_conv(ctx, torch, case, centred=not big_bias)
+    np.testing.assert_array_equal(acc, racc)
+    np.testing.assert_array_equal(q, rq)
