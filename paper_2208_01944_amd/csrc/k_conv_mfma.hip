@@ -516,7 +516,7 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
                                         const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
                                         int l32, int half, const RqConst *rq, const int32_t *rm,
                                         uint32_t rwl = 0, uint32_t rws = 0) {
-  static_assert(!LAZY || PB == 2, "lazy shortcut reads are written for two pixel blocks");
+  static_assert(!LAZY || PB == 2 || PB == 4, "lazy shortcut reads are written for two or four pixel blocks");
   constexpr int bo = BO;
   constexpr uint32_t qmax = (1u << BO) - 1u;
   const int lsc = geo.scale == 16 ? 4 : 0;
@@ -525,7 +525,7 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
     const int kc = ch0 + cb * 32;
     uint32_t qv[PB][4];
     uint32_t rwc[PB][2];
-    if constexpr (RB == 2 && LAZY) {
+    if constexpr (RB == 2 && LAZY && PB == 2) {
       uint2 r0, r1;
       asm volatile(
           "ds_read_b64 %0, %2\n\t"
@@ -535,6 +535,18 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
           : "v"(rwl + 8 * cb), "v"(rwl + 8 * cb + rws));
       rwc[0][0] = r0.x; rwc[0][1] = r0.y;
       rwc[1][0] = r1.x; rwc[1][1] = r1.y;
+    } else if constexpr (RB == 2 && LAZY) {
+      uint2 r[4];
+      asm volatile(
+          "ds_read_b64 %0, %4\n\t"
+          "ds_read_b64 %1, %5\n\t"
+          "ds_read_b64 %2, %6\n\t"
+          "ds_read_b64 %3, %7\n\t"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
+          : "v"(rwl + 8 * cb), "v"(rwl + 8 * cb + rws), "v"(rwl + 8 * cb + 2 * rws), "v"(rwl + 8 * cb + 3 * rws));
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) { rwc[pb][0] = r[pb & 3].x; rwc[pb][1] = r[pb & 3].y; }
     } else {
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb) { rwc[pb][0] = rw[cb][pb][0]; rwc[pb][1] = rw[cb][pb][1]; }
@@ -1065,6 +1077,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   static_assert(FP4 ? (WP == NT / 2 || WP == NT || WP == 2 * NT) : (WLD == 1 || WLD == 2), "weight loads per thread");
   static_assert(XP == NT / 2 || XP % NT == 0, "activation pieces");
   static_assert(!STEM || (XALL && RB == 0), "stem layout");
+  static_assert(STEM || XP <= NT, "grouped layers: at most one activation piece (one pixel) per thread");
   static_assert(!FP4 || !STEM, "FP4 takes 2-bit grouped layers");
   // loads per K-block of the waves with the fewest (the ring waits on that).
   // FP4: the last WP threads load one weight piece each (WP < NT), or all
@@ -1074,11 +1087,12 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   constexpr int RMB = RB ? 2 * TN * 4 : 0;            // their shortcut multipliers
   constexpr int RPX = TN / 4;                          // shortcut code bytes per pixel of a tile
   constexpr int RSB = RB ? TM * RPX : 0;               // shortcut codes of one tile
-  static_assert(RB == 0 || TM * RPX == NT * 16, "one 16-byte shortcut piece per thread");
+  constexpr int RPT = RB ? RSB / (NT * 16) : 0;      // 16-byte shortcut pieces per thread
+  static_assert(RB == 0 || (RPT >= 1 && RSB == RPT * NT * 16), "whole shortcut pieces per thread");
   __shared__ __attribute__((aligned(16))) uint8_t lds[kStages * SST + 2 * RSB];
   __shared__ RqConst rq_area[2 * TN];
   __shared__ int32_t rm_area[RB ? 2 * TN : 1];
-  static_assert(CB == 2 && PB == 2, "compute() below is written out for 2 x 2 blocks");
+  static_assert(CB == 2 && (PB == 2 || (FP4 && PB == 4)), "compute() below is written out for 2 x 2 (FP4: 2 x 4) blocks");
   using Raw = RawT<B, false>;
 
   if (needs_general(a, geo, RB)) return;
@@ -1191,16 +1205,21 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
     const bool live = f_tile < t_end;
     uint8_t *ws = lds + st * SST + h * SSB;
     if constexpr (RB == 2) {
-      if (f_kb == 0) {  // the tile's shortcut codes, 16 bytes per thread
+      if (f_kb == 0) {  // the tile's shortcut codes, RPT 16-byte pieces per thread
         const int pt = f_it.pt;
         const int cbk = f_it.combo % ncb;
         const int gd = (f_it.combo / ncb + a.shuffle) % G;
-        const int m = pt * TM + tid / (RPX / 16);
-        const uint32_t ro = live && m < geo.M
-                                ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.row + cbk * RPX + (tid % (RPX / 16)) * 16)
-                                : kOob;
         uint8_t *rb = lds + kStages * SST + ((f_tile - t_begin) & 1) * RSB;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(rb + wave * 1024), 16, (int)ro, 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < RPT; ++i) {
+          const int c = tid + i * NT;
+          const int m = pt * TM + c / (RPX / 16);
+          const uint32_t ro = live && m < geo.M ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.row + cbk * RPX +
+                                                             (c % (RPX / 16)) * 16)
+                                                : kOob;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(rb + i * NT * 16 + wave * 1024), 16, (int)ro, 0,
+                                                   0, 0);
+        }
       }
     }
     if constexpr (FP4 && WP >= NT) {
@@ -1312,7 +1331,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   // address register a later read of the statement still uses).
   struct OpsG { uint2 x0, x1; v4i a00, a01, a10, a11; };
   struct OpsS { v4i x0a, x0b, x1a, x1b, a00, a01, a10, a11; };  // stem: x[pb] words 0-3 / 4-7
-  struct OpsF { uint2 x0, x1; v4i a0, a1; };                     // FP4: a[cb]
+  struct OpsF { uint2 x[PB]; v4i a0, a1; };                     // FP4: x[pb], a[cb]
   using Ops = typename std::conditional<STEM, OpsS, typename std::conditional<FP4, OpsF, OpsG>::type>::type;
   auto read_ops = [&](int stage, int h, Ops &o) __attribute__((always_inline)) {
     const uint32_t xa = xaddr0 + stage * SST + h * SSB, aa = aaddr0 + stage * SST + h * SSB;
@@ -1331,6 +1350,18 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
             "=&v"(o.a11)
           : "v"(xa), "v"(aa));
       return;
+    } else if constexpr (FP4 && PB == 4) {
+      asm volatile(
+          "ds_read_b64 %0, %6\n\t"
+          "ds_read_b64 %1, %6 offset:512\n\t"
+          "ds_read_b64 %2, %6 offset:1024\n\t"
+          "ds_read_b64 %3, %6 offset:1536\n\t"
+          "ds_read_b128 %4, %7\n\t"
+          "ds_read_b128 %5, %7 offset:1024\n\t"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(o.x[0]), "=&v"(o.x[1]), "=&v"(o.x[2]), "=&v"(o.x[3]), "=&v"(o.a0), "=&v"(o.a1)
+          : "v"(xa), "v"(aa));
+      return;
     } else if constexpr (FP4) {
       asm volatile(
           "ds_read_b64 %0, %4\n\t"
@@ -1338,7 +1369,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
           "ds_read_b128 %2, %5\n\t"
           "ds_read_b128 %3, %5 offset:1024\n\t"
           "s_waitcnt lgkmcnt(0)"
-          : "=&v"(o.x0), "=&v"(o.x1), "=&v"(o.a0), "=&v"(o.a1)
+          : "=&v"(o.x[0]), "=&v"(o.x[1]), "=&v"(o.a0), "=&v"(o.a1)
           : "v"(xa), "v"(aa));
       return;
     } else
@@ -1368,7 +1399,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
     } else if constexpr (FP4) {
       // E2M1 operands use the low four registers of each v8i (the rest is
       // ignored for this format, left undefined here)
-      const uint2 xw[PB] = {o.x0, o.x1};
+      const uint2 *xw = o.x;
       const v4i A[CB] = {o.a0, o.a1};
       v8i Bop[PB], Aop[CB];
 #pragma unroll
@@ -1630,6 +1661,25 @@ int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr) {
   return flag != 0 ? 1 : 0;
 }
 
+// Compute units of the current device (cached per device).
+int cu_count() {
+  static std::mutex mu;
+  static int devs[16], vals[16], used = 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  for (int i = 0; i < used; ++i)
+    if (devs[i] == dev) return vals[i];
+  int cus = 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 256;
+  if (used < 16) {
+    devs[used] = dev;
+    vals[used] = cus;
+    ++used;
+  }
+  return cus;
+}
+
 // Pixel tile of the tiled kernel for 128-channel blocks, for tuning
 // (PALQ_TILE_TM = 64, 128 or 256; 0 = the build's default).
 int tile_tm() {
@@ -1768,6 +1818,22 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
       tm64 = e && atoi(e) == 128 ? 128 : 256;
     }
     const int tm = tile_tm() ? tile_tm() : 128;
+    // 2 x 4 blocks per wave (128-channel blocks, 256-pixel tiles) where the
+    // bigger tiles leave every CU at least one and do not lengthen the
+    // busiest CU's share: 2 ceil(T4 / CUs) <= ceil(T2 / CUs) tile units.
+    // PALQ_TILE_PB = 2 or 4 forces one for tuning.
+    static int pb_env = -1;
+    if (pb_env < 0) {
+      const char *e = getenv("PALQ_TILE_PB");
+      pb_env = e ? atoi(e) : 0;
+    }
+    bool pb4 = pb_env == 4;
+    if (pb_env != 2 && pb_env != 4 && a.cout % 128 == 0) {
+      const int64_t m = geo.M, tiles_per_px = (int64_t)(a.cout / 128) * a.in.groups;
+      const int64_t t2 = (m + 127) / 128 * tiles_per_px, t4 = (m + 255) / 256 * tiles_per_px;
+      const int64_t cus = cu_count();
+      pb4 = t4 >= cus && 2 * ((t4 + cus - 1) / cus) <= (t2 + cus - 1) / cus;
+    }
     static int kpi = -1;  // K-blocks per ring stage (PALQ_TILE_KPI=2 for tuning)
     if (kpi < 0) {
       const char *e = getenv("PALQ_TILE_KPI");
@@ -1775,7 +1841,9 @@ hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t 
     }
     constexpr int S4 = PALQ_TILE_STAGES;
     hipError_t e;
-    if (kpi == 2 && geo.kb_total >= S4 * 2)
+    if (pb4 && a.cout % 128 == 0)
+      e = launch_tile<2, 4, 2, 2, false, S4, true>(a, g4, s);
+    else if (kpi == 2 && geo.kb_total >= S4 * 2)
       e = a.cout % 128 != 0 ? launch_tile<2, 2, 1, 4, false, S4, true, 2>(a, g4, s)
                             : launch_tile<2, 2, 2, 2, false, S4, true, 2>(a, g4, s);
     else
