@@ -105,6 +105,38 @@ __device__ inline int quant_one(float x, float l, float rng, float qmax) {
   return (int)rintf(t * qmax);
 }
 
+// 8-bit codes of 3-channel pixels (one 4-byte row each, the image input):
+// one thread per 4 pixels, three 16-byte loads and one 16-byte store.
+__global__ void quantize_px3_kernel(const float *x, float l, float u, const uint32_t *enc, ActView out,
+                                    int64_t quads) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= quads) return;
+  bool degenerate = false;
+  if (enc) {
+    const bool empty = enc[0] == 0xffffffffu && enc[1] == 0u;
+    l = ord2f(enc[0]);
+    u = ord2f(enc[1]);
+    degenerate = empty || !(u > l);
+  }
+  const float rng = u - l;
+  const int off = out.is_signed ? 128 : 0;
+  const float4 *src = (const float4 *)(x + 12 * t);
+  const float4 f0 = src[0], f1 = src[1], f2 = src[2];
+  const float v[12] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w, f2.x, f2.y, f2.z, f2.w};
+  uint32_t w[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    uint32_t word = 0;
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+      const int q = (degenerate ? 0 : quant_one(v[3 * p + c], l, rng, 255.0f)) - off;
+      word |= ((uint32_t)q & 0xffu) << (8 * c);
+    }
+    w[p] = word;
+  }
+  *(uint4 *)(out.data + 16 * t) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 // One thread per packed word (b in {2, 4, 8}) or 32-code chunk (b = 3).
 __global__ void quantize_kernel(const float *x, float l, float u, const uint32_t *enc, ActView out,
                                 int64_t rows, int units) {
@@ -559,6 +591,12 @@ hipError_t launch_quantize(const float *x, float l, float u, const float *range,
   const int64_t rows = (int64_t)out.n * out.h * out.w * out.groups;
   const int units = out.bits == 3 ? (out.cpg + 31) / 32 : (int)(out.row / 4);
   if (rows == 0) return hipSuccess;
+  if (out.bits == 8 && out.cpg == 3 && out.groups == 1 && out.row == 4 && rows % 4 == 0 &&
+      (((uintptr_t)x | (uintptr_t)out.data) & 15u) == 0) {
+    hipLaunchKernelGGL(quantize_px3_kernel, dim3(grid_for(rows / 4)), dim3(kBlock), 0, s, x, l, u,
+                       (const uint32_t *)range, out, rows / 4);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(quantize_kernel, dim3(grid_for(rows * units)), dim3(kBlock), 0, s, x, l, u,
                      (const uint32_t *)range, out, rows, units);
   return hipGetLastError();

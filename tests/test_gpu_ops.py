@@ -417,3 +417,27 @@ def test_conv_filter_longer_than_lds(ctx, torch, big_bias):
     q, acc, rq, racc = run_conv(ctx, torch, case, centred=not big_bias)
     np.testing.assert_array_equal(acc, racc)
     np.testing.assert_array_equal(q, rq)
+
+
+@pytest.mark.parametrize("signed", [True, False])
+@pytest.mark.parametrize("calibrate", [False, True])
+def test_quantize_image_path(ctx, torch, signed, calibrate):
+    """The 3-channel 8-bit image input (the four-pixels-per-thread path), with
+    NaN/inf and exact ties, fixed and calibrated ranges."""
+    say(f"quantize image 8-bit signed={signed} calibrate={calibrate}")
+    g = np.random.default_rng(31 + signed)
+    x = g.normal(0, 1.2, (2, 9, 14, 3)).astype(np.float32)
+    x.flat[::61] = np.nan
+    if not calibrate:
+        x.flat[5::97] = np.inf
+        x.flat[7::113] = -np.inf
+    x.flat[1:4] = [-3.0 + 6.0 * 0.5 / 255.0, 0.0, 3.0]
+    out = ctx.empty_act(2, 9, 14, 1, 3, 8, signed)
+    if calibrate:
+        ctx.quantize(ctx.upload(x), float("nan"), float("nan"), out)
+        l, u = O.calibrate_range(x)
+    else:
+        l, u = -3.0, 3.0
+        ctx.quantize(ctx.upload(x), l, u, out)
+    ctx.sync()
+    np.testing.assert_array_equal(ctx.unpack(out), O.quantize(x, l, u, 8, signed))
