@@ -1467,6 +1467,297 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   }
 }
 
+// ---------------------------------------------------------------- stem + max pool
+// The 8-bit stem followed by the 3x3 / stride 2 / pad 1 max pool, fused: the
+// max pool is taken over the stem's int32 accumulators and only the pooled
+// values are requantised.  Exact: the requant q = clamp(floor((t M +
+// 2^(sh-1)) / 2^sh), 0, 2^b - 1) is non-decreasing in t for M >= 0 (the
+// fast epilogue, which this kernel has, requires that), so the max of the
+// requantised values equals the requant of the max.
+//
+// A tile is one output row (wo <= 127 columns) of one image and 128 output
+// channels, 2 x 2 waves of 2 x 2 32 x 32 blocks as in the tiled stem (wave
+// (wn, wm): channels 64 wn .. + 63).  Column halves overlap by one column:
+// wm = 0 holds columns 0 .. 63, wm = 1 columns 63 .. 126, lane l of pixel
+// block pb column 63 wm + 2 l + pb.  Pooled column 32 wm + l then needs the
+// lane's two columns and one of its neighbour lane (l - 1 for wm = 0, l + 1
+// for wm = 1), a __shfl within the wave.  Work units are pooled rows
+// (image, channel block, k); a unit takes output rows 2k and 2k + 1, and
+// pooled row k also needs row 2k - 1, which the previous unit of the same
+// run left in registers (a run starting inside an image recomputes it).
+namespace sp {
+constexpr int kSpStages = 3;
+constexpr int NT = 256;
+constexpr int WST = 4 * kSlab;   // four 32-channel weight slabs of a K-block
+constexpr int XST = 128 * 64;    // 128 pixel slots x two filter rows of 8 four-byte taps
+constexpr int SST = WST + XST;
+
+// Row tiles of a run: phase 0 recomputes row 2k - 1, 1 is row 2k, 2 row 2k + 1.
+struct RowIt {
+  int u, phase;
+};
+__device__ __forceinline__ RowIt row_first(int u, int ho2) { return {u, (u % ho2) > 0 ? 0 : 1}; }
+__device__ __forceinline__ void row_next(RowIt &it, int ho, int ho2) {
+  if (it.phase == 0) { it.phase = 1; return; }
+  if (it.phase == 1 && 2 * (it.u % ho2) + 1 < ho) { it.phase = 2; return; }
+  ++it.u;
+  it.phase = 1;
+}
+__device__ __forceinline__ int row_of(const RowIt &it, int ho2) {
+  const int k = it.u % ho2;
+  return it.phase == 0 ? 2 * k - 1 : 2 * k + (it.phase - 1);
+}
+// column of pixel slot s (0 .. 127)
+__device__ __forceinline__ int slot_col(int s) { return 63 * (s >> 6) + 2 * (s & 31) + ((s >> 5) & 1); }
+// LDS swizzle of the activation stage: quarter q of slot s sits at 16-byte
+// unit 4 s + (q ^ xsw(s)), so that the operand reads of 8 (or 16)
+// consecutive lanes, consecutive slots at one quarter, touch distinct banks.
+__device__ __forceinline__ int xsw(int s) { return ((s >> 1) ^ (s >> 3)) & 3; }
+}  // namespace sp
+
+// Runs hold at most ho2 units (the launcher's grid), so a run meets at most
+// two channel blocks, cbb0 and cbb0 + 1 (mod ncb): their requant constants
+// sit in LDS.
+__global__ __launch_bounds__(sp::NT, 3) void stem_pool_kernel(ConvArgs a, Geo geo, ActView po, int units) {
+  using namespace sp;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kSpStages * SST];
+  __shared__ RqConst rq_area[256];
+  if (needs_general(a, geo, 0)) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int wn = wave >> 1, wm = wave & 1;
+  const int ho = a.ho, wo = a.wo, ho2 = po.h, wo2 = po.w;
+  const int ncb = a.cout / 128;
+  // balanced runs of units per XCD (as the tiled kernel's tiles)
+  const int P = (int)gridDim.x >> 3;
+  const int x = (int)(blockIdx.x & 7), y = (int)(blockIdx.x >> 3);
+  const int Tq = units >> 3, Tr = units & 7;
+  const int Tx = Tq + (x < Tr ? 1 : 0);
+  const int base = Tx / P, ex = Tx % P;
+  const int u_begin = x * Tq + min(x, Tr) + y * base + min(y, ex);
+  const int u_end = u_begin + base + (y < ex ? 1 : 0);
+  if (u_begin >= u_end) return;  // no barrier yet
+  const int cbb0 = (u_begin / ho2) % ncb;
+  for (int c = tid; c < 256; c += NT) rq_area[c] = geo.rq[(c < 128 ? cbb0 : (cbb0 + 1) % ncb) * 128 + (c & 127)];
+  __syncthreads();
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
+  typedef __attribute__((address_space(3))) void *lds_ptr;
+  const auto rw_src = make_rsrc(geo.wp, (int64_t)a.cout * geo.kb_total * 64);
+  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
+  const auto rout = make_rsrc(po.data, (int64_t)po.n * po.h * po.w * po.pixel);
+  const int pixb = (int)a.in.pixel, rowb = a.in.w * pixb;
+  const int KB = geo.kb_total;
+
+  // ---- fetcher: K-block f_kb of row tile f_it.  Weight piece p = tid + 256 i
+  // is piece p % 128 of slab p / 128; activation piece p is quarter
+  // q = (p % 4) ^ xsw(s) (filter row 2 kb + q / 2, bytes 16 (q % 2) ..) of
+  // slot s = p / 4.
+  RowIt f_it = row_first(u_begin, ho2);
+  int f_kb = 0;
+  // per thread: the byte offset of each activation piece within an output
+  // row's input rows; per row: the row's offset.  A slot past the row's
+  // last column loads that column again: its accumulators duplicate a
+  // column of the same pooling window (the window of a pooled column that
+  // reaches past the row holds the last column), so the max ignores it.
+  // The two offsets share one register (16 bits each; the launcher checks
+  // that an input row pair fits).
+  uint32_t xcols = 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int sl = (tid >> 2) + 64 * i, c = min(slot_col(sl), wo - 1), q = (tid & 3) ^ xsw(sl);
+    xcols |= (uint32_t)((q >> 1) * rowb + c * a.stride * pixb + (q & 1) * 16) << (16 * i);
+  }
+  asm volatile("" : "+v"(xcols));  // one opaque register (the halves are not kept apart)
+  int xrow = 0;
+  uint32_t wb = 0;
+  const uint32_t wthr = (uint32_t)((tid >> 7) * KB * kSlab + (tid & 127) * 16);
+  auto tile_geometry = [&]() __attribute__((always_inline)) {
+    const int cbb = (f_it.u / ho2) % ncb, n = f_it.u / (ho2 * ncb);
+    wb = (uint32_t)(cbb * 4 * KB) * kSlab;
+    xrow = (n * a.in.h + row_of(f_it, ho2) * a.stride) * rowb;
+  };
+  tile_geometry();
+  auto fetch = [&](int st) __attribute__((always_inline)) {
+    const bool live = f_it.u < u_end;
+    uint8_t *ws = lds + st * SST;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {  // piece tid + 256 i: slab 2 i + tid / 128
+      const uint32_t woff = live ? wb + wthr + (uint32_t)((2 * i * KB + f_kb) * kSlab) : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + i * 4096 + wave * 1024), 16, (int)woff, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      // filter rows past kh (zero weights) may read the next image's rows
+      // or past the end (the buffer bound returns zeros)
+      const uint32_t off = live ? (uint32_t)xrow + __builtin_amdgcn_ubfe(xcols, 16 * i, 16) + (uint32_t)(2 * f_kb * rowb) : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rin, (lds_ptr)(ws + WST + i * 4096 + wave * 1024), 16, (int)off, 0, 0,
+                                               0);
+    }
+    if (++f_kb == KB) {
+      f_kb = 0;
+      row_next(f_it, ho, ho2);
+      tile_geometry();
+    }
+  };
+
+  // ---- compute side
+  RowIt c_it = row_first(u_begin, ho2);
+  int c_kb = 0;
+  v16i acc[2][2];     // [cb][pb]
+  int32_t st[2][16];  // per cb: row 2k - 1 pooled across columns, or the running max of rows 2k - 1, 2k
+  const uint32_t aaddr0 = lds_base + (uint32_t)(wn * 2 * kSlab + (half * 32 + l32) * 16);
+  // this lane's activation quarters 2 half + j of slot 64 wm + l32 (+ 32 pb)
+  const uint32_t xslot = lds_base + WST + (uint32_t)((wm * 64 + l32) * 64);
+  // (quarter 2 half + 1 at xaddr0 ^ 16: the stages are 1024-byte aligned)
+  const uint32_t xaddr0 = xslot + 16 * ((2 * half) ^ xsw(l32));
+  // the lane whose pooling neighbour would be in the other lane half
+  // (column -1 for wm = 0, column 127 for wm = 1)
+  const bool half_edge = wm ? lane == 31 : lane == 32;
+  // pooled column px = 32 wm + l; its byte offset in a pooled row plus this
+  // lane's word of the wave's channels (word 2 (4 cbb + 2 wn + cb) + half)
+  const int px = 32 * wm + l32;
+  int out_lane = px * (int)po.pixel + (wn * 4 + half) * 4;
+  asm volatile("" : "+v"(out_lane));  // kept as one 32-bit register
+  auto finish_row = [&]() __attribute__((always_inline)) {
+    const int k = c_it.u % ho2;
+    const int cbb = (c_it.u / ho2) % ncb, n = c_it.u / (ho2 * ncb);
+    // columns 2p - 1 .. 2p + 1 of pooled column p = 32 wm + l: the lane's
+    // two columns and column 2p - 1 from lane l - 1 (wm = 0) or 2p + 1 from
+    // lane l + 1 (wm = 1); then the rows.  st: row 2k - 1 (pooled across
+    // columns) before row 2k, the max of rows 2k - 1 and 2k before row
+    // 2k + 1; after the last row of pooled row k it holds that row, which is
+    // requantised; row 2k + 1, kept in nx, then becomes st for row k + 1.
+    int32_t nx[2][16];
+    auto pool_row = [&](auto WMC) __attribute__((always_inline)) {
+      constexpr int W = decltype(WMC)::value;
+      // neighbour column by a DPP wave shift (lane i reads lane i - 1 for
+      // wm = 0, i + 1 for wm = 1; the end lane keeps its own value); the
+      // lane whose neighbour lies in the other lane half takes its own
+      // other column instead (a duplicate leaves the max unchanged)
+      auto hmax = [&](int cb, int i) __attribute__((always_inline)) {
+        const int32_t v0 = acc[cb][0][i], v1 = acc[cb][1][i];
+        int32_t nb;
+        if constexpr (W == 0) {
+          nb = __builtin_amdgcn_update_dpp(v1, v1, 0x138 /* wave_shr:1 */, 0xf, 0xf, false);
+          nb = half_edge ? v1 : nb;
+        } else {
+          nb = __builtin_amdgcn_update_dpp(v0, v0, 0x130 /* wave_shl:1 */, 0xf, 0xf, false);
+          nb = half_edge ? v0 : nb;
+        }
+        return max(max(nb, v0), v1);
+      };
+      if (c_it.phase == 2) {
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            nx[cb][i] = hmax(cb, i);
+            st[cb][i] = max(st[cb][i], nx[cb][i]);
+          }
+      } else if (c_it.phase == 1 && k > 0) {
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) st[cb][i] = max(st[cb][i], hmax(cb, i));
+      } else {
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) st[cb][i] = hmax(cb, i);
+      }
+    };
+    if (wm == 0) pool_row(std::integral_constant<int, 0>{});
+    else pool_row(std::integral_constant<int, 1>{});
+    if (c_it.phase == 0 || (c_it.phase == 1 && 2 * k + 1 < ho)) return;
+    // requant the pooled row and store it: channel 128 cbb + 64 wn + 32 cb + 8 qi + 4 half + e
+    const int orow = ((n * ho2 + k) * wo2) * (int)po.pixel;
+    const RqConst *rq = rq_area + (cbb == cbb0 ? 0 : 128) + wn * 64;
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) {
+      uint32_t qv[4];
+#pragma unroll
+      for (int qi = 0; qi < 4; ++qi) {
+        __builtin_amdgcn_sched_barrier(0);  // one quad's constants at a time
+        const int cq = cb * 32 + 8 * qi + 4 * half;
+        uint32_t qword = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const double d = __builtin_fma((double)st[cb][4 * qi + e], rq[cq + e].s, rq[cq + e].o);
+          uint32_t q;
+          asm("v_cvt_u32_f64 %0, %1" : "=v"(q) : "v"(d));
+          qword |= min(q, 3u) << (2 * e);
+        }
+        qv[qi] = qword;
+      }
+      const uint32_t s0 = half ? qv[0] : qv[2];
+      const uint32_t s1 = half ? qv[1] : qv[3];
+      const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
+      const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
+      uint32_t Q[4];
+      if (half == 0) { Q[0] = qv[0]; Q[1] = r0; Q[2] = qv[1]; Q[3] = r1; }
+      else           { Q[0] = r0; Q[1] = qv[2]; Q[2] = r1; Q[3] = qv[3]; }
+      if (px < wo2)
+        __builtin_amdgcn_raw_buffer_store_b32(Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24), rout,
+                                              out_lane + cbb * 32 + cb * 8, orow, 0);
+    }
+    if (c_it.phase == 2) {
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) st[cb][i] = nx[cb][i];
+    }
+  };
+
+  // ring of kSpStages K-blocks over the run's row tiles, fetching
+  // kSpStages - 1 ahead (as the tiled kernel)
+  int rows = 0;
+  for (RowIt it = row_first(u_begin, ho2); it.u < u_end; row_next(it, ho, ho2)) ++rows;
+  const int total = rows * KB;
+  for (int s2 = 0; s2 < kSpStages - 1; ++s2) fetch(s2);
+  for (int gk = 0; gk < total; ++gk) {
+    if (c_kb == 0) {
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0;
+    }
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kSpStages - 2) * 4));
+    ring_barrier();
+    fetch((gk + kSpStages - 1) % kSpStages);
+    const uint32_t so = (uint32_t)((gk % kSpStages) * SST);
+    v4i x0a, x0b, x1a, x1b, a00, a01, a10, a11;
+    asm volatile(
+        "ds_read_b128 %0, %8\n\t"
+        "ds_read_b128 %1, %9\n\t"
+        "ds_read_b128 %2, %8 offset:2048\n\t"
+        "ds_read_b128 %3, %9 offset:2048\n\t"
+        "ds_read_b128 %4, %10\n\t"
+        "ds_read_b128 %5, %10 offset:2048\n\t"
+        "ds_read_b128 %6, %10 offset:1024\n\t"
+        "ds_read_b128 %7, %10 offset:3072\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(x0a), "=&v"(x0b), "=&v"(x1a), "=&v"(x1b), "=&v"(a00), "=&v"(a01), "=&v"(a10), "=&v"(a11)
+        : "v"(xaddr0 + so), "v"((xaddr0 + so) ^ 16u), "v"(aaddr0 + so));
+    __builtin_amdgcn_sched_barrier(0);
+    const v4i X[2][2] = {{x0a, x1a}, {x0b, x1b}};  // [j][pb]
+    const v4i A[2][2] = {{a00, a01}, {a10, a11}};  // [j][cb]
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+          acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[j][cb], X[j][pb], acc[cb][pb], 0, 0, 0);
+    if (++c_kb == KB) {
+      finish_row();
+      c_kb = 0;
+      row_next(c_it, ho, ho2);
+    }
+  }
+}
+
 // ---------------------------------------------------------------- launch
 bool is_stem(const ConvArgs &a) {
   return a.in.bits == 8 && a.in.is_signed && a.w_bits == 8 && a.in.row == 4 && a.kw <= 8 &&
@@ -1787,6 +2078,47 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   else
     hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4, KPI>), dim3((unsigned)nwg), dim3(WN * WM * 64),
                        0, s, a, geo, npt, ncb, nch);
+  return hipGetLastError();
+}
+
+// The stem followed by a 3x3 / stride 2 / pad 1 max pool of its output, on
+// stem_pool_kernel: the stem's tiled-kernel conditions, at most 127 output
+// columns, one input group, and a pooled view of the
+// stem's output shape.  The caller must know the fast epilogue applies
+// (conv_mfma_epilogue == 0): the kernel has no general build.
+bool stem_pool_applies(const ConvArgs &a, const ActView &po, int k, int stride, int pad) {
+  static int off = -1;  // PALQ_STEM_POOL=0: keep the two launches (for comparisons)
+  if (off < 0) {
+    const char *e = getenv("PALQ_STEM_POOL");
+    off = (e && strcmp(e, "0") == 0) ? 1 : 0;
+  }
+  if (off || !stem_tile_applies(a) || a.in.groups != 1 || a.wo < 1 || a.wo > 127 || a.ho < 1) return false;
+  if (k != 3 || stride != 2 || pad != 1) return false;
+  if (po.n != a.out.n || po.h != (a.ho + 1) / 2 || po.w != (a.wo + 1) / 2 || po.groups != a.out.groups ||
+      po.cpg != a.out.cpg || po.bits != 2 || po.pixel != a.out.pixel || po.row != a.out.row)
+    return false;
+  const int64_t in_bytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
+  const int64_t out_bytes = (int64_t)po.n * po.h * po.w * po.pixel;
+  const int64_t units = (int64_t)a.out.n * (a.cout / 128) * po.h;
+  // per-thread activation offsets within an output row's input rows: 16 bits
+  const int64_t xspan = (int64_t)a.in.w * a.in.pixel + (int64_t)(a.wo - 1) * a.stride * a.in.pixel + 16;
+  return in_bytes < 0x7fff0000 && out_bytes < 0x7fff0000 && units < 0x7fffffff && xspan < 0x10000;
+}
+
+hipError_t launch_stem_pool(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, const ActView &po,
+                            hipStream_t s) {
+  Geo geo = make_geo(a);
+  if (geo.M == 0) return hipSuccess;
+  geo.wp = wp;
+  geo.rq = (const RqConst *)thr;
+  const int units = a.out.n * (a.cout / 128) * po.h;
+  const int slots = tile_slots((const void *)stem_pool_kernel, sp::NT);
+  // P workgroups per XCD: all resident slots, no more than the XCD's units,
+  // and runs of at most ho2 units (two channel blocks' constants)
+  const int64_t Tx = (units + 7) / 8;
+  int64_t P = std::max<int64_t>(1, std::min<int64_t>(slots / 8, Tx));
+  if ((Tx + P - 1) / P > po.h) P = (Tx + po.h - 1) / po.h;
+  hipLaunchKernelGGL(stem_pool_kernel, dim3((unsigned)(8 * P)), dim3(sp::NT), 0, s, a, geo, po, units);
   return hipGetLastError();
 }
 

@@ -98,6 +98,12 @@ int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr);
 // epi: the value above, or -1 to start both builds (each checks on the
 // device whether it applies and the other returns at once).
 hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, int epi, hipStream_t s);
+// Stem conv fused with the 3x3 / stride 2 / pad 1 max pool of its output
+// (written to po only; the stem's own output is not written).  Requires the
+// fast epilogue (conv_mfma_epilogue == 0).
+bool stem_pool_applies(const ConvArgs &a, const ActView &po, int k, int stride, int pad);
+hipError_t launch_stem_pool(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, const ActView &po,
+                            hipStream_t s);
 
 hipError_t launch_pack(const void *codes, const ActView &out, hipStream_t s);
 hipError_t launch_unpack(const ActView &in, void *codes, hipStream_t s);

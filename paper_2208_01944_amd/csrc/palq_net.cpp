@@ -46,6 +46,11 @@ struct Layer {
   int8_t *fc_w = nullptr;
   int fc_cin = 0;
   int8_t *fc_scratch = nullptr;  // digit planes of the FC input
+  // stem conv whose output only the following max pool reads: one fused
+  // launch writes the pooled tensor (pool_out) and the pool layer is skipped
+  bool pool_fused = false;
+  bool skip = false;
+  ActView pool_out{};
 };
 
 constexpr int kRing = 64;  // forwards whose layer events can be outstanding
@@ -461,6 +466,20 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       // epilogue on the direct kernel
       if (NL.epi != 0 && !conv_mfma_general_fits(NL.conv)) NL.use_mfma = false;
     }
+  // fuse the stem with a max pool that is its output's only reader
+  if (!(flags & PALQ_NET_KEEP_ALL))
+    for (int i = 0; i + 1 < n_layers; ++i) {
+      Layer &NL = net->layers[i];
+      const palq_layer &P = layers[i + 1];
+      if (layers[i].op != PALQ_OP_CONV || !NL.use_mfma || NL.epi != 0 || P.op != PALQ_OP_MAXPOOL ||
+          P.src != layers[i].dst || net->tensors[layers[i].dst].last_use != i + 1)
+        continue;
+      const ActView po = view_of(&net->tensors[P.dst].d);
+      if (!stem_pool_applies(NL.conv, po, P.pool_k, P.pool_stride, P.pool_pad)) continue;
+      NL.pool_fused = true;
+      NL.pool_out = po;
+      net->layers[i + 1].skip = true;
+    }
   if (flags & PALQ_NET_TIMING) {
     net->events.assign((size_t)kRing * (n_layers + 1), nullptr);
     for (auto &ev : net->events)
@@ -499,6 +518,10 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
   for (size_t i = 0; i < L && e == hipSuccess; ++i) {
     Layer &NL = net->layers[i];
     const palq_layer &sp = NL.spec;
+    if (NL.skip) {
+      if (ev) hipEventRecord(ev[i + 1], s);
+      continue;
+    }
     switch (sp.op) {
       case PALQ_OP_CONV: {
         ConvArgs a = NL.conv;
@@ -512,7 +535,8 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
         }
         if (sp.res_src == 0) a.res.data = (uint8_t *)input;
         if (sp.proj_src == 0) a.proj.data = (uint8_t *)input;
-        e = NL.use_mfma ? launch_conv_mfma(a, NL.wp, NL.thr, NL.epi, s) : launch_conv_direct(a, s);
+        if (NL.pool_fused) e = launch_stem_pool(a, NL.wp, NL.thr, NL.pool_out, s);
+        else e = NL.use_mfma ? launch_conv_mfma(a, NL.wp, NL.thr, NL.epi, s) : launch_conv_direct(a, s);
         break;
       }
       case PALQ_OP_CHANNEL_SHUFFLE: {

@@ -100,6 +100,36 @@ def test_resnet18_with_modules_and_channel_shuffle(ctx, torch):
     np.testing.assert_array_equal(logits, ref)
 
 
+def stem_pool_spec(n, hw, groups, seed):
+    """The stem (7x7/s2 8-bit conv to 64 G channels, 2-bit output) and its
+    3x3/s2 max pool, then the global sum and a small FC."""
+    g = I.rng(seed)
+    x = I.codes(g, (n, hw, hw, 3), 8, True)
+    layers = []
+    cur, nid = I._stem(g, layers, groups, 2)
+    layers.append(dict(op="avgsum", src=cur, dst=nid))
+    layers.append(dict(op="fc", src=nid, dst=nid + 1, w=I.codes(g, (10, 64 * groups), 8, True)))
+    return dict(name="stem_pool", n=n, hw=hw, groups=groups, bits=2, x=x, layers=layers, classes=10)
+
+
+@pytest.mark.parametrize("n,hw,groups", [(3, 64, 4), (2, 50, 2), (1, 250, 4), (2, 33, 8), (1, 9, 2)])
+def test_stem_with_max_pool(ctx, torch, n, hw, groups):
+    """Without NET_KEEP_ALL the stem and its max pool run as one launch that
+    pools the accumulators; the pooled tensor (its buffer is not reused by the
+    sum or the FC) and the logits must match the oracle's.  Sizes cover even
+    and odd conv outputs (25, 125, 17, 3 rows), up to 125 columns, and 128-,
+    256- and 512-channel stems."""
+    say(f"stem + max pool n={n} hw={hw} G={groups}")
+    spec = stem_pool_spec(n, hw, groups, seed=40 + hw)
+    spec = O.calibrate_centring(spec, spec["x"])
+    net, logits = gpu_forward(ctx, torch, spec)
+    ref, tensors, _ = O.run_net(spec, spec["x"], keep=True)
+    got = ctx.unpack(net.tensor(2))
+    np.testing.assert_array_equal(got, tensors[2])
+    np.testing.assert_array_equal(logits, ref)
+    assert len(np.unique(tensors[2])) == 4  # every code occurs
+
+
 def test_resnet50_small_all_tensors(ctx, torch):
     say("resnet50 hw=64 n=2 G=2 b=2 centred")
     spec = I.resnet50(n=2, groups=2, bits=2, hw=64, classes=50, seed=12)
