@@ -343,6 +343,31 @@ __global__ void pad_pixels_kernel(ActView in, int pad, ActView out, int64_t word
   ((uint32_t *)out.data)[t] = v;
 }
 
+// kPadRows output rows (image, padded row y) per workgroup: 32-bit words,
+// zero outside the input rectangle; a thread loads its word of every row
+// before it stores any (independent loads in flight, no per-word division).
+constexpr int kPadRows = 8;
+__global__ void pad_rows_kernel(ActView in, int pad, ActView out, int rows) {
+  const int r0 = (int)blockIdx.x * kPadRows;
+  const int wpp = (int)(out.pixel / 4);
+  const int row_words = out.w * wpp;
+  const int lo = pad * wpp, hi = (pad + in.w) * wpp;
+  for (int w = threadIdx.x; w < row_words; w += blockDim.x) {
+    uint32_t v[kPadRows];
+#pragma unroll
+    for (int j = 0; j < kPadRows; ++j) {
+      const int r = r0 + j;
+      const int y = r % out.h, n = r / out.h, iy = y - pad;
+      v[j] = 0u;
+      if (r < rows && iy >= 0 && iy < in.h && w >= lo && w < hi)
+        v[j] = ((const uint32_t *)(in.data + ((int64_t)n * in.h + iy) * in.w * in.pixel))[w - lo];
+    }
+#pragma unroll
+    for (int j = 0; j < kPadRows; ++j)
+      if (r0 + j < rows) ((uint32_t *)(out.data + (int64_t)(r0 + j) * out.w * out.pixel))[w] = v[j];
+  }
+}
+
 // ------------------------------------------------------------ global sum
 // 2-bit codes, at most 85 pixels (85 x 3 < 256), 16 | cpg: one thread per
 // (image, group, word of 16 codes).  The word's codes k, k+4, k+8, k+12 sit
@@ -649,6 +674,12 @@ hipError_t launch_maxpool(const ActView &in, int k, int stride, int pad, const A
 hipError_t launch_pad_pixels(const ActView &in, int pad, const ActView &out, hipStream_t s) {
   const int64_t words = (int64_t)out.n * out.h * out.w * (out.pixel / 4);
   if (words == 0) return hipSuccess;
+  const int64_t rows = (int64_t)out.n * out.h;
+  if (rows < 0x7fffffff && (int64_t)out.w * out.pixel < 0x7fffffff) {
+    hipLaunchKernelGGL(pad_rows_kernel, dim3((unsigned)((rows + kPadRows - 1) / kPadRows)), dim3(256), 0, s, in, pad,
+                       out, (int)rows);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(pad_pixels_kernel, dim3(grid_for(words)), dim3(kBlock), 0, s, in, pad, out, words);
   return hipGetLastError();
 }
