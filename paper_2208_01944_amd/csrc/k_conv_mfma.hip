@@ -598,13 +598,12 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
 #pragma unroll
     for (int pb = 0; pb < PB; ++pb) {
       const int64_t mp = mbase + pb * 32 + l32;
-      const uint32_t s0 = half ? qv[pb][0] : qv[pb][2];
-      const uint32_t s1 = half ? qv[pb][1] : qv[pb][3];
-      const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
-      const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
-      uint32_t Q[4];
-      if (half == 0) { Q[0] = qv[pb][0]; Q[1] = r0; Q[2] = qv[pb][1]; Q[3] = r1; }
-      else           { Q[0] = r0; Q[1] = qv[pb][2]; Q[2] = r1; Q[3] = qv[pb][3]; }
+      // v_permlane32_swap exchanges the upper lane half of its first
+      // operand with the lower lane half of its second; afterwards every
+      // lane holds words 0, 1 (and 2, 3) of its 32 channels in order
+      const auto p0 = __builtin_amdgcn_permlane32_swap(qv[pb][0], qv[pb][2], false, false);
+      const auto p1 = __builtin_amdgcn_permlane32_swap(qv[pb][1], qv[pb][3], false, false);
+      const uint32_t Q[4] = {p0[0], p0[1], p1[0], p1[1]};
       if (mp >= geo.M) continue;
       uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row) +
                      (int64_t)(kc >> 5) * bo + half * (bo / 2);
@@ -1689,13 +1688,9 @@ __global__ __launch_bounds__(sp::NT, 3) void stem_pool_kernel(ConvArgs a, Geo ge
         }
         qv[qi] = qword;
       }
-      const uint32_t s0 = half ? qv[0] : qv[2];
-      const uint32_t s1 = half ? qv[1] : qv[3];
-      const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
-      const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
-      uint32_t Q[4];
-      if (half == 0) { Q[0] = qv[0]; Q[1] = r0; Q[2] = qv[1]; Q[3] = r1; }
-      else           { Q[0] = r0; Q[1] = qv[2]; Q[2] = r1; Q[3] = qv[3]; }
+      const auto p0 = __builtin_amdgcn_permlane32_swap(qv[0], qv[2], false, false);  // as in epilogue_fast_bo
+      const auto p1 = __builtin_amdgcn_permlane32_swap(qv[1], qv[3], false, false);
+      const uint32_t Q[4] = {p0[0], p0[1], p1[0], p1[1]};
       if (px < wo2)
         __builtin_amdgcn_raw_buffer_store_b32(Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24), rout,
                                               out_lane + cbb * 32 + cb * 8, orow, 0);
