@@ -500,6 +500,7 @@ __global__ __launch_bounds__(256) void fc_kernel(const int32_t *x, int n, int ci
 
 // Four consecutive features per thread (cin % 16 == 0); also clears the
 // logits, which fc_mfma_kernel's K slices add into.
+template <int P>
 __global__ void fc_digits_kernel(const int32_t *x, int64_t count, int8_t *planes, int32_t *logits,
                                  int64_t nlogits) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -507,19 +508,19 @@ __global__ void fc_digits_kernel(const int32_t *x, int64_t count, int8_t *planes
   if (4 * t >= count) return;
   const int4 v4 = *(const int4 *)(x + 4 * t);
   const int32_t v[4] = {v4.x, v4.y, v4.z, v4.w};
-  uint32_t word[4] = {0, 0, 0, 0};
+  uint32_t word[P] = {};
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     int64_t r = v[e];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < P; ++p) {
       const int d = (int)(int8_t)(uint8_t)(r & 255);  // signed digit
       word[p] |= (uint32_t)(uint8_t)d << (8 * e);
       r = (r - d) >> 8;                                 // exact: r - d is a multiple of 256
     }
   }
 #pragma unroll
-  for (int p = 0; p < 4; ++p) *(uint32_t *)(planes + p * count + 4 * t) = word[p];
+  for (int p = 0; p < P; ++p) *(uint32_t *)(planes + p * count + 4 * t) = word[p];
 }
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
@@ -531,6 +532,7 @@ typedef int v16i_t __attribute__((ext_vector_type(16)));
 // atomics: order-free, exact modulo 2^32).  A = weights (rows = outputs),
 // B = one digit plane (columns = images); rows and images past the end
 // read out-of-range offsets (zeros).
+template <int P>
 __global__ __launch_bounds__(256) void fc_mfma_kernel(const int8_t *w, const int8_t *planes, int n, int cin,
                                                       int cout, int32_t *logits) {
   __shared__ int32_t part[3][16][64];
@@ -539,13 +541,13 @@ __global__ __launch_bounds__(256) void fc_mfma_kernel(const int8_t *w, const int
   const int o0 = blockIdx.x * 32, i0 = blockIdx.y * 32;
   const int64_t plane = (int64_t)n * cin;
   const auto rw = __builtin_amdgcn_make_buffer_rsrc((void *)w, (short)0, (int)((int64_t)cout * cin), 0x00020000);
-  const auto rd = __builtin_amdgcn_make_buffer_rsrc((void *)planes, (short)0, (int)(4 * plane), 0x00020000);
+  const auto rd = __builtin_amdgcn_make_buffer_rsrc((void *)planes, (short)0, (int)(P * plane), 0x00020000);
   const uint32_t kOut = 0x80000000u;  // past every buffer this kernel reads
   const uint32_t wrow = o0 + l32 < cout ? (uint32_t)((o0 + l32) * cin + 16 * half) : kOut;
   const uint32_t drow = i0 + l32 < n ? (uint32_t)((i0 + l32) * cin + 16 * half) : kOut;
-  v16i_t acc[4];
+  v16i_t acc[P];
 #pragma unroll
-  for (int p = 0; p < 4; ++p)
+  for (int p = 0; p < P; ++p)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[p][r] = 0;
   const int steps = cin / 32;
@@ -554,7 +556,7 @@ __global__ __launch_bounds__(256) void fc_mfma_kernel(const int8_t *w, const int
   for (int k = 32 * (per * (int)blockIdx.z + wave); k < k_end; k += 128) {
     const v4i_t a = __builtin_bit_cast(v4i_t, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(wrow + k), 0, 0));
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < P; ++p) {
       const uint32_t off = drow == kOut ? kOut : drow + (uint32_t)(p * plane) + k;
       const v4i_t b = __builtin_bit_cast(v4i_t, __builtin_amdgcn_raw_buffer_load_b128(rd, (int)off, 0, 0));
       acc[p] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, acc[p], 0, 0, 0);
@@ -562,9 +564,11 @@ __global__ __launch_bounds__(256) void fc_mfma_kernel(const int8_t *w, const int
   }
   uint32_t tot[16];
 #pragma unroll
-  for (int r = 0; r < 16; ++r)
-    tot[r] = (uint32_t)acc[0][r] + ((uint32_t)acc[1][r] << 8) + ((uint32_t)acc[2][r] << 16) +
-             ((uint32_t)acc[3][r] << 24);
+  for (int r = 0; r < 16; ++r) {
+    tot[r] = 0;
+#pragma unroll
+    for (int p = 0; p < P; ++p) tot[r] += (uint32_t)acc[p][r] << (8 * p);
+  }
   if (wave > 0)
 #pragma unroll
     for (int r = 0; r < 16; ++r) part[wave - 1][r][lane] = (int32_t)tot[r];
@@ -703,14 +707,17 @@ hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s) {
 }
 
 hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout, int32_t *logits,
-                     int8_t *scratch, hipStream_t s) {
+                     int8_t *scratch, hipStream_t s, int64_t xmax) {
   const int64_t items = (int64_t)n * cout;
   if (items == 0) return hipSuccess;
   if (scratch && cin % 32 == 0 && ((uintptr_t)x & 15u) == 0 && (int64_t)4 * n * cin < ((int64_t)1 << 31) &&
       (int64_t)cout * cin < ((int64_t)1 << 31)) {
     const int64_t count = (int64_t)n * cin;
-    hipLaunchKernelGGL(fc_digits_kernel, dim3(grid_for(count / 4)), dim3(kBlock), 0, s, x, count, scratch, logits,
-                       items);
+    // signed base-256 digit planes: one covers |x| <= 127, two |x| <= 32639,
+    // four every int32 (exact modulo 2^32)
+    const int P = xmax >= 0 && xmax <= 127 ? 1 : xmax >= 0 && xmax <= 32639 ? 2 : 4;
+    auto digits = P == 1 ? fc_digits_kernel<1> : P == 2 ? fc_digits_kernel<2> : fc_digits_kernel<4>;
+    hipLaunchKernelGGL(digits, dim3(grid_for(count / 4)), dim3(kBlock), 0, s, x, count, scratch, logits, items);
     // K slices (of at least 4 steps) for about 128 workgroups: more slices
     // only add contended atomics (ResNet-18 batch 64: 2 slices 16 us, 8
     // slices 20 us, 32 slices 48 us)
@@ -721,7 +728,8 @@ hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout
       if (v >= 1 && v <= cin / 32) slices = v;
     }
     dim3 grid((unsigned)((cout + 31) / 32), (unsigned)((n + 31) / 32), (unsigned)slices);
-    hipLaunchKernelGGL(fc_mfma_kernel, grid, dim3(256), 0, s, w, (const int8_t *)scratch, n, cin, cout, logits);
+    auto mm = P == 1 ? fc_mfma_kernel<1> : P == 2 ? fc_mfma_kernel<2> : fc_mfma_kernel<4>;
+    hipLaunchKernelGGL(mm, grid, dim3(256), 0, s, w, (const int8_t *)scratch, n, cin, cout, logits);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(fill_i32_kernel, dim3(grid_for(items)), dim3(kBlock), 0, s, logits, items);

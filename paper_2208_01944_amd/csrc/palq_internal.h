@@ -119,10 +119,11 @@ hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s);
 // out: in's shape grown by 2 pad pixels in h and w, same pixel bytes.
 hipError_t launch_pad_pixels(const ActView &in, int pad, const ActView &out, hipStream_t s);
 // FC: with scratch (fc_scratch_bytes, device) the matrix-core path runs,
-// else (or when that returns 0) the vector path.
+// else (or when that returns 0) the vector path.  xmax: a bound on |x| that
+// the caller knows (fewer digit planes), or -1.
 size_t fc_scratch_bytes(int n, int cin);
 hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout, int32_t *logits,
-                     int8_t *scratch, hipStream_t s);
+                     int8_t *scratch, hipStream_t s, int64_t xmax = -1);
 
 }  // namespace palq
 

@@ -27,6 +27,7 @@ struct Tensor {
   palq_act d{};          // shape/bits; data filled at plan time
   int64_t bytes = 0;
   int last_use = -1;     // index of the last layer reading it
+  int64_t sum_max = -1;  // AVGSUM outputs: bound on every sum
   int buf = -1;          // buffer slot (-1: network input or logits)
 };
 
@@ -46,6 +47,7 @@ struct Layer {
   int8_t *fc_w = nullptr;
   int fc_cin = 0;
   int8_t *fc_scratch = nullptr;  // digit planes of the FC input
+  int64_t fc_xmax = -1;          // bound on the FC input (sums of codes)
   // stem conv whose output only the following max pool reads: one fused
   // launch writes the pooled tensor (pool_out) and the pool layer is skipped
   bool pool_fused = false;
@@ -274,6 +276,7 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       o.n = src.d.n; o.h = 1; o.w = 1; o.groups = 1; o.ch_per_group = src.d.groups * src.d.ch_per_group;
       o.bits = 32; o.is_signed = 1;
       dst.exists = true; dst.kind = kSums; dst.d = o;
+      dst.sum_max = (((int64_t)1 << src.d.bits) - 1) * src.d.h * src.d.w;
       NL.in_view = src.d; NL.out_view = o;
     } else if (L.op == PALQ_OP_FC) {
       if (src.kind != kSums) { bad(PALQ_ERR_ARG, "FC input must be an AVGSUM output"); break; }
@@ -283,6 +286,7 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       o.n = src.d.n; o.h = 1; o.w = 1; o.groups = 1; o.ch_per_group = L.fc_out; o.bits = 32; o.is_signed = 1;
       dst.exists = true; dst.kind = kLogits; dst.d = o;
       NL.fc_cin = src.d.ch_per_group;
+      NL.fc_xmax = src.sum_max;
       off_fc[i] = reserve((int64_t)L.fc_out * NL.fc_cin);
       net->ops += 2 * (int64_t)o.n * L.fc_out * NL.fc_cin;
       net->fc_out = L.fc_out;
@@ -559,7 +563,7 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
         break;
       }
       case PALQ_OP_FC:
-        e = launch_fc(NL.fc_in, net->n, NL.fc_cin, NL.fc_w, sp.fc_out, logits, NL.fc_scratch, s);
+        e = launch_fc(NL.fc_in, net->n, NL.fc_cin, NL.fc_w, sp.fc_out, logits, NL.fc_scratch, s, NL.fc_xmax);
         break;
     }
     if (ev && e == hipSuccess) hipEventRecord(ev[i + 1], s);
