@@ -520,6 +520,19 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
   constexpr int bo = BO;
   constexpr uint32_t qmax = (1u << BO) - 1u;
   const int lsc = geo.scale == 16 ? 4 : 0;
+  // requant constants (and shortcut multipliers) of quad j = 4 cb + qi,
+  // read one quad ahead of their use so that their LDS latency overlaps
+  // the previous quad's arithmetic
+  auto quad_consts = [&](int j, dbl2 (&k)[4], v4i &rmu) __attribute__((always_inline)) {
+    const int c0 = (j >> 2) * 32 + 8 * (j & 3) + 4 * half;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) k[e] = dbl2{rq[c0 + e].s, rq[c0 + e].o};
+    rmu = v4i{0, 0, 0, 0};
+    if constexpr (RB != 0) rmu = *(const v4i *)(rm + c0);
+  };
+  dbl2 k_cur[4];
+  v4i rmu_cur;
+  quad_consts(0, k_cur, rmu_cur);
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     const int kc = ch0 + cb * 32;
@@ -558,10 +571,11 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
       __builtin_amdgcn_sched_barrier(0);
       const int cq = 8 * qi + 4 * half;
       dbl2 k[4];
+      v4i rmu;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) k[e] = dbl2{rq[cb * 32 + cq + e].s, rq[cb * 32 + cq + e].o};
-      v4i rmu = {0, 0, 0, 0};
-      if constexpr (RB != 0) rmu = *(const v4i *)(rm + cb * 32 + cq);
+      for (int e = 0; e < 4; ++e) k[e] = k_cur[e];
+      rmu = rmu_cur;
+      if (4 * cb + qi + 1 < 4 * CB) quad_consts(4 * cb + qi + 1, k_cur, rmu_cur);
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb) {
         constexpr bool FACC = std::is_same<AccV, v16f>::value;
