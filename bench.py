@@ -1,7 +1,8 @@
 """Benchmark: PalQuant ResNet-18 (G=4 parallel 2-bit groups) forward, batch 64.
 
-One step = quantise the fp32 224x224x3 input batch to 8-bit codes (Eq. 2,
-fixed l/u) + the whole network through palq_forward: 8-bit stem, max pool,
+One step = palq_forward_image: quantise the fp32 224x224x3 input batch to
+8-bit codes (Eq. 2, fixed l/u; written straight into the stem's zero-border
+input) + the whole network: 8-bit stem fused with its max pool,
 16 grouped 2-bit 3x3 convs with int32 residual adds and the cyclic
 permutation fused into each block's second conv, 3 fused 1x1 projections,
 integer global sum and the 8-bit FC to int32 logits.  Inputs are resident in
@@ -299,12 +300,12 @@ def main():
     net = palq.Net(ctx, spec)
     net_t = palq.Net(ctx, spec, flags=palq.NET_TIMING)
     xd = ctx.upload(x_f32)
-    codes = ctx.empty_act(n, 224, 224, 1, 3, 8, signed=True)
     logits = torch.empty(n * net.classes, dtype=torch.int32, device=ctx.dev)
 
     def step(nn):
-        ctx.quantize(xd, l, u, codes)
-        nn.forward(codes.buf, logits)
+        # quantise the fp32 batch (Eq. 2) straight into the stem's padded
+        # input and run the network: palq_forward_image
+        nn.forward_image(xd, l, u, logits)
 
     for _ in range(args.warmup):
         step(net)
@@ -401,7 +402,7 @@ def main():
         "dtype": "fp4+int8" if dom == DOMINANT else "int8",
         "data": "synthetic (seeded uniform codes and random fp32 images, random weights)",
         "config": {"workload": "resnet18_palq_G4_b2_224_fwd", "global_batch": n, "image": [224, 224, 3],
-                   "groups": 4, "bits": 2, "step": "quantize fp32 input + palq_forward"},
+                   "groups": 4, "bits": 2, "step": "palq_forward_image (quantize fp32 input + forward)"},
         "effective_tops": tops,
         "int_ops_per_step": total_ops,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak,

@@ -292,6 +292,17 @@ void palq_net_destroy(palq_net *net);
  * and writes logits (device, int32 [n][fc_out]).  Asynchronous. */
 palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_t *logits);
 
+/* The quantiser of Section 3.2 Eq. 2 (as palq_quantize with fixed l, u and
+ * signed 8-bit codes) followed by palq_forward, for a network whose input
+ * descriptor is a signed 8-bit image with one group of 3 channels.  x:
+ * device fp32 [n][h][w][3] of that shape, 4-byte aligned.  Results are
+ * identical to palq_quantize into an input tensor and palq_forward on it;
+ * where the first layer copies its input with a zero border the codes are
+ * written straight into that copy (no separate input tensor or copy).
+ * Errors: PALQ_ERR_ARG for another input format, null or misaligned
+ * pointers, or l, u not finite with u > l.  Asynchronous. */
+palq_status palq_forward_image(palq_ctx *ctx, palq_net *net, const float *x, float l, float u, int32_t *logits);
+
 /* Descriptor (with device data pointer) of tensor `id` after a forward pass.
  * Conv/maxpool outputs are packed codes; an AVGSUM output is reported with
  * bits = 32 (int32 values, one per channel, h = w = 1).  Valid for every id

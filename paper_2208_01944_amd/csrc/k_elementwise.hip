@@ -139,6 +139,40 @@ __global__ void quantize_px3_kernel(const float *x, float l, float u, const uint
   *(uint4 *)(out.data + 16 * t) = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
+// Signed 8-bit codes of 3-channel fp32 pixels written straight into a
+// copy with a `pad`-pixel zero border (4-byte pixel rows): kQPadRows output
+// rows per workgroup, one column per thread, every row's loads issued
+// before any store.  Same arithmetic as quantize_px3_kernel.
+constexpr int kQPadRows = 8;
+__global__ void quantize_pad_kernel(const float *x, float l, float u, int in_h, int in_w, int pad, ActView out,
+                                    int rows) {
+  const int r0 = (int)blockIdx.x * kQPadRows;
+  const float rng = u - l;
+  for (int c = threadIdx.x; c < out.w; c += blockDim.x) {
+    const int ix = c - pad;
+    float v[kQPadRows][3];
+    bool in[kQPadRows];
+#pragma unroll
+    for (int j = 0; j < kQPadRows; ++j) {
+      const int r = r0 + j, y = r % out.h, n = r / out.h, iy = y - pad;
+      in[j] = r < rows && iy >= 0 && iy < in_h && ix >= 0 && ix < in_w;
+      const float *src = x + (((int64_t)n * in_h + (in[j] ? iy : 0)) * in_w + (in[j] ? ix : 0)) * 3;
+#pragma unroll
+      for (int ch = 0; ch < 3; ++ch) v[j][ch] = in[j] ? src[ch] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < kQPadRows; ++j) {
+      if (r0 + j >= rows) break;
+      uint32_t word = 0;
+      if (in[j]) {
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch) word |= ((uint32_t)(quant_one(v[j][ch], l, rng, 255.0f) - 128) & 0xffu) << (8 * ch);
+      }
+      ((uint32_t *)(out.data + ((int64_t)(r0 + j) * out.w + c) * out.pixel))[0] = word;
+    }
+  }
+}
+
 // One thread per packed word (b in {2, 4, 8}) or 32-code chunk (b = 3).
 __global__ void quantize_kernel(const float *x, float l, float u, const uint32_t *enc, ActView out,
                                 int64_t rows, int units) {
@@ -630,6 +664,16 @@ hipError_t launch_quantize(const float *x, float l, float u, const float *range,
   }
   hipLaunchKernelGGL(quantize_kernel, dim3(grid_for(rows * units)), dim3(kBlock), 0, s, x, l, u,
                      (const uint32_t *)range, out, rows, units);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_pad(const float *x, float l, float u, int in_h, int in_w, int pad, const ActView &out,
+                               hipStream_t s) {
+  const int64_t rows = (int64_t)out.n * out.h;
+  if (rows == 0 || out.w == 0) return hipSuccess;
+  if (rows >= 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(quantize_pad_kernel, dim3((unsigned)((rows + kQPadRows - 1) / kQPadRows)), dim3(256), 0, s, x,
+                     l, u, in_h, in_w, pad, out, (int)rows);
   return hipGetLastError();
 }
 

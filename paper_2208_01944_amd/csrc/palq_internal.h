@@ -118,6 +118,11 @@ hipError_t launch_maxpool(const ActView &in, int k, int stride, int pad, const A
 hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s);
 // out: in's shape grown by 2 pad pixels in h and w, same pixel bytes.
 hipError_t launch_pad_pixels(const ActView &in, int pad, const ActView &out, hipStream_t s);
+// Signed 8-bit codes (Eq. 2 with fixed l, u) of an fp32 [n][in_h][in_w][3]
+// tensor written into `out`, a 4-byte-pixel tensor of in_h + 2 pad rows and
+// in_w + 2 pad columns, zero on the border.
+hipError_t launch_quantize_pad(const float *x, float l, float u, int in_h, int in_w, int pad, const ActView &out,
+                               hipStream_t s);
 // FC: with scratch (fc_scratch_bytes, device) the matrix-core path runs,
 // else (or when that returns 0) the vector path.  xmax: a bound on |x| that
 // the caller knows (fewer digit planes), or -1.

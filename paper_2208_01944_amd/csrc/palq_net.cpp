@@ -8,6 +8,8 @@
 // and launches the prepared kernels in order on the context's stream.
 #include <string.h>
 
+#include <cmath>
+
 #include <algorithm>
 #include <new>
 #include <string>
@@ -73,6 +75,13 @@ struct palq_net {
   std::vector<double> ms;          // per layer
   int pending_begin = 0, pending_end = 0;  // ring indices of unread forwards
   int forwards = 0;
+  // palq_forward_image: the input is an 8-bit signed 3-channel image; either
+  // every reader of tensor 0 is a conv that copies it with a zero border
+  // (img_direct: it quantises straight into that copy) or the image is first
+  // quantised into img_codes
+  bool img_input = false, img_direct = false;
+  void *img_codes = nullptr;
+  palq_act input{};
 };
 
 namespace {
@@ -102,6 +111,7 @@ void free_net(palq_net *net) {
   if (net->ctx && net->ctx->device >= 0) hipSetDevice(net->ctx->device);
   for (void *b : net->bufs) if (b) hipFree(b);
   if (net->pool) hipFree(net->pool);
+  if (net->img_codes) hipFree(net->img_codes);
   for (hipEvent_t e : net->events) if (e) hipEventDestroy(e);
   delete net;
 }
@@ -303,6 +313,8 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
     free_net(net);
     return net_fail(ctx, st, err);
   }
+  net->input = *input;  // palq_forward_image's input format
+  net->img_input = input->bits == 8 && input->is_signed && input->groups == 1 && input->ch_per_group == 3;
   if (ctx->device < 0) {  // validate-only context: nothing to allocate
     *out = net;
     return PALQ_OK;
@@ -484,6 +496,26 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       NL.pool_out = po;
       net->layers[i + 1].skip = true;
     }
+  // palq_forward_image: quantise straight into the zero-border copies when
+  // they are the only readers of tensor 0, else into a buffer of its own
+  if (net->img_input) {
+    bool direct = true;
+    for (int i = 0; i < n_layers; ++i) {
+      const palq_layer &L = layers[i];
+      const bool conv = L.op == PALQ_OP_CONV;
+      const bool reads0 = L.src == 0 || (conv && (L.res_src == 0 || L.proj_src == 0));
+      if (reads0 && !(conv && L.src == 0 && net->layers[i].pad > 0 && L.res_src != 0 && L.proj_src != 0))
+        direct = false;
+    }
+    net->img_direct = direct;
+    if (!direct) {
+      if (hipMalloc(&net->img_codes, (size_t)act_bytes(*input) + 256) != hipSuccess) {
+        free_net(net);
+        return net_fail(ctx, PALQ_ERR_NOMEM, "image codes");
+      }
+      net->input.data = net->img_codes;
+    }
+  }
   if (flags & PALQ_NET_TIMING) {
     net->events.assign((size_t)kRing * (n_layers + 1), nullptr);
     for (auto &ev : net->events)
@@ -498,14 +530,11 @@ void palq_net_destroy(palq_net *net) { free_net(net); }
 
 int64_t palq_net_ops(const palq_net *net) { return net ? net->ops : -1; }
 
-palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_t *logits) {
-  if (!ctx || !net) return PALQ_ERR_ARG;
-  if (net->ctx != ctx) return net_fail(ctx, PALQ_ERR_ARG, "network belongs to another context");
-  if (!input || !logits) return net_fail(ctx, PALQ_ERR_ARG, "null input or logits");
-  if (((uintptr_t)input & 15u) || ((uintptr_t)logits & 3u))
-    return net_fail(ctx, PALQ_ERR_ARG, "input must be 16-byte and logits 4-byte aligned");
-  if (ctx->device < 0) return PALQ_OK;
-  hipSetDevice(ctx->device);
+namespace {
+// img != nullptr: the layers that read tensor 0 through a zero-border copy
+// quantise img (fp32, Eq. 2 with l, u) into that copy instead (img_direct).
+palq_status forward_impl(palq_ctx *ctx, palq_net *net, const void *input, int32_t *logits, const float *img,
+                         float l, float u) {
   hipStream_t s = ctx->stream;
   const size_t L = net->layers.size();
   hipEvent_t *ev = nullptr;
@@ -529,7 +558,10 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
     switch (sp.op) {
       case PALQ_OP_CONV: {
         ConvArgs a = NL.conv;
-        if (NL.pad > 0) {
+        if (NL.pad > 0 && img && sp.src == 0) {
+          e = launch_quantize_pad(img, l, u, NL.pad_in.h, NL.pad_in.w, NL.pad, a.in, s);
+          if (e != hipSuccess) break;
+        } else if (NL.pad > 0) {
           ActView src = NL.pad_in;
           if (sp.src == 0) src.data = (uint8_t *)input;
           e = launch_pad_pixels(src, NL.pad, a.in, s);
@@ -570,6 +602,36 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
   }
   if (e != hipSuccess) return net_fail(ctx, PALQ_ERR_DEVICE, std::string("forward: ") + hipGetErrorString(e));
   return PALQ_OK;
+}
+}  // namespace
+
+palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_t *logits) {
+  if (!ctx || !net) return PALQ_ERR_ARG;
+  if (net->ctx != ctx) return net_fail(ctx, PALQ_ERR_ARG, "network belongs to another context");
+  if (!input || !logits) return net_fail(ctx, PALQ_ERR_ARG, "null input or logits");
+  if (((uintptr_t)input & 15u) || ((uintptr_t)logits & 3u))
+    return net_fail(ctx, PALQ_ERR_ARG, "input must be 16-byte and logits 4-byte aligned");
+  if (ctx->device < 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  return forward_impl(ctx, net, input, logits, nullptr, 0.f, 0.f);
+}
+
+palq_status palq_forward_image(palq_ctx *ctx, palq_net *net, const float *x, float l, float u, int32_t *logits) {
+  if (!ctx || !net) return PALQ_ERR_ARG;
+  if (net->ctx != ctx) return net_fail(ctx, PALQ_ERR_ARG, "network belongs to another context");
+  if (!net->img_input)
+    return net_fail(ctx, PALQ_ERR_ARG, "network input is not a signed 8-bit 3-channel image (one group)");
+  if (!x || !logits) return net_fail(ctx, PALQ_ERR_ARG, "null x or logits");
+  if (((uintptr_t)x & 3u) || ((uintptr_t)logits & 3u))
+    return net_fail(ctx, PALQ_ERR_ARG, "x and logits must be 4-byte aligned");
+  if (!std::isfinite(l) || !std::isfinite(u) || !(u > l) || !std::isfinite(u - l))
+    return net_fail(ctx, PALQ_ERR_ARG, "need finite l < u with finite u - l");
+  if (ctx->device < 0) return PALQ_OK;
+  hipSetDevice(ctx->device);
+  if (net->img_direct) return forward_impl(ctx, net, nullptr, logits, x, l, u);
+  const hipError_t e = launch_quantize(x, l, u, nullptr, view_of(&net->input), ctx->stream);
+  if (e != hipSuccess) return net_fail(ctx, PALQ_ERR_DEVICE, std::string("quantize: ") + hipGetErrorString(e));
+  return forward_impl(ctx, net, net->img_codes, logits, nullptr, 0.f, 0.f);
 }
 
 palq_status palq_net_tensor(const palq_net *net, int32_t id, palq_act *desc) {

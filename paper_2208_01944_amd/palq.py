@@ -94,6 +94,7 @@ _net_create = _sig("palq_net_create", c_i32, c_p, P_ACT, ctypes.POINTER(Layer), 
                    ctypes.POINTER(c_p))
 _net_destroy = _sig("palq_net_destroy", None, c_p)
 _forward = _sig("palq_forward", c_i32, c_p, c_p, c_p, c_p)
+_forward_image = _sig("palq_forward_image", c_i32, c_p, c_p, c_p, c_f, c_f, c_p)
 _net_tensor = _sig("palq_net_tensor", c_i32, c_p, c_i32, P_ACT)
 _net_ops = _sig("palq_net_ops", c_i64, c_p)
 _net_layer_times = _sig("palq_net_layer_times", c_i32, c_p, ctypes.POINTER(c_f), ctypes.POINTER(c_i32))
@@ -104,7 +105,7 @@ EXPORTS = ["palq_create", "palq_destroy", "palq_set_stream", "palq_set_conv_fp4"
            "palq_quantize", "palq_group_conv", "palq_shuffle_module", "palq_cyclic_shuffle",
            "palq_channel_shuffle", "palq_maxpool",
            "palq_avgsum", "palq_fc", "palq_net_create", "palq_net_destroy", "palq_forward",
-           "palq_net_tensor", "palq_net_ops", "palq_net_layer_times", "palq_net_reset_times"]
+           "palq_forward_image", "palq_net_tensor", "palq_net_ops", "palq_net_layer_times", "palq_net_reset_times"]
 
 
 class PalqError(RuntimeError):
@@ -351,6 +352,11 @@ class Net:
 
     def forward(self, x_packed, logits):
         self.ctx._check(_forward(self.ctx.h, self.h, _ptr(x_packed), _ptr(logits)))
+
+    def forward_image(self, x_f32, l, u, logits):
+        """palq_forward_image: quantise an fp32 [n][h][w][3] image (Eq. 2,
+        fixed l, u) and run the network on it."""
+        self.ctx._check(_forward_image(self.ctx.h, self.h, _ptr(x_f32), float(l), float(u), _ptr(logits)))
 
     def tensor(self, tid) -> Tensor:
         a = Act()

@@ -185,6 +185,38 @@ def test_validate_only_net_create(P, vctx):
     assert "layer 2" in vctx.last_error()
 
 
+def test_validate_only_forward_image(P, vctx):
+    """palq_forward_image: image-input networks only, finite l < u, non-null
+    aligned pointers (validate-only: no device work)."""
+    inp = P.make_act(2, 16, 16, 1, 3, 8, True, 0)
+    Ls = (P.Layer * 3)()
+    Ls[0] = _layer(P, op=P.OP_CONV, src=0, dst=1, w=P.Filter(1, 128, 3, 7, 7, 8, _fake(1)), stride=2,
+                   pad=3, mult=_fake(2), shift=_fake(3), out_bits=2)
+    Ls[1] = _layer(P, op=P.OP_AVGSUM, src=1, dst=2)
+    Ls[2] = _layer(P, op=P.OP_FC, src=2, dst=3, fc_w=_fake(8), fc_out=10)
+    h = ctypes.c_void_p()
+    assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 3, 0, ctypes.byref(h)) == P.OK
+    fi = P._forward_image
+    assert fi(vctx.h, h, _fake(20), -3.0, 3.0, _fake(21)) == P.OK
+    assert fi(vctx.h, h, _fake(20), 3.0, 3.0, _fake(21)) == P.ERR_ARG          # u == l
+    assert fi(vctx.h, h, _fake(20), float("nan"), 3.0, _fake(21)) == P.ERR_ARG  # no calibration here
+    assert fi(vctx.h, h, _fake(20), -3.0, float("inf"), _fake(21)) == P.ERR_ARG
+    assert fi(vctx.h, h, None, -3.0, 3.0, _fake(21)) == P.ERR_ARG
+    assert fi(vctx.h, h, _fake(20) + 2, -3.0, 3.0, _fake(21)) == P.ERR_ARG      # misaligned
+    P._net_destroy(h)
+    # a network whose input is not an 8-bit 3-channel image
+    inp2 = P.make_act(2, 16, 16, 2, 64, 2, False, 0)
+    Ls2 = (P.Layer * 3)()
+    Ls2[0] = _layer(P, op=P.OP_CONV, src=0, dst=1, w=P.Filter(2, 64, 64, 3, 3, 2, _fake(1)), stride=1,
+                    pad=1, mult=_fake(2), shift=_fake(3), out_bits=2)
+    Ls2[1] = _layer(P, op=P.OP_AVGSUM, src=1, dst=2)
+    Ls2[2] = _layer(P, op=P.OP_FC, src=2, dst=3, fc_w=_fake(8), fc_out=10)
+    assert P._net_create(vctx.h, ctypes.byref(inp2), Ls2, 3, 0, ctypes.byref(h)) == P.OK
+    assert fi(vctx.h, h, _fake(20), -3.0, 3.0, _fake(21)) == P.ERR_ARG
+    assert "image" in vctx.last_error()
+    P._net_destroy(h)
+
+
 def test_validate_only_shuffle_module(P, vctx):
     x = _act(P, c=64)
     out = _act(P, c=64, slot=20)
