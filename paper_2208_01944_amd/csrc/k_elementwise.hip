@@ -173,6 +173,39 @@ __global__ void quantize_pad_kernel(const float *x, float l, float u, int in_h, 
   }
 }
 
+// The same with four input pixels per thread (three 16-byte loads) for
+// rows of at most 4 (64 - 2 pad) pixels, in_w % 4 == 0: 64 threads per
+// output row (quads of interior pixels, then the 2 pad border pixels), four
+// rows per workgroup; border rows are zeroed by all 64.
+__global__ void quantize_pad4_kernel(const float *x, float l, float u, int in_h, int in_w, int pad, ActView out,
+                                     int rows) {
+  const int r = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6), j = (int)(threadIdx.x & 63);
+  if (r >= rows) return;
+  const int y = r % out.h, n = r / out.h, iy = y - pad;
+  uint32_t *row = (uint32_t *)(out.data + (int64_t)r * out.w * out.pixel);
+  if (iy < 0 || iy >= in_h) {
+    for (int c = j; c < out.w; c += 64) row[c] = 0u;
+    return;
+  }
+  const int quads = in_w >> 2;
+  if (j < quads) {
+    const float4 *src = (const float4 *)(x + (((int64_t)n * in_h + iy) * in_w + 4 * j) * 3);
+    const float4 f0 = src[0], f1 = src[1], f2 = src[2];
+    const float v[12] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w, f2.x, f2.y, f2.z, f2.w};
+    const float rng = u - l;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      uint32_t word = 0;
+#pragma unroll
+      for (int ch = 0; ch < 3; ++ch) word |= ((uint32_t)(quant_one(v[3 * p + ch], l, rng, 255.0f) - 128) & 0xffu) << (8 * ch);
+      row[pad + 4 * j + p] = word;
+    }
+  } else if (j - quads < 2 * pad) {
+    const int b = j - quads;
+    row[b < pad ? b : in_w + b] = 0u;
+  }
+}
+
 // One thread per packed word (b in {2, 4, 8}) or 32-code chunk (b = 3).
 __global__ void quantize_kernel(const float *x, float l, float u, const uint32_t *enc, ActView out,
                                 int64_t rows, int units) {
@@ -672,6 +705,16 @@ hipError_t launch_quantize_pad(const float *x, float l, float u, int in_h, int i
   const int64_t rows = (int64_t)out.n * out.h;
   if (rows == 0 || out.w == 0) return hipSuccess;
   if (rows >= 0x7fffffff) return hipErrorInvalidValue;
+  static int v4 = -1;  // PALQ_QPAD4=0: the one-pixel-per-thread kernel (tuning)
+  if (v4 < 0) {
+    const char *e = getenv("PALQ_QPAD4");
+    v4 = e && atoi(e) == 0 ? 0 : 1;
+  }
+  if (v4 && in_w % 4 == 0 && in_w / 4 + 2 * pad <= 64 && out.pixel == 4 && ((uintptr_t)x & 15u) == 0) {
+    hipLaunchKernelGGL(quantize_pad4_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, x, l, u, in_h, in_w,
+                       pad, out, (int)rows);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(quantize_pad_kernel, dim3((unsigned)((rows + kQPadRows - 1) / kQPadRows)), dim3(256), 0, s, x,
                      l, u, in_h, in_w, pad, out, (int)rows);
   return hipGetLastError();

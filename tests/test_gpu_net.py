@@ -130,21 +130,21 @@ def test_stem_with_max_pool(ctx, torch, n, hw, groups):
     assert len(np.unique(tensors[2])) == 4  # every code occurs
 
 
-@pytest.mark.parametrize("stem_pad", [3, 0])
-def test_forward_image_matches_quantize_then_forward(ctx, torch, stem_pad):
+@pytest.mark.parametrize("stem_pad,hw", [(3, 64), (0, 64), (3, 50)])
+def test_forward_image_matches_quantize_then_forward(ctx, torch, stem_pad, hw):
     """palq_forward_image (quantise into the stem's zero-border copy, or, for
     a stem without padding, into a buffer of its own) gives the logits of
     palq_quantize + palq_forward and of the oracle, on fp32 images with
     NaN, infinities and values outside [l, u]."""
     from paper_2208_01944_amd import palq
-    say(f"forward_image stem pad={stem_pad}")
-    spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=17)
+    say(f"forward_image stem pad={stem_pad} hw={hw}")
+    spec = I.resnet18(n=2, groups=4, bits=2, hw=hw, classes=100, seed=17)
     if stem_pad == 0:
         st = dict(spec["layers"][0])
         st["pad"] = 0
         spec["layers"][0] = st
     g = np.random.default_rng(70 + stem_pad)
-    x = g.normal(0, 1.3, (2, 64, 64, 3)).astype(np.float32)
+    x = g.normal(0, 1.3, (2, hw, hw, 3)).astype(np.float32)
     x.flat[::97] = np.nan
     x.flat[3::89] = np.inf
     x.flat[5::101] = -np.inf
@@ -157,7 +157,7 @@ def test_forward_image_matches_quantize_then_forward(ctx, torch, stem_pad):
     out1 = torch.empty(2 * 100, dtype=torch.int32, device=ctx.dev)
     out2 = torch.empty_like(out1)
     net.forward_image(xd, l, u, out1)
-    xt = ctx.empty_act(2, 64, 64, 1, 3, 8, True)
+    xt = ctx.empty_act(2, hw, hw, 1, 3, 8, True)
     ctx.quantize(xd, l, u, xt)
     net.forward(xt.buf, out2)
     net.forward_image(xd, l, u, out1)  # again, after the other path used the buffers
