@@ -37,6 +37,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--batch", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true", help="replay the forward from a captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="wall-clock budget of the oracle sample")
     ap.add_argument("--summarize-profile", metavar="DIR", default=None,
@@ -297,7 +298,9 @@ def main():
 
     ctx = palq.Context(0)
     stream = torch.cuda.current_stream()
-    net = palq.Net(ctx, spec)
+    # eager launches (--graph: replay from a captured HIP graph, which
+    # measured about 1.5 % slower for this network)
+    net = palq.Net(ctx, spec, flags=palq.NET_GRAPH if args.graph else 0)
     net_t = palq.Net(ctx, spec, flags=palq.NET_TIMING)
     xd = ctx.upload(x_f32)
     logits = torch.empty(n * net.classes, dtype=torch.int32, device=ctx.dev)

@@ -240,6 +240,11 @@ palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, con
 
 #define PALQ_NET_KEEP_ALL 1 /* every tensor keeps its own buffer (for inspection) */
 #define PALQ_NET_TIMING 2   /* record a HIP event pair around every layer      */
+#define PALQ_NET_GRAPH 4    /* replay forwards from a captured HIP graph: the
+                             * first forward runs eagerly, later ones capture
+                             * the launch sequence once per (input, logits, l,
+                             * u, stream) and replay it; input contents may
+                             * change between calls.  Not with PALQ_NET_TIMING. */
 
 /* One layer of a network.  Tensor ids: 0 is the network input; each layer
  * writes a new id `dst` larger than every id before it.  Every pointer in

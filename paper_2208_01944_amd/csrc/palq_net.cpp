@@ -82,6 +82,15 @@ struct palq_net {
   bool img_input = false, img_direct = false;
   void *img_codes = nullptr;
   palq_act input{};
+  // PALQ_NET_GRAPH: the replayed graph and the call it was captured for
+  bool graph_warm = false;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t graph_exec = nullptr;
+  hipStream_t cap_stream = nullptr;  // capture only
+  const void *g_input = nullptr, *g_img = nullptr;
+  int32_t *g_logits = nullptr;
+  float g_l = 0.f, g_u = 0.f;
+  hipStream_t g_stream = nullptr;
 };
 
 namespace {
@@ -112,6 +121,9 @@ void free_net(palq_net *net) {
   for (void *b : net->bufs) if (b) hipFree(b);
   if (net->pool) hipFree(net->pool);
   if (net->img_codes) hipFree(net->img_codes);
+  if (net->graph_exec) hipGraphExecDestroy(net->graph_exec);
+  if (net->graph) hipGraphDestroy(net->graph);
+  if (net->cap_stream) hipStreamDestroy(net->cap_stream);
   for (hipEvent_t e : net->events) if (e) hipEventDestroy(e);
   delete net;
 }
@@ -160,7 +172,9 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
     rotate[i] = 1;
   }
   const palq_layer *layers = norm.data();
-  if (flags & ~(PALQ_NET_KEEP_ALL | PALQ_NET_TIMING)) return net_fail(ctx, PALQ_ERR_ARG, "unknown flags");
+  if (flags & ~(PALQ_NET_KEEP_ALL | PALQ_NET_TIMING | PALQ_NET_GRAPH)) return net_fail(ctx, PALQ_ERR_ARG, "unknown flags");
+  if ((flags & PALQ_NET_TIMING) && (flags & PALQ_NET_GRAPH))
+    return net_fail(ctx, PALQ_ERR_ARG, "PALQ_NET_GRAPH does not go with PALQ_NET_TIMING");
   if (input->n < 1 || input->h < 1 || input->w < 1 || input->groups < 1 || input->ch_per_group < 1 ||
       row_bytes(input->ch_per_group, input->bits) < 0)
     return net_fail(ctx, PALQ_ERR_ARG, "bad input descriptor");
@@ -534,8 +548,7 @@ namespace {
 // img != nullptr: the layers that read tensor 0 through a zero-border copy
 // quantise img (fp32, Eq. 2 with l, u) into that copy instead (img_direct).
 palq_status forward_impl(palq_ctx *ctx, palq_net *net, const void *input, int32_t *logits, const float *img,
-                         float l, float u) {
-  hipStream_t s = ctx->stream;
+                         float l, float u, hipStream_t s) {
   const size_t L = net->layers.size();
   hipEvent_t *ev = nullptr;
   if (net->flags & PALQ_NET_TIMING) {
@@ -603,6 +616,53 @@ palq_status forward_impl(palq_ctx *ctx, palq_net *net, const void *input, int32_
   if (e != hipSuccess) return net_fail(ctx, PALQ_ERR_DEVICE, std::string("forward: ") + hipGetErrorString(e));
   return PALQ_OK;
 }
+// PALQ_NET_GRAPH: replay the captured launch sequence when the call matches
+// the one it was captured for, else capture it anew (the first forward runs
+// eagerly, which also fills the launchers' per-kernel caches).
+palq_status forward_dispatch(palq_ctx *ctx, palq_net *net, const void *input, int32_t *logits, const float *img,
+                             float l, float u) {
+  hipStream_t s = ctx->stream;
+  if (!(net->flags & PALQ_NET_GRAPH)) return forward_impl(ctx, net, input, logits, img, l, u, s);
+  if (!net->graph_warm) {
+    net->graph_warm = true;
+    return forward_impl(ctx, net, input, logits, img, l, u, s);
+  }
+  const bool same = net->graph_exec && net->g_input == input && net->g_img == img && net->g_logits == logits &&
+                    net->g_l == l && net->g_u == u && net->g_stream == s;
+  if (!same) {
+    if (net->graph_exec) hipGraphExecDestroy(net->graph_exec);
+    if (net->graph) hipGraphDestroy(net->graph);
+    net->graph_exec = nullptr;
+    net->graph = nullptr;
+    // captured on a stream of the network's own (the caller's may be the
+    // null stream, which cannot capture); the graph is launched on the
+    // caller's stream
+    hipError_t e = hipSuccess;
+    if (!net->cap_stream) e = hipStreamCreateWithFlags(&net->cap_stream, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipStreamBeginCapture(net->cap_stream, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) return net_fail(ctx, PALQ_ERR_DEVICE, std::string("graph capture: ") + hipGetErrorString(e));
+    const palq_status st = forward_impl(ctx, net, input, logits, img, l, u, net->cap_stream);
+    hipGraph_t g = nullptr;
+    e = hipStreamEndCapture(net->cap_stream, &g);
+    if (st != PALQ_OK) {
+      if (g) hipGraphDestroy(g);
+      return st;
+    }
+    if (e != hipSuccess || !g) return net_fail(ctx, PALQ_ERR_DEVICE, std::string("graph capture: ") + hipGetErrorString(e));
+    hipGraphExec_t x = nullptr;
+    e = hipGraphInstantiate(&x, g, nullptr, nullptr, 0);
+    if (e != hipSuccess) {
+      hipGraphDestroy(g);
+      return net_fail(ctx, PALQ_ERR_DEVICE, std::string("graph instantiate: ") + hipGetErrorString(e));
+    }
+    net->graph = g;
+    net->graph_exec = x;
+    net->g_input = input; net->g_img = img; net->g_logits = logits;
+    net->g_l = l; net->g_u = u; net->g_stream = s;
+  }
+  const hipError_t e = hipGraphLaunch(net->graph_exec, s);
+  return e == hipSuccess ? PALQ_OK : net_fail(ctx, PALQ_ERR_DEVICE, std::string("graph launch: ") + hipGetErrorString(e));
+}
 }  // namespace
 
 palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_t *logits) {
@@ -613,7 +673,7 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
     return net_fail(ctx, PALQ_ERR_ARG, "input must be 16-byte and logits 4-byte aligned");
   if (ctx->device < 0) return PALQ_OK;
   hipSetDevice(ctx->device);
-  return forward_impl(ctx, net, input, logits, nullptr, 0.f, 0.f);
+  return forward_dispatch(ctx, net, input, logits, nullptr, 0.f, 0.f);
 }
 
 palq_status palq_forward_image(palq_ctx *ctx, palq_net *net, const float *x, float l, float u, int32_t *logits) {
@@ -628,10 +688,10 @@ palq_status palq_forward_image(palq_ctx *ctx, palq_net *net, const float *x, flo
     return net_fail(ctx, PALQ_ERR_ARG, "need finite l < u with finite u - l");
   if (ctx->device < 0) return PALQ_OK;
   hipSetDevice(ctx->device);
-  if (net->img_direct) return forward_impl(ctx, net, nullptr, logits, x, l, u);
+  if (net->img_direct) return forward_dispatch(ctx, net, nullptr, logits, x, l, u);
   const hipError_t e = launch_quantize(x, l, u, nullptr, view_of(&net->input), ctx->stream);
   if (e != hipSuccess) return net_fail(ctx, PALQ_ERR_DEVICE, std::string("quantize: ") + hipGetErrorString(e));
-  return forward_impl(ctx, net, net->img_codes, logits, nullptr, 0.f, 0.f);
+  return forward_dispatch(ctx, net, net->img_codes, logits, nullptr, 0.f, 0.f);
 }
 
 palq_status palq_net_tensor(const palq_net *net, int32_t id, palq_act *desc) {

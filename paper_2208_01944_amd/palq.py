@@ -30,7 +30,7 @@ c_i32, c_i64, c_p, c_f = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes
 
 OK, ERR_ARG, ERR_UNSUPPORTED, ERR_OVERFLOW, ERR_DEVICE, ERR_NOMEM = 0, -1, -2, -3, -4, -5
 OP_CONV, OP_MAXPOOL, OP_AVGSUM, OP_FC, OP_SHUFFLE_MODULE, OP_CHANNEL_SHUFFLE = 1, 2, 3, 4, 5, 6
-NET_KEEP_ALL, NET_TIMING = 1, 2
+NET_KEEP_ALL, NET_TIMING, NET_GRAPH = 1, 2, 4
 
 
 class Act(ctypes.Structure):

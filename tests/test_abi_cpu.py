@@ -215,6 +215,11 @@ def test_validate_only_forward_image(P, vctx):
     assert fi(vctx.h, h, _fake(20), -3.0, 3.0, _fake(21)) == P.ERR_ARG
     assert "image" in vctx.last_error()
     P._net_destroy(h)
+    # graph replay is a network flag; not together with per-layer timing
+    assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 3, P.NET_GRAPH, ctypes.byref(h)) == P.OK
+    P._net_destroy(h)
+    assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 3, P.NET_GRAPH | P.NET_TIMING, ctypes.byref(h)) == P.ERR_ARG
+    assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 3, 8, ctypes.byref(h)) == P.ERR_ARG  # unknown flag
 
 
 def test_validate_only_shuffle_module(P, vctx):

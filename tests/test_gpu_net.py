@@ -168,6 +168,55 @@ def test_forward_image_matches_quantize_then_forward(ctx, torch, stem_pad, hw):
     np.testing.assert_array_equal(a, ref)
 
 
+def test_graph_replay_matches_eager(ctx, torch):
+    """PALQ_NET_GRAPH: replays of the captured forward (same input buffer,
+    its contents changed between calls, eager work and synchronisations in
+    between) give the eager network's logits every time; a new input pointer
+    or the image entry point captures again."""
+    from paper_2208_01944_amd import palq
+    say("graph replay resnet18 hw=64 n=2")
+    spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=18)
+    spec = O.calibrate_centring(spec, spec["x"])
+    g = np.random.default_rng(81)
+    x2 = I.codes(g, spec["x"].shape, 8, True)
+    net_e = palq.Net(ctx, spec)
+    net_g = palq.Net(ctx, spec, flags=palq.NET_GRAPH)
+    xa, xb = ctx.pack(spec["x"], 1, 8, signed=True), ctx.pack(x2, 1, 8, signed=True)
+    buf = ctx.pack(spec["x"], 1, 8, signed=True)
+    ref = {}
+    for name, xt in (("a", xa), ("b", xb)):
+        out = torch.empty(200, dtype=torch.int32, device=ctx.dev)
+        net_e.forward(xt.buf, out)
+        ctx.sync()
+        ref[name] = out.cpu().numpy().astype(np.int64).reshape(2, 100)
+    np.testing.assert_array_equal(ref["a"], O.run_net(spec, spec["x"]))
+    out = torch.empty(200, dtype=torch.int32, device=ctx.dev)
+    scratch = torch.empty(200, dtype=torch.int32, device=ctx.dev)
+    for it in range(6):
+        name = "ab"[it % 2]
+        buf.buf.copy_((xa if name == "a" else xb).buf)
+        net_g.forward(buf.buf, out)        # it 0 eager, 1 capture, then replays
+        net_e.forward(xb.buf, scratch)     # eager work on the same stream
+        ctx.sync()
+        np.testing.assert_array_equal(out.cpu().numpy().astype(np.int64).reshape(2, 100), ref[name],
+                                      err_msg=f"call {it}")
+    net_g.forward(xb.buf, out)             # another input pointer: captured again
+    ctx.sync()
+    np.testing.assert_array_equal(out.cpu().numpy().astype(np.int64).reshape(2, 100), ref["b"])
+    # the image entry point through the graph, twice
+    xf = g.normal(0, 1.3, (2, 64, 64, 3)).astype(np.float32)
+    xd = ctx.upload(xf)
+    codes = ctx.empty_act(2, 64, 64, 1, 3, 8, True)
+    ctx.quantize(xd, -3.0, 3.0, codes)
+    net_e.forward(codes.buf, scratch)
+    ctx.sync()
+    want = scratch.cpu().numpy().copy()
+    for _ in range(2):
+        net_g.forward_image(xd, -3.0, 3.0, out)
+        ctx.sync()
+        np.testing.assert_array_equal(out.cpu().numpy(), want)
+
+
 def test_resnet50_small_all_tensors(ctx, torch):
     say("resnet50 hw=64 n=2 G=2 b=2 centred")
     spec = I.resnet50(n=2, groups=2, bits=2, hw=64, classes=50, seed=12)
