@@ -468,7 +468,10 @@ __global__ void avgsum2_kernel(ActView in, int32_t *out) {
 // Same sums with one workgroup per (image, group) when 256 is a multiple of
 // the words per row: thread (word, r) takes pixels r, r + R, ... (R = 256 /
 // words), and the R partial byte-lane sums of a word are added in LDS.
-__global__ __launch_bounds__(256) void avgsum2_wg_kernel(ActView in, int32_t *out) {
+// planes (nullable): also the FC's signed base-256 digit planes of the sums
+// (P planes of count bytes), and logits row n zeroed for the FC's atomics.
+__global__ __launch_bounds__(256) void avgsum2_wg_kernel(ActView in, int32_t *out, int8_t *planes, int P,
+                                                        int64_t count, int32_t *logits, int cout) {
   __shared__ uint32_t part[4][256];
   const int wpr = in.cpg / 16;
   const int R = 256 / wpr;
@@ -489,10 +492,22 @@ __global__ __launch_bounds__(256) void avgsum2_wg_kernel(ActView in, int32_t *ou
     const int w2 = idx >> 2, kk = idx & 3;
     uint32_t sum = 0;
     for (int rr = 0; rr < R; ++rr) sum += part[kk][rr * wpr + w2];
-    int32_t *o = out + (int64_t)n * in.groups * in.cpg + (int64_t)g * in.cpg + 16 * w2 + kk;
+    const int64_t c0 = (int64_t)n * in.groups * in.cpg + (int64_t)g * in.cpg + 16 * w2 + kk;
+    int32_t *o = out + c0;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) o[4 * b] = (int32_t)((sum >> (8 * b)) & 255u);
+    for (int b = 0; b < 4; ++b) {
+      const int32_t v = (int32_t)((sum >> (8 * b)) & 255u);
+      o[4 * b] = v;
+      if (planes) {  // v <= 255: digits v (one plane, v <= 127) or v - 256 and 1
+        const int d0 = (int)(int8_t)(uint8_t)v;
+        planes[c0 + 4 * b] = (int8_t)d0;
+        if (P > 1) planes[count + c0 + 4 * b] = (int8_t)((v - d0) >> 8);
+        for (int p = 2; p < P; ++p) planes[p * count + c0 + 4 * b] = 0;
+      }
+    }
   }
+  if (logits && g == 0)
+    for (int i = threadIdx.x; i < cout; i += 256) logits[(int64_t)n * cout + i] = 0;
 }
 __global__ void avgsum_kernel(ActView in, int32_t *out) {
   const int64_t C = (int64_t)in.groups * in.cpg;
@@ -775,13 +790,24 @@ hipError_t launch_pad_pixels(const ActView &in, int pad, const ActView &out, hip
   return hipGetLastError();
 }
 
-hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s) {
+bool avgsum_makes_fc_planes(const ActView &in) {
+  const int wpr = in.cpg / 16;
+  return in.bits == 2 && in.cpg % 16 == 0 && (int64_t)in.h * in.w <= 85 && wpr >= 1 && wpr <= 256 &&
+         256 % wpr == 0 && (int64_t)in.n * in.groups < ((int64_t)1 << 31);
+}
+
+int fc_planes(int64_t xmax) { return xmax >= 0 && xmax <= 127 ? 1 : xmax >= 0 && xmax <= 32639 ? 2 : 4; }
+
+hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s, int8_t *planes, int P, int32_t *logits,
+                         int cout) {
   const int64_t items = (int64_t)in.n * in.groups * in.cpg;
   if (items == 0) return hipSuccess;
+  if (planes && !avgsum_makes_fc_planes(in)) return hipErrorInvalidValue;
   if (in.bits == 2 && in.cpg % 16 == 0 && (int64_t)in.h * in.w <= 85) {
     const int wpr = in.cpg / 16;
     if (wpr <= 256 && 256 % wpr == 0 && (int64_t)in.n * in.groups < ((int64_t)1 << 31)) {
-      hipLaunchKernelGGL(avgsum2_wg_kernel, dim3((unsigned)(in.n * in.groups)), dim3(256), 0, s, in, out);
+      hipLaunchKernelGGL(avgsum2_wg_kernel, dim3((unsigned)(in.n * in.groups)), dim3(256), 0, s, in, out, planes, P,
+                         items, logits, cout);
       return hipGetLastError();
     }
     if (((uintptr_t)out & 15u) == 0) {
@@ -793,18 +819,25 @@ hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s) {
   return hipGetLastError();
 }
 
+bool fc_mfma_applies(const int32_t *x, int n, int cin, int cout, const int8_t *scratch) {
+  return scratch && cin % 32 == 0 && ((uintptr_t)x & 15u) == 0 && (int64_t)4 * n * cin < ((int64_t)1 << 31) &&
+         (int64_t)cout * cin < ((int64_t)1 << 31);
+}
+
 hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout, int32_t *logits,
-                     int8_t *scratch, hipStream_t s, int64_t xmax) {
+                     int8_t *scratch, hipStream_t s, int64_t xmax, bool planes_ready) {
   const int64_t items = (int64_t)n * cout;
   if (items == 0) return hipSuccess;
-  if (scratch && cin % 32 == 0 && ((uintptr_t)x & 15u) == 0 && (int64_t)4 * n * cin < ((int64_t)1 << 31) &&
-      (int64_t)cout * cin < ((int64_t)1 << 31)) {
+  if (fc_mfma_applies(x, n, cin, cout, scratch)) {
     const int64_t count = (int64_t)n * cin;
     // signed base-256 digit planes: one covers |x| <= 127, two |x| <= 32639,
-    // four every int32 (exact modulo 2^32)
-    const int P = xmax >= 0 && xmax <= 127 ? 1 : xmax >= 0 && xmax <= 32639 ? 2 : 4;
-    auto digits = P == 1 ? fc_digits_kernel<1> : P == 2 ? fc_digits_kernel<2> : fc_digits_kernel<4>;
-    hipLaunchKernelGGL(digits, dim3(grid_for(count / 4)), dim3(kBlock), 0, s, x, count, scratch, logits, items);
+    // four every int32 (exact modulo 2^32); planes_ready: the global sum
+    // wrote them and zeroed the logits
+    const int P = fc_planes(xmax);
+    if (!planes_ready) {
+      auto digits = P == 1 ? fc_digits_kernel<1> : P == 2 ? fc_digits_kernel<2> : fc_digits_kernel<4>;
+      hipLaunchKernelGGL(digits, dim3(grid_for(count / 4)), dim3(kBlock), 0, s, x, count, scratch, logits, items);
+    }
     // K slices (of at least 4 steps) for about 128 workgroups: more slices
     // only add contended atomics (ResNet-18 batch 64: 2 slices 16 us, 8
     // slices 20 us, 32 slices 48 us)

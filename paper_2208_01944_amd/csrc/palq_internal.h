@@ -115,7 +115,8 @@ hipError_t launch_shuffle(const ActView &in, int32_t steps, const ActView &out, 
 hipError_t launch_channel_shuffle(const ActView &in, const ActView &out, hipStream_t s);
 hipError_t launch_maxpool(const ActView &in, int k, int stride, int pad, const ActView &out,
                           hipStream_t s);
-hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s);
+hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s, int8_t *planes = nullptr, int P = 0,
+                         int32_t *logits = nullptr, int cout = 0);
 // out: in's shape grown by 2 pad pixels in h and w, same pixel bytes.
 hipError_t launch_pad_pixels(const ActView &in, int pad, const ActView &out, hipStream_t s);
 // Signed 8-bit codes (Eq. 2 with fixed l, u) of an fp32 [n][in_h][in_w][3]
@@ -128,7 +129,13 @@ hipError_t launch_quantize_pad(const float *x, float l, float u, int in_h, int i
 // the caller knows (fewer digit planes), or -1.
 size_t fc_scratch_bytes(int n, int cin);
 hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout, int32_t *logits,
-                     int8_t *scratch, hipStream_t s, int64_t xmax = -1);
+                     int8_t *scratch, hipStream_t s, int64_t xmax = -1, bool planes_ready = false);
+// The matrix-core FC path's conditions; its digit-plane count for |x| <= xmax.
+bool fc_mfma_applies(const int32_t *x, int n, int cin, int cout, const int8_t *scratch);
+int fc_planes(int64_t xmax);
+// Whether the global sum of `in` can also write the FC's digit planes (and
+// zero the logits): launch_avgsum with planes != nullptr.
+bool avgsum_makes_fc_planes(const ActView &in);
 
 }  // namespace palq
 

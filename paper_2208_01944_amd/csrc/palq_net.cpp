@@ -50,6 +50,11 @@ struct Layer {
   int fc_cin = 0;
   int8_t *fc_scratch = nullptr;  // digit planes of the FC input
   int64_t fc_xmax = -1;          // bound on the FC input (sums of codes)
+  // AVGSUM followed by the matrix-core FC: the sum also writes the FC's
+  // digit planes (fc_planes_out, P planes) and zeroes the logits
+  int8_t *fc_planes_out = nullptr;
+  int fc_planes_n = 0, fc_cout = 0;
+  bool fc_planes_ready = false;  // FC: skip its own digit pass
   // stem conv whose output only the following max pool reads: one fused
   // launch writes the pooled tensor (pool_out) and the pool layer is skipped
   bool pool_fused = false;
@@ -484,6 +489,20 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
     }
   }
 
+  // global sum + matrix-core FC: the sum writes the FC's digit planes
+  for (int i = 0; i + 1 < n_layers; ++i) {
+    Layer &A = net->layers[i], &F = net->layers[i + 1];
+    if (layers[i].op != PALQ_OP_AVGSUM || layers[i + 1].op != PALQ_OP_FC || layers[i + 1].src != layers[i].dst)
+      continue;
+    const palq_act &src = net->tensors[layers[i].src].d;
+    if (layers[i].src == 0 || !avgsum_makes_fc_planes(view_of(&src)) ||
+        !fc_mfma_applies(F.fc_in, net->n, F.fc_cin, layers[i + 1].fc_out, F.fc_scratch))
+      continue;
+    A.fc_planes_out = F.fc_scratch;
+    A.fc_planes_n = fc_planes(F.fc_xmax);
+    A.fc_cout = layers[i + 1].fc_out;
+    F.fc_planes_ready = true;
+  }
   if (hipStreamSynchronize(ctx->stream) != hipSuccess) {
     free_net(net);
     return net_fail(ctx, PALQ_ERR_DEVICE, "requant thresholds");
@@ -604,11 +623,13 @@ palq_status forward_impl(palq_ctx *ctx, palq_net *net, const void *input, int32_
       case PALQ_OP_AVGSUM: {
         palq_act iv = net->tensors[sp.src].d;
         if (sp.src == 0) iv.data = (void *)input;
-        e = launch_avgsum(view_of(&iv), NL.sums_out, s);
+        e = launch_avgsum(view_of(&iv), NL.sums_out, s, NL.fc_planes_out, NL.fc_planes_n,
+                          NL.fc_planes_out ? logits : nullptr, NL.fc_cout);
         break;
       }
       case PALQ_OP_FC:
-        e = launch_fc(NL.fc_in, net->n, NL.fc_cin, NL.fc_w, sp.fc_out, logits, NL.fc_scratch, s, NL.fc_xmax);
+        e = launch_fc(NL.fc_in, net->n, NL.fc_cin, NL.fc_w, sp.fc_out, logits, NL.fc_scratch, s, NL.fc_xmax,
+                      NL.fc_planes_ready);
         break;
     }
     if (ev && e == hipSuccess) hipEventRecord(ev[i + 1], s);
