@@ -361,16 +361,26 @@ def main():
                 r = shapes[L["proj_src"]]
                 nbytes += act_bytes(r[0], r[1], r[2], r[3]) + L["proj_w"].size * L["w_bits"] / 8
             kname = conv_kernel(L, ci, co, k)
+            nxt = spec["layers"][i + 1] if i + 1 < len(spec["layers"]) else {}
+            fused_pool = (kname == "conv_tile_kernel[stem]" and nxt.get("op") == "maxpool" and
+                          nxt.get("src") == L["dst"] and (nxt["k"], nxt["stride"], nxt["pad"]) == (3, 2, 1) and
+                          ho <= 127)
+            if fused_pool:  # the stem and its max pool run as one launch (its time includes the quantiser)
+                kname = "quantize_pad4_kernel + stem_pool_kernel"
             per_layer.append(dict(layer=i, op="conv", kernel=kname, ops=ops, bytes=nbytes,
                                   ms=float(layer_ms[i])))
         else:
             if L["op"] == "maxpool":
                 ho = (s[0] + 2 * L["pad"] - L["k"]) // L["stride"] + 1
                 shapes[L["dst"]] = (ho, ho, s[2], s[3])
-                kname = "maxpool_kernel"
+                prev = per_layer[-1] if per_layer else {}
+                kname = ("fused into layer %d (no launch)" % prev["layer"]
+                         if prev.get("kernel", "").endswith("stem_pool_kernel") else "maxpool_kernel")
             else:
                 shapes[L["dst"]] = (1, 1, s[2], 32)
-                kname = "avgsum_kernel" if L["op"] == "avgsum" else "fc_kernel"
+                # this workload's paths: the per-image sum kernel (which also
+                # writes the FC's digit planes) and the matrix-core FC
+                kname = "avgsum2_wg_kernel" if L["op"] == "avgsum" else "fc_mfma_kernel"
             per_layer.append(dict(layer=i, op=L["op"], kernel=kname, ms=float(layer_ms[i])))
         K = kern.setdefault(kname, dict(launches=0, ops=0, bytes=0.0, ms=0.0))
         K["launches"] += 1
