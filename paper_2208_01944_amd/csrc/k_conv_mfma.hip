@@ -2065,12 +2065,18 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   const int64_t T = (int64_t)npt * ncb * a.in.groups;
   if (T <= 0 || T > 0x7fffffff) return hipErrorInvalidValue;
   const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S, FP4, KPI>, WN * WM * 64);
-  // Pixel chunks (tile_at): 8, so that an XCD fetches each input line once
-  // for all groups, unless the filter is the larger read (every XCD then
-  // reads all of it): about 7 W extra against (G - 1) X saved.
+  // Pixel chunks (tile_at): 32 (four per XCD), so that an XCD fetches each
+  // input line once for all groups while a chunk's lines still fit its L2,
+  // unless the filter is the larger read (every XCD then reads all of it):
+  // about 7 W extra against (G - 1) X saved.
   const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * (FP4 ? 32 : 64);
   const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
-  const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(8, npt) : 1;
+  static int nch_env = -1;  // PALQ_TILE_NCH: chunk count when chunked (tuning)
+  if (nch_env < 0) {
+    const char *e = getenv("PALQ_TILE_NCH");
+    nch_env = e && atoi(e) >= 1 && atoi(e) <= 256 ? atoi(e) : 32;
+  }
+  const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(nch_env, npt) : 1;
   // P workgroups per XCD: all resident slots, no more than the XCD's
   // tiles, and runs of at most npt / nch tiles (two (chunk, combo) segments)
   const int64_t Tx = (T + 7) / 8;
