@@ -182,7 +182,7 @@ def conv_layer(x, w, stride, pad, mult, shift, bias, out_bits, shuffle=0,
                res=None, res_mult=None, proj_x=None, proj_w=None, proj_stride=1):
     """A B-bit grouped conv followed by requantisation and the cyclic
     permutation, returning (codes, acc) with both in output (destination)
-    channel order.
+    channel order: step 1 below, then layer_epilogue (steps 2-4).
 
     Steps, in order:
       1. acc = group_conv(x, w)  (source group g, channel k);
@@ -200,8 +200,18 @@ def conv_layer(x, w, stride, pad, mult, shift, bias, out_bits, shuffle=0,
     The returned acc is everything the contraction sums into each output
     channel: the permuted conv accumulator plus the projection accumulator.
     """
-    g = w.shape[0]
     acc = group_conv(x, w, stride, pad)
+    return layer_epilogue(acc, w.shape[0], mult, shift, bias, out_bits, shuffle, res=res,
+                          res_mult=res_mult, proj_x=proj_x, proj_w=proj_w, proj_stride=proj_stride)
+
+
+def layer_epilogue(acc, groups, mult, shift, bias, out_bits, shuffle=0, res=None, res_mult=None,
+                   proj_x=None, proj_w=None, proj_stride=1):
+    """Steps 2-4 of conv_layer on the layer's accumulator acc (source channel
+    order, as group_conv returns it); returns (codes, acc_d) like conv_layer.
+    With shuffle, res and proj_x the same, conv_layer(x, w, ...) equals
+    layer_epilogue(group_conv(x, w, ...), G, ...)."""
+    g = groups
     acc_d = cyclic_permute(acc, g, shuffle)
     bias = np.zeros(acc.shape[-1], np.int64) if bias is None else np.asarray(bias, np.int64)
     bias_d = cyclic_permute(bias, g, shuffle)
@@ -214,6 +224,26 @@ def conv_layer(x, w, stride, pad, mult, shift, bias, out_bits, shuffle=0,
         rm_d = cyclic_permute(np.asarray(res_mult, np.int64), g, shuffle)
         t = t + rm_d * np.asarray(res, np.int64)
     return requant(t, mult_d, shift_d, out_bits), acc_d
+
+
+def centring_bias(acc_d, groups, shuffle=0, res=None, res_mult=None):
+    """The centred variant's conv bias (a test-input recipe, not part of the
+    method): bias_d[c] = -round_half_up(mean over all positions of
+    (acc_d + residual)[c]) at destination channel c, computed exactly with
+    Python integers, returned indexed by the source channel (the permutation
+    undone) as an int32 array.  acc_d: the layer's destination-order
+    accumulator (conv_layer's second result, which already holds any
+    projection accumulator); res/res_mult: the identity shortcut, if any."""
+    from fractions import Fraction
+    t = np.asarray(acc_d, np.int64)
+    if res is not None:
+        rm_d = cyclic_permute(np.asarray(res_mult, np.int64), groups, shuffle)
+        t = t + rm_d * np.asarray(res, np.int64)
+    cnt = int(np.prod(t.shape[:-1]))
+    sums = t.reshape(-1, t.shape[-1]).sum(axis=0)
+    bias_d = np.array([-int((Fraction(int(s), cnt) + Fraction(1, 2)).__floor__()) for s in sums],
+                      dtype=np.int64)
+    return cyclic_permute(bias_d, groups, -shuffle).astype(np.int32)
 
 
 def channel_shuffle(x, groups: int) -> np.ndarray:
@@ -322,59 +352,52 @@ def run_net(net, x, keep=False):
     return out
 
 
-def calibrate_centring(net, x):
+def calibrate_centring(net, x, return_logits=False):
     """Returns a copy of `net` whose conv biases centre every layer's
     pre-requant value: bias[c] = -round_half_up(mean over positions of
-    (acc + residual)[c]), computed exactly (Python integers) in layer order on
+    (acc + residual)[c]) (centring_bias), computed exactly in layer order on
     the oracle's own forward pass over x.  Used only to build non-degenerate
-    test inputs; the biases are then ordinary inputs to both sides."""
+    test inputs; the biases are then ordinary inputs to both sides.  With
+    return_logits the oracle's output of the centred network on x (the
+    last layer's result, equal to run_net(centred, x)) is returned too."""
     import copy
-    from fractions import Fraction
 
     net = copy.deepcopy(net)
     tensors = {0: np.asarray(x, dtype=np.int64)}
+    out = None
     for L in net["layers"]:
         src = tensors[L["src"]]
         if L["op"] == "conv":
             g = L["w"].shape[0]
             res = tensors[L["res"]] if L.get("res", -1) >= 0 else None
             px = tensors[L["proj_src"]] if L.get("proj_src", -1) >= 0 else None
-            zero = np.zeros(L["w"].shape[0] * L["w"].shape[1], np.int64)
-            _, acc_d = conv_layer(src, L["w"], L["stride"], L["pad"], L["mult"], L["shift"], zero,
-                                  L["out_bits"], L.get("shuffle", 0), proj_x=px,
-                                  proj_w=L.get("proj_w"), proj_stride=L.get("proj_stride", 1))
-            t = acc_d
-            if res is not None:
-                rm_d = cyclic_permute(np.asarray(L["res_mult"], np.int64), g, L.get("shuffle", 0))
-                t = t + rm_d * np.asarray(res, np.int64)
-            cnt = t.shape[0] * t.shape[1] * t.shape[2]
-            sums = t.reshape(-1, t.shape[-1]).sum(axis=0)
-            bias_d = np.array([-int((Fraction(int(s), cnt) + Fraction(1, 2)).__floor__()) for s in sums],
-                              dtype=np.int64)
-            # bias is indexed by the source channel: undo the permutation
-            L["bias"] = cyclic_permute(bias_d, g, -L.get("shuffle", 0)).astype(np.int32)
-            q, _ = conv_layer(src, L["w"], L["stride"], L["pad"], L["mult"], L["shift"], L["bias"],
-                              L["out_bits"], L.get("shuffle", 0), res=res, res_mult=L.get("res_mult"),
-                              proj_x=px, proj_w=L.get("proj_w"), proj_stride=L.get("proj_stride", 1))
-            tensors[L["dst"]] = q
+            acc = group_conv(src, L["w"], L["stride"], L["pad"])
+            kw = dict(res=res, res_mult=L.get("res_mult"), proj_x=px, proj_w=L.get("proj_w"),
+                      proj_stride=L.get("proj_stride", 1))
+            _, acc_d = layer_epilogue(acc, g, L["mult"], L["shift"], None, L["out_bits"],
+                                      L.get("shuffle", 0), **kw)
+            L["bias"] = centring_bias(acc_d, g, L.get("shuffle", 0), res=res,
+                                      res_mult=L.get("res_mult"))
+            out, _ = layer_epilogue(acc, g, L["mult"], L["shift"], L["bias"], L["out_bits"],
+                                    L.get("shuffle", 0), **kw)
         elif L["op"] == "shuffle_module":
             _, acc = shuffle_module(src, L["w"], L["mult"], L["shift"], None, L["res_mult"],
                                     L["out_bits"])
             t = acc + np.asarray(L["res_mult"], np.int64) * src
-            cnt = t.shape[0] * t.shape[1] * t.shape[2]
-            sums = t.reshape(-1, t.shape[-1]).sum(axis=0)
-            L["bias"] = np.array([-int((Fraction(int(s), cnt) + Fraction(1, 2)).__floor__()) for s in sums],
-                                 dtype=np.int32)
-            tensors[L["dst"]], _ = shuffle_module(src, L["w"], L["mult"], L["shift"], L["bias"],
-                                                  L["res_mult"], L["out_bits"])
+            L["bias"] = centring_bias(t, L["w"].shape[0])
+            out, _ = shuffle_module(src, L["w"], L["mult"], L["shift"], L["bias"],
+                                    L["res_mult"], L["out_bits"])
         elif L["op"] == "channel_shuffle":
-            tensors[L["dst"]] = channel_shuffle(src, L["groups"])
+            out = channel_shuffle(src, L["groups"])
         elif L["op"] == "maxpool":
-            tensors[L["dst"]] = maxpool(src, L["k"], L["stride"], L["pad"])
+            out = maxpool(src, L["k"], L["stride"], L["pad"])
         elif L["op"] == "avgsum":
-            tensors[L["dst"]] = avgsum(src)
+            out = avgsum(src)
         elif L["op"] == "fc":
-            tensors[L["dst"]] = fc(src, L["w"])
+            out = fc(src, L["w"])
+        tensors[L["dst"]] = out
+    if return_logits:
+        return net, out
     return net
 
 

@@ -423,6 +423,74 @@ def test_conv_layer_shuffle_writes_branch_one_group_on():
     np.testing.assert_array_equal(acc[..., 2 * co:3 * co], plain[..., co:2 * co])
 
 
+@pytest.mark.parametrize("G,shuffle", [(4, 1), (4, 3), (4, -1), (3, 2), (2, 1)])
+def test_conv_layer_projection_shortcut_independent(G, shuffle):
+    """The projection shortcut (reading A10): destination group j receives the
+    main branch of source group (j - s) mod G with that source channel's
+    bias, M and shift (Eq. 8 moves the branch), plus the raw accumulator of
+    the 1x1, stride-s, pad-0 conv of the block input's OWN group j with the
+    projection filter of group j, not permuted.  Rebuilt here from torch
+    float64 convolutions (one per destination group for the projection) and
+    Python-int requantisation, and compared with conv_layer's acc and codes.
+    An odd input size with stride 2 makes a wrong projection stride, pad or
+    pixel index visible; distinct groups make a source/destination mix-up
+    visible."""
+    g = np.random.default_rng(40 + G * 10 + shuffle)
+    ci, co, cp, h, stride = 5, 3, 6, 9, 2
+    x = I.codes(g, (2, h, h, G * ci), 2, False)
+    w = I.codes(g, (G, co, 3, 3, ci), 2, True)
+    px = I.codes(g, (2, h, h, G * cp), 2, False)
+    pw = I.codes(g, (G, co, 1, 1, cp), 2, True)
+    mult = g.integers(1 << 14, 1 << 15, G * co)
+    shift = np.full(G * co, 13)
+    bias = g.integers(20, 90, G * co)
+    q, acc = O.conv_layer(x, w, stride, 1, mult, shift, bias, 8, shuffle=shuffle,
+                          proj_x=px, proj_w=pw, proj_stride=stride)
+    main = _torch_group_conv(x, w, stride, 1)                     # source channel order
+    ho = main.shape[1]
+    assert acc.shape == (2, ho, ho, G * co)
+    want_acc = np.zeros_like(main)
+    want_q = np.zeros_like(main)
+    for j in range(G):
+        src = (j - shuffle) % G
+        pj = _torch_group_conv(px[..., j * cp:(j + 1) * cp], pw[j:j + 1], stride, 0)
+        assert pj.shape == (2, ho, ho, co)
+        for k in range(co):
+            cs, cd = src * co + k, j * co + k
+            want_acc[..., cd] = main[..., cs] + pj[..., k]
+            for idx in np.ndindex(2, ho, ho):
+                t = int(main[idx + (cs,)]) + int(bias[cs]) + int(pj[idx + (k,)])
+                m, sh = int(mult[cs]), int(shift[cs])
+                want_q[idx + (cd,)] = min(max((t * m + (1 << (sh - 1))) >> sh, 0), 255)
+    np.testing.assert_array_equal(acc, want_acc)
+    np.testing.assert_array_equal(q, want_q)
+    assert len(np.unique(want_q)) > 10  # the codes are not degenerate
+
+
+def test_layer_epilogue_and_centring_single_pass():
+    """conv_layer is group_conv followed by layer_epilogue, and the
+    one-pass calibrate_centring returns the logits run_net gives on the
+    centred network (identity and projection shortcuts, shuffles)."""
+    spec = I.resnet18(n=2, groups=2, bits=2, hw=32, classes=10, seed=3, stages=(1, 1, 1, 1))
+    cen, logits = O.calibrate_centring(spec, spec["x"], return_logits=True)
+    np.testing.assert_array_equal(logits, O.run_net(cen, spec["x"]))
+    assert O.calibrate_centring(spec, spec["x"])["layers"][2]["bias"].tolist() == \
+        cen["layers"][2]["bias"].tolist()
+    _, tensors, _ = O.run_net(cen, spec["x"], keep=True)
+    for L in cen["layers"]:
+        if L["op"] == "conv" and L["src"] > 0:
+            codes = tensors[L["dst"]]
+            assert len(np.unique(codes)) >= 3, L["dst"]   # not degenerate (1x1 maps at stage 4)
+    case = I.single_layer(9, n=1, h=6, w=6, groups=3, cin=4, cout=5, residual="identity", shuffle=2)
+    L = case["layer"]
+    a = O.conv_layer(case["x"], L["w"], 1, 1, L["mult"], L["shift"], L["bias"], 2, 2,
+                     res=case["extra"][1], res_mult=L["res_mult"])
+    b = O.layer_epilogue(O.group_conv(case["x"], L["w"], 1, 1), 3, L["mult"], L["shift"], L["bias"],
+                         2, 2, res=case["extra"][1], res_mult=L["res_mult"])
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+
+
 # ---------------------------------------------------------------------------
 # Glue: pooling, sum, FC
 # ---------------------------------------------------------------------------
