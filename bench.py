@@ -35,7 +35,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--batch", type=int, default=64)
+    ap.add_argument("--batch", type=int, default=64, help="batch of the --table2 networks")
+    ap.add_argument("--workload", default="resnet18_g4_b2",
+                    help="resnet18_g4_b2 (the default: ResNet-18 G=4 2-bit, batch 64) or "
+                         "resnet50_g2_b2 (ResNet-50 G=2 2-bit, batch 128)")
+    ap.add_argument("--no-histograms", action="store_true",
+                    help="skip the per-layer output-code histograms (an untimed extra forward)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true", help="replay the forward from a captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -78,16 +83,16 @@ def measured_traffic():
 
 PROFILE_CMDS = {
     "kt": "rocprofv3 --kernel-trace --stats --output-format csv -d DIR/kt -o run -- "
-          "python3 bench.py --steps 20 --warmup 2 --no-cpu-baseline",
+          "python3 bench.py --workload W --steps 20 --warmup 2 --no-cpu-baseline --no-histograms",
     "fetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR/fetch -o run -- "
-             "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
+             "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-histograms",
     "write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d DIR/write -o run -- "
-             "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
+             "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-histograms",
     "cfetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR/cfetch -o run -- "
               "python3 bench.py --hbm-copy-probe 1024",
     "cwrite": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d DIR/cwrite -o run -- "
               "python3 bench.py --hbm-copy-probe 1024",
-    "bench": "python3 bench.py --steps 50 --warmup 5 --no-cpu-baseline > DIR/bench.json",
+    "bench": "python3 bench.py --workload W --steps 50 --warmup 5 --no-cpu-baseline > DIR/bench.json",
 }
 
 
@@ -108,17 +113,20 @@ def family(short):
     return "conv_tile_kernel[fp4]" if len(args) > 7 and args[7] == "true" else "conv_tile_kernel[int8]"
 
 
-def summarize_profile(d):
-    """Writes the kernel-time and HBM-traffic summaries of one profiling
-    session (rocprofv3 csv output) under profiles/."""
+def summarize_profile(d, workload):
+    """Writes the kernel-time summary of one profiling session (rocprofv3
+    csv output under DIR: kt/ and bench.json) and, when DIR also holds the
+    counter passes (fetch/, write/, cfetch/, cwrite/; ResNet-18 workload),
+    the HBM-traffic summary under profiles/."""
     import csv
     import hashlib
     bench = json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
     head = ["# commands (run from the repository root, on one MI355X, `cd /tmp && export TMPDIR=/tmp` first;",
-            "# DIR is any output folder)"]
+            "# DIR is any output folder, W = " + workload + ")"]
     # ---- kernel time
     rows = list(csv.DictReader(open(os.path.join(d, "kt", "run_kernel_stats.csv"))))
-    out = head + ["#   " + PROFILE_CMDS["kt"], "#   " + PROFILE_CMDS["bench"], "",
+    out = head + ["#   " + PROFILE_CMDS["kt"], "#   " + PROFILE_CMDS["bench"],
+                  "#   python3 bench.py --workload W --summarize-profile DIR", "",
                   "Kernel time, rocprofv3 --kernel-trace --stats (all launches of the profiled run:",
                   "create-time weight prepack, 2+20 steps of the plain network and of the HIP-event-timed one)", "",
                   "| kernel | calls | total ms | avg us | min us | max us | % |", "|---|---|---|---|---|---|---|"]
@@ -143,7 +151,12 @@ def summarize_profile(d):
     for L in bench["layers"]:
         out.append(f"| {L['layer']} | {L['op']} | {L.get('kernel', '')} | {L['ms'] * 1e3:.1f} | "
                    f"{L.get('ops', 0):.3e} | {L.get('bytes', 0):.3e} |")
-    open(os.path.join(ROOT, "profiles", "resnet18_g4_b2_bs64_kernel_stats.md"), "w").write("\n".join(out) + "\n")
+    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    out += ["", "kernel_source_sha256: " + src]
+    open(kernel_stats_file(workload), "w").write("\n".join(out) + "\n")
+    print("wrote", kernel_stats_file(workload))
+    if not os.path.isdir(os.path.join(d, "fetch")):
+        return
 
     # ---- traffic
     def load(sub):
@@ -161,7 +174,6 @@ def summarize_profile(d):
     assert len(gl) % nl == 0
     nf = len(gl) // nl
     per_launch = sum(a + b for a, b in gl) / len(gl)
-    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
     out = head + ["#   " + PROFILE_CMDS[k] for k in ("fetch", "write", "cfetch", "cwrite")] + [
         "",
         "HBM traffic of %s, ResNet-18 PalQuant G=4 2-bit, batch 64 (%d forwards x %d launches)"
@@ -193,25 +205,6 @@ def copy_probe(mib):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 3}))
-
-
-def conv_kernel(L, ci, co, k):
-    """Which kernel family the library's selection rules give a conv layer of
-    this workload (the stem and 2-bit grouped layers take the tiled kernel;
-    2-bit layers run on FP4 matrix cores unless PALQ_CONV_FP4=0)."""
-    stem = L["in_bits"] == 8 and L["in_signed"] and L["w_bits"] == 8 and ci <= 4 and k <= 8
-    if stem:
-        tiled = co % 128 == 0 and L.get("res", -1) < 0 and L["out_bits"] == 2
-        return "conv_tile_kernel[stem]" if tiled else "conv_stem_kernel"
-    grouped = co % 32 == 0 and ci % 64 == 0 and L["in_bits"] == L["w_bits"] and not L["in_signed"]
-    if not grouped:
-        return "conv_direct_kernel"
-    tiled = L["in_bits"] == 2 and co % 64 == 0 and L["out_bits"] == 2
-    if not tiled:
-        return "conv_grouped_kernel"
-    bound = k * k * ci * 3 * 2 + (L["proj_w"].shape[-1] * 3 * 2 if L.get("proj_w") is not None else 0)
-    fp4 = os.environ.get("PALQ_CONV_FP4", "1") != "0" and bound < (1 << 23)
-    return "conv_tile_kernel[fp4]" if fp4 else "conv_tile_kernel[int8]"
 
 
 def table2(args):
@@ -254,6 +247,26 @@ def table2(args):
         print(json.dumps(row), flush=True)
 
 
+def host_cpu():
+    """nproc and the CPU model name of this host (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    model = None
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except (OSError, subprocess.SubprocessError):
+        pass
+    if model is None and os.path.exists("/proc/cpuinfo"):
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    return os.cpu_count(), model
+
+
 def cpu_baseline(spec, x_f32, l, u, budget_s):
     """The oracle (as it stands) on a bounded sample of the same workload:
     whole images (quantise + forward), one at a time, until the budget is
@@ -268,38 +281,116 @@ def cpu_baseline(spec, x_f32, l, u, budget_s):
         if time.perf_counter() - t0 >= budget_s:
             break
     dt = time.perf_counter() - t0
+    nproc, model = host_cpu()
     return {"value": done / dt, "unit": "images/s", "cores": O.threads(), "kind": "oracle",
+            "threads_used": O.threads(), "nproc": nproc, "cpu_model": model,
             "sample": f"{done} of {spec['n']} images of the same batch, quantise + full forward, "
-                      f"{dt:.1f} s wall"}
+                      f"{dt:.1f} s wall (the oracle's C convolution loop on an OpenMP team of "
+                      f"{O.threads()} threads; its numpy requant and glue single-threaded)"}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
-        sys.exit(2)
-    if args.summarize_profile:
-        summarize_profile(args.summarize_profile)
-        return
-    if args.hbm_copy_probe:
-        copy_probe(args.hbm_copy_probe)
-        return
-    if args.table2:
-        table2(args)
-        return
+NETWORKS = {
+    # workload name -> (config name in the JSON line, metric)
+    "resnet18_g4_b2": ("resnet18_palq_G4_b2_224_fwd_centred", METRIC),
+    "resnet50_g2_b2": ("resnet50_palq_G2_b2_224_fwd_centred",
+                       "effective int TOPS + images/s, ResNet-50-shaped G=2 2-bit fwd, batch 128"),
+}
+
+
+def kernel_stats_file(workload):
+    return os.path.join(ROOT, "profiles", f"{workload}_kernel_stats.md")
+
+
+def rocprof_avg_us(workload, kernel):
+    """Average launch duration of `kernel` in the committed rocprofv3
+    summary of this workload, or None when the summary is missing or the
+    kernel source changed since it was taken."""
+    import hashlib
+    path = kernel_stats_file(workload)
+    if not os.path.exists(path):
+        return None
+    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    avg, sha = None, None
+    for line in open(path):
+        if line.startswith("kernel_source_sha256:"):
+            sha = line.split(":", 1)[1].strip()
+        if line.startswith(kernel + ", all instantiations:"):
+            avg = float(line.split("average", 1)[1].split("us")[0])
+    return avg if sha == src else None
+
+
+def network_algorithmic(spec, n):
+    """Per layer: 2 x MACs and the bytes a launch must move at least once
+    (packed input codes, packed weights, packed output codes, the residual /
+    projection input and the per-channel requant arrays)."""
+    def act_bytes(h, w, c, bits):
+        return n * h * w * c * bits / 8
+
+    shapes = {0: (spec["hw"], spec["hw"], 3, 8)}
+    out = []
+    for L in spec["layers"]:
+        s = shapes[L["src"]]
+        if L["op"] == "conv":
+            g, co, k, _, ci = L["w"].shape
+            ho = (s[0] + 2 * L["pad"] - k) // L["stride"] + 1
+            kk = k * k * ci + (L["proj_w"].shape[-1] if L.get("proj_w") is not None else 0)
+            ops = 2 * n * ho * ho * g * co * kk
+            shapes[L["dst"]] = (ho, ho, g * co, L["out_bits"])
+            nbytes = act_bytes(s[0], s[1], s[2], s[3]) + g * co * k * k * ci * L["w_bits"] / 8 \
+                + act_bytes(ho, ho, g * co, L["out_bits"]) + 3 * 4 * g * co
+            if L.get("res", -1) >= 0:
+                r = shapes[L["res"]]
+                nbytes += act_bytes(r[0], r[1], r[2], r[3]) + 4 * g * co
+            if L.get("proj_src", -1) >= 0:
+                r = shapes[L["proj_src"]]
+                nbytes += act_bytes(r[0], r[1], r[2], r[3]) + L["proj_w"].size * L["w_bits"] / 8
+            out.append(dict(ops=ops, bytes=nbytes))
+        else:
+            if L["op"] == "maxpool":
+                ho = (s[0] + 2 * L["pad"] - L["k"]) // L["stride"] + 1
+                shapes[L["dst"]] = (ho, ho, s[2], s[3])
+            else:
+                shapes[L["dst"]] = (1, 1, s[2], 32)
+            out.append({})
+    return out
+
+
+def code_histograms(ctx, spec, xd, l, u):
+    """Per conv layer of the network: how often each output code occurs on
+    this batch (a KEEP_ALL build of the same network, untimed)."""
+    import torch
+    from paper_2208_01944_amd import palq
+    net = palq.Net(ctx, spec, flags=palq.NET_KEEP_ALL)
+    logits = torch.empty(spec["n"] * net.classes, dtype=torch.int32, device=ctx.dev)
+    net.forward_image(xd, l, u, logits)
+    ctx.sync()
+    hist = {}
+    for i, L in enumerate(spec["layers"]):
+        if L["op"] == "conv":
+            t = net.tensor(L["dst"])
+            a = t.act
+            nb = a.n * a.h * a.w * a.groups * a.ch_per_group
+            codes = torch.empty(nb, dtype=torch.uint8, device=ctx.dev)
+            ctx._check(palq._unpack(ctx.h, palq.ctypes.byref(a), codes.data_ptr()))
+            hist[str(i)] = torch.bincount(codes, minlength=1 << L["out_bits"]).cpu().tolist()
+    del net
+    return hist
+
+
+def run_network(args, workload):
     import torch
     from paper_2208_01944_amd import inputs as I
     from paper_2208_01944_amd import palq
 
-    n = args.batch
-    spec = I.resnet18(n=n, groups=4, bits=2)
-    x_f32 = I.image_fp32(I.SEED_BASE + 30, n)
-    l, u = -3.0, 3.0
+    cfg_name, metric = NETWORKS[workload]
+    spec, x_f32, calib = I.workload(workload)
+    spec = I.with_stored_biases(spec, workload)  # the centred variant (oracle-calibrated biases)
+    n = spec["n"]
+    l, u = I.IMAGE_RANGE
 
     ctx = palq.Context(0)
-    stream = torch.cuda.current_stream()
     # eager launches (--graph: replay from a captured HIP graph, which
-    # measured about 1.5 % slower for this network)
+    # measured about 1.5 % slower for the ResNet-18 network)
     net = palq.Net(ctx, spec, flags=palq.NET_GRAPH if args.graph else 0)
     net_t = palq.Net(ctx, spec, flags=palq.NET_TIMING)
     xd = ctx.upload(x_f32)
@@ -314,6 +405,9 @@ def main():
         step(net)
         step(net_t)
     torch.cuda.synchronize()
+    distinct = int(torch.unique(logits).numel())
+    if distinct < 100:
+        raise SystemExit(f"the network's logits are degenerate ({distinct} distinct values)")
 
     # timed region: K whole steps
     t0 = time.perf_counter()
@@ -333,76 +427,36 @@ def main():
     wall_t = time.perf_counter() - t1
     layer_ms, fw = net_t.layer_times()
     layer_ms = layer_ms / max(fw, 1)
-
-    # algorithmic work per layer (2 x MACs, and the bytes a launch must move
-    # at least once: packed input codes, packed weights, packed output codes,
-    # the residual / projection input and the per-channel requant arrays) and
-    # which kernel runs it
-    def act_bytes(h, w, c, bits):
-        return n * h * w * c * bits / 8
+    labels = net_t.layer_kernels(image=True)
+    alg = network_algorithmic(spec, n)
 
     kern = {}
-    shapes = {0: (224, 224, 3, 8)}
     per_layer = []
     for i, L in enumerate(spec["layers"]):
-        s = shapes[L["src"]]
-        if L["op"] == "conv":
-            g, co, k, _, ci = L["w"].shape
-            ho = (s[0] + 2 * L["pad"] - k) // L["stride"] + 1
-            kk = k * k * ci + (L["proj_w"].shape[-1] if L.get("proj_w") is not None else 0)
-            ops = 2 * n * ho * ho * g * co * kk
-            shapes[L["dst"]] = (ho, ho, g * co, L["out_bits"])
-            nbytes = act_bytes(s[0], s[1], s[2], s[3]) + g * co * k * k * ci * L["w_bits"] / 8 \
-                + act_bytes(ho, ho, g * co, L["out_bits"]) + 3 * 4 * g * co
-            if L.get("res", -1) >= 0:
-                r = shapes[L["res"]]
-                nbytes += act_bytes(r[0], r[1], r[2], r[3]) + 4 * g * co
-            if L.get("proj_src", -1) >= 0:
-                r = shapes[L["proj_src"]]
-                nbytes += act_bytes(r[0], r[1], r[2], r[3]) + L["proj_w"].size * L["w_bits"] / 8
-            kname = conv_kernel(L, ci, co, k)
-            nxt = spec["layers"][i + 1] if i + 1 < len(spec["layers"]) else {}
-            fused_pool = (kname == "conv_tile_kernel[stem]" and nxt.get("op") == "maxpool" and
-                          nxt.get("src") == L["dst"] and (nxt["k"], nxt["stride"], nxt["pad"]) == (3, 2, 1) and
-                          ho <= 127)
-            if fused_pool:  # the stem and its max pool run as one launch (its time includes the quantiser)
-                kname = "quantize_pad4_kernel + stem_pool_kernel"
-            per_layer.append(dict(layer=i, op="conv", kernel=kname, ops=ops, bytes=nbytes,
-                                  ms=float(layer_ms[i])))
-        else:
-            if L["op"] == "maxpool":
-                ho = (s[0] + 2 * L["pad"] - L["k"]) // L["stride"] + 1
-                shapes[L["dst"]] = (ho, ho, s[2], s[3])
-                prev = per_layer[-1] if per_layer else {}
-                kname = ("fused into layer %d (no launch)" % prev["layer"]
-                         if prev.get("kernel", "").endswith("stem_pool_kernel") else "maxpool_kernel")
-            else:
-                shapes[L["dst"]] = (1, 1, s[2], 32)
-                # this workload's paths: the per-image sum kernel (which also
-                # writes the FC's digit planes) and the matrix-core FC
-                kname = "avgsum2_wg_kernel" if L["op"] == "avgsum" else "fc_mfma_kernel"
-            per_layer.append(dict(layer=i, op=L["op"], kernel=kname, ms=float(layer_ms[i])))
+        kname = labels[i] or "(covered by layer %d's launch)" % (i - 1)
+        row = dict(layer=i, op=L["op"], kernel=kname, ms=float(layer_ms[i]), **alg[i])
+        per_layer.append(row)
         K = kern.setdefault(kname, dict(launches=0, ops=0, bytes=0.0, ms=0.0))
         K["launches"] += 1
-        K["ms"] += float(layer_ms[i])
-        K["ops"] += per_layer[-1].get("ops", 0)
-        K["bytes"] += per_layer[-1].get("bytes", 0.0)
+        K["ms"] += row["ms"]
+        K["ops"] += row.get("ops", 0)
+        K["bytes"] += row.get("bytes", 0.0)
 
     total_ops = net.ops
     img_s = n / (ms_per_step / 1e3)
     tops = total_ops / (ms_per_step / 1e3) / 1e12
-    # the dominant kernel: the grouped 2-bit conv (3x3 convs of the residual
-    # blocks, projections fused), 16 launches per step, on FP4 matrix cores
-    # (int8 with PALQ_CONV_FP4=0); its peak is that of the format it runs on
+    # the dominant kernel: the grouped 2-bit conv on FP4 matrix cores (int8
+    # with PALQ_CONV_FP4=0); its peak is that of the format it runs on
     dom = DOMINANT if DOMINANT in kern else "conv_tile_kernel[int8]"
     D = kern[dom]
     peak = FP4_MFMA_PEAK_TFLOPS if dom == DOMINANT else INT8_MFMA_PEAK_TOPS
     launch_ms = D["ms"] / D["launches"]
     ops_per_launch = D["ops"] / D["launches"]
     achieved = ops_per_launch / (launch_ms / 1e3) / 1e12
-    traffic = measured_traffic() if dom == DOMINANT else None
+    traffic = measured_traffic() if (dom == DOMINANT and workload == "resnet18_g4_b2") else None
+    rp = rocprof_avg_us(workload, dom)
     res = {
-        "metric": METRIC,
+        "metric": metric,
         "value": img_s,
         "unit": "images/s",
         "n_gpus": 1,
@@ -413,9 +467,11 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "fp4+int8" if dom == DOMINANT else "int8",
-        "data": "synthetic (seeded uniform codes and random fp32 images, random weights)",
-        "config": {"workload": "resnet18_palq_G4_b2_224_fwd", "global_batch": n, "image": [224, 224, 3],
-                   "groups": 4, "bits": 2, "step": "palq_forward_image (quantize fp32 input + forward)"},
+        "data": "synthetic (seeded random weights and codes, standard-normal fp32 images; "
+                "centred conv biases calibrated by the oracle on images %s)" % calib,
+        "config": {"workload": cfg_name, "global_batch": n, "image": [spec["hw"], spec["hw"], 3],
+                   "groups": spec["groups"], "bits": spec["bits"], "variant": "centred",
+                   "step": "palq_forward_image (quantize fp32 input + forward)"},
         "effective_tops": tops,
         "int_ops_per_step": total_ops,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak,
@@ -423,14 +479,43 @@ def main():
                      "kernel": dom, "launches_per_step": D["launches"],
                      "avg_launch_us": launch_ms * 1e3, "int_ops_per_launch": ops_per_launch,
                      "algorithmic_bytes_per_launch": D["bytes"] / D["launches"],
+                     "avg_launch_us_rocprof": rp,
+                     "frac_rocprof": (ops_per_launch / (rp * 1e-6) / 1e12 / peak) if rp else None,
+                     "timing": "avg_launch_us: HIP events on the library stream in this run; "
+                               "avg_launch_us_rocprof: the committed rocprofv3 kernel trace of this "
+                               "workload (null once the kernel source has changed)",
                      "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"},
         "kernels": {k: dict(v, avg_launch_us=v["ms"] * 1e3 / v["launches"]) for k, v in kern.items()},
         "timing_pass_ms_per_step": wall_t * 1e3 / args.steps,
         "layers": per_layer,
+        "distinct_logits": distinct,
     }
+    if not args.no_histograms:
+        res["code_histograms"] = code_histograms(ctx, spec, xd, l, u)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(spec, x_f32, l, u, args.cpu_seconds)
-    print(json.dumps(res))
+    print(json.dumps(res), flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1 "
+                                   "(a batch-parallel split over GPUs is described in the design notes)"}))
+        sys.exit(2)
+    if args.summarize_profile:
+        summarize_profile(args.summarize_profile, args.workload)
+        return
+    if args.hbm_copy_probe:
+        copy_probe(args.hbm_copy_probe)
+        return
+    if args.table2:
+        table2(args)
+        return
+    if args.workload in NETWORKS:
+        run_network(args, args.workload)
+        return
+    raise SystemExit(f"unknown workload {args.workload}")
 
 
 if __name__ == "__main__":

@@ -318,6 +318,17 @@ palq_status palq_net_tensor(const palq_net *net, int32_t id, palq_act *desc);
  * conv (main and projection) and FC layer (host). */
 int64_t palq_net_ops(const palq_net *net);
 
+/* The kernels a forward pass launches for layer `layer`, as the library's
+ * own selection rules pick them at create time (host string owned by net,
+ * valid until palq_net_destroy): e.g. "conv_tile_kernel[fp4]" or
+ * "quantize_pad4_kernel + stem_pool_kernel"; "" for a layer that an earlier
+ * layer's launch already covers (a max pool fused into the stem) and for
+ * every layer of a validate-only network.  image = 0: palq_forward,
+ * 1: palq_forward_image; layer = -1 names forward_image's quantiser pass
+ * into a buffer of its own ("" when the codes go straight into the stem's
+ * zero-border input).  NULL for a null net, a bad index or image. */
+const char *palq_net_layer_kernels(const palq_net *net, int32_t layer, int32_t image);
+
 /* With PALQ_NET_TIMING: per-layer device time of every forward since the
  * last reset, summed, in milliseconds (host array of n_layers floats), and
  * the number of forwards it covers.  Synchronises the stream. */

@@ -17,7 +17,8 @@ __device__ inline int64_t requant_one(int64_t t, int32_t m, int32_t sh, int qmax
   return q > qmax ? qmax : q;
 }
 
-__global__ void conv_direct_kernel(ConvArgs a, int chunks) {
+__global__ void conv_direct_kernel(ConvArgs a, int chunks, const int32_t *only_if_flag) {
+  if (only_if_flag && *only_if_flag == 0) return;
   const int G = a.in.groups;
   const int64_t rows = (int64_t)a.out.n * a.ho * a.wo * G;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -83,12 +84,12 @@ __global__ void conv_direct_kernel(ConvArgs a, int chunks) {
 
 }  // namespace
 
-hipError_t launch_conv_direct(const ConvArgs &a, hipStream_t s) {
+hipError_t launch_conv_direct(const ConvArgs &a, hipStream_t s, const int32_t *only_if_flag) {
   const int chunks = (a.cout + 31) / 32;
   const int64_t items = (int64_t)a.out.n * a.ho * a.wo * a.in.groups * chunks;
   if (items == 0) return hipSuccess;
   const int64_t grid = (items + 255) / 256;
-  hipLaunchKernelGGL(conv_direct_kernel, dim3((unsigned)grid), dim3(256), 0, s, a, chunks);
+  hipLaunchKernelGGL(conv_direct_kernel, dim3((unsigned)grid), dim3(256), 0, s, a, chunks, only_if_flag);
   return hipGetLastError();
 }
 

@@ -658,12 +658,27 @@ __device__ inline void finish_tile(const ConvArgs &a, const Geo &geo, v16i (&acc
                                  a.res_mult + (int64_t)g * a.cout + ch0);
 }
 
-// Whether a layer needs the general epilogue: the int64 requant fallback
-// (flag written by requant_prep_kernel), the accumulator dump, 3-bit
-// outputs or an identity shortcut of other than 2 bits.  Uniform.
+// The layer's int64-requant flag (written by requant_prep_kernel after its
+// constants): set when some channel's fp64 requant could be inexact.
+__device__ inline bool int64_flag(const ConvArgs &a, const Geo &geo) {
+  return ((const int32_t *)(geo.rq + (int64_t)a.in.groups * a.cout))[0] != 0;
+}
+
+// Whether a layer needs the general epilogue: the int64 requant fallback,
+// the accumulator dump, 3-bit outputs or an identity shortcut of other than
+// 2 bits.  Uniform.
 __device__ inline bool needs_general(const ConvArgs &a, const Geo &geo, int rb) {
-  return ((const int32_t *)(geo.rq + (int64_t)a.in.groups * a.cout))[0] != 0 || a.acc_dump != nullptr ||
-         a.out.bits == 3 || rb < 0;
+  return int64_flag(a, geo) || a.acc_dump != nullptr || a.out.bits == 3 || rb < 0;
+}
+
+// Whether this build of a persistent kernel leaves at once.  a.gated: the
+// launch is the general partner of a tiled launch (which covers every case
+// but the int64 requant), so only the general build runs, and only when the
+// flag is set; otherwise the fast and the general build split by
+// needs_general.
+__device__ inline bool skip_build(const ConvArgs &a, const Geo &geo, int rb, bool gen) {
+  if (a.gated) return !gen || !int64_flag(a, geo);
+  return needs_general(a, geo, rb) != gen;
 }
 
 // Loads of the K loop, the LDS operand reads and the MFMAs of one K-block
@@ -726,7 +741,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
 
   // the launcher may start both builds when it cannot tell which applies:
   // the other one leaves at once (before any barrier)
-  if (needs_general(a, geo, RB) != GEN) return;
+  if (skip_build(a, geo, RB, GEN)) return;
   stage_block<CB>(a, geo, g, lds);
   const int first = blockIdx.x * kNW + wave;
   const int tstride = gridDim.x * kNW;
@@ -873,7 +888,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo
 
   // the launcher may start both builds when it cannot tell which applies:
   // the other one leaves at once (before any barrier)
-  if (needs_general(a, geo, RB) != GEN) return;
+  if (skip_build(a, geo, RB, GEN)) return;
   stage_block<CB>(a, geo, g, lds);
   const int first = blockIdx.x * kNW + wave;
   const int tstride = gridDim.x * kNW;
@@ -1068,9 +1083,10 @@ __device__ __forceinline__ void tile_next(TileIt &it, int npt, int ncombo, int n
 // the accumulator fp32 (t / 4, exact: the launcher takes only layers whose
 // accumulator bound is below 2^23, so every partial sum is a multiple of
 // 1/4 below 2^21).
-// KPI: K-blocks per ring stage (one wait and barrier per stage).
+// DUMP: also write the int32 accumulators to a.acc_dump (destination channel
+// order; the FP4 accumulator times 4, the int8 one without its operand scale).
 template <int CB, int PB, int WN, int WM, int RB, bool STEM = false, int kStages = PALQ_TILE_STAGES,
-          bool FP4 = false, int KPI = 1>
+          bool FP4 = false, bool DUMP = false>
 __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, Geo geo, int npt,
                                                                                       int ncb, int nch) {
   constexpr int B = 2;
@@ -1081,7 +1097,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   constexpr int WST = TN / 32 * SLAB;  // weight bytes of one K-block
   constexpr int XST = TM * BLK;       // activation bytes of one K-block
   constexpr int SSB = WST + XST;      // one K-block of a ring stage
-  constexpr int SST = KPI * SSB;      // one ring stage
+  constexpr int SST = SSB;            // one ring stage
   constexpr int WP = WST / 16;        // 16-byte weight pieces of a K-block
   constexpr int WLD = FP4 && WP < NT ? 1 : WP / NT;  // weight loads per loading thread and K-block
   constexpr int XP = XST / 16;          // 16-byte activation pieces of a K-block
@@ -1108,7 +1124,9 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   static_assert(CB == 2 && (PB == 2 || (FP4 && PB == 4)), "compute() below is written out for 2 x 2 (FP4: 2 x 4) blocks");
   using Raw = RawT<B, false>;
 
-  if (needs_general(a, geo, RB)) return;
+  // the launcher takes 2-bit outputs and 2-bit (or no) shortcuts only; a
+  // layer whose fp64 requant could be inexact runs on the general partner
+  if (int64_flag(a, geo) || a.out.bits != 2 || RB < 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
   const int wn = wave / WM, wm = wave % WM;
@@ -1214,9 +1232,9 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   // the last tile read out-of-range offsets (zeros), so every call issues
   // the same loads.
   const auto rres = make_rsrc(a.res.data, a.res.data ? (int64_t)a.res.n * a.res.h * a.res.w * a.res.pixel : 0);
-  auto fetch = [&](int st, int h) __attribute__((always_inline)) {
+  auto fetch = [&](int st) __attribute__((always_inline)) {
     const bool live = f_tile < t_end;
-    uint8_t *ws = lds + st * SST + h * SSB;
+    uint8_t *ws = lds + st * SST;
     if constexpr (RB == 2) {
       if (f_kb == 0) {  // the tile's shortcut codes, RPT 16-byte pieces per thread
         const int pt = f_it.pt;
@@ -1329,6 +1347,28 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
       rw[0][1][0] = r10.x; rw[0][1][1] = r10.y;
       rw[1][1][0] = r11.x; rw[1][1][1] = r11.y;
     }
+    if constexpr (DUMP) {
+      // accumulators of pixel mbase + 32 pb + l32, channels kc + 8 qi + 4 half + e
+      const int64_t outC = (int64_t)G * a.cout, mbase = (int64_t)pt * TM + wm * PB * 32;
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb) {
+          const int64_t mp = mbase + pb * 32 + l32;
+          if (mp >= geo.M) continue;
+          int32_t *dst = a.acc_dump + mp * outC + (int64_t)gd * a.cout + cbk * TN + wn * CB * 32 + cb * 32 + 4 * half;
+#pragma unroll
+          for (int qi = 0; qi < 4; ++qi) {
+            v4i dv;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              if constexpr (FP4) dv[e] = (int)(acc[cb][pb][4 * qi + e] * 4.0f);  // exact: |4 acc| < 2^23
+              else dv[e] = (int)acc[cb][pb][4 * qi + e] >> (geo.scale == 16 ? 4 : 0);
+            }
+            *(v4i *)(dst + 8 * qi) = dv;
+          }
+        }
+    }
     const int rec = (c_it.combo == combo0 ? 0 : TN) + wn * CB * 32;  // first record of this wave's channels
     epilogue_fast_bo<2, CB, PB, RB, typename std::remove_reference<decltype(acc[0][0])>::type, FP4>(
         a, geo, acc, rw, (int64_t)pt * TM + wm * PB * 32, g, gd, cbk * TN + wn * CB * 32, l32, half, rq_area + rec,
@@ -1346,8 +1386,8 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   struct OpsS { v4i x0a, x0b, x1a, x1b, a00, a01, a10, a11; };  // stem: x[pb] words 0-3 / 4-7
   struct OpsF { uint2 x[PB]; v4i a0, a1; };                     // FP4: x[pb], a[cb]
   using Ops = typename std::conditional<STEM, OpsS, typename std::conditional<FP4, OpsF, OpsG>::type>::type;
-  auto read_ops = [&](int stage, int h, Ops &o) __attribute__((always_inline)) {
-    const uint32_t xa = xaddr0 + stage * SST + h * SSB, aa = aaddr0 + stage * SST + h * SSB;
+  auto read_ops = [&](int stage, Ops &o) __attribute__((always_inline)) {
+    const uint32_t xa = xaddr0 + stage * SST, aa = aaddr0 + stage * SST;
     if constexpr (STEM) {
       asm volatile(
           "ds_read_b128 %0, %8\n\t"
@@ -1447,35 +1487,28 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
     }
     }
   };
-  // Stage of K-blocks gk .. gk + KPI - 1: wait until this wave's loads of
-  // it have landed, barrier (everyone's have, and everyone is done with the
-  // previous stage, which the next fetch reuses), fetch the stage kStages - 1
-  // ahead, then per K-block read the operands, run the MFMAs, and finish the
-  // tile after its last K-block.  A tile's shortcut codes (two buffers) are
-  // safe while kb_total >= kStages * KPI.
-  for (int st = 0; st < kStages - 1; ++st)
-#pragma unroll
-    for (int h = 0; h < KPI; ++h) fetch(st, h);
-  for (int gk = 0; gk < total; gk += KPI) {
-    const int st = (gk / KPI) % kStages;
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kStages - 2) * KPI * LPK));
+  // K-block gk: wait until this wave's loads of it have landed, barrier
+  // (everyone's have, and everyone is done with the previous stage, which
+  // the next fetch reuses), fetch the K-block kStages - 1 ahead, then read
+  // the operands, run the MFMAs, and finish the tile after its last
+  // K-block.  A tile's shortcut codes (two buffers) are safe while
+  // kb_total >= kStages.
+  for (int st = 0; st < kStages - 1; ++st) fetch(st);
+  for (int gk = 0; gk < total; ++gk) {
+    const int st = gk % kStages;
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kStages - 2) * LPK));
     ring_barrier();
-#pragma unroll
-    for (int h = 0; h < KPI; ++h) fetch((st + kStages - 1) % kStages, h);
-#pragma unroll
-    for (int h = 0; h < KPI; ++h) {
-      if (KPI > 1 && gk + h >= total) break;  // uniform: the run's last stage may be half used
-      if (c_kb == 0) tile_start();
-      Ops o;
-      read_ops(st, h, o);
-      __builtin_amdgcn_sched_barrier(0);
-      mfmas(o);
-      if (++c_kb == KB) {
-        tile_end();
-        c_kb = 0;
-        ++c_tile;
-        tile_next(c_it, npt, ncb * G, nch);
-      }
+    fetch((st + kStages - 1) % kStages);
+    if (c_kb == 0) tile_start();
+    Ops o;
+    read_ops(st, o);
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas(o);
+    if (++c_kb == KB) {
+      tile_end();
+      c_kb = 0;
+      ++c_tile;
+      tile_next(c_it, npt, ncb * G, nch);
     }
   }
 }
@@ -1801,20 +1834,6 @@ int pick_cb(const ConvArgs &a, const Geo &geo) {
   return 0;
 }
 
-// Optional tile override for tuning sweeps: PALQ_CONV_TILE="cb,pb".
-void tile_override(const ConvArgs &a, const Geo &geo, int &cb, int &pb) {
-  static int ocb = -1, opb = -1;
-  if (ocb < 0) {
-    ocb = opb = 0;
-    if (const char *e = getenv("PALQ_CONV_TILE")) {
-      int x = 0, y = 0;
-      if (sscanf(e, "%d,%d", &x, &y) == 2) { ocb = x; opb = y; }
-    }
-  }
-  if (ocb == 1 || (ocb == 2 && a.cout % 64 == 0 && lds_bytes(geo, 2) <= kLdsBudget)) cb = ocb;
-  if (opb == 1 || opb == 2) pb = opb;
-}
-
 template <typename K>
 hipError_t launch_persistent(K kern, const ConvArgs &a, const Geo &geo, int cb, int pb, hipStream_t s) {
   const size_t lds = lds_bytes(geo, cb);
@@ -1862,8 +1881,8 @@ hipError_t launch_stem(const ConvArgs &a, const Geo &geo, int epi, hipStream_t s
 
 template <int B>
 hipError_t dispatch_bits(const ConvArgs &a, const Geo &geo, int cb, int pb, int epi, hipStream_t s) {
-  if (cb == 2) return pb == 2 ? launch_grouped<B, 2, 2>(a, geo, epi, s) : launch_grouped<B, 2, 1>(a, geo, epi, s);
-  return pb == 2 ? launch_grouped<B, 1, 2>(a, geo, epi, s) : launch_grouped<B, 1, 1>(a, geo, epi, s);
+  (void)pb;  // one 32-pixel block per wave
+  return cb == 2 ? launch_grouped<B, 2, 1>(a, geo, epi, s) : launch_grouped<B, 1, 1>(a, geo, epi, s);
 }
 
 // Largest magnitude of a code of the given width and sign.
@@ -1953,7 +1972,7 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
 bool conv_mfma_pads_input(const ConvArgs &a) { return is_stem(a) && a.pad > 0; }
 
 int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr) {
-  if (a.acc_dump || a.out.bits == 3 || (a.res.data && a.res.bits != 2)) return 1;
+  if (a.out.bits == 3 || (a.res.data && a.res.bits != 2)) return 1;
   int32_t flag = 0;
   const RqConst *rq = (const RqConst *)thr;
   if (hipMemcpy(&flag, rq + (int64_t)a.in.groups * a.cout, sizeof(flag), hipMemcpyDeviceToHost) != hipSuccess)
@@ -1980,30 +1999,14 @@ int cu_count() {
   return cus;
 }
 
-// Pixel tile of the tiled kernel for 128-channel blocks, for tuning
-// (PALQ_TILE_TM = 64, 128 or 256; 0 = the build's default).
-int tile_tm() {
-  static int v = -1;
-  if (v < 0) {
-    v = 0;
-    if (const char *e = getenv("PALQ_TILE_TM")) v = atoi(e);
-    if (v != 64 && v != 128 && v != 256) v = 0;
-  }
-  return v;
-}
-
 // Persistent workgroups of a tiled-kernel build: as many as are resident at
 // once (registers and LDS decide; the variants with and without a shortcut
-// need about the same), a multiple of 8.  PALQ_TILE_WGS overrides.
+// need about the same), a multiple of 8.
 int tile_slots(const void *kern, int threads) {
-  if (const char *e = getenv("PALQ_TILE_WGS")) {
-    const int v = atoi(e);
-    if (v >= 8 && v <= 65536) return v / 8 * 8;
-  }
-  // cached per kernel and device (a handful of builds)
+  // cached per kernel and device (a few dozen builds)
   static std::mutex mu;
-  static const void *keys[32];
-  static int devs[32], vals[32], used = 0;
+  static const void *keys[64];
+  static int devs[64], vals[64], used = 0;
   int dev = 0;
   hipGetDevice(&dev);
   std::lock_guard<std::mutex> lock(mu);
@@ -2013,7 +2016,7 @@ int tile_slots(const void *kern, int threads) {
   hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kern, threads, 0) != hipSuccess || per < 1) per = 1;
   const int v = std::max(8, cus * per / 8 * 8);
-  if (used < 32) {
+  if (used < 64) {
     keys[used] = kern;
     devs[used] = dev;
     vals[used] = v;
@@ -2022,19 +2025,13 @@ int tile_slots(const void *kern, int threads) {
   return v;
 }
 
-// The tiled kernel takes 2-bit grouped layers with 64-channel blocks whose
-// epilogue is the fast one, with 2-bit outputs (PALQ_CONV_KERNEL=persistent
-// turns it off).
+// The tiled kernel takes 2-bit grouped layers with 64-channel blocks and
+// 2-bit outputs (and 2-bit or no identity shortcut); a layer whose requant
+// needs the int64 path runs on the general partner launched beside it.
 bool tile_kernel_applies(const ConvArgs &a) {
-  static int off = -1;
-  if (off < 0) {
-    const char *e = getenv("PALQ_CONV_KERNEL");
-    off = (e && strcmp(e, "persistent") == 0) ? 1 : 0;
-  }
   const int64_t wbytes = (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64;
-  return !off && !is_stem(a) && a.in.bits == 2 && a.w_bits == 2 && a.cout % 64 == 0 && !a.acc_dump &&
-         wbytes < ((int64_t)1 << 30) && make_geo(a).kb_total >= kStages && a.out.bits == 2 &&
-         (!a.res.data || a.res.bits == 2);
+  return !is_stem(a) && a.in.bits == 2 && a.w_bits == 2 && a.cout % 64 == 0 && wbytes < ((int64_t)1 << 30) &&
+         make_geo(a).kb_total >= kStages && a.out.bits == 2 && (!a.res.data || a.res.bits == 2);
 }
 
 // FP4 matrix cores for a tiled-kernel layer whose accumulator bound is below
@@ -2045,54 +2042,82 @@ bool fp4_applies(const ConvArgs &a) {
 }
 
 // The stem on the tiled kernel: explicit zero border (pad 0), 128-channel
-// blocks, no shortcut, fast epilogue.
+// blocks, no shortcut, no accumulator dump.
 bool stem_tile_applies(const ConvArgs &a) {
-  static int off = -1;
-  if (off < 0) {
-    const char *e = getenv("PALQ_CONV_KERNEL");
-    off = (e && strcmp(e, "persistent") == 0) ? 1 : 0;
-  }
-  return !off && is_stem(a) && a.pad == 0 && a.cout % 128 == 0 && !a.res.data && !a.acc_dump && a.out.bits == 2 &&
+  return is_stem(a) && a.pad == 0 && a.cout % 128 == 0 && !a.res.data && !a.acc_dump && a.out.bits == 2 &&
          (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64 < ((int64_t)1 << 30);
 }
 
-template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES, bool FP4 = false, int KPI = 1>
+// Tiled-kernel builds (tile shape per wave CB x PB blocks of 32 x 32, WN x WM
+// waves): the 8-bit stem; 2-bit layers on FP4 with 64-channel blocks (1 x 4
+// waves, 256-pixel tiles), 128-channel blocks (2 x 2 waves, 128 pixels) or
+// 128-channel blocks with 2 x 4 blocks per wave (256 pixels); 2-bit layers on
+// int8 with 64- or 128-channel blocks (256 pixels).
+enum TileBuild { kTileNone = 0, kTileStem, kTileFp4C64, kTileFp4C128, kTileFp4C128P4, kTileI8C64, kTileI8C128 };
+
+// 2 x 4 blocks per wave (256-pixel tiles) for 128-channel FP4 layers where
+// the bigger tiles leave every CU at least one and do not lengthen the
+// busiest CU's share: 2 ceil(T4 / CUs) <= ceil(T2 / CUs) tile units.
+bool fp4_pb4_pays(const ConvArgs &a, const Geo &geo) {
+  const int64_t m = geo.M, tiles_per_px = (int64_t)(a.cout / 128) * a.in.groups;
+  const int64_t t2 = (m + 127) / 128 * tiles_per_px, t4 = (m + 255) / 256 * tiles_per_px;
+  const int64_t cus = cu_count();
+  return t4 >= cus && 2 * ((t4 + cus - 1) / cus) <= (t2 + cus - 1) / cus;
+}
+
+// The one selection rule of the conv launches: which tiled build (if any)
+// takes the layer given the epilogue build epi (0 fast, 1 general, -1 not
+// known: a tiled build is then launched with its general partner, which
+// runs only if the layer's int64-requant flag is set).
+struct ConvChoice {
+  int tile;  // TileBuild
+  int cb;    // channel blocks of the persistent build (0: it does not fit LDS)
+};
+
+ConvChoice conv_choice(const ConvArgs &a, const Geo &geo, int epi) {
+  ConvChoice c{kTileNone, pick_cb(a, geo)};
+  if (a.out.bits == 3 || epi == 1) return c;
+  if (stem_tile_applies(a)) c.tile = kTileStem;
+  else if (fp4_applies(a)) c.tile = a.cout % 128 ? kTileFp4C64 : fp4_pb4_pays(a, geo) ? kTileFp4C128P4 : kTileFp4C128;
+  else if (tile_kernel_applies(a)) c.tile = a.cout % 128 ? kTileI8C64 : kTileI8C128;
+  return c;
+}
+
+template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES, bool FP4 = false>
 hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
-  if (geo.kb_total < S * KPI) return hipErrorInvalidValue;
+  if (geo.kb_total < S) return hipErrorInvalidValue;
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
   const int npt = (int)((geo.M + TM - 1) / TM);
   const int ncb = a.cout / TN;
   const int64_t T = (int64_t)npt * ncb * a.in.groups;
   if (T <= 0 || T > 0x7fffffff) return hipErrorInvalidValue;
-  const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S, FP4, KPI>, WN * WM * 64);
+  const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S, FP4>, WN * WM * 64);
   // Pixel chunks (tile_at): 32 (four per XCD), so that an XCD fetches each
   // input line once for all groups while a chunk's lines still fit its L2,
   // unless the filter is the larger read (every XCD then reads all of it):
   // about 7 W extra against (G - 1) X saved.
   const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * (FP4 ? 32 : 64);
   const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
-  static int nch_env = -1;  // PALQ_TILE_NCH: chunk count when chunked (tuning)
-  if (nch_env < 0) {
-    const char *e = getenv("PALQ_TILE_NCH");
-    nch_env = e && atoi(e) >= 1 && atoi(e) <= 256 ? atoi(e) : 32;
-  }
-  const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(nch_env, npt) : 1;
+  const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(32, npt) : 1;
   // P workgroups per XCD: all resident slots, no more than the XCD's
   // tiles, and runs of at most npt / nch tiles (two (chunk, combo) segments)
   const int64_t Tx = (T + 7) / 8;
   const int maxlen = npt / nch;
   int64_t P = std::max<int64_t>(1, std::min<int64_t>(slots / 8, Tx));
   if ((Tx + P - 1) / P > maxlen) P = (Tx + maxlen - 1) / maxlen;
-  const int nwg = (int)(8 * P);
+  const dim3 grid((unsigned)(8 * P)), block(WN * WM * 64);
   if constexpr (STEM)
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, true, S>), dim3((unsigned)nwg), dim3(WN * WM * 64), 0, s,
-                       a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, true, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+  else if (!a.res.data && !a.acc_dump)
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, FP4>), grid, block, 0, s, a, geo, npt, ncb, nch);
+  else if (!a.acc_dump)
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else if (!a.res.data)
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, FP4, KPI>), dim3((unsigned)nwg), dim3(WN * WM * 64),
-                       0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, FP4, true>), grid, block, 0, s, a, geo, npt, ncb,
+                       nch);
   else
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4, KPI>), dim3((unsigned)nwg), dim3(WN * WM * 64),
-                       0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4, true>), grid, block, 0, s, a, geo, npt, ncb,
+                       nch);
   return hipGetLastError();
 }
 
@@ -2102,12 +2127,7 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
 // stem's output shape.  The caller must know the fast epilogue applies
 // (conv_mfma_epilogue == 0): the kernel has no general build.
 bool stem_pool_applies(const ConvArgs &a, const ActView &po, int k, int stride, int pad) {
-  static int off = -1;  // PALQ_STEM_POOL=0: keep the two launches (for comparisons)
-  if (off < 0) {
-    const char *e = getenv("PALQ_STEM_POOL");
-    off = (e && strcmp(e, "0") == 0) ? 1 : 0;
-  }
-  if (off || !stem_tile_applies(a) || a.in.groups != 1 || a.wo < 1 || a.wo > 127 || a.ho < 1) return false;
+  if (!stem_tile_applies(a) || a.in.groups != 1 || a.wo < 1 || a.wo > 127 || a.ho < 1) return false;
   if (k != 3 || stride != 2 || pad != 1) return false;
   if (po.n != a.out.n || po.h != (a.ho + 1) / 2 || po.w != (a.wo + 1) / 2 || po.groups != a.out.groups ||
       po.cpg != a.out.cpg || po.bits != 2 || po.pixel != a.out.pixel || po.row != a.out.row)
@@ -2137,83 +2157,50 @@ hipError_t launch_stem_pool(const ConvArgs &a, const uint8_t *wp, const int32_t 
   return hipGetLastError();
 }
 
-hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, int epi, hipStream_t s) {
+const char *conv_kernel_label(const ConvArgs &a, int epi) {
+  const Geo geo = make_geo(a);
+  switch (conv_choice(a, geo, epi).tile) {
+    case kTileStem: return "conv_tile_kernel[stem]";
+    case kTileFp4C64: case kTileFp4C128: case kTileFp4C128P4: return "conv_tile_kernel[fp4]";
+    case kTileI8C64: case kTileI8C128: return "conv_tile_kernel[int8]";
+    default: return is_stem(a) ? "conv_stem_kernel" : "conv_grouped_kernel";
+  }
+}
+
+hipError_t launch_conv_mfma(const ConvArgs &a_in, const uint8_t *wp, const int32_t *thr, int epi, hipStream_t s) {
+  ConvArgs a = a_in;
+  a.gated = 0;
   Geo geo = make_geo(a);
   if (geo.M == 0) return hipSuccess;
   geo.wp = wp;
   geo.rq = (const RqConst *)thr;
-  int cb = pick_cb(a, geo);
-  if (cb == 0 && epi != 0) return hipErrorNotSupported;  // no general build for this layer
-  int pb = 1;
-  if (cb > 0) tile_override(a, geo, cb, pb);
-  if (a.acc_dump || a.out.bits == 3) epi = 1;
-  if (epi != 1 && stem_tile_applies(a)) {
-    hipError_t e = launch_tile<2, 2, 2, 2, true, PALQ_STEM_STAGES>(a, geo, s);
-    if (e != hipSuccess || epi == 0) return e;
-    return launch_stem<2, 1>(a, geo, 1, s);  // unknown: the general build decides on the device
+  const ConvChoice c = conv_choice(a, geo, epi);
+  if (c.cb == 0 && c.tile == kTileNone) return hipErrorNotSupported;  // no build for this layer
+  hipError_t e = hipSuccess;
+  const int nch = a.in.groups * a.cout;
+  Geo g4 = geo;  // FP4 slabs and constants follow the int8 ones
+  g4.wp = wp + (size_t)nch * geo.kb_total * 64;
+  g4.rq = geo.rq + nch + 1;
+  constexpr int S4 = PALQ_TILE_STAGES;
+  switch (c.tile) {
+    case kTileStem: e = launch_tile<2, 2, 2, 2, true, PALQ_STEM_STAGES>(a, geo, s); break;
+    case kTileFp4C64: e = launch_tile<2, 2, 1, 4, false, S4, true>(a, g4, s); break;
+    case kTileFp4C128: e = launch_tile<2, 2, 2, 2, false, S4, true>(a, g4, s); break;
+    case kTileFp4C128P4: e = launch_tile<2, 4, 2, 2, false, S4, true>(a, g4, s); break;
+    case kTileI8C64: e = launch_tile<2, 2, 1, 4>(a, geo, s); break;
+    case kTileI8C128: e = launch_tile<2, 2, 2, 4>(a, geo, s); break;
+    default: break;
   }
-  if (epi != 1 && fp4_applies(a)) {
-    const int nch = a.in.groups * a.cout;
-    Geo g4 = geo;
-    g4.wp = wp + (size_t)nch * geo.kb_total * 64;
-    g4.rq = geo.rq + nch + 1;
-    // pixel tile: 128 (256 / 64 for tuning via PALQ_TILE_TM); 64-channel
-    // layers: TM = 256 or (PALQ_TILE_TM64=128) 128
-    static int tm64 = -1;
-    if (tm64 < 0) {
-      const char *e = getenv("PALQ_TILE_TM64");
-      tm64 = e && atoi(e) == 128 ? 128 : 256;
-    }
-    const int tm = tile_tm() ? tile_tm() : 128;
-    // 2 x 4 blocks per wave (128-channel blocks, 256-pixel tiles) where the
-    // bigger tiles leave every CU at least one and do not lengthen the
-    // busiest CU's share: 2 ceil(T4 / CUs) <= ceil(T2 / CUs) tile units.
-    // PALQ_TILE_PB = 2 or 4 forces one for tuning.
-    static int pb_env = -1;
-    if (pb_env < 0) {
-      const char *e = getenv("PALQ_TILE_PB");
-      pb_env = e ? atoi(e) : 0;
-    }
-    bool pb4 = pb_env == 4;
-    if (pb_env != 2 && pb_env != 4 && a.cout % 128 == 0) {
-      const int64_t m = geo.M, tiles_per_px = (int64_t)(a.cout / 128) * a.in.groups;
-      const int64_t t2 = (m + 127) / 128 * tiles_per_px, t4 = (m + 255) / 256 * tiles_per_px;
-      const int64_t cus = cu_count();
-      pb4 = t4 >= cus && 2 * ((t4 + cus - 1) / cus) <= (t2 + cus - 1) / cus;
-    }
-    static int kpi = -1;  // K-blocks per ring stage (PALQ_TILE_KPI=2 for tuning)
-    if (kpi < 0) {
-      const char *e = getenv("PALQ_TILE_KPI");
-      kpi = e && atoi(e) == 2 ? 2 : 1;
-    }
-    constexpr int S4 = PALQ_TILE_STAGES;
-    hipError_t e;
-    if (pb4 && a.cout % 128 == 0)
-      e = launch_tile<2, 4, 2, 2, false, S4, true>(a, g4, s);
-    else if (kpi == 2 && geo.kb_total >= S4 * 2)
-      e = a.cout % 128 != 0 ? launch_tile<2, 2, 1, 4, false, S4, true, 2>(a, g4, s)
-                            : launch_tile<2, 2, 2, 2, false, S4, true, 2>(a, g4, s);
-    else
-      e = a.cout % 128 != 0 ? (tm64 == 128 ? launch_tile<2, 2, 1, 2, false, S4, true>(a, g4, s)
-                                           : launch_tile<2, 2, 1, 4, false, S4, true>(a, g4, s))
-          : tm == 64  ? launch_tile<2, 2, 2, 1, false, S4, true>(a, g4, s)
-          : tm == 128 ? launch_tile<2, 2, 2, 2, false, S4, true>(a, g4, s)
-                      : launch_tile<2, 2, 2, 4, false, S4, true>(a, g4, s);
-    if (e != hipSuccess || epi == 0) return e;
-    return dispatch_bits<2>(a, geo, cb, pb, 1, s);  // unknown: the general build decides on the device
+  if (e != hipSuccess) return e;
+  if (c.tile != kTileNone) {
+    if (epi == 0) return hipSuccess;
+    // epi unknown: the general partner, which runs only if the flag is set
+    a.gated = 1;
+    if (c.cb == 0) return launch_conv_direct(a, s, (const int32_t *)(geo.rq + nch));
+    epi = 1;
   }
-  if (epi != 1 && tile_kernel_applies(a)) {
-    hipError_t e = a.cout % 128 != 0 ? launch_tile<2, 2, 1, 4>(a, geo, s)
-                   : tile_tm() == 128 || tile_tm() == 64 ? launch_tile<2, 2, 2, 2>(a, geo, s)
-                                      : launch_tile<2, 2, 2, 4>(a, geo, s);
-    if (e != hipSuccess || epi == 0) return e;
-    return dispatch_bits<2>(a, geo, cb, pb, 1, s);  // unknown: the general build decides on the device
-  }
-  if (cb == 0) return hipErrorNotSupported;  // neither tiled build took the layer
-  if (is_stem(a)) {
-    if (cb == 2) return pb == 2 ? launch_stem<2, 2>(a, geo, epi, s) : launch_stem<2, 1>(a, geo, epi, s);
-    return pb == 2 ? launch_stem<1, 2>(a, geo, epi, s) : launch_stem<1, 1>(a, geo, epi, s);
-  }
+  const int cb = c.cb, pb = 1;
+  if (is_stem(a)) return cb == 2 ? launch_stem<2, 1>(a, geo, epi, s) : launch_stem<1, 1>(a, geo, epi, s);
   switch (a.in.bits) {
     case 2: return dispatch_bits<2>(a, geo, cb, pb, epi, s);
     case 3: return dispatch_bits<3>(a, geo, cb, pb, epi, s);

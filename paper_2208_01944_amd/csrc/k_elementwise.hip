@@ -699,13 +699,23 @@ hipError_t launch_minmax(const float *x, int64_t count, float *range, hipStream_
   return hipGetLastError();
 }
 
+// Four 3-channel 8-bit pixels per thread with 16-byte loads and stores.
+bool quantize_by_pixels(const float *x, const ActView &out) {
+  const int64_t rows = (int64_t)out.n * out.h * out.w * out.groups;
+  return out.bits == 8 && out.cpg == 3 && out.groups == 1 && out.row == 4 && rows % 4 == 0 &&
+         (((uintptr_t)x | (uintptr_t)out.data) & 15u) == 0;
+}
+
+const char *quantize_label(const float *x, const ActView &out) {
+  return quantize_by_pixels(x, out) ? "quantize_px3_kernel" : "quantize_kernel";
+}
+
 hipError_t launch_quantize(const float *x, float l, float u, const float *range, const ActView &out,
                            hipStream_t s) {
   const int64_t rows = (int64_t)out.n * out.h * out.w * out.groups;
   const int units = out.bits == 3 ? (out.cpg + 31) / 32 : (int)(out.row / 4);
   if (rows == 0) return hipSuccess;
-  if (out.bits == 8 && out.cpg == 3 && out.groups == 1 && out.row == 4 && rows % 4 == 0 &&
-      (((uintptr_t)x | (uintptr_t)out.data) & 15u) == 0) {
+  if (quantize_by_pixels(x, out)) {
     hipLaunchKernelGGL(quantize_px3_kernel, dim3(grid_for(rows / 4)), dim3(kBlock), 0, s, x, l, u,
                        (const uint32_t *)range, out, rows / 4);
     return hipGetLastError();
@@ -715,17 +725,22 @@ hipError_t launch_quantize(const float *x, float l, float u, const float *range,
   return hipGetLastError();
 }
 
+// Four input pixels per thread with 16-byte loads (rows of up to 256 + 2 pad
+// pixels, 4-byte output pixels, 16-byte aligned input).
+bool quantize_pad_vector(const float *x, int in_w, int pad, const ActView &out) {
+  return in_w % 4 == 0 && in_w / 4 + 2 * pad <= 64 && out.pixel == 4 && ((uintptr_t)x & 15u) == 0;
+}
+
+const char *quantize_pad_label(const float *x, int in_w, int pad, const ActView &out) {
+  return quantize_pad_vector(x, in_w, pad, out) ? "quantize_pad4_kernel" : "quantize_pad_kernel";
+}
+
 hipError_t launch_quantize_pad(const float *x, float l, float u, int in_h, int in_w, int pad, const ActView &out,
                                hipStream_t s) {
   const int64_t rows = (int64_t)out.n * out.h;
   if (rows == 0 || out.w == 0) return hipSuccess;
   if (rows >= 0x7fffffff) return hipErrorInvalidValue;
-  static int v4 = -1;  // PALQ_QPAD4=0: the one-pixel-per-thread kernel (tuning)
-  if (v4 < 0) {
-    const char *e = getenv("PALQ_QPAD4");
-    v4 = e && atoi(e) == 0 ? 0 : 1;
-  }
-  if (v4 && in_w % 4 == 0 && in_w / 4 + 2 * pad <= 64 && out.pixel == 4 && ((uintptr_t)x & 15u) == 0) {
+  if (quantize_pad_vector(x, in_w, pad, out)) {
     hipLaunchKernelGGL(quantize_pad4_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, x, l, u, in_h, in_w,
                        pad, out, (int)rows);
     return hipGetLastError();
@@ -759,14 +774,23 @@ hipError_t launch_channel_shuffle(const ActView &in, const ActView &out, hipStre
   return hipGetLastError();
 }
 
+// 2-bit rows of a multiple of 16 bytes: 64 codes per thread (SWAR max).
+bool maxpool_vector(const ActView &in, const ActView &out) {
+  return in.bits == 2 && out.row % 16 == 0 && out.h <= 65535 && out.n <= 65535 &&
+         (((uintptr_t)in.data | (uintptr_t)out.data) & 15u) == 0 &&
+         (int64_t)out.w * out.groups * (out.row / 16) < ((int64_t)1 << 30);
+}
+
+const char *maxpool_label(const ActView &in, const ActView &out) {
+  return maxpool_vector(in, out) ? "maxpool2_kernel" : "maxpool_kernel";
+}
+
 hipError_t launch_maxpool(const ActView &in, int k, int stride, int pad, const ActView &out,
                           hipStream_t s) {
   const int64_t rows = (int64_t)out.n * out.h * out.w * out.groups;
   const int units = out.bits == 3 ? (out.cpg + 31) / 32 : (int)(out.row / 4);
   if (rows == 0) return hipSuccess;
-  if (in.bits == 2 && out.row % 16 == 0 && out.h <= 65535 && out.n <= 65535 &&
-      (((uintptr_t)in.data | (uintptr_t)out.data) & 15u) == 0 &&
-      (int64_t)out.w * out.groups * (out.row / 16) < ((int64_t)1 << 30)) {
+  if (maxpool_vector(in, out)) {
     const int64_t per_row = (int64_t)out.w * out.groups * (out.row / 16);
     dim3 grid((unsigned)((per_row + kBlock - 1) / kBlock), (unsigned)out.h, (unsigned)out.n);
     hipLaunchKernelGGL(maxpool2_kernel, grid, dim3(kBlock), 0, s, in, k, stride, pad, out);
@@ -777,11 +801,17 @@ hipError_t launch_maxpool(const ActView &in, int k, int stride, int pad, const A
   return hipGetLastError();
 }
 
+bool pad_by_rows(const ActView &out) {
+  return (int64_t)out.n * out.h < 0x7fffffff && (int64_t)out.w * out.pixel < 0x7fffffff;
+}
+
+const char *pad_pixels_label(const ActView &out) { return pad_by_rows(out) ? "pad_rows_kernel" : "pad_pixels_kernel"; }
+
 hipError_t launch_pad_pixels(const ActView &in, int pad, const ActView &out, hipStream_t s) {
   const int64_t words = (int64_t)out.n * out.h * out.w * (out.pixel / 4);
   if (words == 0) return hipSuccess;
   const int64_t rows = (int64_t)out.n * out.h;
-  if (rows < 0x7fffffff && (int64_t)out.w * out.pixel < 0x7fffffff) {
+  if (pad_by_rows(out)) {
     hipLaunchKernelGGL(pad_rows_kernel, dim3((unsigned)((rows + kPadRows - 1) / kPadRows)), dim3(256), 0, s, in, pad,
                        out, (int)rows);
     return hipGetLastError();
@@ -798,22 +828,37 @@ bool avgsum_makes_fc_planes(const ActView &in) {
 
 int fc_planes(int64_t xmax) { return xmax >= 0 && xmax <= 127 ? 1 : xmax >= 0 && xmax <= 32639 ? 2 : 4; }
 
+// 0: one thread per channel; 1: byte-lane sums of 2-bit rows (16 codes per
+// thread); 2: the same with one workgroup per image row block (which can
+// also write the FC's digit planes).
+int avgsum_path(const ActView &in, const int32_t *out) {
+  if (in.bits == 2 && in.cpg % 16 == 0 && (int64_t)in.h * in.w <= 85) {
+    const int wpr = in.cpg / 16;
+    if (wpr <= 256 && 256 % wpr == 0 && (int64_t)in.n * in.groups < ((int64_t)1 << 31)) return 2;
+    if (((uintptr_t)out & 15u) == 0) return 1;
+  }
+  return 0;
+}
+
+const char *avgsum_label(const ActView &in, const int32_t *out) {
+  static const char *names[3] = {"avgsum_kernel", "avgsum2_kernel", "avgsum2_wg_kernel"};
+  return names[avgsum_path(in, out)];
+}
+
 hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s, int8_t *planes, int P, int32_t *logits,
                          int cout) {
   const int64_t items = (int64_t)in.n * in.groups * in.cpg;
   if (items == 0) return hipSuccess;
   if (planes && !avgsum_makes_fc_planes(in)) return hipErrorInvalidValue;
-  if (in.bits == 2 && in.cpg % 16 == 0 && (int64_t)in.h * in.w <= 85) {
-    const int wpr = in.cpg / 16;
-    if (wpr <= 256 && 256 % wpr == 0 && (int64_t)in.n * in.groups < ((int64_t)1 << 31)) {
-      hipLaunchKernelGGL(avgsum2_wg_kernel, dim3((unsigned)(in.n * in.groups)), dim3(256), 0, s, in, out, planes, P,
-                         items, logits, cout);
-      return hipGetLastError();
-    }
-    if (((uintptr_t)out & 15u) == 0) {
-      hipLaunchKernelGGL(avgsum2_kernel, dim3(grid_for(items / 16)), dim3(kBlock), 0, s, in, out);
-      return hipGetLastError();
-    }
+  const int path = avgsum_path(in, out);
+  if (path == 2) {
+    hipLaunchKernelGGL(avgsum2_wg_kernel, dim3((unsigned)(in.n * in.groups)), dim3(256), 0, s, in, out, planes, P,
+                       items, logits, cout);
+    return hipGetLastError();
+  }
+  if (path == 1) {
+    hipLaunchKernelGGL(avgsum2_kernel, dim3(grid_for(items / 16)), dim3(kBlock), 0, s, in, out);
+    return hipGetLastError();
   }
   hipLaunchKernelGGL(avgsum_kernel, dim3(grid_for(items)), dim3(kBlock), 0, s, in, out);
   return hipGetLastError();
@@ -822,6 +867,11 @@ hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s, int8_t 
 bool fc_mfma_applies(const int32_t *x, int n, int cin, int cout, const int8_t *scratch) {
   return scratch && cin % 32 == 0 && ((uintptr_t)x & 15u) == 0 && (int64_t)4 * n * cin < ((int64_t)1 << 31) &&
          (int64_t)cout * cin < ((int64_t)1 << 31);
+}
+
+const char *fc_label(const int32_t *x, int n, int cin, int cout, const int8_t *scratch, bool planes_ready) {
+  if (!fc_mfma_applies(x, n, cin, cout, scratch)) return "fill_i32_kernel + fc_kernel";
+  return planes_ready ? "fc_mfma_kernel" : "fc_digits_kernel + fc_mfma_kernel";
 }
 
 hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout, int32_t *logits,
@@ -843,10 +893,6 @@ hipError_t launch_fc(const int32_t *x, int n, int cin, const int8_t *w, int cout
     // slices 20 us, 32 slices 48 us)
     const int64_t blocks = (int64_t)((cout + 31) / 32) * ((n + 31) / 32);
     int slices = (int)std::max<int64_t>(1, std::min<int64_t>((128 + blocks - 1) / blocks, cin / 128));
-    if (const char *e = getenv("PALQ_FC_SLICES")) {  // tuning
-      const int v = atoi(e);
-      if (v >= 1 && v <= cin / 32) slices = v;
-    }
     dim3 grid((unsigned)((cout + 31) / 32), (unsigned)((n + 31) / 32), (unsigned)slices);
     auto mm = P == 1 ? fc_mfma_kernel<1> : P == 2 ? fc_mfma_kernel<2> : fc_mfma_kernel<4>;
     hipLaunchKernelGGL(mm, grid, dim3(256), 0, s, w, (const int8_t *)scratch, n, cin, cout, logits);

@@ -383,14 +383,9 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
     uint8_t *wp = ctx->conv_scratch;
     int32_t *thr = (int32_t *)(ctx->conv_scratch + wbytes);
     e = launch_conv_prepare(a, wp, thr, ctx->stream);
-    int epi = -1;  // unknown: both epilogue builds start, the one that applies runs
-    if (e == hipSuccess && !conv_mfma_general_fits(a)) {
-      // only the tiled kernel's fast epilogue exists for this layer: read the
-      // requant flag now (synchronous) and take the direct kernel if needed
-      epi = conv_mfma_epilogue(a, thr);
-      if (epi < 0) e = hipErrorUnknown;
-    }
-    if (e == hipSuccess) e = epi == 1 ? launch_conv_direct(a, ctx->stream) : launch_conv_mfma(a, wp, thr, epi, ctx->stream);
+    // the epilogue build is not known on the host: both start and the one
+    // that applies runs (decided on the device from the requant flag)
+    if (e == hipSuccess) e = launch_conv_mfma(a, wp, thr, -1, ctx->stream);
   } else {
     e = launch_conv_direct(a, ctx->stream);
   }

@@ -68,10 +68,13 @@ struct ConvArgs {
   int32_t proj_stride;
   int32_t *acc_dump;     // may be null
   int32_t fp4;           // 1: 2-bit layers may run on the FP4 matrix cores (where exact)
+  int32_t gated;         // set by the launcher: general partner of a tiled launch
 };
 
 // Kernel launchers (return hipError_t of the launch).
-hipError_t launch_conv_direct(const ConvArgs &a, hipStream_t s);
+// only_if_flag (device, nullable): the kernel does nothing unless *only_if_flag
+// is non-zero (the general partner of a tiled launch, see launch_conv_mfma).
+hipError_t launch_conv_direct(const ConvArgs &a, hipStream_t s, const int32_t *only_if_flag = nullptr);
 // Whether the MFMA kernels take this layer.
 bool conv_mfma_supported(const ConvArgs &a);
 // Whether the general (persistent, filter-in-LDS) build fits this layer;
@@ -95,9 +98,14 @@ bool conv_mfma_pads_input(const ConvArgs &a);
 // the stream has drained: 0 fast, 1 general, -1 unknown (copy failed).
 // Synchronous; for planning only.
 int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr);
-// epi: the value above, or -1 to start both builds (each checks on the
-// device whether it applies and the other returns at once).
+// epi: the value above, or -1 when it is not known on the host: both builds
+// start and each checks on the device whether it applies (the other returns
+// at once); no host synchronisation either way.
 hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, int epi, hipStream_t s);
+// Kernel family launch_conv_mfma runs for the layer with epi 0 or 1 (static
+// string: "conv_tile_kernel[fp4]", "conv_tile_kernel[int8]",
+// "conv_tile_kernel[stem]", "conv_grouped_kernel" or "conv_stem_kernel").
+const char *conv_kernel_label(const ConvArgs &a, int epi);
 // Stem conv fused with the 3x3 / stride 2 / pad 1 max pool of its output
 // (written to po only; the stem's own output is not written).  Requires the
 // fast epilogue (conv_mfma_epilogue == 0).
@@ -136,6 +144,15 @@ int fc_planes(int64_t xmax);
 // Whether the global sum of `in` can also write the FC's digit planes (and
 // zero the logits): launch_avgsum with planes != nullptr.
 bool avgsum_makes_fc_planes(const ActView &in);
+
+// Names of the kernels the launchers above run for these arguments (static
+// strings; the same conditions the launchers test).
+const char *quantize_label(const float *x, const ActView &out);
+const char *quantize_pad_label(const float *x, int in_w, int pad, const ActView &out);
+const char *pad_pixels_label(const ActView &out);
+const char *maxpool_label(const ActView &in, const ActView &out);
+const char *avgsum_label(const ActView &in, const int32_t *out);
+const char *fc_label(const int32_t *x, int n, int cin, int cout, const int8_t *scratch, bool planes_ready);
 
 }  // namespace palq
 

@@ -96,6 +96,10 @@ struct palq_net {
   int32_t *g_logits = nullptr;
   float g_l = 0.f, g_u = 0.f;
   hipStream_t g_stream = nullptr;
+  // palq_net_layer_kernels: per layer, the kernels palq_forward (0) and
+  // palq_forward_image (1) launch; img_label: forward_image's own quantiser
+  std::vector<std::string> labels[2];
+  std::string img_label;
 };
 
 namespace {
@@ -549,6 +553,33 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       net->input.data = net->img_codes;
     }
   }
+  // the kernels each layer launches (the launchers' own selection rules)
+  for (int v = 0; v < 2; ++v) net->labels[v].assign(n_layers, std::string());
+  for (int i = 0; i < n_layers; ++i) {
+    const palq_layer &L = layers[i];
+    const Layer &NL = net->layers[i];
+    if (NL.skip) continue;
+    std::string k;
+    if (L.op == PALQ_OP_CONV) {
+      k = NL.pool_fused ? "stem_pool_kernel" : NL.use_mfma ? conv_kernel_label(NL.conv, NL.epi) : "conv_direct_kernel";
+    } else if (L.op == PALQ_OP_CHANNEL_SHUFFLE) {
+      k = "channel_shuffle_kernel";
+    } else if (L.op == PALQ_OP_MAXPOOL) {
+      k = maxpool_label(view_of(&net->tensors[L.src].d), view_of(&net->tensors[L.dst].d));
+    } else if (L.op == PALQ_OP_AVGSUM) {
+      k = avgsum_label(view_of(&net->tensors[L.src].d), NL.sums_out);
+    } else if (L.op == PALQ_OP_FC) {
+      k = fc_label(NL.fc_in, net->n, NL.fc_cin, L.fc_out, NL.fc_scratch, NL.fc_planes_ready);
+    }
+    net->labels[0][i] = net->labels[1][i] = k;
+    if (L.op == PALQ_OP_CONV && NL.pad > 0) {
+      net->labels[0][i] = std::string(pad_pixels_label(NL.conv.in)) + " + " + k;
+      net->labels[1][i] = (net->img_direct && L.src == 0)
+                              ? std::string(quantize_pad_label((const float *)fake_ptr(0), NL.pad_in.w, NL.pad, NL.conv.in)) + " + " + k
+                              : net->labels[0][i];
+    }
+  }
+  if (net->img_input && !net->img_direct) net->img_label = quantize_label((const float *)fake_ptr(0), view_of(&net->input));
   if (flags & PALQ_NET_TIMING) {
     net->events.assign((size_t)kRing * (n_layers + 1), nullptr);
     for (auto &ev : net->events)
@@ -713,6 +744,13 @@ palq_status palq_forward_image(palq_ctx *ctx, palq_net *net, const float *x, flo
   const hipError_t e = launch_quantize(x, l, u, nullptr, view_of(&net->input), ctx->stream);
   if (e != hipSuccess) return net_fail(ctx, PALQ_ERR_DEVICE, std::string("quantize: ") + hipGetErrorString(e));
   return forward_dispatch(ctx, net, net->img_codes, logits, nullptr, 0.f, 0.f);
+}
+
+const char *palq_net_layer_kernels(const palq_net *net, int32_t layer, int32_t image) {
+  if (!net || (image != 0 && image != 1) || layer < -1 || layer >= (int32_t)net->layers.size()) return nullptr;
+  if (layer == -1) return image ? net->img_label.c_str() : "";
+  if (net->labels[image].size() != net->layers.size()) return "";  // validate-only network: nothing planned
+  return net->labels[image][layer].c_str();
 }
 
 palq_status palq_net_tensor(const palq_net *net, int32_t id, palq_act *desc) {

@@ -22,6 +22,7 @@ the network input):
 from __future__ import annotations
 
 import math
+import os
 
 import numpy as np
 
@@ -261,3 +262,47 @@ def image_fp32(seed, n, hw=224, c=3):
     """Synthetic fp32 image batch (standard-normal pixels, NHWC) for the
     quantiser in front of the stem."""
     return rng(seed).standard_normal((n, hw, hw, c), dtype=np.float32)
+
+
+# ---------------------------------------------------------------------------
+# Benchmark workloads (fp32 image batches in front of the 8-bit stem) and
+# their centred variants
+# ---------------------------------------------------------------------------
+# Images: standard-normal fp32 pixels quantised over [-3, 3] (Eq. 2) to
+# signed 8-bit codes by the network's first step.
+IMAGE_RANGE = (-3.0, 3.0)
+GOLDEN_DIR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "tests", "golden")
+
+
+def workload(name):
+    """(spec, fp32 images, images the centring is calibrated on) of a
+    benchmark network: "resnet18_g4_b2" (ResNet-18 topology, G=4, 2-bit,
+    batch 64, 224x224) or "resnet50_g2_b2" (ResNet-50 v1.5 bottlenecks, G=2,
+    2-bit, batch 128, 224x224)."""
+    if name == "resnet18_g4_b2":
+        return resnet18(n=64, groups=4, bits=2), image_fp32(SEED_BASE + 30, 64), [0, 63]
+    if name == "resnet50_g2_b2":
+        return resnet50(n=128, groups=2, bits=2), image_fp32(SEED_BASE + 50, 128), [0, 127]
+    raise ValueError(name)
+
+
+def centred_path(name):
+    return os.path.join(GOLDEN_DIR, f"centred_bias_{name}.npz")
+
+
+def with_stored_biases(spec, name):
+    """A copy of `spec` whose conv biases are the stored centred ones of
+    workload `name` (tests/golden/centred_bias_<name>.npz, written by
+    tests/golden/make_centred_bias.py from the oracle's calibration on the
+    workload's calibration images): layer i's bias is array "layer<i>"."""
+    import copy
+    spec = copy.deepcopy(spec)
+    with np.load(centred_path(name), allow_pickle=False) as z:
+        for i, L in enumerate(spec["layers"]):
+            if L["op"] in ("conv", "shuffle_module"):
+                b = z[f"layer{i}"]
+                if b.shape != (L["w"].shape[0] * L["w"].shape[1],):
+                    raise ValueError(f"stored bias of layer {i} has shape {b.shape}")
+                L["bias"] = b.astype(np.int32)
+    spec["name"] = spec["name"] + "_centred"
+    return spec

@@ -97,6 +97,7 @@ _forward = _sig("palq_forward", c_i32, c_p, c_p, c_p, c_p)
 _forward_image = _sig("palq_forward_image", c_i32, c_p, c_p, c_p, c_f, c_f, c_p)
 _net_tensor = _sig("palq_net_tensor", c_i32, c_p, c_i32, P_ACT)
 _net_ops = _sig("palq_net_ops", c_i64, c_p)
+_net_layer_kernels = _sig("palq_net_layer_kernels", ctypes.c_char_p, c_p, c_i32, c_i32)
 _net_layer_times = _sig("palq_net_layer_times", c_i32, c_p, ctypes.POINTER(c_f), ctypes.POINTER(c_i32))
 _net_reset_times = _sig("palq_net_reset_times", c_i32, c_p)
 
@@ -105,7 +106,8 @@ EXPORTS = ["palq_create", "palq_destroy", "palq_set_stream", "palq_set_conv_fp4"
            "palq_quantize", "palq_group_conv", "palq_shuffle_module", "palq_cyclic_shuffle",
            "palq_channel_shuffle", "palq_maxpool",
            "palq_avgsum", "palq_fc", "palq_net_create", "palq_net_destroy", "palq_forward",
-           "palq_forward_image", "palq_net_tensor", "palq_net_ops", "palq_net_layer_times", "palq_net_reset_times"]
+           "palq_forward_image", "palq_net_tensor", "palq_net_ops", "palq_net_layer_kernels", "palq_net_layer_times",
+           "palq_net_reset_times"]
 
 
 class PalqError(RuntimeError):
@@ -364,6 +366,22 @@ class Net:
         if st != OK:
             raise PalqError(st, f"no tensor {tid}")
         return Tensor(None, a)
+
+    def layer_kernels(self, image=False):
+        """The kernels each layer launches in palq_forward (or, image=True,
+        palq_forward_image), as the library's selection picked them."""
+        out = []
+        for i in range(self.n_layers):
+            r = _net_layer_kernels(self.h, i, int(bool(image)))
+            if r is None:
+                raise PalqError(ERR_ARG, f"palq_net_layer_kernels({i})")
+            out.append(r.decode())
+        return out
+
+    def input_kernel(self):
+        """palq_forward_image's own quantiser pass ("" when the stem's
+        bordered input takes the codes directly)."""
+        return _net_layer_kernels(self.h, -1, 1).decode()
 
     def layer_times(self):
         ms = (c_f * self.n_layers)()

@@ -1,0 +1,45 @@
+"""Writes tests/golden/centred_bias_<workload>.npz: the centred variant's
+conv biases of each benchmark network (reading A14 of the design notes:
+bias = -round_half_up(mean of the layer's pre-requant value), layer by
+layer), calibrated by the CPU oracle on the workload's calibration images.
+
+Calls only the oracle and the seeded input generators:
+
+    python tests/golden/make_centred_bias.py [workload ...]
+
+Array "layer<i>" holds layer i's int32 bias (source channel order, as the
+layer's requant arrays); "calib_images" the image indices used.
+"""
+import os
+import sys
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+sys.path.insert(0, ROOT)
+
+from oracle import oracle as O  # noqa: E402
+from paper_2208_01944_amd import inputs as I  # noqa: E402
+
+WORKLOADS = ["resnet18_g4_b2", "resnet50_g2_b2"]
+
+
+def calibrate(name):
+    spec, x, calib = I.workload(name)
+    l, u = I.IMAGE_RANGE
+    codes = O.quantize(x[calib], l, u, 8, signed=True)
+    return O.calibrate_centring(spec, codes), calib
+
+
+def main(names):
+    for name in names:
+        cen, calib = calibrate(name)
+        arrays = {f"layer{i}": np.asarray(L["bias"], np.int32)
+                  for i, L in enumerate(cen["layers"]) if L["op"] in ("conv", "shuffle_module")}
+        arrays["calib_images"] = np.asarray(calib, np.int32)
+        np.savez_compressed(I.centred_path(name), **arrays)
+        print("wrote", I.centred_path(name))
+
+
+if __name__ == "__main__":
+    main(sys.argv[1:] or WORKLOADS)

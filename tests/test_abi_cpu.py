@@ -173,6 +173,11 @@ def test_validate_only_net_create(P, vctx):
     assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 5, 0, ctypes.byref(h)) == P.OK
     # 2 * MACs: 2*(2*8*8*128*27) + 2*(2*4*4*128*576) + 2*(2*128*10)
     assert P._net_ops(h) == 2 * (2 * 8 * 8 * 128 * 27) + 2 * (2 * 4 * 4 * 128 * 576) + 2 * (2 * 128 * 10)
+    # kernel names: nothing is planned on a validate-only network; bad indices give NULL
+    assert [P._net_layer_kernels(h, i, 0) for i in range(5)] == [b""] * 5
+    assert P._net_layer_kernels(h, -1, 1) == b"" and P._net_layer_kernels(h, -1, 0) == b""
+    assert P._net_layer_kernels(h, 5, 0) is None and P._net_layer_kernels(h, -2, 0) is None
+    assert P._net_layer_kernels(h, 0, 2) is None and P._net_layer_kernels(None, 0, 0) is None
     P._net_destroy(h)
     # FC not last / wrong input / reused id
     Ls[4] = _layer(P, op=P.OP_FC, src=3, dst=5, fc_w=_fake(8), fc_out=10)

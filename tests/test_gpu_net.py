@@ -235,24 +235,68 @@ def test_resnet18_bits3_g3(ctx, torch):
     np.testing.assert_array_equal(logits, O.run_net(spec, spec["x"]))
 
 
-def test_c3_full_size_sampled(ctx, torch):
-    """The benchmark workload (ResNet-18 topology, G=4, 2-bit, 224x224,
-    batch 64) at full size; the oracle runs the first and last image."""
-    say("C3 resnet18 n=64 224x224 G=4 b=2 (centred on images 0 and 63)")
-    spec = I.resnet18()
-    pick = [0, 63]
-    spec = O.calibrate_centring(spec, spec["x"][pick])
-    net, logits = gpu_forward(ctx, torch, spec)
-    ref = O.run_net(spec, spec["x"][pick])
-    np.testing.assert_array_equal(logits[pick], ref)
+def full_size_run(ctx, torch, name):
+    """The benchmark's network (stored centred biases, default flags) on
+    the workload's whole fp32 image batch through palq_forward_image, as
+    bench.py times it: (centred spec, the batch's 8-bit codes (oracle's
+    quantiser), GPU logits, the kernels each layer launched)."""
+    from paper_2208_01944_amd import palq
+    spec, x, _ = I.workload(name)
+    spec = I.with_stored_biases(spec, name)
+    l, u = I.IMAGE_RANGE
+    net = palq.Net(ctx, spec)
+    logits = torch.empty(x.shape[0] * net.classes, dtype=torch.int32, device=ctx.dev)
+    net.forward_image(ctx.upload(x), l, u, logits)
+    ctx.sync()
+    got = logits.cpu().numpy().astype(np.int64).reshape(x.shape[0], net.classes)
+    kernels = net.layer_kernels(image=True)
+    del net
+    return spec, O.quantize(x, l, u, 8, signed=True), got, kernels
+
+
+@pytest.fixture(scope="module")
+def c3_run(ctx, torch):
+    say("C3 resnet18 n=64 224x224 G=4 b=2 centred: GPU forward_image of the whole batch")
+    return full_size_run(ctx, torch, "resnet18_g4_b2")
+
+
+@pytest.fixture(scope="module")
+def c5_run(ctx, torch):
+    say("C5 resnet50 n=128 224x224 G=2 b=2 centred: GPU forward_image of the whole batch")
+    return full_size_run(ctx, torch, "resnet50_g2_b2")
+
+
+def test_c3_launches_the_benchmark_kernels(c3_run):
+    """The full-size network runs the kernels the benchmark reports: the
+    fused stem + max pool and the 2-bit grouped layers on FP4 matrix cores."""
+    kernels = c3_run[3]
+    assert kernels[0] == "quantize_pad4_kernel + stem_pool_kernel", kernels[0]
+    assert kernels[1] == "", kernels[1]
+    assert kernels.count("conv_tile_kernel[fp4]") == 16, kernels
+    assert kernels[-2:] == ["avgsum2_wg_kernel", "fc_mfma_kernel"], kernels[-2:]
+
+
+@pytest.mark.parametrize("chunk", range(8))
+def test_c3_full_size_every_image(c3_run, chunk):
+    """C3 at full size: the logits of every image of the batch (8 per test)
+    against the oracle's forward of the same centred network."""
+    spec, codes, got, _ = c3_run
+    sl = slice(8 * chunk, 8 * chunk + 8)
+    say(f"C3 oracle images {sl.start}..{sl.stop - 1}")
+    ref = O.run_net(spec, codes[sl])
+    np.testing.assert_array_equal(got[sl], ref)
     assert len(np.unique(ref)) > 100  # logits are not degenerate
 
 
-def test_c5_full_size_sampled(ctx, torch):
-    say("C5 resnet50 n=128 224x224 G=2 b=2 (centred on image 127)")
-    spec = I.resnet50()
-    pick = [127]
-    spec = O.calibrate_centring(spec, spec["x"][pick])
-    net, logits = gpu_forward(ctx, torch, spec)
-    ref = O.run_net(spec, spec["x"][pick])
-    np.testing.assert_array_equal(logits[pick], ref)
+@pytest.mark.parametrize("chunk", range(16))
+def test_c5_full_size_every_image(c5_run, chunk):
+    """C5 (ResNet-50, G=2, 2-bit, batch 128) at full size: every image's
+    logits (8 per test) against the oracle."""
+    spec, codes, got, kernels = c5_run
+    if chunk == 0:
+        assert kernels.count("conv_tile_kernel[fp4]") >= 40, kernels
+    sl = slice(8 * chunk, 8 * chunk + 8)
+    say(f"C5 oracle images {sl.start}..{sl.stop - 1}")
+    ref = O.run_net(spec, codes[sl])
+    np.testing.assert_array_equal(got[sl], ref)
+    assert len(np.unique(ref)) > 100

@@ -203,28 +203,10 @@ def test_conv_empty_batch(ctx, torch):
     assert q.size == 0 and racc.size == 0
 
 
-@pytest.mark.parametrize("fp4", [True, False])
-@pytest.mark.parametrize("layer", range(4))
-def test_conv_c2_full_batch_sampled(ctx, torch, layer, fp4):
-    """Each ResNet-18 stage shape at G=4, batch 32, in the launch the benchmark
-    uses (FP4 matrix cores, and int8 only); the oracle checks the first and
-    last image."""
-    say(f"conv C2 layer {layer} batch 32 fp4={fp4}")
-    case = I.config_c2(layer)
-    ctx.set_conv_fp4(fp4)
-    try:
-        full = run_conv_full(ctx, torch, case)
-    finally:
-        ctx.set_conv_fp4(True)
-    for img in (0, 31):
-        sub = dict(case, x=case["x"][img:img + 1])
-        _, _, rq, racc = run_conv(ctx, torch, sub)
-        np.testing.assert_array_equal(full[0][img:img + 1], rq)
-        np.testing.assert_array_equal(full[1][img:img + 1], racc)
-
-
-def run_conv_full(ctx, torch, case):
-    """GPU only (no oracle): codes and accumulators of the whole batch."""
+def run_conv_full(ctx, torch, case, bias):
+    """GPU only (no oracle): codes of the whole batch from the plain launch,
+    then codes and accumulators from the accumulator-dump launch (the same
+    kernel family with its dump build)."""
     L = case["layer"]
     x = case["x"]
     G, co, kh, kw, ci = L["w"].shape
@@ -236,39 +218,96 @@ def run_conv_full(ctx, torch, case):
     out = ctx.empty_act(n, ho, wo, G, co, L["out_bits"])
     dump = torch.zeros(n * ho * wo * G * co, dtype=torch.int32, device=ctx.dev)
     i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
-    ctx.group_conv(xt, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(L["bias"]),
-                   out, shuffle=L["shuffle"])
+    args = (xt, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(bias), out)
+    ctx.group_conv(*args, shuffle=L["shuffle"])
     ctx.sync()
     q_plain = ctx.unpack(out)
-    ctx.group_conv(xt, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(L["bias"]),
-                   out, shuffle=L["shuffle"], acc_dump=dump)
+    dump.fill_(-1)
+    ctx.group_conv(*args, shuffle=L["shuffle"], acc_dump=dump)
     ctx.sync()
     acc = dump.cpu().numpy().astype(np.int64).reshape(n, ho, wo, G * co)
-    q = ctx.unpack(out)
-    np.testing.assert_array_equal(q_plain, q)
-    return q, acc
+    return q_plain, ctx.unpack(out), acc
+
+
+def oracle_full(case):
+    """The oracle on the whole batch, accumulator once: (acc_d, stated codes,
+    centred bias, centred codes).  The centred bias (reading A14) is the
+    oracle's centring over the positions whose window lies inside the image
+    (stride-1 layers): border pixels, with fewer taps, then saturate while
+    the interior spreads over every code (centring over all positions leaves
+    7x7 and 14x14 maps with almost no middle codes)."""
+    L = case["layer"]
+    G = L["w"].shape[0]
+    acc = O.group_conv(case["x"], L["w"], L["stride"], L["pad"])
+    q_stated, acc_d = O.layer_epilogue(acc, G, L["mult"], L["shift"], L["bias"], L["out_bits"], L["shuffle"])
+    p = L["pad"] if L["stride"] == 1 else 0
+    bias_c = O.centring_bias(acc_d[:, p:acc_d.shape[1] - p, p:acc_d.shape[2] - p], G, L["shuffle"])
+    q_centred, _ = O.layer_epilogue(acc, G, L["mult"], L["shift"], bias_c, L["out_bits"], L["shuffle"])
+    return acc_d, q_stated, bias_c, q_centred
+
+
+def check_full(ctx, torch, case, fp4_modes=(True, False)):
+    """Every image of a full-size single-layer case, stated and centred, in
+    the launch the benchmark uses (FP4 matrix cores for 2-bit layers) and
+    with int8 matrix cores only: accumulators (from the dump build of the
+    same kernel) and codes of both builds bit-exact; every output code
+    occurs in the centred codes."""
+    L = case["layer"]
+    acc_d, q_stated, bias_c, q_centred = oracle_full(case)
+    hist = np.bincount(q_centred.reshape(-1), minlength=1 << L["out_bits"])
+    assert np.all(hist >= 0.01 * q_centred.size / len(hist)), hist  # every output code occurs
+    for fp4 in fp4_modes:
+        ctx.set_conv_fp4(fp4)
+        try:
+            for name, bias, want in (("centred", bias_c, q_centred), ("stated", L["bias"], q_stated)):
+                say(f"  fp4={fp4} {name}")
+                q_plain, q_dump, acc = run_conv_full(ctx, torch, case, bias)
+                np.testing.assert_array_equal(acc, acc_d, err_msg=f"acc fp4={fp4} {name}")
+                np.testing.assert_array_equal(q_dump, want, err_msg=f"codes (dump build) fp4={fp4} {name}")
+                np.testing.assert_array_equal(q_plain, want, err_msg=f"codes fp4={fp4} {name}")
+        finally:
+            ctx.set_conv_fp4(True)
+
+
+@pytest.mark.parametrize("layer", range(4))
+def test_conv_c2_full_batch_every_image(ctx, torch, layer):
+    """Each ResNet-18 stage shape at G=4, batch 32: every image, every
+    output code and accumulator."""
+    say(f"conv C2 layer {layer} batch 32 (every image)")
+    check_full(ctx, torch, I.config_c2(layer))
 
 
 @pytest.mark.parametrize("groups", [1, 2, 4])
 @pytest.mark.parametrize("bits", [2, 3, 4])
-def test_conv_c4_sweep_sampled(ctx, torch, groups, bits):
-    say(f"conv C4 G={groups} b={bits} batch 128")
-    case = I.config_c4(groups, bits)
-    full = run_conv_full(ctx, torch, case)
-    for img in (0, 127):
-        sub = dict(case, x=case["x"][img:img + 1])
-        _, _, rq, racc = run_conv(ctx, torch, sub)
-        np.testing.assert_array_equal(full[1][img:img + 1], racc)
-        np.testing.assert_array_equal(full[0][img:img + 1], rq)
+def test_conv_c4_sweep_every_image(ctx, torch, groups, bits):
+    """The G x B sweep on the 14x14 / 256-channel layer at batch 128: every
+    image (3- and 4-bit layers have no FP4 path)."""
+    say(f"conv C4 G={groups} b={bits} batch 128 (every image)")
+    check_full(ctx, torch, I.config_c4(groups, bits), (True, False) if bits == 2 else (True,))
+
+
+@pytest.mark.parametrize("pb4", [False, True])
+def test_conv_tile_chunked_xcd_order_centred(ctx, torch, pb4):
+    """Small centred cases that reach the tiled kernel's chunked tile order
+    (the packed input outweighs the filter by 7x, so 32 pixel chunks) and,
+    with pb4, its 2 x 4 accumulator blocks (256-pixel tiles on 128-channel
+    layers, chosen when they do not lengthen the busiest CU's share)."""
+    if pb4:
+        # M = 16384 pixels per group: 64 tiles of 256 pixels x 4 groups = 256 (one per CU)
+        case = I.single_layer(2201, n=16, h=32, w=32, groups=4, cin=128, cout=128, shuffle=1)
+    else:
+        case = I.single_layer(2202, n=8, h=28, w=28, groups=4, cin=64, cout=64, shuffle=3)
+    say(f"conv tiled chunk order pb4={pb4} {case['x'].shape}")
+    check_full(ctx, torch, case)
 
 
 def test_conv_deterministic(ctx, torch):
     say("conv determinism")
     case = I.config_c2(1, n=4)
-    a = run_conv_full(ctx, torch, case)
-    b = run_conv_full(ctx, torch, case)
-    np.testing.assert_array_equal(a[0], b[0])
-    np.testing.assert_array_equal(a[1], b[1])
+    a = run_conv_full(ctx, torch, case, case["layer"]["bias"])
+    b = run_conv_full(ctx, torch, case, case["layer"]["bias"])
+    for u, v in zip(a, b):
+        np.testing.assert_array_equal(u, v)
 
 
 # ---------------------------------------------------------------- shuffle & glue

@@ -578,3 +578,29 @@ def test_bitops_match_paper_tables():
         macs = cache[key]
         got = O.bitops(macs, dense or B, dense or B) / 1e9
         assert abs(got - printed) / printed < 0.005, (net, B, G, dense, got, printed, " ".join(src))
+
+
+# ---------------------------------------------------------------------------
+# Stored inputs: the benchmark networks' centred biases
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["resnet18_g4_b2", "resnet50_g2_b2"])
+def test_stored_centred_biases_match_oracle_calibration(name):
+    """tests/golden/centred_bias_<name>.npz holds what the oracle's centring
+    calibration gives today on the workload's calibration images (so the
+    benchmark times, and the full-size tests check, the centred network the
+    oracle defines)."""
+    import importlib.util
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "make_centred_bias.py")
+    spec_m = importlib.util.spec_from_file_location("make_centred_bias", path)
+    mk = importlib.util.module_from_spec(spec_m)
+    spec_m.loader.exec_module(mk)
+    cen, calib = mk.calibrate(name)
+    stored = I.with_stored_biases(I.workload(name)[0], name)
+    with np.load(I.centred_path(name), allow_pickle=False) as z:
+        assert z["calib_images"].tolist() == list(calib)
+    n_conv = 0
+    for L, S in zip(cen["layers"], stored["layers"]):
+        if L["op"] == "conv":
+            np.testing.assert_array_equal(S["bias"], L["bias"])
+            n_conv += 1
+    assert n_conv >= 17  # ResNet-18: stem + 16 (projections are fused)
