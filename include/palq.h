@@ -182,6 +182,23 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
                             int32_t pad, const palq_requant *rq, const palq_residual *res,
                             int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump);
 
+/* palq_group_conv for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, checks, arithmetic and results as
+ * palq_group_conv, but the layer's prepacked filter and requant constants go
+ * into a static device buffer of PALQ_NOALLOC_SCRATCH_BYTES that the library
+ * holds on every GPU it runs on (until the process ends) instead of context
+ * memory, and the call allocates, frees and synchronises nothing.  Every
+ * call on one GPU shares that buffer and it keeps the last call's contents:
+ * calls on one stream are ordered, calls that overlap on one GPU (other
+ * streams, contexts or host threads) race.  PALQ_ERR_UNSUPPORTED (nothing
+ * written) when the prepacked filter and constants of the layer exceed the
+ * buffer; PALQ_ERR_DEVICE when the buffer is unavailable on this device. */
+#define PALQ_NOALLOC_SCRATCH_BYTES (16 << 20)
+palq_status palq_group_conv_noalloc(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
+                                    int32_t pad, const palq_requant *rq, const palq_residual *res,
+                                    int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump);
+
 /* The cyclic permutation of Section 4.2 (Eq. 6-8) on its own:
  * out[pixel, (g + steps) mod G, :] = in[pixel, g, :], any integer steps.
  * in and out have the same shape and bits and must not overlap. */

@@ -2209,4 +2209,36 @@ hipError_t launch_conv_mfma(const ConvArgs &a_in, const uint8_t *wp, const int32
   return hipErrorNotSupported;
 }
 
+// ---------------------------------------------------------------- static scratch
+// palq_group_conv_noalloc's prepacked filter and requant constants: a
+// file-scope device array, one copy on every GPU that loads the library
+// (held until the process ends).  In host code `scratch` is only a handle
+// for the runtime; kernels receive the device address that
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) uint8_t scratch[PALQ_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t *g_scratch_ptr[kMaxScratchDevices];
+bool g_scratch_looked_up[kMaxScratchDevices];
+}  // namespace
+
+hipError_t noalloc_scratch_init(int device) {
+  if (device < 0 || device >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_looked_up[device]) return g_scratch_ptr[device] ? hipSuccess : hipErrorInvalidSymbol;
+  void *p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  g_scratch_looked_up[device] = true;
+  g_scratch_ptr[device] = (e == hipSuccess && p) ? (uint8_t *)p : nullptr;
+  return e;
+}
+
+uint8_t *noalloc_scratch(int device) {
+  if (device < 0 || device >= kMaxScratchDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  return g_scratch_ptr[device];
+}
+
 }  // namespace palq

@@ -112,6 +112,9 @@ palq_status palq_create(int32_t device, void *hip_stream, palq_ctx **out) {
       return PALQ_ERR_DEVICE;
     }
     e = hipSetDevice(device);
+    // the no-alloc call's static buffer: its address on this device, looked
+    // up once per device (a failure only disables palq_group_conv_noalloc)
+    if (e == hipSuccess) noalloc_scratch_init(device);
     if (e == hipSuccess) e = hipMalloc(&ctx->range_scratch, 2 * sizeof(float));
     if (e != hipSuccess) {
       delete ctx;
@@ -278,9 +281,13 @@ palq_status palq_shuffle_module(palq_ctx *ctx, const palq_act *in, const palq_fi
 }
 
 // ------------------------------------------------------------ group conv
-palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
+namespace {
+// palq_group_conv (noalloc = false: prepacked filter and constants in the
+// context's scratch, grown on demand) and palq_group_conv_noalloc (the
+// library's static per-GPU buffer; no allocation, free or synchronisation).
+palq_status group_conv_impl(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
                             int32_t pad, const palq_requant *rq, const palq_residual *res,
-                            int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump) {
+                            int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump, bool noalloc) {
   if (!ctx) return PALQ_ERR_ARG;
   palq_status st;
   if ((st = check_act(ctx, in, "in")) || (st = check_filter(ctx, w, "w")) ||
@@ -350,7 +357,6 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
   const int64_t dump_bytes = (int64_t)out->n * ho * wo * w->groups * w->cout_pg * 4;
   if (acc_dump && (((uintptr_t)acc_dump & 15u) != 0 || overlaps(acc_dump, dump_bytes, out->data, ob)))
     return fail(ctx, PALQ_ERR_ARG, "acc_dump misaligned or overlapping the output");
-  if (ctx->device < 0) return PALQ_OK;
 
   ConvArgs a{};
   a.in = view_of(in);
@@ -365,13 +371,25 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
   if (rid) { a.res = view_of(rid); a.res_mult = res->res_mult; }
   if (pin) { a.proj = view_of(pin); a.proj_w = (const uint8_t *)pw->data; a.proj_stride = res->proj_stride; }
   a.acc_dump = acc_dump;
-  if (out->n == 0) return PALQ_OK;
+  const bool mfma = conv_mfma_supported(a);
+  const ConvPlan plan = mfma ? conv_mfma_plan(a) : ConvPlan{0, 0};
+  const size_t wbytes = (plan.w_bytes + 255) & ~(size_t)255;
+  const size_t need = wbytes + plan.thr_bytes;
+  if (noalloc && need > (size_t)PALQ_NOALLOC_SCRATCH_BYTES)
+    return fail(ctx, PALQ_ERR_UNSUPPORTED,
+                "no-alloc call: the prepacked filter and requant constants need " + std::to_string(need) +
+                    " bytes; the library's static buffer holds " + std::to_string((long long)PALQ_NOALLOC_SCRATCH_BYTES));
+  if (ctx->device < 0 || out->n == 0) return PALQ_OK;
   hipSetDevice(ctx->device);
   hipError_t e;
-  if (conv_mfma_supported(a)) {
-    const ConvPlan plan = conv_mfma_plan(a);
-    const size_t wbytes = (plan.w_bytes + 255) & ~(size_t)255;
-    const size_t need = wbytes + plan.thr_bytes;
+  if (mfma && noalloc) {
+    uint8_t *base = noalloc_scratch(ctx->device);
+    if (!base) return fail(ctx, PALQ_ERR_DEVICE, "no-alloc call: the static scratch of this device is unavailable");
+    uint8_t *wp = base;
+    int32_t *thr = (int32_t *)(base + wbytes);
+    e = launch_conv_prepare(a, wp, thr, ctx->stream);
+    if (e == hipSuccess) e = launch_conv_mfma(a, wp, thr, -1, ctx->stream);
+  } else if (mfma) {
     if (need > ctx->conv_scratch_bytes) {
       if (ctx->conv_scratch) hipFree(ctx->conv_scratch);  // waits for work still reading it
       ctx->conv_scratch = nullptr;
@@ -390,6 +408,19 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
     e = launch_conv_direct(a, ctx->stream);
   }
   return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "group conv");
+}
+}  // namespace
+
+palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
+                            int32_t pad, const palq_requant *rq, const palq_residual *res,
+                            int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump) {
+  return group_conv_impl(ctx, in, w, stride, pad, rq, res, shuffle_steps, out, acc_dump, false);
+}
+
+palq_status palq_group_conv_noalloc(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
+                                    int32_t pad, const palq_requant *rq, const palq_residual *res,
+                                    int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump) {
+  return group_conv_impl(ctx, in, w, stride, pad, rq, res, shuffle_steps, out, acc_dump, true);
 }
 
 // ------------------------------------------------------------ shuffle

@@ -102,6 +102,12 @@ int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr);
 // start and each checks on the device whether it applies (the other returns
 // at once); no host synchronisation either way.
 hipError_t launch_conv_mfma(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, int epi, hipStream_t s);
+// The static per-GPU buffer of palq_group_conv_noalloc (PALQ_NOALLOC_SCRATCH_BYTES):
+// noalloc_scratch_init looks its address up on `device` (which must be the
+// current device) once per device; noalloc_scratch returns it (nullptr if
+// the lookup failed or was not made).
+hipError_t noalloc_scratch_init(int device);
+uint8_t *noalloc_scratch(int device);
 // Kernel family launch_conv_mfma runs for the layer with epi 0 or 1 (static
 // string: "conv_tile_kernel[fp4]", "conv_tile_kernel[int8]",
 // "conv_tile_kernel[stem]", "conv_grouped_kernel" or "conv_stem_kernel").

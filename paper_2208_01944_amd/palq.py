@@ -84,6 +84,9 @@ _unpack = _sig("palq_unpack", c_i32, c_p, P_ACT, c_p)
 _quantize = _sig("palq_quantize", c_i32, c_p, c_p, c_f, c_f, P_ACT, c_p)
 _group_conv = _sig("palq_group_conv", c_i32, c_p, P_ACT, P_FIL, c_i32, c_i32,
                    ctypes.POINTER(Requant), ctypes.POINTER(Residual), c_i32, P_ACT, c_p)
+_group_conv_noalloc = _sig("palq_group_conv_noalloc", c_i32, c_p, P_ACT, P_FIL, c_i32, c_i32,
+                           ctypes.POINTER(Requant), ctypes.POINTER(Residual), c_i32, P_ACT, c_p)
+NOALLOC_SCRATCH_BYTES = 16 << 20
 _shuffle = _sig("palq_cyclic_shuffle", c_i32, c_p, P_ACT, c_i32, P_ACT)
 _channel_shuffle = _sig("palq_channel_shuffle", c_i32, c_p, P_ACT, P_ACT)
 _shuffle_module = _sig("palq_shuffle_module", c_i32, c_p, P_ACT, P_FIL, ctypes.POINTER(Requant), c_p, P_ACT)
@@ -103,7 +106,7 @@ _net_reset_times = _sig("palq_net_reset_times", c_i32, c_p)
 
 EXPORTS = ["palq_create", "palq_destroy", "palq_set_stream", "palq_set_conv_fp4", "palq_sync", "palq_last_error",
            "palq_version", "palq_row_bytes", "palq_act_bytes", "palq_pack", "palq_unpack",
-           "palq_quantize", "palq_group_conv", "palq_shuffle_module", "palq_cyclic_shuffle",
+           "palq_quantize", "palq_group_conv", "palq_group_conv_noalloc", "palq_shuffle_module", "palq_cyclic_shuffle",
            "palq_channel_shuffle", "palq_maxpool",
            "palq_avgsum", "palq_fc", "palq_net_create", "palq_net_destroy", "palq_forward",
            "palq_forward_image", "palq_net_tensor", "palq_net_ops", "palq_net_layer_kernels", "palq_net_layer_times",
@@ -186,6 +189,10 @@ class Context:
     def sync(self):
         self._check(_sync(self.h))
 
+    def set_stream(self, stream):
+        """palq_set_stream: later calls enqueue on `stream` (a torch stream)."""
+        self._check(_set_stream(self.h, stream.cuda_stream))
+
     def set_conv_fp4(self, enable: bool):
         """FP4 matrix cores for exact 2-bit layers (True) or int8 only."""
         self._check(_set_conv_fp4(self.h, int(bool(enable))))
@@ -236,7 +243,8 @@ class Context:
 
     def group_conv(self, x: Tensor, w: Filter, stride, pad, mult, shift, bias, out: Tensor,
                    shuffle=0, identity: Tensor = None, res_mult=None, proj_in: Tensor = None,
-                   proj_w: Filter = None, proj_stride=1, acc_dump=None):
+                   proj_w: Filter = None, proj_stride=1, acc_dump=None, noalloc=False):
+        """palq_group_conv (noalloc: palq_group_conv_noalloc)."""
         rq = Requant(_ptr(mult), _ptr(shift), _ptr(bias), out.act.bits)
         res = None
         if identity is not None or proj_in is not None:
@@ -248,9 +256,10 @@ class Context:
                 res.proj_in = ctypes.pointer(proj_in.act)
                 res.proj_w = ctypes.pointer(proj_w)
                 res.proj_stride = proj_stride
-        self._check(_group_conv(self.h, ctypes.byref(x.act), ctypes.byref(w), stride, pad,
-                                ctypes.byref(rq), ctypes.byref(res) if res is not None else None,
-                                shuffle, ctypes.byref(out.act), _ptr(acc_dump)))
+        fn = _group_conv_noalloc if noalloc else _group_conv
+        self._check(fn(self.h, ctypes.byref(x.act), ctypes.byref(w), stride, pad,
+                       ctypes.byref(rq), ctypes.byref(res) if res is not None else None,
+                       shuffle, ctypes.byref(out.act), _ptr(acc_dump)))
 
     def shuffle_module(self, x: Tensor, w: Filter, mult, shift, bias, res_mult, out: Tensor):
         rq = Requant(_ptr(mult), _ptr(shift), _ptr(bias), out.act.bits)

@@ -280,3 +280,23 @@ def test_validate_only_channel_shuffle(P, vctx):
     assert P._channel_shuffle(vctx.h, ctypes.byref(a), ctypes.byref(c)) == P.ERR_ARG      # bits differ
     d = _act(P, g=2, c=74, bits=3, slot=5)
     assert P._channel_shuffle(vctx.h, ctypes.byref(a), ctypes.byref(d)) == P.ERR_ARG      # grouping differs
+
+
+def test_validate_only_group_conv_noalloc(P, vctx):
+    """palq_group_conv_noalloc takes palq_group_conv's arguments and checks;
+    a layer whose prepacked filter and requant constants exceed the static
+    buffer is refused on the host (nothing enqueued)."""
+    def call(x, f, out):
+        rq = P.Requant(_fake(30), _fake(31), None, 2)
+        return P._group_conv_noalloc(vctx.h, ctypes.byref(x), ctypes.byref(f), 1, 1, ctypes.byref(rq), None, 1,
+                                     ctypes.byref(out), None)
+    assert call(_act(P), P.Filter(2, 32, 64, 3, 3, 2, _fake(10)), _act(P, c=32, slot=20)) == P.OK
+    assert call(_act(P, bits=5), P.Filter(2, 32, 64, 3, 3, 2, _fake(10)), _act(P, c=32, slot=20)) == P.ERR_ARG
+    # ResNet-18's largest 3x3 at G = 4 (512 -> 512 per group) fits: int8 + FP4 slabs of 72 K-blocks
+    big_ok = P.Filter(4, 512, 512, 3, 3, 2, _fake(10))
+    assert call(_act(P, g=4, c=512), big_ok, _act(P, g=4, c=512, slot=20)) == P.OK
+    # twice the groups does not: 8 x 512 x 72 x 96 bytes > 16 MiB
+    too_big = P.Filter(8, 512, 512, 3, 3, 2, _fake(10))
+    assert call(_act(P, g=8, c=512), too_big, _act(P, g=8, c=512, slot=20)) == P.ERR_UNSUPPORTED
+    assert "static buffer" in vctx.last_error()
+    assert P.NOALLOC_SCRATCH_BYTES == 16 << 20
