@@ -37,8 +37,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--batch", type=int, default=64, help="batch of the --table2 networks")
     ap.add_argument("--workload", default="resnet18_g4_b2",
-                    help="resnet18_g4_b2 (the default: ResNet-18 G=4 2-bit, batch 64) or "
-                         "resnet50_g2_b2 (ResNet-50 G=2 2-bit, batch 128)")
+                    help="resnet18_g4_b2 (the default: ResNet-18 G=4 2-bit, batch 64), "
+                         "resnet50_g2_b2 (ResNet-50 G=2 2-bit, batch 128), or single layers: c1, c2 "
+                         "(its four layers c2_l0..c2_l3), c4 (its nine cells c4_g<G>_b<B>) or "
+                         "layers (all of them); one JSON line per network or layer")
     ap.add_argument("--no-histograms", action="store_true",
                     help="skip the per-layer output-code histograms (an untimed extra forward)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -49,6 +51,9 @@ def parse():
                     help="only turn the rocprofv3 outputs under DIR (kt/, fetch/, write/, cfetch/, "
                          "cwrite/ and bench.json, made by the commands written into the summaries) "
                          "into the text summaries under profiles/ and exit")
+    ap.add_argument("--summarize-counters", metavar="DIR", default=None,
+                    help="only turn the SQ counter passes under DIR (p1/, p2/, p3/ and bench.json) into "
+                         "profiles/<workload>_sq_counters.md and exit")
     ap.add_argument("--table2", action="store_true",
                     help="only run the Table 2 analogue (PalQuant against the dense M-bit network and "
                          "the bit-decomposition workload, forward only, batch --batch) and exit")
@@ -59,7 +64,7 @@ def parse():
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_tile_kernel_fp4_resnet18_g4_b2_bs64_traffic.txt")
-DOMINANT = "conv_tile_kernel[fp4]"
+DOMINANT = "conv_fp4_kernel"
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2208_01944_amd", "csrc", "k_conv_mfma.hip")
 
 
@@ -101,9 +106,11 @@ def _short(name):
 
 
 def family(short):
-    """Kernel family of a demangled kernel name: the tiled convolution splits
-    by its template arguments (CB, PB, WN, WM, RB, STEM, stages, FP4) into the
-    stem, the grouped FP4 and the grouped int8 builds."""
+    """Kernel family of a demangled kernel name: the tiled convolution
+    (conv_tile_kernel) splits by its template arguments (CB, PB, WN, WM, RB,
+    STEM, stages, FP4, DUMP) into the stem, the grouped FP4 and the grouped
+    int8 builds; other kernels are their base name (conv_fp4_kernel: the
+    2-bit grouped layers on FP4 matrix cores)."""
     base = short.split("<")[0]
     if base != "conv_tile_kernel" or "<" not in short:
         return base
@@ -193,6 +200,85 @@ def summarize_profile(d, workload):
             "algorithmic_bytes_per_launch: %.0f" % rf["algorithmic_bytes_per_launch"]]
     open(TRAFFIC_FILE, "w").write("\n".join(out) + "\n")
     print("wrote", TRAFFIC_FILE)
+
+
+COUNTER_PASSES = [
+    "SQ_WAVES SQ_BUSY_CYCLES SQ_WAVE_CYCLES SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_LDS SQ_INSTS_SALU "
+    "SQ_VALU_MFMA_BUSY_CYCLES",
+    "SQ_ACTIVE_INST_LDS SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_VMEM SQ_INST_CYCLES_VMEM_RD SQ_LDS_BANK_CONFLICT "
+    "SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_WAIT_INST_LDS",
+    "GRBM_GUI_ACTIVE SQ_CYCLES SQ_ACTIVE_INST_ANY SQ_INSTS_VMEM_RD SQ_ACTIVE_INST_SCA SQ_INST_LEVEL_VMEM",
+]
+COUNTER_CMD = ("timeout -s KILL 120 rocprofv3 --pmc COUNTERS --output-format csv -d DIR/pPASS -o run -- "
+               "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-histograms")
+
+
+def summarize_counters(d, workload):
+    """Per-layer SQ counter summary of the network's conv launches (three
+    rocprofv3 --pmc passes under DIR/p1..p3 and the bench JSON DIR/bench.json)
+    written to profiles/<workload>_sq_counters.md.  Counters are summed over
+    the chip per dispatch; per-SIMD figures divide by 4 x CUs (256 CUs)."""
+    import csv
+    import hashlib
+    bench = json.loads(open(os.path.join(d, "bench.json")).read().strip().splitlines()[-1])
+    convs = [L for L in bench["layers"] if L["op"] == "conv"]
+    fams = {"stem_pool_kernel": [], DOMINANT: []}
+    for L in convs:
+        k = L["kernel"].split(" + ")[-1]
+        if k in fams:
+            fams[k].append(L)
+    vals = {}  # (family, layer index within family) -> counter -> [values]
+    for p in range(1, len(COUNTER_PASSES) + 1):
+        rows = list(csv.DictReader(open(os.path.join(d, f"p{p}", "run_counter_collection.csv"))))
+        seen = {}
+        for r in rows:
+            f = family(_short(r["Kernel_Name"]))
+            if f not in fams or not fams[f]:
+                continue
+            key = (f, int(r["Dispatch_Id"]))
+            seen.setdefault(f, {})
+            if key not in seen[f]:
+                seen[f][key] = len(seen[f])
+            idx = seen[f][key] % len(fams[f])
+            vals.setdefault((f, idx), {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    simds = 4 * 256
+    out = ["# commands (from the repository root, on one MI355X, `cd /tmp && export TMPDIR=/tmp` first; DIR any folder)"]
+    for i, c in enumerate(COUNTER_PASSES):
+        out.append("#   " + COUNTER_CMD.replace("COUNTERS", c).replace("PASS", str(i + 1)))
+    out += ["#   python3 bench.py --steps 50 --warmup 5 --no-cpu-baseline > DIR/bench.json",
+            "#   python3 bench.py --summarize-counters DIR", "",
+            "SQ counters per dispatch of the %s network's conv kernels (mean over the profiled forwards)." % workload,
+            "Per SIMD = chip total / 1024.  mfma_busy = SQ_VALU_MFMA_BUSY_CYCLES per SIMD / (layer time x clock);",
+            "valu_busy = 4 x SQ_INSTS_VALU per SIMD / the same cycles (a wave64 VALU instruction occupies a SIMD 4 cycles);",
+            "lds_conflict = SQ_LDS_BANK_CONFLICT / SQ_ACTIVE_INST_LDS; clock from GRBM_GUI_ACTIVE / 8 XCDs over the",
+            "layer's HIP-event time.", "",
+            "| layer | kernel | us | MFMA instr | VALU/MFMA | SALU/MFMA | LDS/MFMA | mfma_busy | valu_busy | "
+            "lds_conflict | wait_inst_lds/wave | clock GHz |",
+            "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for f, Ls in fams.items():
+        for i, L in enumerate(Ls):
+            v = {k: sum(x) / len(x) for k, x in vals.get((f, i), {}).items()}
+            if not v:
+                continue
+            us = L["ms"] * 1e3
+            cyc = v.get("GRBM_GUI_ACTIVE", 0) / 8
+            clock = cyc / (us * 1e3) if us else 0
+            mf = max(v.get("SQ_INSTS_MFMA", 1), 1)
+            out.append("| %d | %s | %.1f | %d | %.1f | %.1f | %.2f | %.3f | %.3f | %.3f | %.0f | %.2f |" % (
+                L["layer"], f, us, v.get("SQ_INSTS_MFMA", 0), v.get("SQ_INSTS_VALU", 0) / mf,
+                v.get("SQ_INSTS_SALU", 0) / mf, v.get("SQ_INSTS_LDS", 0) / mf,
+                v.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) / simds / max(cyc, 1),
+                4 * v.get("SQ_INSTS_VALU", 0) / simds / max(cyc, 1),
+                v.get("SQ_LDS_BANK_CONFLICT", 0) / max(v.get("SQ_ACTIVE_INST_LDS", 1), 1),
+                v.get("SQ_WAIT_INST_LDS", 0) / max(v.get("SQ_WAVES", 1), 1), clock))
+    out += ["", "raw means per dispatch (chip totals):", ""]
+    for (f, i), cv in sorted(vals.items()):
+        out.append("%s #%d: " % (f, i) + ", ".join("%s=%.0f" % (k, sum(x) / len(x)) for k, x in sorted(cv.items())))
+    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    out += ["", "kernel_source_sha256: " + src]
+    path = os.path.join(ROOT, "profiles", f"{workload}_sq_counters.md")
+    open(path, "w").write("\n".join(out) + "\n")
+    print("wrote", path)
 
 
 def copy_probe(mib):
@@ -497,6 +583,121 @@ def run_network(args, workload):
     print(json.dumps(res), flush=True)
 
 
+SINGLE_DESC = {
+    "c1": "single PalQuant 3x3 conv, batch 1, 56x56, G=2 x 64->64, 2-bit",
+    "c2_l0": "ResNet-18 stage-1 3x3 conv, batch 32, 56x56, G=4 x 64->64, 2-bit",
+    "c2_l1": "ResNet-18 stage-2 3x3 conv, batch 32, 28x28, G=4 x 128->128, 2-bit",
+    "c2_l2": "ResNet-18 stage-3 3x3 conv, batch 32, 14x14, G=4 x 256->256, 2-bit",
+    "c2_l3": "ResNet-18 stage-4 3x3 conv, batch 32, 7x7, G=4 x 512->512, 2-bit",
+}
+
+
+def oracle_layer_time(case, budget_s, single_thread):
+    """Wall time per image of the oracle on one layer (C convolution loop +
+    numpy epilogue), on whole images of the case's batch until the budget is
+    spent.  single_thread: in a child process with OMP_NUM_THREADS=1."""
+    import subprocess
+    code = (
+        "import sys, time, json; sys.path.insert(0, %r)\n"
+        "from oracle import oracle as O\n"
+        "from paper_2208_01944_amd import inputs as I\n"
+        "case = I.single_workload(%r); L = case['layer']; x = case['x']; G = L['w'].shape[0]\n"
+        "t0 = time.perf_counter(); done = 0\n"
+        "while done < x.shape[0]:\n"
+        "    acc = O.group_conv(x[done:done + 1], L['w'], L['stride'], L['pad'])\n"
+        "    O.layer_epilogue(acc, G, L['mult'], L['shift'], L['bias'], L['out_bits'], L['shuffle'])\n"
+        "    done += 1\n"
+        "    if time.perf_counter() - t0 >= %r: break\n"
+        "print(json.dumps(dict(images=done, seconds=time.perf_counter() - t0, threads=O.threads())))\n"
+    ) % (ROOT, case, budget_s)
+    env = dict(os.environ)
+    if single_thread:
+        env["OMP_NUM_THREADS"] = "1"
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, timeout=600)
+    if r.returncode != 0:
+        raise RuntimeError(r.stderr[-2000:])
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
+def run_single_layers(args, names):
+    """One JSON line per single-layer case: the planned layer (palq_conv_run)
+    timed over K runs with HIP events on the library's stream, its roofline
+    fractions and the oracle's time on the same layer."""
+    import torch
+    from paper_2208_01944_amd import inputs as I
+    from paper_2208_01944_amd import palq
+    ctx = palq.Context(0)
+    for name in names:
+        case = I.single_workload(name)
+        L = case["layer"]
+        G, co, kh, kw, ci = L["w"].shape
+        n, h, w, _ = case["x"].shape
+        ho = (h + 2 * L["pad"] - kh) // L["stride"] + 1
+        wo = (w + 2 * L["pad"] - kw) // L["stride"] + 1
+        bias = I.single_stored_bias(name)
+        i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
+        x = ctx.pack(case["x"], G, L["in_bits"])
+        wt, wf = ctx.pack_filter(L["w"], L["w_bits"])
+        out = ctx.empty_act(n, ho, wo, G, co, L["out_bits"])
+        plan = palq.ConvPlan(ctx, x, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(bias), out,
+                             shuffle=L["shuffle"])
+        for _ in range(max(args.warmup, 1)):
+            plan.run(x, out)
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        ev0.record()
+        for _ in range(args.steps):
+            plan.run(x, out)
+        ev1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        us = ev0.elapsed_time(ev1) * 1e3 / args.steps
+        codes = ctx.unpack(out)
+        hist = np.bincount(codes.reshape(-1), minlength=1 << L["out_bits"]).tolist()
+        macs = n * ho * wo * G * co * kh * kw * ci
+        ops = 2 * macs
+        nbytes = (n * h * w * G * ci * L["in_bits"] + G * co * kh * kw * ci * L["w_bits"] +
+                  n * ho * wo * G * co * L["out_bits"]) / 8 + 12 * G * co
+        kern = plan.kernels
+        fp4 = kern == DOMINANT
+        peak = FP4_MFMA_PEAK_TFLOPS if fp4 else INT8_MFMA_PEAK_TOPS
+        tops = ops / (us * 1e-6) / 1e12
+        gbs = nbytes / (us * 1e-6) / 1e9
+        res = {
+            "metric": "effective int TOPS of one PalQuant layer (palq_conv_run)",
+            "value": tops, "unit": "TOPS", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": us / 1e3, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "fp4" if fp4 else "int8",
+            "data": "synthetic (seeded uniform codes and weights; centred bias over the batch's interior positions)",
+            "config": {"workload": name, "description": SINGLE_DESC.get(name, f"ResNet-18 stage-3 3x3 conv, batch 128, "
+                                                                             f"14x14, G={G} x 256->256, {L['in_bits']}-bit"),
+                       "batch": n, "groups": G, "bits": L["in_bits"], "ci": ci, "co": co, "hw": h},
+            "us_per_launch": us, "wall_us_per_launch": wall * 1e6 / args.steps, "kernel": kern,
+            "int_ops": ops, "algorithmic_bytes": nbytes,
+            "roofline": {"bound": "mfma", "achieved": tops, "peak": peak, "unit": "TFLOP/s" if fp4 else "TOP/s",
+                         "frac": tops / peak, "traffic": None,
+                         "hbm_gbs": gbs, "hbm_frac": gbs / HBM_PEAK_GBS,
+                         "arithmetic_intensity": ops / nbytes},
+            "code_histogram": hist,
+        }
+        if not args.no_cpu_baseline:
+            nproc, model = host_cpu()
+            cb = {}
+            for st in (False, True):
+                if st and name.startswith("c4_g") and not name.startswith("c4_g1_b2"):
+                    continue  # single-thread figures for C1, C2 and the G=1, b=2 sweep cell
+                r = oracle_layer_time(name, args.cpu_seconds / 2, st)
+                per = r["seconds"] / r["images"]
+                cb["single_thread" if st else "all_threads"] = {
+                    "value": macs * 2 / n / per / 1e9, "unit": "G int ops/s", "cores": r["threads"],
+                    "us_per_batch": per * n * 1e6, "sample": f"{r['images']} of {n} images, {r['seconds']:.1f} s"}
+            res["cpu_baseline"] = dict(cb["all_threads"], kind="oracle", nproc=nproc, cpu_model=model,
+                                       single_thread=cb.get("single_thread"))
+        print(json.dumps(res), flush=True)
+        del plan
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -506,6 +707,9 @@ def main():
     if args.summarize_profile:
         summarize_profile(args.summarize_profile, args.workload)
         return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, args.workload)
+        return
     if args.hbm_copy_probe:
         copy_probe(args.hbm_copy_probe)
         return
@@ -514,6 +718,14 @@ def main():
         return
     if args.workload in NETWORKS:
         run_network(args, args.workload)
+        return
+    from paper_2208_01944_amd import inputs as I
+    if args.workload == "layers":
+        run_single_layers(args, I.SINGLE_WORKLOADS)
+        return
+    if args.workload in I.SINGLE_WORKLOADS or args.workload in ("c2", "c4"):
+        names = [w for w in I.SINGLE_WORKLOADS if w == args.workload or w.startswith(args.workload + "_")]
+        run_single_layers(args, names)
         return
     raise SystemExit(f"unknown workload {args.workload}")
 

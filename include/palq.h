@@ -119,6 +119,9 @@ typedef struct {
  * Returns PALQ_ERR_DEVICE when the device cannot be used. */
 palq_status palq_create(int32_t device, void *hip_stream, palq_ctx **out);
 void palq_destroy(palq_ctx *ctx);
+/* Later calls enqueue on hip_stream.  The new stream first waits for the
+ * work already queued on the old one (which may still read context memory
+ * that later calls reuse). */
 palq_status palq_set_stream(palq_ctx *ctx, void *hip_stream);
 /* Matrix-core format of 2-bit grouped convolutions (Section 4.1): with
  * enable = 1 (the default; environment PALQ_CONV_FP4=0 starts a context at
@@ -177,7 +180,10 @@ palq_status palq_quantize(palq_ctx *ctx, const float *x, float l, float u, const
  *         the permuted main accumulator plus any projection accumulator).
  * PALQ_ERR_OVERFLOW when K*max|code|*max|weight| (K = kh*kw*cin_pg), plus
  * the same bound of the projection product, reaches 2^26.  out must not
- * overlap any input. */
+ * overlap any input.  Every call prepacks the filter again, into context
+ * memory that it grows (allocating) when a call needs more than any before;
+ * it never synchronises.  A loop over one layer plans it once instead
+ * (palq_conv_plan_create) and runs the plan (palq_conv_run). */
 palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
                             int32_t pad, const palq_requant *rq, const palq_residual *res,
                             int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump);
@@ -198,6 +204,40 @@ palq_status palq_group_conv(palq_ctx *ctx, const palq_act *in, const palq_filter
 palq_status palq_group_conv_noalloc(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
                                     int32_t pad, const palq_requant *rq, const palq_residual *res,
                                     int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump);
+
+/* A planned layer: the filter, the requant and shortcut parameters of one
+ * palq_group_conv layer, prepacked into the matrix-core operand order with
+ * its requant constants and its kernel chosen, once, for repeated runs. */
+typedef struct palq_conv_plan palq_conv_plan;
+
+/* Plans the layer palq_group_conv computes (same arguments and checks,
+ * Section 4.1 / Eq. 1 per group, Eq. 8 as the write address): copies w,
+ * rq's arrays, res->res_mult and res->proj_w into device memory the plan
+ * owns, prepacks the filter, computes the requant constants and reads back
+ * which epilogue applies (this call synchronises the context's stream once).
+ * Only the shapes, bits and signs of in, out, res->identity and res->proj_in
+ * are used; their data pointers are ignored.  The caller may free the
+ * parameter arrays once this returns.  A validate-only context returns a
+ * plan that runs nothing.  Errors as palq_group_conv; PALQ_ERR_NOMEM. */
+palq_status palq_conv_plan_create(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
+                                  int32_t pad, const palq_requant *rq, const palq_residual *res,
+                                  int32_t shuffle_steps, const palq_act *out, palq_conv_plan **plan);
+/* Runs a plan on device tensors of the planned shapes: in, out, res_in (the
+ * identity shortcut's codes or the projection input, as planned; NULL when
+ * the plan has no shortcut) and acc_dump (nullable; as in palq_group_conv),
+ * all 16-byte aligned.  Enqueues the planned kernels on the context's
+ * stream and nothing else: no allocation, no synchronisation, no host copy,
+ * so it may be captured into a HIP graph.  PALQ_ERR_ARG for a plan of
+ * another context, null, misaligned or overlapping pointers, or a shortcut
+ * input that does not match the plan. */
+palq_status palq_conv_run(palq_ctx *ctx, const palq_conv_plan *plan, const void *in, const void *res_in, void *out,
+                          int32_t *acc_dump);
+/* Frees a plan (waits for device work that still reads it). */
+void palq_conv_plan_destroy(palq_conv_plan *plan);
+/* The kernel family a plan runs without an accumulator dump (static host
+ * string, e.g. "conv_tile_kernel[fp4]"; "" for a validate-only plan; NULL
+ * for a null plan). */
+const char *palq_conv_plan_kernels(const palq_conv_plan *plan);
 
 /* The cyclic permutation of Section 4.2 (Eq. 6-8) on its own:
  * out[pixel, (g + steps) mod G, :] = in[pixel, g, :], any integer steps.

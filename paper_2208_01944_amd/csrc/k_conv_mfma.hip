@@ -1800,6 +1800,293 @@ __global__ __launch_bounds__(sp::NT, 3) void stem_pool_kernel(ConvArgs a, Geo ge
   }
 }
 
+// ---------------------------------------------------------------- FP4 grouped kernel
+// 2-bit grouped layers on the FP4 (E2M1) matrix cores, one workgroup per
+// tile.  A tile is TN = WN CB 32 output channels x TM = WM PB 32 output
+// pixels of one group; wave (wn, wm) owns CB x PB blocks of 32 x 32.  Per
+// 64-code K-block the workgroup stages TN / 32 FP4 weight slabs (1 KB each,
+// prepack_fp4_kernel) and the TM pixels' packed codes (16 bytes each) in a
+// ring of S LDS stages with buffer_load ... lds, S - 1 K-blocks ahead of the
+// MFMAs (one barrier per K-block).  Per K-block a lane's fetch offsets change
+// only through the scalar offset (K-block within the tap, weight slab step);
+// the per-lane activation offset and its in-image test are redone when the
+// tap changes.  The K-blocks of a fused projection follow the main ones.
+// Tiles are dealt in XCD-contiguous runs (workgroup i runs on XCD i mod 8),
+// in the chunked order of tile_at, so an XCD's L2 holds the input lines its
+// in-flight tiles share.  Epilogue: epilogue_fast_bo (fp64-exact requant);
+// a layer whose requant needs the int64 path leaves at once (its general
+// partner runs instead).  DUMP: also write the int32 accumulators.
+// A value the compiler is told is the same in every lane of the wave.
+__device__ __forceinline__ int uniform_int(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+namespace f4 {
+template <int CB, int PB, int WN, int WM>
+struct Cfg {
+  static constexpr int NT = WN * WM * 64;
+  static constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
+  static constexpr int WST = TN / 32 * kSlab4;  // weight bytes of a K-block
+  static constexpr int XST = TM * 16;           // activation bytes of a K-block
+  static constexpr int SST = WST + XST;
+  static constexpr int WP = WST / 16, XP = XST / 16;  // 16-byte pieces
+  static_assert(WP % 64 == 0 && XP % 64 == 0 && WP <= 2 * NT && XP <= 2 * NT, "whole waves of pieces");
+  static constexpr int WL = WP > NT ? 2 : 1, XL = XP > NT ? 2 : 1;  // loads per loading thread
+  // loads per K-block of the waves with the fewest (the ring waits on that)
+  static constexpr int LPK = (WP >= NT ? WL : 0) + (XP >= NT ? XL : 0) > 0 ? (WP >= NT ? WL : 0) + (XP >= NT ? XL : 0) : 1;
+  static constexpr int RPX = TN / 4;          // shortcut code bytes per pixel
+  static constexpr int RSB = TM * RPX;        // shortcut codes of a tile
+};
+}  // namespace f4
+
+template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S>
+__global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, Geo geo, int npt, int ncb, int nch) {
+  using C = f4::Cfg<CB, PB, WN, WM>;
+  constexpr int NT = C::NT, TN = C::TN, TM = C::TM, WST = C::WST, SST = C::SST;
+  constexpr int RPT = RB ? C::RSB / (NT * 16) : 0;  // 16-byte shortcut pieces per thread
+  static_assert(RB == 0 || RPT * NT * 16 == C::RSB, "whole shortcut pieces per thread");
+  static_assert(CB == 2 && (PB == 2 || PB == 4), "operand reads are written for 2 x 2 and 2 x 4 blocks");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[S * SST + (RB ? C::RSB : 16)];
+  __shared__ RqConst rq_area[TN];
+  __shared__ int32_t rm_area[RB ? TN : 1];
+
+  // the launcher takes 2-bit outputs and 2-bit (or no) shortcuts only; a
+  // layer whose fp64 requant could be inexact runs on the general partner
+  if (int64_flag(a, geo) || a.out.bits != 2 || RB < 0) return;
+  const int G = a.in.groups;
+  const int T = npt * ncb * G;
+  // workgroup i -> XCD x = i mod 8, which takes the x-th eighth of the tiles
+  const int x8 = (int)(blockIdx.x & 7), j = (int)(blockIdx.x >> 3);
+  const int Tq = T >> 3, Tr = T & 7;
+  if (j >= Tq + (x8 < Tr ? 1 : 0)) return;  // no barrier yet
+  const int t = x8 * Tq + min(x8, Tr) + j;
+  const TileIt it = tile_at(t, npt, ncb * G, nch);
+  const int pt = it.pt, cbk = it.combo % ncb, g = it.combo / ncb;
+  const int gd = (g + a.shuffle) % G;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = uniform_int(tid >> 6);  // LDS destinations in scalar registers
+  const int l32 = lane & 31, half = lane >> 5;
+  const int wn = wave / WM, wm = wave % WM;
+  const int KB = geo.kb_total, KM = geo.kb_main;
+
+  // requant constants (and shortcut multipliers) of the tile's TN channels
+  const int64_t ch0 = (int64_t)g * a.cout + cbk * TN;
+  for (int c = tid; c < TN; c += NT) {
+    rq_area[c] = geo.rq[ch0 + c];
+    if constexpr (RB != 0) rm_area[c] = a.res_mult[ch0 + c];
+  }
+  typedef __attribute__((address_space(3))) void *lds_ptr;
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
+
+  const auto rw_src = make_rsrc(geo.wp, (int64_t)G * a.cout * KB * (kSlab4 / 32));
+  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
+  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, (int64_t)a.proj.n * a.proj.h * a.proj.w * a.proj.pixel)
+                               : make_rsrc(a.in.data, 0);
+  const auto rres = make_rsrc(a.res.data, a.res.data ? (int64_t)a.res.n * a.res.h * a.res.w * a.res.pixel : 0);
+  const int pixb = (int)a.in.pixel, rowb = a.in.w * pixb;
+
+  // ---- this thread's fetch pieces.  Weights: piece c = tid - (NT - WP)
+  // (+ NT) of the tile's slabs: slab c / 64, lane operand c % 64.
+  // Activations: piece tid (+ NT) = pixel tid (+ NT) of the tile.
+  const bool wload = C::WP >= NT || tid >= NT - C::WP;  // wave-uniform
+  const int wc = C::WP >= NT ? tid : tid - (NT - C::WP);
+  uint32_t woff[C::WL];
+#pragma unroll
+  for (int i = 0; i < C::WL; ++i) {
+    const int c = wc + i * NT;
+    woff[i] = (uint32_t)((((int64_t)g * (a.cout / 32) + cbk * (TN / 32) + (c >> 6)) * KB) * kSlab4 + (c & 63) * 16);
+  }
+  const bool xload = C::XP >= NT || tid < C::XP;  // wave-uniform
+  const int HW = a.ho * a.wo;
+  const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
+  int off0[C::XL], poff[C::XL];
+  uint32_t tmask[C::XL];
+#pragma unroll
+  for (int i = 0; i < C::XL; ++i) {
+    const int m = pt * TM + tid + i * NT;
+    const bool valid = m < geo.M;
+    const int mm = valid ? m : 0;
+    const int n = fdiv(mm, HW, inv_hw);
+    const int rem = mm - n * HW;
+    const int oy = fdiv(rem, a.wo, inv_wo);
+    const int ox = rem - oy * a.wo;
+    const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
+    off0[i] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.row;
+    const int xlo = max(0, -ix0), xhi = min(a.kw, a.in.w - ix0);
+    const uint32_t below = xhi >= 32 ? 0xffffffffu : ((1u << max(xhi, 0)) - 1u);
+    const uint32_t cols = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
+    const int ylo = max(0, -iy0), yhi = min(a.kh, a.in.h - iy0);
+    uint32_t mk = 0;
+    for (int ky = ylo; ky < yhi; ++ky) mk |= cols << (ky * a.kw);
+    tmask[i] = valid ? mk : 0u;
+    poff[i] = (a.proj.data && valid)
+                  ? (((n * a.proj.h + oy * a.proj_stride) * a.proj.w + ox * a.proj_stride) * (int)a.proj.pixel +
+                     gd * (int)a.proj.row)
+                  : (int)kOob;
+  }
+  // fetch cursor: K-block f_kb = tap f_tap, block f_c of it; vo: the
+  // activation pieces' offsets for the current tap (kOob if outside)
+  int f_kb = 0, f_c = 0, f_tap = 0, f_kx = 0, f_tapoff = 0;
+  uint32_t vo[C::XL];
+  auto tap_offsets = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < C::XL; ++i) vo[i] = ((tmask[i] >> f_tap) & 1u) ? (uint32_t)(off0[i] + f_tapoff) : kOob;
+  };
+  tap_offsets();
+  auto fetch = [&](int st) __attribute__((always_inline)) {
+    uint8_t *ws = lds + st * SST;
+    if constexpr (RB == 2) {
+      if (f_kb == 0) {  // the tile's shortcut codes, RPT pieces per thread (before K-block 0's loads)
+#pragma unroll
+        for (int i = 0; i < RPT; ++i) {
+          const int c = tid + i * NT;
+          const int m = pt * TM + c / (C::RPX / 16);
+          const uint32_t ro = m < geo.M ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.row + cbk * C::RPX +
+                                                     (c % (C::RPX / 16)) * 16)
+                                        : kOob;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(lds + S * SST + i * NT * 16 + wave * 1024), 16,
+                                                   (int)ro, 0, 0, 0);
+        }
+      }
+    }
+    if (wload) {
+#pragma unroll
+      for (int i = 0; i < C::WL; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + ((wc + i * NT) & ~63) * 16), 16, (int)woff[i],
+                                                 f_kb * kSlab4, 0, 0);
+    }
+    if (xload) {
+      if (f_kb < KM) {
+#pragma unroll
+        for (int i = 0; i < C::XL; ++i)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rin, (lds_ptr)(ws + WST + i * NT * 16 + wave * 1024), 16, (int)vo[i],
+                                                   f_c * 16, 0, 0);
+      } else {
+#pragma unroll
+        for (int i = 0; i < C::XL; ++i)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rpj, (lds_ptr)(ws + WST + i * NT * 16 + wave * 1024), 16,
+                                                   (int)poff[i], (f_kb - KM) * 16, 0, 0);
+      }
+    }
+    ++f_kb;
+    if (++f_c == geo.cpb) {  // next tap
+      f_c = 0;
+      ++f_tap;
+      f_tapoff += pixb;
+      if (++f_kx == a.kw) {
+        f_kx = 0;
+        f_tapoff += rowb - a.kw * pixb;
+      }
+      tap_offsets();
+    }
+  };
+
+  // ---- compute side
+  v16f acc[CB][PB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0.f;
+  // LDS addresses of this lane's operands in stage 0: activation half row of
+  // pixel block 0 (blocks 512 bytes apart), weight unit of channel block 0
+  // (blocks 1 KB apart)
+  const uint32_t xaddr0 = lds_base + WST + (uint32_t)((wm * PB * 32 + l32) * 16 + half * 8);
+  const uint32_t aaddr0 = lds_base + (uint32_t)((wn * CB) * kSlab4 + (half * 32 + l32) * 16);
+  auto kblock = [&](int st) __attribute__((always_inline)) {
+    const uint32_t xa = xaddr0 + st * SST, aa = aaddr0 + st * SST;
+    uint2 xw[PB];
+    v4i A0, A1;
+    if constexpr (PB == 4) {
+      asm volatile(
+          "ds_read_b64 %0, %6\n\t"
+          "ds_read_b64 %1, %6 offset:512\n\t"
+          "ds_read_b64 %2, %6 offset:1024\n\t"
+          "ds_read_b64 %3, %6 offset:1536\n\t"
+          "ds_read_b128 %4, %7\n\t"
+          "ds_read_b128 %5, %7 offset:1024\n\t"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(xw[0]), "=&v"(xw[1]), "=&v"(xw[2]), "=&v"(xw[3]), "=&v"(A0), "=&v"(A1)
+          : "v"(xa), "v"(aa));
+    } else {
+      asm volatile(
+          "ds_read_b64 %0, %4\n\t"
+          "ds_read_b64 %1, %4 offset:512\n\t"
+          "ds_read_b128 %2, %5\n\t"
+          "ds_read_b128 %3, %5 offset:1024\n\t"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(xw[0]), "=&v"(xw[1]), "=&v"(A0), "=&v"(A1)
+          : "v"(xa), "v"(aa));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // E2M1 operands use the low four registers of each v8i (the rest is
+    // ignored for this format)
+    const v8i Aop[CB] = {__builtin_shufflevector(A0, A0, 0, 1, 2, 3, -1, -1, -1, -1),
+                         __builtin_shufflevector(A1, A1, 0, 1, 2, 3, -1, -1, -1, -1)};
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const uint32_t m = 0x33333333u;
+      const v4i b = {(int)(xw[pb].x & m), (int)((xw[pb].x >> 2) & m), (int)(xw[pb].y & m), (int)((xw[pb].y >> 2) & m)};
+      const v8i Bop = __builtin_shufflevector(b, b, 0, 1, 2, 3, -1, -1, -1, -1);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+        acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop[cb], Bop, acc[cb][pb], 4, 4, 0, 0, 0, 0);
+    }
+  };
+
+  __syncthreads();  // the tile's constants are in LDS
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st)
+    if (st < KB) fetch(st);
+  // steady state: K-block kb's loads were issued S - 1 fetches ago; at most
+  // (S - 2) LPK of this wave's loads are younger
+  int kb = 0;
+  for (; kb + S - 1 < KB; ++kb) {
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((S - 2) * C::LPK));
+    ring_barrier();
+    fetch((kb + S - 1) % S);
+    kblock(kb % S);
+  }
+  // the last S - 1 K-blocks: no more fetches, the waits tighten
+#pragma unroll
+  for (int i = 0; i < S - 1; ++i) {
+    if (kb >= KB) break;  // uniform (KB < S - 1)
+    if (KB - 1 - kb >= 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * C::LPK));
+    else if (KB - 1 - kb == 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::LPK));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    ring_barrier();
+    kblock(kb % S);
+    ++kb;
+  }
+
+  // ---- epilogue
+  const int64_t mbase = (int64_t)pt * TM + wm * PB * 32;
+  if constexpr (DUMP) {
+    const int64_t outC = (int64_t)G * a.cout;
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        const int64_t mp = mbase + pb * 32 + l32;
+        if (mp >= geo.M) continue;
+        int32_t *dst = a.acc_dump + mp * outC + (int64_t)gd * a.cout + cbk * TN + wn * CB * 32 + cb * 32 + 4 * half;
+#pragma unroll
+        for (int qi = 0; qi < 4; ++qi) {
+          v4i dv;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dv[e] = (int)(acc[cb][pb][4 * qi + e] * 4.0f);  // exact: |4 acc| < 2^23
+          *(v4i *)(dst + 8 * qi) = dv;
+        }
+      }
+  }
+  // this lane's shortcut codes: pixel block pb, channel block cb at
+  // ra + pb 32 RPX + 8 cb (read per channel block by the epilogue)
+  const uint32_t ra = RB == 2 ? lds_base + S * SST + (uint32_t)((wm * PB * 32 + l32) * C::RPX + wn * CB * 8) : 0u;
+  uint32_t rw[CB][PB][2] = {};
+  epilogue_fast_bo<2, CB, PB, RB, v16f, true>(a, geo, acc, rw, mbase, g, gd, cbk * TN + wn * CB * 32, l32, half,
+                                                rq_area + wn * CB * 32, rm_area + (RB ? wn * CB * 32 : 0), ra,
+                                                32 * C::RPX);
+}
+
 // ---------------------------------------------------------------- launch
 bool is_stem(const ConvArgs &a) {
   return a.in.bits == 8 && a.in.is_signed && a.w_bits == 8 && a.in.row == 4 && a.kw <= 8 &&
@@ -2083,6 +2370,32 @@ ConvChoice conv_choice(const ConvArgs &a, const Geo &geo, int epi) {
   return c;
 }
 
+// The FP4 grouped kernel: one workgroup per tile, XCD-contiguous runs of the
+// chunked tile order (32 chunks where the packed input outweighs the filter,
+// as in launch_tile).
+template <int CB, int PB, int WN, int WM>
+hipError_t launch_fp4(const ConvArgs &a, const Geo &geo, hipStream_t s) {
+  constexpr int S = 4;
+  using C = f4::Cfg<CB, PB, WN, WM>;
+  const int npt = (int)((geo.M + C::TM - 1) / C::TM);
+  const int ncb = a.cout / C::TN;
+  const int64_t T = (int64_t)npt * ncb * a.in.groups;
+  if (T <= 0 || T > 0x3fffffff || geo.kb_total < 1) return hipErrorInvalidValue;
+  const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * 32;
+  const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
+  const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(32, npt) : 1;
+  const dim3 grid((unsigned)((T + 7) / 8 * 8)), block(C::NT);
+  if (!a.res.data && !a.acc_dump)
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, false, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+  else if (!a.acc_dump)
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, false, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+  else if (!a.res.data)
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, true, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+  else
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, true, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+  return hipGetLastError();
+}
+
 template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES, bool FP4 = false>
 hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   if (geo.kb_total < S) return hipErrorInvalidValue;
@@ -2161,7 +2474,7 @@ const char *conv_kernel_label(const ConvArgs &a, int epi) {
   const Geo geo = make_geo(a);
   switch (conv_choice(a, geo, epi).tile) {
     case kTileStem: return "conv_tile_kernel[stem]";
-    case kTileFp4C64: case kTileFp4C128: case kTileFp4C128P4: return "conv_tile_kernel[fp4]";
+    case kTileFp4C64: case kTileFp4C128: case kTileFp4C128P4: return "conv_fp4_kernel";
     case kTileI8C64: case kTileI8C128: return "conv_tile_kernel[int8]";
     default: return is_stem(a) ? "conv_stem_kernel" : "conv_grouped_kernel";
   }
@@ -2176,6 +2489,7 @@ hipError_t launch_conv_mfma(const ConvArgs &a_in, const uint8_t *wp, const int32
   geo.rq = (const RqConst *)thr;
   const ConvChoice c = conv_choice(a, geo, epi);
   if (c.cb == 0 && c.tile == kTileNone) return hipErrorNotSupported;  // no build for this layer
+  if (a.acc_dump && c.tile == kTileNone) epi = 1;  // only the general persistent build dumps
   hipError_t e = hipSuccess;
   const int nch = a.in.groups * a.cout;
   Geo g4 = geo;  // FP4 slabs and constants follow the int8 ones
@@ -2184,9 +2498,9 @@ hipError_t launch_conv_mfma(const ConvArgs &a_in, const uint8_t *wp, const int32
   constexpr int S4 = PALQ_TILE_STAGES;
   switch (c.tile) {
     case kTileStem: e = launch_tile<2, 2, 2, 2, true, PALQ_STEM_STAGES>(a, geo, s); break;
-    case kTileFp4C64: e = launch_tile<2, 2, 1, 4, false, S4, true>(a, g4, s); break;
-    case kTileFp4C128: e = launch_tile<2, 2, 2, 2, false, S4, true>(a, g4, s); break;
-    case kTileFp4C128P4: e = launch_tile<2, 4, 2, 2, false, S4, true>(a, g4, s); break;
+    case kTileFp4C64: e = launch_fp4<2, 2, 1, 4>(a, g4, s); break;
+    case kTileFp4C128: e = launch_fp4<2, 2, 2, 2>(a, g4, s); break;
+    case kTileFp4C128P4: e = launch_fp4<2, 4, 2, 2>(a, g4, s); break;
     case kTileI8C64: e = launch_tile<2, 2, 1, 4>(a, geo, s); break;
     case kTileI8C128: e = launch_tile<2, 2, 2, 4>(a, geo, s); break;
     default: break;

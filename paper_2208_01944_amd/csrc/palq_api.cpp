@@ -6,6 +6,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <string>
 
@@ -116,7 +117,9 @@ palq_status palq_create(int32_t device, void *hip_stream, palq_ctx **out) {
     // up once per device (a failure only disables palq_group_conv_noalloc)
     if (e == hipSuccess) noalloc_scratch_init(device);
     if (e == hipSuccess) e = hipMalloc(&ctx->range_scratch, 2 * sizeof(float));
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&ctx->order_event, hipEventDisableTiming);
     if (e != hipSuccess) {
+      if (ctx->range_scratch) hipFree(ctx->range_scratch);
       delete ctx;
       return PALQ_ERR_DEVICE;
     }
@@ -133,13 +136,24 @@ void palq_destroy(palq_ctx *ctx) {
     if (ctx->conv_scratch) hipFree(ctx->conv_scratch);
     if (ctx->fc_scratch) hipFree(ctx->fc_scratch);
     if (ctx->mod_scratch) hipFree(ctx->mod_scratch);
+    if (ctx->order_event) hipEventDestroy(ctx->order_event);
   }
   delete ctx;
 }
 
 palq_status palq_set_stream(palq_ctx *ctx, void *hip_stream) {
   if (!ctx) return PALQ_ERR_ARG;
-  ctx->stream = (hipStream_t)hip_stream;
+  const hipStream_t ns = (hipStream_t)hip_stream;
+  if (ctx->device >= 0 && ns != ctx->stream) {
+    // work still queued on the old stream may read the context's scratch
+    // (prepacked filters, parameters) that the next call on the new stream
+    // overwrites: the new stream waits for everything queued so far
+    hipSetDevice(ctx->device);
+    hipError_t e = hipEventRecord(ctx->order_event, ctx->stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(ns, ctx->order_event, 0);
+    if (e != hipSuccess) return device_fail(ctx, e, "set stream");
+  }
+  ctx->stream = ns;
   return PALQ_OK;
 }
 
@@ -421,6 +435,161 @@ palq_status palq_group_conv_noalloc(palq_ctx *ctx, const palq_act *in, const pal
                                     int32_t pad, const palq_requant *rq, const palq_residual *res,
                                     int32_t shuffle_steps, const palq_act *out, int32_t *acc_dump) {
   return group_conv_impl(ctx, in, w, stride, pad, rq, res, shuffle_steps, out, acc_dump, true);
+}
+
+// ------------------------------------------------------------ planned layers
+namespace {
+void *plan_fake(uintptr_t slot) { return (void *)(uintptr_t)(0x100000000ull * (slot + 1)); }
+
+void free_plan(palq_conv_plan *p) {
+  if (!p) return;
+  if (p->mem && p->ctx && p->ctx->device >= 0) {
+    hipSetDevice(p->ctx->device);
+    hipFree(p->mem);  // waits for work still reading it
+  }
+  delete p;
+}
+}  // namespace
+
+palq_status palq_conv_plan_create(palq_ctx *ctx, const palq_act *in, const palq_filter *w, int32_t stride,
+                                  int32_t pad, const palq_requant *rq, const palq_residual *res,
+                                  int32_t shuffle_steps, const palq_act *out, palq_conv_plan **plan) {
+  if (!ctx || !plan) return PALQ_ERR_ARG;
+  *plan = nullptr;
+  if (!in || !out) return fail(ctx, PALQ_ERR_ARG, "plan: null descriptor");
+  // the layer's checks on stand-in tensor addresses (their data pointers are
+  // ignored); the filter, requant and shortcut-scale pointers are the real ones
+  palq_act fi = *in, fo = *out, fr{}, fp{};
+  fi.data = plan_fake(1);
+  fo.data = plan_fake(1000);
+  palq_residual fres{};
+  const palq_residual *resp = nullptr;
+  if (res) {
+    fres = *res;
+    if (res->identity) { fr = *res->identity; fr.data = plan_fake(2000); fres.identity = &fr; }
+    if (res->proj_in) { fp = *res->proj_in; fp.data = plan_fake(3000); fres.proj_in = &fp; }
+    resp = &fres;
+  }
+  {
+    palq_ctx vctx;
+    vctx.device = -1;
+    const palq_status st = palq_group_conv(&vctx, &fi, w, stride, pad, rq, resp, shuffle_steps, &fo, nullptr);
+    if (st != PALQ_OK) return fail(ctx, st, "plan: " + vctx.err);
+  }
+  palq_conv_plan *p = new (std::nothrow) palq_conv_plan();
+  if (!p) return fail(ctx, PALQ_ERR_NOMEM, "plan");
+  p->ctx = ctx;
+  const int G = w->groups;
+  const int64_t nch = (int64_t)G * w->cout_pg;
+  ConvArgs &a = p->a;
+  a.in = view_of(&fi);
+  a.out = view_of(&fo);
+  a.in.data = a.out.data = nullptr;
+  a.cout = w->cout_pg; a.kh = w->kh; a.kw = w->kw; a.stride = stride; a.pad = pad;
+  a.w_bits = w->bits;
+  a.ho = out->h; a.wo = out->w;
+  a.shuffle = (int32_t)(((int64_t)shuffle_steps % G + G) % G);
+  a.fp4 = ctx->conv_fp4;
+  p->in_bytes = palq_act_bytes(in);
+  p->out_bytes = palq_act_bytes(out);
+  p->dump_bytes = (int64_t)out->n * out->h * out->w * nch * 4;
+  if (res && res->identity) { a.res = view_of(&fr); a.res.data = nullptr; p->res_kind = 1; p->res_bytes = palq_act_bytes(&fr); }
+  if (res && res->proj_in) {
+    a.proj = view_of(&fp); a.proj.data = nullptr; a.proj_stride = res->proj_stride;
+    p->res_kind = 2; p->res_bytes = palq_act_bytes(&fp);
+  }
+  if (ctx->device < 0) {  // validate only: nothing to prepare
+    *plan = p;
+    return PALQ_OK;
+  }
+  // own copies of the parameters (the caller may free theirs), then the
+  // prepacked filter and requant constants
+  auto up = [](int64_t b) { return (b + 255) & ~(int64_t)255; };
+  const int64_t wb = filter_bytes(w), cb = nch * 4;
+  const int64_t pwb = (res && res->proj_w) ? filter_bytes(res->proj_w) : 0;
+  int64_t off = 0;
+  const int64_t o_w = off; off += up(wb);
+  const int64_t o_pw = off; off += up(pwb);
+  const int64_t o_m = off; off += up(cb);
+  const int64_t o_s = off; off += up(cb);
+  const int64_t o_b = off; off += up(cb);
+  const int64_t o_r = off; off += up(cb);
+  a.in.data = (uint8_t *)plan_fake(1);  // for the kernel choice only: no device access
+  a.out.data = (uint8_t *)plan_fake(1000);
+  if (a.res.cpg) a.res.data = (uint8_t *)plan_fake(2000);
+  if (a.proj.cpg) a.proj.data = (uint8_t *)plan_fake(3000);
+  a.proj_w = pwb ? (const uint8_t *)plan_fake(4000) : nullptr;
+  p->mfma = conv_mfma_supported(a);
+  const ConvPlan cp = p->mfma ? conv_mfma_plan(a) : ConvPlan{0, 0};
+  const int64_t o_wp = off; off += up((int64_t)cp.w_bytes);
+  const int64_t o_thr = off; off += up((int64_t)cp.thr_bytes);
+  hipSetDevice(ctx->device);
+  hipError_t e = hipMalloc(&p->mem, (size_t)std::max<int64_t>(off, 256));
+  if (e != hipSuccess) { free_plan(p); return fail(ctx, PALQ_ERR_NOMEM, "plan: device memory"); }
+  uint8_t *m = (uint8_t *)p->mem;
+  auto cp_ = [&](int64_t o, const void *src, int64_t bytes) {
+    if (e == hipSuccess && src && bytes > 0) e = hipMemcpyAsync(m + o, src, bytes, hipMemcpyDefault, ctx->stream);
+    return src ? m + o : nullptr;
+  };
+  a.w = cp_(o_w, w->data, wb);
+  a.proj_w = pwb ? cp_(o_pw, res->proj_w->data, pwb) : nullptr;
+  a.mult = (const int32_t *)cp_(o_m, rq->mult, cb);
+  a.shift = (const int32_t *)cp_(o_s, rq->shift, cb);
+  a.bias = (const int32_t *)cp_(o_b, rq->bias, cb);
+  a.res_mult = (res && res->identity) ? (const int32_t *)cp_(o_r, res->res_mult, cb) : nullptr;
+  if (p->mfma) {
+    p->wp = m + o_wp;
+    p->thr = (int32_t *)(m + o_thr);
+    if (e == hipSuccess) e = launch_conv_prepare(a, p->wp, p->thr, ctx->stream);
+  }
+  if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) { free_plan(p); return device_fail(ctx, e, "plan: parameters"); }
+  if (p->mfma) {
+    p->epi = conv_mfma_epilogue(a, p->thr);
+    if (p->epi < 0) { free_plan(p); return fail(ctx, PALQ_ERR_DEVICE, "plan: requant flag"); }
+    // a layer too long for the general build's LDS runs its general
+    // epilogue on the direct kernel
+    if (p->epi == 1 && !conv_mfma_general_fits(a)) p->mfma = false;
+  }
+  a.in.data = a.out.data = a.res.data = a.proj.data = nullptr;
+  *plan = p;
+  return PALQ_OK;
+}
+
+palq_status palq_conv_run(palq_ctx *ctx, const palq_conv_plan *plan, const void *in, const void *res_in, void *out,
+                          int32_t *acc_dump) {
+  if (!ctx || !plan) return PALQ_ERR_ARG;
+  if (plan->ctx != ctx) return fail(ctx, PALQ_ERR_ARG, "plan belongs to another context");
+  const bool work = plan->a.out.n > 0;
+  if (work && (!in || !out)) return fail(ctx, PALQ_ERR_ARG, "null input or output");
+  if (((uintptr_t)in | (uintptr_t)out | (uintptr_t)res_in | (uintptr_t)acc_dump) & 15u)
+    return fail(ctx, PALQ_ERR_ARG, "tensors must be 16-byte aligned");
+  if (plan->res_kind && work && !res_in) return fail(ctx, PALQ_ERR_ARG, "the plan's shortcut input is missing");
+  if (!plan->res_kind && res_in) return fail(ctx, PALQ_ERR_ARG, "the plan has no shortcut input");
+  if (overlaps(out, plan->out_bytes, in, plan->in_bytes) || overlaps(out, plan->out_bytes, res_in, plan->res_bytes))
+    return fail(ctx, PALQ_ERR_ARG, "output overlaps an input");
+  if (acc_dump && (overlaps(acc_dump, plan->dump_bytes, out, plan->out_bytes) ||
+                   overlaps(acc_dump, plan->dump_bytes, in, plan->in_bytes)))
+    return fail(ctx, PALQ_ERR_ARG, "acc_dump overlaps a tensor");
+  if (ctx->device < 0 || !work) return PALQ_OK;
+  ConvArgs a = plan->a;
+  a.in.data = (uint8_t *)in;
+  a.out.data = (uint8_t *)out;
+  if (plan->res_kind == 1) a.res.data = (uint8_t *)res_in;
+  if (plan->res_kind == 2) a.proj.data = (uint8_t *)res_in;
+  a.acc_dump = acc_dump;
+  hipSetDevice(ctx->device);
+  const hipError_t e = plan->mfma ? launch_conv_mfma(a, plan->wp, plan->thr, plan->epi, ctx->stream)
+                                  : launch_conv_direct(a, ctx->stream);
+  return e == hipSuccess ? PALQ_OK : device_fail(ctx, e, "conv run");
+}
+
+void palq_conv_plan_destroy(palq_conv_plan *plan) { free_plan(plan); }
+
+const char *palq_conv_plan_kernels(const palq_conv_plan *plan) {
+  if (!plan) return nullptr;
+  if (!plan->ctx || plan->ctx->device < 0) return "";
+  return plan->mfma ? conv_kernel_label(plan->a, plan->epi) : "conv_direct_kernel";
 }
 
 // ------------------------------------------------------------ shuffle

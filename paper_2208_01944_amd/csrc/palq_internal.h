@@ -175,4 +175,18 @@ struct palq_ctx {
   int conv_fp4 = 1;                // palq_set_conv_fp4 (initial value: PALQ_CONV_FP4, default 1)
   uint8_t *mod_scratch = nullptr;  // rotated parameters of the last shuffle-module call
   size_t mod_scratch_bytes = 0;
+  hipEvent_t order_event = nullptr;  // palq_set_stream: the new stream waits for the old one
+};
+
+// A planned single layer (palq_conv_plan_create / palq_conv_run).
+struct palq_conv_plan {
+  palq_ctx *ctx = nullptr;
+  palq::ConvArgs a{};        // planned launch (tensor pointers patched per run)
+  bool mfma = false;         // matrix-core kernels (else the direct kernel)
+  int epi = -1;              // their epilogue build (conv_mfma_epilogue)
+  void *mem = nullptr;       // owned device memory: parameters, prepacked filter, constants
+  uint8_t *wp = nullptr;
+  int32_t *thr = nullptr;
+  int64_t in_bytes = 0, out_bytes = 0, res_bytes = 0, dump_bytes = 0;
+  int res_kind = 0;          // 0 none, 1 identity codes, 2 projection input
 };

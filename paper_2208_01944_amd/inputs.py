@@ -306,3 +306,28 @@ def with_stored_biases(spec, name):
                 L["bias"] = b.astype(np.int32)
     spec["name"] = spec["name"] + "_centred"
     return spec
+
+
+# Single-layer benchmark cases: C1 (the 56x56 G=2 layer at batch 1), the
+# four ResNet-18 stage layers at G=4 and batch 32, and the G x B sweep on the
+# stage-3 layer at batch 128.
+SINGLE_WORKLOADS = ["c1"] + [f"c2_l{i}" for i in range(4)] + \
+    [f"c4_g{g}_b{b}" for g in (1, 2, 4) for b in (2, 3, 4)]
+
+
+def single_workload(name):
+    if name == "c1":
+        return config_c1()
+    if name.startswith("c2_l"):
+        return config_c2(int(name[4:]))
+    if name.startswith("c4_g"):
+        g, b = name[4:].split("_b")
+        return config_c4(int(g), int(b))
+    raise ValueError(name)
+
+
+def single_stored_bias(name):
+    """The stored centred bias of single-layer case `name`
+    (tests/golden/centred_bias_single.npz, array `name`)."""
+    with np.load(os.path.join(GOLDEN_DIR, "centred_bias_single.npz"), allow_pickle=False) as z:
+        return z[name].astype(np.int32)

@@ -87,6 +87,11 @@ _group_conv = _sig("palq_group_conv", c_i32, c_p, P_ACT, P_FIL, c_i32, c_i32,
 _group_conv_noalloc = _sig("palq_group_conv_noalloc", c_i32, c_p, P_ACT, P_FIL, c_i32, c_i32,
                            ctypes.POINTER(Requant), ctypes.POINTER(Residual), c_i32, P_ACT, c_p)
 NOALLOC_SCRATCH_BYTES = 16 << 20
+_conv_plan_create = _sig("palq_conv_plan_create", c_i32, c_p, P_ACT, P_FIL, c_i32, c_i32, ctypes.POINTER(Requant),
+                         ctypes.POINTER(Residual), c_i32, P_ACT, ctypes.POINTER(c_p))
+_conv_run = _sig("palq_conv_run", c_i32, c_p, c_p, c_p, c_p, c_p, c_p)
+_conv_plan_destroy = _sig("palq_conv_plan_destroy", None, c_p)
+_conv_plan_kernels = _sig("palq_conv_plan_kernels", ctypes.c_char_p, c_p)
 _shuffle = _sig("palq_cyclic_shuffle", c_i32, c_p, P_ACT, c_i32, P_ACT)
 _channel_shuffle = _sig("palq_channel_shuffle", c_i32, c_p, P_ACT, P_ACT)
 _shuffle_module = _sig("palq_shuffle_module", c_i32, c_p, P_ACT, P_FIL, ctypes.POINTER(Requant), c_p, P_ACT)
@@ -106,7 +111,8 @@ _net_reset_times = _sig("palq_net_reset_times", c_i32, c_p)
 
 EXPORTS = ["palq_create", "palq_destroy", "palq_set_stream", "palq_set_conv_fp4", "palq_sync", "palq_last_error",
            "palq_version", "palq_row_bytes", "palq_act_bytes", "palq_pack", "palq_unpack",
-           "palq_quantize", "palq_group_conv", "palq_group_conv_noalloc", "palq_shuffle_module", "palq_cyclic_shuffle",
+           "palq_quantize", "palq_group_conv", "palq_group_conv_noalloc", "palq_conv_plan_create",
+           "palq_conv_run", "palq_conv_plan_destroy", "palq_conv_plan_kernels", "palq_shuffle_module", "palq_cyclic_shuffle",
            "palq_channel_shuffle", "palq_maxpool",
            "palq_avgsum", "palq_fc", "palq_net_create", "palq_net_destroy", "palq_forward",
            "palq_forward_image", "palq_net_tensor", "palq_net_ops", "palq_net_layer_kernels", "palq_net_layer_times",
@@ -280,6 +286,47 @@ class Context:
 
     def fc(self, x, n, cin, w, cout, logits):
         self._check(_fc(self.h, _ptr(x), n, cin, _ptr(w), cout, _ptr(logits)))
+
+
+class ConvPlan:
+    """A planned layer (palq_conv_plan_create): the filter, requant arrays
+    and shortcut scale are consumed at creation; run() takes tensors of the
+    planned shapes."""
+
+    def __init__(self, ctx: Context, x: Tensor, w: Filter, stride, pad, mult, shift, bias, out: Tensor,
+                 shuffle=0, identity: Tensor = None, res_mult=None, proj_in: Tensor = None,
+                 proj_w: Filter = None, proj_stride=1):
+        self.ctx = ctx
+        rq = Requant(_ptr(mult), _ptr(shift), _ptr(bias), out.act.bits)
+        res = None
+        if identity is not None or proj_in is not None:
+            res = Residual()
+            if identity is not None:
+                res.identity = ctypes.pointer(identity.act)
+                res.res_mult = _ptr(res_mult)
+            if proj_in is not None:
+                res.proj_in = ctypes.pointer(proj_in.act)
+                res.proj_w = ctypes.pointer(proj_w)
+                res.proj_stride = proj_stride
+        h = c_p()
+        ctx._check(_conv_plan_create(ctx.h, ctypes.byref(x.act), ctypes.byref(w), stride, pad, ctypes.byref(rq),
+                                     ctypes.byref(res) if res is not None else None, shuffle,
+                                     ctypes.byref(out.act), ctypes.byref(h)))
+        self.h = h
+
+    @property
+    def kernels(self) -> str:
+        return _conv_plan_kernels(self.h).decode()
+
+    def run(self, x: Tensor, out: Tensor, res_in: Tensor = None, acc_dump=None):
+        self.ctx._check(_conv_run(self.ctx.h, self.h, x.act.data, res_in.act.data if res_in is not None else None,
+                                  out.act.data, _ptr(acc_dump)))
+
+    def __del__(self):
+        h = getattr(self, "h", None)
+        if h:
+            _conv_plan_destroy(h)
+            self.h = None
 
 
 class Net:

@@ -1,7 +1,10 @@
 """Writes tests/golden/centred_bias_<workload>.npz: the centred variant's
 conv biases of each benchmark network (reading A14 of the design notes:
 bias = -round_half_up(mean of the layer's pre-requant value), layer by
-layer), calibrated by the CPU oracle on the workload's calibration images.
+layer), calibrated by the CPU oracle on the workload's calibration images;
+and tests/golden/centred_bias_single.npz: the centred bias of each
+single-layer case, over the whole batch's interior positions (whose window
+lies inside the image), as the full-size single-layer tests compute it.
 
 Calls only the oracle and the seeded input generators:
 
@@ -21,7 +24,17 @@ sys.path.insert(0, ROOT)
 from oracle import oracle as O  # noqa: E402
 from paper_2208_01944_amd import inputs as I  # noqa: E402
 
-WORKLOADS = ["resnet18_g4_b2", "resnet50_g2_b2"]
+WORKLOADS = ["resnet18_g4_b2", "resnet50_g2_b2", "single"]
+
+
+def single_bias(name):
+    case = I.single_workload(name)
+    L = case["layer"]
+    G = L["w"].shape[0]
+    acc = O.group_conv(case["x"], L["w"], L["stride"], L["pad"])
+    _, acc_d = O.layer_epilogue(acc, G, L["mult"], L["shift"], None, L["out_bits"], L["shuffle"])
+    p = L["pad"] if L["stride"] == 1 else 0
+    return O.centring_bias(acc_d[:, p:acc_d.shape[1] - p, p:acc_d.shape[2] - p], G, L["shuffle"])
 
 
 def calibrate(name):
@@ -33,6 +46,11 @@ def calibrate(name):
 
 def main(names):
     for name in names:
+        if name == "single":
+            path = os.path.join(I.GOLDEN_DIR, "centred_bias_single.npz")
+            np.savez_compressed(path, **{n: single_bias(n) for n in I.SINGLE_WORKLOADS})
+            print("wrote", path)
+            continue
         cen, calib = calibrate(name)
         arrays = {f"layer{i}": np.asarray(L["bias"], np.int32)
                   for i, L in enumerate(cen["layers"]) if L["op"] in ("conv", "shuffle_module")}

@@ -300,3 +300,37 @@ def test_validate_only_group_conv_noalloc(P, vctx):
     assert call(_act(P, g=8, c=512), too_big, _act(P, g=8, c=512, slot=20)) == P.ERR_UNSUPPORTED
     assert "static buffer" in vctx.last_error()
     assert P.NOALLOC_SCRATCH_BYTES == 16 << 20
+
+
+def test_validate_only_conv_plan(P, vctx):
+    """palq_conv_plan_create checks like palq_group_conv; palq_conv_run checks
+    pointers against the plan (validate-only: nothing runs)."""
+    x, f, out = _act(P), P.Filter(2, 32, 64, 3, 3, 2, _fake(10)), _act(P, c=32, slot=20)
+    rq = P.Requant(_fake(30), _fake(31), None, 2)
+    h = ctypes.c_void_p()
+    assert P._conv_plan_create(vctx.h, ctypes.byref(x), ctypes.byref(f), 1, 1, ctypes.byref(rq), None, 1,
+                               ctypes.byref(out), ctypes.byref(h)) == P.OK
+    assert P._conv_run(vctx.h, h, _fake(1), None, _fake(40), None) == P.OK
+    assert P._conv_plan_kernels(h) == b"" and P._conv_plan_kernels(None) is None
+    assert P._conv_run(vctx.h, h, None, None, _fake(40), None) == P.ERR_ARG           # null input
+    assert P._conv_run(vctx.h, h, _fake(1) + 8, None, _fake(40), None) == P.ERR_ARG   # misaligned
+    assert P._conv_run(vctx.h, h, _fake(1), _fake(3), _fake(40), None) == P.ERR_ARG   # no shortcut planned
+    assert P._conv_run(vctx.h, h, _fake(1), None, _fake(1), None) == P.ERR_ARG        # out aliases in
+    other = P.Context(-1)
+    assert P._conv_run(other.h, h, _fake(1), None, _fake(40), None) == P.ERR_ARG      # another context
+    P._conv_plan_destroy(h)
+    # the layer's own checks apply at plan time
+    bad = _act(P, c=32, bits=3, slot=20)
+    assert P._conv_plan_create(vctx.h, ctypes.byref(x), ctypes.byref(f), 1, 1, ctypes.byref(rq), None, 1,
+                               ctypes.byref(bad), ctypes.byref(h)) == P.ERR_ARG
+    assert "plan:" in vctx.last_error()
+    # a planned identity shortcut needs its input at run time
+    res = P.Residual()
+    ident = _act(P, c=32, slot=50)
+    res.identity = ctypes.pointer(ident)
+    res.res_mult = _fake(32)
+    assert P._conv_plan_create(vctx.h, ctypes.byref(x), ctypes.byref(f), 1, 1, ctypes.byref(rq), ctypes.byref(res), 1,
+                               ctypes.byref(out), ctypes.byref(h)) == P.OK
+    assert P._conv_run(vctx.h, h, _fake(1), None, _fake(40), None) == P.ERR_ARG
+    assert P._conv_run(vctx.h, h, _fake(1), _fake(3), _fake(40), None) == P.OK
+    P._conv_plan_destroy(h)

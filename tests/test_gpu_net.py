@@ -272,7 +272,7 @@ def test_c3_launches_the_benchmark_kernels(c3_run):
     kernels = c3_run[3]
     assert kernels[0] == "quantize_pad4_kernel + stem_pool_kernel", kernels[0]
     assert kernels[1] == "", kernels[1]
-    assert kernels.count("conv_tile_kernel[fp4]") == 16, kernels
+    assert kernels.count("conv_fp4_kernel") == 16, kernels
     assert kernels[-2:] == ["avgsum2_wg_kernel", "fc_mfma_kernel"], kernels[-2:]
 
 
@@ -294,7 +294,7 @@ def test_c5_full_size_every_image(c5_run, chunk):
     logits (8 per test) against the oracle."""
     spec, codes, got, kernels = c5_run
     if chunk == 0:
-        assert kernels.count("conv_tile_kernel[fp4]") >= 40, kernels
+        assert kernels.count("conv_fp4_kernel") >= 40, kernels
     sl = slice(8 * chunk, 8 * chunk + 8)
     say(f"C5 oracle images {sl.start}..{sl.stop - 1}")
     ref = O.run_net(spec, codes[sl])

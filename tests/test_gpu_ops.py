@@ -480,3 +480,111 @@ def test_quantize_image_path(ctx, torch, signed, calibrate):
         ctx.quantize(ctx.upload(x), l, u, out)
     ctx.sync()
     np.testing.assert_array_equal(ctx.unpack(out), O.quantize(x, l, u, 8, signed))
+
+
+# ---------------------------------------------------------------- planned layers
+def _layer_tensors(ctx, case, bias):
+    L = case["layer"]
+    G, co, kh, kw, ci = L["w"].shape
+    n, h, w, _ = case["x"].shape
+    ho = (h + 2 * L["pad"] - kh) // L["stride"] + 1
+    wo = (w + 2 * L["pad"] - kw) // L["stride"] + 1
+    i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
+    t = dict(x=ctx.pack(case["x"], G, L["in_bits"]), out=ctx.empty_act(n, ho, wo, G, co, L["out_bits"]),
+             mult=i32(L["mult"]), shift=i32(L["shift"]), bias=i32(bias), shape=(n, ho, wo, G * co))
+    t["wt"], t["w"] = ctx.pack_filter(L["w"], L["w_bits"])
+    if L["res"] >= 0:
+        t["res_in"] = ctx.pack(case["extra"][1], G, L["out_bits"])
+        t["kw"] = dict(identity=t["res_in"], res_mult=i32(L["res_mult"]))
+    elif L["proj_src"] >= 0:
+        t["res_in"] = ctx.pack(case["extra"][1], G, L["in_bits"])
+        pt, pw = ctx.pack_filter(L["proj_w"], L["w_bits"])
+        t["kw"] = dict(proj_in=t["res_in"], proj_w=pw, proj_stride=L["proj_stride"])
+        t["pt"] = pt
+    else:
+        t["res_in"], t["kw"] = None, {}
+    return t
+
+
+@pytest.mark.parametrize("kind", ["plain", "identity", "projection", "bits3"])
+def test_conv_plan_runs(ctx, torch, kind):
+    """A planned layer run on two inputs after its parameter arrays are gone,
+    with and without the accumulator dump, and captured into a HIP graph
+    (capture fails on any allocation or synchronisation) replayed with other
+    work between replays: every result equals the oracle's."""
+    from paper_2208_01944_amd import palq
+    say(f"conv plan {kind}")
+    p = dict(n=2, h=14, w=14, groups=4, cin=128, cout=128, shuffle=1)
+    if kind == "identity":
+        p.update(residual="identity")
+    elif kind == "projection":
+        p.update(residual="projection", stride=2, h=15, w=15)
+    elif kind == "bits3":
+        p.update(bits=3, cin=64, cout=64, groups=3)
+    cases = [I.single_layer(4100 + s, **p) for s in range(2)]
+    for c in cases[1:]:  # the second input shares the first case's filter and parameters
+        c["layer"] = cases[0]["layer"]
+    L = cases[0]["layer"]
+    refs = []
+    for c in cases:
+        res = c["extra"].get(1) if L["res"] >= 0 else None
+        px = c["extra"].get(1) if L["proj_src"] >= 0 else None
+        refs.append(O.conv_layer(c["x"], L["w"], L["stride"], L["pad"], L["mult"], L["shift"], L["bias"],
+                                 L["out_bits"], L["shuffle"], res=res, res_mult=L["res_mult"], proj_x=px,
+                                 proj_w=L["proj_w"], proj_stride=L["proj_stride"]))
+    t0 = _layer_tensors(ctx, cases[0], L["bias"])
+    plan = palq.ConvPlan(ctx, t0["x"], t0["w"], L["stride"], L["pad"], t0["mult"], t0["shift"], t0["bias"],
+                         t0["out"], shuffle=L["shuffle"], **t0["kw"])
+    for k in ("mult", "shift", "bias", "wt", "pt"):
+        t0.pop(k, None)  # the plan holds its own copies
+    torch.cuda.synchronize()
+    tens = [t0, _layer_tensors(ctx, cases[1], L["bias"])]
+    for t, (rq, racc) in zip(tens, refs):
+        dump = torch.full((int(np.prod(t["shape"])),), -7, dtype=torch.int32, device=ctx.dev)
+        plan.run(t["x"], t["out"], t["res_in"])
+        ctx.sync()
+        np.testing.assert_array_equal(ctx.unpack(t["out"]), rq)
+        plan.run(t["x"], t["out"], t["res_in"], acc_dump=dump)
+        ctx.sync()
+        np.testing.assert_array_equal(dump.cpu().numpy().astype(np.int64).reshape(t["shape"]), racc)
+        np.testing.assert_array_equal(ctx.unpack(t["out"]), rq)
+    # graph capture and replays of the second input's run
+    t = tens[1]
+    side = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(side):
+        ctx.set_stream(side)
+        graph.capture_begin()
+        plan.run(t["x"], t["out"], t["res_in"])
+        graph.capture_end()
+    ctx.set_stream(torch.cuda.current_stream())
+    for r in range(3):
+        t["out"].buf.fill_(0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(ctx.unpack(t["out"]), refs[1][0], err_msg=f"replay {r}")
+        plan.run(tens[0]["x"], tens[0]["out"], tens[0]["res_in"])  # other work between replays
+        ctx.sync()
+
+
+def test_set_stream_orders_context_scratch(ctx, torch):
+    """Two group_conv calls with different filters on two streams: the
+    second call's prepack reuses the context's scratch, so the new stream
+    must wait for the first call (palq_set_stream orders them)."""
+    say("set_stream ordering")
+    cases = [I.single_layer(4200 + s, n=16, h=28, w=28, groups=4, cin=128, cout=128, shuffle=1) for s in range(2)]
+    refs = [O.conv_layer(c["x"], c["layer"]["w"], 1, 1, c["layer"]["mult"], c["layer"]["shift"], c["layer"]["bias"],
+                         2, 1)[0] for c in cases]
+    tens = [_layer_tensors(ctx, c, c["layer"]["bias"]) for c in cases]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t, s in zip(tens, streams):
+            ctx.set_stream(s)
+            ctx.group_conv(t["x"], t["w"], 1, 1, t["mult"], t["shift"], t["bias"], t["out"], shuffle=1)
+        ctx.set_stream(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        for t, r in zip(tens, refs):
+            np.testing.assert_array_equal(ctx.unpack(t["out"]), r, err_msg=f"round {rep}")
