@@ -1521,24 +1521,36 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
 // fast epilogue, which this kernel has, requires that), so the max of the
 // requantised values equals the requant of the max.
 //
-// A tile is one output row (wo <= 127 columns) of one image and 128 output
-// channels, 2 x 2 waves of 2 x 2 32 x 32 blocks as in the tiled stem (wave
-// (wn, wm): channels 64 wn .. + 63).  Column halves overlap by one column:
-// wm = 0 holds columns 0 .. 63, wm = 1 columns 63 .. 126, lane l of pixel
-// block pb column 63 wm + 2 l + pb.  Pooled column 32 wm + l then needs the
-// lane's two columns and one of its neighbour lane (l - 1 for wm = 0, l + 1
-// for wm = 1), a __shfl within the wave.  Work units are pooled rows
-// (image, channel block, k); a unit takes output rows 2k and 2k + 1, and
-// pooled row k also needs row 2k - 1, which the previous unit of the same
-// run left in registers (a run starting inside an image recomputes it).
+// The stem is a 7x7 / stride 2 filter over 4-byte pixels (3 channels and a
+// zero byte) with an explicit zero border.  Its K is laid out as one 32-byte
+// K-step per filter row (8 taps x 4 bytes, tap 7 and the fourth byte with
+// zero weight): 7 K-steps, 224 of which 147 are real.  Lane half h of an
+// MFMA operand holds taps 4h .. 4h + 3 of the row, which for output column c
+// are the 16 contiguous input bytes 8c + 16h ..: the operand is read straight
+// out of the staged input row, so the activations are staged once per
+// output row (its 7 input rows) instead of once per K-step and pixel.  Each
+// row is staged twice, the second copy 8 bytes on, so that odd columns
+// (8 mod 16 bytes) also read 16-byte aligned operands.  The weights of a
+// wave's 64 channels (7 x 2 K-steps of 16 bytes a lane) stay in registers.
+//
+// A step is one output row (wo <= 125 columns) of one image and 128 output
+// channels, 2 x 2 waves of 2 x 2 32 x 32 blocks (wave (wn, wm): channels
+// 64 wn .. + 63).  Column halves overlap by one column: wm = 0 holds columns
+// 0 .. 63, wm = 1 columns 63 .. 126, lane l of pixel block pb column
+// 63 wm + 2 l + pb.  Pooled column 32 wm + l then needs the lane's two
+// columns and one of its neighbour lane (l - 1 for wm = 0, l + 1 for
+// wm = 1), a DPP shift within the wave.  Work units are pooled rows (image,
+// channel block, k); a unit takes output rows 2k and 2k + 1, and pooled row
+// k also needs row 2k - 1, which the previous unit of the same run left in
+// registers (a run starting inside an image recomputes it).
 namespace sp {
-constexpr int kSpStages = 3;
 constexpr int NT = 256;
-constexpr int WST = 4 * kSlab;   // four 32-channel weight slabs of a K-block
-constexpr int XST = 128 * 64;    // 128 pixel slots x two filter rows of 8 four-byte taps
-constexpr int SST = WST + XST;
+constexpr int KH = 7;                // filter rows = K-steps
+constexpr int RB = 1024;             // LDS bytes of one staged copy of an input row
+constexpr int SET = 8 * 2 * RB;      // an output row's input rows 0 .. 7, two copies each
+constexpr int kSets = 3;             // ring of staged output rows, two ahead of the MFMAs
 
-// Row tiles of a run: phase 0 recomputes row 2k - 1, 1 is row 2k, 2 row 2k + 1.
+// Row steps of a run: phase 0 recomputes row 2k - 1, 1 is row 2k, 2 row 2k + 1.
 struct RowIt {
   int u, phase;
 };
@@ -1553,20 +1565,35 @@ __device__ __forceinline__ int row_of(const RowIt &it, int ho2) {
   const int k = it.u % ho2;
   return it.phase == 0 ? 2 * k - 1 : 2 * k + (it.phase - 1);
 }
-// column of pixel slot s (0 .. 127)
-__device__ __forceinline__ int slot_col(int s) { return 63 * (s >> 6) + 2 * (s & 31) + ((s >> 5) & 1); }
-// LDS swizzle of the activation stage: quarter q of slot s sits at 16-byte
-// unit 4 s + (q ^ xsw(s)), so that the operand reads of 8 (or 16)
-// consecutive lanes, consecutive slots at one quarter, touch distinct banks.
-__device__ __forceinline__ int xsw(int s) { return ((s >> 1) ^ (s >> 3)) & 3; }
 }  // namespace sp
+
+// Stem weights by filter row: [cout / 32][KH][half][ch][16 B], lane (half,
+// ch) of K-step r holding taps 4 half .. + 3 of row r for channel ch, the
+// input's padding byte and taps past kw masked to zero.  One thread per
+// 16-byte lane operand.
+__global__ void prepack_stem_rows_kernel(ConvArgs a, uint8_t *wp) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)a.cout * sp::KH * 2) return;
+  const int lane = (int)(t & 63), r = (int)((t >> 6) % sp::KH);
+  const int k = (int)(t / (64 * sp::KH)) * 32 + (lane & 31), h = lane >> 5;
+  const uint32_t *wr = (const uint32_t *)(a.w + ((int64_t)k * a.kh + r) * a.kw * 4);
+  const uint32_t cmask = a.in.cpg >= 4 ? 0xffffffffu : ((1u << (8 * a.in.cpg)) - 1u);
+  uint32_t o[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const int kx = 4 * h + d;
+    o[d] = kx < a.kw ? (wr[kx] & cmask) : 0u;
+  }
+  *(uint4 *)(wp + t * 16) = make_uint4(o[0], o[1], o[2], o[3]);
+}
 
 // Runs hold at most ho2 units (the launcher's grid), so a run meets at most
 // two channel blocks, cbb0 and cbb0 + 1 (mod ncb): their requant constants
 // sit in LDS.
-__global__ __launch_bounds__(sp::NT, 3) void stem_pool_kernel(ConvArgs a, Geo geo, ActView po, int units) {
+__global__ __launch_bounds__(sp::NT, 2) void stem_pool_kernel(ConvArgs a, Geo geo, ActView po, const uint8_t *wrow,
+                                                              int units) {
   using namespace sp;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kSpStages * SST];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kSets * SET];
   __shared__ RqConst rq_area[256];
   if (needs_general(a, geo, 0)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1588,74 +1615,46 @@ __global__ __launch_bounds__(sp::NT, 3) void stem_pool_kernel(ConvArgs a, Geo ge
   __syncthreads();
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
   typedef __attribute__((address_space(3))) void *lds_ptr;
-  const auto rw_src = make_rsrc(geo.wp, (int64_t)a.cout * geo.kb_total * 64);
   const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
   const auto rout = make_rsrc(po.data, (int64_t)po.n * po.h * po.w * po.pixel);
-  const int pixb = (int)a.in.pixel, rowb = a.in.w * pixb;
-  const int KB = geo.kb_total;
+  const int rowb = a.in.w * (int)a.in.pixel;  // <= RB (launcher)
 
-  // ---- fetcher: K-block f_kb of row tile f_it.  Weight piece p = tid + 256 i
-  // is piece p % 128 of slab p / 128; activation piece p is quarter
-  // q = (p % 4) ^ xsw(s) (filter row 2 kb + q / 2, bytes 16 (q % 2) ..) of
-  // slot s = p / 4.
+  // ---- fetcher: output row f_it.  Wave w stages input rows w and w + 4 of
+  // the row's window (row 7 is never read: no filter row 7); copy 1 of a row
+  // starts 8 bytes on.  Lanes past the row's end load the next row's first
+  // bytes (or zeros past the tensor), which no operand reads.
   RowIt f_it = row_first(u_begin, ho2);
-  int f_kb = 0;
-  // per thread: the byte offset of each activation piece within an output
-  // row's input rows; per row: the row's offset.  A slot past the row's
-  // last column loads that column again: its accumulators duplicate a
-  // column of the same pooling window (the window of a pooled column that
-  // reaches past the row holds the last column), so the max ignores it.
-  // The two offsets share one register (16 bits each; the launcher checks
-  // that an input row pair fits).
-  uint32_t xcols = 0;
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int sl = (tid >> 2) + 64 * i, c = min(slot_col(sl), wo - 1), q = (tid & 3) ^ xsw(sl);
-    xcols |= (uint32_t)((q >> 1) * rowb + c * a.stride * pixb + (q & 1) * 16) << (16 * i);
-  }
-  asm volatile("" : "+v"(xcols));  // one opaque register (the halves are not kept apart)
-  int xrow = 0;
-  uint32_t wb = 0;
-  const uint32_t wthr = (uint32_t)((tid >> 7) * KB * kSlab + (tid & 127) * 16);
-  auto tile_geometry = [&]() __attribute__((always_inline)) {
-    const int cbb = (f_it.u / ho2) % ncb, n = f_it.u / (ho2 * ncb);
-    wb = (uint32_t)(cbb * 4 * KB) * kSlab;
-    xrow = (n * a.in.h + row_of(f_it, ho2) * a.stride) * rowb;
-  };
-  tile_geometry();
-  auto fetch = [&](int st) __attribute__((always_inline)) {
+  int f_set = 0;
+  auto fetch = [&]() __attribute__((always_inline)) {
     const bool live = f_it.u < u_end;
-    uint8_t *ws = lds + st * SST;
+    const int n = f_it.u / (ho2 * ncb);
+    const uint32_t rbase = live ? (uint32_t)((n * a.in.h + 2 * row_of(f_it, ho2) + wave) * rowb + lane * 16) : kOob;
+    uint8_t *ws = lds + f_set * SET + wave * 2 * RB;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {  // piece tid + 256 i: slab 2 i + tid / 128
-      const uint32_t woff = live ? wb + wthr + (uint32_t)((2 * i * KB + f_kb) * kSlab) : kOob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + i * 4096 + wave * 1024), 16, (int)woff, 0, 0, 0);
-    }
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      // filter rows past kh (zero weights) may read the next image's rows
-      // or past the end (the buffer bound returns zeros)
-      const uint32_t off = live ? (uint32_t)xrow + __builtin_amdgcn_ubfe(xcols, 16 * i, 16) + (uint32_t)(2 * f_kb * rowb) : kOob;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rin, (lds_ptr)(ws + WST + i * 4096 + wave * 1024), 16, (int)off, 0, 0,
-                                               0);
-    }
-    if (++f_kb == KB) {
-      f_kb = 0;
-      row_next(f_it, ho, ho2);
-      tile_geometry();
-    }
+      for (int cp = 0; cp < 2; ++cp)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rin, (lds_ptr)(ws + (8 * i + cp) * RB), 16,
+                                                 (int)(rbase + (uint32_t)(4 * i * rowb + 8 * cp)), 0, 0, 0);
+    if (live) row_next(f_it, ho, ho2);
+    f_set = f_set == kSets - 1 ? 0 : f_set + 1;
   };
 
   // ---- compute side
   RowIt c_it = row_first(u_begin, ho2);
-  int c_kb = 0;
+  int c_set = 0, w_cbb = -1;
   v16i acc[2][2];     // [cb][pb]
   int32_t st[2][16];  // per cb: row 2k - 1 pooled across columns, or the running max of rows 2k - 1, 2k
-  const uint32_t aaddr0 = lds_base + (uint32_t)(wn * 2 * kSlab + (half * 32 + l32) * 16);
-  // this lane's activation quarters 2 half + j of slot 64 wm + l32 (+ 32 pb)
-  const uint32_t xslot = lds_base + WST + (uint32_t)((wm * 64 + l32) * 64);
-  // (quarter 2 half + 1 at xaddr0 ^ 16: the stages are 1024-byte aligned)
-  const uint32_t xaddr0 = xslot + 16 * ((2 * half) ^ xsw(l32));
+  v4i W[KH][2];       // [K-step][cb]
+  // operand address of pixel block pb: column c (slots past the last column
+  // read the last column again: the window of a pooled column reaching past
+  // the row holds the last column, so the duplicate leaves the max unchanged)
+  uint32_t xa[2];
+#pragma unroll
+  for (int pb = 0; pb < 2; ++pb) {
+    const int c = min(63 * wm + 2 * l32 + pb, wo - 1);
+    xa[pb] = lds_base + (uint32_t)((c & 1) * RB + 16 * (c >> 1) + 16 * half);
+  }
   // the lane whose pooling neighbour would be in the other lane half
   // (column -1 for wm = 0, column 127 for wm = 1)
   const bool half_edge = wm ? lane == 31 : lane == 32;
@@ -1675,22 +1674,24 @@ __global__ __launch_bounds__(sp::NT, 3) void stem_pool_kernel(ConvArgs a, Geo ge
     // requantised; row 2k + 1, kept in nx, then becomes st for row k + 1.
     int32_t nx[2][16];
     auto pool_row = [&](auto WMC) __attribute__((always_inline)) {
-      constexpr int W = decltype(WMC)::value;
-      // neighbour column by a DPP wave shift (lane i reads lane i - 1 for
-      // wm = 0, i + 1 for wm = 1; the end lane keeps its own value); the
-      // lane whose neighbour lies in the other lane half takes its own
-      // other column instead (a duplicate leaves the max unchanged)
+      constexpr int WMV = decltype(WMC)::value;
+      // neighbour column by a DPP wave shift folded into the max (lane i
+      // reads lane i - 1 for wm = 0, i + 1 for wm = 1; the end lane, which
+      // has no source, takes the identity INT_MIN); the lane whose
+      // neighbour lies in the other lane half takes its own column instead
+      // (a duplicate leaves the max unchanged)
       auto hmax = [&](int cb, int i) __attribute__((always_inline)) {
         const int32_t v0 = acc[cb][0][i], v1 = acc[cb][1][i];
-        int32_t nb;
-        if constexpr (W == 0) {
-          nb = __builtin_amdgcn_update_dpp(v1, v1, 0x138 /* wave_shr:1 */, 0xf, 0xf, false);
-          nb = half_edge ? v1 : nb;
+        int32_t t;
+        if constexpr (WMV == 0) {
+          t = max(__builtin_amdgcn_update_dpp((int)0x80000000, v1, 0x138 /* wave_shr:1 */, 0xf, 0xf, false), v0);
+          t = half_edge ? v0 : t;
+          return max(t, v1);
         } else {
-          nb = __builtin_amdgcn_update_dpp(v0, v0, 0x130 /* wave_shl:1 */, 0xf, 0xf, false);
-          nb = half_edge ? v0 : nb;
+          t = max(__builtin_amdgcn_update_dpp((int)0x80000000, v0, 0x130 /* wave_shl:1 */, 0xf, 0xf, false), v1);
+          t = half_edge ? v1 : t;
+          return max(t, v0);
         }
-        return max(max(nb, v0), v1);
       };
       if (c_it.phase == 2) {
 #pragma unroll
@@ -1750,54 +1751,86 @@ __global__ __launch_bounds__(sp::NT, 3) void stem_pool_kernel(ConvArgs a, Geo ge
     }
   };
 
-  // ring of kSpStages K-blocks over the run's row tiles, fetching
-  // kSpStages - 1 ahead (as the tiled kernel)
   int rows = 0;
   for (RowIt it = row_first(u_begin, ho2); it.u < u_end; row_next(it, ho, ho2)) ++rows;
-  const int total = rows * KB;
-  for (int s2 = 0; s2 < kSpStages - 1; ++s2) fetch(s2);
-  for (int gk = 0; gk < total; ++gk) {
-    if (c_kb == 0) {
+  fetch();
+  fetch();
+  for (int gk = 0; gk < rows; ++gk) {
+    // the wave's weights, loaded when the channel block changes (at most
+    // twice a run)
+    const int cbb = (c_it.u / ho2) % ncb;
+    if (cbb != w_cbb) {
+      w_cbb = cbb;
+      const uint8_t *wsrc = wrow + ((int64_t)(cbb * 4 + 2 * wn) * KH * 64 + lane) * 16;
 #pragma unroll
       for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-        for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0;
+        for (int r = 0; r < KH; ++r) W[r][cb] = *(const v4i *)(wsrc + (cb * KH + r) * 1024);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // here, not inside every later row's MFMAs
     }
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm((kSpStages - 2) * 4));
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0;
+    // this row's rows staged (each wave its own four loads; one row ahead
+    // stays in flight), then visible to every wave, and the set of the row
+    // before free for the row two ahead
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(4));
     ring_barrier();
-    fetch((gk + kSpStages - 1) % kSpStages);
-    const uint32_t so = (uint32_t)((gk % kSpStages) * SST);
-    v4i x0a, x0b, x1a, x1b, a00, a01, a10, a11;
+    fetch();
+    const uint32_t so = (uint32_t)(c_set * SET);
+    const uint32_t x0 = xa[0] + so, x1 = xa[1] + so;
+    v4i X[KH][2];
     asm volatile(
         "ds_read_b128 %0, %8\n\t"
         "ds_read_b128 %1, %9\n\t"
         "ds_read_b128 %2, %8 offset:2048\n\t"
         "ds_read_b128 %3, %9 offset:2048\n\t"
-        "ds_read_b128 %4, %10\n\t"
-        "ds_read_b128 %5, %10 offset:2048\n\t"
-        "ds_read_b128 %6, %10 offset:1024\n\t"
-        "ds_read_b128 %7, %10 offset:3072\n\t"
-        "s_waitcnt lgkmcnt(0)"
-        : "=&v"(x0a), "=&v"(x0b), "=&v"(x1a), "=&v"(x1b), "=&v"(a00), "=&v"(a01), "=&v"(a10), "=&v"(a11)
-        : "v"(xaddr0 + so), "v"((xaddr0 + so) ^ 16u), "v"(aaddr0 + so));
-    __builtin_amdgcn_sched_barrier(0);
-    const v4i X[2][2] = {{x0a, x1a}, {x0b, x1b}};  // [j][pb]
-    const v4i A[2][2] = {{a00, a01}, {a10, a11}};  // [j][cb]
+        "ds_read_b128 %4, %8 offset:4096\n\t"
+        "ds_read_b128 %5, %9 offset:4096\n\t"
+        "ds_read_b128 %6, %8 offset:6144\n\t"
+        "ds_read_b128 %7, %9 offset:6144"
+        : "=&v"(X[0][0]), "=&v"(X[0][1]), "=&v"(X[1][0]), "=&v"(X[1][1]), "=&v"(X[2][0]), "=&v"(X[2][1]),
+          "=&v"(X[3][0]), "=&v"(X[3][1])
+        : "v"(x0), "v"(x1));
+    asm volatile(
+        "ds_read_b128 %0, %6 offset:8192\n\t"
+        "ds_read_b128 %1, %7 offset:8192\n\t"
+        "ds_read_b128 %2, %6 offset:10240\n\t"
+        "ds_read_b128 %3, %7 offset:10240\n\t"
+        "ds_read_b128 %4, %6 offset:12288\n\t"
+        "ds_read_b128 %5, %7 offset:12288"
+        : "=&v"(X[4][0]), "=&v"(X[4][1]), "=&v"(X[5][0]), "=&v"(X[5][1]), "=&v"(X[6][0]), "=&v"(X[6][1])
+        : "v"(x0), "v"(x1));
+    // the first eight reads have landed (LDS reads complete in order)
+    asm volatile("s_waitcnt lgkmcnt(6)"
+                 : "+v"(X[0][0]), "+v"(X[0][1]), "+v"(X[1][0]), "+v"(X[1][1]), "+v"(X[2][0]), "+v"(X[2][1]),
+                   "+v"(X[3][0]), "+v"(X[3][1]));
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int r = 0; r < 4; ++r)
 #pragma unroll
       for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb)
-          acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[j][cb], X[j][pb], acc[cb][pb], 0, 0, 0);
-    if (++c_kb == KB) {
-      finish_row();
-      c_kb = 0;
-      row_next(c_it, ho, ho2);
-    }
+          acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(W[r][cb], X[r][pb], acc[cb][pb], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);  // the rows 0 - 3 MFMAs issue before the last reads are awaited
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(X[4][0]), "+v"(X[4][1]), "+v"(X[5][0]), "+v"(X[5][1]), "+v"(X[6][0]), "+v"(X[6][1]));
+#pragma unroll
+    for (int r = 4; r < KH; ++r)
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+          acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(W[r][cb], X[r][pb], acc[cb][pb], 0, 0, 0);
+    finish_row();
+    row_next(c_it, ho, ho2);
+    c_set = c_set == kSets - 1 ? 0 : c_set + 1;
   }
+  // no staging load may land after the workgroup's LDS is released
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
 }
 
 // ---------------------------------------------------------------- FP4 grouped kernel
@@ -2190,6 +2223,8 @@ int64_t acc_bound_of(const ConvArgs &a) {
 bool fp4_applies(const ConvArgs &a);
 bool tile_kernel_applies(const ConvArgs &a);
 bool stem_tile_applies(const ConvArgs &a);
+bool stem_rows(const ConvArgs &a);
+size_t stem_rows_offset(const ConvArgs &a);
 
 bool conv_mfma_general_fits(const ConvArgs &a) { return pick_cb(a, make_geo(a)) > 0; }
 
@@ -2215,6 +2250,7 @@ ConvPlan conv_mfma_plan(const ConvArgs &a) {
   const Geo geo = make_geo(a);
   p.w_bytes = (size_t)a.in.groups * a.cout * geo.kb_total * 64;
   p.thr_bytes = (size_t)a.in.groups * a.cout * sizeof(RqConst) + 16;  // + int64-path flag
+  if (stem_rows(a)) p.w_bytes += (size_t)a.cout * sp::KH * 32;  // the filter-row copy
   if (fp4_applies(a)) {  // FP4 slabs and constants after the int8 ones (the general build keeps those)
     p.w_bytes += (size_t)a.in.groups * a.cout * geo.kb_total * 32;
     p.thr_bytes *= 2;
@@ -2228,6 +2264,11 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
   const unsigned grid = (unsigned)((chunks + 255) / 256);
   if (is_stem(a)) {
     hipLaunchKernelGGL((prepack_kernel<8, true>), dim3(grid), dim3(256), 0, s, a, geo, wp);
+    if (stem_rows(a)) {
+      const int64_t pieces = (int64_t)a.cout * sp::KH * 2;
+      hipLaunchKernelGGL(prepack_stem_rows_kernel, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, s, a,
+                         wp + stem_rows_offset(a));
+    }
   } else {
     switch (a.in.bits) {
       case 2: hipLaunchKernelGGL((prepack_kernel<2, false>), dim3(grid), dim3(256), 0, s, a, geo, wp); break;
@@ -2335,6 +2376,14 @@ bool stem_tile_applies(const ConvArgs &a) {
          (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64 < ((int64_t)1 << 30);
 }
 
+// Stems whose weights are also prepacked by filter row (prepack_stem_rows_kernel,
+// after the K-block slabs): one input group, 7 filter rows of at most 8 taps,
+// stride 2.
+bool stem_rows(const ConvArgs &a) {
+  return stem_tile_applies(a) && a.in.groups == 1 && a.kh == sp::KH && a.kw <= 8 && a.stride == 2;
+}
+size_t stem_rows_offset(const ConvArgs &a) { return (size_t)a.in.groups * a.cout * make_geo(a).kb_total * 64; }
+
 // Tiled-kernel builds (tile shape per wave CB x PB blocks of 32 x 32, WN x WM
 // waves): the 8-bit stem; 2-bit layers on FP4 with 64-channel blocks (1 x 4
 // waves, 256-pixel tiles), 128-channel blocks (2 x 2 waves, 128 pixels) or
@@ -2435,12 +2484,14 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
 }
 
 // The stem followed by a 3x3 / stride 2 / pad 1 max pool of its output, on
-// stem_pool_kernel: the stem's tiled-kernel conditions, at most 127 output
-// columns, one input group, and a pooled view of the
-// stem's output shape.  The caller must know the fast epilogue applies
-// (conv_mfma_epilogue == 0): the kernel has no general build.
+// stem_pool_kernel: the stem's tiled-kernel conditions with a 7-row filter
+// at stride 2 and its weights also prepacked by filter row (stem_rows), an
+// input row of at most 1024 bytes (so at most 125 output columns), and a
+// pooled view of the stem's output shape.  The caller must know the fast
+// epilogue applies (conv_mfma_epilogue == 0): the kernel has no general
+// build.
 bool stem_pool_applies(const ConvArgs &a, const ActView &po, int k, int stride, int pad) {
-  if (!stem_tile_applies(a) || a.in.groups != 1 || a.wo < 1 || a.wo > 127 || a.ho < 1) return false;
+  if (!stem_rows(a) || a.wo < 1 || a.ho < 1) return false;
   if (k != 3 || stride != 2 || pad != 1) return false;
   if (po.n != a.out.n || po.h != (a.ho + 1) / 2 || po.w != (a.wo + 1) / 2 || po.groups != a.out.groups ||
       po.cpg != a.out.cpg || po.bits != 2 || po.pixel != a.out.pixel || po.row != a.out.row)
@@ -2448,9 +2499,8 @@ bool stem_pool_applies(const ConvArgs &a, const ActView &po, int k, int stride, 
   const int64_t in_bytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
   const int64_t out_bytes = (int64_t)po.n * po.h * po.w * po.pixel;
   const int64_t units = (int64_t)a.out.n * (a.cout / 128) * po.h;
-  // per-thread activation offsets within an output row's input rows: 16 bits
-  const int64_t xspan = (int64_t)a.in.w * a.in.pixel + (int64_t)(a.wo - 1) * a.stride * a.in.pixel + 16;
-  return in_bytes < 0x7fff0000 && out_bytes < 0x7fff0000 && units < 0x7fffffff && xspan < 0x10000;
+  return (int64_t)a.in.w * a.in.pixel <= sp::RB && in_bytes < 0x7fff0000 && out_bytes < 0x7fff0000 &&
+         units < 0x7fffffff;
 }
 
 hipError_t launch_stem_pool(const ConvArgs &a, const uint8_t *wp, const int32_t *thr, const ActView &po,
@@ -2459,6 +2509,7 @@ hipError_t launch_stem_pool(const ConvArgs &a, const uint8_t *wp, const int32_t 
   if (geo.M == 0) return hipSuccess;
   geo.wp = wp;
   geo.rq = (const RqConst *)thr;
+  const uint8_t *wrow = wp + stem_rows_offset(a);
   const int units = a.out.n * (a.cout / 128) * po.h;
   const int slots = tile_slots((const void *)stem_pool_kernel, sp::NT);
   // P workgroups per XCD: all resident slots, no more than the XCD's units,
@@ -2466,7 +2517,7 @@ hipError_t launch_stem_pool(const ConvArgs &a, const uint8_t *wp, const int32_t 
   const int64_t Tx = (units + 7) / 8;
   int64_t P = std::max<int64_t>(1, std::min<int64_t>(slots / 8, Tx));
   if ((Tx + P - 1) / P > po.h) P = (Tx + po.h - 1) / po.h;
-  hipLaunchKernelGGL(stem_pool_kernel, dim3((unsigned)(8 * P)), dim3(sp::NT), 0, s, a, geo, po, units);
+  hipLaunchKernelGGL(stem_pool_kernel, dim3((unsigned)(8 * P)), dim3(sp::NT), 0, s, a, geo, po, wrow, units);
   return hipGetLastError();
 }
 
