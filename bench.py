@@ -26,7 +26,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "effective int TOPS + images/s, ResNet-18-shaped G=4 2-bit fwd, batch 64"
 INT8_MFMA_PEAK_TOPS = 5000.0   # MI355X dense int8 MFMA, 5.0 POP/s
-FP4_MFMA_PEAK_TFLOPS = 10100.0  # MI355X dense FP4 MFMA, 10.1 PFLOP/s
+FP4_MFMA_PEAK_TFLOPS = 10100.0  # MI355X dense FP4 (and FP6) MFMA, 10.1 PFLOP/s
 HBM_PEAK_GBS = 8000.0
 
 
@@ -660,7 +660,8 @@ def run_single_layers(args, names):
         nbytes = (n * h * w * G * ci * L["in_bits"] + G * co * kh * kw * ci * L["w_bits"] +
                   n * ho * wo * G * co * L["out_bits"]) / 8 + 12 * G * co
         kern = plan.kernels
-        fp4 = kern == DOMINANT
+        fmt = {DOMINANT: "fp4", "conv_fp6_kernel": "fp6"}.get(kern, "int8")
+        fp4 = fmt != "int8"  # FP4 and FP6 share the 10.1 PFLOP/s dense peak
         peak = FP4_MFMA_PEAK_TFLOPS if fp4 else INT8_MFMA_PEAK_TOPS
         tops = ops / (us * 1e-6) / 1e12
         gbs = nbytes / (us * 1e-6) / 1e9
@@ -668,7 +669,7 @@ def run_single_layers(args, names):
             "metric": "effective int TOPS of one PalQuant layer (palq_conv_run)",
             "value": tops, "unit": "TOPS", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
             "ms_per_step": us / 1e3, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-            "dtype": "fp4" if fp4 else "int8",
+            "dtype": fmt,
             "data": "synthetic (seeded uniform codes and weights; centred bias over the batch's interior positions)",
             "config": {"workload": name, "description": SINGLE_DESC.get(name, f"ResNet-18 stage-3 3x3 conv, batch 128, "
                                                                              f"14x14, G={G} x 256->256, {L['in_bits']}-bit"),

@@ -34,7 +34,8 @@
  *     zero codes), 12 bytes each.  In a chunk, bytes 0-7 are a little-endian
  *     64-bit field holding bits 0-1 of code j at bits [2j, 2j+2); bytes 8-11
  *     are a little-endian 32-bit field holding bit 2 of code j at bit
- *     8*((j>>2)&3) + 4*(j>>4) + (j&3).
+ *     2*(j & 15) + (j >> 4) (codes 0-15 at the even bits, 16-31 at the odd
+ *     bits).
  *  Signed codes are b-bit two's complement, unsigned codes are plain binary.
  *  Padding bits are written as zero and ignored when read.
  *  A filter [G][C^out][kh][kw][C^in] has the layout of an activation tensor
@@ -123,11 +124,13 @@ void palq_destroy(palq_ctx *ctx);
  * work already queued on the old one (which may still read context memory
  * that later calls reuse). */
 palq_status palq_set_stream(palq_ctx *ctx, void *hip_stream);
-/* Matrix-core format of 2-bit grouped convolutions (Section 4.1): with
- * enable = 1 (the default; environment PALQ_CONV_FP4=0 starts a context at
- * 0) a layer whose accumulator bound sum |w| |x| stays below 2^23 runs on the
- * FP4 (E2M1) matrix cores, where its fp32 accumulator is exact; with 0 every
- * layer runs on int8.  Results are identical either way.  Applies to
+/* Matrix-core format of 2- and 3-bit grouped convolutions (Section 4.1):
+ * with enable = 1 (the default; environment PALQ_CONV_FP4=0 starts a context
+ * at 0) a layer whose accumulator bound sum |w| |x| stays below 2^23 runs on
+ * the FP4 (E2M1) matrix cores if it is a 2-bit layer, on the FP6 (E2M3)
+ * matrix cores if it is a 3-bit layer with 3-bit outputs, 64-channel blocks
+ * and no shortcut, where its fp32 accumulator is exact; with 0 every layer
+ * runs on int8.  Results are identical either way.  Applies to
  * palq_group_conv calls and networks created after the call.
  * PALQ_ERR_ARG: enable not 0 or 1. */
 palq_status palq_set_conv_fp4(palq_ctx *ctx, int32_t enable);

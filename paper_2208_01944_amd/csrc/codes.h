@@ -8,9 +8,10 @@
 
 namespace palq {
 
-// Bit position of bit 2 of code jj (0..31) inside a 3-bit chunk's high word.
+// Bit position of bit 2 of code jj (0..31) inside a 3-bit chunk's high word:
+// codes 0-15 at the even bits, codes 16-31 at the odd bits.
 __host__ __device__ inline int b3_hi_pos(int jj) {
-  return 8 * ((jj >> 2) & 3) + 4 * (jj >> 4) + (jj & 3);
+  return 2 * (jj & 15) + (jj >> 4);
 }
 
 __device__ inline int sext(uint32_t v, int bits) {

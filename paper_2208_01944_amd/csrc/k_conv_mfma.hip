@@ -45,6 +45,7 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 
 
@@ -97,12 +98,13 @@ __device__ inline v4i wt_unpack4(uint32_t y0, uint32_t y1) {
 }
 
 // B = 3: unit j (0/1) of a 32-code chunk: low word lo = bits 0-1 of its 16
-// codes, hi = the chunk's bit-2 word (bit 8e + 4j + d for code 4e + d).
+// codes, hi = the chunk's bit-2 word (bit 8e + 2d + j for code 4e + d of
+// unit j).
 __device__ inline v4i unpack3(uint32_t lo, uint32_t hi, int j) {
   v4i r;
   _Pragma("unroll") for (int d = 0; d < 4; ++d) {
     const uint32_t l2 = (lo >> (2 * d)) & 0x03030303u;
-    const uint32_t h1 = (hi >> (4 * j + d)) & 0x01010101u;
+    const uint32_t h1 = (hi >> (2 * d + j)) & 0x01010101u;
     r[d] = (int)(l2 | (h1 << 2));
   }
   return r;
@@ -299,6 +301,7 @@ __global__ void prepack_kernel(ConvArgs a, Geo geo, uint8_t *wp) {
 // same code index there (as c / 2), so every product is exact and carries a
 // factor 1/4.  One thread per 16-byte lane operand.
 constexpr int kSlab4 = 1024;
+constexpr int kSlab6 = 1536;
 __global__ void prepack_fp4_kernel(ConvArgs a, Geo geo, uint8_t *wp) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int nc32 = a.cout / 32;
@@ -328,6 +331,72 @@ __global__ void prepack_fp4_kernel(ConvArgs a, Geo geo, uint8_t *wp) {
     o[q] = w;
   }
   *(uint4 *)(wp + t * 16) = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+// FP6 (E2M3) weight slabs for 3-bit grouped layers, one MFMA (32 x 32 x 64)
+// per K-block: [G][cout/32][kb_total][1536 B], a slab holding bytes 0-15 of
+// every lane's 24-byte operand (lane l at 16 l), then bytes 16-23 (at
+// 1024 + 8 l).  Field f (bits 6f .. 6f + 5 of the 192-bit operand) of lane
+// (ch, half) holds E2M3 of the weight w of code 32 half + fp6_code(f) of the
+// K-block, exact for w in -4 .. 3; the activation operand (fp6_operand)
+// puts the same code there as the subnormal c / 8, so every product is exact
+// and carries a factor 1/8.
+// K order inside a 32-code chunk: the fields of output word 3 u + d (u: the
+// chunk's low word) take the codes 16 u + 3 m + r(d) (r = 0, 2, 1 for d = 0,
+// 1, 2), whose low bits the word can mask out of the low word in place.
+__host__ __device__ inline int fp6_code(int f) {
+  constexpr int kPerm[16] = {0, 3, 6, 9, 12, 15, 2, 5, 8, 11, 14, 1, 4, 7, 10, 13};
+  return (f & 16) + kPerm[f & 15];
+}
+__global__ void prepack_fp6_kernel(ConvArgs a, Geo geo, uint8_t *wp) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int nc32 = a.cout / 32;
+  const int64_t total = (int64_t)a.in.groups * nc32 * geo.kb_total * 64;
+  if (t >= total) return;
+  const int lane = (int)(t & 63);
+  const int64_t rest = t >> 6;
+  const int kb = (int)(rest % geo.kb_total);
+  const int64_t r2 = rest / geo.kb_total;
+  const int cblk = (int)(r2 % nc32);
+  const int g = (int)(r2 / nc32);
+  const int half = lane >> 5, k = cblk * 32 + (lane & 31);
+  // the K-block's chunk of this lane half: low words, then the bit-2 word
+  const uint32_t *c = (const uint32_t *)(a.w + ((int64_t)g * a.cout + k) * geo.w_ch + (int64_t)kb * 24 + 12 * half);
+  const uint32_t lo0 = c[0], lo1 = c[1], hi = c[2];
+  uint32_t o[6] = {0, 0, 0, 0, 0, 0};
+  for (int f = 0; f < 32; ++f) {
+    const int j = fp6_code(f);
+    const uint32_t v = (((j < 16 ? lo0 : lo1) >> (2 * (j & 15))) & 3u) | (((hi >> b3_hi_pos(j)) & 1u) << 2);
+    // E2M3 (sign, 2 exponent bits with bias 1, 3 mantissa bits) of the
+    // two's complement code v: 0, 1, 2, 3, -4, -3, -2, -1
+    constexpr uint32_t kE2M3[8] = {0x00, 0x08, 0x10, 0x14, 0x38, 0x34, 0x30, 0x28};
+    const uint32_t e = kE2M3[v];
+    const int bit = 6 * f;
+    o[bit >> 5] |= e << (bit & 31);
+    if ((bit & 31) > 26) o[(bit >> 5) + 1] |= e >> (32 - (bit & 31));
+  }
+  uint8_t *slab = wp + (t >> 6) * kSlab6;
+  *(uint4 *)(slab + lane * 16) = make_uint4(o[0], o[1], o[2], o[3]);
+  *(uint2 *)(slab + 1024 + lane * 8) = make_uint2(o[4], o[5]);
+}
+
+// MFMA operand of a lane's 32-code chunk (x: low words 0, 1 and the bit-2
+// word) as E2M3 subnormals c / 8, fields in the fp6_code order: word 3 u + d
+// = low word u masked to its fields' code pairs, or'ed with the bit-2 word
+// rotated so that bit 2 of each of those codes lands two bits above its pair
+// (codes 0-15 sit at even bits: rotate by 2; codes 16-31 at odd bits: by 1).
+__device__ inline v8i fp6_operand(uint32_t lo0, uint32_t lo1, uint32_t hi) {
+  const uint32_t r0 = __builtin_amdgcn_alignbit(hi, hi, 30), r1 = __builtin_amdgcn_alignbit(hi, hi, 31);
+  v8i d;
+  d[0] = (int)((lo0 & 0xC30C30C3u) | (r0 & 0x04104104u));
+  d[1] = (int)((lo0 & 0x30C30C30u) | (r0 & 0x41041041u));
+  d[2] = (int)((lo0 & 0x0C30C30Cu) | (r0 & 0x10410410u));
+  d[3] = (int)((lo1 & 0xC30C30C3u) | (r1 & 0x04104104u));
+  d[4] = (int)((lo1 & 0x30C30C30u) | (r1 & 0x41041041u));
+  d[5] = (int)((lo1 & 0x0C30C30Cu) | (r1 & 0x10410410u));
+  d[6] = 0;
+  d[7] = 0;
+  return d;
 }
 
 // Buffer resource over `bytes` bytes at `base`: loads at an offset >= bytes
@@ -445,7 +514,7 @@ __device__ __forceinline__ void epilogue(const ConvArgs &a, const Geo &geo, v16i
           }
           if (bo == 3) {
             qword |= (uint32_t)(q & 3) << (2 * e);
-            hword |= (uint32_t)((q >> 2) & 1) << e;
+            hword |= (uint32_t)((q >> 2) & 1) << (2 * e);
           } else {
             qword |= (uint32_t)q << (bo * e);
           }
@@ -473,10 +542,8 @@ __device__ __forceinline__ void epilogue(const ConvArgs &a, const Geo &geo, v16i
       uint32_t hpart = 0;
       if (bo == 3) {
 #pragma unroll
-        for (int qi = 0; qi < 4; ++qi) {
-          const int Qn = 2 * qi + half;
-          hpart |= hq[pb][qi] << (8 * (Qn & 3) + 4 * (Qn >> 2));
-        }
+        for (int qi = 0; qi < 4; ++qi)  // channel 8 qi + 4 half + e at bit 2 (c & 15) + (c >> 4)
+          hpart |= hq[pb][qi] << (16 * (qi & 1) + 8 * half + (qi >> 1));
         hpart |= (uint32_t)__shfl_xor((int)hpart, 32);
       }
       if (mp >= geo.M) continue;
@@ -503,7 +570,9 @@ typedef double dbl2 __attribute__((ext_vector_type(2)));
 
 // Output width BO is a compile-time constant here; fma -> saturating
 // unsigned conversion (negative values and NaN give 0, which is the ReLU
-// clamp) -> min with 2^BO - 1 -> shift into the quad's word.
+// clamp) -> min with 2^BO - 1 -> shift into the quad's word.  BO = 3: the
+// quad's low bit pairs form the 2-bit word as for BO = 2 and its bit 2 go
+// to the chunk's bit-2 word (the two lane halves' parts or'ed together).
 // AccV = v16f: the FP4 tile kernel's accumulator, t / 4 held exactly (the
 // constants carry the factor 4); its shortcut term rm c / 4 is added in
 // fp32, exact because the layer's |t| + 3 |rm| stays below 2^24 (a multiple
@@ -537,6 +606,7 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
   for (int cb = 0; cb < CB; ++cb) {
     const int kc = ch0 + cb * 32;
     uint32_t qv[PB][4];
+    uint32_t hv[PB][4];
     uint32_t rwc[PB][2];
     if constexpr (RB == 2 && LAZY && PB == 2) {
       uint2 r0, r1;
@@ -598,15 +668,22 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] += (rmu[e] * rc[e]) << lsc;
         }
-        uint32_t qword = 0;
+        uint32_t qword = 0, hword = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const double d = __builtin_fma((double)v[e], k[e].x, k[e].y);
           uint32_t q;
           asm("v_cvt_u32_f64 %0, %1" : "=v"(q) : "v"(d));
-          qword |= min(q, qmax) << (bo * e);
+          if constexpr (BO == 3) {
+            const uint32_t qq = min(q, qmax);
+            qword |= (qq & 3u) << (2 * e);
+            hword |= (qq >> 2) << (2 * e);
+          } else {
+            qword |= min(q, qmax) << (bo * e);
+          }
         }
         qv[pb][qi] = qword;
+        hv[pb][qi] = hword;
       }
     }
 #pragma unroll
@@ -618,6 +695,19 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
       const auto p0 = __builtin_amdgcn_permlane32_swap(qv[pb][0], qv[pb][2], false, false);
       const auto p1 = __builtin_amdgcn_permlane32_swap(qv[pb][1], qv[pb][3], false, false);
       const uint32_t Q[4] = {p0[0], p0[1], p1[0], p1[1]};
+      if constexpr (BO == 3) {
+        // bit 2 of channel c = 8 qi + 4 half + e at bit 2 (c & 15) + (c >> 4)
+        uint32_t hp = 0;
+#pragma unroll
+        for (int qi = 0; qi < 4; ++qi) hp |= hv[pb][qi] << (16 * (qi & 1) + 8 * half + (qi >> 1));
+        const auto hs = __builtin_amdgcn_permlane32_swap(hp, hp, false, false);
+        const uint32_t hw = hs[0] | hs[1];
+        if (mp >= geo.M) continue;
+        uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row) + (int64_t)(kc >> 5) * 3;
+        cw[half] = Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24);
+        if (half == 0) cw[2] = hw;
+        continue;
+      }
       if (mp >= geo.M) continue;
       uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row) +
                      (int64_t)(kc >> 5) * bo + half * (bo / 2);
@@ -1853,37 +1943,63 @@ __global__ __launch_bounds__(sp::NT, 2) void stem_pool_kernel(ConvArgs a, Geo ge
 __device__ __forceinline__ int uniform_int(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 namespace f4 {
-template <int CB, int PB, int WN, int WM>
+template <int CB, int PB, int WN, int WM, int B = 2>
 struct Cfg {
   static constexpr int NT = WN * WM * 64;
   static constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
-  static constexpr int WST = TN / 32 * kSlab4;  // weight bytes of a K-block
-  static constexpr int XST = TM * 16;           // activation bytes of a K-block
+  static constexpr int SLAB = B == 2 ? kSlab4 : kSlab6;  // weight bytes per 32 channels and K-block
+  static constexpr int PPX = B == 2 ? 1 : 2;             // 16-byte activation pieces per pixel and K-block
+  static constexpr int WST = TN / 32 * SLAB;  // weight bytes of a K-block
+  static constexpr int XST = TM * 16 * PPX;   // activation bytes of a K-block
   static constexpr int SST = WST + XST;
   static constexpr int WP = WST / 16, XP = XST / 16;  // 16-byte pieces
   static_assert(WP % 64 == 0 && XP % 64 == 0 && WP <= 2 * NT && XP <= 2 * NT, "whole waves of pieces");
   static constexpr int WL = WP > NT ? 2 : 1, XL = XP > NT ? 2 : 1;  // loads per loading thread
+  // whether wave w issues weight (activation) load i: fewer pieces than
+  // threads go to the last (first) waves, more to every thread and then to
+  // the first waves
+  static constexpr bool wloads(int w, int i) { return WP < NT ? (i == 0 && 64 * w >= NT - WP) : 64 * w + i * NT < WP; }
+  static constexpr bool xloads(int w, int i) { return XP < NT ? (i == 0 && 64 * w < XP) : 64 * w + i * NT < XP; }
+  static constexpr int loads(int w) {
+    int n = 0;
+    for (int i = 0; i < WL; ++i) n += wloads(w, i) ? 1 : 0;
+    for (int i = 0; i < XL; ++i) n += xloads(w, i) ? 1 : 0;
+    return n;
+  }
+  static constexpr int min_loads() {
+    int m = 1 << 30;
+    for (int w = 0; w < NT / 64; ++w) m = loads(w) < m ? loads(w) : m;
+    return m;
+  }
   // loads per K-block of the waves with the fewest (the ring waits on that)
-  static constexpr int LPK = (WP >= NT ? WL : 0) + (XP >= NT ? XL : 0) > 0 ? (WP >= NT ? WL : 0) + (XP >= NT ? XL : 0) : 1;
+  static constexpr int LPK = min_loads();
+  static_assert(LPK >= 1, "every wave loads in every K-block");
   static constexpr int RPX = TN / 4;          // shortcut code bytes per pixel
   static constexpr int RSB = TM * RPX;        // shortcut codes of a tile
 };
 }  // namespace f4
 
-template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S>
-__global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, Geo geo, int npt, int ncb, int nch) {
-  using C = f4::Cfg<CB, PB, WN, WM>;
+// B = 2: FP4 operands (conv_fp4_kernel); B = 3: 3-bit layers on FP6 (E2M3)
+// matrix cores (conv_fp6_kernel): 1536-byte weight slabs (prepack_fp6_kernel),
+// each pixel's K-block staged as its two 12-byte chunks in 16-byte pieces
+// (the chunk's three words at the start of each), fp6_operand, and a 3-bit
+// fast epilogue; no shortcut.
+template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S, int B>
+__device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo, int npt, int ncb, int nch) {
+  using C = f4::Cfg<CB, PB, WN, WM, B>;
   constexpr int NT = C::NT, TN = C::TN, TM = C::TM, WST = C::WST, SST = C::SST;
   constexpr int RPT = RB ? C::RSB / (NT * 16) : 0;  // 16-byte shortcut pieces per thread
   static_assert(RB == 0 || RPT * NT * 16 == C::RSB, "whole shortcut pieces per thread");
   static_assert(CB == 2 && (PB == 2 || PB == 4), "operand reads are written for 2 x 2 and 2 x 4 blocks");
+  static_assert(B == 2 || (B == 3 && PB == 2 && RB == 0), "FP6: 2 x 2 blocks, no shortcut");
+  constexpr int XB = B == 2 ? 16 : 24;  // activation bytes of a pixel's K-block
   __shared__ __attribute__((aligned(1024))) uint8_t lds[S * SST + (RB ? C::RSB : 16)];
   __shared__ RqConst rq_area[TN];
   __shared__ int32_t rm_area[RB ? TN : 1];
 
   // the launcher takes 2-bit outputs and 2-bit (or no) shortcuts only; a
   // layer whose fp64 requant could be inexact runs on the general partner
-  if (int64_flag(a, geo) || a.out.bits != 2 || RB < 0) return;
+  if (int64_flag(a, geo) || a.out.bits != B || RB < 0) return;
   const int G = a.in.groups;
   const int T = npt * ncb * G;
   // workgroup i -> XCD x = i mod 8, which takes the x-th eighth of the tiles
@@ -1909,32 +2025,34 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, G
   typedef __attribute__((address_space(3))) void *lds_ptr;
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
 
-  const auto rw_src = make_rsrc(geo.wp, (int64_t)G * a.cout * KB * (kSlab4 / 32));
+  const auto rw_src = make_rsrc(geo.wp, (int64_t)G * a.cout * KB * (C::SLAB / 32));
   const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
   const auto rpj = a.proj.data ? make_rsrc(a.proj.data, (int64_t)a.proj.n * a.proj.h * a.proj.w * a.proj.pixel)
                                : make_rsrc(a.in.data, 0);
   const auto rres = make_rsrc(a.res.data, a.res.data ? (int64_t)a.res.n * a.res.h * a.res.w * a.res.pixel : 0);
   const int pixb = (int)a.in.pixel, rowb = a.in.w * pixb;
 
-  // ---- this thread's fetch pieces.  Weights: piece c = tid - (NT - WP)
-  // (+ NT) of the tile's slabs: slab c / 64, lane operand c % 64.
-  // Activations: piece tid (+ NT) = pixel tid (+ NT) of the tile.
-  const bool wload = C::WP >= NT || tid >= NT - C::WP;  // wave-uniform
+  // ---- this thread's fetch pieces (wave w issues load i if C::wloads /
+  // C::xloads (w, i)).  Weights: piece c = tid - (NT - WP) (or tid + i NT)
+  // of the tile's slabs: slab c / (SLAB / 16), 16-byte piece c % (SLAB / 16).
+  // Activations, piece q = tid + i NT: B = 2, pixel q of the tile; B = 3,
+  // chunk (q >> 5) & 1 of pixel 32 (q >> 6) + (q & 31).
+  constexpr int PPS = C::SLAB / 16;  // pieces per slab
   const int wc = C::WP >= NT ? tid : tid - (NT - C::WP);
   uint32_t woff[C::WL];
 #pragma unroll
   for (int i = 0; i < C::WL; ++i) {
     const int c = wc + i * NT;
-    woff[i] = (uint32_t)((((int64_t)g * (a.cout / 32) + cbk * (TN / 32) + (c >> 6)) * KB) * kSlab4 + (c & 63) * 16);
+    woff[i] = (uint32_t)((((int64_t)g * (a.cout / 32) + cbk * (TN / 32) + c / PPS) * KB) * C::SLAB + (c % PPS) * 16);
   }
-  const bool xload = C::XP >= NT || tid < C::XP;  // wave-uniform
   const int HW = a.ho * a.wo;
   const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
   int off0[C::XL], poff[C::XL];
   uint32_t tmask[C::XL];
 #pragma unroll
   for (int i = 0; i < C::XL; ++i) {
-    const int m = pt * TM + tid + i * NT;
+    const int q = tid + i * NT;
+    const int m = pt * TM + (B == 2 ? q : 32 * (q >> 6) + (q & 31));
     const bool valid = m < geo.M;
     const int mm = valid ? m : 0;
     const int n = fdiv(mm, HW, inv_hw);
@@ -1942,7 +2060,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, G
     const int oy = fdiv(rem, a.wo, inv_wo);
     const int ox = rem - oy * a.wo;
     const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
-    off0[i] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.row;
+    off0[i] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.row + (B == 3 ? 12 * ((q >> 5) & 1) : 0);
     const int xlo = max(0, -ix0), xhi = min(a.kw, a.in.w - ix0);
     const uint32_t below = xhi >= 32 ? 0xffffffffu : ((1u << max(xhi, 0)) - 1u);
     const uint32_t cols = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
@@ -1980,24 +2098,23 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, G
         }
       }
     }
-    if (wload) {
 #pragma unroll
-      for (int i = 0; i < C::WL; ++i)
+    for (int i = 0; i < C::WL; ++i)
+      if (C::wloads(wave, i))
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + ((wc + i * NT) & ~63) * 16), 16, (int)woff[i],
-                                                 f_kb * kSlab4, 0, 0);
-    }
-    if (xload) {
-      if (f_kb < KM) {
+                                                 f_kb * C::SLAB, 0, 0);
+    if (f_kb < KM) {
 #pragma unroll
-        for (int i = 0; i < C::XL; ++i)
+      for (int i = 0; i < C::XL; ++i)
+        if (C::xloads(wave, i))
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rin, (lds_ptr)(ws + WST + i * NT * 16 + wave * 1024), 16, (int)vo[i],
-                                                   f_c * 16, 0, 0);
-      } else {
+                                                   f_c * XB, 0, 0);
+    } else {
 #pragma unroll
-        for (int i = 0; i < C::XL; ++i)
+      for (int i = 0; i < C::XL; ++i)
+        if (C::xloads(wave, i))
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rpj, (lds_ptr)(ws + WST + i * NT * 16 + wave * 1024), 16,
                                                    (int)poff[i], (f_kb - KM) * 16, 0, 0);
-      }
     }
     ++f_kb;
     if (++f_c == geo.cpb) {  // next tap
@@ -2023,10 +2140,42 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, G
   // LDS addresses of this lane's operands in stage 0: activation half row of
   // pixel block 0 (blocks 512 bytes apart), weight unit of channel block 0
   // (blocks 1 KB apart)
-  const uint32_t xaddr0 = lds_base + WST + (uint32_t)((wm * PB * 32 + l32) * 16 + half * 8);
-  const uint32_t aaddr0 = lds_base + (uint32_t)((wn * CB) * kSlab4 + (half * 32 + l32) * 16);
+  // (B = 3: chunk half of pixel block 0 at 1 KB blocks, the weight unit's
+  // first 16 bytes and its last 8 bytes, slabs 1536 bytes apart)
+  const uint32_t xaddr0 = lds_base + WST +
+                          (uint32_t)(B == 2 ? (wm * PB * 32 + l32) * 16 + half * 8 : ((wm * PB) * 64 + lane) * 16);
+  const uint32_t aaddr0 = lds_base + (uint32_t)((wn * CB) * C::SLAB + lane * 16);
+  const uint32_t baddr0 = lds_base + (uint32_t)((wn * CB) * C::SLAB + 1024 + lane * 8);
   auto kblock = [&](int st) __attribute__((always_inline)) {
     const uint32_t xa = xaddr0 + st * SST, aa = aaddr0 + st * SST;
+    if constexpr (B == 3) {
+      const uint32_t ba = baddr0 + st * SST;
+      v4i x0, x1, A0, A1;
+      v2i B0, B1;
+      asm volatile(
+          "ds_read_b128 %0, %6\n\t"
+          "ds_read_b128 %1, %6 offset:1024\n\t"
+          "ds_read_b128 %2, %7\n\t"
+          "ds_read_b64 %3, %8\n\t"
+          "ds_read_b128 %4, %7 offset:1536\n\t"
+          "ds_read_b64 %5, %8 offset:1536\n\t"
+          "s_waitcnt lgkmcnt(0)"
+          : "=&v"(x0), "=&v"(x1), "=&v"(A0), "=&v"(B0), "=&v"(A1), "=&v"(B1)
+          : "v"(xa), "v"(aa), "v"(ba));
+      __builtin_amdgcn_sched_barrier(0);
+      const v4i B0w = __builtin_shufflevector(B0, B0, 0, 1, -1, -1), B1w = __builtin_shufflevector(B1, B1, 0, 1, -1, -1);
+      const v8i Aop[CB] = {__builtin_shufflevector(A0, B0w, 0, 1, 2, 3, 4, 5, -1, -1),
+                           __builtin_shufflevector(A1, B1w, 0, 1, 2, 3, 4, 5, -1, -1)};
+      const v4i X[2] = {x0, x1};
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        const v8i Bop = fp6_operand((uint32_t)X[pb][0], (uint32_t)X[pb][1], (uint32_t)X[pb][2]);
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+          acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop[cb], Bop, acc[cb][pb], 2, 2, 0, 0, 0, 0);
+      }
+      return;
+    }
     uint2 xw[PB];
     v4i A0, A1;
     if constexpr (PB == 4) {
@@ -2106,7 +2255,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, G
         for (int qi = 0; qi < 4; ++qi) {
           v4i dv;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) dv[e] = (int)(acc[cb][pb][4 * qi + e] * 4.0f);  // exact: |4 acc| < 2^23
+          for (int e = 0; e < 4; ++e) dv[e] = (int)(acc[cb][pb][4 * qi + e] * (B == 2 ? 4.0f : 8.0f));  // exact: |t| < 2^23
           *(v4i *)(dst + 8 * qi) = dv;
         }
       }
@@ -2115,9 +2264,18 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, G
   // ra + pb 32 RPX + 8 cb (read per channel block by the epilogue)
   const uint32_t ra = RB == 2 ? lds_base + S * SST + (uint32_t)((wm * PB * 32 + l32) * C::RPX + wn * CB * 8) : 0u;
   uint32_t rw[CB][PB][2] = {};
-  epilogue_fast_bo<2, CB, PB, RB, v16f, true>(a, geo, acc, rw, mbase, g, gd, cbk * TN + wn * CB * 32, l32, half,
+  epilogue_fast_bo<B, CB, PB, RB, v16f, true>(a, geo, acc, rw, mbase, g, gd, cbk * TN + wn * CB * 32, l32, half,
                                                 rq_area + wn * CB * 32, rm_area + (RB ? wn * CB * 32 : 0), ra,
                                                 32 * C::RPX);
+}
+
+template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S>
+__global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, Geo geo, int npt, int ncb, int nch) {
+  conv_fpx_tile<CB, PB, WN, WM, RB, DUMP, S, 2>(a, geo, npt, ncb, nch);
+}
+template <int CB, int PB, int WN, int WM, bool DUMP, int S>
+__global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp6_kernel(ConvArgs a, Geo geo, int npt, int ncb, int nch) {
+  conv_fpx_tile<CB, PB, WN, WM, 0, DUMP, S, 3>(a, geo, npt, ncb, nch);
 }
 
 // ---------------------------------------------------------------- launch
@@ -2221,6 +2379,7 @@ int64_t acc_bound_of(const ConvArgs &a) {
 }  // namespace
 
 bool fp4_applies(const ConvArgs &a);
+bool fp6_applies(const ConvArgs &a);
 bool tile_kernel_applies(const ConvArgs &a);
 bool stem_tile_applies(const ConvArgs &a);
 bool stem_rows(const ConvArgs &a);
@@ -2251,6 +2410,10 @@ ConvPlan conv_mfma_plan(const ConvArgs &a) {
   p.w_bytes = (size_t)a.in.groups * a.cout * geo.kb_total * 64;
   p.thr_bytes = (size_t)a.in.groups * a.cout * sizeof(RqConst) + 16;  // + int64-path flag
   if (stem_rows(a)) p.w_bytes += (size_t)a.cout * sp::KH * 32;  // the filter-row copy
+  if (fp6_applies(a)) {  // FP6 slabs and constants after the int8 ones
+    p.w_bytes += (size_t)a.in.groups * a.cout * geo.kb_total * 48;
+    p.thr_bytes *= 2;
+  }
   if (fp4_applies(a)) {  // FP4 slabs and constants after the int8 ones (the general build keeps those)
     p.w_bytes += (size_t)a.in.groups * a.cout * geo.kb_total * 32;
     p.thr_bytes *= 2;
@@ -2287,6 +2450,15 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
   hipLaunchKernelGGL(requant_prep_kernel, dim3(1), dim3(256), 0, s, a.mult, a.shift, a.bias, a.res.data ? a.res_mult : nullptr,
                      res_max, nch, lscale, acc_bound, rq, (int32_t *)(rq + nch));
   e = hipGetLastError();
+  if (e == hipSuccess && fp6_applies(a)) {
+    const int64_t lanes = (int64_t)a.in.groups * (a.cout / 32) * geo.kb_total * 64;
+    hipLaunchKernelGGL(prepack_fp6_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, s, a, geo,
+                       wp + (size_t)a.in.groups * a.cout * geo.kb_total * 64);
+    RqConst *rq6 = rq + nch + 1;  // the FP6 accumulator is t / 8
+    hipLaunchKernelGGL(requant_prep_kernel, dim3(1), dim3(256), 0, s, a.mult, a.shift, a.bias, nullptr, 0, nch, -3,
+                       acc_bound, rq6, (int32_t *)(rq6 + nch));
+    return hipGetLastError();
+  }
   if (e != hipSuccess || !fp4_applies(a)) return e;
   const int64_t pieces = (int64_t)a.in.groups * (a.cout / 32) * geo.kb_total * 64;
   hipLaunchKernelGGL(prepack_fp4_kernel, dim3((unsigned)((pieces + 255) / 256)), dim3(256), 0, s, a, geo,
@@ -2300,7 +2472,7 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
 bool conv_mfma_pads_input(const ConvArgs &a) { return is_stem(a) && a.pad > 0; }
 
 int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr) {
-  if (a.out.bits == 3 || (a.res.data && a.res.bits != 2)) return 1;
+  if ((a.out.bits == 3 && !fp6_applies(a)) || (a.res.data && a.res.bits != 2)) return 1;
   int32_t flag = 0;
   const RqConst *rq = (const RqConst *)thr;
   if (hipMemcpy(&flag, rq + (int64_t)a.in.groups * a.cout, sizeof(flag), hipMemcpyDeviceToHost) != hipSuccess)
@@ -2369,6 +2541,17 @@ bool fp4_applies(const ConvArgs &a) {
   return a.fp4 && tile_kernel_applies(a) && acc_bound_of(a) < ((int64_t)1 << 23);
 }
 
+// FP6 matrix cores for 3-bit grouped layers with 3-bit outputs, 64-channel
+// blocks and no shortcut, under the same accumulator bound (the fp32
+// accumulator holds t / 8: a multiple of 1/8 below 2^20 is exact) and the
+// same context switch.
+bool fp6_applies(const ConvArgs &a) {
+  const int64_t wbytes = (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64;
+  return a.fp4 && !is_stem(a) && a.in.bits == 3 && a.w_bits == 3 && a.out.bits == 3 && !a.in.is_signed &&
+         !a.res.data && !a.proj.data && a.cout % 64 == 0 && a.in.cpg % 64 == 0 && wbytes < ((int64_t)1 << 30) &&
+         acc_bound_of(a) < ((int64_t)1 << 23);
+}
+
 // The stem on the tiled kernel: explicit zero border (pad 0), 128-channel
 // blocks, no shortcut, no accumulator dump.
 bool stem_tile_applies(const ConvArgs &a) {
@@ -2389,7 +2572,12 @@ size_t stem_rows_offset(const ConvArgs &a) { return (size_t)a.in.groups * a.cout
 // waves, 256-pixel tiles), 128-channel blocks (2 x 2 waves, 128 pixels) or
 // 128-channel blocks with 2 x 4 blocks per wave (256 pixels); 2-bit layers on
 // int8 with 64- or 128-channel blocks (256 pixels).
-enum TileBuild { kTileNone = 0, kTileStem, kTileFp4C64, kTileFp4C128, kTileFp4C128P4, kTileI8C64, kTileI8C128 };
+// 3-bit layers on FP6 with 64-channel (1 x 4 waves, 256 pixels) or
+// 128-channel blocks (2 x 2 waves, 128 pixels).
+enum TileBuild {
+  kTileNone = 0, kTileStem, kTileFp4C64, kTileFp4C128, kTileFp4C128P4, kTileFp6C64, kTileFp6C128, kTileI8C64,
+  kTileI8C128
+};
 
 // 2 x 4 blocks per wave (256-pixel tiles) for 128-channel FP4 layers where
 // the bigger tiles leave every CU at least one and do not lengthen the
@@ -2412,7 +2600,12 @@ struct ConvChoice {
 
 ConvChoice conv_choice(const ConvArgs &a, const Geo &geo, int epi) {
   ConvChoice c{kTileNone, pick_cb(a, geo)};
-  if (a.out.bits == 3 || epi == 1) return c;
+  if (epi == 1) return c;
+  if (fp6_applies(a)) {
+    c.tile = a.cout % 128 ? kTileFp6C64 : kTileFp6C128;
+    return c;
+  }
+  if (a.out.bits == 3) return c;
   if (stem_tile_applies(a)) c.tile = kTileStem;
   else if (fp4_applies(a)) c.tile = a.cout % 128 ? kTileFp4C64 : fp4_pb4_pays(a, geo) ? kTileFp4C128P4 : kTileFp4C128;
   else if (tile_kernel_applies(a)) c.tile = a.cout % 128 ? kTileI8C64 : kTileI8C128;
@@ -2422,18 +2615,26 @@ ConvChoice conv_choice(const ConvArgs &a, const Geo &geo, int epi) {
 // The FP4 grouped kernel: one workgroup per tile, XCD-contiguous runs of the
 // chunked tile order (32 chunks where the packed input outweighs the filter,
 // as in launch_tile).
-template <int CB, int PB, int WN, int WM>
-hipError_t launch_fp4(const ConvArgs &a, const Geo &geo, hipStream_t s) {
+template <int B, int CB, int PB, int WN, int WM>
+hipError_t launch_fpx(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   constexpr int S = 4;
-  using C = f4::Cfg<CB, PB, WN, WM>;
+  using C = f4::Cfg<CB, PB, WN, WM, B>;
   const int npt = (int)((geo.M + C::TM - 1) / C::TM);
   const int ncb = a.cout / C::TN;
   const int64_t T = (int64_t)npt * ncb * a.in.groups;
   if (T <= 0 || T > 0x3fffffff || geo.kb_total < 1) return hipErrorInvalidValue;
-  const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * 32;
+  const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * (C::SLAB / 32);
   const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
   const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(32, npt) : 1;
   const dim3 grid((unsigned)((T + 7) / 8 * 8)), block(C::NT);
+  if constexpr (B == 3) {
+    if (a.res.data || a.proj.data) return hipErrorNotSupported;
+    if (!a.acc_dump)
+      hipLaunchKernelGGL((conv_fp6_kernel<CB, PB, WN, WM, false, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    else
+      hipLaunchKernelGGL((conv_fp6_kernel<CB, PB, WN, WM, true, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    return hipGetLastError();
+  }
   if (!a.res.data && !a.acc_dump)
     hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, false, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else if (!a.acc_dump)
@@ -2526,6 +2727,7 @@ const char *conv_kernel_label(const ConvArgs &a, int epi) {
   switch (conv_choice(a, geo, epi).tile) {
     case kTileStem: return "conv_tile_kernel[stem]";
     case kTileFp4C64: case kTileFp4C128: case kTileFp4C128P4: return "conv_fp4_kernel";
+    case kTileFp6C64: case kTileFp6C128: return "conv_fp6_kernel";
     case kTileI8C64: case kTileI8C128: return "conv_tile_kernel[int8]";
     default: return is_stem(a) ? "conv_stem_kernel" : "conv_grouped_kernel";
   }
@@ -2543,15 +2745,17 @@ hipError_t launch_conv_mfma(const ConvArgs &a_in, const uint8_t *wp, const int32
   if (a.acc_dump && c.tile == kTileNone) epi = 1;  // only the general persistent build dumps
   hipError_t e = hipSuccess;
   const int nch = a.in.groups * a.cout;
-  Geo g4 = geo;  // FP4 slabs and constants follow the int8 ones
+  Geo g4 = geo;  // FP4 (FP6) slabs and constants follow the int8 ones
   g4.wp = wp + (size_t)nch * geo.kb_total * 64;
   g4.rq = geo.rq + nch + 1;
   constexpr int S4 = PALQ_TILE_STAGES;
   switch (c.tile) {
     case kTileStem: e = launch_tile<2, 2, 2, 2, true, PALQ_STEM_STAGES>(a, geo, s); break;
-    case kTileFp4C64: e = launch_fp4<2, 2, 1, 4>(a, g4, s); break;
-    case kTileFp4C128: e = launch_fp4<2, 2, 2, 2>(a, g4, s); break;
-    case kTileFp4C128P4: e = launch_fp4<2, 4, 2, 2>(a, g4, s); break;
+    case kTileFp4C64: e = launch_fpx<2, 2, 2, 1, 4>(a, g4, s); break;
+    case kTileFp4C128: e = launch_fpx<2, 2, 2, 2, 2>(a, g4, s); break;
+    case kTileFp4C128P4: e = launch_fpx<2, 2, 4, 2, 2>(a, g4, s); break;
+    case kTileFp6C64: e = launch_fpx<3, 2, 2, 1, 4>(a, g4, s); break;
+    case kTileFp6C128: e = launch_fpx<3, 2, 2, 2, 2>(a, g4, s); break;
     case kTileI8C64: e = launch_tile<2, 2, 1, 4>(a, geo, s); break;
     case kTileI8C128: e = launch_tile<2, 2, 2, 4>(a, geo, s); break;
     default: break;

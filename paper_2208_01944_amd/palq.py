@@ -200,7 +200,8 @@ class Context:
         self._check(_set_stream(self.h, stream.cuda_stream))
 
     def set_conv_fp4(self, enable: bool):
-        """FP4 matrix cores for exact 2-bit layers (True) or int8 only."""
+        """FP4 (2-bit) and FP6 (3-bit) matrix cores for exact layers (True) or
+        int8 only."""
         self._check(_set_conv_fp4(self.h, int(bool(enable))))
 
     # ----------------------------------------------------------- memory

@@ -13,7 +13,7 @@ def row_bytes(codes: int, bits: int) -> int:
 
 
 def b3_hi_pos(j: int) -> int:
-    return 8 * ((j >> 2) & 3) + 4 * (j >> 4) + (j & 3)
+    return 2 * (j & 15) + (j >> 4)
 
 
 def pack_row(codes, bits: int) -> bytes:

@@ -50,8 +50,10 @@ def test_packref_golden_bytes():
     # 3-bit: code 5 (0b101) at j=0 -> low bits 01 at bit 0, bit 2 at hi bit 0
     b = packref.pack_row([5] + [0] * 31, 3)
     assert b[0] == 1 and b[8] == 1 and sum(b) == 2
-    b = packref.pack_row([0] * 17 + [4] + [0] * 14, 3)  # j=17: hi bit 8*0+4*1+1 = 5
-    assert int.from_bytes(b[8:12], "little") == 1 << 5 and sum(b[:8]) == 0
+    b = packref.pack_row([0] * 17 + [4] + [0] * 14, 3)  # j=17: hi bit 2*(17 & 15) + 1 = 3
+    assert int.from_bytes(b[8:12], "little") == 1 << 3 and sum(b[:8]) == 0
+    b = packref.pack_row([0] * 5 + [4] + [0] * 25 + [4], 3)  # j=5: hi bit 10; j=31: hi bit 31
+    assert int.from_bytes(b[8:12], "little") == (1 << 10) | (1 << 31) and sum(b[:8]) == 0
 
 
 @pytest.mark.parametrize("bits", [2, 3, 4, 8])

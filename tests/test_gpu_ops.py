@@ -173,9 +173,10 @@ def test_conv_cases(ctx, torch, i, shuffle):
     check_conv(ctx, torch, case, centred=(shuffle == 1))
 
 
-@pytest.mark.parametrize("i", [0, 1, 2, 5, 9, 10])
+@pytest.mark.parametrize("i", [0, 1, 2, 3, 5, 9, 10])
 def test_conv_cases_int8_matrix_cores(ctx, torch, i):
-    """The 2-bit cases with the FP4 matrix cores switched off (int8 only)."""
+    """The 2-bit cases (and the 3-bit one) with the FP4 / FP6 matrix cores
+    switched off (int8 only)."""
     p = dict(CONV_CASES[i])
     say(f"conv case {i} {p} int8 only")
     case = I.single_layer(1000 + i, shuffle=1, **p)
@@ -281,9 +282,10 @@ def test_conv_c2_full_batch_every_image(ctx, torch, layer):
 @pytest.mark.parametrize("bits", [2, 3, 4])
 def test_conv_c4_sweep_every_image(ctx, torch, groups, bits):
     """The G x B sweep on the 14x14 / 256-channel layer at batch 128: every
-    image (3- and 4-bit layers have no FP4 path)."""
+    image, on the FP4 (2-bit) and FP6 (3-bit) matrix cores and on int8
+    (4-bit layers have only the int8 path)."""
     say(f"conv C4 G={groups} b={bits} batch 128 (every image)")
-    check_full(ctx, torch, I.config_c4(groups, bits), (True, False) if bits == 2 else (True,))
+    check_full(ctx, torch, I.config_c4(groups, bits), (True, False) if bits in (2, 3) else (True,))
 
 
 @pytest.mark.parametrize("pb4", [False, True])
@@ -298,6 +300,38 @@ def test_conv_tile_chunked_xcd_order_centred(ctx, torch, pb4):
     else:
         case = I.single_layer(2202, n=8, h=28, w=28, groups=4, cin=64, cout=64, shuffle=3)
     say(f"conv tiled chunk order pb4={pb4} {case['x'].shape}")
+    check_full(ctx, torch, case)
+
+
+FP6_CASES = {
+    # 64-channel build in the chunked tile order (the packed input outweighs the filter 7x)
+    "c64_chunked": dict(n=8, h=28, w=28, groups=4, cin=64, cout=64, shuffle=3),
+    # 128-channel build, ragged last tile, 128-channel input (two K-blocks per tap)
+    "c128_ragged": dict(n=3, h=11, w=13, groups=2, cin=128, cout=128, shuffle=1),
+    # strided 1x1 layer, three groups
+    "c64_1x1_s2": dict(n=4, h=16, w=16, groups=3, cin=64, cout=192, k=1, stride=2, pad=0, shuffle=-1),
+}
+
+
+@pytest.mark.parametrize("name", sorted(FP6_CASES))
+def test_conv_fp6_builds(ctx, torch, name):
+    """3-bit layers on the FP6 (E2M3) matrix cores: the layer's plan names
+    conv_fp6_kernel (conv_grouped_kernel with the low-precision formats
+    switched off), and every image's accumulators (dump build) and codes,
+    stated and centred, equal the oracle's on both paths."""
+    from paper_2208_01944_amd import palq
+    case = I.single_layer(2300 + sorted(FP6_CASES).index(name), bits=3, **FP6_CASES[name])
+    L = case["layer"]
+    say(f"conv FP6 {name} {case['x'].shape}")
+    for fp, want in ((True, "conv_fp6_kernel"), (False, "conv_grouped_kernel")):
+        ctx.set_conv_fp4(fp)
+        try:
+            t = _layer_tensors(ctx, case, L["bias"])
+            plan = palq.ConvPlan(ctx, t["x"], t["w"], L["stride"], L["pad"], t["mult"], t["shift"], t["bias"],
+                                 t["out"], shuffle=L["shuffle"])
+            assert plan.kernels == want, plan.kernels
+        finally:
+            ctx.set_conv_fp4(True)
     check_full(ctx, torch, case)
 
 
