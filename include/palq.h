@@ -30,6 +30,8 @@
  *   - b in {2, 4, 8}: code j sits at bits [b*j, b*j + b) of the row read as
  *     one little-endian bit string; the row is padded with zero bits to a
  *     multiple of 32 bits.
+ *   - b = 6: stored as b = 8 (code j in bits 0-5 of byte j, bits 6-7 zero),
+ *     for dense 6-bit baselines.
  *   - b = 3: the row is cut into chunks of 32 codes (the last one padded with
  *     zero codes), 12 bytes each.  In a chunk, bytes 0-7 are a little-endian
  *     64-bit field holding bits 0-1 of code j at bits [2j, 2j+2); bytes 8-11
@@ -174,7 +176,7 @@ palq_status palq_quantize(palq_ctx *ctx, const float *x, float l, float u, const
  * optional shortcut (palq_residual), and the cyclic permutation of Eq. 8
  * applied `shuffle_steps` times as the write address: the result of source
  * group g is stored in group (g + shuffle_steps) mod G.
- *   in  : unsigned codes of 2, 3 or 4 bits, or signed 8-bit codes;
+ *   in  : unsigned codes of 2, 3, 4, 6 or 8 bits, or signed 8-bit codes;
  *         groups == w->groups, ch_per_group == w->cin_pg
  *   out : n x ho x wo, groups == w->groups, ch_per_group == w->cout_pg,
  *         bits == rq->out_bits, unsigned; ho = (h + 2 pad - kh)/stride + 1
@@ -182,7 +184,9 @@ palq_status palq_quantize(palq_ctx *ctx, const float *x, float l, float u, const
  *         products that land in each output channel (destination order:
  *         the permuted main accumulator plus any projection accumulator).
  * PALQ_ERR_OVERFLOW when K*max|code|*max|weight| (K = kh*kw*cin_pg), plus
- * the same bound of the projection product, reaches 2^26.  out must not
+ * the same bound of the projection product, reaches 2^26 for 2-bit inputs
+ * or 2^30 for wider ones; a projection input is unsigned codes.  out
+ * must not
  * overlap any input.  Every call prepacks the filter again, into context
  * memory that it grows (allocating) when a call needs more than any before;
  * it never synchronises.  A loop over one layer plans it once instead

@@ -75,7 +75,7 @@ __global__ void conv_direct_kernel(ConvArgs a, int chunks, const int32_t *only_i
   }
   uint32_t words[8];
   pack_chunk(q, nc, a.out.bits, words);
-  const int per_chunk = a.out.bits == 3 ? 3 : a.out.bits;
+  const int per_chunk = a.out.bits == 3 ? 3 : store_bits(a.out.bits);
   const int nw = chunk_words_in_row(ci, a.out.bits, a.out.row / 4);
   uint32_t *dst = (uint32_t *)(a.out.data + p * a.out.pixel + (int64_t)gd * a.out.row) +
                   (int64_t)ci * per_chunk;

@@ -125,11 +125,19 @@ template <int B> struct Blk {
 // stem layout holds eight 4-byte pixels.
 template <int B, bool STEM> struct RawT { uint32_t w[STEM ? 8 : B]; };
 
-// MFMA B operand for K-step j (0/1) from a lane's raw half block.
+// MFMA B operand for K-step j (0/1) from a lane's raw half block.  B = 8
+// (unsigned 8-bit codes, and 6-bit codes stored one per byte): the bytes
+// with their top bit flipped, x - 128 as int8; the kernel starts each
+// accumulator at 128 sum(w) of its channel (Geo::acc0), which restores
+// sum(w x) exactly, out-of-image taps included (their code 0 reads as -128
+// as well).
 template <int B>
 __device__ inline v4i act_operand(const RawT<B, false> &r, int j) {
   if constexpr (B == 2) return act_unpack2(r.w[j]);
   else if constexpr (B == 4) return unpack4_nibbles(r.w[2 * j], r.w[2 * j + 1]);
+  else if constexpr (B == 8)
+    return v4i{(int)(r.w[4 * j] ^ 0x80808080u), (int)(r.w[4 * j + 1] ^ 0x80808080u),
+               (int)(r.w[4 * j + 2] ^ 0x80808080u), (int)(r.w[4 * j + 3] ^ 0x80808080u)};
   else return unpack3(r.w[j], r.w[2], j);
 }
 
@@ -139,6 +147,7 @@ __device__ inline v4i load_weight_unit(const uint8_t *p, int u) {
   const uint32_t *q = (const uint32_t *)p;
   if constexpr (B == 2) return wt_unpack2(q[u]);
   else if constexpr (B == 4) return wt_unpack4(q[2 * u], q[2 * u + 1]);
+  else if constexpr (B == 8) return v4i{(int)q[4 * u], (int)q[4 * u + 1], (int)q[4 * u + 2], (int)q[4 * u + 3]};
   else return wt_unpack3(q[3 * (u >> 1) + (u & 1)], q[3 * (u >> 1) + 2], u & 1);
 }
 
@@ -157,7 +166,7 @@ __device__ inline int chunk_code(const uint32_t *cw, int j, int bits) {
     const uint32_t v = (cw[j >> 4] >> (2 * (j & 15))) & 3u;
     return (int)(v | (((cw[2] >> b3_hi_pos(j)) & 1u) << 2));
   }
-  const int bit = j * bits;
+  const int bit = j * store_bits(bits);
   return (int)((cw[bit >> 5] >> (bit & 31)) & ((1u << bits) - 1u));
 }
 
@@ -174,11 +183,12 @@ __device__ inline void row_quad(const uint8_t *row, int c0, int bits, int out[4]
       out[e] = (int)(((lo >> (2 * e)) & 3u) | (((hi >> b3_hi_pos(j0 + e)) & 1u) << 2));
     return;
   }
-  const int bit = c0 * bits;
+  const int sb = store_bits(bits);
+  const int bit = c0 * sb;
   const uint32_t v = w[bit >> 5] >> (bit & 31);
   const uint32_t mask = (1u << bits) - 1u;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) out[e] = (int)((v >> (bits * e)) & mask);
+  for (int e = 0; e < 4; ++e) out[e] = (int)((v >> (sb * e)) & mask);
 }
 
 // Per-channel requant constants in fp64.  With v = 2^lscale (acc + residual)
@@ -235,6 +245,7 @@ struct Geo {
   int32_t scale;      // operand scale of the accumulator (16 for 2-bit codes)
   const uint8_t *wp;  // weights in MFMA operand order (see prepack_kernel)
   const RqConst *rq;  // per-channel requant constants, then the int64-path flag
+  const int32_t *acc0;  // B = 8: per-channel accumulator start 128 sum(w) (act_operand)
 };
 
 // A (kb, 32-channel block) slab of prepacked weights: [j][half][ch][16 B].
@@ -268,6 +279,11 @@ __device__ inline v4i weight_unit(const ConvArgs &a, const Geo &geo, int g, int 
                              : a.proj_w + ((int64_t)gd * a.cout + k) * geo.pw_ch +
                                    (int64_t)(kb - geo.kb_main) * BLK;
       v = load_weight_unit<B>(p, u);
+      if constexpr (B == 8) {
+        if (a.w_bits == 6)  // 6-bit codes stored one per byte: sign-extend from bit 5
+#pragma unroll
+          for (int d = 0; d < 4; ++d) v[d] = (int)sext_bytes<6>((uint32_t)v[d]);
+      }
     }
   }
   return v;
@@ -291,6 +307,25 @@ __global__ void prepack_kernel(ConvArgs a, Geo geo, uint8_t *wp) {
   const int j = within >> 6, half = (within >> 5) & 1, ch = within & 31;
   const int gd = (g + a.shuffle) % a.in.groups;
   *(v4i *)(wp + t * 16) = weight_unit<B, STEM>(a, geo, g, gd, cblk * 32 + ch, kb, 2 * half + j);
+}
+
+// Geo::acc0 of an unsigned 6/8-bit layer: 128 times the sum of each output
+// channel's weights (sign-extended from w_bits), one thread per channel.
+__global__ void wsum_kernel(ConvArgs a, Geo geo, int32_t *acc0) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= (int64_t)a.in.groups * a.cout) return;
+  const int sh = 8 - a.w_bits;
+  auto wsum = [&](const int8_t *w, int K) {
+    int32_t sum = 0;
+    for (int k = 0; k < K; ++k) sum += (int32_t)(int8_t)(w[k] << sh) >> sh;
+    return sum;
+  };
+  int32_t sum = wsum((const int8_t *)(a.w + c * geo.w_ch), a.kh * a.kw * a.in.cpg);
+  if (a.proj.data) {  // the fused projection of destination group (g + s) mod G (its inputs get the same flip)
+    const int g = (int)(c / a.cout), k = (int)(c % a.cout), gd = (g + a.shuffle) % a.in.groups;
+    sum += wsum((const int8_t *)(a.proj_w + ((int64_t)gd * a.cout + k) * geo.pw_ch), a.proj.cpg);
+  }
+  acc0[c] = 128 * sum;
 }
 
 // FP4 (E2M1) weight slabs for the 2-bit grouped tile kernel, one MFMA
@@ -418,6 +453,11 @@ __device__ inline RawT<B, false> buf_half(__amdgpu_buffer_rsrc_t r, uint32_t vof
     const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, soff, 0);
     const uint4 u = __builtin_bit_cast(uint4, v);
     x.w[0] = u.x; x.w[1] = u.y; x.w[2] = u.z; x.w[3] = u.w;
+  } else if constexpr (B == 8) {
+    const uint4 u0 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, soff, 0));
+    const uint4 u1 = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, soff + 16, 0));
+    x.w[0] = u0.x; x.w[1] = u0.y; x.w[2] = u0.z; x.w[3] = u0.w;
+    x.w[4] = u1.x; x.w[5] = u1.y; x.w[6] = u1.z; x.w[7] = u1.w;
   } else {
     const auto v = __builtin_amdgcn_raw_buffer_load_b96(r, (int)voff, soff, 0);
     x.w[0] = v[0]; x.w[1] = v[1]; x.w[2] = v[2];
@@ -463,8 +503,8 @@ __device__ inline void stage_block(const ConvArgs &a, const Geo &geo, int g, uin
 template <int CB, int PB, int RB>
 __device__ __forceinline__ void epilogue(const ConvArgs &a, const Geo &geo, v16i (&acc)[CB][PB], const uint32_t (&rw)[CB][PB][2],
                                 int64_t mbase, int g, int gd, int ch0, int l32, int half, const RqConst *rq) {
-  const int bo = a.out.bits;
-  const int qmax = (1 << bo) - 1;
+  const int bo = store_bits(a.out.bits);  // 6-bit codes are stored as bytes
+  const int qmax = (1 << a.out.bits) - 1;
   const int64_t outC = (int64_t)a.in.groups * a.cout;
   const int lsc = geo.scale == 16 ? 4 : 0;
   const bool exact64 = ((const int32_t *)(geo.rq + (int64_t)a.in.groups * a.cout))[0] != 0;
@@ -587,7 +627,8 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
                                         uint32_t rwl = 0, uint32_t rws = 0) {
   static_assert(!LAZY || PB == 2 || PB == 4, "lazy shortcut reads are written for two or four pixel blocks");
   constexpr int bo = BO;
-  constexpr uint32_t qmax = (1u << BO) - 1u;
+  // BO = 8 also stores 6-bit codes (one per byte), clamped at 63
+  const uint32_t qmax = BO == 8 ? (1u << a.out.bits) - 1u : (1u << BO) - 1u;
   const int lsc = geo.scale == 16 ? 4 : 0;
   // requant constants (and shortcut multipliers) of quad j = 4 cb + qi,
   // read one quad ahead of their use so that their LDS latency overlaps
@@ -732,7 +773,7 @@ __device__ __forceinline__ void epilogue_fast(const ConvArgs &a, const Geo &geo,
     epilogue_fast_bo<2, CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rm);
   else if (a.out.bits == 4)
     epilogue_fast_bo<4, CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rm);
-  else
+  else  // 6 or 8
     epilogue_fast_bo<8, CB, PB, RB>(a, geo, acc, rw, mbase, g, gd, ch0, l32, half, rq, rm);
 }
 
@@ -945,7 +986,13 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0;
+        for (int r = 0; r < 16; ++r) {
+          // row r of the 32 x 32 block is channel 8 (r / 4) + 4 half + r % 4
+          if constexpr (B == 8)
+            acc[cb][pb][r] = geo.acc0[(int64_t)g * a.cout + ch0 + cb * 32 + 8 * (r >> 2) + 4 * half + (r & 3)];
+          else
+            acc[cb][pb][r] = 0;
+        }
     if (phase == 0) PALQ_KLOOP(xs0, xs1, xs2)
     else if (phase == 1) PALQ_KLOOP(xs1, xs2, xs0)
     else PALQ_KLOOP(xs2, xs0, xs1)
@@ -2360,6 +2407,9 @@ hipError_t launch_stem(const ConvArgs &a, const Geo &geo, int epi, hipStream_t s
 template <int B>
 hipError_t dispatch_bits(const ConvArgs &a, const Geo &geo, int cb, int pb, int epi, hipStream_t s) {
   (void)pb;  // one 32-pixel block per wave
+  // 8-bit codes with a shortcut: the 64-channel general build would spill
+  if constexpr (B == 8)
+    if (a.res.data) return launch_grouped<B, 1, 1>(a, geo, epi, s);
   return cb == 2 ? launch_grouped<B, 2, 1>(a, geo, epi, s) : launch_grouped<B, 1, 1>(a, geo, epi, s);
 }
 
@@ -2395,7 +2445,7 @@ bool conv_mfma_supported(const ConvArgs &a) {
   if ((int64_t)a.out.n * a.ho * a.wo >= (1 << 24)) return false;
   if (!is_stem(a)) {
     const int b = a.in.bits;
-    if (a.in.is_signed || (b != 2 && b != 3 && b != 4) || a.w_bits != b) return false;
+    if (a.in.is_signed || (b != 2 && b != 3 && b != 4 && b != 6 && b != 8) || a.w_bits != b) return false;
     if (a.in.cpg % 64 != 0 || a.kh * a.kw > 32) return false;
     if (a.proj.data && (a.proj.bits != b || a.proj.cpg % 64 != 0 || a.proj.is_signed)) return false;
   }
@@ -2408,6 +2458,7 @@ ConvPlan conv_mfma_plan(const ConvArgs &a) {
   ConvPlan p{};
   const Geo geo = make_geo(a);
   p.w_bytes = (size_t)a.in.groups * a.cout * geo.kb_total * 64;
+  if (!is_stem(a) && a.in.bits >= 6) p.w_bytes += (size_t)a.in.groups * a.cout * 4;  // Geo::acc0
   p.thr_bytes = (size_t)a.in.groups * a.cout * sizeof(RqConst) + 16;  // + int64-path flag
   if (stem_rows(a)) p.w_bytes += (size_t)a.cout * sp::KH * 32;  // the filter-row copy
   if (fp6_applies(a)) {  // FP6 slabs and constants after the int8 ones
@@ -2437,6 +2488,11 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
       case 2: hipLaunchKernelGGL((prepack_kernel<2, false>), dim3(grid), dim3(256), 0, s, a, geo, wp); break;
       case 3: hipLaunchKernelGGL((prepack_kernel<3, false>), dim3(grid), dim3(256), 0, s, a, geo, wp); break;
       case 4: hipLaunchKernelGGL((prepack_kernel<4, false>), dim3(grid), dim3(256), 0, s, a, geo, wp); break;
+      case 6: case 8:
+        hipLaunchKernelGGL((prepack_kernel<8, false>), dim3(grid), dim3(256), 0, s, a, geo, wp);
+        hipLaunchKernelGGL(wsum_kernel, dim3((unsigned)((a.in.groups * a.cout + 255) / 256)), dim3(256), 0, s, a,
+                           geo, (int32_t *)(wp + (size_t)a.in.groups * a.cout * geo.kb_total * 64));
+        break;
       default: return hipErrorNotSupported;
     }
   }
@@ -2774,6 +2830,9 @@ hipError_t launch_conv_mfma(const ConvArgs &a_in, const uint8_t *wp, const int32
     case 2: return dispatch_bits<2>(a, geo, cb, pb, epi, s);
     case 3: return dispatch_bits<3>(a, geo, cb, pb, epi, s);
     case 4: return dispatch_bits<4>(a, geo, cb, pb, epi, s);
+    case 6: case 8:
+      geo.acc0 = (const int32_t *)(wp + (size_t)nch * geo.kb_total * 64);
+      return dispatch_bits<8>(a, geo, cb, pb, epi, s);
   }
   return hipErrorNotSupported;
 }

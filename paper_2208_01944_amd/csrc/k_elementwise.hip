@@ -37,7 +37,7 @@ __global__ void pack_kernel(const uint8_t *codes, ActView out, int64_t rows, int
   for (int j = 0; j < 32; ++j) c[j] = j < nc ? (int)src[j] : 0;
   uint32_t words[8];
   pack_chunk(c, nc, out.bits, words);
-  const int per_chunk = out.bits == 3 ? 3 : out.bits;
+  const int per_chunk = out.bits == 3 ? 3 : store_bits(out.bits);
   const int nw = chunk_words_in_row(ci, out.bits, out.row / 4);
   uint32_t *dst = (uint32_t *)(out.data + r * out.row) + (int64_t)ci * per_chunk;
   for (int k = 0; k < nw; ++k) dst[k] = words[k];
@@ -238,14 +238,14 @@ __global__ void quantize_kernel(const float *x, float l, float u, const uint32_t
     dst[3 * wi + 2] = words[2];
     return;
   }
-  const int per = 32 / out.bits;
+  const int per = 32 / store_bits(out.bits);
   const int j0 = wi * per;
   const int nc = min(per, out.cpg - j0);
   const uint32_t mask = (1u << out.bits) - 1u;
   uint32_t w = 0;
   for (int k = 0; k < nc; ++k) {
     const int q = (degenerate ? 0 : quant_one(src[j0 + k], l, rng, qmax)) - off;
-    w |= ((uint32_t)q & mask) << (k * out.bits);
+    w |= ((uint32_t)q & mask) << (k * store_bits(out.bits));
   }
   dst[wi] = w;
 }
@@ -291,7 +291,7 @@ __global__ void channel_shuffle_kernel(ActView in, ActView out, int64_t pixels, 
   }
   uint32_t words[8];
   pack_chunk(c, n, out.bits, words);
-  uint32_t *dst = (uint32_t *)(out.data + p * out.pixel + (int64_t)gq * out.row) + (int64_t)ci * (out.bits == 3 ? 3 : out.bits);
+  uint32_t *dst = (uint32_t *)(out.data + p * out.pixel + (int64_t)gq * out.row) + (int64_t)ci * (out.bits == 3 ? 3 : store_bits(out.bits));
   const int nw = chunk_words_in_row(ci, out.bits, out.row / 4);
   for (int wi = 0; wi < nw; ++wi) dst[wi] = words[wi];
 }
@@ -336,7 +336,7 @@ __global__ void maxpool_kernel(ActView in, int k, int stride, int pad, ActView o
     dst[wi] = used >= 32 ? m : (m & ((1u << used) - 1u));
     return;
   }
-  const int per = in.bits == 3 ? 32 : 32 / in.bits;
+  const int per = in.bits == 3 ? 32 : 32 / store_bits(in.bits);
   const int j0 = wi * per;
   const int nc = min(per, out.cpg - j0);
   int c[32];
@@ -359,7 +359,7 @@ __global__ void maxpool_kernel(ActView in, int k, int stride, int pad, ActView o
     dst[3 * wi + 2] = words[2];
   } else {
     uint32_t w = 0;
-    for (int j = 0; j < nc; ++j) w |= (uint32_t)c[j] << (j * in.bits);
+    for (int j = 0; j < nc; ++j) w |= (uint32_t)c[j] << (j * store_bits(in.bits));
     dst[wi] = w;
   }
 }

@@ -25,7 +25,7 @@ palq_status device_fail(palq_ctx *ctx, hipError_t e, const char *what) {
   return fail(ctx, PALQ_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-bool valid_bits(int b) { return b == 2 || b == 3 || b == 4 || b == 8; }
+bool valid_bits(int b) { return b == 2 || b == 3 || b == 4 || b == 6 || b == 8; }
 
 int64_t act_elems(const palq_act *a) {
   return (int64_t)a->n * a->h * a->w * a->groups * a->ch_per_group;
@@ -36,7 +36,7 @@ palq_status check_act(palq_ctx *ctx, const palq_act *a, const char *what) {
   if (!a) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": null descriptor");
   if (a->n < 0 || a->h < 1 || a->w < 1 || a->groups < 1 || a->ch_per_group < 1)
     return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": non-positive size");
-  if (!valid_bits(a->bits)) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": bits not in {2,3,4,8}");
+  if (!valid_bits(a->bits)) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": bits not in {2,3,4,6,8}");
   if (a->is_signed != 0 && a->is_signed != 1)
     return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": is_signed must be 0 or 1");
   const int64_t row = row_bytes(a->ch_per_group, a->bits);
@@ -52,7 +52,7 @@ palq_status check_filter(palq_ctx *ctx, const palq_filter *f, const char *what) 
   if (!f) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": null filter");
   if (f->groups < 1 || f->cout_pg < 1 || f->cin_pg < 1 || f->kh < 1 || f->kw < 1)
     return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": non-positive size");
-  if (!valid_bits(f->bits)) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": bits not in {2,3,4,8}");
+  if (!valid_bits(f->bits)) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": bits not in {2,3,4,6,8}");
   if (!f->data) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": null data");
   if (((uintptr_t)f->data & 15u) != 0)
     return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": data not 16-byte aligned");
@@ -314,13 +314,12 @@ palq_status group_conv_impl(palq_ctx *ctx, const palq_act *in, const palq_filter
     return fail(ctx, PALQ_ERR_ARG, "res_mult must be 16-byte aligned");
   if (w->groups * (int64_t)w->cout_pg > (1 << 24))
     return fail(ctx, PALQ_ERR_UNSUPPORTED, "more than 2^24 output channels");
-  if (!valid_bits(rq->out_bits)) return fail(ctx, PALQ_ERR_ARG, "requant: out_bits not in {2,3,4,8}");
+  if (!valid_bits(rq->out_bits)) return fail(ctx, PALQ_ERR_ARG, "requant: out_bits not in {2,3,4,6,8}");
   if (stride < 1 || pad < 0) return fail(ctx, PALQ_ERR_ARG, "stride must be >= 1 and pad >= 0");
   if (in->groups != w->groups || in->ch_per_group != w->cin_pg)
     return fail(ctx, PALQ_ERR_ARG, "input groups/channels do not match the filter");
-  if (in->is_signed ? in->bits != 8 : in->bits == 8)
-    return fail(ctx, PALQ_ERR_UNSUPPORTED,
-                "input codes must be unsigned 2/3/4-bit or signed 8-bit");
+  if (in->is_signed && in->bits != 8)
+    return fail(ctx, PALQ_ERR_UNSUPPORTED, "signed input codes must be 8-bit");
   const int64_t ho = ((int64_t)in->h + 2 * pad - w->kh) / stride + 1;
   const int64_t wo = ((int64_t)in->w + 2 * pad - w->kw) / stride + 1;
   if ((int64_t)in->h + 2 * pad < w->kh || (int64_t)in->w + 2 * pad < w->kw || ho < 1 || wo < 1)
@@ -331,9 +330,11 @@ palq_status group_conv_impl(palq_ctx *ctx, const palq_act *in, const palq_filter
   if (out->bits != rq->out_bits || out->is_signed)
     return fail(ctx, PALQ_ERR_ARG, "output must be unsigned codes of requant.out_bits bits");
   const int64_t K = (int64_t)w->kh * w->kw * w->cin_pg;
-  const int64_t lim = (int64_t)1 << 26;
+  // 2-bit inputs: the int8 path carries a factor 16 in its accumulator
+  const int64_t lim = (int64_t)1 << (in->bits == 2 ? 26 : 30);
   if (K * max_code(in->bits, in->is_signed) * max_code(w->bits, 1) >= lim)
-    return fail(ctx, PALQ_ERR_OVERFLOW, "accumulator bound K*max|a|*max|w| >= 2^26");
+    return fail(ctx, PALQ_ERR_OVERFLOW, in->bits == 2 ? "accumulator bound K*max|a|*max|w| >= 2^26"
+                                                      : "accumulator bound K*max|a|*max|w| >= 2^30");
 
   const palq_act *rid = res ? res->identity : nullptr;
   const palq_act *pin = res ? res->proj_in : nullptr;
@@ -352,15 +353,14 @@ palq_status group_conv_impl(palq_ctx *ctx, const palq_act *in, const palq_filter
     if (pw->kh != 1 || pw->kw != 1 || pw->groups != w->groups || pw->cout_pg != w->cout_pg ||
         pin->groups != pw->groups || pin->ch_per_group != pw->cin_pg)
       return fail(ctx, PALQ_ERR_ARG, "projection filter/input do not match");
-    if (pin->is_signed || pin->bits == 8)
-      return fail(ctx, PALQ_ERR_UNSUPPORTED, "projection input must be unsigned 2/3/4-bit codes");
+    if (pin->is_signed) return fail(ctx, PALQ_ERR_UNSUPPORTED, "projection input must be unsigned codes");
     if (res->proj_stride < 1) return fail(ctx, PALQ_ERR_ARG, "proj_stride must be >= 1");
     if (pin->n != in->n || ((int64_t)pin->h - 1) / res->proj_stride + 1 != ho ||
         ((int64_t)pin->w - 1) / res->proj_stride + 1 != wo)
       return fail(ctx, PALQ_ERR_ARG, "projection output size differs from the convolution's");
     if (K * max_code(in->bits, in->is_signed) * max_code(w->bits, 1) +
             (int64_t)pw->cin_pg * max_code(pin->bits, 0) * max_code(pw->bits, 1) >= lim)
-      return fail(ctx, PALQ_ERR_OVERFLOW, "projection accumulator bound >= 2^26");
+      return fail(ctx, PALQ_ERR_OVERFLOW, "projection accumulator bound over the limit");
   }
   const int64_t ob = palq_act_bytes(out);
   if (overlaps(out->data, ob, in->data, palq_act_bytes(in)) ||

@@ -12,12 +12,13 @@ namespace palq {
 
 // ----------------------------------------------------------------- layout
 // Bytes of a packed row of `codes` codes at `bits` bits (the layout of
-// include/palq.h): 4-byte words for b in {2,4,8}, 12-byte chunks of 32
-// codes for b = 3.
+// include/palq.h): 4-byte words for b in {2,4,8} (and 6, stored as 8),
+// 12-byte chunks of 32 codes for b = 3.
 __host__ __device__ inline int64_t row_bytes(int64_t codes, int bits) {
   if (codes <= 0) return -1;
   switch (bits) {
     case 2: case 4: case 8: return 4 * ((codes * bits + 31) / 32);
+    case 6: return 4 * ((codes * 8 + 31) / 32);
     case 3: return 12 * ((codes + 31) / 32);
     default: return -1;
   }
@@ -27,7 +28,7 @@ __host__ __device__ inline int64_t row_bytes(int64_t codes, int bits) {
 // rows can be re-grouped without moving data.
 __host__ __device__ inline bool row_exact(int64_t codes, int bits) {
   if (bits == 3) return codes % 32 == 0;
-  return (codes * bits) % 32 == 0;
+  return (codes * (bits == 6 ? 8 : bits)) % 32 == 0;
 }
 
 // Device view of an activation tensor.

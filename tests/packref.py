@@ -6,10 +6,15 @@ the bytes the device pack produces and to read device-packed buffers.
 import numpy as np
 
 
+def store_bits(bits: int) -> int:
+    """Bits a code takes in a row: 6-bit codes are stored one per byte."""
+    return 8 if bits == 6 else bits
+
+
 def row_bytes(codes: int, bits: int) -> int:
     if bits == 3:
         return 12 * ((codes + 31) // 32)
-    return 4 * ((codes * bits + 31) // 32)
+    return 4 * ((codes * store_bits(bits) + 31) // 32)
 
 
 def b3_hi_pos(j: int) -> int:
@@ -34,7 +39,7 @@ def pack_row(codes, bits: int) -> bytes:
         return bytes(out)
     v = 0
     for j, c in enumerate(codes):
-        v |= c << (bits * j)
+        v |= c << (store_bits(bits) * j)
     return v.to_bytes(nb, "little")
 
 
@@ -49,7 +54,7 @@ def unpack_row(buf: bytes, n: int, bits: int, signed: bool):
             out.append(((lo >> (2 * jj)) & 3) | (((hi >> b3_hi_pos(jj)) & 1) << 2))
     else:
         v = int.from_bytes(buf[:row_bytes(n, bits)], "little")
-        out = [(v >> (bits * j)) & ((1 << bits) - 1) for j in range(n)]
+        out = [(v >> (store_bits(bits) * j)) & ((1 << bits) - 1) for j in range(n)]
     if signed:
         out = [c - (1 << bits) if c >= (1 << (bits - 1)) else c for c in out]
     return out

@@ -97,12 +97,21 @@ def test_validate_only_group_conv_errors(P, vctx):
     assert _conv(P, vctx, rq=P.Requant(None, _fake(31), None, 2)) == P.ERR_ARG
     assert _conv(P, vctx, rq=P.Requant(_fake(30) + 4, _fake(31), None, 2)) == P.ERR_ARG  # misaligned
     assert _conv(P, vctx, stride=0) == P.ERR_ARG
-    assert _conv(P, vctx, x=_act(P, bits=8)) == P.ERR_UNSUPPORTED          # unsigned 8-bit input
+    # unsigned 6- and 8-bit inputs (the dense baselines) with weights of their width
+    for b in (6, 8):
+        assert _conv(P, vctx, x=_act(P, bits=b), f=P.Filter(2, 32, 64, 3, 3, b, _fake(10))) == P.OK
+    assert _conv(P, vctx, x=_act(P, bits=4, signed=True)) == P.ERR_UNSUPPORTED  # signed input below 8 bits
+    assert P.row_bytes(10, 6) == 12 and P.row_bytes(10, 5) == -1  # 6-bit codes one per byte
     # signed 8-bit input is the stem format
     assert _conv(P, vctx, x=_act(P, bits=8, signed=True), f=P.Filter(2, 32, 64, 3, 3, 8, _fake(10))) == P.OK
     # accumulator bound: K * 255... 8-bit weights with a huge K
     big = P.Filter(1, 32, 8192, 3, 3, 8, _fake(10))
     assert _conv(P, vctx, x=_act(P, g=1, c=8192, bits=8, signed=True), f=big,
+                 out=_act(P, g=1, c=32, slot=20)) == P.ERR_OVERFLOW
+    assert "2^30" in vctx.last_error()
+    # 2-bit inputs (the int8 path scales their accumulator by 16): 2^26
+    wide = 1 << 22
+    assert _conv(P, vctx, x=_act(P, g=1, c=wide), f=P.Filter(1, 32, wide, 3, 3, 2, _fake(10)),
                  out=_act(P, g=1, c=32, slot=20)) == P.ERR_OVERFLOW
     assert "2^26" in vctx.last_error()
 

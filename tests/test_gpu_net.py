@@ -227,6 +227,20 @@ def test_resnet50_small_all_tensors(ctx, torch):
     np.testing.assert_array_equal(logits, ref)
 
 
+@pytest.mark.parametrize("bits", [6, 8])
+def test_resnet18_dense_wide_codes(ctx, torch, bits):
+    """The dense (G = 1) M-bit network of the Table 2 baselines at M = 6 and
+    8: unsigned codes of M bits throughout (8-bit projections included),
+    every tensor and the logits equal the oracle's."""
+    say(f"resnet18 hw=32 n=2 G=1 b={bits} centred")
+    spec = I.resnet18(n=2, groups=1, bits=bits, hw=32, classes=10, seed=15 + bits)
+    spec = O.calibrate_centring(spec, spec["x"])
+    net, logits = gpu_forward(ctx, torch, spec, keep=True)
+    ref, tensors, _ = O.run_net(spec, spec["x"], keep=True)
+    compare_tensors(ctx, net, spec, tensors, slice(None))
+    np.testing.assert_array_equal(logits, ref)
+
+
 def test_resnet18_bits3_g3(ctx, torch):
     say("resnet18 hw=32 n=3 G=3 b=3 centred")
     spec = I.resnet18(n=3, groups=3, bits=3, hw=32, classes=10, seed=13)

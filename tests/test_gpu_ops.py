@@ -161,6 +161,13 @@ CONV_CASES = [
     dict(n=2, h=6, w=6, groups=2, cin=20, cout=20, k=3, stride=1, pad=0, bits=3, residual="identity"),
     dict(n=2, h=7, w=7, groups=2, cin=24, cout=32, k=3, stride=2, pad=1, bits=2, residual="projection"),
     dict(n=2, h=6, w=6, groups=2, cin=64, cout=64, k=3, stride=1, pad=1, bits=2, w_bits=4),
+    # unsigned 8- and 6-bit codes (the dense baselines): int8 matrix cores with the flipped-byte operand
+    dict(n=2, h=10, w=10, groups=2, cin=64, cout=64, k=3, stride=1, pad=1, bits=8),
+    dict(n=2, h=9, w=9, groups=1, cin=64, cout=128, k=3, stride=2, pad=1, bits=6),
+    dict(n=2, h=8, w=8, groups=2, cin=64, cout=64, k=3, stride=1, pad=1, bits=8, residual="identity"),
+    dict(n=2, h=9, w=9, groups=1, cin=64, cout=64, k=3, stride=2, pad=1, bits=8, residual="projection"),
+    dict(n=2, h=7, w=6, groups=2, cin=20, cout=24, k=3, stride=1, pad=1, bits=8),  # direct path
+    dict(n=2, h=7, w=7, groups=2, cin=64, cout=64, k=3, stride=1, pad=1, bits=6, residual="identity"),
 ]
 
 
