@@ -136,6 +136,18 @@ palq_status palq_set_stream(palq_ctx *ctx, void *hip_stream);
  * palq_group_conv calls and networks created after the call.
  * PALQ_ERR_ARG: enable not 0 or 1. */
 palq_status palq_set_conv_fp4(palq_ctx *ctx, int32_t enable);
+/* Execution of wide grouped convolutions as the bit-level decomposition of
+ * Section 3.2 (Eq. 4), the baseline PalQuant is set against (Section 5.2,
+ * Table 2): with enable = 1 a layer with unsigned M-bit inputs, M-bit
+ * weights and M-bit outputs, M in {4, 6, 8}, 64-channel blocks and an
+ * optional M-bit identity or projection shortcut splits every code into
+ * M / 2 2-bit chunks and runs the (M / 2)^2 chunk products of each MAC on
+ * the FP4 matrix cores, shifted by 4^(i+j) and summed exactly
+ * ("conv_bitdecomp_kernel"), where the accumulator bounds allow it; with 0
+ * (the default) such layers run directly on int8.  Results are identical
+ * either way.  Applies to palq_group_conv calls and networks created after
+ * the call.  PALQ_ERR_ARG: enable not 0 or 1. */
+palq_status palq_set_conv_bitdecomp(palq_ctx *ctx, int32_t enable);
 /* Waits for all work on the context's stream; reports deferred device errors. */
 palq_status palq_sync(palq_ctx *ctx);
 /* Reason for the last failed call on ctx; owned by ctx, valid until its next call. */

@@ -2325,6 +2325,363 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp6_kernel(ConvArgs a, G
   conv_fpx_tile<CB, PB, WN, WM, 0, DUMP, S, 3>(a, geo, npt, ncb, nch);
 }
 
+// ---------------------------------------------------------------- Eq. 4 bit decomposition
+// The M-bit baseline of Section 3.2 run on the 2-bit (FP4) matrix cores:
+// every unsigned M-bit activation code x and signed M-bit weight w (M = 4,
+// 6, 8) is split into G = M / 2 2-bit chunks, x = sum_i 4^i x_i and
+// w = sum_j 4^j w_j (w_j unsigned for j < G - 1, the top chunk signed), and
+// each MAC becomes the G^2 chunk products of Eq. 4, 4^(i+j) x_i w_j, summed
+// exactly.  A K-block (tap, 64 input channels) stages the pixels' M-bit
+// codes (32 or 64 bytes a pixel) and the G chunk slabs of the weights
+// (prepack_bd_kernel); a lane then builds its G activation chunk operands in
+// registers and runs G^2 FP4 MFMAs per 32 x 32 block, the factor 4^(i+j)
+// given as the E8M0 scale of the activation operand.  Operands are E2M1 of
+// c / 2 (chunks 0..3 and the top chunk -2..1), so the fp32 accumulator
+// holds T / 4 with T the integer sum; M = 8 keeps the pairs with i + j >= 3
+// in a second accumulator scaled by 4^-3, so that each stays below 2^24 in T
+// (bd_applies checks the bounds).  Tiles as conv_fpx_tile (128 x 128,
+// XCD-contiguous runs in the chunked order).  Epilogue in fp64: lo + 64 hi,
+// plus the identity shortcut rm c / 4 (M-bit codes), then the FP4-scaled
+// requant constants.  A fused projection adds its own decomposed K-blocks.
+namespace bd {
+template <int M, int WN>
+struct Cfg {
+  static constexpr int GC = M / 2;  // chunks of a code
+  static constexpr int CB = 2, PB = 2, WM = 2;  // WN = 1: 64-channel tiles, 2: 128
+  static constexpr int NT = WN * WM * 64;
+  static constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
+  static constexpr int XB = M == 4 ? 32 : 64;  // bytes of a pixel's 64-code K-block
+  static constexpr int Q = XB / 32;            // 16-byte pieces of a lane half
+  static constexpr int WST = TN / 32 * GC * kSlab4;
+  static constexpr int XST = TM * XB;
+  static constexpr int SST = WST + XST;
+  static constexpr int WP = WST / 16, XP = XST / 16;
+  static_assert(WP % NT == 0 && XP % NT == 0, "every thread loads whole pieces");
+  static constexpr int WL = WP / NT, XL = XP / NT;
+  static constexpr int LPK = WL + XL;  // loads per K-block, the same for every wave
+  static constexpr bool SPLIT = M == 8;
+  static constexpr int S = 3;  // ring stages
+};
+// Code index (within a lane's 32) of operand nibble n: M = 4 codes are
+// nibbles already; byte codes pair dwords 2r and 2r + 1 into one nibble word.
+__host__ __device__ inline int bd_code(int M, int n) {
+  return M == 4 ? n : 8 * (n >> 3) + 4 * (n & 1) + ((n >> 1) & 3);
+}
+}  // namespace bd
+
+// Weights -> [G][cout/32][kb_total][GC chunk slabs of 1 KB][half][ch][16 B]:
+// nibble n of lane (ch, half) of slab j holds E2M1 of w_j / 2 for the
+// K-block code 32 half + bd_code(M, n).  One thread per 16-byte lane operand.
+__global__ void prepack_bd_kernel(ConvArgs a, Geo geo, uint8_t *wp) {
+  const int M = a.w_bits, GC = M / 2, sb = M == 4 ? 4 : 8;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int nc32 = a.cout / 32;
+  const int64_t total = (int64_t)a.in.groups * nc32 * geo.kb_total * GC * 64;
+  if (t >= total) return;
+  const int lane = (int)(t & 63), j = (int)((t >> 6) % GC);
+  const int64_t rest = (t >> 6) / GC;
+  const int kb = (int)(rest % geo.kb_total);
+  const int64_t r2 = rest / geo.kb_total;
+  const int cblk = (int)(r2 % nc32), g = (int)(r2 / nc32);
+  const int half = lane >> 5, k = cblk * 32 + (lane & 31);
+  const int gd = (g + a.shuffle) % a.in.groups;
+  const int kbytes = 64 * sb / 8;  // bytes of a K-block of one channel
+  const uint8_t *p = kb < geo.kb_main ? a.w + ((int64_t)g * a.cout + k) * geo.w_ch + (int64_t)kb * kbytes
+                                      : a.proj_w + ((int64_t)gd * a.cout + k) * geo.pw_ch +
+                                            (int64_t)(kb - geo.kb_main) * kbytes;
+  uint32_t o[4] = {0, 0, 0, 0};
+  for (int n = 0; n < 32; ++n) {
+    const int m = 32 * half + bd::bd_code(M, n);
+    const int raw = sb == 4 ? (p[m >> 1] >> (4 * (m & 1))) & 15 : p[m];
+    const int w = (raw << (32 - M)) >> (32 - M);  // sign-extend the M-bit code
+    int c = w >> (2 * j);                          // chunk j: top chunk signed, others 0..3
+    if (j < GC - 1) c &= 3;
+    const uint32_t e = j < GC - 1 ? (uint32_t)c                        // E2M1 of c / 2 for c = 0..3
+                                  : (0x9A10u >> (4 * (c & 3))) & 15u;  // -2, -1, 0, 1 -> -1, -0.5, 0, 0.5
+    o[n >> 3] |= e << (4 * (n & 7));
+  }
+  *(uint4 *)(wp + t * 16) = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+// Chunk i of a lane's 32 M-bit codes (raw: 4 words of nibbles, or 8 words of
+// bytes) as an E2M1 operand of c_i / 2 in bd_code order.
+template <int M>
+__device__ inline v8i bd_operand(const uint32_t (&raw)[M == 4 ? 4 : 8], int i) {
+  v8i d;
+  if constexpr (M == 4) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) d[q] = (int)((raw[q] >> (2 * i)) & 0x33333333u);
+  } else {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint32_t e = (raw[2 * r] >> (2 * i)) & 0x03030303u, o = (raw[2 * r + 1] >> (2 * i)) & 0x03030303u;
+      d[r] = (int)(e | (o << 4));
+    }
+  }
+  d[4] = d[5] = d[6] = d[7] = 0;
+  return d;
+}
+
+template <int M, int WN, int RB, bool DUMP>
+__global__ __launch_bounds__(WN * 128, 2) void conv_bitdecomp_kernel(ConvArgs a, Geo geo, int npt, int ncb, int nch) {
+  using C = bd::Cfg<M, WN>;
+  constexpr int NT = C::NT, TN = C::TN, TM = C::TM, WST = C::WST, SST = C::SST, S = C::S, GC = C::GC;
+  // (local copies: a member of the dependent C inside a builtin's argument
+  // costs the host pass this kernel's launch stub)
+  constexpr int CB = C::CB, PB = C::PB, Q = C::Q, XB = C::XB;
+  constexpr int BO = M == 4 ? 4 : 8;  // output storage bits (6-bit codes as bytes)
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
+  RqConst *rq_area = (RqConst *)(lds + S * SST);
+  int32_t *rm_area = (int32_t *)(rq_area + TN);
+
+  if (int64_flag(a, geo)) return;  // the general partner takes the layer
+  const int G = a.in.groups;
+  const int T = npt * ncb * G;
+  const int x8 = (int)(blockIdx.x & 7), jx = (int)(blockIdx.x >> 3);
+  const int Tq = T >> 3, Tr = T & 7;
+  if (jx >= Tq + (x8 < Tr ? 1 : 0)) return;  // no barrier yet
+  const int t = x8 * Tq + min(x8, Tr) + jx;
+  const TileIt it = tile_at(t, npt, ncb * G, nch);
+  const int pt = it.pt, cbk = it.combo % ncb, g = it.combo / ncb;
+  const int gd = (g + a.shuffle) % G;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = uniform_int(tid >> 6);
+  const int l32 = lane & 31, half = lane >> 5;
+  const int wn = wave / C::WM, wm = wave % C::WM;
+  const int KB = geo.kb_total, KM = geo.kb_main;
+
+  const int64_t ch0 = (int64_t)g * a.cout + cbk * TN;
+  for (int c = tid; c < TN; c += NT) {
+    rq_area[c] = geo.rq[ch0 + c];
+    rm_area[c] = RB != 0 ? a.res_mult[ch0 + c] : 0;
+  }
+  typedef __attribute__((address_space(3))) void *lds_ptr;
+  const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
+  const auto rw_src = make_rsrc(geo.wp, (int64_t)G * a.cout * KB * GC * (kSlab4 / 32));
+  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
+  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, (int64_t)a.proj.n * a.proj.h * a.proj.w * a.proj.pixel)
+                               : make_rsrc(a.in.data, 0);
+  const int pixb = (int)a.in.pixel, rowb = a.in.w * pixb;
+
+  // ---- fetch pieces.  Weights: piece c = tid + i NT of the tile's K-block:
+  // 32-channel block c / (64 GC), chunk slab (c / 64) % GC, lane c % 64.
+  // Activations: piece q = tid + i NT: 32-pixel block (q / 64) / Q, part
+  // (q / 64) % Q (16 bytes) of lane half (q / 32) & 1, pixel q % 32.
+  uint32_t woff[C::WL];
+#pragma unroll
+  for (int i = 0; i < C::WL; ++i) {
+    const int c = tid + i * NT;
+    woff[i] = (uint32_t)((((int64_t)g * (a.cout / 32) + cbk * (TN / 32) + c / (64 * GC)) * KB) * GC * kSlab4 +
+                         (c % (64 * GC)) * 16);
+  }
+  const int HW = a.ho * a.wo;
+  const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
+  int off0[C::XL], poff[C::XL];
+  uint32_t tmask[C::XL];
+#pragma unroll
+  for (int i = 0; i < C::XL; ++i) {
+    const int q = tid + i * NT, bp = q >> 6;
+    const int part = bp % Q, m = pt * TM + 32 * (bp / Q) + (q & 31);
+    const int hoff = XB / 2 * ((q >> 5) & 1) + 16 * part;  // bytes of the lane half's part
+    const bool valid = m < geo.M;
+    const int mm = valid ? m : 0;
+    const int n = fdiv(mm, HW, inv_hw);
+    const int rem = mm - n * HW;
+    const int oy = fdiv(rem, a.wo, inv_wo);
+    const int ox = rem - oy * a.wo;
+    const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
+    off0[i] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.row + hoff;
+    const int xlo = max(0, -ix0), xhi = min(a.kw, a.in.w - ix0);
+    const uint32_t below = xhi >= 32 ? 0xffffffffu : ((1u << max(xhi, 0)) - 1u);
+    const uint32_t cols = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
+    const int ylo = max(0, -iy0), yhi = min(a.kh, a.in.h - iy0);
+    uint32_t mk = 0;
+    for (int ky = ylo; ky < yhi; ++ky) mk |= cols << (ky * a.kw);
+    tmask[i] = valid ? mk : 0u;
+    poff[i] = (a.proj.data && valid)
+                  ? (((n * a.proj.h + oy * a.proj_stride) * a.proj.w + ox * a.proj_stride) * (int)a.proj.pixel +
+                     gd * (int)a.proj.row + hoff)
+                  : (int)kOob;
+  }
+  int f_kb = 0, f_c = 0, f_tap = 0, f_kx = 0, f_tapoff = 0;
+  uint32_t vo[C::XL];
+  auto tap_offsets = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < C::XL; ++i) vo[i] = ((tmask[i] >> f_tap) & 1u) ? (uint32_t)(off0[i] + f_tapoff) : kOob;
+  };
+  tap_offsets();
+  auto fetch = [&](int st) __attribute__((always_inline)) {
+    uint8_t *ws = lds + st * SST;
+#pragma unroll
+    for (int i = 0; i < C::WL; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + i * NT * 16 + wave * 1024), 16, (int)woff[i],
+                                               f_kb * GC * kSlab4, 0, 0);
+    if (f_kb < KM) {
+#pragma unroll
+      for (int i = 0; i < C::XL; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rin, (lds_ptr)(ws + WST + i * NT * 16 + wave * 1024), 16, (int)vo[i],
+                                                 f_c * XB, 0, 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < C::XL; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rpj, (lds_ptr)(ws + WST + i * NT * 16 + wave * 1024), 16,
+                                                 (int)poff[i], (f_kb - KM) * XB, 0, 0);
+    }
+    ++f_kb;
+    if (++f_c == geo.cpb) {  // next tap
+      f_c = 0;
+      ++f_tap;
+      f_tapoff += pixb;
+      if (++f_kx == a.kw) {
+        f_kx = 0;
+        f_tapoff += rowb - a.kw * pixb;
+      }
+      tap_offsets();
+    }
+  };
+
+  // ---- compute side
+  v16f acc[CB][PB], ach[C::SPLIT ? CB : 1][C::SPLIT ? PB : 1];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        acc[cb][pb][r] = 0.f;
+        if constexpr (C::SPLIT) ach[cb][pb][r] = 0.f;
+      }
+  // this lane's operands in stage 0: weight slab j of channel block cb at
+  // ((wn CB + cb) GC + j) KB; activation part p of pixel block pb at
+  // ((wm PB + pb) Q + p) KB
+  const uint32_t aaddr0 = lds_base + (uint32_t)(wn * CB * GC * kSlab4 + lane * 16);
+  const uint32_t xaddr0 = lds_base + WST + (uint32_t)(wm * PB * Q * 1024 + lane * 16);
+  auto kblock = [&](int st) __attribute__((always_inline)) {
+    const uint32_t aa = aaddr0 + st * SST, xa = xaddr0 + st * SST;
+    // operand reads as asm (the compiler would wait for every staging load
+    // before an LDS read it sees), one wait, then each value is tied to it
+    v4i A[CB][GC], X[PB][Q];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int j = 0; j < GC; ++j)
+        asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(A[cb][j]) : "v"(aa), "i"((cb * GC + j) * kSlab4));
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+      for (int p = 0; p < Q; ++p)
+        asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(X[pb][p]) : "v"(xa), "i"((pb * Q + p) * 1024));
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int j = 0; j < GC; ++j) asm volatile("" : "+v"(A[cb][j]));
+    uint32_t raw[PB][M == 4 ? 4 : 8];
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+      for (int p = 0; p < Q; ++p) {
+        asm volatile("" : "+v"(X[pb][p]));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) raw[pb][4 * p + e] = (uint32_t)X[pb][p][e];
+      }
+#pragma unroll
+    for (int i = 0; i < GC; ++i)
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        const v8i Bop = bd_operand<M>(raw[pb], i);
+#pragma unroll
+        for (int j = 0; j < GC; ++j)
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) {
+            const v8i Aop = __builtin_shufflevector(A[cb][j], A[cb][j], 0, 1, 2, 3, -1, -1, -1, -1);
+            const bool hi = C::SPLIT && i + j >= 3;
+            const int sc = 127 + 2 * (i + j) - (hi ? 6 : 0);  // E8M0 of 4^(i+j) (4^(i+j-3) for the second sum)
+            if (hi)
+              ach[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop, Bop, ach[cb][pb], 4, 4, 0, 127, 0, sc);
+            else
+              acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop, Bop, acc[cb][pb], 4, 4, 0, 127, 0, sc);
+          }
+      }
+  };
+
+  __syncthreads();  // the tile's constants are in LDS
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st)
+    if (st < KB) fetch(st);
+  int kb = 0;
+  for (; kb + S - 1 < KB; ++kb) {
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((S - 2) * C::LPK));
+    ring_barrier();
+    fetch((kb + S - 1) % S);
+    kblock(kb % S);
+  }
+#pragma unroll
+  for (int i = 0; i < S - 1; ++i) {
+    if (kb >= KB) break;  // uniform
+    if (KB - 1 - kb >= 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::LPK));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    ring_barrier();
+    kblock(kb % S);
+    ++kb;
+  }
+
+  // ---- epilogue (fp64): v = T / 4 (+ the shortcut rm c / 4), then
+  // q = min(trunc(v s + o), 2^out_bits - 1) with the FP4 requant constants
+  const int64_t mbase = (int64_t)pt * TM + wm * PB * 32;
+  const int64_t outC = (int64_t)G * a.cout;
+  const uint32_t qmax = (1u << a.out.bits) - 1u;
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int kc = cbk * TN + wn * CB * 32 + cb * 32;  // first channel of this 32-channel block
+    const int lc = wn * CB * 32 + cb * 32;             // the same within the tile
+    uint32_t qv[PB][4];
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const int64_t mp = mbase + pb * 32 + l32;
+      const bool live = mp < geo.M;
+#pragma unroll
+      for (int qi = 0; qi < 4; ++qi) {
+        const int cq = 8 * qi + 4 * half;
+        int rc[4] = {0, 0, 0, 0};
+        if constexpr (RB < 0)
+          row_quad(a.res.data + (live ? mp : 0) * a.res.pixel + (int64_t)gd * a.res.row, kc + cq, a.res.bits, rc);
+        uint32_t qword = 0;
+        v4i dv;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          double v = (double)acc[cb][pb][4 * qi + e];
+          if constexpr (C::SPLIT) v += 64.0 * (double)ach[cb][pb][4 * qi + e];
+          dv[e] = (int)(4.0 * v);  // T: exact, |T| < 2^31
+          if constexpr (RB < 0) v += 0.25 * (double)rm_area[lc + cq + e] * (double)rc[e];
+          const RqConst k = rq_area[lc + cq + e];
+          const double d = __builtin_fma(v, k.s, k.o);
+          uint32_t q;
+          asm("v_cvt_u32_f64 %0, %1" : "=v"(q) : "v"(d));
+          qword |= min(q, qmax) << (BO * e);
+        }
+        qv[pb][qi] = qword;
+        if constexpr (DUMP)
+          if (live) *(v4i *)(a.acc_dump + mp * outC + (int64_t)gd * a.cout + kc + cq) = dv;
+      }
+    }
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const int64_t mp = mbase + pb * 32 + l32;
+      // as in epilogue_fast_bo: after the swaps every lane holds its 32
+      // channels' quads in order (16 of them per lane half)
+      const auto p0 = __builtin_amdgcn_permlane32_swap(qv[pb][0], qv[pb][2], false, false);
+      const auto p1 = __builtin_amdgcn_permlane32_swap(qv[pb][1], qv[pb][3], false, false);
+      const uint32_t Qw[4] = {p0[0], p0[1], p1[0], p1[1]};
+      if (mp >= geo.M) continue;
+      uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row) + (int64_t)(kc >> 5) * BO +
+                     half * (BO / 2);
+      if constexpr (BO == 4) *(uint2 *)cw = make_uint2(Qw[0] | (Qw[1] << 16), Qw[2] | (Qw[3] << 16));
+      else *(uint4 *)cw = make_uint4(Qw[0], Qw[1], Qw[2], Qw[3]);
+    }
+  }
+}
+
 // ---------------------------------------------------------------- launch
 bool is_stem(const ConvArgs &a) {
   return a.in.bits == 8 && a.in.is_signed && a.w_bits == 8 && a.in.row == 4 && a.kw <= 8 &&
@@ -2430,6 +2787,8 @@ int64_t acc_bound_of(const ConvArgs &a) {
 
 bool fp4_applies(const ConvArgs &a);
 bool fp6_applies(const ConvArgs &a);
+bool bd_applies(const ConvArgs &a);
+size_t bd_offset(const ConvArgs &a);
 bool tile_kernel_applies(const ConvArgs &a);
 bool stem_tile_applies(const ConvArgs &a);
 bool stem_rows(const ConvArgs &a);
@@ -2463,6 +2822,10 @@ ConvPlan conv_mfma_plan(const ConvArgs &a) {
   if (stem_rows(a)) p.w_bytes += (size_t)a.cout * sp::KH * 32;  // the filter-row copy
   if (fp6_applies(a)) {  // FP6 slabs and constants after the int8 ones
     p.w_bytes += (size_t)a.in.groups * a.cout * geo.kb_total * 48;
+    p.thr_bytes *= 2;
+  }
+  if (bd_applies(a)) {  // the decomposition's chunk slabs and FP4-scaled constants
+    p.w_bytes = bd_offset(a) + (size_t)a.in.groups * a.cout * geo.kb_total * (a.in.bits / 2) * 32;
     p.thr_bytes *= 2;
   }
   if (fp4_applies(a)) {  // FP4 slabs and constants after the int8 ones (the general build keeps those)
@@ -2506,6 +2869,15 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
   hipLaunchKernelGGL(requant_prep_kernel, dim3(1), dim3(256), 0, s, a.mult, a.shift, a.bias, a.res.data ? a.res_mult : nullptr,
                      res_max, nch, lscale, acc_bound, rq, (int32_t *)(rq + nch));
   e = hipGetLastError();
+  if (e == hipSuccess && bd_applies(a)) {
+    const int64_t lanes = (int64_t)a.in.groups * (a.cout / 32) * geo.kb_total * (a.in.bits / 2) * 64;
+    hipLaunchKernelGGL(prepack_bd_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, s, a, geo,
+                       wp + bd_offset(a));
+    RqConst *rqb = rq + nch + 1;  // the decomposition's accumulator is T / 4
+    hipLaunchKernelGGL(requant_prep_kernel, dim3(1), dim3(256), 0, s, a.mult, a.shift, a.bias,
+                       a.res.data ? a.res_mult : nullptr, res_max, nch, -2, acc_bound, rqb, (int32_t *)(rqb + nch));
+    return hipGetLastError();
+  }
   if (e == hipSuccess && fp6_applies(a)) {
     const int64_t lanes = (int64_t)a.in.groups * (a.cout / 32) * geo.kb_total * 64;
     hipLaunchKernelGGL(prepack_fp6_kernel, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, s, a, geo,
@@ -2528,7 +2900,7 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
 bool conv_mfma_pads_input(const ConvArgs &a) { return is_stem(a) && a.pad > 0; }
 
 int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr) {
-  if ((a.out.bits == 3 && !fp6_applies(a)) || (a.res.data && a.res.bits != 2)) return 1;
+  if (!bd_applies(a) && ((a.out.bits == 3 && !fp6_applies(a)) || (a.res.data && a.res.bits != 2))) return 1;
   int32_t flag = 0;
   const RqConst *rq = (const RqConst *)thr;
   if (hipMemcpy(&flag, rq + (int64_t)a.in.groups * a.cout, sizeof(flag), hipMemcpyDeviceToHost) != hipSuccess)
@@ -2608,6 +2980,35 @@ bool fp6_applies(const ConvArgs &a) {
          acc_bound_of(a) < ((int64_t)1 << 23);
 }
 
+// The Eq. 4 bit decomposition (palq_set_conv_bitdecomp) for an unsigned
+// M-bit layer (M in {4, 6, 8}) with M-bit weights, outputs and shortcut
+// codes and 64-channel blocks, when each fp32 accumulator stays exact: its
+// bound K sum 4^(i+j-base) max|x_i| max|w_j| over the chunk pairs it takes
+// (x_i <= 3, w_j <= 3 or, the top chunk, 2 in magnitude) is below 2^24.
+bool bd_applies(const ConvArgs &a) {
+  const int M = a.in.bits, GC = M / 2;
+  if (!a.bitdecomp || is_stem(a) || a.in.is_signed || (M != 4 && M != 6 && M != 8) || a.w_bits != M ||
+      a.out.bits != M || a.in.cpg % 64 != 0 || a.cout % 64 != 0)
+    return false;
+  if (a.res.data && (a.res.bits != M || a.res.is_signed)) return false;
+  if (a.proj.data && (a.proj.bits != M || a.proj.cpg % 64 != 0 || a.proj.is_signed)) return false;
+  if ((int64_t)a.in.groups * a.cout * make_geo(a).kb_total * GC * 32 >= ((int64_t)1 << 30)) return false;
+  const int64_t K = (int64_t)a.kh * a.kw * a.in.cpg + (a.proj.data ? a.proj.cpg : 0);
+  int64_t lo = 0, hi = 0;
+  for (int i = 0; i < GC; ++i)
+    for (int j = 0; j < GC; ++j) {
+      const int64_t term = ((int64_t)1 << (2 * (i + j))) * 3 * (j == GC - 1 ? 2 : 3);
+      if (M == 8 && i + j >= 3) hi += term >> 6;
+      else lo += term;
+    }
+  return K * lo < ((int64_t)1 << 24) && K * hi < ((int64_t)1 << 24);
+}
+// The decomposition's weight slabs follow the int8 slabs (and Geo::acc0).
+size_t bd_offset(const ConvArgs &a) {
+  const size_t nch = (size_t)a.in.groups * a.cout;
+  return (nch * make_geo(a).kb_total * 64 + (a.in.bits >= 6 ? nch * 4 : 0) + 255) & ~(size_t)255;
+}
+
 // The stem on the tiled kernel: explicit zero border (pad 0), 128-channel
 // blocks, no shortcut, no accumulator dump.
 bool stem_tile_applies(const ConvArgs &a) {
@@ -2630,9 +3031,10 @@ size_t stem_rows_offset(const ConvArgs &a) { return (size_t)a.in.groups * a.cout
 // int8 with 64- or 128-channel blocks (256 pixels).
 // 3-bit layers on FP6 with 64-channel (1 x 4 waves, 256 pixels) or
 // 128-channel blocks (2 x 2 waves, 128 pixels).
+// Wide layers as the Eq. 4 decomposition with 64- or 128-channel tiles.
 enum TileBuild {
   kTileNone = 0, kTileStem, kTileFp4C64, kTileFp4C128, kTileFp4C128P4, kTileFp6C64, kTileFp6C128, kTileI8C64,
-  kTileI8C128
+  kTileI8C128, kTileBdC64, kTileBdC128
 };
 
 // 2 x 4 blocks per wave (256-pixel tiles) for 128-channel FP4 layers where
@@ -2657,6 +3059,10 @@ struct ConvChoice {
 ConvChoice conv_choice(const ConvArgs &a, const Geo &geo, int epi) {
   ConvChoice c{kTileNone, pick_cb(a, geo)};
   if (epi == 1) return c;
+  if (bd_applies(a)) {
+    c.tile = a.cout % 128 ? kTileBdC64 : kTileBdC128;
+    return c;
+  }
   if (fp6_applies(a)) {
     c.tile = a.cout % 128 ? kTileFp6C64 : kTileFp6C128;
     return c;
@@ -2700,6 +3106,41 @@ hipError_t launch_fpx(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   else
     hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, true, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
   return hipGetLastError();
+}
+
+// A tile kernel whose LDS is dynamic (lds bytes, above the static limit).
+template <typename K>
+hipError_t launch_dyn(K kern, const ConvArgs &a, const Geo &geo, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                      int npt, int ncb, int nch) {
+  hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, grid, block, lds, s, a, geo, npt, ncb, nch);
+  return hipGetLastError();
+}
+
+// The Eq. 4 decomposition: as launch_fpx, with the ring in dynamic LDS.
+template <int M, int WN>
+hipError_t launch_bd(const ConvArgs &a, const Geo &geo, hipStream_t s) {
+  using C = bd::Cfg<M, WN>;
+  const int npt = (int)((geo.M + C::TM - 1) / C::TM);
+  const int ncb = a.cout / C::TN;
+  const int64_t T = (int64_t)npt * ncb * a.in.groups;
+  if (T <= 0 || T > 0x3fffffff || geo.kb_total < 1) return hipErrorInvalidValue;
+  const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * C::GC * 32;
+  const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
+  const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(32, npt) : 1;
+  const size_t lds = (size_t)C::S * C::SST + (size_t)C::TN * (sizeof(RqConst) + 4);
+  const dim3 grid((unsigned)((T + 7) / 8 * 8)), block(C::NT);
+  if (a.res.data)
+    return a.acc_dump ? launch_dyn(conv_bitdecomp_kernel<M, WN, -1, true>, a, geo, grid, block, lds, s, npt, ncb, nch)
+                      : launch_dyn(conv_bitdecomp_kernel<M, WN, -1, false>, a, geo, grid, block, lds, s, npt, ncb, nch);
+  return a.acc_dump ? launch_dyn(conv_bitdecomp_kernel<M, WN, 0, true>, a, geo, grid, block, lds, s, npt, ncb, nch)
+                    : launch_dyn(conv_bitdecomp_kernel<M, WN, 0, false>, a, geo, grid, block, lds, s, npt, ncb, nch);
+}
+
+template <int M>
+hipError_t launch_bd_m(const ConvArgs &a, const Geo &geo, int tile, hipStream_t s) {
+  return tile == kTileBdC64 ? launch_bd<M, 1>(a, geo, s) : launch_bd<M, 2>(a, geo, s);
 }
 
 template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES, bool FP4 = false>
@@ -2784,6 +3225,7 @@ const char *conv_kernel_label(const ConvArgs &a, int epi) {
     case kTileStem: return "conv_tile_kernel[stem]";
     case kTileFp4C64: case kTileFp4C128: case kTileFp4C128P4: return "conv_fp4_kernel";
     case kTileFp6C64: case kTileFp6C128: return "conv_fp6_kernel";
+    case kTileBdC64: case kTileBdC128: return "conv_bitdecomp_kernel";
     case kTileI8C64: case kTileI8C128: return "conv_tile_kernel[int8]";
     default: return is_stem(a) ? "conv_stem_kernel" : "conv_grouped_kernel";
   }
@@ -2811,6 +3253,13 @@ hipError_t launch_conv_mfma(const ConvArgs &a_in, const uint8_t *wp, const int32
     case kTileFp4C128: e = launch_fpx<2, 2, 2, 2, 2>(a, g4, s); break;
     case kTileFp4C128P4: e = launch_fpx<2, 2, 4, 2, 2>(a, g4, s); break;
     case kTileFp6C64: e = launch_fpx<3, 2, 2, 1, 4>(a, g4, s); break;
+    case kTileBdC64: case kTileBdC128: {
+      Geo gb = g4;
+      gb.wp = wp + bd_offset(a);
+      e = a.in.bits == 4 ? launch_bd_m<4>(a, gb, c.tile, s)
+                         : a.in.bits == 6 ? launch_bd_m<6>(a, gb, c.tile, s) : launch_bd_m<8>(a, gb, c.tile, s);
+      break;
+    }
     case kTileFp6C128: e = launch_fpx<3, 2, 2, 2, 2>(a, g4, s); break;
     case kTileI8C64: e = launch_tile<2, 2, 1, 4>(a, geo, s); break;
     case kTileI8C128: e = launch_tile<2, 2, 2, 4>(a, geo, s); break;

@@ -163,6 +163,12 @@ palq_status palq_set_conv_fp4(palq_ctx *ctx, int32_t enable) {
   return PALQ_OK;
 }
 
+palq_status palq_set_conv_bitdecomp(palq_ctx *ctx, int32_t enable) {
+  if (!ctx || (enable != 0 && enable != 1)) return PALQ_ERR_ARG;
+  ctx->conv_bitdecomp = enable;
+  return PALQ_OK;
+}
+
 palq_status palq_sync(palq_ctx *ctx) {
   if (!ctx) return PALQ_ERR_ARG;
   if (ctx->device < 0) return PALQ_OK;
@@ -382,6 +388,7 @@ palq_status group_conv_impl(palq_ctx *ctx, const palq_act *in, const palq_filter
   a.mult = rq->mult; a.shift = rq->shift; a.bias = rq->bias;
   a.shuffle = (int32_t)(((int64_t)shuffle_steps % w->groups + w->groups) % w->groups);
   a.fp4 = ctx->conv_fp4;
+  a.bitdecomp = ctx->conv_bitdecomp;
   if (rid) { a.res = view_of(rid); a.res_mult = res->res_mult; }
   if (pin) { a.proj = view_of(pin); a.proj_w = (const uint8_t *)pw->data; a.proj_stride = res->proj_stride; }
   a.acc_dump = acc_dump;
@@ -490,6 +497,7 @@ palq_status palq_conv_plan_create(palq_ctx *ctx, const palq_act *in, const palq_
   a.ho = out->h; a.wo = out->w;
   a.shuffle = (int32_t)(((int64_t)shuffle_steps % G + G) % G);
   a.fp4 = ctx->conv_fp4;
+  a.bitdecomp = ctx->conv_bitdecomp;
   p->in_bytes = palq_act_bytes(in);
   p->out_bytes = palq_act_bytes(out);
   p->dump_bytes = (int64_t)out->n * out->h * out->w * nch * 4;

@@ -69,6 +69,7 @@ struct ConvArgs {
   int32_t proj_stride;
   int32_t *acc_dump;     // may be null
   int32_t fp4;           // 1: 2-bit layers may run on the FP4 matrix cores (where exact)
+  int32_t bitdecomp;     // 1: M-bit layers run as the Eq. 4 bit decomposition on FP4
   int32_t gated;         // set by the launcher: general partner of a tiled launch
 };
 
@@ -174,6 +175,7 @@ struct palq_ctx {
   int8_t *fc_scratch = nullptr;    // digit planes of the last FC call
   size_t fc_scratch_bytes = 0;
   int conv_fp4 = 1;                // palq_set_conv_fp4 (initial value: PALQ_CONV_FP4, default 1)
+  int conv_bitdecomp = 0;          // palq_set_conv_bitdecomp
   uint8_t *mod_scratch = nullptr;  // rotated parameters of the last shuffle-module call
   size_t mod_scratch_bytes = 0;
   hipEvent_t order_event = nullptr;  // palq_set_stream: the new stream waits for the old one

@@ -379,6 +379,7 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       a.cout = L.w.cout_pg; a.kh = L.w.kh; a.kw = L.w.kw; a.stride = L.stride; a.pad = L.pad;
       a.w_bits = L.w.bits;
       a.fp4 = ctx->conv_fp4;
+      a.bitdecomp = ctx->conv_bitdecomp;
       a.ho = NL.out_view.h; a.wo = NL.out_view.w;
       a.shuffle = (int32_t)(((int64_t)L.shuffle_steps % L.w.groups + L.w.groups) % L.w.groups);
       a.proj_stride = L.proj_stride;

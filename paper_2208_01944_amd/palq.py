@@ -75,6 +75,7 @@ _destroy = _sig("palq_destroy", None, c_p)
 _set_stream = _sig("palq_set_stream", c_i32, c_p, c_p)
 _sync = _sig("palq_sync", c_i32, c_p)
 _set_conv_fp4 = _sig("palq_set_conv_fp4", c_i32, c_p, c_i32)
+_set_conv_bitdecomp = _sig("palq_set_conv_bitdecomp", c_i32, c_p, c_i32)
 _last_error = _sig("palq_last_error", ctypes.c_char_p, c_p)
 _version = _sig("palq_version", ctypes.c_char_p)
 _row_bytes = _sig("palq_row_bytes", c_i64, c_i32, c_i32)
@@ -109,7 +110,7 @@ _net_layer_kernels = _sig("palq_net_layer_kernels", ctypes.c_char_p, c_p, c_i32,
 _net_layer_times = _sig("palq_net_layer_times", c_i32, c_p, ctypes.POINTER(c_f), ctypes.POINTER(c_i32))
 _net_reset_times = _sig("palq_net_reset_times", c_i32, c_p)
 
-EXPORTS = ["palq_create", "palq_destroy", "palq_set_stream", "palq_set_conv_fp4", "palq_sync", "palq_last_error",
+EXPORTS = ["palq_create", "palq_destroy", "palq_set_stream", "palq_set_conv_fp4", "palq_set_conv_bitdecomp", "palq_sync", "palq_last_error",
            "palq_version", "palq_row_bytes", "palq_act_bytes", "palq_pack", "palq_unpack",
            "palq_quantize", "palq_group_conv", "palq_group_conv_noalloc", "palq_conv_plan_create",
            "palq_conv_run", "palq_conv_plan_destroy", "palq_conv_plan_kernels", "palq_shuffle_module", "palq_cyclic_shuffle",
@@ -203,6 +204,11 @@ class Context:
         """FP4 (2-bit) and FP6 (3-bit) matrix cores for exact layers (True) or
         int8 only."""
         self._check(_set_conv_fp4(self.h, int(bool(enable))))
+
+    def set_conv_bitdecomp(self, enable: bool):
+        """Wide (4/6/8-bit) layers as the Eq. 4 bit decomposition on FP4
+        matrix cores (True) or directly on int8 (False, the default)."""
+        self._check(_set_conv_bitdecomp(self.h, int(bool(enable))))
 
     # ----------------------------------------------------------- memory
     def empty_act(self, n, h, w, groups, cpg, bits, signed=False) -> Tensor:

@@ -241,6 +241,28 @@ def test_resnet18_dense_wide_codes(ctx, torch, bits):
     np.testing.assert_array_equal(logits, ref)
 
 
+@pytest.mark.parametrize("bits", [4, 6, 8])
+def test_resnet18_dense_bitdecomp(ctx, torch, bits):
+    """The dense M-bit network run with every grouped layer as the Eq. 4 bit
+    decomposition on FP4 matrix cores: each of those layers launches
+    conv_bitdecomp_kernel, and every tensor and the logits equal the
+    oracle's (which computes the M-bit products directly)."""
+    say(f"resnet18 hw=32 n=2 G=1 b={bits} Eq. 4")
+    spec = I.resnet18(n=2, groups=1, bits=bits, hw=32, classes=10, seed=25 + bits)
+    spec = O.calibrate_centring(spec, spec["x"])
+    ctx.set_conv_bitdecomp(True)
+    try:
+        net, logits = gpu_forward(ctx, torch, spec, keep=True)
+    finally:
+        ctx.set_conv_bitdecomp(False)
+    convs = [i for i, L in enumerate(spec["layers"]) if L["op"] == "conv" and not L["in_signed"]]
+    kernels = net.layer_kernels()
+    assert all(kernels[i] == "conv_bitdecomp_kernel" for i in convs), kernels
+    ref, tensors, _ = O.run_net(spec, spec["x"], keep=True)
+    compare_tensors(ctx, net, spec, tensors, slice(None))
+    np.testing.assert_array_equal(logits, ref)
+
+
 def test_resnet18_bits3_g3(ctx, torch):
     say("resnet18 hw=32 n=3 G=3 b=3 centred")
     spec = I.resnet18(n=3, groups=3, bits=3, hw=32, classes=10, seed=13)
