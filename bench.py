@@ -120,6 +120,38 @@ def family(short):
     return "conv_tile_kernel[fp4]" if len(args) > 7 and args[7] == "true" else "conv_tile_kernel[int8]"
 
 
+def summarize_single_profile(d, workload):
+    """Kernel-time summary of one single-layer bench session (rocprofv3 csv
+    under DIR/kt, the bench's JSON lines in DIR/bench.json, one per layer or
+    sweep cell) written to profiles/<workload>_kernel_stats.md."""
+    import csv
+    import hashlib
+    lines = [json.loads(x) for x in open(os.path.join(d, "bench.json")).read().splitlines() if x.startswith("{")]
+    rows = list(csv.DictReader(open(os.path.join(d, "kt", "run_kernel_stats.csv"))))
+    out = ["# commands (run from the repository root, on one MI355X, `cd /tmp && export TMPDIR=/tmp` first;",
+           "# DIR is any output folder, W = " + workload + ")",
+           "#   rocprofv3 --kernel-trace --stats --output-format csv -d DIR/kt -o run -- "
+           "python3 bench.py --workload W --steps 50 --warmup 5 --no-cpu-baseline",
+           "#   python3 bench.py --workload W --steps 50 --warmup 5 --no-cpu-baseline > DIR/bench.json",
+           "#   python3 bench.py --workload W --summarize-profile DIR", "",
+           "Kernel time, rocprofv3 --kernel-trace --stats (all launches of the profiled run: plan-time",
+           "prepack and requant constants, warm-up and timed launches of every layer of the workload)", "",
+           "| kernel | calls | total ms | avg us | min us | max us | % |", "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        out.append(f"| {_short(r['Name'])} | {r['Calls']} | {int(r['TotalDurationNs']) / 1e6:.3f} | "
+                   f"{float(r['AverageNs']) / 1e3:.1f} | {int(r['MinNs']) / 1e3:.1f} | {int(r['MaxNs']) / 1e3:.1f} | "
+                   f"{float(r['Percentage']):.2f} |")
+    out += ["", "bench.py (HIP events around palq_conv_run, separate run):", "",
+            "| workload | kernel | us per launch | TOPS | roofline frac | peak |", "|---|---|---|---|---|---|"]
+    for b in lines:
+        rf = b["roofline"]
+        out.append(f"| {b['config']['workload']} | {b['kernel']} | {b['us_per_launch']:.1f} | {b['value']:.0f} | "
+                   f"{rf['frac']:.3f} | {rf['peak']:.0f} {rf['unit']} |")
+    out += ["", "kernel_source_sha256: " + hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()]
+    open(kernel_stats_file(workload), "w").write("\n".join(out) + "\n")
+    print("wrote", kernel_stats_file(workload))
+
+
 def summarize_profile(d, workload):
     """Writes the kernel-time summary of one profiling session (rocprofv3
     csv output under DIR: kt/ and bench.json) and, when DIR also holds the
@@ -725,7 +757,10 @@ def main():
                                    "(a batch-parallel split over GPUs is described in the design notes)"}))
         sys.exit(2)
     if args.summarize_profile:
-        summarize_profile(args.summarize_profile, args.workload)
+        if args.workload in NETWORKS:
+            summarize_profile(args.summarize_profile, args.workload)
+        else:
+            summarize_single_profile(args.summarize_profile, args.workload)
         return
     if args.summarize_counters:
         summarize_counters(args.summarize_counters, args.workload)

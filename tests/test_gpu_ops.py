@@ -383,6 +383,25 @@ def test_conv_bitdecomp(ctx, torch, name, bits):
         ctx.set_conv_bitdecomp(False)
 
 
+FEW_TILE_CASES = {
+    # 27 K-blocks (3 per tap), 16 tiles
+    "odd_kblocks": dict(n=2, h=14, w=14, groups=4, cin=192, cout=128, shuffle=1),
+    "identity": dict(n=2, h=14, w=14, groups=4, cin=128, cout=128, shuffle=1, residual="identity"),
+    "projection": dict(n=2, h=15, w=15, groups=4, cin=128, cout=128, stride=2, shuffle=3, residual="projection"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(FEW_TILE_CASES))
+def test_conv_fp4_c128_few_tiles(ctx, torch, name):
+    """128-channel FP4 layers with few tiles and long K-loops (an odd
+    K-block count, identity and projection shortcuts): every image's
+    accumulators (dump build) and codes, stated and centred, equal the
+    oracle's, also on int8 matrix cores."""
+    case = I.single_layer(2500 + sorted(FEW_TILE_CASES).index(name), **FEW_TILE_CASES[name])
+    say(f"conv FP4 few tiles {name} {case['x'].shape}")
+    check_full(ctx, torch, case)
+
+
 def test_conv_deterministic(ctx, torch):
     say("conv determinism")
     case = I.config_c2(1, n=4)
