@@ -63,7 +63,7 @@ def parse():
     return ap.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_tile_kernel_fp4_resnet18_g4_b2_bs64_traffic.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_fp4_kernel_resnet18_g4_b2_traffic.txt")
 DOMINANT = "conv_fp4_kernel"
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2208_01944_amd", "csrc", "k_conv_mfma.hip")
 
