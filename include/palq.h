@@ -254,7 +254,7 @@ palq_status palq_conv_run(palq_ctx *ctx, const palq_conv_plan *plan, const void 
 /* Frees a plan (waits for device work that still reads it). */
 void palq_conv_plan_destroy(palq_conv_plan *plan);
 /* The kernel family a plan runs without an accumulator dump (static host
- * string, e.g. "conv_tile_kernel[fp4]"; "" for a validate-only plan; NULL
+ * string, e.g. "conv_fp4_kernel"; "" for a validate-only plan; NULL
  * for a null plan). */
 const char *palq_conv_plan_kernels(const palq_conv_plan *plan);
 
@@ -396,7 +396,7 @@ int64_t palq_net_ops(const palq_net *net);
 
 /* The kernels a forward pass launches for layer `layer`, as the library's
  * own selection rules pick them at create time (host string owned by net,
- * valid until palq_net_destroy): e.g. "conv_tile_kernel[fp4]" or
+ * valid until palq_net_destroy): e.g. "conv_fp4_kernel" or
  * "quantize_pad4_kernel + stem_pool_kernel"; "" for a layer that an earlier
  * layer's launch already covers (a max pool fused into the stem) and for
  * every layer of a validate-only network.  image = 0: palq_forward,

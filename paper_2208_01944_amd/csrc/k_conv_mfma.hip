@@ -2956,18 +2956,24 @@ int tile_slots(const void *kern, int threads) {
 // The tiled kernel takes 2-bit grouped layers with 64-channel blocks and
 // 2-bit outputs (and 2-bit or no identity shortcut); a layer whose requant
 // needs the int64 path runs on the general partner launched beside it.
-bool tile_kernel_applies(const ConvArgs &a) {
+// 2-bit grouped layers with 2-bit outputs (and shortcut codes) and 64-channel
+// blocks: the layers the tiled 2-bit builds take.
+static bool grouped2_tiles(const ConvArgs &a) {
   const int64_t wbytes = (int64_t)a.in.groups * a.cout * make_geo(a).kb_total * 64;
   return !is_stem(a) && a.in.bits == 2 && a.w_bits == 2 && a.cout % 64 == 0 && wbytes < ((int64_t)1 << 30) &&
-         make_geo(a).kb_total >= kStages && a.out.bits == 2 && (!a.res.data || a.res.bits == 2);
+         a.out.bits == 2 && (!a.res.data || a.res.bits == 2);
 }
 
-// FP4 matrix cores for a tiled-kernel layer whose accumulator bound is below
+// The persistent int8 tile kernel keeps its ring full across tiles: at least
+// kStages K-blocks per tile.
+bool tile_kernel_applies(const ConvArgs &a) { return grouped2_tiles(a) && make_geo(a).kb_total >= kStages; }
+
+// FP4 matrix cores for a 2-bit tiled layer whose accumulator bound is below
 // 2^23 (the fp32 accumulator then holds every partial sum, and the shortcut
-// term, exactly), unless the context keeps layers on int8 (a.fp4 = 0).
-bool fp4_applies(const ConvArgs &a) {
-  return a.fp4 && tile_kernel_applies(a) && acc_bound_of(a) < ((int64_t)1 << 23);
-}
+// term, exactly), unless the context keeps layers on int8 (a.fp4 = 0).  The
+// FP4 kernel runs one tile per workgroup and takes any K-block count (1 x 1
+// layers over 64 or 128 input channels included).
+bool fp4_applies(const ConvArgs &a) { return a.fp4 && grouped2_tiles(a) && acc_bound_of(a) < ((int64_t)1 << 23); }
 
 // FP6 matrix cores for 3-bit grouped layers with 3-bit outputs, 64-channel
 // blocks and no shortcut, under the same accumulator bound (the fp32

@@ -402,6 +402,43 @@ def test_conv_fp4_c128_few_tiles(ctx, torch, name):
     check_full(ctx, torch, case)
 
 
+SHORT_K_CASES = {
+    # 1 x 1 layers with one or two K-blocks (the bottleneck 1 x 1 convs of
+    # ResNet-50's first two stages): 64-channel tiles, 128-channel tiles with
+    # an identity shortcut, and a projection that adds its own K-block
+    "c64_kb1": dict(n=2, h=13, w=14, groups=2, cin=64, cout=64, k=1, pad=0, shuffle=1),
+    "c256_kb1_identity": dict(n=2, h=14, w=14, groups=2, cin=64, cout=256, k=1, pad=0, shuffle=0,
+                              residual="identity"),
+    "c256_kb2_projection": dict(n=2, h=14, w=14, groups=2, cin=64, cout=256, k=1, pad=0, shuffle=0,
+                                residual="projection"),
+    "c512_kb2_identity": dict(n=2, h=7, w=9, groups=2, cin=128, cout=512, k=1, pad=0, shuffle=1,
+                              residual="identity", shift=18),  # one below the A13 shift: every code occurs
+    "c128_kb3_s2": dict(n=3, h=15, w=15, groups=3, cin=192, cout=128, k=1, stride=2, pad=0, shuffle=-1),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SHORT_K_CASES))
+def test_conv_fp4_short_k(ctx, torch, name):
+    """2-bit layers with fewer K-blocks than the ring has stages run on the
+    FP4 kernel (the plan names conv_fp4_kernel, conv_grouped_kernel with
+    FP4 switched off); every image's accumulators (dump build) and codes,
+    stated and centred, equal the oracle's on both paths."""
+    from paper_2208_01944_amd import palq
+    case = I.single_layer(2700 + sorted(SHORT_K_CASES).index(name), **SHORT_K_CASES[name])
+    L = case["layer"]
+    say(f"conv FP4 short K {name} {case['x'].shape}")
+    for fp, want in ((True, "conv_fp4_kernel"), (False, "conv_grouped_kernel")):
+        ctx.set_conv_fp4(fp)
+        try:
+            t = _layer_tensors(ctx, case, L["bias"])
+            plan = palq.ConvPlan(ctx, t["x"], t["w"], L["stride"], L["pad"], t["mult"], t["shift"], t["bias"],
+                                 t["out"], shuffle=L["shuffle"], **t["kw"])
+            assert plan.kernels == want, plan.kernels
+        finally:
+            ctx.set_conv_fp4(True)
+    check_full(ctx, torch, case)
+
+
 def test_conv_deterministic(ctx, torch):
     say("conv determinism")
     case = I.config_c2(1, n=4)
