@@ -246,6 +246,7 @@ struct Geo {
   const uint8_t *wp;  // weights in MFMA operand order (see prepack_kernel)
   const RqConst *rq;  // per-channel requant constants, then the int64-path flag
   const int32_t *acc0;  // B = 8: per-channel accumulator start 128 sum(w) (act_operand)
+  float inv_hw, inv_wo;  // 1 / (ho wo) and 1 / wo, rounded to fp32 (fdiv's estimates)
 };
 
 // A (kb, 32-channel block) slab of prepacked weights: [j][half][ch][16 B].
@@ -885,7 +886,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
   const int pixb = (int)a.in.pixel;
   const int rowb = a.in.w * pixb;
   const int HW = a.ho * a.wo;
-  const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
+  const float inv_hw = geo.inv_hw, inv_wo = geo.inv_wo;
 
   // ---- loader: tile lt, K-block cursor; geometry of tile lt per pixel block
   int lt = first, l_kb = 0, l_tap = 0, l_cblk = 0, l_ky = 0, l_kx = 0, l_tapoff = 0;
@@ -1035,7 +1036,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo
   const int pixb = (int)a.in.pixel;
   const int rowb = a.in.w * pixb;
   const int HW = a.ho * a.wo;
-  const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
+  const float inv_hw = geo.inv_hw, inv_wo = geo.inv_wo;
 
   int lt = first, l_kb = 0;
   int off0[PB], iy0[PB];
@@ -1307,7 +1308,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   const int pixb = (int)a.in.pixel;
   const int rowb = a.in.w * pixb;
   const int HW = a.ho * a.wo;
-  const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
+  const float inv_hw = geo.inv_hw, inv_wo = geo.inv_wo;
 
   // ---- fetcher: this thread's share of K-block f_kb of tile f_tile
   // weights: 16-byte pieces tid + i * NT of the K-block's TN/32 slabs;
@@ -2093,7 +2094,7 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
     woff[i] = (uint32_t)((((int64_t)g * (a.cout / 32) + cbk * (TN / 32) + c / PPS) * KB) * C::SLAB + (c % PPS) * 16);
   }
   const int HW = a.ho * a.wo;
-  const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
+  const float inv_hw = geo.inv_hw, inv_wo = geo.inv_wo;
   int off0[C::XL], poff[C::XL];
   uint32_t tmask[C::XL];
 #pragma unroll
@@ -2176,14 +2177,9 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
     }
   };
 
-  // ---- compute side
+  // ---- compute side (K-block 0's MFMAs take a zero C operand, so the
+  // accumulators need no initialisation)
   v16f acc[CB][PB];
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb)
-#pragma unroll
-    for (int pb = 0; pb < PB; ++pb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[cb][pb][r] = 0.f;
   // LDS addresses of this lane's operands in stage 0: activation half row of
   // pixel block 0 (blocks 512 bytes apart), weight unit of channel block 0
   // (blocks 1 KB apart)
@@ -2193,7 +2189,7 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
                           (uint32_t)(B == 2 ? (wm * PB * 32 + l32) * 16 + half * 8 : ((wm * PB) * 64 + lane) * 16);
   const uint32_t aaddr0 = lds_base + (uint32_t)((wn * CB) * C::SLAB + lane * 16);
   const uint32_t baddr0 = lds_base + (uint32_t)((wn * CB) * C::SLAB + 1024 + lane * 8);
-  auto kblock = [&](int st) __attribute__((always_inline)) {
+  auto kblock = [&](int st, bool first) __attribute__((always_inline)) {
     const uint32_t xa = xaddr0 + st * SST, aa = aaddr0 + st * SST;
     if constexpr (B == 3) {
       const uint32_t ba = baddr0 + st * SST;
@@ -2219,7 +2215,8 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
         const v8i Bop = fp6_operand((uint32_t)X[pb][0], (uint32_t)X[pb][1], (uint32_t)X[pb][2]);
 #pragma unroll
         for (int cb = 0; cb < CB; ++cb)
-          acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop[cb], Bop, acc[cb][pb], 2, 2, 0, 0, 0, 0);
+          acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop[cb], Bop, first ? v16f{} : acc[cb][pb], 2,
+                                                                        2, 0, 0, 0, 0);
       }
       return;
     }
@@ -2258,32 +2255,45 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
       const v8i Bop = __builtin_shufflevector(b, b, 0, 1, 2, 3, -1, -1, -1, -1);
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
-        acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop[cb], Bop, acc[cb][pb], 4, 4, 0, 0, 0, 0);
+        acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop[cb], Bop, first ? v16f{} : acc[cb][pb], 4, 4,
+                                                                      0, 0, 0, 0);
     }
   };
 
+  static_assert(S == 4, "the waits below count at most two younger fetches");
+  // wait until K-block kb's loads have landed, y of this wave's fetches
+  // (LPK loads or more each) being younger
+  auto wait_younger = [&](int y) __attribute__((always_inline)) {
+    if (y >= 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * C::LPK));
+    else if (y == 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::LPK));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  };
   __syncthreads();  // the tile's constants are in LDS
 #pragma unroll
   for (int st = 0; st < S - 1; ++st)
     if (st < KB) fetch(st);
+  // K-block 0 (KB >= 1)
+  const bool steady0 = KB > S - 1;
+  wait_younger(steady0 ? S - 2 : KB - 1);
+  ring_barrier();
+  if (steady0) fetch(S - 1);
+  kblock(0, true);
   // steady state: K-block kb's loads were issued S - 1 fetches ago; at most
   // (S - 2) LPK of this wave's loads are younger
-  int kb = 0;
+  int kb = 1;
   for (; kb + S - 1 < KB; ++kb) {
     __builtin_amdgcn_s_waitcnt(waitcnt_vm((S - 2) * C::LPK));
     ring_barrier();
     fetch((kb + S - 1) % S);
-    kblock(kb % S);
+    kblock(kb % S, false);
   }
   // the last S - 1 K-blocks: no more fetches, the waits tighten
 #pragma unroll
   for (int i = 0; i < S - 1; ++i) {
-    if (kb >= KB) break;  // uniform (KB < S - 1)
-    if (KB - 1 - kb >= 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * C::LPK));
-    else if (KB - 1 - kb == 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(C::LPK));
-    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    if (kb >= KB) break;  // uniform
+    wait_younger(KB - 1 - kb);
     ring_barrier();
-    kblock(kb % S);
+    kblock(kb % S, false);
     ++kb;
   }
 
@@ -2475,7 +2485,7 @@ __global__ __launch_bounds__(WN * 128, 2) void conv_bitdecomp_kernel(ConvArgs a,
                          (c % (64 * GC)) * 16);
   }
   const int HW = a.ho * a.wo;
-  const float inv_hw = 1.0f / (float)HW, inv_wo = 1.0f / (float)a.wo;
+  const float inv_hw = geo.inv_hw, inv_wo = geo.inv_wo;
   int off0[C::XL], poff[C::XL];
   uint32_t tmask[C::XL];
 #pragma unroll
@@ -2691,6 +2701,8 @@ bool is_stem(const ConvArgs &a) {
 Geo make_geo(const ConvArgs &a) {
   Geo geo{};
   geo.M = a.out.n * a.ho * a.wo;
+  geo.inv_hw = a.ho * a.wo > 0 ? 1.0f / (float)(a.ho * a.wo) : 0.0f;
+  geo.inv_wo = a.wo > 0 ? 1.0f / (float)a.wo : 0.0f;
   if (is_stem(a)) {
     geo.kb_main = (a.kh + 1) / 2;  // two filter rows per K-block
     geo.kb_total = geo.kb_main;
