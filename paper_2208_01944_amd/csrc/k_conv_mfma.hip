@@ -47,6 +47,7 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef int v2i __attribute__((ext_vector_type(2)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 
 // ---------------------------------------------------------------- unpack
@@ -232,6 +233,41 @@ __global__ void requant_prep_kernel(const int32_t *mult, const int32_t *shift, c
   if (bad) atomicOr(&any, 1);
   __syncthreads();
   if (threadIdx.x == 0) *flag = any;
+}
+
+// The FP4 kernel's fp32 requant (2-bit outputs).  The accumulator starts at
+// b4 = bias / 4 and adds the products as multiples of 1/4, so it holds
+// u / 4 with u = t + bias (the identity shortcut's rm c / 4 added in fp32);
+// every partial value is exact when |t| + |bias| + 3 |rm| < 2^24.  With
+// sc = M 2^(2 - sh) (exact for |M| < 2^24) one fma gives
+//   y = RN(u M 2^-sh + 1/2) = RN(x),  x = (u M + 2^(sh-1)) 2^-sh,
+// a single rounding of x.  x 2^sh is an integer, so below an integer k <= 3
+// x stays at least 2^-sh <= 2^-22 under k, more than half the fp32 spacing
+// there (2^-23): RN(x) < k whenever x < k, and RN(x) >= floor(x) always.
+// Hence min(trunc(y), 3) (v_cvt_u32_f32 truncates and takes negative values
+// to 0) equals clamp(floor(x), 0, 3), the definition, for sh <= 22.  flag:
+// 1 when every channel meets the bounds (else the fp64 epilogue runs).
+__global__ void requant_prep_f32_kernel(const int32_t *mult, const int32_t *shift, const int32_t *bias,
+                                        const int32_t *res_mult, int res_max, int nch, int64_t acc_bound, float *sc,
+                                        float *b4, int32_t *flag) {
+  __shared__ int any_bad;
+  if (threadIdx.x == 0) any_bad = 0;
+  __syncthreads();
+  int bad = 0;
+  for (int c = threadIdx.x; c < nch; c += blockDim.x) {
+    const int64_t m = mult[c];
+    const int sh = shift[c];
+    const int64_t b = bias ? bias[c] : 0;
+    const int64_t rm = res_mult ? res_mult[c] : 0;
+    const int64_t lim = (int64_t)1 << 24;
+    const int64_t umax = acc_bound + (b < 0 ? -b : b) + (rm < 0 ? -rm : rm) * res_max;
+    if (sh < 1 || sh > 22 || m <= -lim || m >= lim || umax >= lim) bad = 1;
+    sc[c] = bad ? 0.0f : ldexpf((float)m, 2 - sh);
+    b4[c] = bad ? 0.0f : (float)b * 0.25f;
+  }
+  if (bad) atomicOr(&any_bad, 1);
+  __syncthreads();
+  if (threadIdx.x == 0) *flag = any_bad ? 0 : 1;
 }
 
 // ---------------------------------------------------------------- geometry
@@ -621,12 +657,17 @@ typedef double dbl2 __attribute__((ext_vector_type(2)));
 // LAZY (2-bit shortcut, PB = 2): rw is unused; each channel block's shortcut
 // words are read from LDS at rwl + 8 cb (pixel block 0) and + rws (pixel
 // block 1) when that block is processed, which keeps fewer registers live.
-template <int BO, int CB, int PB, int RB, typename AccV, bool LAZY = false>
+// F32 (FP4 accumulator, 2-bit outputs): the accumulator already holds
+// (t + bias) / 4 and scf[c] is the channel's fp32 scale M 2^(2 - sh); the
+// requant is min(trunc(fma(v, scf, 1/2)), 3), exact under the bounds
+// requant_prep_f32_kernel checks (rq is then unused).
+template <int BO, int CB, int PB, int RB, typename AccV, bool LAZY = false, bool F32 = false>
 __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &geo, AccV (&acc)[CB][PB],
                                         const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
                                         int l32, int half, const RqConst *rq, const int32_t *rm,
-                                        uint32_t rwl = 0, uint32_t rws = 0) {
+                                        uint32_t rwl = 0, uint32_t rws = 0, const float *scf = nullptr) {
   static_assert(!LAZY || PB == 2 || PB == 4, "lazy shortcut reads are written for two or four pixel blocks");
+  static_assert(!F32 || (BO == 2 && std::is_same<AccV, v16f>::value), "the fp32 requant takes FP4 accumulators");
   constexpr int bo = BO;
   // BO = 8 also stores 6-bit codes (one per byte), clamped at 63
   const uint32_t qmax = BO == 8 ? (1u << a.out.bits) - 1u : (1u << BO) - 1u;
@@ -634,16 +675,26 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
   // requant constants (and shortcut multipliers) of quad j = 4 cb + qi,
   // read one quad ahead of their use so that their LDS latency overlaps
   // the previous quad's arithmetic
-  auto quad_consts = [&](int j, dbl2 (&k)[4], v4i &rmu) __attribute__((always_inline)) {
+  auto quad_consts = [&](int j, dbl2 (&k)[4], v4f &kf, v4i &rmu) __attribute__((always_inline)) {
     const int c0 = (j >> 2) * 32 + 8 * (j & 3) + 4 * half;
+    if constexpr (F32) {
+      kf = *(const v4f *)(scf + c0);
+    } else {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) k[e] = dbl2{rq[c0 + e].s, rq[c0 + e].o};
+      for (int e = 0; e < 4; ++e) k[e] = dbl2{rq[c0 + e].s, rq[c0 + e].o};
+    }
     rmu = v4i{0, 0, 0, 0};
     if constexpr (RB != 0) rmu = *(const v4i *)(rm + c0);
   };
   dbl2 k_cur[4];
+  v4f kf_cur;
   v4i rmu_cur;
-  quad_consts(0, k_cur, rmu_cur);
+  quad_consts(0, k_cur, kf_cur, rmu_cur);
+  // 2-bit codes of two channel blocks and an even number of pixel blocks:
+  // each lane gathers its pixel's 64 channels (16 bytes) and stores them at
+  // once; w2[cb][pb] holds the lane's 16 channels of block (cb, pb)
+  constexpr bool ST16 = BO == 2 && CB == 2 && PB % 2 == 0;
+  uint32_t w2[CB][PB];
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     const int kc = ch0 + cb * 32;
@@ -683,11 +734,12 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
       __builtin_amdgcn_sched_barrier(0);
       const int cq = 8 * qi + 4 * half;
       dbl2 k[4];
+      v4f kf = kf_cur;
       v4i rmu;
 #pragma unroll
       for (int e = 0; e < 4; ++e) k[e] = k_cur[e];
       rmu = rmu_cur;
-      if (4 * cb + qi + 1 < 4 * CB) quad_consts(4 * cb + qi + 1, k_cur, rmu_cur);
+      if (4 * cb + qi + 1 < 4 * CB) quad_consts(4 * cb + qi + 1, k_cur, kf_cur, rmu_cur);
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb) {
         constexpr bool FACC = std::is_same<AccV, v16f>::value;
@@ -713,9 +765,14 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
         uint32_t qword = 0, hword = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const double d = __builtin_fma((double)v[e], k[e].x, k[e].y);
           uint32_t q;
-          asm("v_cvt_u32_f64 %0, %1" : "=v"(q) : "v"(d));
+          if constexpr (F32) {
+            const float y = __builtin_fmaf((float)v[e], kf[e], 0.5f);
+            asm("v_cvt_u32_f32 %0, %1" : "=v"(q) : "v"(y));
+          } else {
+            const double d = __builtin_fma((double)v[e], k[e].x, k[e].y);
+            asm("v_cvt_u32_f64 %0, %1" : "=v"(q) : "v"(d));
+          }
           if constexpr (BO == 3) {
             const uint32_t qq = min(q, qmax);
             qword |= (qq & 3u) << (2 * e);
@@ -750,6 +807,10 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
         if (half == 0) cw[2] = hw;
         continue;
       }
+      if constexpr (ST16) {
+        w2[cb][pb] = Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24);
+        continue;
+      }
       if (mp >= geo.M) continue;
       uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row) +
                      (int64_t)(kc >> 5) * bo + half * (bo / 2);
@@ -760,6 +821,20 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
       } else {
         *(uint4 *)cw = make_uint4(Q[0], Q[1], Q[2], Q[3]);
       }
+    }
+  }
+  if constexpr (ST16) {
+    // pixel blocks 2 i and 2 i + 1: lanes of half 0 take block 2 i, lanes of
+    // half 1 block 2 i + 1; per channel block the swap brings the other
+    // half's 16 channels of that pixel (words ordered cb, half as stored)
+#pragma unroll
+    for (int i = 0; i < PB / 2; ++i) {
+      const auto s0 = __builtin_amdgcn_permlane32_swap(w2[0][2 * i], w2[0][2 * i + 1], false, false);
+      const auto s1 = __builtin_amdgcn_permlane32_swap(w2[1][2 * i], w2[1][2 * i + 1], false, false);
+      const int64_t mp = mbase + (2 * i + half) * 32 + l32;
+      if (mp >= geo.M) continue;
+      uint8_t *dst = a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row + (int64_t)(ch0 >> 5) * 8;
+      *(uint4 *)dst = make_uint4(s0[0], s0[1], s1[0], s1[1]);
     }
   }
 }
@@ -2032,7 +2107,9 @@ struct Cfg {
 // each pixel's K-block staged as its two 12-byte chunks in 16-byte pieces
 // (the chunk's three words at the start of each), fp6_operand, and a 3-bit
 // fast epilogue; no shortcut.
-template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S, int B>
+// F32 (B = 2): the fp32 requant of requant_prep_f32_kernel; K-block 0's
+// MFMAs start from the channels' bias / 4 instead of zero.
+template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S, int B, bool F32 = false>
 __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo, int npt, int ncb, int nch) {
   using C = f4::Cfg<CB, PB, WN, WM, B>;
   constexpr int NT = C::NT, TN = C::TN, TM = C::TM, WST = C::WST, SST = C::SST;
@@ -2040,6 +2117,7 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   static_assert(RB == 0 || RPT * NT * 16 == C::RSB, "whole shortcut pieces per thread");
   static_assert(CB == 2 && (PB == 2 || PB == 4), "operand reads are written for 2 x 2 and 2 x 4 blocks");
   static_assert(B == 2 || (B == 3 && PB == 2 && RB == 0), "FP6: 2 x 2 blocks, no shortcut");
+  static_assert(!F32 || B == 2, "the fp32 requant takes FP4 accumulators");
   constexpr int XB = B == 2 ? 16 : 24;  // activation bytes of a pixel's K-block
   __shared__ __attribute__((aligned(1024))) uint8_t lds[S * SST + (RB ? C::RSB : 16)];
   __shared__ RqConst rq_area[TN];
@@ -2064,10 +2142,19 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   const int wn = wave / WM, wm = wave % WM;
   const int KB = geo.kb_total, KM = geo.kb_main;
 
-  // requant constants (and shortcut multipliers) of the tile's TN channels
+  // requant constants (and shortcut multipliers) of the tile's TN channels;
+  // F32: the fp32 scales, then bias / 4, in rq_area's bytes
   const int64_t ch0 = (int64_t)g * a.cout + cbk * TN;
+  float *const sc_area = (float *)rq_area, *const b4_area = sc_area + TN;
   for (int c = tid; c < TN; c += NT) {
-    rq_area[c] = geo.rq[ch0 + c];
+    if constexpr (F32) {
+      const int64_t nall = (int64_t)G * a.cout;
+      const float *f32c = (const float *)(geo.rq + nall + 1);
+      sc_area[c] = f32c[ch0 + c];
+      b4_area[c] = f32c[nall + ch0 + c];
+    } else {
+      rq_area[c] = geo.rq[ch0 + c];
+    }
     if constexpr (RB != 0) rm_area[c] = a.res_mult[ch0 + c];
   }
   typedef __attribute__((address_space(3))) void *lds_ptr;
@@ -2177,9 +2264,10 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
     }
   };
 
-  // ---- compute side (K-block 0's MFMAs take a zero C operand, so the
-  // accumulators need no initialisation)
+  // ---- compute side (K-block 0's MFMAs take a zero C operand, or F32 the
+  // channels' bias / 4, so the accumulators need no initialisation)
   v16f acc[CB][PB];
+  v16f c0[CB];  // F32: K-block 0's C operand of channel block cb
   // LDS addresses of this lane's operands in stage 0: activation half row of
   // pixel block 0 (blocks 512 bytes apart), weight unit of channel block 0
   // (blocks 1 KB apart)
@@ -2255,8 +2343,8 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
       const v8i Bop = __builtin_shufflevector(b, b, 0, 1, 2, 3, -1, -1, -1, -1);
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb)
-        acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop[cb], Bop, first ? v16f{} : acc[cb][pb], 4, 4,
-                                                                      0, 0, 0, 0);
+        acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+            Aop[cb], Bop, first ? (F32 ? c0[cb] : v16f{}) : acc[cb][pb], 4, 4, 0, 0, 0, 0);
     }
   };
 
@@ -2272,6 +2360,18 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
 #pragma unroll
   for (int st = 0; st < S - 1; ++st)
     if (st < KB) fetch(st);
+  if constexpr (F32) {
+    // element r of block cb is channel 32 cb + 8 (r / 4) + 4 half + r % 4
+    // of the wave's channels
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int qi = 0; qi < 4; ++qi) {
+        const v4f b = *(const v4f *)(b4_area + wn * CB * 32 + cb * 32 + 8 * qi + 4 * half);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) c0[cb][4 * qi + e] = b[e];
+      }
+  }
   // K-block 0 (KB >= 1)
   const bool steady0 = KB > S - 1;
   wait_younger(steady0 ? S - 2 : KB - 1);
@@ -2312,7 +2412,11 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
         for (int qi = 0; qi < 4; ++qi) {
           v4i dv;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) dv[e] = (int)(acc[cb][pb][4 * qi + e] * (B == 2 ? 4.0f : 8.0f));  // exact: |t| < 2^23
+          for (int e = 0; e < 4; ++e) {
+            // exact: |t| < 2^23 (F32: the accumulator is (t + bias) / 4, each term below 2^22)
+            const float b = F32 ? b4_area[wn * CB * 32 + cb * 32 + 8 * qi + 4 * half + e] : 0.0f;
+            dv[e] = (int)((acc[cb][pb][4 * qi + e] - b) * (B == 2 ? 4.0f : 8.0f));
+          }
           *(v4i *)(dst + 8 * qi) = dv;
         }
       }
@@ -2321,14 +2425,14 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   // ra + pb 32 RPX + 8 cb (read per channel block by the epilogue)
   const uint32_t ra = RB == 2 ? lds_base + S * SST + (uint32_t)((wm * PB * 32 + l32) * C::RPX + wn * CB * 8) : 0u;
   uint32_t rw[CB][PB][2] = {};
-  epilogue_fast_bo<B, CB, PB, RB, v16f, true>(a, geo, acc, rw, mbase, g, gd, cbk * TN + wn * CB * 32, l32, half,
-                                                rq_area + wn * CB * 32, rm_area + (RB ? wn * CB * 32 : 0), ra,
-                                                32 * C::RPX);
+  epilogue_fast_bo<B, CB, PB, RB, v16f, true, F32>(a, geo, acc, rw, mbase, g, gd, cbk * TN + wn * CB * 32, l32, half,
+                                                     rq_area + wn * CB * 32, rm_area + (RB ? wn * CB * 32 : 0), ra,
+                                                     32 * C::RPX, sc_area + wn * CB * 32);
 }
 
-template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S>
+template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S, bool F32>
 __global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, Geo geo, int npt, int ncb, int nch) {
-  conv_fpx_tile<CB, PB, WN, WM, RB, DUMP, S, 2>(a, geo, npt, ncb, nch);
+  conv_fpx_tile<CB, PB, WN, WM, RB, DUMP, S, 2, F32>(a, geo, npt, ncb, nch);
 }
 template <int CB, int PB, int WN, int WM, bool DUMP, int S>
 __global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp6_kernel(ConvArgs a, Geo geo, int npt, int ncb, int nch) {
@@ -2843,6 +2947,7 @@ ConvPlan conv_mfma_plan(const ConvArgs &a) {
   if (fp4_applies(a)) {  // FP4 slabs and constants after the int8 ones (the general build keeps those)
     p.w_bytes += (size_t)a.in.groups * a.cout * geo.kb_total * 32;
     p.thr_bytes *= 2;
+    p.thr_bytes += (size_t)a.in.groups * a.cout * 8 + 16;  // fp32 scale and bias / 4, flag
   }
   return p;
 }
@@ -2906,10 +3011,23 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
   RqConst *rq4 = rq + nch + 1;  // the FP4 accumulator is t / 4
   hipLaunchKernelGGL(requant_prep_kernel, dim3(1), dim3(256), 0, s, a.mult, a.shift, a.bias, a.res.data ? a.res_mult : nullptr,
                      res_max, nch, -2, acc_bound, rq4, (int32_t *)(rq4 + nch));
+  float *f32c = (float *)(rq4 + nch + 1);
+  hipLaunchKernelGGL(requant_prep_f32_kernel, dim3(1), dim3(256), 0, s, a.mult, a.shift, a.bias,
+                     a.res.data ? a.res_mult : nullptr, res_max, nch, acc_bound, f32c, f32c + nch,
+                     (int32_t *)(f32c + 2 * nch));
   return hipGetLastError();
 }
 
 bool conv_mfma_pads_input(const ConvArgs &a) { return is_stem(a) && a.pad > 0; }
+
+bool conv_mfma_f32(const ConvArgs &a, const int32_t *thr) {
+  if (!fp4_applies(a) || bd_applies(a) || fp6_applies(a)) return false;
+  const int64_t nch = (int64_t)a.in.groups * a.cout;
+  const float *f32c = (const float *)((const RqConst *)thr + 2 * (nch + 1));
+  int32_t ok = 0;
+  if (hipMemcpy(&ok, f32c + 2 * nch, sizeof(ok), hipMemcpyDeviceToHost) != hipSuccess) return false;
+  return ok == 1;
+}
 
 int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr) {
   if (!bd_applies(a) && ((a.out.bits == 3 && !fp6_applies(a)) || (a.res.data && a.res.bits != 2))) return 1;
@@ -3115,14 +3233,26 @@ hipError_t launch_fpx(const ConvArgs &a, const Geo &geo, hipStream_t s) {
       hipLaunchKernelGGL((conv_fp6_kernel<CB, PB, WN, WM, true, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
     return hipGetLastError();
   }
+  // the fp32 requant where the plan found it exact for every channel
+  if (a.f32ep) {
+    if (!a.res.data && !a.acc_dump)
+      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, false, S, true>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    else if (!a.acc_dump)
+      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, false, S, true>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    else if (!a.res.data)
+      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, true, S, true>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    else
+      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, true, S, true>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    return hipGetLastError();
+  }
   if (!a.res.data && !a.acc_dump)
-    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, false, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, false, S, false>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else if (!a.acc_dump)
-    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, false, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, false, S, false>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else if (!a.res.data)
-    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, true, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, true, S, false>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else
-    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, true, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, true, S, false>), grid, block, 0, s, a, geo, npt, ncb, nch);
   return hipGetLastError();
 }
 

@@ -558,6 +558,7 @@ palq_status palq_conv_plan_create(palq_ctx *ctx, const palq_act *in, const palq_
     // a layer too long for the general build's LDS runs its general
     // epilogue on the direct kernel
     if (p->epi == 1 && !conv_mfma_general_fits(a)) p->mfma = false;
+    a.f32ep = p->mfma && p->epi == 0 && conv_mfma_f32(a, p->thr);
   }
   a.in.data = a.out.data = a.res.data = a.proj.data = nullptr;
   *plan = p;

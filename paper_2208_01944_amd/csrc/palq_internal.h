@@ -71,6 +71,7 @@ struct ConvArgs {
   int32_t fp4;           // 1: 2-bit layers may run on the FP4 matrix cores (where exact)
   int32_t bitdecomp;     // 1: M-bit layers run as the Eq. 4 bit decomposition on FP4
   int32_t gated;         // set by the launcher: general partner of a tiled launch
+  int32_t f32ep;         // 1: the FP4 kernel's exact fp32 requant applies (conv_mfma_f32)
 };
 
 // Kernel launchers (return hipError_t of the launch).
@@ -100,6 +101,10 @@ bool conv_mfma_pads_input(const ConvArgs &a);
 // the stream has drained: 0 fast, 1 general, -1 unknown (copy failed).
 // Synchronous; for planning only.
 int conv_mfma_epilogue(const ConvArgs &a, const int32_t *thr);
+// For a layer on the FP4 kernel with the fast epilogue: whether every
+// channel's requant is exact in fp32 (written by launch_conv_prepare; reads
+// one flag word back, blocking).  Callers keep the answer in ConvArgs::f32ep.
+bool conv_mfma_f32(const ConvArgs &a, const int32_t *thr);
 // epi: the value above, or -1 when it is not known on the host: both builds
 // start and each checks on the device whether it applies (the other returns
 // at once); no host synchronisation either way.

@@ -519,6 +519,7 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
       // a layer too long for the general build's LDS runs its general
       // epilogue on the direct kernel
       if (NL.epi != 0 && !conv_mfma_general_fits(NL.conv)) NL.use_mfma = false;
+      NL.conv.f32ep = NL.use_mfma && NL.epi == 0 && conv_mfma_f32(NL.conv, NL.thr);
     }
   // fuse the stem with a max pool that is its output's only reader
   if (!(flags & PALQ_NET_KEEP_ALL))

@@ -211,10 +211,28 @@ def test_conv_empty_batch(ctx, torch):
     assert q.size == 0 and racc.size == 0
 
 
+def _residual_args(ctx, case):
+    """The layer's shortcut as palq keyword arguments (identity codes with
+    their multipliers, or the projection input and filter), {} if none."""
+    L = case["layer"]
+    G = L["w"].shape[0]
+    i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
+    if L["res"] >= 0:
+        return dict(identity=ctx.pack(case["extra"][1], G, L["out_bits"]), res_mult=i32(L["res_mult"]))
+    if L["proj_src"] >= 0:
+        pt, pw = ctx.pack_filter(L["proj_w"], L["w_bits"])
+        return dict(proj_in=ctx.pack(case["extra"][1], G, L["in_bits"]), proj_w=pw,
+                    proj_stride=L["proj_stride"], _keep=pt)
+    return {}
+
+
 def run_conv_full(ctx, torch, case, bias):
-    """GPU only (no oracle): codes of the whole batch from the plain launch,
-    then codes and accumulators from the accumulator-dump launch (the same
-    kernel family with its dump build)."""
+    """GPU only (no oracle), the layer with its shortcut: codes of the whole
+    batch from palq_group_conv, then from a plan of the layer (the launch
+    networks and the benchmark use) without and with the accumulator dump
+    (the same kernel family with its dump build).  Returns (group_conv
+    codes, plan codes, plan dump-build codes, dumped accumulators)."""
+    from paper_2208_01944_amd import palq
     L = case["layer"]
     x = case["x"]
     G, co, kh, kw, ci = L["w"].shape
@@ -226,31 +244,46 @@ def run_conv_full(ctx, torch, case, bias):
     out = ctx.empty_act(n, ho, wo, G, co, L["out_bits"])
     dump = torch.zeros(n * ho * wo * G * co, dtype=torch.int32, device=ctx.dev)
     i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
+    res = _residual_args(ctx, case)
+    keep = res.pop("_keep", None)
     args = (xt, wf, L["stride"], L["pad"], i32(L["mult"]), i32(L["shift"]), i32(bias), out)
-    ctx.group_conv(*args, shuffle=L["shuffle"])
+    ctx.group_conv(*args, shuffle=L["shuffle"], **res)
+    ctx.sync()
+    q_direct = ctx.unpack(out)
+    plan = palq.ConvPlan(ctx, *args, shuffle=L["shuffle"], **res)
+    res_in = res.get("identity", res.get("proj_in"))
+    out.buf.fill_(0)
+    plan.run(xt, out, res_in)
     ctx.sync()
     q_plain = ctx.unpack(out)
     dump.fill_(-1)
-    ctx.group_conv(*args, shuffle=L["shuffle"], acc_dump=dump)
+    plan.run(xt, out, res_in, acc_dump=dump)
     ctx.sync()
+    del keep
     acc = dump.cpu().numpy().astype(np.int64).reshape(n, ho, wo, G * co)
-    return q_plain, ctx.unpack(out), acc
+    return q_direct, q_plain, ctx.unpack(out), acc
 
 
 def oracle_full(case):
     """The oracle on the whole batch, accumulator once: (acc_d, stated codes,
-    centred bias, centred codes).  The centred bias (reading A14) is the
-    oracle's centring over the positions whose window lies inside the image
-    (stride-1 layers): border pixels, with fewer taps, then saturate while
-    the interior spreads over every code (centring over all positions leaves
-    7x7 and 14x14 maps with almost no middle codes)."""
+    centred bias, centred codes), shortcut included (acc_d holds a fused
+    projection's accumulator, not an identity shortcut).  The centred bias
+    (reading A14) is the oracle's centring over the positions whose window
+    lies inside the image (stride-1 layers): border pixels, with fewer taps,
+    then saturate while the interior spreads over every code (centring over
+    all positions leaves 7x7 and 14x14 maps with almost no middle codes)."""
     L = case["layer"]
     G = L["w"].shape[0]
     acc = O.group_conv(case["x"], L["w"], L["stride"], L["pad"])
-    q_stated, acc_d = O.layer_epilogue(acc, G, L["mult"], L["shift"], L["bias"], L["out_bits"], L["shuffle"])
+    res = case["extra"].get(1) if L["res"] >= 0 else None
+    px = case["extra"].get(1) if L["proj_src"] >= 0 else None
+    sc = dict(res=res, res_mult=L["res_mult"] if res is not None else None, proj_x=px,
+              proj_w=L["proj_w"] if px is not None else None, proj_stride=L["proj_stride"])
+    q_stated, acc_d = O.layer_epilogue(acc, G, L["mult"], L["shift"], L["bias"], L["out_bits"], L["shuffle"], **sc)
     p = L["pad"] if L["stride"] == 1 else 0
-    bias_c = O.centring_bias(acc_d[:, p:acc_d.shape[1] - p, p:acc_d.shape[2] - p], G, L["shuffle"])
-    q_centred, _ = O.layer_epilogue(acc, G, L["mult"], L["shift"], bias_c, L["out_bits"], L["shuffle"])
+    crop = lambda a: a[:, p:a.shape[1] - p, p:a.shape[2] - p] if a is not None else None
+    bias_c = O.centring_bias(crop(acc_d), G, L["shuffle"], res=crop(res), res_mult=sc["res_mult"])
+    q_centred, _ = O.layer_epilogue(acc, G, L["mult"], L["shift"], bias_c, L["out_bits"], L["shuffle"], **sc)
     return acc_d, q_stated, bias_c, q_centred
 
 
@@ -273,10 +306,11 @@ def check_full(ctx, torch, case, fp4_modes=(True, False), all_codes=True):
         try:
             for name, bias, want in (("centred", bias_c, q_centred), ("stated", L["bias"], q_stated)):
                 say(f"  fp4={fp4} {name}")
-                q_plain, q_dump, acc = run_conv_full(ctx, torch, case, bias)
+                q_direct, q_plain, q_dump, acc = run_conv_full(ctx, torch, case, bias)
                 np.testing.assert_array_equal(acc, acc_d, err_msg=f"acc fp4={fp4} {name}")
                 np.testing.assert_array_equal(q_dump, want, err_msg=f"codes (dump build) fp4={fp4} {name}")
                 np.testing.assert_array_equal(q_plain, want, err_msg=f"codes fp4={fp4} {name}")
+                np.testing.assert_array_equal(q_direct, want, err_msg=f"codes (palq_group_conv) fp4={fp4} {name}")
         finally:
             ctx.set_conv_fp4(True)
 
