@@ -473,6 +473,24 @@ def test_conv_fp4_short_k(ctx, torch, name):
     check_full(ctx, torch, case)
 
 
+@pytest.mark.parametrize("kind", ["shift23", "big_bias"])
+def test_conv_fp4_requant_outside_fp32_bounds(ctx, torch, kind):
+    """FP4 layers whose requant leaves the fp32 epilogue's bounds (a shift
+    of 23; biases of magnitude 2^24 on some channels, with an identity
+    shortcut) run the fp64 epilogue of the same kernel in a plan: every
+    image's codes and accumulators, stated and centred, equal the oracle's."""
+    if kind == "shift23":
+        case = I.single_layer(2800, n=2, h=14, w=14, groups=4, cin=64, cout=64, shuffle=1, shift=23)
+    else:
+        case = I.single_layer(2801, n=2, h=14, w=14, groups=2, cin=128, cout=128, shuffle=1, residual="identity")
+        b = np.array(case["layer"]["bias"], np.int64)
+        b[::7] = 1 << 24
+        b[3::7] = -(1 << 24)
+        case["layer"]["bias"] = b.astype(np.int32)
+    say(f"conv FP4 requant outside the fp32 bounds: {kind}")
+    check_full(ctx, torch, case, fp4_modes=(True,), all_codes=False)
+
+
 def test_conv_deterministic(ctx, torch):
     say("conv determinism")
     case = I.config_c2(1, n=4)
