@@ -52,7 +52,7 @@ def parse():
                          "cwrite/ and bench.json, made by the commands written into the summaries) "
                          "into the text summaries under profiles/ and exit")
     ap.add_argument("--summarize-counters", metavar="DIR", default=None,
-                    help="only turn the SQ counter passes under DIR (p1/, p2/, p3/ and bench.json) into "
+                    help="only turn the counter passes under DIR (p1/ .. p5/ and bench.json) into "
                          "profiles/<workload>_sq_counters.md and exit")
     ap.add_argument("--table2", action="store_true",
                     help="only run the Table 2 analogue (PalQuant against the dense M-bit network and "
@@ -240,14 +240,22 @@ COUNTER_PASSES = [
     "SQ_ACTIVE_INST_LDS SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_VMEM SQ_INST_CYCLES_VMEM_RD SQ_LDS_BANK_CONFLICT "
     "SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_WAIT_INST_LDS",
     "GRBM_GUI_ACTIVE SQ_CYCLES SQ_ACTIVE_INST_ANY SQ_INSTS_VMEM_RD SQ_ACTIVE_INST_SCA SQ_INST_LEVEL_VMEM",
+    # the memory path: address (TA) and data (TD) units, vector L1 (TCP)
+    "TA_BUSY_avr TA_BUFFER_TOTAL_CYCLES_sum GRBM_GUI_ACTIVE TD_TD_BUSY_sum TD_TC_STALL_sum "
+    "TCP_PENDING_STALL_CYCLES_sum TCP_TCP_TA_DATA_STALL_CYCLES_sum TCP_TCR_TCP_STALL_CYCLES_sum "
+    "TCP_READ_TAGCONFLICT_STALL_CYCLES_sum",
+    "TCP_TCC_READ_REQ_sum TCP_TCC_READ_REQ_LATENCY_sum TCP_TOTAL_CACHE_ACCESSES_sum TCP_TCP_LATENCY_sum "
+    "TA_ADDR_STALLED_BY_TC_CYCLES_sum TA_DATA_STALLED_BY_TC_CYCLES_sum GRBM_GUI_ACTIVE",
 ]
 COUNTER_CMD = ("timeout -s KILL 120 rocprofv3 --pmc COUNTERS --output-format csv -d DIR/pPASS -o run -- "
                "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-histograms")
 
 
 def summarize_counters(d, workload):
-    """Per-layer SQ counter summary of the network's conv launches (three
-    rocprofv3 --pmc passes under DIR/p1..p3 and the bench JSON DIR/bench.json)
+    """Per-layer counter summary of the network's conv launches (the
+    rocprofv3 --pmc passes of COUNTER_PASSES under DIR/p1, p2, ... and the
+    bench JSON DIR/bench.json): SQ instruction mix and busy fractions, then
+    the memory path (TA, TD, vector L1 and its L2 requests)
     written to profiles/<workload>_sq_counters.md.  Counters are summed over
     the chip per dispatch; per-SIMD figures divide by 4 x CUs (256 CUs)."""
     import csv
@@ -303,6 +311,25 @@ def summarize_counters(d, workload):
                 4 * v.get("SQ_INSTS_VALU", 0) / simds / max(cyc, 1),
                 v.get("SQ_LDS_BANK_CONFLICT", 0) / max(v.get("SQ_ACTIVE_INST_LDS", 1), 1),
                 v.get("SQ_WAIT_INST_LDS", 0) / max(v.get("SQ_WAVES", 1), 1), clock))
+    cus = 256
+    out += ["", "Memory path per dispatch (passes 4 and 5): busy and stall cycles per CU / (GRBM_GUI_ACTIVE / 8 XCDs);",
+            "L2 requests = TCP_TCC_READ_REQ_sum (vector L1 misses sent to the L2), their mean latency in cycles.", "",
+            "| layer | kernel | TA busy | TA buffer cycles/CU | TD busy/CU | TD stalled on TC | TCP pending stall | "
+            "L2 read requests | L2 latency | L1 accesses | L1 latency |",
+            "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for f, Ls in fams.items():
+        for i, L in enumerate(Ls):
+            v = {k: sum(x) / len(x) for k, x in vals.get((f, i), {}).items()}
+            if "TA_BUSY_avr" not in v:
+                continue
+            cyc = max(v.get("GRBM_GUI_ACTIVE", 0) / 8, 1)
+            req = max(v.get("TCP_TCC_READ_REQ_sum", 0), 1)
+            acc = max(v.get("TCP_TOTAL_CACHE_ACCESSES_sum", 0), 1)
+            out.append("| %d | %s | %.2f | %.2f | %.2f | %.2f | %.2f | %.0f | %.0f | %.0f | %.0f |" % (
+                L["layer"], f, v["TA_BUSY_avr"] / cyc, v.get("TA_BUFFER_TOTAL_CYCLES_sum", 0) / cus / cyc,
+                v.get("TD_TD_BUSY_sum", 0) / cus / cyc, v.get("TD_TC_STALL_sum", 0) / cus / cyc,
+                v.get("TCP_PENDING_STALL_CYCLES_sum", 0) / cus / cyc, req,
+                v.get("TCP_TCC_READ_REQ_LATENCY_sum", 0) / req, acc, v.get("TCP_TCP_LATENCY_sum", 0) / acc))
     out += ["", "raw means per dispatch (chip totals):", ""]
     for (f, i), cv in sorted(vals.items()):
         out.append("%s #%d: " % (f, i) + ", ".join("%s=%.0f" % (k, sum(x) / len(x)) for k, x in sorted(cv.items())))
