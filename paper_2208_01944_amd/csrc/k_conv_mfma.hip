@@ -1290,41 +1290,35 @@ __device__ __forceinline__ void tile_next(TileIt &it, int npt, int ncombo, int n
 // (pad 0): a K-block is two filter rows of 8 four-byte taps, 64 bytes per
 // pixel, fetched as four 16-byte pieces (lane half h of the MFMA takes row
 // 2 kb + h, its 8 taps being the two 16-code operand units); no unpack.
-// FP4: 2-bit layers on the FP4 (E2M1) matrix cores, one 32 x 32 x 64 MFMA
-// per K-block and 32-channel block (prepack_fp4_kernel); the activation
-// operand is the packed word split into its even and odd codes (values c / 2),
-// the accumulator fp32 (t / 4, exact: the launcher takes only layers whose
-// accumulator bound is below 2^23, so every partial sum is a multiple of
-// 1/4 below 2^21).
 // DUMP: also write the int32 accumulators to a.acc_dump (destination channel
-// order; the FP4 accumulator times 4, the int8 one without its operand scale).
+// order, without the operand scale).  (2-bit layers on the FP4 matrix cores
+// run on conv_fp4_kernel instead.)
 template <int CB, int PB, int WN, int WM, int RB, bool STEM = false, int kStages = PALQ_TILE_STAGES,
-          bool FP4 = false, bool DUMP = false>
+          bool DUMP = false>
 __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, Geo geo, int npt,
                                                                                       int ncb, int nch) {
   constexpr int B = 2;
   constexpr int NT = WN * WM * 64;
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
   constexpr int BLK = STEM ? 64 : Blk<B>::bytes;  // activation bytes of one pixel's K-block
-  constexpr int SLAB = FP4 ? kSlab4 : kSlab;  // weight bytes of a (K-block, 32 channels)
+  constexpr int SLAB = kSlab;        // weight bytes of a (K-block, 32 channels)
   constexpr int WST = TN / 32 * SLAB;  // weight bytes of one K-block
   constexpr int XST = TM * BLK;       // activation bytes of one K-block
   constexpr int SSB = WST + XST;      // one K-block of a ring stage
   constexpr int SST = SSB;            // one ring stage
   constexpr int WP = WST / 16;        // 16-byte weight pieces of a K-block
-  constexpr int WLD = FP4 && WP < NT ? 1 : WP / NT;  // weight loads per loading thread and K-block
+  constexpr int WLD = WP / NT;       // weight loads per thread and K-block
   constexpr int XP = XST / 16;          // 16-byte activation pieces of a K-block
   constexpr bool XALL = XP >= NT;       // every thread loads (XLD pieces), else the first XP threads one
   constexpr int XLD = XALL ? XP / NT : 1;
-  static_assert(FP4 ? (WP == NT / 2 || WP == NT || WP == 2 * NT) : (WLD == 1 || WLD == 2), "weight loads per thread");
+  static_assert(WLD == 1 || WLD == 2, "weight loads per thread");
   static_assert(XP == NT / 2 || XP % NT == 0, "activation pieces");
   static_assert(!STEM || (XALL && RB == 0), "stem layout");
   static_assert(STEM || XP <= NT, "grouped layers: at most one activation piece (one pixel) per thread");
-  static_assert(!FP4 || !STEM, "FP4 takes 2-bit grouped layers");
-  // loads per K-block of the waves with the fewest (the ring waits on that).
-  // FP4: the last WP threads load one weight piece each (WP < NT), or all
-  // WLD pieces; the first XP threads (or all) the activations.
-  constexpr int LPK = FP4 && WP < NT ? (XALL ? XLD : 1) : WLD + (XALL ? XLD : 0);
+  // loads per K-block of the waves with the fewest (the ring waits on that):
+  // every thread loads WLD weight pieces, the first XP threads (or all) the
+  // activations
+  constexpr int LPK = WLD + (XALL ? XLD : 0);
   constexpr int RQB = 2 * TN * (int)sizeof(RqConst);  // requant constants of two channel blocks
   constexpr int RMB = RB ? 2 * TN * 4 : 0;            // their shortcut multipliers
   constexpr int RPX = TN / 4;                          // shortcut code bytes per pixel of a tile
@@ -1334,7 +1328,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   __shared__ __attribute__((aligned(16))) uint8_t lds[kStages * SST + 2 * RSB];
   __shared__ RqConst rq_area[2 * TN];
   __shared__ int32_t rm_area[RB ? 2 * TN : 1];
-  static_assert(CB == 2 && (PB == 2 || (FP4 && PB == 4)), "compute() below is written out for 2 x 2 (FP4: 2 x 4) blocks");
+  static_assert(CB == 2 && PB == 2, "compute() below is written out for 2 x 2 blocks");
   using Raw = RawT<B, false>;
 
   // the launcher takes 2-bit outputs and 2-bit (or no) shortcuts only; a
@@ -1466,27 +1460,12 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
         }
       }
     }
-    if constexpr (FP4 && WP >= NT) {
 #pragma unroll
-      for (int i = 0; i < WLD; ++i) {
-        const int c = tid + i * NT;  // piece c: slab c / 64, lane operand c % 64
-        const uint32_t woff = live ? wbase + (uint32_t)((c >> 6) * KB + f_kb) * SLAB + (c & 63) * 16 : kOob;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + (c & ~63) * 16), 16, (int)woff, 0, 0, 0);
-      }
-    } else if constexpr (FP4) {
-      if (tid >= NT - WP) {  // wave-uniform: WP is a multiple of 64
-        const int c = tid - (NT - WP);  // piece c: slab c / 64, lane operand c % 64
-        const uint32_t woff = live ? wbase + (uint32_t)((c >> 6) * KB + f_kb) * SLAB + (c & 63) * 16 : kOob;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + (c & ~63) * 16), 16, (int)woff, 0, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < WLD; ++i) {
-        const int c = tid + i * NT;  // piece of the K-block's weights
-        const uint32_t woff = live ? wbase + (uint32_t)((c >> 7) * KB + f_kb) * kSlab + (c & 127) * 16 : kOob;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + i * NT * 16 + wave * 1024), 16, (int)woff, 0, 0,
-                                                 0);
-      }
+    for (int i = 0; i < WLD; ++i) {
+      const int c = tid + i * NT;  // piece of the K-block's weights
+      const uint32_t woff = live ? wbase + (uint32_t)((c >> 7) * KB + f_kb) * kSlab + (c & 127) * 16 : kOob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + i * NT * 16 + wave * 1024), 16, (int)woff, 0, 0,
+                                               0);
     }
     if constexpr (STEM) {
 #pragma unroll
@@ -1524,7 +1503,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   // ---- compute side: tile c_tile, K-block c_kb
   int c_tile = t_begin, c_kb = 0;
   TileIt c_it = tile_at(t_begin, npt, ncb * G, nch);
-  typename std::conditional<FP4, v16f, v16i>::type acc[CB][PB];
+  v16i acc[CB][PB];
   // Per tile, at its first K-block: zeroed accumulators.
   auto tile_start = [&]() __attribute__((always_inline)) {
 #pragma unroll
@@ -1541,11 +1520,11 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
     const int gd = (g + a.shuffle) % G;
     uint32_t rw[CB][PB][2] = {};
     // this lane's shortcut codes: pixel block pb, channel block cb at
-    // ra + pb 32 RPX + 8 cb (the FP4 build reads them per channel block)
+    // ra + pb 32 RPX + 8 cb
     const uint32_t ra = RB == 2 ? lds_base + kStages * SST + ((c_tile - t_begin) & 1) * RSB +
                                       (uint32_t)((wm * PB * 32 + l32) * RPX + wn * CB * 8)
                                 : 0u;
-    if constexpr (RB == 2 && !FP4) {
+    if constexpr (RB == 2) {
       uint2 r00, r01, r10, r11;  // r[pb][cb]
       asm volatile(
           "ds_read_b64 %0, %4\n\t"
@@ -1574,16 +1553,13 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
           for (int qi = 0; qi < 4; ++qi) {
             v4i dv;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              if constexpr (FP4) dv[e] = (int)(acc[cb][pb][4 * qi + e] * 4.0f);  // exact: |4 acc| < 2^23
-              else dv[e] = (int)acc[cb][pb][4 * qi + e] >> (geo.scale == 16 ? 4 : 0);
-            }
+            for (int e = 0; e < 4; ++e) dv[e] = acc[cb][pb][4 * qi + e] >> (geo.scale == 16 ? 4 : 0);
             *(v4i *)(dst + 8 * qi) = dv;
           }
         }
     }
     const int rec = (c_it.combo == combo0 ? 0 : TN) + wn * CB * 32;  // first record of this wave's channels
-    epilogue_fast_bo<2, CB, PB, RB, typename std::remove_reference<decltype(acc[0][0])>::type, FP4>(
+    epilogue_fast_bo<2, CB, PB, RB, v16i>(
         a, geo, acc, rw, (int64_t)pt * TM + wm * PB * 32, g, gd, cbk * TN + wn * CB * 32, l32, half, rq_area + rec,
         rm_area + (RB ? rec : 0), ra, 32 * RPX);
   };
@@ -1597,8 +1573,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   // address register a later read of the statement still uses).
   struct OpsG { uint2 x0, x1; v4i a00, a01, a10, a11; };
   struct OpsS { v4i x0a, x0b, x1a, x1b, a00, a01, a10, a11; };  // stem: x[pb] words 0-3 / 4-7
-  struct OpsF { uint2 x[PB]; v4i a0, a1; };                     // FP4: x[pb], a[cb]
-  using Ops = typename std::conditional<STEM, OpsS, typename std::conditional<FP4, OpsF, OpsG>::type>::type;
+  using Ops = typename std::conditional<STEM, OpsS, OpsG>::type;
   auto read_ops = [&](int stage, Ops &o) __attribute__((always_inline)) {
     const uint32_t xa = xaddr0 + stage * SST, aa = aaddr0 + stage * SST;
     if constexpr (STEM) {
@@ -1614,28 +1589,6 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
           "s_waitcnt lgkmcnt(0)"
           : "=&v"(o.x0a), "=&v"(o.x0b), "=&v"(o.x1a), "=&v"(o.x1b), "=&v"(o.a00), "=&v"(o.a01), "=&v"(o.a10),
             "=&v"(o.a11)
-          : "v"(xa), "v"(aa));
-      return;
-    } else if constexpr (FP4 && PB == 4) {
-      asm volatile(
-          "ds_read_b64 %0, %6\n\t"
-          "ds_read_b64 %1, %6 offset:512\n\t"
-          "ds_read_b64 %2, %6 offset:1024\n\t"
-          "ds_read_b64 %3, %6 offset:1536\n\t"
-          "ds_read_b128 %4, %7\n\t"
-          "ds_read_b128 %5, %7 offset:1024\n\t"
-          "s_waitcnt lgkmcnt(0)"
-          : "=&v"(o.x[0]), "=&v"(o.x[1]), "=&v"(o.x[2]), "=&v"(o.x[3]), "=&v"(o.a0), "=&v"(o.a1)
-          : "v"(xa), "v"(aa));
-      return;
-    } else if constexpr (FP4) {
-      asm volatile(
-          "ds_read_b64 %0, %4\n\t"
-          "ds_read_b64 %1, %4 offset:512\n\t"
-          "ds_read_b128 %2, %5\n\t"
-          "ds_read_b128 %3, %5 offset:1024\n\t"
-          "s_waitcnt lgkmcnt(0)"
-          : "=&v"(o.x[0]), "=&v"(o.x[1]), "=&v"(o.a0), "=&v"(o.a1)
           : "v"(xa), "v"(aa));
       return;
     } else
@@ -1661,27 +1614,6 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
 #pragma unroll
           for (int cb = 0; cb < CB; ++cb)
             acc[cb][pb] = __builtin_amdgcn_mfma_i32_32x32x32_i8(A[j][cb], X[j][pb], acc[cb][pb], 0, 0, 0);
-      return;
-    } else if constexpr (FP4) {
-      // E2M1 operands use the low four registers of each v8i (the rest is
-      // ignored for this format, left undefined here)
-      const uint2 *xw = o.x;
-      const v4i A[CB] = {o.a0, o.a1};
-      v8i Bop[PB], Aop[CB];
-#pragma unroll
-      for (int pb = 0; pb < PB; ++pb) {
-        const uint32_t m = 0x33333333u;
-        const v4i b = {(int)(xw[pb].x & m), (int)((xw[pb].x >> 2) & m), (int)(xw[pb].y & m),
-                       (int)((xw[pb].y >> 2) & m)};
-        Bop[pb] = __builtin_shufflevector(b, b, 0, 1, 2, 3, -1, -1, -1, -1);
-      }
-#pragma unroll
-      for (int cb = 0; cb < CB; ++cb) Aop[cb] = __builtin_shufflevector(A[cb], A[cb], 0, 1, 2, 3, -1, -1, -1, -1);
-#pragma unroll
-      for (int pb = 0; pb < PB; ++pb)
-#pragma unroll
-        for (int cb = 0; cb < CB; ++cb)
-          acc[cb][pb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(Aop[cb], Bop[pb], acc[cb][pb], 4, 4, 0, 0, 0, 0);
       return;
     } else {
     Raw xr[PB];
@@ -3291,7 +3223,7 @@ hipError_t launch_bd_m(const ConvArgs &a, const Geo &geo, int tile, hipStream_t 
   return tile == kTileBdC64 ? launch_bd<M, 1>(a, geo, s) : launch_bd<M, 2>(a, geo, s);
 }
 
-template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES, bool FP4 = false>
+template <int CB, int PB, int WN, int WM, bool STEM = false, int S = PALQ_TILE_STAGES>
 hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   if (geo.kb_total < S) return hipErrorInvalidValue;
   constexpr int TN = WN * CB * 32, TM = WM * PB * 32;
@@ -3299,12 +3231,12 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   const int ncb = a.cout / TN;
   const int64_t T = (int64_t)npt * ncb * a.in.groups;
   if (T <= 0 || T > 0x7fffffff) return hipErrorInvalidValue;
-  const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S, FP4>, WN * WM * 64);
+  const int slots = tile_slots((const void *)conv_tile_kernel<CB, PB, WN, WM, STEM ? 0 : 2, STEM, S>, WN * WM * 64);
   // Pixel chunks (tile_at): 32 (four per XCD), so that an XCD fetches each
   // input line once for all groups while a chunk's lines still fit its L2,
   // unless the filter is the larger read (every XCD then reads all of it):
   // about 7 W extra against (G - 1) X saved.
-  const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * (FP4 ? 32 : 64);
+  const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * 64;
   const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
   const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(32, npt) : 1;
   // P workgroups per XCD: all resident slots, no more than the XCD's
@@ -3317,15 +3249,13 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   if constexpr (STEM)
     hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, true, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else if (!a.res.data && !a.acc_dump)
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, FP4>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else if (!a.acc_dump)
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else if (!a.res.data)
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, FP4, true>), grid, block, 0, s, a, geo, npt, ncb,
-                       nch);
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 0, false, S, true>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else
-    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, FP4, true>), grid, block, 0, s, a, geo, npt, ncb,
-                       nch);
+    hipLaunchKernelGGL((conv_tile_kernel<CB, PB, WN, WM, 2, false, S, true>), grid, block, 0, s, a, geo, npt, ncb, nch);
   return hipGetLastError();
 }
 
