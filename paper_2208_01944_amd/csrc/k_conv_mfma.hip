@@ -2041,17 +2041,29 @@ struct Cfg {
 // fast epilogue; no shortcut.
 // F32 (B = 2): the fp32 requant of requant_prep_f32_kernel; K-block 0's
 // MFMAs start from the channels' bias / 4 instead of zero.
-template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S, int B, bool F32 = false>
+// KS = 2 (B = 2, for layers with few tiles): the workgroup is two groups of
+// WN x WM waves; a ring stage holds two consecutive K-blocks (the same tap:
+// the host takes this build only for an even K-block count per tap and an
+// even projection), group h fetching and multiplying K-block 2 s + h of
+// stage s; at the end group 1 adds its accumulators to group 0's through
+// LDS (the two partial sums are exact, so is their sum) and group 0 runs
+// the epilogue.  Twice the waves per tile, half the K loop each.
+template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S, int B, bool F32 = false, int KS = 1>
 __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo, int npt, int ncb, int nch) {
   using C = f4::Cfg<CB, PB, WN, WM, B>;
-  constexpr int NT = C::NT, TN = C::TN, TM = C::TM, WST = C::WST, SST = C::SST;
+  // NT: the threads of one group; SSB: one K-block of a stage; SST: a stage
+  constexpr int NT = C::NT, TN = C::TN, TM = C::TM, WST = C::WST, SSB = C::SST, SST = KS * SSB;
+  static_assert(KS == 1 || (KS == 2 && B == 2 && PB == 2), "the K split takes FP4 layers with 2 x 2 blocks");
+  // the K split's reduction buffer: group 0's waves x 16 chunks x 64 lanes x 16 bytes, over the ring
+  constexpr int RED = KS == 2 ? (NT / 64) * 16 * 64 * 16 : 0;
+  constexpr int RING = S * SST > RED ? S * SST : RED;
   constexpr int RPT = RB ? C::RSB / (NT * 16) : 0;  // 16-byte shortcut pieces per thread
   static_assert(RB == 0 || RPT * NT * 16 == C::RSB, "whole shortcut pieces per thread");
   static_assert(CB == 2 && (PB == 2 || PB == 4), "operand reads are written for 2 x 2 and 2 x 4 blocks");
   static_assert(B == 2 || (B == 3 && PB == 2 && RB == 0), "FP6: 2 x 2 blocks, no shortcut");
   static_assert(!F32 || B == 2, "the fp32 requant takes FP4 accumulators");
   constexpr int XB = B == 2 ? 16 : 24;  // activation bytes of a pixel's K-block
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[S * SST + (RB ? C::RSB : 16)];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[RING + (RB ? C::RSB : 16)];
   __shared__ RqConst rq_area[TN];
   __shared__ int32_t rm_area[RB ? TN : 1];
 
@@ -2068,7 +2080,9 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   const TileIt it = tile_at(t, npt, ncb * G, nch);
   const int pt = it.pt, cbk = it.combo % ncb, g = it.combo / ncb;
   const int gd = (g + a.shuffle) % G;
-  const int tid = threadIdx.x, lane = tid & 63;
+  // tid, wave: within the thread's group kh (KS = 2: of the two)
+  const int kh = KS == 2 ? uniform_int((int)threadIdx.x / NT) : 0;
+  const int tid = (int)threadIdx.x - kh * NT, lane = tid & 63;
   const int wave = uniform_int(tid >> 6);  // LDS destinations in scalar registers
   const int l32 = lane & 31, half = lane >> 5;
   const int wn = wave / WM, wm = wave % WM;
@@ -2078,7 +2092,7 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   // F32: the fp32 scales, then bias / 4, in rq_area's bytes
   const int64_t ch0 = (int64_t)g * a.cout + cbk * TN;
   float *const sc_area = (float *)rq_area, *const b4_area = sc_area + TN;
-  for (int c = tid; c < TN; c += NT) {
+  for (int c = (int)threadIdx.x; c < TN; c += NT * KS) {
     if constexpr (F32) {
       const int64_t nall = (int64_t)G * a.cout;
       const float *f32c = (const float *)(geo.rq + nall + 1);
@@ -2150,9 +2164,9 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   };
   tap_offsets();
   auto fetch = [&](int st) __attribute__((always_inline)) {
-    uint8_t *ws = lds + st * SST;
+    uint8_t *ws = lds + st * SST + kh * SSB;  // this group's K-block f_kb + kh of the stage
     if constexpr (RB == 2) {
-      if (f_kb == 0) {  // the tile's shortcut codes, RPT pieces per thread (before K-block 0's loads)
+      if (f_kb == 0 && kh == 0) {  // the tile's shortcut codes, RPT pieces per thread (before K-block 0's loads)
 #pragma unroll
         for (int i = 0; i < RPT; ++i) {
           const int c = tid + i * NT;
@@ -2160,7 +2174,7 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
           const uint32_t ro = m < geo.M ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.row + cbk * C::RPX +
                                                      (c % (C::RPX / 16)) * 16)
                                         : kOob;
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(lds + S * SST + i * NT * 16 + wave * 1024), 16,
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(lds + RING + i * NT * 16 + wave * 1024), 16,
                                                    (int)ro, 0, 0, 0);
         }
       }
@@ -2169,22 +2183,23 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
     for (int i = 0; i < C::WL; ++i)
       if (C::wloads(wave, i))
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rw_src, (lds_ptr)(ws + ((wc + i * NT) & ~63) * 16), 16, (int)woff[i],
-                                                 f_kb * C::SLAB, 0, 0);
+                                                 (f_kb + kh) * C::SLAB, 0, 0);
     if (f_kb < KM) {
 #pragma unroll
       for (int i = 0; i < C::XL; ++i)
         if (C::xloads(wave, i))
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rin, (lds_ptr)(ws + WST + i * NT * 16 + wave * 1024), 16, (int)vo[i],
-                                                   f_c * XB, 0, 0);
+                                                   (f_c + kh) * XB, 0, 0);
     } else {
 #pragma unroll
       for (int i = 0; i < C::XL; ++i)
         if (C::xloads(wave, i))
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rpj, (lds_ptr)(ws + WST + i * NT * 16 + wave * 1024), 16,
-                                                   (int)poff[i], (f_kb - KM) * 16, 0, 0);
+                                                   (int)poff[i], (f_kb + kh - KM) * 16, 0, 0);
     }
-    ++f_kb;
-    if (++f_c == geo.cpb) {  // next tap
+    f_kb += KS;
+    f_c += KS;
+    if (f_c == geo.cpb) {  // next tap
       f_c = 0;
       ++f_tap;
       f_tapoff += pixb;
@@ -2205,10 +2220,12 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   // (blocks 1 KB apart)
   // (B = 3: chunk half of pixel block 0 at 1 KB blocks, the weight unit's
   // first 16 bytes and its last 8 bytes, slabs 1536 bytes apart)
-  const uint32_t xaddr0 = lds_base + WST +
+  // (KS = 2: in this group's half of the stage)
+  const uint32_t gbase = lds_base + (uint32_t)(kh * SSB);
+  const uint32_t xaddr0 = gbase + WST +
                           (uint32_t)(B == 2 ? (wm * PB * 32 + l32) * 16 + half * 8 : ((wm * PB) * 64 + lane) * 16);
-  const uint32_t aaddr0 = lds_base + (uint32_t)((wn * CB) * C::SLAB + lane * 16);
-  const uint32_t baddr0 = lds_base + (uint32_t)((wn * CB) * C::SLAB + 1024 + lane * 8);
+  const uint32_t aaddr0 = gbase + (uint32_t)((wn * CB) * C::SLAB + lane * 16);
+  const uint32_t baddr0 = gbase + (uint32_t)((wn * CB) * C::SLAB + 1024 + lane * 8);
   auto kblock = [&](int st, bool first) __attribute__((always_inline)) {
     const uint32_t xa = xaddr0 + st * SST, aa = aaddr0 + st * SST;
     if constexpr (B == 3) {
@@ -2289,9 +2306,10 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
     else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   };
   __syncthreads();  // the tile's constants are in LDS
+  const int NS = KB / KS;  // ring stages (the host takes KS = 2 only for an even KB)
 #pragma unroll
   for (int st = 0; st < S - 1; ++st)
-    if (st < KB) fetch(st);
+    if (st < NS) fetch(st);
   if constexpr (F32) {
     // element r of block cb is channel 32 cb + 8 (r / 4) + 4 half + r % 4
     // of the wave's channels
@@ -2301,19 +2319,19 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
       for (int qi = 0; qi < 4; ++qi) {
         const v4f b = *(const v4f *)(b4_area + wn * CB * 32 + cb * 32 + 8 * qi + 4 * half);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) c0[cb][4 * qi + e] = b[e];
+        for (int e = 0; e < 4; ++e) c0[cb][4 * qi + e] = kh == 0 ? b[e] : 0.0f;  // the bias once
       }
   }
-  // K-block 0 (KB >= 1)
-  const bool steady0 = KB > S - 1;
-  wait_younger(steady0 ? S - 2 : KB - 1);
+  // stage 0 (NS >= 1)
+  const bool steady0 = NS > S - 1;
+  wait_younger(steady0 ? S - 2 : NS - 1);
   ring_barrier();
   if (steady0) fetch(S - 1);
   kblock(0, true);
   // steady state: K-block kb's loads were issued S - 1 fetches ago; at most
   // (S - 2) LPK of this wave's loads are younger
   int kb = 1;
-  for (; kb + S - 1 < KB; ++kb) {
+  for (; kb + S - 1 < NS; ++kb) {
     __builtin_amdgcn_s_waitcnt(waitcnt_vm((S - 2) * C::LPK));
     ring_barrier();
     fetch((kb + S - 1) % S);
@@ -2322,11 +2340,44 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   // the last S - 1 K-blocks: no more fetches, the waits tighten
 #pragma unroll
   for (int i = 0; i < S - 1; ++i) {
-    if (kb >= KB) break;  // uniform
-    wait_younger(KB - 1 - kb);
+    if (kb >= NS) break;  // uniform
+    wait_younger(NS - 1 - kb);
     ring_barrier();
     kblock(kb % S, false);
     ++kb;
+  }
+
+  if constexpr (KS == 2) {
+    // group 1's accumulators into group 0's: chunk c (4 values) of wave w at
+    // ((w 16 + c) 64 + lane) 16 bytes, over the ring, which every wave has
+    // finished reading at the first barrier
+    __syncthreads();
+    float *red = (float *)lds;
+    if (kh == 1) {
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int c = (cb * PB + pb) * 4 + q;
+            *(v4f *)(red + ((wave * 16 + c) * 64 + lane) * 4) =
+                v4f{acc[cb][pb][4 * q], acc[cb][pb][4 * q + 1], acc[cb][pb][4 * q + 2], acc[cb][pb][4 * q + 3]};
+          }
+    }
+    __syncthreads();
+    if (kh == 1) return;
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = (cb * PB + pb) * 4 + q;
+          const v4f r = *(const v4f *)(red + ((wave * 16 + c) * 64 + lane) * 4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[cb][pb][4 * q + e] += r[e];  // exact (multiples of 1/4 below 2^22)
+        }
   }
 
   // ---- epilogue
@@ -2355,16 +2406,16 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   }
   // this lane's shortcut codes: pixel block pb, channel block cb at
   // ra + pb 32 RPX + 8 cb (read per channel block by the epilogue)
-  const uint32_t ra = RB == 2 ? lds_base + S * SST + (uint32_t)((wm * PB * 32 + l32) * C::RPX + wn * CB * 8) : 0u;
+  const uint32_t ra = RB == 2 ? lds_base + RING + (uint32_t)((wm * PB * 32 + l32) * C::RPX + wn * CB * 8) : 0u;
   uint32_t rw[CB][PB][2] = {};
   epilogue_fast_bo<B, CB, PB, RB, v16f, true, F32>(a, geo, acc, rw, mbase, g, gd, cbk * TN + wn * CB * 32, l32, half,
                                                      rq_area + wn * CB * 32, rm_area + (RB ? wn * CB * 32 : 0), ra,
                                                      32 * C::RPX, sc_area + wn * CB * 32);
 }
 
-template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S, bool F32>
-__global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp4_kernel(ConvArgs a, Geo geo, int npt, int ncb, int nch) {
-  conv_fpx_tile<CB, PB, WN, WM, RB, DUMP, S, 2, F32>(a, geo, npt, ncb, nch);
+template <int CB, int PB, int WN, int WM, int RB, bool DUMP, int S, bool F32, int KS = 1>
+__global__ __launch_bounds__(WN * WM * 64 * KS, 2) void conv_fp4_kernel(ConvArgs a, Geo geo, int npt, int ncb, int nch) {
+  conv_fpx_tile<CB, PB, WN, WM, RB, DUMP, S, 2, F32, KS>(a, geo, npt, ncb, nch);
 }
 template <int CB, int PB, int WN, int WM, bool DUMP, int S>
 __global__ __launch_bounds__(WN * WM * 64, 2) void conv_fp6_kernel(ConvArgs a, Geo geo, int npt, int ncb, int nch) {
@@ -3101,8 +3152,8 @@ size_t stem_rows_offset(const ConvArgs &a) { return (size_t)a.in.groups * a.cout
 // 128-channel blocks (2 x 2 waves, 128 pixels).
 // Wide layers as the Eq. 4 decomposition with 64- or 128-channel tiles.
 enum TileBuild {
-  kTileNone = 0, kTileStem, kTileFp4C64, kTileFp4C128, kTileFp4C128P4, kTileFp6C64, kTileFp6C128, kTileI8C64,
-  kTileI8C128, kTileBdC64, kTileBdC128
+  kTileNone = 0, kTileStem, kTileFp4C64, kTileFp4C128, kTileFp4C128P4, kTileFp4C128K2, kTileFp6C64, kTileFp6C128,
+  kTileI8C64, kTileI8C128, kTileBdC64, kTileBdC128
 };
 
 // 2 x 4 blocks per wave (256-pixel tiles) for 128-channel FP4 layers where
@@ -3113,6 +3164,16 @@ bool fp4_pb4_pays(const ConvArgs &a, const Geo &geo) {
   const int64_t t2 = (m + 127) / 128 * tiles_per_px, t4 = (m + 255) / 256 * tiles_per_px;
   const int64_t cus = cu_count();
   return t4 >= cus && 2 * ((t4 + cus - 1) / cus) <= (t2 + cus - 1) / cus;
+}
+
+// The in-workgroup K split (conv_fpx_tile, KS = 2) for 128-channel FP4
+// layers with fewer 128 x 128 tiles than twice the CUs (the deep layers,
+// whose tiles leave most SIMDs with one wave): an even number of K-blocks
+// per tap, an even projection and at least 8 K-blocks.
+bool fp4_ksplit_pays(const ConvArgs &a, const Geo &geo) {
+  const int64_t t2 = (geo.M + 127) / 128 * (a.cout / 128) * a.in.groups;
+  const int pk = geo.kb_total - geo.kb_main;
+  return geo.cpb % 2 == 0 && pk % 2 == 0 && geo.kb_total >= 8 && t2 < 2 * (int64_t)cu_count();
 }
 
 // The one selection rule of the conv launches: which tiled build (if any)
@@ -3137,7 +3198,11 @@ ConvChoice conv_choice(const ConvArgs &a, const Geo &geo, int epi) {
   }
   if (a.out.bits == 3) return c;
   if (stem_tile_applies(a)) c.tile = kTileStem;
-  else if (fp4_applies(a)) c.tile = a.cout % 128 ? kTileFp4C64 : fp4_pb4_pays(a, geo) ? kTileFp4C128P4 : kTileFp4C128;
+  else if (fp4_applies(a))
+    c.tile = a.cout % 128             ? kTileFp4C64
+             : fp4_pb4_pays(a, geo)    ? kTileFp4C128P4
+             : fp4_ksplit_pays(a, geo) ? kTileFp4C128K2
+                                       : kTileFp4C128;
   else if (tile_kernel_applies(a)) c.tile = a.cout % 128 ? kTileI8C64 : kTileI8C128;
   return c;
 }
@@ -3145,7 +3210,7 @@ ConvChoice conv_choice(const ConvArgs &a, const Geo &geo, int epi) {
 // The FP4 grouped kernel: one workgroup per tile, XCD-contiguous runs of the
 // chunked tile order (32 chunks where the packed input outweighs the filter,
 // as in launch_tile).
-template <int B, int CB, int PB, int WN, int WM>
+template <int B, int CB, int PB, int WN, int WM, int KS = 1>
 hipError_t launch_fpx(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   constexpr int S = 4;
   using C = f4::Cfg<CB, PB, WN, WM, B>;
@@ -3156,7 +3221,8 @@ hipError_t launch_fpx(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * (C::SLAB / 32);
   const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
   const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(32, npt) : 1;
-  const dim3 grid((unsigned)((T + 7) / 8 * 8)), block(C::NT);
+  if (KS == 2 && (geo.kb_total % 2 != 0 || geo.cpb % 2 != 0)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)((T + 7) / 8 * 8)), block(C::NT * KS);
   if constexpr (B == 3) {
     if (a.res.data || a.proj.data) return hipErrorNotSupported;
     if (!a.acc_dump)
@@ -3168,23 +3234,23 @@ hipError_t launch_fpx(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   // the fp32 requant where the plan found it exact for every channel
   if (a.f32ep) {
     if (!a.res.data && !a.acc_dump)
-      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, false, S, true>), grid, block, 0, s, a, geo, npt, ncb, nch);
+      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, false, S, true, KS>), grid, block, 0, s, a, geo, npt, ncb, nch);
     else if (!a.acc_dump)
-      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, false, S, true>), grid, block, 0, s, a, geo, npt, ncb, nch);
+      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, false, S, true, KS>), grid, block, 0, s, a, geo, npt, ncb, nch);
     else if (!a.res.data)
-      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, true, S, true>), grid, block, 0, s, a, geo, npt, ncb, nch);
+      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, true, S, true, KS>), grid, block, 0, s, a, geo, npt, ncb, nch);
     else
-      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, true, S, true>), grid, block, 0, s, a, geo, npt, ncb, nch);
+      hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, true, S, true, KS>), grid, block, 0, s, a, geo, npt, ncb, nch);
     return hipGetLastError();
   }
   if (!a.res.data && !a.acc_dump)
-    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, false, S, false>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, false, S, false, KS>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else if (!a.acc_dump)
-    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, false, S, false>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, false, S, false, KS>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else if (!a.res.data)
-    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, true, S, false>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 0, true, S, false, KS>), grid, block, 0, s, a, geo, npt, ncb, nch);
   else
-    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, true, S, false>), grid, block, 0, s, a, geo, npt, ncb, nch);
+    hipLaunchKernelGGL((conv_fp4_kernel<CB, PB, WN, WM, 2, true, S, false, KS>), grid, block, 0, s, a, geo, npt, ncb, nch);
   return hipGetLastError();
 }
 
@@ -3301,7 +3367,7 @@ const char *conv_kernel_label(const ConvArgs &a, int epi) {
   const Geo geo = make_geo(a);
   switch (conv_choice(a, geo, epi).tile) {
     case kTileStem: return "conv_tile_kernel[stem]";
-    case kTileFp4C64: case kTileFp4C128: case kTileFp4C128P4: return "conv_fp4_kernel";
+    case kTileFp4C64: case kTileFp4C128: case kTileFp4C128P4: case kTileFp4C128K2: return "conv_fp4_kernel";
     case kTileFp6C64: case kTileFp6C128: return "conv_fp6_kernel";
     case kTileBdC64: case kTileBdC128: return "conv_bitdecomp_kernel";
     case kTileI8C64: case kTileI8C128: return "conv_tile_kernel[int8]";
@@ -3330,6 +3396,7 @@ hipError_t launch_conv_mfma(const ConvArgs &a_in, const uint8_t *wp, const int32
     case kTileFp4C64: e = launch_fpx<2, 2, 2, 1, 4>(a, g4, s); break;
     case kTileFp4C128: e = launch_fpx<2, 2, 2, 2, 2>(a, g4, s); break;
     case kTileFp4C128P4: e = launch_fpx<2, 2, 4, 2, 2>(a, g4, s); break;
+    case kTileFp4C128K2: e = launch_fpx<2, 2, 2, 2, 2, 2>(a, g4, s); break;
     case kTileFp6C64: e = launch_fpx<3, 2, 2, 1, 4>(a, g4, s); break;
     case kTileBdC64: case kTileBdC128: {
       Geo gb = g4;
