@@ -635,14 +635,35 @@ __global__ __launch_bounds__(256) void fc_mfma_kernel(const int8_t *w, const int
   const int steps = cin / 32;
   const int per = (steps + gridDim.z - 1) / gridDim.z;
   const int k_end = 32 * min(steps, per * (int)(blockIdx.z + 1));
-  for (int k = 32 * (per * (int)blockIdx.z + wave); k < k_end; k += 128) {
-    const v4i_t a = __builtin_bit_cast(v4i_t, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(wrow + k), 0, 0));
+  // the wave's K steps k, k + 128, ...: the operands of U steps are loaded
+  // before their MFMAs, so that U loads are in flight at once
+  constexpr int U = 4;
+  auto wload = [&](int k) __attribute__((always_inline)) {
+    return __builtin_bit_cast(v4i_t, __builtin_amdgcn_raw_buffer_load_b128(rw, (int)(wrow + k), 0, 0));
+  };
+  auto dload = [&](int k, int p) __attribute__((always_inline)) {
+    const uint32_t off = drow == kOut ? kOut : drow + (uint32_t)(p * plane) + k;
+    return __builtin_bit_cast(v4i_t, __builtin_amdgcn_raw_buffer_load_b128(rd, (int)off, 0, 0));
+  };
+  int k = 32 * (per * (int)blockIdx.z + wave);
+  for (; k + 128 * (U - 1) < k_end; k += 128 * U) {
+    v4i_t a[U], b[U][P];
 #pragma unroll
-    for (int p = 0; p < P; ++p) {
-      const uint32_t off = drow == kOut ? kOut : drow + (uint32_t)(p * plane) + k;
-      const v4i_t b = __builtin_bit_cast(v4i_t, __builtin_amdgcn_raw_buffer_load_b128(rd, (int)off, 0, 0));
-      acc[p] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, acc[p], 0, 0, 0);
+    for (int u = 0; u < U; ++u) {
+      a[u] = wload(k + 128 * u);
+#pragma unroll
+      for (int p = 0; p < P; ++p) b[u][p] = dload(k + 128 * u, p);
     }
+    __builtin_amdgcn_sched_barrier(0);  // every load issued before the first wait
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int p = 0; p < P; ++p) acc[p] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[u], b[u][p], acc[p], 0, 0, 0);
+  }
+  for (; k < k_end; k += 128) {
+    const v4i_t a = wload(k);
+#pragma unroll
+    for (int p = 0; p < P; ++p) acc[p] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, dload(k, p), acc[p], 0, 0, 0);
   }
   uint32_t tot[16];
 #pragma unroll
