@@ -245,11 +245,12 @@ __global__ void requant_prep_kernel(const int32_t *mult, const int32_t *shift, c
 // x stays at least 2^-sh <= 2^-22 under k, more than half the fp32 spacing
 // there (2^-23): RN(x) < k whenever x < k, and RN(x) >= floor(x) always.
 // Hence min(trunc(y), 3) (v_cvt_u32_f32 truncates and takes negative values
-// to 0) equals clamp(floor(x), 0, 3), the definition, for sh <= 22.  flag:
-// 1 when every channel meets the bounds (else the fp64 epilogue runs).
+// to 0) equals clamp(floor(x), 0, 3), the definition, for sh <= 22.  rm4:
+// the shortcut scale res_mult / 4 (exact, |res_mult| < 2^15).  flag: 1 when
+// every channel meets the bounds (else the fp64 epilogue runs).
 __global__ void requant_prep_f32_kernel(const int32_t *mult, const int32_t *shift, const int32_t *bias,
                                         const int32_t *res_mult, int res_max, int nch, int64_t acc_bound, float *sc,
-                                        float *b4, int32_t *flag) {
+                                        float *b4, float *rm4, int32_t *flag) {
   __shared__ int any_bad;
   if (threadIdx.x == 0) any_bad = 0;
   __syncthreads();
@@ -264,6 +265,7 @@ __global__ void requant_prep_f32_kernel(const int32_t *mult, const int32_t *shif
     if (sh < 1 || sh > 22 || m <= -lim || m >= lim || umax >= lim) bad = 1;
     sc[c] = bad ? 0.0f : ldexpf((float)m, 2 - sh);
     b4[c] = bad ? 0.0f : (float)b * 0.25f;
+    rm4[c] = bad ? 0.0f : (float)rm * 0.25f;
   }
   if (bad) atomicOr(&any_bad, 1);
   __syncthreads();
@@ -660,7 +662,8 @@ typedef double dbl2 __attribute__((ext_vector_type(2)));
 // F32 (FP4 accumulator, 2-bit outputs): the accumulator already holds
 // (t + bias) / 4 and scf[c] is the channel's fp32 scale M 2^(2 - sh); the
 // requant is min(trunc(fma(v, scf, 1/2)), 3), exact under the bounds
-// requant_prep_f32_kernel checks (rq is then unused).
+// requant_prep_f32_kernel checks (rq is then unused); rm holds the shortcut
+// scales res_mult / 4 as fp32 bits.
 template <int BO, int CB, int PB, int RB, typename AccV, bool LAZY = false, bool F32 = false>
 __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &geo, AccV (&acc)[CB][PB],
                                         const uint32_t (&rw)[CB][PB][2], int64_t mbase, int g, int gd, int ch0,
@@ -747,9 +750,15 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[cb][pb][4 * qi + e];
         if constexpr (RB == 2 && FACC) {
+          // F32: rm holds res_mult / 4 as fp32 bits (each element copied to
+          // a scalar first: a bit cast of a vector element would read the
+          // vector's first element)
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            v[e] = __builtin_fmaf((float)rmu[e] * 0.25f, (float)chunk_code(rwc[pb], cq + e, 2), v[e]);
+          for (int e = 0; e < 4; ++e) {
+            const int32_t ri = rmu[e];
+            v[e] = __builtin_fmaf(F32 ? __builtin_bit_cast(float, ri) : (float)ri * 0.25f,
+                                  (float)chunk_code(rwc[pb], cq + e, 2), v[e]);
+          }
         } else if constexpr (RB == 2) {
           // |res_mult| < 2^15 and codes < 4: 24-bit signed products
 #pragma unroll
@@ -2089,7 +2098,8 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   const int KB = geo.kb_total, KM = geo.kb_main;
 
   // requant constants (and shortcut multipliers) of the tile's TN channels;
-  // F32: the fp32 scales, then bias / 4, in rq_area's bytes
+  // F32: the fp32 scales, then bias / 4, in rq_area's bytes, and the
+  // shortcut scales res_mult / 4 as fp32 bits in rm_area
   const int64_t ch0 = (int64_t)g * a.cout + cbk * TN;
   float *const sc_area = (float *)rq_area, *const b4_area = sc_area + TN;
   for (int c = (int)threadIdx.x; c < TN; c += NT * KS) {
@@ -2098,10 +2108,11 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
       const float *f32c = (const float *)(geo.rq + nall + 1);
       sc_area[c] = f32c[ch0 + c];
       b4_area[c] = f32c[nall + ch0 + c];
+      if constexpr (RB != 0) rm_area[c] = __builtin_bit_cast(int32_t, f32c[2 * nall + ch0 + c]);
     } else {
       rq_area[c] = geo.rq[ch0 + c];
+      if constexpr (RB != 0) rm_area[c] = a.res_mult[ch0 + c];
     }
-    if constexpr (RB != 0) rm_area[c] = a.res_mult[ch0 + c];
   }
   typedef __attribute__((address_space(3))) void *lds_ptr;
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
@@ -2930,7 +2941,7 @@ ConvPlan conv_mfma_plan(const ConvArgs &a) {
   if (fp4_applies(a)) {  // FP4 slabs and constants after the int8 ones (the general build keeps those)
     p.w_bytes += (size_t)a.in.groups * a.cout * geo.kb_total * 32;
     p.thr_bytes *= 2;
-    p.thr_bytes += (size_t)a.in.groups * a.cout * 8 + 16;  // fp32 scale and bias / 4, flag
+    p.thr_bytes += (size_t)a.in.groups * a.cout * 12 + 16;  // fp32 scale, bias / 4, res_mult / 4, flag
   }
   return p;
 }
@@ -2996,8 +3007,8 @@ hipError_t launch_conv_prepare(const ConvArgs &a, uint8_t *wp, int32_t *thr, hip
                      res_max, nch, -2, acc_bound, rq4, (int32_t *)(rq4 + nch));
   float *f32c = (float *)(rq4 + nch + 1);
   hipLaunchKernelGGL(requant_prep_f32_kernel, dim3(1), dim3(256), 0, s, a.mult, a.shift, a.bias,
-                     a.res.data ? a.res_mult : nullptr, res_max, nch, acc_bound, f32c, f32c + nch,
-                     (int32_t *)(f32c + 2 * nch));
+                     a.res.data ? a.res_mult : nullptr, res_max, nch, acc_bound, f32c, f32c + nch, f32c + 2 * nch,
+                     (int32_t *)(f32c + 3 * nch));
   return hipGetLastError();
 }
 
@@ -3008,7 +3019,7 @@ bool conv_mfma_f32(const ConvArgs &a, const int32_t *thr) {
   const int64_t nch = (int64_t)a.in.groups * a.cout;
   const float *f32c = (const float *)((const RqConst *)thr + 2 * (nch + 1));
   int32_t ok = 0;
-  if (hipMemcpy(&ok, f32c + 2 * nch, sizeof(ok), hipMemcpyDeviceToHost) != hipSuccess) return false;
+  if (hipMemcpy(&ok, f32c + 3 * nch, sizeof(ok), hipMemcpyDeviceToHost) != hipSuccess) return false;
   return ok == 1;
 }
 
