@@ -38,7 +38,8 @@ def parse():
     ap.add_argument("--batch", type=int, default=64, help="batch of the --table2 networks")
     ap.add_argument("--workload", default="resnet18_g4_b2",
                     help="resnet18_g4_b2 (the default: ResNet-18 G=4 2-bit, batch 64), "
-                         "resnet50_g2_b2 (ResNet-50 G=2 2-bit, batch 128), or single layers: c1, c2 "
+                         "resnet18_g4_b2_shuffles (the same with cyclic shuffle modules and channel "
+                         "shuffles), resnet50_g2_b2 (ResNet-50 G=2 2-bit, batch 128), or single layers: c1, c2 "
                          "(its four layers c2_l0..c2_l3), c4 (its nine cells c4_g<G>_b<B>) or "
                          "layers (all of them); one JSON line per network or layer")
     ap.add_argument("--no-histograms", action="store_true",
@@ -456,6 +457,9 @@ def cpu_baseline(spec, x_f32, l, u, budget_s):
 NETWORKS = {
     # workload name -> (config name in the JSON line, metric)
     "resnet18_g4_b2": ("resnet18_palq_G4_b2_224_fwd_centred", METRIC),
+    "resnet18_g4_b2_shuffles": ("resnet18_palq_G4_b2_224_fwd_centred_with_shuffle_modules_and_channel_shuffles",
+                                "effective int TOPS + images/s, ResNet-18-shaped G=4 2-bit fwd with cyclic "
+                                "shuffle modules and channel shuffles, batch 64"),
     "resnet50_g2_b2": ("resnet50_palq_G2_b2_224_fwd_centred",
                        "effective int TOPS + images/s, ResNet-50-shaped G=2 2-bit fwd, batch 128"),
 }
@@ -509,6 +513,18 @@ def network_algorithmic(spec, n):
                 r = shapes[L["proj_src"]]
                 nbytes += act_bytes(r[0], r[1], r[2], r[3]) + L["proj_w"].size * L["w_bits"] / 8
             out.append(dict(ops=ops, bytes=nbytes))
+        elif L["op"] == "shuffle_module":
+            # 1x1 group conv on the cyclically permuted input plus the
+            # unpermuted shortcut (Eq. 9-10): the input is read once
+            g, co, _, _, ci = L["w"].shape
+            ops = 2 * n * s[0] * s[1] * g * co * ci
+            shapes[L["dst"]] = (s[0], s[1], g * co, L["out_bits"])
+            nbytes = act_bytes(s[0], s[1], s[2], s[3]) + g * co * ci * L["w_bits"] / 8 \
+                + act_bytes(s[0], s[1], g * co, L["out_bits"]) + 4 * 4 * g * co
+            out.append(dict(ops=ops, bytes=nbytes))
+        elif L["op"] == "channel_shuffle":
+            shapes[L["dst"]] = s
+            out.append(dict(bytes=2 * act_bytes(s[0], s[1], s[2], s[3])))
         else:
             if L["op"] == "maxpool":
                 ho = (s[0] + 2 * L["pad"] - L["k"]) // L["stride"] + 1

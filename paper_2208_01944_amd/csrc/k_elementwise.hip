@@ -296,6 +296,44 @@ __global__ void channel_shuffle_kernel(ActView in, ActView out, int64_t pixels, 
   for (int wi = 0; wi < nw; ++wi) dst[wi] = words[wi];
 }
 
+// Unpadded rows of b in {2, 4, 8} with G a power of two up to 16: the
+// output's flat code o = 4F t + f (F codes per word, thread t) takes code
+// (4F t + f) / G of group f mod G, so each group hands a thread one aligned
+// run of 128 / G bits and the G runs interleave field by field into four
+// whole output words, written with one 16-byte store.
+template <int B, int G>
+__global__ void channel_shuffle_words_kernel(ActView in, ActView out, int64_t threads, int tpp) {
+  constexpr int F = 32 / B;      // codes per word
+  constexpr int GB = 128 / G;    // bits each group hands a thread
+  constexpr int NW = GB >= 32 ? GB / 32 : 1;
+  constexpr uint32_t mask = (1u << B) - 1u;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= threads) return;
+  const int64_t p = t / tpp;
+  const int tl = (int)(t - p * tpp);
+  const uint8_t *src = in.data + p * in.pixel;
+  uint32_t s[G][NW];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const uint32_t *r = (const uint32_t *)(src + (int64_t)g * in.row);
+    if constexpr (GB >= 32) {
+#pragma unroll
+      for (int j = 0; j < NW; ++j) s[g][j] = r[tl * NW + j];
+    } else {
+      constexpr int PER = 32 / GB;
+      s[g][0] = r[tl / PER] >> ((tl % PER) * GB);
+    }
+  }
+  uint32_t o[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int f = 0; f < 4 * F; ++f) {
+    const int g = f % G, i = f / G;
+    const uint32_t v = (s[g][(i * B) / 32] >> ((i * B) % 32)) & mask;
+    o[f / F] |= v << ((f % F) * B);
+  }
+  *(uint4 *)(out.data + 16 * t) = make_uint4(o[0], o[1], o[2], o[3]);
+}
+
 // ------------------------------------------------------------ max pool
 // Field-wise max of sixteen 2-bit unsigned fields packed in a word.
 __device__ inline uint32_t max2x16(uint32_t a, uint32_t b) {
@@ -785,8 +823,44 @@ hipError_t launch_shuffle(const ActView &in, int32_t steps, const ActView &out, 
   return hipGetLastError();
 }
 
+// The word-level build: b in {2, 4, 8}, rows without padding (C a multiple
+// of the codes per word), a pixel a whole number of 16-byte stores, G a
+// power of two up to 16 and both tensors 16-byte aligned.
+static bool channel_shuffle_words(const ActView &in, const ActView &out) {
+  const int b = in.bits, G = in.groups;
+  if (b != 2 && b != 4 && b != 8) return false;
+  if (G != 2 && G != 4 && G != 8 && G != 16) return false;
+  const int F = 32 / b;
+  return in.cpg % F == 0 && ((int64_t)G * in.cpg) % (4 * F) == 0 && out.pixel == in.pixel &&
+         (((uintptr_t)in.data | (uintptr_t)out.data) & 15u) == 0 &&
+         (int64_t)G * in.cpg / (4 * F) < ((int64_t)1 << 30);
+}
+
+const char *channel_shuffle_label(const ActView &in, const ActView &out) {
+  return channel_shuffle_words(in, out) ? "channel_shuffle_words_kernel" : "channel_shuffle_kernel";
+}
+
+template <int B>
+static hipError_t launch_channel_shuffle_words(const ActView &in, const ActView &out, int64_t threads, int tpp,
+                                        hipStream_t s) {
+  switch (in.groups) {
+    case 2: hipLaunchKernelGGL((channel_shuffle_words_kernel<B, 2>), dim3(grid_for(threads)), dim3(kBlock), 0, s, in, out, threads, tpp); break;
+    case 4: hipLaunchKernelGGL((channel_shuffle_words_kernel<B, 4>), dim3(grid_for(threads)), dim3(kBlock), 0, s, in, out, threads, tpp); break;
+    case 8: hipLaunchKernelGGL((channel_shuffle_words_kernel<B, 8>), dim3(grid_for(threads)), dim3(kBlock), 0, s, in, out, threads, tpp); break;
+    default: hipLaunchKernelGGL((channel_shuffle_words_kernel<B, 16>), dim3(grid_for(threads)), dim3(kBlock), 0, s, in, out, threads, tpp); break;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_channel_shuffle(const ActView &in, const ActView &out, hipStream_t s) {
   const int64_t pixels = (int64_t)in.n * in.h * in.w;
+  if (pixels > 0 && channel_shuffle_words(in, out)) {
+    const int tpp = (int)(in.pixel / 16);
+    const int64_t threads = pixels * tpp;
+    if (in.bits == 2) return launch_channel_shuffle_words<2>(in, out, threads, tpp, s);
+    if (in.bits == 4) return launch_channel_shuffle_words<4>(in, out, threads, tpp, s);
+    return launch_channel_shuffle_words<8>(in, out, threads, tpp, s);
+  }
   const int chunks = (in.cpg + 31) / 32;
   const int64_t items = pixels * in.groups * chunks;
   if (items == 0) return hipSuccess;

@@ -134,6 +134,7 @@ hipError_t launch_quantize(const float *x, float l, float u, const float *range,
                            hipStream_t s);
 hipError_t launch_shuffle(const ActView &in, int32_t steps, const ActView &out, hipStream_t s);
 hipError_t launch_channel_shuffle(const ActView &in, const ActView &out, hipStream_t s);
+const char *channel_shuffle_label(const ActView &in, const ActView &out);
 hipError_t launch_maxpool(const ActView &in, int k, int stride, int pad, const ActView &out,
                           hipStream_t s);
 hipError_t launch_avgsum(const ActView &in, int32_t *out, hipStream_t s, int8_t *planes = nullptr, int P = 0,

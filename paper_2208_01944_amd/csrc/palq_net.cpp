@@ -565,7 +565,7 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
     if (L.op == PALQ_OP_CONV) {
       k = NL.pool_fused ? "stem_pool_kernel" : NL.use_mfma ? conv_kernel_label(NL.conv, NL.epi) : "conv_direct_kernel";
     } else if (L.op == PALQ_OP_CHANNEL_SHUFFLE) {
-      k = "channel_shuffle_kernel";
+      k = channel_shuffle_label(view_of(&net->tensors[L.src].d), view_of(&net->tensors[L.dst].d));
     } else if (L.op == PALQ_OP_MAXPOOL) {
       k = maxpool_label(view_of(&net->tensors[L.src].d), view_of(&net->tensors[L.dst].d));
     } else if (L.op == PALQ_OP_AVGSUM) {

@@ -277,12 +277,18 @@ GOLDEN_DIR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file
 def workload(name):
     """(spec, fp32 images, images the centring is calibrated on) of a
     benchmark network: "resnet18_g4_b2" (ResNet-18 topology, G=4, 2-bit,
-    batch 64, 224x224) or "resnet50_g2_b2" (ResNet-50 v1.5 bottlenecks, G=2,
-    2-bit, batch 128, 224x224)."""
+    batch 64, 224x224), "resnet18_g4_b2_shuffles" (the same with the cyclic
+    shuffle modules and channel shuffles) or "resnet50_g2_b2" (ResNet-50
+    v1.5 bottlenecks, G=2, 2-bit, batch 128, 224x224)."""
     if name == "resnet18_g4_b2":
         return resnet18(n=64, groups=4, bits=2), image_fp32(SEED_BASE + 30, 64), [0, 63]
     if name == "resnet50_g2_b2":
         return resnet50(n=128, groups=2, bits=2), image_fp32(SEED_BASE + 50, 128), [0, 127]
+    if name == "resnet18_g4_b2_shuffles":
+        # the same network with a cyclic shuffle module at the start of stages
+        # 2-4 and the per-stage channel shuffle (Section 4.3, Table 3)
+        return (resnet18(n=64, groups=4, bits=2, modules=True, channel_shuffle=True),
+                image_fp32(SEED_BASE + 30, 64), [0, 63])
     raise ValueError(name)
 
 

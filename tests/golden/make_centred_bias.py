@@ -24,7 +24,7 @@ sys.path.insert(0, ROOT)
 from oracle import oracle as O  # noqa: E402
 from paper_2208_01944_amd import inputs as I  # noqa: E402
 
-WORKLOADS = ["resnet18_g4_b2", "resnet50_g2_b2", "single"]
+WORKLOADS = ["resnet18_g4_b2", "resnet18_g4_b2_shuffles", "resnet50_g2_b2", "single"]
 
 
 def single_bias(name):

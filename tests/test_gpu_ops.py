@@ -619,13 +619,25 @@ def test_shuffle_module_matches_oracle(ctx, torch, G, C, bits, n, h, w):
     assert np.count_nonzero(hist) >= 2, hist
 
 
-@pytest.mark.parametrize("bits,G,C", [(2, 4, 64), (2, 2, 37), (3, 3, 48), (4, 4, 128), (8, 2, 40), (2, 4, 512)])
-def test_channel_shuffle_matches_oracle(ctx, bits, G, C):
-    say(f"channel shuffle b={bits} G={G} C={C}")
+# (bits, G, C, image shape): the word-level build takes b in {2, 4, 8}, G in
+# {2, 4, 8, 16}, unpadded rows and whole 16-byte stores per pixel; the rest
+# (3-bit, G = 3, padded rows, a pixel that is not whole stores) takes the
+# per-chunk build.  The 28 x 28 case spans many workgroups with a ragged tail.
+CHANNEL_SHUFFLE_CASES = [
+    (2, 4, 64, (2, 5, 3)), (2, 2, 37, (2, 5, 3)), (3, 3, 48, (2, 5, 3)), (4, 4, 128, (2, 5, 3)),
+    (8, 2, 40, (2, 5, 3)), (2, 4, 512, (2, 5, 3)), (2, 8, 32, (2, 5, 3)), (2, 16, 16, (2, 5, 3)),
+    (2, 2, 16, (2, 5, 3)), (4, 8, 16, (2, 5, 3)), (8, 16, 4, (2, 5, 3)), (4, 2, 24, (2, 5, 3)),
+    (2, 8, 8, (2, 5, 3)), (2, 4, 32, (4, 28, 28)), (8, 4, 16, (3, 7, 9)),
+]
+
+
+@pytest.mark.parametrize("bits,G,C,shape", CHANNEL_SHUFFLE_CASES)
+def test_channel_shuffle_matches_oracle(ctx, bits, G, C, shape):
+    say(f"channel shuffle b={bits} G={G} C={C} shape={shape}")
     g = np.random.default_rng(bits * 100 + G * 10 + C)
-    x = I.codes(g, (2, 5, 3, G * C), bits, False).astype(np.int64)
+    x = I.codes(g, shape + (G * C,), bits, False).astype(np.int64)
     xt = ctx.pack(x, G, bits)
-    out = ctx.empty_act(2, 5, 3, G, C, bits)
+    out = ctx.empty_act(*shape, G, C, bits)
     ctx.channel_shuffle(xt, out)
     ctx.sync()
     np.testing.assert_array_equal(ctx.unpack(out), O.channel_shuffle(x, G))

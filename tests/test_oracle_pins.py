@@ -583,7 +583,7 @@ def test_bitops_match_paper_tables():
 # ---------------------------------------------------------------------------
 # Stored inputs: the benchmark networks' centred biases
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("name", ["resnet18_g4_b2", "resnet50_g2_b2"])
+@pytest.mark.parametrize("name", ["resnet18_g4_b2", "resnet18_g4_b2_shuffles", "resnet50_g2_b2"])
 def test_stored_centred_biases_match_oracle_calibration(name):
     """tests/golden/centred_bias_<name>.npz holds what the oracle's centring
     calibration gives today on the workload's calibration images (so the
