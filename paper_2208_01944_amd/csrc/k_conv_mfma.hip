@@ -1809,9 +1809,10 @@ __global__ __launch_bounds__(sp::NT, 2) void stem_pool_kernel(ConvArgs a, Geo ge
     const int c = min(63 * wm + 2 * l32 + pb, wo - 1);
     xa[pb] = lds_base + (uint32_t)((c & 1) * RB + 16 * (c >> 1) + 16 * half);
   }
-  // the lane whose pooling neighbour would be in the other lane half
-  // (column -1 for wm = 0, column 127 for wm = 1)
-  const bool half_edge = wm ? lane == 31 : lane == 32;
+  // the lanes whose pooling neighbour is missing from the DPP shift: the
+  // wave's end lane (no source lane) and the lane whose source lies in the
+  // other lane half (column -1 for wm = 0, column 127 for wm = 1)
+  const bool half_edge = wm ? l32 == 31 : l32 == 0;
   // pooled column px = 32 wm + l; its byte offset in a pooled row plus this
   // lane's word of the wave's channels (word 2 (4 cbb + 2 wn + cb) + half)
   const int px = 32 * wm + l32;
@@ -1831,18 +1832,18 @@ __global__ __launch_bounds__(sp::NT, 2) void stem_pool_kernel(ConvArgs a, Geo ge
       constexpr int WMV = decltype(WMC)::value;
       // neighbour column by a DPP wave shift folded into the max (lane i
       // reads lane i - 1 for wm = 0, i + 1 for wm = 1; the end lane, which
-      // has no source, takes the identity INT_MIN); the lane whose
-      // neighbour lies in the other lane half takes its own column instead
-      // (a duplicate leaves the max unchanged)
+      // has no source, reads zero); the edge lanes (that end lane and the
+      // lane whose neighbour lies in the other lane half) take their own
+      // column instead (a duplicate leaves the max unchanged)
       auto hmax = [&](int cb, int i) __attribute__((always_inline)) {
         const int32_t v0 = acc[cb][0][i], v1 = acc[cb][1][i];
         int32_t t;
         if constexpr (WMV == 0) {
-          t = max(__builtin_amdgcn_update_dpp((int)0x80000000, v1, 0x138 /* wave_shr:1 */, 0xf, 0xf, false), v0);
+          t = max(__builtin_amdgcn_update_dpp(0, v1, 0x138 /* wave_shr:1 */, 0xf, 0xf, true), v0);
           t = half_edge ? v0 : t;
           return max(t, v1);
         } else {
-          t = max(__builtin_amdgcn_update_dpp((int)0x80000000, v0, 0x130 /* wave_shl:1 */, 0xf, 0xf, false), v1);
+          t = max(__builtin_amdgcn_update_dpp(0, v0, 0x130 /* wave_shl:1 */, 0xf, 0xf, true), v1);
           t = half_edge ? v1 : t;
           return max(t, v0);
         }
@@ -1873,17 +1874,28 @@ __global__ __launch_bounds__(sp::NT, 2) void stem_pool_kernel(ConvArgs a, Geo ge
     // requant the pooled row and store it: channel 128 cbb + 64 wn + 32 cb + 8 qi + 4 half + e
     const int orow = ((n * ho2 + k) * wo2) * (int)po.pixel;
     const RqConst *rq = rq_area + (cbb == cbb0 ? 0 : 128) + wn * 64;
+    // the constants of quad j + 1 are read while quad j is requantised (two
+    // quads' constants in registers, which the dead accumulators free)
+    RqConst qc[2][4];
+    auto load_quad = [&](int j) __attribute__((always_inline)) {
+      const int cq = (j >> 2) * 32 + 8 * (j & 3) + 4 * half;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) qc[j & 1][e] = rq[cq + e];
+    };
+    load_quad(0);
 #pragma unroll
     for (int cb = 0; cb < 2; ++cb) {
       uint32_t qv[4];
 #pragma unroll
       for (int qi = 0; qi < 4; ++qi) {
-        __builtin_amdgcn_sched_barrier(0);  // one quad's constants at a time
-        const int cq = cb * 32 + 8 * qi + 4 * half;
+        const int j = 4 * cb + qi;
+        __builtin_amdgcn_sched_barrier(0);
+        if (j < 7) load_quad(j + 1);
+        __builtin_amdgcn_sched_barrier(0);
         uint32_t qword = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const double d = __builtin_fma((double)st[cb][4 * qi + e], rq[cq + e].s, rq[cq + e].o);
+          const double d = __builtin_fma((double)st[cb][4 * qi + e], qc[j & 1][e].s, qc[j & 1][e].o);
           uint32_t q;
           asm("v_cvt_u32_f64 %0, %1" : "=v"(q) : "v"(d));
           qword |= min(q, 3u) << (2 * e);
