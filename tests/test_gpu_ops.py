@@ -643,6 +643,20 @@ def test_channel_shuffle_matches_oracle(ctx, bits, G, C, shape):
     np.testing.assert_array_equal(ctx.unpack(out), O.channel_shuffle(x, G))
 
 
+def test_channel_shuffle_full_size(ctx):
+    """The stage-2 channel shuffle of the batch-64 ResNet-18 G = 4 2-bit
+    network with shuffles (64 x 56 x 56 pixels, 4 groups of 64 channels),
+    every code against the oracle's transposition."""
+    say("channel shuffle full size 64x56x56 G=4 C=64 b=2")
+    g = np.random.default_rng(2208)
+    x = I.codes(g, (64, 56, 56, 256), 2, False)
+    xt = ctx.pack(x, 4, 2)
+    out = ctx.empty_act(64, 56, 56, 4, 64, 2)
+    ctx.channel_shuffle(xt, out)
+    ctx.sync()
+    np.testing.assert_array_equal(ctx.unpack(out).reshape(x.shape), O.channel_shuffle(x, 4))
+
+
 @pytest.mark.parametrize("big_bias", [False, True])
 def test_conv_filter_longer_than_lds(ctx, torch, big_bias):
     """A 2-bit layer whose filter (K = 9 x 1024) is too long for the general
