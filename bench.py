@@ -46,6 +46,9 @@ def parse():
                     help="skip the per-layer output-code histograms (an untimed extra forward)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true", help="replay the forward from a captured HIP graph")
+    ap.add_argument("--pixel-layout", action="store_true",
+                    help="keep every intermediate tensor in the pixel layout (the network stores "
+                         "conv outputs group by group by default)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="wall-clock budget of the oracle sample")
     ap.add_argument("--summarize-profile", metavar="DIR", default=None,
@@ -571,8 +574,9 @@ def run_network(args, workload):
     ctx = palq.Context(0)
     # eager launches (--graph: replay from a captured HIP graph, which
     # measured about 1.5 % slower for the ResNet-18 network)
-    net = palq.Net(ctx, spec, flags=palq.NET_GRAPH if args.graph else 0)
-    net_t = palq.Net(ctx, spec, flags=palq.NET_TIMING)
+    lay = palq.NET_PIXEL_LAYOUT if args.pixel_layout else 0
+    net = palq.Net(ctx, spec, flags=(palq.NET_GRAPH if args.graph else 0) | lay)
+    net_t = palq.Net(ctx, spec, flags=palq.NET_TIMING | lay)
     xd = ctx.upload(x_f32)
     logits = torch.empty(n * net.classes, dtype=torch.int32, device=ctx.dev)
 
@@ -651,6 +655,7 @@ def run_network(args, workload):
                 "centred conv biases calibrated by the oracle on images %s)" % calib,
         "config": {"workload": cfg_name, "global_batch": n, "image": [spec["hw"], spec["hw"], 3],
                    "groups": spec["groups"], "bits": spec["bits"], "variant": "centred",
+                   "tensor_layout": "pixel" if args.pixel_layout else "group (conv outputs)",
                    "step": "palq_forward_image (quantize fp32 input + forward)"},
         "effective_tops": tops,
         "int_ops_per_step": total_ops,

@@ -26,7 +26,11 @@
  *  A tensor [N][H][W][G][C^] of b-bit codes is stored NHWC, group-major
  *  (channel g*C^ + j, the [N, G, C^, H, W] view of Section 4.2).  Each
  *  (pixel, group) row of C^ codes occupies palq_row_bytes(C^, b) bytes and
- *  rows follow each other with no gap; a pixel is G rows.
+ *  rows follow each other with no gap; a pixel is G rows.  That is layout
+ *  PALQ_LAYOUT_PIXEL.  PALQ_LAYOUT_GROUP stores the same rows as
+ *  [G][N][H][W]: all of group 0's rows in pixel order, then group 1's, ...
+ *  (a group's rows of consecutive pixels are adjacent, so one group's tile
+ *  of pixels is one contiguous run).  Both take palq_act_bytes() bytes.
  *   - b in {2, 4, 8}: code j sits at bits [b*j, b*j + b) of the row read as
  *     one little-endian bit string; the row is padded with zero bits to a
  *     multiple of 32 bits.
@@ -64,12 +68,18 @@ typedef struct palq_ctx palq_ctx;
 typedef struct palq_net palq_net;
 
 /* An activation tensor: n x h x w pixels of `groups` rows of ch_per_group
- * codes, `bits` in {2, 3, 4, 8}.  data: device, palq_act_bytes() bytes. */
+ * codes, `bits` in {2, 3, 4, 8}.  data: device, palq_act_bytes() bytes.
+ * layout: PALQ_LAYOUT_PIXEL (0, what a zeroed descriptor holds) or
+ * PALQ_LAYOUT_GROUP (see the packed code layout above); every call takes
+ * either, and the tensors of one call may mix them. */
+#define PALQ_LAYOUT_PIXEL 0
+#define PALQ_LAYOUT_GROUP 1
 typedef struct {
   int32_t n, h, w;
   int32_t groups, ch_per_group;
   int32_t bits;
   int32_t is_signed;
+  int32_t layout;
   void *data;
 } palq_act;
 
@@ -234,7 +244,7 @@ typedef struct palq_conv_plan palq_conv_plan;
  * rq's arrays, res->res_mult and res->proj_w into device memory the plan
  * owns, prepacks the filter, computes the requant constants and reads back
  * which epilogue applies (this call synchronises the context's stream once).
- * Only the shapes, bits and signs of in, out, res->identity and res->proj_in
+ * Only the shapes, bits, signs and layouts of in, out, res->identity and res->proj_in
  * are used; their data pointers are ignored.  The caller may free the
  * parameter arrays once this returns.  A validate-only context returns a
  * plan that runs nothing.  Errors as palq_group_conv; PALQ_ERR_NOMEM. */
@@ -321,6 +331,10 @@ palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, con
                              * the launch sequence once per (input, logits, l,
                              * u, stream) and replay it; input contents may
                              * change between calls.  Not with PALQ_NET_TIMING. */
+#define PALQ_NET_PIXEL_LAYOUT 8 /* keep every tensor in PALQ_LAYOUT_PIXEL; by
+                                 * default a conv output of several groups
+                                 * whose every reader takes it with those
+                                 * groups is stored in PALQ_LAYOUT_GROUP */
 
 /* One layer of a network.  Tensor ids: 0 is the network input; each layer
  * writes a new id `dst` larger than every id before it.  Every pointer in

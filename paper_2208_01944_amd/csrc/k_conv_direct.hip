@@ -48,7 +48,7 @@ __global__ void conv_direct_kernel(ConvArgs a, int chunks, const int32_t *only_i
         const int ix = ox * a.stride - a.pad + kx;
         if (ix < 0 || ix >= a.in.w) continue;
         const uint8_t *xr = a.in.data + (((int64_t)n * a.in.h + iy) * a.in.w + ix) * a.in.pixel +
-                            (int64_t)g * a.in.row;
+                            (int64_t)g * a.in.gstride;
         const uint8_t *wr = a.w + ((((int64_t)g * a.cout + k) * a.kh + ky) * a.kw + kx) * wrow;
         for (int c = 0; c < cin; ++c)
           acc += (int64_t)read_code(xr, c, a.in.bits, a.in.is_signed) * read_code(wr, c, a.w_bits, 1);
@@ -57,7 +57,7 @@ __global__ void conv_direct_kernel(ConvArgs a, int chunks, const int32_t *only_i
     if (a.proj.data) {
       const int iy = oy * a.proj_stride, ix = ox * a.proj_stride;
       const uint8_t *xr = a.proj.data + (((int64_t)n * a.proj.h + iy) * a.proj.w + ix) * a.proj.pixel +
-                          (int64_t)gd * a.proj.row;
+                          (int64_t)gd * a.proj.gstride;
       const int pc = a.proj.cpg;
       const uint8_t *wr = a.proj_w + ((int64_t)gd * a.cout + k) * row_bytes(pc, a.w_bits);
       for (int c = 0; c < pc; ++c)
@@ -68,7 +68,7 @@ __global__ void conv_direct_kernel(ConvArgs a, int chunks, const int32_t *only_i
     if (a.acc_dump) a.acc_dump[p * (int64_t)G * a.cout + cd] = (int32_t)acc;
     int64_t tt = acc + (a.bias ? a.bias[cs] : 0);
     if (a.res.data) {
-      const uint8_t *rr = a.res.data + p * a.res.pixel + (int64_t)gd * a.res.row;
+      const uint8_t *rr = a.res.data + p * a.res.pixel + (int64_t)gd * a.res.gstride;
       tt += (int64_t)a.res_mult[cs] * read_code(rr, k, a.res.bits, 0);
     }
     q[jj] = (int)requant_one(tt, a.mult[cs], a.shift[cs], qmax);
@@ -77,7 +77,7 @@ __global__ void conv_direct_kernel(ConvArgs a, int chunks, const int32_t *only_i
   pack_chunk(q, nc, a.out.bits, words);
   const int per_chunk = a.out.bits == 3 ? 3 : store_bits(a.out.bits);
   const int nw = chunk_words_in_row(ci, a.out.bits, a.out.row / 4);
-  uint32_t *dst = (uint32_t *)(a.out.data + p * a.out.pixel + (int64_t)gd * a.out.row) +
+  uint32_t *dst = (uint32_t *)(a.out.data + p * a.out.pixel + (int64_t)gd * a.out.gstride) +
                   (int64_t)ci * per_chunk;
   for (int kk = 0; kk < nw; ++kk) dst[kk] = words[kk];
 }

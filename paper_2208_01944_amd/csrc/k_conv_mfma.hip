@@ -575,7 +575,7 @@ __device__ __forceinline__ void epilogue(const ConvArgs &a, const Geo &geo, v16i
           for (int e = 0; e < 4; ++e) v[e] += (rmu[e] * chunk_code(rw[cb][pb], cq + e, 2)) << lsc;
         } else if constexpr (RB < 0) {
           int rc[4];
-          row_quad(a.res.data + (mp < geo.M ? mp : 0) * a.res.pixel + (int64_t)gd * a.res.row, kc + cq,
+          row_quad(a.res.data + (mp < geo.M ? mp : 0) * a.res.pixel + (int64_t)gd * a.res.gstride, kc + cq,
                    a.res.bits, rc);
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] += (rmu[e] * rc[e]) << lsc;
@@ -626,7 +626,7 @@ __device__ __forceinline__ void epilogue(const ConvArgs &a, const Geo &geo, v16i
         hpart |= (uint32_t)__shfl_xor((int)hpart, 32);
       }
       if (mp >= geo.M) continue;
-      uint8_t *orow = a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row;
+      uint8_t *orow = a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.gstride;
       if (bo == 3) {
         uint32_t *cw = (uint32_t *)orow + (int64_t)(kc >> 5) * 3;
         cw[half] = Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24);
@@ -766,7 +766,7 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
         } else if constexpr (RB < 0) {
           const int64_t mp = mbase + pb * 32 + l32;
           int rc[4];
-          row_quad(a.res.data + (mp < geo.M ? mp : 0) * a.res.pixel + (int64_t)gd * a.res.row, kc + cq,
+          row_quad(a.res.data + (mp < geo.M ? mp : 0) * a.res.pixel + (int64_t)gd * a.res.gstride, kc + cq,
                    a.res.bits, rc);
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] += (rmu[e] * rc[e]) << lsc;
@@ -811,7 +811,7 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
         const auto hs = __builtin_amdgcn_permlane32_swap(hp, hp, false, false);
         const uint32_t hw = hs[0] | hs[1];
         if (mp >= geo.M) continue;
-        uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row) + (int64_t)(kc >> 5) * 3;
+        uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.gstride) + (int64_t)(kc >> 5) * 3;
         cw[half] = Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24);
         if (half == 0) cw[2] = hw;
         continue;
@@ -821,7 +821,7 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
         continue;
       }
       if (mp >= geo.M) continue;
-      uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row) +
+      uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.gstride) +
                      (int64_t)(kc >> 5) * bo + half * (bo / 2);
       if (bo == 2) {
         cw[0] = Q[0] | (Q[1] << 8) | (Q[2] << 16) | (Q[3] << 24);
@@ -842,7 +842,7 @@ __device__ __forceinline__ void epilogue_fast_bo(const ConvArgs &a, const Geo &g
       const auto s1 = __builtin_amdgcn_permlane32_swap(w2[1][2 * i], w2[1][2 * i + 1], false, false);
       const int64_t mp = mbase + (2 * i + half) * 32 + l32;
       if (mp >= geo.M) continue;
-      uint8_t *dst = a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row + (int64_t)(ch0 >> 5) * 8;
+      uint8_t *dst = a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.gstride + (int64_t)(ch0 >> 5) * 8;
       *(uint4 *)dst = make_uint4(s0[0], s0[1], s1[0], s1[1]);
     }
   }
@@ -963,9 +963,9 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
   const int tstride = gridDim.x * kNW;
   if (first >= tiles) return;  // no barrier follows
 
-  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
+  const auto rin = make_rsrc(a.in.data, a.in.bytes);
   // without a projection this resource has no bytes: every load returns 0
-  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, (int64_t)a.proj.n * a.proj.h * a.proj.w * a.proj.pixel)
+  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, a.proj.bytes)
                                : make_rsrc(a.in.data, 0);
   const int pixb = (int)a.in.pixel;
   const int rowb = a.in.w * pixb;
@@ -987,7 +987,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
       const int oy = fdiv(rem, a.wo, inv_wo);
       const int ox = rem - oy * a.wo;
       const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
-      off0[pb] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.row + half * (BLK / 2);
+      off0[pb] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.gstride + half * (BLK / 2);
       const int xlo = max(0, -ix0), xhi = min(a.kw, a.in.w - ix0);
       const uint32_t below = xhi >= 32 ? 0xffffffffu : ((1u << max(xhi, 0)) - 1u);
       const uint32_t cols = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
@@ -998,7 +998,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
       poff[pb] = (a.proj.data && valid)
                      ? (uint32_t)(((n * a.proj.h + oy * a.proj_stride) * a.proj.w + ox * a.proj_stride) *
                                       (int)a.proj.pixel +
-                                  gd * (int)a.proj.row + half * (BLK / 2))
+                                  gd * (int)a.proj.gstride + half * (BLK / 2))
                      : kOob;
     }
   };
@@ -1046,7 +1046,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
   load_next(xs0);
   load_next(xs1);
   int phase = 0;
-  const auto rres = make_rsrc(a.res.data, a.res.data ? (int64_t)a.res.n * a.res.h * a.res.w * a.res.pixel : 0);
+  const auto rres = make_rsrc(a.res.data, a.res.data ? a.res.bytes : 0);
   for (int ct = first; ct < tiles; ct += tstride) {
     // shortcut codes of this tile (2-bit): fetched now, used by the epilogue
     uint32_t rw[CB][PB][2];
@@ -1057,7 +1057,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_grouped_kernel(ConvArgs a, Geo 
         rw[cb][pb][0] = rw[cb][pb][1] = 0;
         if constexpr (RB == 2) {
           const int m = ct * PB * 32 + pb * 32 + l32;
-          const uint32_t ro = m < geo.M ? (uint32_t)(m * (int)a.res.pixel + gd * (int)a.res.row + ((ch0 + cb * 32) >> 5) * 8)
+          const uint32_t ro = m < geo.M ? (uint32_t)(m * (int)a.res.pixel + gd * (int)a.res.gstride + ((ch0 + cb * 32) >> 5) * 8)
                                         : kOob;
           const auto v = __builtin_amdgcn_raw_buffer_load_b64(rres, (int)ro, 0, 0);
           const uint2 u = __builtin_bit_cast(uint2, v);
@@ -1116,7 +1116,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo
   const int tstride = gridDim.x * kNW;
   if (first >= tiles) return;
 
-  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
+  const auto rin = make_rsrc(a.in.data, a.in.bytes);
   const int pixb = (int)a.in.pixel;
   const int rowb = a.in.w * pixb;
   const int HW = a.ho * a.wo;
@@ -1137,7 +1137,7 @@ __global__ __launch_bounds__(kNW * 64) void conv_stem_kernel(ConvArgs a, Geo geo
       const int ox = rem - oy * a.wo;
       iy0[pb] = valid ? oy * a.stride - a.pad : -(1 << 20);  // invalid pixel: every row out of range
       const int ix0 = ox * a.stride - a.pad;
-      off0[pb] = ((n * a.in.h + oy * a.stride - a.pad) * a.in.w + ix0) * pixb + g * (int)a.in.row;
+      off0[pb] = ((n * a.in.h + oy * a.stride - a.pad) * a.in.w + ix0) * pixb + g * (int)a.in.gstride;
       const int xlo = max(0, -ix0), xhi = min(min(8, a.kw), a.in.w - ix0);
       const uint32_t below = (1u << max(xhi, 0)) - 1u;
       xmask[pb] = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
@@ -1380,8 +1380,8 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
 
   const auto rw_src = make_rsrc(geo.wp, (int64_t)G * a.cout * KB * (SLAB / 32));
-  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
-  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, (int64_t)a.proj.n * a.proj.h * a.proj.w * a.proj.pixel)
+  const auto rin = make_rsrc(a.in.data, a.in.bytes);
+  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, a.proj.bytes)
                                : make_rsrc(a.in.data, 0);
   const int pixb = (int)a.in.pixel;
   const int rowb = a.in.w * pixb;
@@ -1416,7 +1416,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
         const int rem = mm - n * HW;
         const int oy = fdiv(rem, a.wo, inv_wo);
         const int ox = rem - oy * a.wo;
-        soff[i] = valid ? ((n * a.in.h + oy * a.stride) * a.in.w + ox * a.stride) * pixb + g * (int)a.in.row +
+        soff[i] = valid ? ((n * a.in.h + oy * a.stride) * a.in.w + ox * a.stride) * pixb + g * (int)a.in.gstride +
                               ((tid >> 1) & 1) * rowb + (tid & 1) * 16
                         : -1;
       }
@@ -1430,7 +1430,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
     const int oy = fdiv(rem, a.wo, inv_wo);
     const int ox = rem - oy * a.wo;
     const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
-    off0 = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.row + xb;
+    off0 = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.gstride + xb;
     const int xlo = max(0, -ix0), xhi = min(a.kw, a.in.w - ix0);
     const uint32_t below = xhi >= 32 ? 0xffffffffu : ((1u << max(xhi, 0)) - 1u);
     const uint32_t cols = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
@@ -1440,14 +1440,14 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
     tmask = valid ? mk : 0u;
     poff = (a.proj.data && valid)
                ? (((n * a.proj.h + oy * a.proj_stride) * a.proj.w + ox * a.proj_stride) * (int)a.proj.pixel +
-                  gd * (int)a.proj.row + xb)
+                  gd * (int)a.proj.gstride + xb)
                : (int)kOob;
   };
   tile_geometry();
   // Fetches K-block f_kb of tile f_tile into ring stage st.  Fetches past
   // the last tile read out-of-range offsets (zeros), so every call issues
   // the same loads.
-  const auto rres = make_rsrc(a.res.data, a.res.data ? (int64_t)a.res.n * a.res.h * a.res.w * a.res.pixel : 0);
+  const auto rres = make_rsrc(a.res.data, a.res.data ? a.res.bytes : 0);
   auto fetch = [&](int st) __attribute__((always_inline)) {
     const bool live = f_tile < t_end;
     uint8_t *ws = lds + st * SST;
@@ -1461,7 +1461,7 @@ __global__ __launch_bounds__(WN * WM * 64, 2) void conv_tile_kernel(ConvArgs a, 
         for (int i = 0; i < RPT; ++i) {
           const int c = tid + i * NT;
           const int m = pt * TM + c / (RPX / 16);
-          const uint32_t ro = live && m < geo.M ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.row + cbk * RPX +
+          const uint32_t ro = live && m < geo.M ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.gstride + cbk * RPX +
                                                              (c % (RPX / 16)) * 16)
                                                 : kOob;
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(rb + i * NT * 16 + wave * 1024), 16, (int)ro, 0,
@@ -1769,8 +1769,8 @@ __global__ __launch_bounds__(sp::NT, 2) void stem_pool_kernel(ConvArgs a, Geo ge
   __syncthreads();
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
   typedef __attribute__((address_space(3))) void *lds_ptr;
-  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
-  const auto rout = make_rsrc(po.data, (int64_t)po.n * po.h * po.w * po.pixel);
+  const auto rin = make_rsrc(a.in.data, a.in.bytes);
+  const auto rout = make_rsrc(po.data, po.bytes);
   const int rowb = a.in.w * (int)a.in.pixel;  // <= RB (launcher)
 
   // ---- fetcher: output row f_it.  Wave w stages input rows w and w + 4 of
@@ -2130,10 +2130,10 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
 
   const auto rw_src = make_rsrc(geo.wp, (int64_t)G * a.cout * KB * (C::SLAB / 32));
-  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
-  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, (int64_t)a.proj.n * a.proj.h * a.proj.w * a.proj.pixel)
+  const auto rin = make_rsrc(a.in.data, a.in.bytes);
+  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, a.proj.bytes)
                                : make_rsrc(a.in.data, 0);
-  const auto rres = make_rsrc(a.res.data, a.res.data ? (int64_t)a.res.n * a.res.h * a.res.w * a.res.pixel : 0);
+  const auto rres = make_rsrc(a.res.data, a.res.data ? a.res.bytes : 0);
   const int pixb = (int)a.in.pixel, rowb = a.in.w * pixb;
 
   // ---- this thread's fetch pieces (wave w issues load i if C::wloads /
@@ -2164,7 +2164,7 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
     const int oy = fdiv(rem, a.wo, inv_wo);
     const int ox = rem - oy * a.wo;
     const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
-    off0[i] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.row + (B == 3 ? 12 * ((q >> 5) & 1) : 0);
+    off0[i] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.gstride + (B == 3 ? 12 * ((q >> 5) & 1) : 0);
     const int xlo = max(0, -ix0), xhi = min(a.kw, a.in.w - ix0);
     const uint32_t below = xhi >= 32 ? 0xffffffffu : ((1u << max(xhi, 0)) - 1u);
     const uint32_t cols = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
@@ -2174,7 +2174,7 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
     tmask[i] = valid ? mk : 0u;
     poff[i] = (a.proj.data && valid)
                   ? (((n * a.proj.h + oy * a.proj_stride) * a.proj.w + ox * a.proj_stride) * (int)a.proj.pixel +
-                     gd * (int)a.proj.row)
+                     gd * (int)a.proj.gstride)
                   : (int)kOob;
   }
   // fetch cursor: K-block f_kb = tap f_tap, block f_c of it; vo: the
@@ -2194,7 +2194,7 @@ __device__ __forceinline__ void conv_fpx_tile(const ConvArgs &a, const Geo &geo,
         for (int i = 0; i < RPT; ++i) {
           const int c = tid + i * NT;
           const int m = pt * TM + c / (C::RPX / 16);
-          const uint32_t ro = m < geo.M ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.row + cbk * C::RPX +
+          const uint32_t ro = m < geo.M ? (uint32_t)((int64_t)m * a.res.pixel + gd * a.res.gstride + cbk * C::RPX +
                                                      (c % (C::RPX / 16)) * 16)
                                         : kOob;
           __builtin_amdgcn_raw_ptr_buffer_load_lds(rres, (lds_ptr)(lds + RING + i * NT * 16 + wave * 1024), 16,
@@ -2578,8 +2578,8 @@ __global__ __launch_bounds__(WN * 128, 2) void conv_bitdecomp_kernel(ConvArgs a,
   typedef __attribute__((address_space(3))) void *lds_ptr;
   const uint32_t lds_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t *)lds;
   const auto rw_src = make_rsrc(geo.wp, (int64_t)G * a.cout * KB * GC * (kSlab4 / 32));
-  const auto rin = make_rsrc(a.in.data, (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel);
-  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, (int64_t)a.proj.n * a.proj.h * a.proj.w * a.proj.pixel)
+  const auto rin = make_rsrc(a.in.data, a.in.bytes);
+  const auto rpj = a.proj.data ? make_rsrc(a.proj.data, a.proj.bytes)
                                : make_rsrc(a.in.data, 0);
   const int pixb = (int)a.in.pixel, rowb = a.in.w * pixb;
 
@@ -2610,7 +2610,7 @@ __global__ __launch_bounds__(WN * 128, 2) void conv_bitdecomp_kernel(ConvArgs a,
     const int oy = fdiv(rem, a.wo, inv_wo);
     const int ox = rem - oy * a.wo;
     const int iy0 = oy * a.stride - a.pad, ix0 = ox * a.stride - a.pad;
-    off0[i] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.row + hoff;
+    off0[i] = ((n * a.in.h + iy0) * a.in.w + ix0) * pixb + g * (int)a.in.gstride + hoff;
     const int xlo = max(0, -ix0), xhi = min(a.kw, a.in.w - ix0);
     const uint32_t below = xhi >= 32 ? 0xffffffffu : ((1u << max(xhi, 0)) - 1u);
     const uint32_t cols = xhi > xlo ? (below & ~((1u << xlo) - 1u)) : 0u;
@@ -2620,7 +2620,7 @@ __global__ __launch_bounds__(WN * 128, 2) void conv_bitdecomp_kernel(ConvArgs a,
     tmask[i] = valid ? mk : 0u;
     poff[i] = (a.proj.data && valid)
                   ? (((n * a.proj.h + oy * a.proj_stride) * a.proj.w + ox * a.proj_stride) * (int)a.proj.pixel +
-                     gd * (int)a.proj.row + hoff)
+                     gd * (int)a.proj.gstride + hoff)
                   : (int)kOob;
   }
   int f_kb = 0, f_c = 0, f_tap = 0, f_kx = 0, f_tapoff = 0;
@@ -2765,7 +2765,7 @@ __global__ __launch_bounds__(WN * 128, 2) void conv_bitdecomp_kernel(ConvArgs a,
         const int cq = 8 * qi + 4 * half;
         int rc[4] = {0, 0, 0, 0};
         if constexpr (RB < 0)
-          row_quad(a.res.data + (live ? mp : 0) * a.res.pixel + (int64_t)gd * a.res.row, kc + cq, a.res.bits, rc);
+          row_quad(a.res.data + (live ? mp : 0) * a.res.pixel + (int64_t)gd * a.res.gstride, kc + cq, a.res.bits, rc);
         uint32_t qword = 0;
         v4i dv;
 #pragma unroll
@@ -2794,7 +2794,7 @@ __global__ __launch_bounds__(WN * 128, 2) void conv_bitdecomp_kernel(ConvArgs a,
       const auto p1 = __builtin_amdgcn_permlane32_swap(qv[pb][1], qv[pb][3], false, false);
       const uint32_t Qw[4] = {p0[0], p0[1], p1[0], p1[1]};
       if (mp >= geo.M) continue;
-      uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.row) + (int64_t)(kc >> 5) * BO +
+      uint32_t *cw = (uint32_t *)(a.out.data + mp * a.out.pixel + (int64_t)gd * a.out.gstride) + (int64_t)(kc >> 5) * BO +
                      half * (BO / 2);
       if constexpr (BO == 4) *(uint2 *)cw = make_uint2(Qw[0] | (Qw[1] << 16), Qw[2] | (Qw[3] << 16));
       else *(uint4 *)cw = make_uint4(Qw[0], Qw[1], Qw[2], Qw[3]);
@@ -2921,7 +2921,7 @@ bool conv_mfma_general_fits(const ConvArgs &a) { return pick_cb(a, make_geo(a)) 
 bool conv_mfma_supported(const ConvArgs &a) {
   if (a.cout % 32 != 0) return false;
   const int64_t lim = (int64_t)1 << 30;
-  auto bytes = [](const ActView &v) { return v.data ? (int64_t)v.n * v.h * v.w * v.pixel : 0; };
+  auto bytes = [](const ActView &v) { return v.data ? v.bytes : 0; };
   if (bytes(a.in) >= lim || bytes(a.out) >= lim || bytes(a.res) >= lim || bytes(a.proj) >= lim) return false;
   if ((int64_t)a.out.n * a.ho * a.wo >= (1 << 24)) return false;
   if (!is_stem(a)) {
@@ -3242,7 +3242,7 @@ hipError_t launch_fpx(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   const int64_t T = (int64_t)npt * ncb * a.in.groups;
   if (T <= 0 || T > 0x3fffffff || geo.kb_total < 1) return hipErrorInvalidValue;
   const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * (C::SLAB / 32);
-  const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
+  const int64_t xbytes = a.in.bytes;
   const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(32, npt) : 1;
   if (KS == 2 && (geo.kb_total % 2 != 0 || geo.cpb % 2 != 0)) return hipErrorInvalidValue;
   const dim3 grid((unsigned)((T + 7) / 8 * 8)), block(C::NT * KS);
@@ -3296,7 +3296,7 @@ hipError_t launch_bd(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   const int64_t T = (int64_t)npt * ncb * a.in.groups;
   if (T <= 0 || T > 0x3fffffff || geo.kb_total < 1) return hipErrorInvalidValue;
   const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * C::GC * 32;
-  const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
+  const int64_t xbytes = a.in.bytes;
   const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(32, npt) : 1;
   const size_t lds = (size_t)C::S * C::SST + (size_t)C::TN * (sizeof(RqConst) + 4);
   const dim3 grid((unsigned)((T + 7) / 8 * 8)), block(C::NT);
@@ -3326,7 +3326,7 @@ hipError_t launch_tile(const ConvArgs &a, const Geo &geo, hipStream_t s) {
   // unless the filter is the larger read (every XCD then reads all of it):
   // about 7 W extra against (G - 1) X saved.
   const int64_t wbytes = (int64_t)a.in.groups * a.cout * geo.kb_total * 64;
-  const int64_t xbytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
+  const int64_t xbytes = a.in.bytes;
   const int nch = 7 * wbytes < (int64_t)(a.in.groups - 1) * xbytes ? std::min(32, npt) : 1;
   // P workgroups per XCD: all resident slots, no more than the XCD's
   // tiles, and runs of at most npt / nch tiles (two (chunk, combo) segments)
@@ -3359,10 +3359,11 @@ bool stem_pool_applies(const ConvArgs &a, const ActView &po, int k, int stride, 
   if (!stem_rows(a) || a.wo < 1 || a.ho < 1) return false;
   if (k != 3 || stride != 2 || pad != 1) return false;
   if (po.n != a.out.n || po.h != (a.ho + 1) / 2 || po.w != (a.wo + 1) / 2 || po.groups != a.out.groups ||
-      po.cpg != a.out.cpg || po.bits != 2 || po.pixel != a.out.pixel || po.row != a.out.row)
+      po.cpg != a.out.cpg || po.bits != 2 || po.pixel != a.out.pixel || po.row != a.out.row ||
+      po.gstride != po.row)  // the store offsets take a pixel's groups as adjacent rows
     return false;
-  const int64_t in_bytes = (int64_t)a.in.n * a.in.h * a.in.w * a.in.pixel;
-  const int64_t out_bytes = (int64_t)po.n * po.h * po.w * po.pixel;
+  const int64_t in_bytes = a.in.bytes;
+  const int64_t out_bytes = po.bytes;
   const int64_t units = (int64_t)a.out.n * (a.cout / 128) * po.h;
   return (int64_t)a.in.w * a.in.pixel <= sp::RB && in_bytes < 0x7fff0000 && out_bytes < 0x7fff0000 &&
          units < 0x7fffffff;

@@ -39,7 +39,7 @@ __global__ void pack_kernel(const uint8_t *codes, ActView out, int64_t rows, int
   pack_chunk(c, nc, out.bits, words);
   const int per_chunk = out.bits == 3 ? 3 : store_bits(out.bits);
   const int nw = chunk_words_in_row(ci, out.bits, out.row / 4);
-  uint32_t *dst = (uint32_t *)(out.data + r * out.row) + (int64_t)ci * per_chunk;
+  uint32_t *dst = (uint32_t *)row_at(out, r) + (int64_t)ci * per_chunk;
   for (int k = 0; k < nw; ++k) dst[k] = words[k];
 }
 
@@ -50,7 +50,7 @@ __global__ void unpack_kernel(ActView in, uint8_t *codes, int64_t rows, int chun
   const int ci = (int)(t % chunks);
   const int j0 = ci * 32;
   const int nc = min(32, in.cpg - j0);
-  const uint8_t *row = in.data + r * in.row;
+  const uint8_t *row = row_at(in, r);
   uint8_t *dst = codes + r * in.cpg + j0;
   for (int j = 0; j < nc; ++j) dst[j] = (uint8_t)read_code(row, j0 + j, in.bits, in.is_signed);
 }
@@ -224,7 +224,7 @@ __global__ void quantize_kernel(const float *x, float l, float u, const uint32_t
   const float rng = u - l;
   const int off = out.is_signed ? (1 << (out.bits - 1)) : 0;
   const float *src = x + r * out.cpg;
-  uint32_t *dst = (uint32_t *)(out.data + r * out.row);
+  uint32_t *dst = (uint32_t *)row_at(out, r);
   if (out.bits == 3) {
     int c[32];
     const int j0 = wi * 32;
@@ -261,8 +261,8 @@ __global__ void shuffle_kernel(ActView in, int steps, ActView out, int64_t pixel
   const int g = (int)(rem / words);
   const int64_t wi = rem % words;
   const int gd = (g + steps) % in.groups;
-  const uint32_t *src = (const uint32_t *)(in.data + p * in.pixel + g * in.row);
-  uint32_t *dst = (uint32_t *)(out.data + p * out.pixel + gd * out.row);
+  const uint32_t *src = (const uint32_t *)(in.data + p * in.pixel + g * in.gstride);
+  uint32_t *dst = (uint32_t *)(out.data + p * out.pixel + gd * out.gstride);
   dst[wi] = src[wi];
 }
 
@@ -284,14 +284,14 @@ __global__ void channel_shuffle_kernel(ActView in, ActView out, int64_t pixels, 
   for (int j = 0; j < 32; ++j) {
     if (j < n) {
       const int o = gq * C + ci * 32 + j;
-      c[j] = read_code(src + (int64_t)(o % G) * in.row, o / G, in.bits, in.is_signed);
+      c[j] = read_code(src + (int64_t)(o % G) * in.gstride, o / G, in.bits, in.is_signed);
     } else {
       c[j] = 0;
     }
   }
   uint32_t words[8];
   pack_chunk(c, n, out.bits, words);
-  uint32_t *dst = (uint32_t *)(out.data + p * out.pixel + (int64_t)gq * out.row) + (int64_t)ci * (out.bits == 3 ? 3 : store_bits(out.bits));
+  uint32_t *dst = (uint32_t *)(out.data + p * out.pixel + (int64_t)gq * out.gstride) + (int64_t)ci * (out.bits == 3 ? 3 : store_bits(out.bits));
   const int nw = chunk_words_in_row(ci, out.bits, out.row / 4);
   for (int wi = 0; wi < nw; ++wi) dst[wi] = words[wi];
 }
@@ -315,7 +315,7 @@ __global__ void channel_shuffle_words_kernel(ActView in, ActView out, int64_t th
   uint32_t s[G][NW];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    const uint32_t *r = (const uint32_t *)(src + (int64_t)g * in.row);
+    const uint32_t *r = (const uint32_t *)(src + (int64_t)g * in.gstride);
     if constexpr (GB >= 32) {
 #pragma unroll
       for (int j = 0; j < NW; ++j) s[g][j] = r[tl * NW + j];
@@ -356,7 +356,7 @@ __global__ void maxpool_kernel(ActView in, int k, int stride, int pad, ActView o
   const int ox = (int)(p % out.w);
   const int oy = (int)((p / out.w) % out.h);
   const int n = (int)(p / ((int64_t)out.w * out.h));
-  uint32_t *dst = (uint32_t *)(out.data + r * out.row);
+  uint32_t *dst = (uint32_t *)row_at(out, r);
   if (in.bits == 2) {
     uint32_t m = 0;
     for (int ky = 0; ky < k; ++ky) {
@@ -366,7 +366,7 @@ __global__ void maxpool_kernel(ActView in, int k, int stride, int pad, ActView o
         const int ix = ox * stride - pad + kx;
         if (ix < 0 || ix >= in.w) continue;
         const uint32_t *row = (const uint32_t *)(in.data + (((int64_t)n * in.h + iy) * in.w + ix) * in.pixel +
-                                                 (int64_t)g * in.row);
+                                                 (int64_t)g * in.gstride);
         m = max2x16(m, row[wi]);
       }
     }
@@ -385,7 +385,7 @@ __global__ void maxpool_kernel(ActView in, int k, int stride, int pad, ActView o
     for (int kx = 0; kx < k; ++kx) {
       const int ix = ox * stride - pad + kx;
       if (ix < 0 || ix >= in.w) continue;
-      const uint8_t *row = in.data + (((int64_t)n * in.h + iy) * in.w + ix) * in.pixel + g * in.row;
+      const uint8_t *row = in.data + (((int64_t)n * in.h + iy) * in.w + ix) * in.pixel + g * in.gstride;
       for (int j = 0; j < nc; ++j) c[j] = max(c[j], read_code(row, j0 + j, in.bits, 0));
     }
   }
@@ -419,13 +419,13 @@ __global__ void maxpool2_kernel(ActView in, int k, int stride, int pad, ActView 
   for (int iy = ylo; iy < yhi; ++iy)
     for (int ix = xlo; ix < xhi; ++ix) {
       const uint4 v = *(const uint4 *)(in.data + (((int64_t)n * in.h + iy) * in.w + ix) * in.pixel +
-                                       (int64_t)g * in.row + 16 * q);
+                                       (int64_t)g * in.gstride + 16 * q);
       m.x = max2x16(m.x, v.x);
       m.y = max2x16(m.y, v.y);
       m.z = max2x16(m.z, v.z);
       m.w = max2x16(m.w, v.w);
     }
-  *(uint4 *)(out.data + (((int64_t)n * out.h + oy) * out.w + ox) * out.pixel + (int64_t)g * out.row + 16 * q) = m;
+  *(uint4 *)(out.data + (((int64_t)n * out.h + oy) * out.w + ox) * out.pixel + (int64_t)g * out.gstride + 16 * q) = m;
 }
 
 // ------------------------------------------------------------ zero border
@@ -487,7 +487,7 @@ __global__ void avgsum2_kernel(ActView in, int32_t *out) {
   const int g = (int)(r % in.groups);
   const int n = (int)(r / in.groups);
   const int hw = in.h * in.w;
-  const uint8_t *base = in.data + (int64_t)n * hw * in.pixel + (int64_t)g * in.row + 4 * wi;
+  const uint8_t *base = in.data + (int64_t)n * hw * in.pixel + (int64_t)g * in.gstride + 4 * wi;
   uint32_t acc[4] = {0, 0, 0, 0};
   for (int p = 0; p < hw; ++p) {
     const uint32_t w = *(const uint32_t *)(base + (int64_t)p * in.pixel);
@@ -516,7 +516,7 @@ __global__ __launch_bounds__(256) void avgsum2_wg_kernel(ActView in, int32_t *ou
   const int n = (int)(blockIdx.x / in.groups), g = (int)(blockIdx.x % in.groups);
   const int wi = threadIdx.x % wpr, r = threadIdx.x / wpr;
   const int hw = in.h * in.w;
-  const uint8_t *base = in.data + (int64_t)n * hw * in.pixel + (int64_t)g * in.row + 4 * wi;
+  const uint8_t *base = in.data + (int64_t)n * hw * in.pixel + (int64_t)g * in.gstride + 4 * wi;
   uint32_t acc[4] = {0, 0, 0, 0};
   for (int p = r; p < hw; p += R) {
     const uint32_t w = *(const uint32_t *)(base + (int64_t)p * in.pixel);
@@ -557,7 +557,7 @@ __global__ void avgsum_kernel(ActView in, int32_t *out) {
   int32_t s = 0;
   const int64_t hw = (int64_t)in.h * in.w;
   for (int64_t p = 0; p < hw; ++p)
-    s += read_code(in.data + ((int64_t)n * hw + p) * in.pixel + g * in.row, j, in.bits, 0);
+    s += read_code(in.data + ((int64_t)n * hw + p) * in.pixel + g * in.gstride, j, in.bits, 0);
   out[t] = s;
 }
 
@@ -825,13 +825,15 @@ hipError_t launch_shuffle(const ActView &in, int32_t steps, const ActView &out, 
 
 // The word-level build: b in {2, 4, 8}, rows without padding (C a multiple
 // of the codes per word), a pixel a whole number of 16-byte stores, G a
-// power of two up to 16 and both tensors 16-byte aligned.
+// power of two up to 16, both tensors in the pixel layout and 16-byte
+// aligned.
 static bool channel_shuffle_words(const ActView &in, const ActView &out) {
   const int b = in.bits, G = in.groups;
   if (b != 2 && b != 4 && b != 8) return false;
   if (G != 2 && G != 4 && G != 8 && G != 16) return false;
   const int F = 32 / b;
-  return in.cpg % F == 0 && ((int64_t)G * in.cpg) % (4 * F) == 0 && out.pixel == in.pixel &&
+  return in.cpg % F == 0 && ((int64_t)G * in.cpg) % (4 * F) == 0 && in.gstride == in.row &&
+         out.gstride == out.row && out.pixel == in.pixel &&
          (((uintptr_t)in.data | (uintptr_t)out.data) & 15u) == 0 &&
          (int64_t)G * in.cpg / (4 * F) < ((int64_t)1 << 30);
 }

@@ -39,6 +39,8 @@ palq_status check_act(palq_ctx *ctx, const palq_act *a, const char *what) {
   if (!valid_bits(a->bits)) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": bits not in {2,3,4,6,8}");
   if (a->is_signed != 0 && a->is_signed != 1)
     return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": is_signed must be 0 or 1");
+  if (a->layout != PALQ_LAYOUT_PIXEL && a->layout != PALQ_LAYOUT_GROUP)
+    return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": layout must be PALQ_LAYOUT_PIXEL or PALQ_LAYOUT_GROUP");
   const int64_t row = row_bytes(a->ch_per_group, a->bits);
   const double bytes = (double)a->n * a->h * a->w * a->groups * (double)row;
   if (bytes > 9.0e18) return fail(ctx, PALQ_ERR_ARG, std::string(what) + ": tensor too large");

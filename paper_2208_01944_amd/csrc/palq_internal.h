@@ -31,12 +31,16 @@ __host__ __device__ inline bool row_exact(int64_t codes, int bits) {
   return (codes * (bits == 6 ? 8 : bits)) % 32 == 0;
 }
 
-// Device view of an activation tensor.
+// Device view of an activation tensor.  Row (pixel p, group g) starts at
+// data + p * pixel + g * gstride: the pixel layout has pixel = groups * row,
+// gstride = row; the group layout pixel = row, gstride = pixels * row.
 struct ActView {
   uint8_t *data;
   int32_t n, h, w, groups, cpg, bits, is_signed;
-  int64_t row;    // bytes per (pixel, group) row
-  int64_t pixel;  // bytes per pixel = groups * row
+  int64_t row;      // bytes per (pixel, group) row
+  int64_t pixel;    // bytes from one pixel's row to the next pixel's (same group)
+  int64_t gstride;  // bytes from one group's row to the next group's (same pixel)
+  int64_t bytes;    // the whole tensor
 };
 
 inline ActView view_of(const palq_act *a) {
@@ -46,8 +50,22 @@ inline ActView view_of(const palq_act *a) {
   v.groups = a->groups; v.cpg = a->ch_per_group;
   v.bits = a->bits; v.is_signed = a->is_signed;
   v.row = row_bytes(a->ch_per_group, a->bits);
-  v.pixel = v.row * a->groups;
+  const int64_t pixels = (int64_t)a->n * a->h * a->w;
+  if (a->layout == PALQ_LAYOUT_GROUP) {
+    v.pixel = v.row;
+    v.gstride = v.row * pixels;
+  } else {
+    v.pixel = v.row * a->groups;
+    v.gstride = v.row;
+  }
+  v.bytes = v.row * a->groups * pixels;
   return v;
+}
+
+// Start of row r of a view, rows counted pixel by pixel (r = p * groups + g).
+__host__ __device__ inline uint8_t *row_at(const ActView &v, int64_t r) {
+  const int64_t p = r / v.groups, g = r - p * v.groups;
+  return v.data + p * v.pixel + g * v.gstride;
 }
 
 // ----------------------------------------------------------------- conv

@@ -116,6 +116,8 @@ int64_t act_bytes(const palq_act &a) {
 // View tensor t as `groups` rows of cpg codes (same data, same bits).
 bool regroup(const palq_act &t, int groups, int cpg, palq_act *out) {
   if ((int64_t)t.groups * t.ch_per_group != (int64_t)groups * cpg) return false;
+  // a group-layout tensor keeps each group's rows apart: no other split
+  if (t.layout == PALQ_LAYOUT_GROUP && t.groups != groups) return false;
   if (t.groups != groups && !(row_exact(t.ch_per_group, t.bits) && row_exact(cpg, t.bits)))
     return false;
   *out = t;
@@ -181,7 +183,8 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
     rotate[i] = 1;
   }
   const palq_layer *layers = norm.data();
-  if (flags & ~(PALQ_NET_KEEP_ALL | PALQ_NET_TIMING | PALQ_NET_GRAPH)) return net_fail(ctx, PALQ_ERR_ARG, "unknown flags");
+  if (flags & ~(PALQ_NET_KEEP_ALL | PALQ_NET_TIMING | PALQ_NET_GRAPH | PALQ_NET_PIXEL_LAYOUT))
+    return net_fail(ctx, PALQ_ERR_ARG, "unknown flags");
   if ((flags & PALQ_NET_TIMING) && (flags & PALQ_NET_GRAPH))
     return net_fail(ctx, PALQ_ERR_ARG, "PALQ_NET_GRAPH does not go with PALQ_NET_TIMING");
   if (input->n < 1 || input->h < 1 || input->w < 1 || input->groups < 1 || input->ch_per_group < 1 ||
@@ -335,6 +338,32 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
   if (st != PALQ_OK) {
     free_net(net);
     return net_fail(ctx, st, err);
+  }
+  // ---- tensor layouts: a conv output of several groups whose every reader
+  // takes it with those groups is stored group by group
+  // (PALQ_LAYOUT_GROUP), so that a tile of one group's pixels is one
+  // contiguous run for the conv operand fetches, shortcut reads and stores
+  if (!(flags & PALQ_NET_PIXEL_LAYOUT)) {
+    std::vector<char> by_conv(net->tensors.size(), 0), split(net->tensors.size(), 0);
+    for (int i = 0; i < n_layers; ++i) {
+      const palq_layer &L = layers[i];
+      if (L.op != PALQ_OP_CONV) continue;
+      by_conv[L.dst] = 1;
+      if (L.w.groups != net->tensors[L.src].d.groups) split[L.src] = 1;
+      if (L.res_src >= 0 && L.w.groups != net->tensors[L.res_src].d.groups) split[L.res_src] = 1;
+      if (L.proj_src >= 0 && L.proj_w.groups != net->tensors[L.proj_src].d.groups) split[L.proj_src] = 1;
+    }
+    for (size_t t = 1; t < net->tensors.size(); ++t) {
+      Tensor &T = net->tensors[t];
+      if (T.exists && T.kind == kCodes && by_conv[t] && !split[t] && T.d.groups > 1) T.d.layout = PALQ_LAYOUT_GROUP;
+    }
+    for (int i = 0; i < n_layers; ++i) {
+      const palq_layer &L = layers[i];
+      Layer &NL = net->layers[i];
+      if (L.op != PALQ_OP_CONV) continue;
+      NL.in_view.layout = net->tensors[L.src].d.layout;
+      NL.out_view.layout = net->tensors[L.dst].d.layout;
+    }
   }
   net->input = *input;  // palq_forward_image's input format
   net->img_input = input->bits == 8 && input->is_signed && input->groups == 1 && input->ch_per_group == 3;

@@ -30,12 +30,14 @@ c_i32, c_i64, c_p, c_f = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes
 
 OK, ERR_ARG, ERR_UNSUPPORTED, ERR_OVERFLOW, ERR_DEVICE, ERR_NOMEM = 0, -1, -2, -3, -4, -5
 OP_CONV, OP_MAXPOOL, OP_AVGSUM, OP_FC, OP_SHUFFLE_MODULE, OP_CHANNEL_SHUFFLE = 1, 2, 3, 4, 5, 6
-NET_KEEP_ALL, NET_TIMING, NET_GRAPH = 1, 2, 4
+NET_KEEP_ALL, NET_TIMING, NET_GRAPH, NET_PIXEL_LAYOUT = 1, 2, 4, 8
+LAYOUT_PIXEL, LAYOUT_GROUP = 0, 1
 
 
 class Act(ctypes.Structure):
     _fields_ = [("n", c_i32), ("h", c_i32), ("w", c_i32), ("groups", c_i32),
-                ("ch_per_group", c_i32), ("bits", c_i32), ("is_signed", c_i32), ("data", c_p)]
+                ("ch_per_group", c_i32), ("bits", c_i32), ("is_signed", c_i32), ("layout", c_i32),
+                ("data", c_p)]
 
 
 class Filter(ctypes.Structure):
@@ -134,8 +136,8 @@ def version() -> str:
     return _version().decode()
 
 
-def make_act(n, h, w, groups, cpg, bits, signed=False, data=0) -> Act:
-    return Act(n, h, w, groups, cpg, bits, int(bool(signed)), data)
+def make_act(n, h, w, groups, cpg, bits, signed=False, data=0, layout=LAYOUT_PIXEL) -> Act:
+    return Act(n, h, w, groups, cpg, bits, int(bool(signed)), layout, data)
 
 
 def act_bytes(a: Act) -> int:
@@ -211,8 +213,8 @@ class Context:
         self._check(_set_conv_bitdecomp(self.h, int(bool(enable))))
 
     # ----------------------------------------------------------- memory
-    def empty_act(self, n, h, w, groups, cpg, bits, signed=False) -> Tensor:
-        a = make_act(n, h, w, groups, cpg, bits, signed)
+    def empty_act(self, n, h, w, groups, cpg, bits, signed=False, layout=LAYOUT_PIXEL) -> Tensor:
+        a = make_act(n, h, w, groups, cpg, bits, signed, layout=layout)
         nb = act_bytes(a)
         if nb < 0:
             raise PalqError(ERR_ARG, "invalid activation descriptor")
@@ -225,10 +227,10 @@ class Context:
         return t.to(self.dev)
 
     # ----------------------------------------------------------- layout
-    def pack(self, codes, groups, bits, signed=False) -> Tensor:
+    def pack(self, codes, groups, bits, signed=False, layout=LAYOUT_PIXEL) -> Tensor:
         """codes: numpy [n, h, w, groups*cpg] integer codes -> packed device tensor."""
         n, h, w, c = codes.shape
-        out = self.empty_act(n, h, w, groups, c // groups, bits, signed)
+        out = self.empty_act(n, h, w, groups, c // groups, bits, signed, layout=layout)
         dt = np.int8 if signed else np.uint8
         src = self.upload(np.asarray(codes).astype(dt))
         self._check(_pack(self.h, src.data_ptr(), ctypes.byref(out.act)))

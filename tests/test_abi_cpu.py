@@ -154,6 +154,15 @@ def test_validate_only_other_calls(P, vctx):
     assert P._fc(vctx.h, _fake(9), 4, 128, _fake(11), 10, _fake(12)) == P.OK
     assert P._fc(vctx.h, _fake(9), 4, 0, _fake(11), 10, _fake(12)) == P.ERR_ARG
     assert P._pack(vctx.h, None, ctypes.byref(a)) == P.ERR_ARG
+    # layouts: either is taken, any other value is an argument error
+    g = _act(P, slot=13)
+    g.layout = P.LAYOUT_GROUP
+    assert P._shuffle(vctx.h, ctypes.byref(a), 3, ctypes.byref(g)) == P.OK
+    assert P._maxpool(vctx.h, ctypes.byref(g), 3, 2, 1, ctypes.byref(pooled)) == P.OK
+    g.layout = 2
+    assert P._shuffle(vctx.h, ctypes.byref(a), 3, ctypes.byref(g)) == P.ERR_ARG
+    assert "layout" in vctx.last_error()
+    assert P._avgsum(vctx.h, ctypes.byref(g), _fake(9)) == P.ERR_ARG
     assert P._set_conv_fp4(vctx.h, 0) == P.OK
     assert P._set_conv_fp4(vctx.h, 1) == P.OK
     assert P._set_conv_fp4(vctx.h, 2) == P.ERR_ARG
@@ -235,7 +244,7 @@ def test_validate_only_forward_image(P, vctx):
     assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 3, P.NET_GRAPH, ctypes.byref(h)) == P.OK
     P._net_destroy(h)
     assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 3, P.NET_GRAPH | P.NET_TIMING, ctypes.byref(h)) == P.ERR_ARG
-    assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 3, 8, ctypes.byref(h)) == P.ERR_ARG  # unknown flag
+    assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 3, 16, ctypes.byref(h)) == P.ERR_ARG  # unknown flag
 
 
 def test_validate_only_shuffle_module(P, vctx):

@@ -58,6 +58,30 @@ def test_resnet18_small_all_tensors(ctx, torch, variant):
     np.testing.assert_array_equal(logits, ref)
 
 
+def test_resnet18_group_layout_matches_pixel_layout(ctx, torch):
+    """The network stores a conv output of several groups that every reader
+    takes with those groups in the group layout (default); with
+    PALQ_NET_PIXEL_LAYOUT it keeps the pixel layout.  Both give the oracle's
+    tensors and logits."""
+    from paper_2208_01944_amd import palq
+    say("resnet18 hw=64 n=2 G=4 b=2 centred, group vs pixel layout")
+    spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=12)
+    spec = O.calibrate_centring(spec, spec["x"])
+    ref, tensors, _ = O.run_net(spec, spec["x"], keep=True)
+    xt = ctx.pack(spec["x"], 1, 8, signed=True)
+    for flags, want in ((palq.NET_KEEP_ALL, palq.LAYOUT_GROUP),
+                        (palq.NET_KEEP_ALL | palq.NET_PIXEL_LAYOUT, palq.LAYOUT_PIXEL)):
+        net = palq.Net(ctx, spec, flags=flags)
+        logits = torch.empty(2 * net.classes, dtype=torch.int32, device=ctx.dev)
+        net.forward(xt.buf, logits)
+        ctx.sync()
+        for L in spec["layers"]:
+            if L["op"] == "conv" and L["w"].shape[0] > 1:
+                assert net.tensor(L["dst"]).act.layout == want, (flags, L["dst"])
+        compare_tensors(ctx, net, spec, tensors, slice(None))
+        np.testing.assert_array_equal(logits.cpu().numpy().astype(np.int64).reshape(2, -1), ref)
+
+
 def test_resnet18_small_int8_matrix_cores(ctx, torch):
     say("resnet18 hw=64 n=2 G=4 b=2 centred, int8 only")
     spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=14)

@@ -34,23 +34,32 @@ def torch():
 
 
 # ---------------------------------------------------------------- layout
+def group_major(packed, pixels, groups):
+    """Pixel-layout packed bytes [pixels][groups][row] reordered to the group
+    layout [groups][pixels][row]."""
+    return np.asarray(packed).reshape(pixels, groups, -1).transpose(1, 0, 2).reshape(-1)
+
+
 @pytest.mark.parametrize("bits", [2, 3, 4, 8])
 @pytest.mark.parametrize("cpg", [1, 5, 16, 37, 64, 96])
-def test_pack_bytes_match_reference(ctx, bits, cpg):
-    say(f"pack bits={bits} cpg={cpg}")
+@pytest.mark.parametrize("layout", [0, 1])
+def test_pack_bytes_match_reference(ctx, bits, cpg, layout):
+    say(f"pack bits={bits} cpg={cpg} layout={layout}")
     g = np.random.default_rng(bits * 100 + cpg)
     for signed in (False, True):
         x = I.codes(g, (2, 3, 5, 3 * cpg), bits, signed).astype(np.int64)
-        t = ctx.pack(x, 3, bits, signed)
+        t = ctx.pack(x, 3, bits, signed, layout=layout)
         got = t.buf[:packref.row_bytes(cpg, bits) * 2 * 3 * 5 * 3].cpu().numpy()
-        np.testing.assert_array_equal(got, packref.pack(x, 3, bits))
+        ref = packref.pack(x, 3, bits)
+        np.testing.assert_array_equal(got, group_major(ref, 2 * 3 * 5, 3) if layout else ref)
         np.testing.assert_array_equal(ctx.unpack(t), x)
 
 
 # ---------------------------------------------------------------- quantiser
 @pytest.mark.parametrize("bits,signed", [(2, False), (3, False), (4, False), (8, True), (2, True)])
-def test_quantize_matches_oracle(ctx, torch, bits, signed):
-    say(f"quantize bits={bits} signed={signed}")
+@pytest.mark.parametrize("layout", [0, 1])
+def test_quantize_matches_oracle(ctx, torch, bits, signed, layout):
+    say(f"quantize bits={bits} signed={signed} layout={layout}")
     g = np.random.default_rng(bits)
     x = g.normal(0, 1.5, (3, 17, 11, 2 * 21)).astype(np.float32)
     x.flat[::97] = np.nan
@@ -59,7 +68,7 @@ def test_quantize_matches_oracle(ctx, torch, bits, signed):
     # exact ties of Eq. 2 for l=0, u=3 at 2 bits
     x.flat[:3] = [0.5, 1.5, 2.5]
     xd = ctx.upload(x)
-    out = ctx.empty_act(3, 17, 11, 2, 21, bits, signed)
+    out = ctx.empty_act(3, 17, 11, 2, 21, bits, signed, layout=layout)
     rng = torch.empty(2, dtype=torch.float32, device=ctx.dev)
     ctx.quantize(xd, -2.0, 3.0, out, rng)
     np.testing.assert_array_equal(ctx.unpack(out), O.quantize(x, -2.0, 3.0, bits, signed))
@@ -73,8 +82,9 @@ def test_quantize_matches_oracle(ctx, torch, bits, signed):
 
 
 # ---------------------------------------------------------------- conv
-def run_conv(ctx, torch, case, centred=False):
-    """Runs a single_layer() case on the GPU; returns (codes, acc, ref_codes, ref_acc)."""
+def run_conv(ctx, torch, case, centred=False, layout=(0, 0, 0)):
+    """Runs a single_layer() case on the GPU; returns (codes, acc, ref_codes,
+    ref_acc).  layout: the (input, output, shortcut input) tensor layouts."""
     L = case["layer"]
     x = case["x"]
     G, co, kh, kw, ci = L["w"].shape
@@ -94,20 +104,20 @@ def run_conv(ctx, torch, case, centred=False):
                                   L["out_bits"], L["shuffle"], res=res, res_mult=L["res_mult"],
                                   proj_x=px, proj_w=L["proj_w"], proj_stride=L["proj_stride"])
     in_signed = bool(L["in_signed"])
-    xt = ctx.pack(x, G, L["in_bits"], in_signed)
+    xt = ctx.pack(x, G, L["in_bits"], in_signed, layout=layout[0])
     wt, wf = ctx.pack_filter(L["w"], L["w_bits"])
     n, h, w, _ = x.shape
     ho = (h + 2 * L["pad"] - kh) // L["stride"] + 1
     wo = (w + 2 * L["pad"] - kw) // L["stride"] + 1
-    out = ctx.empty_act(n, ho, wo, G, co, L["out_bits"])
+    out = ctx.empty_act(n, ho, wo, G, co, L["out_bits"], layout=layout[1])
     dump = torch.zeros(max(n * ho * wo * G * co, 4), dtype=torch.int32, device=ctx.dev)
     i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
     kw_ = {}
     if res is not None:
-        kw_["identity"] = ctx.pack(res, G, L["out_bits"])
+        kw_["identity"] = ctx.pack(res, G, L["out_bits"], layout=layout[2])
         kw_["res_mult"] = i32(L["res_mult"])
     if px is not None:
-        kw_["proj_in"] = ctx.pack(px, G, L["in_bits"])
+        kw_["proj_in"] = ctx.pack(px, G, L["in_bits"], layout=layout[2])
         pt, kw_["proj_w"] = ctx.pack_filter(L["proj_w"], L["w_bits"])
         kw_["proj_stride"] = L["proj_stride"]
     # without the accumulator dump (the kernels' common-case epilogue) ...
@@ -125,8 +135,8 @@ def run_conv(ctx, torch, case, centred=False):
     return q, acc, ref_q, ref_acc
 
 
-def check_conv(ctx, torch, case, centred=False, spread=False):
-    q, acc, rq, racc = run_conv(ctx, torch, case, centred)
+def check_conv(ctx, torch, case, centred=False, spread=False, layout=(0, 0, 0)):
+    q, acc, rq, racc = run_conv(ctx, torch, case, centred, layout)
     np.testing.assert_array_equal(acc, racc)
     np.testing.assert_array_equal(q, rq)
     if spread:  # the centred variant must exercise every output code
@@ -178,6 +188,16 @@ def test_conv_cases(ctx, torch, i, shuffle):
     say(f"conv case {i} {p} shuffle={shuffle}")
     case = I.single_layer(1000 + i, shuffle=shuffle, **p)
     check_conv(ctx, torch, case, centred=(shuffle == 1))
+
+
+@pytest.mark.parametrize("i", range(len(CONV_CASES)))
+@pytest.mark.parametrize("layout", [(1, 1, 1), (0, 1, 0), (1, 0, 1)])
+def test_conv_cases_group_layout(ctx, torch, i, layout):
+    """Every conv case with its tensors in the group layout (and mixed)."""
+    p = dict(CONV_CASES[i])
+    say(f"conv case {i} {p} layouts={layout}")
+    case = I.single_layer(1000 + i, shuffle=1, **p)
+    check_conv(ctx, torch, case, centred=True, layout=layout)
 
 
 @pytest.mark.parametrize("i", [0, 1, 2, 3, 5, 9, 10])
@@ -502,28 +522,31 @@ def test_conv_deterministic(ctx, torch):
 
 # ---------------------------------------------------------------- shuffle & glue
 @pytest.mark.parametrize("bits", [2, 3, 4, 8])
-def test_cyclic_shuffle(ctx, bits):
-    say(f"shuffle bits={bits}")
+@pytest.mark.parametrize("layout", [(0, 0), (1, 1), (1, 0)])
+def test_cyclic_shuffle(ctx, bits, layout):
+    say(f"shuffle bits={bits} layouts={layout}")
     g = np.random.default_rng(bits)
     x = I.codes(g, (2, 5, 4, 4 * 40), bits, False).astype(np.int64)
-    t = ctx.pack(x, 4, bits)
-    out = ctx.empty_act(2, 5, 4, 4, 40, bits)
+    t = ctx.pack(x, 4, bits, layout=layout[0])
+    out = ctx.empty_act(2, 5, 4, 4, 40, bits, layout=layout[1])
     for s in (0, 1, 3, 4, -1, 9):
         ctx.cyclic_shuffle(t, s, out)
         np.testing.assert_array_equal(ctx.unpack(out), O.cyclic_permute(x, 4, s))
 
 
 @pytest.mark.parametrize("bits,cpg", [(2, 48), (2, 21), (3, 48), (4, 48), (4, 7)])
-def test_maxpool_avgsum_fc(ctx, torch, bits, cpg):
-    say(f"maxpool/avgsum/fc bits={bits} cpg={cpg}")
+@pytest.mark.parametrize("layout", [(0, 0), (1, 1), (0, 1)])
+def test_maxpool_avgsum_fc(ctx, torch, bits, cpg, layout):
+    say(f"maxpool/avgsum/fc bits={bits} cpg={cpg} layouts={layout}")
     g = np.random.default_rng(bits)
     x = I.codes(g, (3, 13, 12, 2 * cpg), bits, False).astype(np.int64)
-    t = ctx.pack(x, 2, bits)
-    out = ctx.empty_act(3, 7, 6, 2, cpg, bits)
+    t = ctx.pack(x, 2, bits, layout=layout[0])
+    out = ctx.empty_act(3, 7, 6, 2, cpg, bits, layout=layout[1])
     ctx.maxpool(t, 3, 2, 1, out)
     np.testing.assert_array_equal(ctx.unpack(out), O.maxpool(x, 3, 2, 1))
     got = out.buf.cpu().numpy()[:3 * 7 * 6 * 2 * packref.row_bytes(cpg, bits)]
-    np.testing.assert_array_equal(got, packref.pack(O.maxpool(x, 3, 2, 1), 2, bits))  # zero padding
+    ref = packref.pack(O.maxpool(x, 3, 2, 1), 2, bits)
+    np.testing.assert_array_equal(got, group_major(ref, 3 * 7 * 6, 2) if layout[1] else ref)  # zero padding
     C = 2 * cpg
     sums = torch.empty(3 * C, dtype=torch.int32, device=ctx.dev)
     ctx.avgsum(t, sums)
@@ -537,17 +560,18 @@ def test_maxpool_avgsum_fc(ctx, torch, bits, cpg):
 
 
 @pytest.mark.parametrize("cpg,h,w", [(64, 9, 9), (16, 5, 17), (128, 7, 7), (64, 12, 11), (48, 7, 7), (512, 3, 5), (2048, 2, 2), (4096, 1, 3)])
-def test_maxpool_avgsum_2bit_vector_paths(ctx, torch, cpg, h, w):
+@pytest.mark.parametrize("layout", [0, 1])
+def test_maxpool_avgsum_2bit_vector_paths(ctx, torch, cpg, h, w, layout):
     """2-bit rows of a multiple of 16 bytes take the vector max pool; at
     most 85 pixels take the byte-lane global sum (85 x 3 = 255 is the
     largest sum a byte holds; 12 x 11 = 132 pixels takes the other path)."""
-    say(f"2-bit maxpool/avgsum cpg={cpg} {h}x{w}")
+    say(f"2-bit maxpool/avgsum cpg={cpg} {h}x{w} layout={layout}")
     g = np.random.default_rng(cpg + h)
     x = I.codes(g, (3, h, w, 2 * cpg), 2, False).astype(np.int64)
     x[1] = 3  # every code at its maximum: sums reach 3 * h * w
-    t = ctx.pack(x, 2, 2)
+    t = ctx.pack(x, 2, 2, layout=layout)
     ho, wo = O.out_size(h, 3, 2, 1), O.out_size(w, 3, 2, 1)
-    out = ctx.empty_act(3, ho, wo, 2, cpg, 2)
+    out = ctx.empty_act(3, ho, wo, 2, cpg, 2, layout=layout)
     ctx.maxpool(t, 3, 2, 1, out)
     np.testing.assert_array_equal(ctx.unpack(out), O.maxpool(x, 3, 2, 1))
     sums = torch.empty(3 * 2 * cpg, dtype=torch.int32, device=ctx.dev)
@@ -632,12 +656,13 @@ CHANNEL_SHUFFLE_CASES = [
 
 
 @pytest.mark.parametrize("bits,G,C,shape", CHANNEL_SHUFFLE_CASES)
-def test_channel_shuffle_matches_oracle(ctx, bits, G, C, shape):
-    say(f"channel shuffle b={bits} G={G} C={C} shape={shape}")
+@pytest.mark.parametrize("layout", [(0, 0), (1, 1), (1, 0)])
+def test_channel_shuffle_matches_oracle(ctx, bits, G, C, shape, layout):
+    say(f"channel shuffle b={bits} G={G} C={C} shape={shape} layouts={layout}")
     g = np.random.default_rng(bits * 100 + G * 10 + C)
     x = I.codes(g, shape + (G * C,), bits, False).astype(np.int64)
-    xt = ctx.pack(x, G, bits)
-    out = ctx.empty_act(*shape, G, C, bits)
+    xt = ctx.pack(x, G, bits, layout=layout[0])
+    out = ctx.empty_act(*shape, G, C, bits, layout=layout[1])
     ctx.channel_shuffle(xt, out)
     ctx.sync()
     np.testing.assert_array_equal(ctx.unpack(out), O.channel_shuffle(x, G))
