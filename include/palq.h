@@ -332,9 +332,11 @@ palq_status palq_fc(palq_ctx *ctx, const int32_t *x, int32_t n, int32_t cin, con
                              * u, stream) and replay it; input contents may
                              * change between calls.  Not with PALQ_NET_TIMING. */
 #define PALQ_NET_PIXEL_LAYOUT 8 /* keep every tensor in PALQ_LAYOUT_PIXEL; by
-                                 * default a conv output of several groups
-                                 * whose every reader takes it with those
-                                 * groups is stored in PALQ_LAYOUT_GROUP */
+                                 * default a conv, channel shuffle or max pool
+                                 * output of several groups whose every reader
+                                 * takes it with those groups is stored in
+                                 * PALQ_LAYOUT_GROUP (palq_net_tensor reports
+                                 * each tensor's layout) */
 
 /* One layer of a network.  Tensor ids: 0 is the network input; each layer
  * writes a new id `dst` larger than every id before it.  Every pointer in

@@ -331,7 +331,10 @@ __global__ void channel_shuffle_words_kernel(ActView in, ActView out, int64_t th
     const uint32_t v = (s[g][(i * B) / 32] >> ((i * B) % 32)) & mask;
     o[f / F] |= v << ((f % F) * B);
   }
-  *(uint4 *)(out.data + 16 * t) = make_uint4(o[0], o[1], o[2], o[3]);
+  // bytes 16 tl .. of the pixel's G rows: row gq, 16-byte aligned inside it
+  const int b = 16 * tl, gq = b / (int)out.row;
+  *(uint4 *)(out.data + p * out.pixel + gq * out.gstride + (b - gq * (int)out.row)) =
+      make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 // ------------------------------------------------------------ max pool
@@ -824,16 +827,18 @@ hipError_t launch_shuffle(const ActView &in, int32_t steps, const ActView &out, 
 }
 
 // The word-level build: b in {2, 4, 8}, rows without padding (C a multiple
-// of the codes per word), a pixel a whole number of 16-byte stores, G a
-// power of two up to 16, both tensors in the pixel layout and 16-byte
-// aligned.
+// of the codes per word), a pixel a whole number of 16-byte stores (in the
+// group layout, each row), G a power of two up to 16 and both tensors
+// 16-byte aligned.
 static bool channel_shuffle_words(const ActView &in, const ActView &out) {
   const int b = in.bits, G = in.groups;
   if (b != 2 && b != 4 && b != 8) return false;
   if (G != 2 && G != 4 && G != 8 && G != 16) return false;
   const int F = 32 / b;
-  return in.cpg % F == 0 && ((int64_t)G * in.cpg) % (4 * F) == 0 && in.gstride == in.row &&
-         out.gstride == out.row && out.pixel == in.pixel &&
+  // a pixel's output rows are one run in the pixel layout; in the group
+  // layout every 16-byte store must stay inside one row
+  const bool run = out.gstride == out.row;
+  return in.cpg % F == 0 && ((int64_t)G * in.cpg) % (4 * F) == 0 && (run || out.row % 16 == 0) &&
          (((uintptr_t)in.data | (uintptr_t)out.data) & 15u) == 0 &&
          (int64_t)G * in.cpg / (4 * F) < ((int64_t)1 << 30);
 }
@@ -857,7 +862,7 @@ static hipError_t launch_channel_shuffle_words(const ActView &in, const ActView 
 hipError_t launch_channel_shuffle(const ActView &in, const ActView &out, hipStream_t s) {
   const int64_t pixels = (int64_t)in.n * in.h * in.w;
   if (pixels > 0 && channel_shuffle_words(in, out)) {
-    const int tpp = (int)(in.pixel / 16);
+    const int tpp = (int)(in.row * in.groups / 16);
     const int64_t threads = pixels * tpp;
     if (in.bits == 2) return launch_channel_shuffle_words<2>(in, out, threads, tpp, s);
     if (in.bits == 4) return launch_channel_shuffle_words<4>(in, out, threads, tpp, s);

@@ -339,23 +339,25 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
     free_net(net);
     return net_fail(ctx, st, err);
   }
-  // ---- tensor layouts: a conv output of several groups whose every reader
-  // takes it with those groups is stored group by group
+  // ---- tensor layouts: a conv, channel shuffle or max pool output of
+  // several groups whose every reader takes it with those groups is stored
+  // group by group
   // (PALQ_LAYOUT_GROUP), so that a tile of one group's pixels is one
   // contiguous run for the conv operand fetches, shortcut reads and stores
   if (!(flags & PALQ_NET_PIXEL_LAYOUT)) {
-    std::vector<char> by_conv(net->tensors.size(), 0), split(net->tensors.size(), 0);
+    std::vector<char> grouped_out(net->tensors.size(), 0), split(net->tensors.size(), 0);
     for (int i = 0; i < n_layers; ++i) {
       const palq_layer &L = layers[i];
+      if (L.op == PALQ_OP_CHANNEL_SHUFFLE || L.op == PALQ_OP_MAXPOOL) grouped_out[L.dst] = 1;
       if (L.op != PALQ_OP_CONV) continue;
-      by_conv[L.dst] = 1;
+      grouped_out[L.dst] = 1;
       if (L.w.groups != net->tensors[L.src].d.groups) split[L.src] = 1;
       if (L.res_src >= 0 && L.w.groups != net->tensors[L.res_src].d.groups) split[L.res_src] = 1;
       if (L.proj_src >= 0 && L.proj_w.groups != net->tensors[L.proj_src].d.groups) split[L.proj_src] = 1;
     }
     for (size_t t = 1; t < net->tensors.size(); ++t) {
       Tensor &T = net->tensors[t];
-      if (T.exists && T.kind == kCodes && by_conv[t] && !split[t] && T.d.groups > 1) T.d.layout = PALQ_LAYOUT_GROUP;
+      if (T.exists && T.kind == kCodes && grouped_out[t] && !split[t] && T.d.groups > 1) T.d.layout = PALQ_LAYOUT_GROUP;
     }
     for (int i = 0; i < n_layers; ++i) {
       const palq_layer &L = layers[i];
