@@ -35,20 +35,20 @@ def centred(case):
 class Layer:
     """Device copies of one single_layer() case for repeated calls."""
 
-    def __init__(self, ctx, torch, case, bias):
+    def __init__(self, ctx, torch, case, bias, layout=0):
         L = case["layer"]
-        self.ctx, self.case = ctx, case
+        self.ctx, self.case, self.layout = ctx, case, layout
         G, co, kh, kw, ci = L["w"].shape
         n, h, w, _ = case["x"].shape
         self.ho = (h + 2 * L["pad"] - kh) // L["stride"] + 1
         self.wo = (w + 2 * L["pad"] - kw) // L["stride"] + 1
-        self.xt = ctx.pack(case["x"], G, L["in_bits"])
+        self.xt = ctx.pack(case["x"], G, L["in_bits"], layout=layout)
         self.wt, self.wf = ctx.pack_filter(L["w"], L["w_bits"])
         i32 = lambda a: ctx.upload(np.asarray(a, np.int32))
         self.rq = (i32(L["mult"]), i32(L["shift"]), i32(bias))
         self.kw = {}
         if L["res"] >= 0:
-            self.kw["identity"] = ctx.pack(case["extra"][1], G, L["out_bits"])
+            self.kw["identity"] = ctx.pack(case["extra"][1], G, L["out_bits"], layout=layout)
             self.kw["res_mult"] = i32(L["res_mult"])
         self.shape = (n, self.ho, self.wo, G * co)
         self.nout = n * self.ho * self.wo * G * co
@@ -56,7 +56,8 @@ class Layer:
 
     def outputs(self, torch):
         L = self.case["layer"]
-        out = self.ctx.empty_act(self.shape[0], self.ho, self.wo, self.G, self.co, L["out_bits"])
+        out = self.ctx.empty_act(self.shape[0], self.ho, self.wo, self.G, self.co, L["out_bits"],
+                                 layout=self.layout)
         dump = torch.full((self.nout,), -7, dtype=torch.int32, device=self.ctx.dev)
         return out, dump
 
@@ -70,19 +71,21 @@ class Layer:
         return self.ctx.unpack(out), dump.cpu().numpy().astype(np.int64).reshape(self.shape)
 
 
-def test_noalloc_matches_group_conv_two_calls():
+@pytest.mark.parametrize("layout", [0, 1])
+def test_noalloc_matches_group_conv_two_calls(layout):
     """Two no-alloc calls in a row, the second with a smaller input (and
     another filter, so the static buffer's previous contents would show):
-    codes and accumulators equal palq_group_conv's and the oracle's."""
+    codes and accumulators equal palq_group_conv's and the oracle's, with
+    the tensors in the pixel (0) and the group (1) layout."""
     import torch
     from paper_2208_01944_amd import palq
     ctx = palq.Context(0)
     cases = [I.single_layer(3101, n=8, h=28, w=28, groups=4, cin=128, cout=128, shuffle=1),
              I.single_layer(3102, n=2, h=14, w=14, groups=4, cin=64, cout=64, shuffle=3, residual="identity")]
     for i, case in enumerate(cases):
-        say(f"no-alloc call {i}: x {case['x'].shape}")
+        say(f"no-alloc call {i}: x {case['x'].shape} layout {layout}")
         bias, q_ref, acc_ref = centred(case)
-        lay = Layer(ctx, torch, case, bias)
+        lay = Layer(ctx, torch, case, bias, layout)
         out_n, dump_n = lay.outputs(torch)
         lay.run(out_n, dump_n, noalloc=True)
         q_n, acc_n = lay.read(out_n, dump_n)
