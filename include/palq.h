@@ -401,9 +401,11 @@ palq_status palq_forward(palq_ctx *ctx, palq_net *net, const void *input, int32_
 palq_status palq_forward_image(palq_ctx *ctx, palq_net *net, const float *x, float l, float u, int32_t *logits);
 
 /* Descriptor (with device data pointer) of tensor `id` after a forward pass.
- * Conv/maxpool outputs are packed codes; an AVGSUM output is reported with
- * bits = 32 (int32 values, one per channel, h = w = 1).  Valid for every id
- * only with PALQ_NET_KEEP_ALL; otherwise buffers are reused between layers. */
+ * Conv/maxpool outputs are packed codes in the layout the descriptor names
+ * (see PALQ_NET_PIXEL_LAYOUT; palq_unpack reads either); an AVGSUM output
+ * is reported with bits = 32 (int32 values, one per channel, h = w = 1).
+ * Valid for every id only with PALQ_NET_KEEP_ALL; otherwise buffers are
+ * reused between layers. */
 palq_status palq_net_tensor(const palq_net *net, int32_t id, palq_act *desc);
 
 /* Algorithmic work of one forward pass: 2 * multiply-accumulates of every
