@@ -341,9 +341,9 @@ palq_status palq_net_create(palq_ctx *ctx, const palq_act *input, const palq_lay
   }
   // ---- tensor layouts: a conv, channel shuffle or max pool output of
   // several groups whose every reader takes it with those groups is stored
-  // group by group
-  // (PALQ_LAYOUT_GROUP), so that a tile of one group's pixels is one
-  // contiguous run for the conv operand fetches, shortcut reads and stores
+  // group by group (PALQ_LAYOUT_GROUP), so that a tile of one group's
+  // pixels is one contiguous run for the conv operand fetches, shortcut
+  // reads and stores
   if (!(flags & PALQ_NET_PIXEL_LAYOUT)) {
     std::vector<char> grouped_out(net->tensors.size(), 0), split(net->tensors.size(), 0);
     for (int i = 0; i < n_layers; ++i) {
