@@ -521,10 +521,18 @@ __global__ __launch_bounds__(256) void avgsum2_wg_kernel(ActView in, int32_t *ou
   const int hw = in.h * in.w;
   const uint8_t *base = in.data + (int64_t)n * hw * in.pixel + (int64_t)g * in.gstride + 4 * wi;
   uint32_t acc[4] = {0, 0, 0, 0};
-  for (int p = r; p < hw; p += R) {
-    const uint32_t w = *(const uint32_t *)(base + (int64_t)p * in.pixel);
+  // eight pixels' loads in flight before their sums
+  for (int p0 = r; p0 < hw; p0 += 8 * R) {
+    uint32_t w[8];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) acc[kk] += (w >> (2 * kk)) & 0x03030303u;
+    for (int u = 0; u < 8; ++u) {
+      const int p = p0 + u * R;
+      w[u] = p < hw ? *(const uint32_t *)(base + (int64_t)p * in.pixel) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) acc[kk] += (w[u] >> (2 * kk)) & 0x03030303u;
   }
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) part[kk][threadIdx.x] = acc[kk];
