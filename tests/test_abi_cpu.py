@@ -210,6 +210,41 @@ def test_validate_only_net_create(P, vctx):
     assert "layer 2" in vctx.last_error()
 
 
+def test_validate_only_net_tensor_layouts(P, vctx):
+    """Which tensors a network stores group by group: outputs of several
+    groups whose every reader keeps those groups; a tensor that a reader
+    re-splits, a one-group tensor and, with PALQ_NET_PIXEL_LAYOUT, every
+    tensor stay in the pixel layout."""
+    inp = P.make_act(2, 16, 16, 1, 3, 8, True, 0)
+    Ls = (P.Layer * 8)()
+    Ls[0] = _layer(P, op=P.OP_CONV, src=0, dst=1, w=P.Filter(1, 128, 3, 3, 3, 8, _fake(1)), stride=2,
+                   pad=1, mult=_fake(2), shift=_fake(3), out_bits=2)
+    Ls[1] = _layer(P, op=P.OP_MAXPOOL, src=1, dst=2, pool_k=3, pool_stride=2, pool_pad=1)
+    Ls[2] = _layer(P, op=P.OP_CONV, src=2, dst=3, w=P.Filter(2, 64, 64, 3, 3, 2, _fake(4)), stride=1,
+                   pad=1, mult=_fake(5), shift=_fake(6), out_bits=2)
+    Ls[3] = _layer(P, op=P.OP_CONV, src=3, dst=4, w=P.Filter(2, 64, 64, 3, 3, 2, _fake(7)), stride=1,
+                   pad=1, mult=_fake(8), shift=_fake(9), out_bits=2, res_src=3, res_mult=_fake(10))
+    Ls[4] = _layer(P, op=P.OP_CHANNEL_SHUFFLE, src=4, dst=5)
+    Ls[5] = _layer(P, op=P.OP_CONV, src=5, dst=6, w=P.Filter(4, 32, 32, 3, 3, 2, _fake(11)), stride=1,
+                   pad=1, mult=_fake(12), shift=_fake(13), out_bits=2)
+    Ls[6] = _layer(P, op=P.OP_AVGSUM, src=6, dst=7)
+    Ls[7] = _layer(P, op=P.OP_FC, src=7, dst=8, fc_w=_fake(14), fc_out=10)
+    want = {1: P.LAYOUT_PIXEL,   # one group
+            2: P.LAYOUT_PIXEL,   # one group (the next conv re-splits it)
+            3: P.LAYOUT_GROUP,   # conv input and identity shortcut, both with its 2 groups
+            4: P.LAYOUT_GROUP,   # read by the channel shuffle
+            5: P.LAYOUT_PIXEL,   # re-split into 4 groups by the next conv
+            6: P.LAYOUT_GROUP}   # read by the global sum
+    for flags, expect in ((0, want), (P.NET_PIXEL_LAYOUT, {t: P.LAYOUT_PIXEL for t in want})):
+        h = ctypes.c_void_p()
+        assert P._net_create(vctx.h, ctypes.byref(inp), Ls, 8, flags, ctypes.byref(h)) == P.OK, vctx.last_error()
+        for t, lay in expect.items():
+            d = P.Act()
+            assert P._net_tensor(h, t, ctypes.byref(d)) == P.OK
+            assert d.layout == lay, (flags, t, d.layout)
+        P._net_destroy(h)
+
+
 def test_validate_only_forward_image(P, vctx):
     """palq_forward_image: image-input networks only, finite l < u, non-null
     aligned pointers (validate-only: no device work)."""
