@@ -417,12 +417,25 @@ class Net:
     def ops(self) -> int:
         return int(_net_ops(self.h))
 
+    @staticmethod
+    def _require(t, nbytes, what):
+        """The C calls take plain pointers: refuse a torch tensor smaller than
+        the network's batch needs before handing it over."""
+        if hasattr(t, "numel") and t.numel() * t.element_size() < nbytes:
+            raise PalqError(ERR_ARG, f"{what} holds fewer bytes than the network's batch needs")
+
     def forward(self, x_packed, logits):
+        a = self.input_act
+        self._require(x_packed, act_bytes(a), "input")
+        self._require(logits, 4 * a.n * self.classes, "logits")
         self.ctx._check(_forward(self.ctx.h, self.h, _ptr(x_packed), _ptr(logits)))
 
     def forward_image(self, x_f32, l, u, logits):
         """palq_forward_image: quantise an fp32 [n][h][w][3] image (Eq. 2,
         fixed l, u) and run the network on it."""
+        a = self.input_act
+        self._require(x_f32, 4 * a.n * a.h * a.w * a.ch_per_group, "input")
+        self._require(logits, 4 * a.n * self.classes, "logits")
         self.ctx._check(_forward_image(self.ctx.h, self.h, _ptr(x_f32), float(l), float(u), _ptr(logits)))
 
     def tensor(self, tid) -> Tensor:

@@ -82,6 +82,26 @@ def test_resnet18_group_layout_matches_pixel_layout(ctx, torch):
         np.testing.assert_array_equal(logits.cpu().numpy().astype(np.int64).reshape(2, -1), ref)
 
 
+def test_forward_refuses_buffers_smaller_than_the_batch(ctx, torch):
+    """The binding checks the input and logits tensors against the network's
+    batch before the C call (which takes plain pointers): a short buffer
+    raises, nothing is launched."""
+    from paper_2208_01944_amd import palq
+    spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=13)
+    net = palq.Net(ctx, spec)
+    x = torch.zeros(2 * 64 * 64 * 3, dtype=torch.float32, device=ctx.dev)
+    logits = torch.empty(2 * net.classes, dtype=torch.int32, device=ctx.dev)
+    with pytest.raises(palq.PalqError):
+        net.forward_image(x[: 64 * 64 * 3], -1.0, 1.0, logits)
+    with pytest.raises(palq.PalqError):
+        net.forward_image(x, -1.0, 1.0, logits[: net.classes])
+    xt = ctx.pack(spec["x"], 1, 8, signed=True)
+    with pytest.raises(palq.PalqError):
+        net.forward(xt.buf[: xt.buf.numel() // 2], logits)
+    net.forward_image(x, -1.0, 1.0, logits)
+    ctx.sync()
+
+
 def test_resnet18_small_int8_matrix_cores(ctx, torch):
     say("resnet18 hw=64 n=2 G=4 b=2 centred, int8 only")
     spec = I.resnet18(n=2, groups=4, bits=2, hw=64, classes=100, seed=14)
